@@ -1,0 +1,454 @@
+"""Pins of the CPU oracle to things other than itself (no GPU needed).
+
+Each test ties one oracle function to what the paper or the mathematics
+fixes: hand-derived Eq. 2 counts, brute force on tiny inputs, closed forms,
+invariants, and independent library routines (torch CPU float64). They are
+chosen so that a dropped term, a wrong sign or index, a transposed operand or
+a wrong mask in the oracle fails at least one of them.
+"""
+import itertools
+import json
+import math
+import os
+
+import numpy as np
+import pytest
+import torch
+import torch.nn.functional as F
+
+from oracle import zsa_oracle as O
+from paper_2509_01190_amd import workloads as W
+
+GOLDEN = os.path.join(os.path.dirname(__file__), "golden")
+
+
+# ---------------------------------------------------------------- Eq. 2
+def test_keep_schedule_golden():
+    with open(os.path.join(GOLDEN, "keep_schedule.json")) as f:
+        cases = json.load(f)["cases"]
+    for c in cases:
+        got = [row[0] for row in O.keep_schedule([c["n"]], [c["alpha"]], 5, c["points"])]
+        assert got == c["counts"], c
+
+
+def test_keep_count_properties():
+    alphas = np.linspace(0.0, 1.0, 101)
+    for n in [0, 1, 4, 5, 6, 37, 128, 512, 4096]:
+        prev = -1
+        for a in alphas:
+            k = O.keep_count(n, float(a), 5)
+            assert 0 <= k <= n
+            assert k >= min(n, 5)                  # the tau floor
+            assert k >= prev                       # monotone in alpha
+            prev = k
+        assert O.keep_count(n, 1.0, 5) == n        # alpha = 1 keeps everything
+    # the count is the largest integer not above alpha*n (then floored at tau)
+    for n in [10, 99, 1000]:
+        for a in [0.13, 0.37, 0.5, 0.61, 0.875]:
+            k = O.keep_count(n, a, 1)
+            assert k <= a * n + 1e-6 < k + 1
+
+
+@pytest.mark.parametrize("bad", [float("nan"), -0.01, 1.01, float("inf")])
+def test_keep_count_rejects(bad):
+    with pytest.raises(ValueError):
+        O.keep_count(100, bad, 5)
+
+
+def test_keep_count_tau():
+    with pytest.raises(ValueError):
+        O.keep_count(100, 0.5, 0)
+    assert O.keep_count(100, 0.01, 7) == 7
+    assert O.keep_count(100, 0.01, 1) == 1
+
+
+# ------------------------------------------------------ bf16 rounding
+def test_bf16_round_matches_torch_conversion():
+    g = np.random.default_rng(7)
+    x = (g.standard_normal(200_000) * np.exp2(g.integers(-60, 60, 200_000))).astype(np.float32)
+    ref = torch.from_numpy(x).to(torch.bfloat16).to(torch.float64).numpy()
+    got = O.bf16_round(x.astype(np.float64))
+    assert np.array_equal(got, ref)
+
+
+def test_bf16_round_ties_to_even():
+    ulp = 2.0 ** -7                                   # bf16 spacing in [1, 2)
+    assert O.bf16_round(1.0 + ulp / 2) == 1.0           # tie -> even mantissa 0
+    assert O.bf16_round(1.0 + ulp + ulp / 2) == 1.0 + 2 * ulp   # tie -> even mantissa 2
+    assert O.bf16_round(1.0 + ulp / 2 + 1e-12) == 1.0 + ulp     # above the tie
+    assert O.bf16_round(-3.0) == -3.0
+    assert O.bf16_round(0.0) == 0.0
+
+
+# ------------------------------------------------------ backbone pieces
+def test_layer_norm_vs_torch():
+    g = np.random.default_rng(1)
+    x = g.standard_normal((9, 48)) * 3 + 1
+    w = g.standard_normal(48)
+    b = g.standard_normal(48)
+    ref = F.layer_norm(torch.from_numpy(x), (48,), torch.from_numpy(w), torch.from_numpy(b), 1e-5)
+    assert np.allclose(O.layer_norm(x, w, b, 1e-5), ref.numpy(), rtol=1e-12, atol=1e-12)
+
+
+def test_rms_norm_vs_torch():
+    g = np.random.default_rng(2)
+    x = g.standard_normal((9, 64)) * 2
+    w = g.standard_normal(64)
+    ref = F.rms_norm(torch.from_numpy(x), (64,), torch.from_numpy(w), 1e-5)
+    assert np.allclose(O.rms_norm(x, w, 1e-5), ref.numpy(), rtol=1e-12, atol=1e-12)
+    y = O.rms_norm(x, np.ones(64), 0.0)
+    assert np.allclose(np.sqrt((y * y).mean(axis=1)), 1.0, rtol=1e-12)
+
+
+def test_gelu_and_silu():
+    # textbook values of the standard normal CDF: Phi(1) = 0.8413447460685429,
+    # Phi(2) = 0.9772498680518208, so GELU(z) = z * Phi(z)
+    assert O.gelu(np.array(1.0)) == pytest.approx(0.8413447460685429, abs=1e-15)
+    assert O.gelu(np.array(-1.0)) == pytest.approx(-(1 - 0.8413447460685429), abs=1e-15)
+    assert O.gelu(np.array(2.0)) == pytest.approx(2 * 0.9772498680518208, abs=1e-14)
+    assert O.gelu(np.array(0.0)) == 0.0
+    z = np.linspace(-8, 8, 1001)
+    assert np.allclose(O.gelu(z), F.gelu(torch.from_numpy(z), approximate="none").numpy(),
+                       rtol=1e-13, atol=1e-15)
+    assert np.allclose(O.silu(z), F.silu(torch.from_numpy(z)).numpy(), rtol=1e-13, atol=1e-15)
+
+
+def test_rope_hand_example():
+    # hd = 4: channel 0 pairs with 2 (frequency theta^0 = 1 rad per position),
+    # channel 1 pairs with 3 (frequency theta^(-2/4) = 0.01 for theta = 1e4)
+    p = 7.0
+    x = np.array([[1.0, 0.0, 0.0, 0.0]])
+    y = O.rope(x, np.array([p]), 1, 10000.0)
+    assert np.allclose(y, [[math.cos(p), 0.0, math.sin(p), 0.0]], atol=1e-15)
+    x = np.array([[0.0, 1.0, 0.0, 0.0]])
+    y = O.rope(x, np.array([p]), 1, 10000.0)
+    assert np.allclose(y, [[0.0, math.cos(0.01 * p), 0.0, math.sin(0.01 * p)]], atol=1e-15)
+    x = np.array([[0.0, 0.0, 1.0, 0.0]])
+    y = O.rope(x, np.array([p]), 1, 10000.0)
+    assert np.allclose(y, [[-math.sin(p), 0.0, math.cos(p), 0.0]], atol=1e-15)
+
+
+def test_rope_invariances():
+    g = np.random.default_rng(3)
+    H, hd = 3, 16
+    q = g.standard_normal((1, H * hd))
+    k = g.standard_normal((1, H * hd))
+    # position 0 is the identity; every pair keeps its norm
+    assert np.allclose(O.rope(q, np.array([0]), H, 1e4), q)
+    r = O.rope(q, np.array([123]), H, 1e4)
+    assert np.allclose(np.linalg.norm(r), np.linalg.norm(q))
+    # per head, <R(m) q, R(n) k> depends only on m - n
+    def dots(m, n):
+        a = O.rope(q, np.array([m]), H, 1e4)
+        b = O.rope(k, np.array([n]), H, 1e4)
+        return [float(a[0, h * hd:(h + 1) * hd] @ b[0, h * hd:(h + 1) * hd]) for h in range(H)]
+    assert np.allclose(dots(10, 3), dots(107, 100), rtol=1e-10)
+    assert not np.allclose(dots(10, 3), dots(10, 4), rtol=1e-6)
+
+
+# ------------------------------------------------------ Eq. 1 attention
+def _brute_attention(q, k, v, pos, H, causal):
+    """Triple loops straight from Eq. 1 and the column-sum reading."""
+    n, d = len(q), len(q[0])
+    hd = d // H
+    o = [[0.0] * d for _ in range(n)]
+    lse = [[0.0] * n for _ in range(H)]
+    s = [0.0] * n
+    for h in range(H):
+        for i in range(n):
+            logits = []
+            for j in range(n):
+                if causal and pos[j] > pos[i]:
+                    logits.append(None)
+                    continue
+                dot = sum(q[i][h * hd + c] * k[j][h * hd + c] for c in range(hd))
+                logits.append(dot / math.sqrt(hd))
+            m = max(x for x in logits if x is not None)
+            z = sum(math.exp(x - m) for x in logits if x is not None)
+            lse[h][i] = m + math.log(z)
+            for j in range(n):
+                if logits[j] is None:
+                    continue
+                p = math.exp(logits[j] - m) / z
+                s[j] += p
+                for c in range(hd):
+                    o[i][h * hd + c] += p * v[j][h * hd + c]
+    return np.array(o), np.array(lse), np.array(s)
+
+
+@pytest.mark.parametrize("causal", [False, True])
+def test_attention_brute_force(causal):
+    g = np.random.default_rng(11)
+    n, H, hd = 6, 2, 4
+    q = g.standard_normal((n, H * hd)) * 1.5
+    k = g.standard_normal((n, H * hd)) * 1.5
+    v = g.standard_normal((n, H * hd))
+    pos = np.array([0, 2, 3, 7, 8, 11])                # compacted positions keep order
+    o, lse, s = O.attention(q, k, v, pos, H, causal)
+    bo, blse, bs = _brute_attention(q.tolist(), k.tolist(), v.tolist(), pos.tolist(), H, causal)
+    assert np.allclose(o, bo, rtol=1e-12, atol=1e-12)
+    assert np.allclose(lse, blse, rtol=1e-12, atol=1e-12)
+    assert np.allclose(s, bs, rtol=1e-12, atol=1e-12)
+
+
+@pytest.mark.parametrize("causal", [False, True])
+def test_attention_vs_torch_sdpa(causal):
+    g = np.random.default_rng(12)
+    n, H, hd = 37, 4, 32
+    q = g.standard_normal((n, H * hd))
+    k = g.standard_normal((n, H * hd))
+    v = g.standard_normal((n, H * hd))
+    o, lse, s = O.attention(q, k, v, np.arange(n), H, causal)
+    tq, tk, tv = (torch.from_numpy(a).view(n, H, hd).transpose(0, 1).contiguous() for a in (q, k, v))
+    ref = F.scaled_dot_product_attention(tq, tk, tv, is_causal=causal)
+    assert np.allclose(o, ref.transpose(0, 1).reshape(n, H * hd).numpy(), rtol=1e-11, atol=1e-12)
+    logits = (tq @ tk.transpose(1, 2)) / math.sqrt(hd)
+    if causal:
+        logits = logits.masked_fill(torch.ones(n, n, dtype=torch.bool).triu(1), float("-inf"))
+    assert np.allclose(lse, torch.logsumexp(logits, dim=-1).numpy(), rtol=1e-12, atol=1e-12)
+    assert np.allclose(s, torch.softmax(logits, dim=-1).sum(dim=(0, 1)).numpy(), rtol=1e-12)
+
+
+@pytest.mark.parametrize("causal", [False, True])
+def test_scores_total_mass(causal):
+    # every softmax row sums to 1, so the column sums add up to H * n
+    g = np.random.default_rng(13)
+    n, H, hd = 50, 3, 8
+    q, k, v = (g.standard_normal((n, H * hd)) * 2 for _ in range(3))
+    _, _, s = O.attention(q, k, v, np.arange(n), H, causal)
+    assert s.sum() == pytest.approx(H * n, rel=1e-12)
+    assert (s >= 0).all()
+    if causal:
+        # the last row is the only one that sees the last column
+        qh = q[-1:, :]
+        logits = [(qh[0, h * hd:(h + 1) * hd] @ k[:, h * hd:(h + 1) * hd].T) / math.sqrt(hd)
+                  for h in range(H)]
+        p_last = sum(math.exp(l[-1] - l.max()) / np.exp(l - l.max()).sum() for l in logits)
+        assert s[-1] == pytest.approx(p_last, rel=1e-12)
+
+
+def _harmonic(m):
+    return sum(1.0 / t for t in range(1, m + 1))
+
+
+@pytest.mark.parametrize("kind", [W.ENCODER, W.DECODER])
+def test_scores_closed_form_uniform_attention(kind):
+    # W_q = 0 makes every query zero: all logits are 0, attention is uniform.
+    # Bidirectional: s_j = H for all j (all tie, kept set = first k rows).
+    # Causal: row i spreads 1/(i+1) over j <= i, so s_j = H (Harm(n) - Harm(j)).
+    causal = kind == W.DECODER
+    p = W.shrink(W.PRESETS["tiny"], kind=kind, causal=causal, n_layers=1, batch=1, seq_len=24)
+    w = {k: (None if v is None else v.astype(np.float64))
+         for k, v in W.layer_weights(p, 0, seed=3, norm_jitter=True, zero_wq=True).items()}
+    cfg = O.LayerCfg(kind, p.d_model, p.n_heads, p.d_ff, causal)
+    n = p.seq_len
+    x = W.hidden(p, seed=3, lens=[n]).astype(np.float64)
+    res = O.sequence_layer(x, np.arange(n), w, cfg, "exact", want_scores=True)
+    H = p.n_heads
+    if causal:
+        expect = np.array([H * (_harmonic(n) - _harmonic(j)) for j in range(n)])
+    else:
+        expect = np.full(n, float(H))
+    assert np.allclose(res["scores"], expect, rtol=1e-12, atol=1e-12)
+    out = O.layer_forward(x, np.arange(n), [0, n], w, cfg, keep_rate=[0.5])
+    assert list(out["kept_rows"]) == list(range(12))
+
+
+# ------------------------------------------------------ top-k selection
+def _brute_topk(s, k):
+    """The unique subset of size k whose members all beat all non-members
+    under (score desc, index asc)."""
+    n = len(s)
+    beats = lambda a, b: s[a] > s[b] or (s[a] == s[b] and a < b)
+    found = []
+    for sub in itertools.combinations(range(n), k):
+        inside = set(sub)
+        if all(beats(a, b) for a in inside for b in range(n) if b not in inside):
+            found.append(list(sub))
+    assert len(found) == 1
+    return found[0]
+
+
+def test_select_topk_brute_force():
+    g = np.random.default_rng(5)
+    for trial in range(60):
+        n = int(g.integers(1, 11))
+        vals = g.choice([0.0, -0.0, 0.5, 1.0, 1.0, 2.0, 3.25], size=n)
+        if trial % 3 == 0:
+            vals = g.standard_normal(n)
+        for k in range(n + 1):
+            got = list(O.select_topk(vals, k))
+            assert got == _brute_topk(list(vals), k), (vals, k)
+
+
+def test_select_topk_reject_nan():
+    with pytest.raises(ValueError):
+        O.select_topk(np.array([1.0, np.nan]), 1)
+
+
+# ------------------------------------------------------ one layer
+def test_encoder_layer_vs_torch_transformer_layer():
+    # torch's own pre-norm encoder layer (LayerNorm eps 1e-5, exact GELU,
+    # fused QKV in the same [q; k; v] row layout) in float64
+    p = W.shrink(W.PRESETS["tiny"], n_layers=1, batch=1, seq_len=29)
+    w = {k: v.astype(np.float64) for k, v in W.layer_weights(p, 0, 4, norm_jitter=True).items()}
+    w["w_qkv"] *= 25.0   # sharper attention than the 0.02 init gives
+    d, H, Fd = p.d_model, p.n_heads, p.d_ff
+    layer = torch.nn.TransformerEncoderLayer(d, H, Fd, dropout=0.0, activation="gelu",
+                                             layer_norm_eps=1e-5, batch_first=True,
+                                             norm_first=True, dtype=torch.float64)
+    t = lambda a: torch.from_numpy(a)
+    with torch.no_grad():
+        layer.self_attn.in_proj_weight.copy_(t(w["w_qkv"]))
+        layer.self_attn.in_proj_bias.copy_(t(w["b_qkv"]))
+        layer.self_attn.out_proj.weight.copy_(t(w["w_o"]))
+        layer.self_attn.out_proj.bias.copy_(t(w["b_o"]))
+        layer.norm1.weight.copy_(t(w["norm1_w"]))
+        layer.norm1.bias.copy_(t(w["norm1_b"]))
+        layer.norm2.weight.copy_(t(w["norm2_w"]))
+        layer.norm2.bias.copy_(t(w["norm2_b"]))
+        layer.linear1.weight.copy_(t(w["w_up"]))
+        layer.linear1.bias.copy_(t(w["b_up"]))
+        layer.linear2.weight.copy_(t(w["w_down"]))
+        layer.linear2.bias.copy_(t(w["b_down"]))
+    layer.eval()
+    x = W.hidden(p, 4, [29]).astype(np.float64)
+    with torch.no_grad():
+        ref = layer(t(x)[None])[0].numpy()
+    cfg = O.LayerCfg(W.ENCODER, d, H, Fd, False)
+    got = O.sequence_layer(x, np.arange(29), w, cfg)["x"]
+    assert np.allclose(got, ref, rtol=1e-10, atol=1e-10)
+
+
+def test_decoder_layer_vs_torch_composition():
+    # RMSNorm, causal SDPA and SiLU from torch; RoPE from the oracle (pinned above)
+    p = W.shrink(W.PRESETS["tiny"], kind=W.DECODER, causal=True, n_layers=1, batch=1, seq_len=21)
+    w = {k: (None if v is None else v.astype(np.float64))
+         for k, v in W.layer_weights(p, 0, 5, norm_jitter=True).items()}
+    w["w_qkv"] *= 25.0
+    d, H, Fd = p.d_model, p.n_heads, p.d_ff
+    hd = d // H
+    n = 21
+    pos = np.arange(n)
+    x = W.hidden(p, 5, [n]).astype(np.float64)
+    t = torch.from_numpy
+    h = F.rms_norm(t(x), (d,), t(w["norm1_w"]), 1e-5)
+    qkv = h @ t(w["w_qkv"]).T
+    q = t(O.rope(qkv[:, :d].numpy(), pos, H, 1e4))
+    k = t(O.rope(qkv[:, d:2 * d].numpy(), pos, H, 1e4))
+    v = qkv[:, 2 * d:]
+    heads = lambda a: a.view(n, H, hd).transpose(0, 1).contiguous()
+    o = F.scaled_dot_product_attention(heads(q), heads(k), heads(v), is_causal=True)
+    x1 = t(x) + o.transpose(0, 1).reshape(n, d) @ t(w["w_o"]).T
+    h2 = F.rms_norm(x1, (d,), t(w["norm2_w"]), 1e-5)
+    z = h2 @ t(w["w_up"]).T
+    ref = (x1 + (F.silu(z[:, 0::2]) * z[:, 1::2]) @ t(w["w_down"]).T).numpy()
+    cfg = O.LayerCfg(W.DECODER, d, H, Fd, True)
+    got = O.sequence_layer(x, pos, w, cfg)["x"]
+    assert np.allclose(got, ref, rtol=1e-10, atol=1e-10)
+
+
+def test_causal_layer_ignores_future_rows():
+    p = W.shrink(W.PRESETS["tiny"], kind=W.DECODER, causal=True, n_layers=1, batch=1, seq_len=16)
+    w = {k: (None if v is None else v.astype(np.float64))
+         for k, v in W.layer_weights(p, 0, 6).items()}
+    cfg = O.LayerCfg(W.DECODER, p.d_model, p.n_heads, p.d_ff, True)
+    x = W.hidden(p, 6, [16]).astype(np.float64)
+    y = O.sequence_layer(x, np.arange(16), w, cfg)["x"]
+    x2 = x.copy()
+    x2[9:] += 1.0
+    y2 = O.sequence_layer(x2, np.arange(16), w, cfg)["x"]
+    assert np.array_equal(y[:9], y2[:9])
+    assert not np.allclose(y[9:], y2[9:])
+
+
+def test_bidirectional_layer_is_permutation_equivariant():
+    p = W.shrink(W.PRESETS["tiny"], n_layers=1, batch=1, seq_len=20)
+    w = {k: v.astype(np.float64) for k, v in W.layer_weights(p, 0, 8).items()}
+    w["w_qkv"] *= 20.0
+    cfg = O.LayerCfg(W.ENCODER, p.d_model, p.n_heads, p.d_ff, False)
+    x = W.hidden(p, 8, [20]).astype(np.float64)
+    perm = np.random.default_rng(0).permutation(20)
+    a = O.sequence_layer(x, np.arange(20), w, cfg, want_scores=True)
+    b = O.sequence_layer(x[perm], np.arange(20), w, cfg, want_scores=True)
+    assert np.allclose(a["x"][perm], b["x"], rtol=1e-12, atol=1e-12)
+    assert np.allclose(a["scores"][perm], b["scores"], rtol=1e-12, atol=1e-12)
+
+
+# ------------------------------------------------------ the stack
+def _stack_inputs(kind, lens, seed, n_layers=3):
+    causal = kind == W.DECODER
+    p = W.shrink(W.PRESETS["tiny"], kind=kind, causal=causal, n_layers=n_layers,
+                 batch=len(lens), d_model=64, n_heads=4, d_ff=128)
+    ws = [{k: (None if v is None else v.astype(np.float64)) for k, v in wd.items()}
+          for wd in W.stack_weights(p, seed, norm_jitter=True)]
+    for wd in ws:
+        wd["w_qkv"] *= 20.0
+    x = W.hidden(p, seed, lens).astype(np.float64)
+    pos = W.positions(lens).astype(np.int64)
+    cu = W.cu_seqlens(lens)
+    cfg = O.LayerCfg(kind, p.d_model, p.n_heads, p.d_ff, causal)
+    return x, pos, cu, ws, cfg
+
+
+@pytest.mark.parametrize("kind", [W.ENCODER, W.DECODER])
+def test_stack_keep_rate_one_is_unpruned(kind):
+    lens = [17, 5, 30]
+    x, pos, cu, ws, cfg = _stack_inputs(kind, lens, 21)
+    a = O.stack_forward(x, pos, cu, ws, cfg, [1, 2], [1.0] * 3)
+    b = O.stack_forward(x, pos, cu, ws, cfg, [], [1.0] * 3)
+    assert np.array_equal(a["x"], b["x"])
+    assert np.array_equal(a["pos"], b["pos"])
+
+
+@pytest.mark.parametrize("kind", [W.ENCODER, W.DECODER])
+def test_stack_sequences_are_independent(kind):
+    lens = [17, 3, 30, 9]
+    rates = [0.5, 0.9, 0.3, 0.7]
+    x, pos, cu, ws, cfg = _stack_inputs(kind, lens, 22)
+    full = O.stack_forward(x, pos, cu, ws, cfg, [1, 2], rates)
+    for b in range(len(lens)):
+        lo, hi = cu[b], cu[b + 1]
+        one = O.stack_forward(x[lo:hi], pos[lo:hi], [0, hi - lo], ws, cfg, [1, 2], [rates[b]])
+        flo, fhi = full["cu"][b], full["cu"][b + 1]
+        assert np.array_equal(one["x"], full["x"][flo:fhi])
+        assert np.array_equal(one["pos"], full["pos"][flo:fhi])
+
+
+@pytest.mark.parametrize("kind", [W.ENCODER, W.DECODER])
+def test_stack_counts_and_kept_sets(kind):
+    lens = [40, 11, 26]
+    rates = [0.6, 0.2, 0.45]
+    x, pos, cu, ws, cfg = _stack_inputs(kind, lens, 23)
+    res = O.stack_forward(x, pos, cu, ws, cfg, [1, 2], rates)
+    sched = O.keep_schedule(lens, rates, 5, 2)
+    cur_cu = list(cu)
+    for p_i, point in enumerate(res["points"]):
+        assert point["k"] == sched[p_i]
+        assert list(np.diff(point["cu"])) == sched[p_i]
+        for b in range(len(lens)):
+            lo, hi = cur_cu[b], cur_cu[b + 1]
+            s = point["scores"][lo:hi]
+            # the kept rows are exactly the k best of this layer's own scores
+            kept_local = point["kept_rows"][(point["kept_rows"] >= lo) & (point["kept_rows"] < hi)] - lo
+            order = sorted(range(hi - lo), key=lambda j: (-s[j], j))[: sched[p_i][b]]
+            assert sorted(order) == list(kept_local)
+            assert (np.diff(point["pos"][point["cu"][b]:point["cu"][b + 1]]) > 0).all()
+        cur_cu = list(point["cu"])
+    # causal pruning keeps mostly early positions (Appendix B trend)
+    if kind == W.DECODER:
+        first = res["points"][0]
+        kept = first["pos"][first["cu"][0]:first["cu"][1]]
+        assert np.mean(kept) < np.mean(np.arange(40))
+
+
+def test_bf16_mode_rounds_storage_points():
+    lens = [12]
+    x, pos, cu, ws, cfg = _stack_inputs(W.ENCODER, lens, 24, n_layers=1)
+    x = O.bf16_round(x)
+    res = O.sequence_layer(x, pos, ws[0], cfg, "bf16")
+    for key in ("x", "h", "q", "k", "v", "o", "x_mid", "f"):
+        assert np.array_equal(res[key], O.bf16_round(res[key])), key
+    ex = O.sequence_layer(x, pos, ws[0], cfg, "exact")["x"]
+    assert not np.array_equal(ex, res["x"])
+    assert np.allclose(ex, res["x"], rtol=0.05, atol=0.05)
