@@ -1,0 +1,302 @@
+// Attention of Eq. 1, softmax(Q K^T * scale + M) V, per sequence and head,
+// over packed variable-length rows; also writes the natural-log
+// log-sum-exp of every score row (used by the contribution scores).
+//
+// bf16, head_dim 64/128 (MFMA): one 256-thread workgroup per (128-query
+// block, head, sequence); each wave owns 32 queries and walks 64-key tiles
+// staged in LDS (K row-major, V transposed). The wave computes the
+// *transposed* score tile S^T = K Q^T with v_mfma_f32_32x32x16_bf16, so a
+// lane holds 32 key scores of one query: the online-softmax max and sum are
+// in-lane plus one swap with lane l^32, and the probabilities already sit in
+// the B-operand layout of O^T += V^T P^T (P rounded to bf16), with no trip
+// through LDS. The k-slot order of P^T is whatever the accumulator gives; V^T
+// is read from LDS in that same order, which leaves the contraction unchanged.
+// Causal blocks skip key tiles above the diagonal and are scheduled
+// heaviest-first.
+//
+// fp32 (and any other head_dim): one thread per query with the row in
+// registers, 32-key LDS tiles, the same online softmax.
+#include <math.h>
+
+#include "zsa_internal.h"
+
+namespace zsa {
+namespace {
+
+typedef __bf16 bf16x8_t __attribute__((ext_vector_type(8)));
+typedef float f32x16_t __attribute__((ext_vector_type(16)));
+
+constexpr float kLog2e = 1.4426950408889634f;
+constexpr float kLn2 = 0.6931471805599453f;
+
+__device__ __forceinline__ uint32_t bf16_at(const uint4& v, int e) {
+  const uint32_t w = e < 2 ? v.x : e < 4 ? v.y : e < 6 ? v.z : v.w;
+  return (e & 1) ? (w >> 16) : (w & 0xffffu);
+}
+
+template <int HD>
+__global__ __launch_bounds__(256) void attn_mfma_kernel(
+    const bf16_t* __restrict__ Q, const bf16_t* __restrict__ K, const bf16_t* __restrict__ V,
+    int64_t rs, int causal, float scale_log2, const int32_t* __restrict__ cu,
+    bf16_t* __restrict__ O, int64_t os, float* __restrict__ lse, int T) {
+  constexpr int BQ = 128, BKEY = 64;
+  constexpr int KLD = HD + 8;    // K tile row stride (bf16)
+  constexpr int VLD = BKEY + 8;  // V^T tile row stride (bf16)
+  constexpr int OLD = HD + 8;    // output staging row stride
+  constexpr int KBYTES = BKEY * KLD * 2, VBYTES = HD * VLD * 2;
+  constexpr int SBYTES = KBYTES + VBYTES > 4 * 32 * OLD * 2 ? KBYTES + VBYTES : 4 * 32 * OLD * 2;
+  __shared__ __align__(16) unsigned char smem[SBYTES];
+  bf16_t* Ks = reinterpret_cast<bf16_t*>(smem);
+  bf16_t* Vt = reinterpret_cast<bf16_t*>(smem + KBYTES);
+
+  const int b = blockIdx.z, h = blockIdx.y;
+  const int lo = cu[b];
+  const int n = cu[b + 1] - lo;
+  const int nqb = (n + BQ - 1) / BQ;
+  if (static_cast<int>(blockIdx.x) >= nqb) return;
+  const int qb = causal ? nqb - 1 - static_cast<int>(blockIdx.x) : static_cast<int>(blockIdx.x);
+  const int q0 = qb * BQ;
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int half = lane >> 5, l32 = lane & 31;
+  const int qrow = q0 + wave * 32 + l32;
+  const uint4 zero = make_uint4(0, 0, 0, 0);
+
+  bf16x8_t qf[HD / 16];
+#pragma unroll
+  for (int kk = 0; kk < HD / 16; ++kk) {
+    const uint4 v = qrow < n ? *reinterpret_cast<const uint4*>(
+                                   Q + static_cast<int64_t>(lo + qrow) * rs + h * HD + kk * 16 + half * 8)
+                             : zero;
+    qf[kk] = __builtin_bit_cast(bf16x8_t, v);
+  }
+
+  float m_run = -INFINITY, l_run = 0.f;
+  f32x16_t o[HD / 32];
+#pragma unroll
+  for (int ct = 0; ct < HD / 32; ++ct)
+#pragma unroll
+    for (int r = 0; r < 16; ++r) o[ct][r] = 0.f;
+
+  const int kend = causal ? min(n, q0 + BQ) : n;
+  const int wave_qmax = q0 + wave * 32 + 31;
+  for (int j0 = 0; j0 < kend; j0 += BKEY) {
+    for (int c = tid; c < BKEY * HD / 8; c += 256) {
+      const int r = c / (HD / 8), ch = (c % (HD / 8)) * 8;
+      const int jr = j0 + r;
+      *reinterpret_cast<uint4*>(Ks + r * KLD + ch) =
+          jr < n ? *reinterpret_cast<const uint4*>(K + static_cast<int64_t>(lo + jr) * rs + h * HD + ch)
+                 : zero;
+    }
+    for (int c = tid; c < (BKEY / 2) * (HD / 8); c += 256) {
+      const int rp = c / (HD / 8), ch = (c % (HD / 8)) * 8;
+      const int jr = j0 + 2 * rp;
+      const uint4 v0 = jr < n ? *reinterpret_cast<const uint4*>(V + static_cast<int64_t>(lo + jr) * rs + h * HD + ch)
+                              : zero;
+      const uint4 v1 = jr + 1 < n ? *reinterpret_cast<const uint4*>(V + static_cast<int64_t>(lo + jr + 1) * rs + h * HD + ch)
+                                  : zero;
+#pragma unroll
+      for (int e = 0; e < 8; ++e)
+        *reinterpret_cast<uint32_t*>(Vt + (ch + e) * VLD + 2 * rp) = bf16_at(v0, e) | (bf16_at(v1, e) << 16);
+    }
+    __syncthreads();
+    if (!causal || j0 <= wave_qmax) {
+      f32x16_t s[2];
+#pragma unroll
+      for (int ks = 0; ks < 2; ++ks) {
+#pragma unroll
+        for (int r = 0; r < 16; ++r) s[ks][r] = 0.f;
+#pragma unroll
+        for (int kk = 0; kk < HD / 16; ++kk) {
+          const bf16x8_t a = __builtin_bit_cast(
+              bf16x8_t, *reinterpret_cast<const uint4*>(Ks + (ks * 32 + l32) * KLD + kk * 16 + half * 8));
+          s[ks] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, qf[kk], s[ks], 0, 0, 0);
+        }
+      }
+      // s[ks][r]: query qrow, key j0 + 32 ks + 8 (r/4) + 4 half + r%4
+      float mloc = -INFINITY;
+#pragma unroll
+      for (int ks = 0; ks < 2; ++ks)
+#pragma unroll
+        for (int r = 0; r < 16; ++r) {
+          const int j = j0 + ks * 32 + 8 * (r >> 2) + 4 * half + (r & 3);
+          float x = s[ks][r] * scale_log2;
+          if (j >= n || (causal && j > qrow)) x = -INFINITY;
+          s[ks][r] = x;
+          mloc = fmaxf(mloc, x);
+        }
+      mloc = fmaxf(mloc, __shfl_xor(mloc, 32, 64));
+      const float m_new = fmaxf(m_run, mloc);
+      const float m_use = m_new == -INFINITY ? 0.f : m_new;
+      const float alpha = exp2f(m_run - m_use);
+      float rsum = 0.f;
+#pragma unroll
+      for (int ks = 0; ks < 2; ++ks)
+#pragma unroll
+        for (int r = 0; r < 16; ++r) {
+          const float p = exp2f(s[ks][r] - m_use);
+          s[ks][r] = p;
+          rsum += p;
+        }
+      rsum += __shfl_xor(rsum, 32, 64);
+      l_run = l_run * alpha + rsum;
+      m_run = m_new;
+#pragma unroll
+      for (int ct = 0; ct < HD / 32; ++ct)
+#pragma unroll
+        for (int r = 0; r < 16; ++r) o[ct][r] *= alpha;
+#pragma unroll
+      for (int g = 0; g < 4; ++g) {
+        const int ks = g >> 1, rb = (g & 1) * 8;
+        uint32_t pw[4];
+#pragma unroll
+        for (int t = 0; t < 4; ++t)
+          pw[t] = static_cast<uint32_t>(f32_to_bf16(s[ks][rb + 2 * t])) |
+                  (static_cast<uint32_t>(f32_to_bf16(s[ks][rb + 2 * t + 1])) << 16);
+        const bf16x8_t pb = __builtin_bit_cast(bf16x8_t, make_uint4(pw[0], pw[1], pw[2], pw[3]));
+        const int base = ks * 32 + (g & 1) * 16 + 4 * half;
+#pragma unroll
+        for (int ct = 0; ct < HD / 32; ++ct) {
+          const bf16_t* vr = Vt + (ct * 32 + l32) * VLD + base;
+          const uint2 lo4 = *reinterpret_cast<const uint2*>(vr);
+          const uint2 hi4 = *reinterpret_cast<const uint2*>(vr + 8);
+          const bf16x8_t a = __builtin_bit_cast(bf16x8_t, make_uint4(lo4.x, lo4.y, hi4.x, hi4.y));
+          o[ct] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, pb, o[ct], 0, 0, 0);
+        }
+      }
+    }
+    __syncthreads();
+  }
+
+  // o[ct][r] = O^T[channel ct*32 + 8 (r/4) + 4 half + r%4][query qrow]
+  const float inv_l = l_run > 0.f ? 1.0f / l_run : 0.f;
+  bf16_t* Os = reinterpret_cast<bf16_t*>(smem) + wave * 32 * OLD;
+#pragma unroll
+  for (int ct = 0; ct < HD / 32; ++ct)
+#pragma unroll
+    for (int r = 0; r < 16; ++r) {
+      const int c = ct * 32 + 8 * (r >> 2) + 4 * half + (r & 3);
+      Os[l32 * OLD + c] = f32_to_bf16(o[ct][r] * inv_l);
+    }
+  __syncthreads();
+  for (int c = lane; c < 32 * HD / 8; c += 64) {
+    const int r = c / (HD / 8), ch = (c % (HD / 8)) * 8;
+    const int qr = q0 + wave * 32 + r;
+    if (qr < n)
+      *reinterpret_cast<uint4*>(O + static_cast<int64_t>(lo + qr) * os + h * HD + ch) =
+          *reinterpret_cast<const uint4*>(Os + r * OLD + ch);
+  }
+  if (lse != nullptr && half == 0 && qrow < n)
+    lse[static_cast<int64_t>(h) * T + lo + qrow] = (m_run + log2f(l_run)) * kLn2;
+}
+
+template <typename T, int HD>
+__global__ __launch_bounds__(64) void attn_valu_kernel(const T* __restrict__ Q,
+                                                       const T* __restrict__ K,
+                                                       const T* __restrict__ V, int64_t rs,
+                                                       int causal, float scale,
+                                                       const int32_t* __restrict__ cu,
+                                                       T* __restrict__ O, int64_t os,
+                                                       float* __restrict__ lse, int Tn) {
+  constexpr int BKEY = 32;
+  __shared__ float Ks[BKEY][HD];
+  __shared__ float Vs[BKEY][HD];
+  const int b = blockIdx.z, h = blockIdx.y;
+  const int lo = cu[b];
+  const int n = cu[b + 1] - lo;
+  const int qbase = blockIdx.x * 64;
+  if (qbase >= n) return;
+  const int q = qbase + threadIdx.x;
+  const bool active = q < n;
+  float qv[HD], o[HD];
+#pragma unroll
+  for (int c = 0; c < HD; ++c) {
+    qv[c] = active ? to_f32(Q[static_cast<int64_t>(lo + q) * rs + h * HD + c]) * scale : 0.f;
+    o[c] = 0.f;
+  }
+  float m = -INFINITY, l = 0.f;
+  const int kend = causal ? min(n, qbase + 64) : n;
+  for (int j0 = 0; j0 < kend; j0 += BKEY) {
+    for (int e = threadIdx.x; e < BKEY * HD; e += 64) {
+      const int r = e / HD, c = e % HD;
+      const int j = j0 + r;
+      Ks[r][c] = j < n ? to_f32(K[static_cast<int64_t>(lo + j) * rs + h * HD + c]) : 0.f;
+      Vs[r][c] = j < n ? to_f32(V[static_cast<int64_t>(lo + j) * rs + h * HD + c]) : 0.f;
+    }
+    __syncthreads();
+    if (active) {
+      for (int jj = 0; jj < BKEY; ++jj) {
+        const int j = j0 + jj;
+        if (j >= n || (causal && j > q)) continue;
+        float sc = 0.f;
+#pragma unroll
+        for (int c = 0; c < HD; ++c) sc += qv[c] * Ks[jj][c];
+        if (sc > m) {
+          const float corr = expf(m - sc);
+          l *= corr;
+#pragma unroll
+          for (int c = 0; c < HD; ++c) o[c] *= corr;
+          m = sc;
+        }
+        const float p = expf(sc - m);
+        l += p;
+#pragma unroll
+        for (int c = 0; c < HD; ++c) o[c] += p * Vs[jj][c];
+      }
+    }
+    __syncthreads();
+  }
+  if (active) {
+    const float inv = 1.0f / l;
+#pragma unroll
+    for (int c = 0; c < HD; ++c)
+      O[static_cast<int64_t>(lo + q) * os + h * HD + c] = from_f32<T>(o[c] * inv);
+    if (lse != nullptr) lse[static_cast<int64_t>(h) * Tn + lo + q] = m + logf(l);
+  }
+}
+
+template <typename T>
+hipError_t valu_dispatch(hipStream_t s, const void* q, const void* k, const void* v, int64_t rs,
+                         int H, int hd, int causal, float scale, int B, int max_len, int Trows,
+                         const int32_t* cu, void* out, int64_t os, float* lse) {
+  const dim3 grid((max_len + 63) / 64, H, B), block(64);
+  const T* qp = static_cast<const T*>(q);
+  const T* kp = static_cast<const T*>(k);
+  const T* vp = static_cast<const T*>(v);
+  T* op = static_cast<T*>(out);
+  switch (hd) {
+    case 16: return launch(K_ATTENTION, attn_valu_kernel<T, 16>, grid, block, 0, s, qp, kp, vp, rs, causal, scale, cu, op, os, lse, Trows);
+    case 32: return launch(K_ATTENTION, attn_valu_kernel<T, 32>, grid, block, 0, s, qp, kp, vp, rs, causal, scale, cu, op, os, lse, Trows);
+    case 64: return launch(K_ATTENTION, attn_valu_kernel<T, 64>, grid, block, 0, s, qp, kp, vp, rs, causal, scale, cu, op, os, lse, Trows);
+    case 128: return launch(K_ATTENTION, attn_valu_kernel<T, 128>, grid, block, 0, s, qp, kp, vp, rs, causal, scale, cu, op, os, lse, Trows);
+    default: return hipErrorInvalidValue;
+  }
+}
+
+}  // namespace
+
+hipError_t launch_attention(hipStream_t s, int dtype, const void* q, const void* k,
+                            const void* v, int64_t row_stride, int H, int hd, int causal,
+                            float scale, int B, int max_len, int T, const int32_t* cu_dev,
+                            void* out, int64_t out_stride, float* lse) {
+  if (B == 0 || max_len == 0) return hipSuccess;
+  if (dtype == 1 && (hd == 64 || hd == 128)) {
+    const dim3 grid((max_len + 127) / 128, H, B), block(256);
+    const bf16_t* qp = static_cast<const bf16_t*>(q);
+    const bf16_t* kp = static_cast<const bf16_t*>(k);
+    const bf16_t* vp = static_cast<const bf16_t*>(v);
+    bf16_t* op = static_cast<bf16_t*>(out);
+    const float sl = scale * kLog2e;
+    if (hd == 64)
+      return launch(K_ATTENTION, attn_mfma_kernel<64>, grid, block, 0, s, qp, kp, vp, row_stride,
+                    causal, sl, cu_dev, op, out_stride, lse, T);
+    return launch(K_ATTENTION, attn_mfma_kernel<128>, grid, block, 0, s, qp, kp, vp, row_stride,
+                  causal, sl, cu_dev, op, out_stride, lse, T);
+  }
+  if (dtype == 1)
+    return valu_dispatch<bf16_t>(s, q, k, v, row_stride, H, hd, causal, scale, B, max_len, T,
+                                 cu_dev, out, out_stride, lse);
+  return valu_dispatch<float>(s, q, k, v, row_stride, H, hd, causal, scale, B, max_len, T,
+                              cu_dev, out, out_stride, lse);
+}
+
+}  // namespace zsa

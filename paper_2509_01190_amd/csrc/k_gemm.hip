@@ -1,0 +1,348 @@
+// Projections of the pre-norm block: y = epilogue(x W^T + bias).
+//
+// x [M, K] and W [N, K] are both K-contiguous ("NT" GEMM, PyTorch Linear
+// layout), so every MFMA operand fragment is one 16-byte load of 8
+// consecutive K values from a row of x or of W.
+//
+// bf16: 128x128 output tile per 256-thread workgroup (2x2 waves of 64x64),
+// K step 64, v_mfma_f32_32x32x16_bf16 with fp32 accumulation. Global tiles
+// are staged through registers into double-buffered, row-padded LDS (row
+// stride 72 bf16 = 144 bytes, so the 16 lanes of an LDS read phase hit 16
+// distinct 4-bank groups). One barrier per K step.
+// fp32: a 64x128 vector-ALU tile (4x8 outputs per thread).
+//
+// Both finish through the same epilogue: the fp32 accumulator tile is
+// written to LDS, then each thread produces 8 consecutive outputs of a row
+// (bias, exact GELU, SwiGLU on interleaved gate/up columns, residual add, or
+// the rotary rotation of head channel pairs (i, i+hd/2), which needs the
+// partner column of the same row) and stores them as one 16-byte vector.
+#include <math.h>
+
+#include "zsa_internal.h"
+
+namespace zsa {
+namespace {
+
+typedef __bf16 bf16x8_t __attribute__((ext_vector_type(8)));
+typedef float f32x16_t __attribute__((ext_vector_type(16)));
+
+template <typename T>
+__device__ __forceinline__ void load8(const T* p, float* v);
+template <>
+__device__ __forceinline__ void load8<bf16_t>(const bf16_t* p, float* v) {
+  unpack16(*reinterpret_cast<const uint4*>(p), v, bf16_t());
+}
+template <>
+__device__ __forceinline__ void load8<float>(const float* p, float* v) {
+  unpack16(reinterpret_cast<const uint4*>(p)[0], v, 0.f);
+  unpack16(reinterpret_cast<const uint4*>(p)[1], v + 4, 0.f);
+}
+template <typename T>
+__device__ __forceinline__ void store8(T* p, const float* v);
+template <>
+__device__ __forceinline__ void store8<bf16_t>(bf16_t* p, const float* v) {
+  *reinterpret_cast<uint4*>(p) = pack16(v, bf16_t());
+}
+template <>
+__device__ __forceinline__ void store8<float>(float* p, const float* v) {
+  reinterpret_cast<uint4*>(p)[0] = pack16(v, 0.f);
+  reinterpret_cast<uint4*>(p)[1] = pack16(v + 4, 0.f);
+}
+
+// angle reduction for the rotary epilogue: the angle pos * inv_freq is
+// formed in double and reduced to [-pi, pi] with a two-constant
+// (Cody-Waite) subtraction of multiples of 2*pi before the fp32 sincos.
+__device__ __forceinline__ void rope_sincos(int p, double inv_freq, float* s, float* c) {
+  const double two_pi_hi = 6.283185307179586;       // nearest double to 2*pi
+  const double two_pi_lo = 2.4492935982947064e-16;  // 2*pi - two_pi_hi
+  const double a = static_cast<double>(p) * inv_freq;
+  const double q = rint(a * 0.15915494309189535);   // a / (2*pi)
+  double r = fma(-q, two_pi_hi, a);
+  r = fma(-q, two_pi_lo, r);
+  sincosf(static_cast<float>(r), s, c);
+}
+
+__device__ __forceinline__ float gelu_erf(float z) {
+  return 0.5f * z * (1.0f + erff(z * 0.70710678118654752f));
+}
+__device__ __forceinline__ float silu(float z) { return z / (1.0f + expf(-z)); }
+
+// tile: fp32 [BM][ldt] in LDS holding (x W^T) for rows m0.., columns n0..
+template <typename T, int BM, int BN, int NT>
+__device__ void epilogue_tile(const float* tile, int ldt, int m0, int n0, int M, int N,
+                              const EpiParams& ep) {
+  const T* bias = static_cast<const T*>(ep.bias);
+  T* y = static_cast<T*>(ep.y);
+  const int tid = threadIdx.x;
+  if (ep.epi == EPI_SWIGLU) {
+    constexpr int OPR = BN / 2 / 8;  // 8-wide output items per row
+    for (int it = tid; it < BM * OPR; it += NT) {
+      const int r = it / OPR;
+      const int cv = it - r * OPR;
+      const int m = m0 + r;
+      const int oc = n0 / 2 + cv * 8;
+      if (m >= M || oc >= N / 2) continue;
+      float out[8];
+#pragma unroll
+      for (int e = 0; e < 8; ++e) {
+        const int zc = 2 * (cv * 8 + e);
+        float g = tile[r * ldt + zc];
+        float u = tile[r * ldt + zc + 1];
+        if (bias != nullptr) {
+          g += to_f32(bias[n0 + zc]);
+          u += to_f32(bias[n0 + zc + 1]);
+        }
+        out[e] = silu(g) * u;
+      }
+      store8<T>(y + static_cast<int64_t>(m) * ep.ldy + oc, out);
+    }
+    return;
+  }
+  constexpr int IPR = BN / 8;
+  const int hd = ep.head_dim;
+  const int half = hd >> 1;
+  for (int it = tid; it < BM * IPR; it += NT) {
+    const int r = it / IPR;
+    const int cv = it - r * IPR;
+    const int m = m0 + r;
+    const int n = n0 + cv * 8;
+    if (m >= M || n >= N) continue;
+    float z[8];
+#pragma unroll
+    for (int e = 0; e < 8; ++e) z[e] = tile[r * ldt + cv * 8 + e];
+    if (bias != nullptr) {
+      float bv[8];
+      load8<T>(bias + n, bv);
+#pragma unroll
+      for (int e = 0; e < 8; ++e) z[e] += bv[e];
+    }
+    if (ep.epi == EPI_GELU) {
+#pragma unroll
+      for (int e = 0; e < 8; ++e) z[e] = gelu_erf(z[e]);
+    } else if (ep.epi == EPI_RESIDUAL) {
+      float rv[8];
+      load8<T>(static_cast<const T*>(ep.residual) + static_cast<int64_t>(m) * ep.ldy + n, rv);
+#pragma unroll
+      for (int e = 0; e < 8; ++e) z[e] += rv[e];
+    } else if (ep.epi == EPI_ROPE && n < ep.rope_cols) {
+      const int p = ep.pos[m];
+      const int c0 = n % hd;  // head-local channel of the first of the 8 outputs
+      const bool lower = c0 < half;
+      const int pcol = cv * 8 + (lower ? half : -half);  // partner columns in the tile
+      float pb[8];
+      if (bias != nullptr) {
+        load8<T>(bias + n + (lower ? half : -half), pb);
+      } else {
+#pragma unroll
+        for (int e = 0; e < 8; ++e) pb[e] = 0.f;
+      }
+#pragma unroll
+      for (int e = 0; e < 8; ++e) {
+        const float zp = tile[r * ldt + pcol + e] + pb[e];
+        const int i = (c0 + e) - (lower ? 0 : half);
+        float sn, cs;
+        rope_sincos(p, ep.inv_freq[i], &sn, &cs);
+        z[e] = lower ? (z[e] * cs - zp * sn) : (z[e] * cs + zp * sn);
+      }
+    }
+    store8<T>(y + static_cast<int64_t>(m) * ep.ldy + n, z);
+  }
+}
+
+// ---------------------------------------------------------------------------
+// bf16 MFMA GEMM
+// ---------------------------------------------------------------------------
+constexpr int kBM = 128, kBN = 128, kBK = 64, kLDK = kBK + 8;
+constexpr int kMfmaLds = 2 * (kBM + kBN) * kLDK * 2;  // bytes, double-buffered A and B
+constexpr int kTileLd = kBN + 4;
+static_assert(kBM * kTileLd * 4 <= kMfmaLds, "epilogue tile must fit in the operand buffers");
+
+__global__ __launch_bounds__(256) void gemm_bf16_mfma_kernel(const bf16_t* __restrict__ X,
+                                                             const bf16_t* __restrict__ W,
+                                                             int M, int N, int K, EpiParams ep) {
+  extern __shared__ __align__(16) unsigned char smem[];
+  bf16_t* As = reinterpret_cast<bf16_t*>(smem);  // [2][kBM][kLDK]
+  bf16_t* Bs = As + 2 * kBM * kLDK;              // [2][kBN][kLDK]
+  const int tid = threadIdx.x;
+  const int lane = tid & 63;
+  const int wave = tid >> 6;
+  const int wm = wave >> 1, wn = wave & 1;
+  const int m0 = blockIdx.x * kBM;
+  const int n0 = blockIdx.y * kBN;
+  constexpr int TM = kBM / 2 / 32, TN = kBN / 2 / 32;
+  constexpr int ACH = kBM * kBK / 8 / 256, BCH = kBN * kBK / 8 / 256;
+
+  uint4 ra[ACH], rb[BCH];
+  const uint4 zero = make_uint4(0, 0, 0, 0);
+  auto gload = [&](int k0) {
+#pragma unroll
+    for (int i = 0; i < ACH; ++i) {
+      const int c = tid + i * 256;
+      const int r = c >> 3, kc = (c & 7) * 8;
+      const int gm = m0 + r;
+      ra[i] = gm < M ? *reinterpret_cast<const uint4*>(X + static_cast<int64_t>(gm) * K + k0 + kc)
+                     : zero;
+    }
+#pragma unroll
+    for (int i = 0; i < BCH; ++i) {
+      const int c = tid + i * 256;
+      const int r = c >> 3, kc = (c & 7) * 8;
+      const int gn = n0 + r;
+      rb[i] = gn < N ? *reinterpret_cast<const uint4*>(W + static_cast<int64_t>(gn) * K + k0 + kc)
+                     : zero;
+    }
+  };
+  auto sstore = [&](int buf) {
+#pragma unroll
+    for (int i = 0; i < ACH; ++i) {
+      const int c = tid + i * 256;
+      const int r = c >> 3, kc = (c & 7) * 8;
+      *reinterpret_cast<uint4*>(As + (buf * kBM + r) * kLDK + kc) = ra[i];
+    }
+#pragma unroll
+    for (int i = 0; i < BCH; ++i) {
+      const int c = tid + i * 256;
+      const int r = c >> 3, kc = (c & 7) * 8;
+      *reinterpret_cast<uint4*>(Bs + (buf * kBN + r) * kLDK + kc) = rb[i];
+    }
+  };
+
+  f32x16_t acc[TM][TN];
+#pragma unroll
+  for (int i = 0; i < TM; ++i)
+#pragma unroll
+    for (int j = 0; j < TN; ++j)
+#pragma unroll
+      for (int r = 0; r < 16; ++r) acc[i][j][r] = 0.f;
+
+  const int KT = K / kBK;
+  gload(0);
+  sstore(0);
+  __syncthreads();
+  for (int kt = 0; kt < KT; ++kt) {
+    const int buf = kt & 1;
+    if (kt + 1 < KT) gload((kt + 1) * kBK);
+    const bf16_t* Ab = As + (buf * kBM + wm * (kBM / 2) + (lane & 31)) * kLDK + (lane >> 5) * 8;
+    const bf16_t* Bb = Bs + (buf * kBN + wn * (kBN / 2) + (lane & 31)) * kLDK + (lane >> 5) * 8;
+#pragma unroll
+    for (int kk = 0; kk < kBK / 16; ++kk) {
+      bf16x8_t a[TM], b[TN];
+#pragma unroll
+      for (int i = 0; i < TM; ++i)
+        a[i] = __builtin_bit_cast(bf16x8_t,
+                                  *reinterpret_cast<const uint4*>(Ab + i * 32 * kLDK + kk * 16));
+#pragma unroll
+      for (int j = 0; j < TN; ++j)
+        b[j] = __builtin_bit_cast(bf16x8_t,
+                                  *reinterpret_cast<const uint4*>(Bb + j * 32 * kLDK + kk * 16));
+#pragma unroll
+      for (int i = 0; i < TM; ++i)
+#pragma unroll
+        for (int j = 0; j < TN; ++j)
+          acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a[i], b[j], acc[i][j], 0, 0, 0);
+    }
+    if (kt + 1 < KT) sstore(buf ^ 1);
+    __syncthreads();
+  }
+
+  // accumulator layout of a 32x32 MFMA tile: lane l, register r holds
+  // row 8*(r/4) + 4*(l/32) + r%4, column l%32
+  float* tile = reinterpret_cast<float*>(smem);
+#pragma unroll
+  for (int i = 0; i < TM; ++i)
+#pragma unroll
+    for (int j = 0; j < TN; ++j)
+#pragma unroll
+      for (int r = 0; r < 16; ++r) {
+        const int row = wm * (kBM / 2) + i * 32 + (r >> 2) * 8 + (lane >> 5) * 4 + (r & 3);
+        const int col = wn * (kBN / 2) + j * 32 + (lane & 31);
+        tile[row * kTileLd + col] = acc[i][j][r];
+      }
+  __syncthreads();
+  epilogue_tile<bf16_t, kBM, kBN, 256>(tile, kTileLd, m0, n0, M, N, ep);
+}
+
+// ---------------------------------------------------------------------------
+// vector-ALU GEMM (fp32 storage, and any shape)
+// ---------------------------------------------------------------------------
+constexpr int vBM = 64, vBN = 128, vBK = 16;
+
+template <typename T>
+__global__ __launch_bounds__(256) void gemm_valu_kernel(const T* __restrict__ X,
+                                                        const T* __restrict__ W, int M, int N,
+                                                        int K, EpiParams ep) {
+  __shared__ float As[vBK][vBM + 4];
+  __shared__ float Bs[vBK][vBN + 4];
+  __shared__ float tile[vBM * (vBN + 4)];
+  const int tid = threadIdx.x;
+  const int tx = tid & 15, ty = tid >> 4;
+  const int m0 = blockIdx.x * vBM, n0 = blockIdx.y * vBN;
+  float acc[4][8];
+#pragma unroll
+  for (int i = 0; i < 4; ++i)
+#pragma unroll
+    for (int j = 0; j < 8; ++j) acc[i][j] = 0.f;
+  for (int k0 = 0; k0 < K; k0 += vBK) {
+#pragma unroll
+    for (int i = 0; i < vBM * vBK / 256; ++i) {
+      const int e = tid + i * 256;
+      const int mm = e / vBK, kk = e % vBK;
+      const int gm = m0 + mm, gk = k0 + kk;
+      As[kk][mm] = (gm < M && gk < K) ? to_f32(X[static_cast<int64_t>(gm) * K + gk]) : 0.f;
+    }
+#pragma unroll
+    for (int i = 0; i < vBN * vBK / 256; ++i) {
+      const int e = tid + i * 256;
+      const int nn = e / vBK, kk = e % vBK;
+      const int gn = n0 + nn, gk = k0 + kk;
+      Bs[kk][nn] = (gn < N && gk < K) ? to_f32(W[static_cast<int64_t>(gn) * K + gk]) : 0.f;
+    }
+    __syncthreads();
+#pragma unroll
+    for (int kk = 0; kk < vBK; ++kk) {
+      float a[4], b[8];
+#pragma unroll
+      for (int i = 0; i < 4; ++i) a[i] = As[kk][ty * 4 + i];
+#pragma unroll
+      for (int j = 0; j < 8; ++j) b[j] = Bs[kk][tx * 8 + j];
+#pragma unroll
+      for (int i = 0; i < 4; ++i)
+#pragma unroll
+        for (int j = 0; j < 8; ++j) acc[i][j] += a[i] * b[j];
+    }
+    __syncthreads();
+  }
+#pragma unroll
+  for (int i = 0; i < 4; ++i)
+#pragma unroll
+    for (int j = 0; j < 8; ++j) tile[(ty * 4 + i) * (vBN + 4) + tx * 8 + j] = acc[i][j];
+  __syncthreads();
+  epilogue_tile<T, vBM, vBN, 256>(tile, vBN + 4, m0, n0, M, N, ep);
+}
+
+}  // namespace
+
+hipError_t launch_gemm(hipStream_t s, int dtype, const void* x, int M, int K, const void* w,
+                       int N, const EpiParams& ep) {
+  if (M == 0 || N == 0) return hipSuccess;
+  if (dtype == 1 && K % kBK == 0) {
+    static bool lds_raised = false;  // > 64 KiB of dynamic LDS per workgroup
+    if (!lds_raised) {
+      const hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void*>(gemm_bf16_mfma_kernel),
+                                               hipFuncAttributeMaxDynamicSharedMemorySize, kMfmaLds);
+      if (e != hipSuccess) return e;
+      lds_raised = true;
+    }
+    const dim3 grid((M + kBM - 1) / kBM, (N + kBN - 1) / kBN);
+    return launch(K_GEMM, gemm_bf16_mfma_kernel, grid, dim3(256), kMfmaLds, s,
+                  static_cast<const bf16_t*>(x), static_cast<const bf16_t*>(w), M, N, K, ep);
+  }
+  const dim3 grid((M + vBM - 1) / vBM, (N + vBN - 1) / vBN);
+  if (dtype == 1)
+    return launch(K_GEMM, gemm_valu_kernel<bf16_t>, grid, dim3(256), 0, s,
+                  static_cast<const bf16_t*>(x), static_cast<const bf16_t*>(w), M, N, K, ep);
+  return launch(K_GEMM, gemm_valu_kernel<float>, grid, dim3(256), 0, s,
+                static_cast<const float*>(x), static_cast<const float*>(w), M, N, K, ep);
+}
+
+}  // namespace zsa

@@ -1,0 +1,761 @@
+// C-ABI of libzsa: argument validation, the Eq. 2 keep-count schedule,
+// workspace layout and the orchestration of the per-layer kernels.
+// Everything here runs on the host and only enqueues work on the caller's
+// stream; no call synchronises, allocates device memory or copies from host
+// memory (host values reach kernels as launch arguments).
+#include <math.h>
+#include <stdarg.h>
+#include <stdio.h>
+#include <string.h>
+
+#include <string>
+#include <vector>
+
+#include "../../include/zsa.h"
+#include "zsa_internal.h"
+
+namespace {
+
+thread_local std::string g_err;
+
+int fail(int code, const char* fmt, ...) {
+  char buf[512];
+  va_list ap;
+  va_start(ap, fmt);
+  vsnprintf(buf, sizeof(buf), fmt, ap);
+  va_end(ap);
+  g_err = buf;
+  return code;
+}
+
+int hip_fail(hipError_t e, const char* what) {
+  return fail(ZSA_EHIP, "%s: %s", what, hipGetErrorString(e));
+}
+
+#define HIP_TRY(expr, what)                          \
+  do {                                               \
+    const hipError_t e_ = (expr);                    \
+    if (e_ != hipSuccess) return hip_fail(e_, what); \
+  } while (0)
+
+#define CHECK(expr)            \
+  do {                         \
+    const int rc_ = (expr);    \
+    if (rc_ != ZSA_OK) return rc_; \
+  } while (0)
+
+inline bool aligned16(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 15u) == 0; }
+inline size_t esize(int dtype) { return dtype == ZSA_BF16 ? 2 : 4; }
+inline size_t round256(size_t b) { return (b + 255) & ~static_cast<size_t>(255); }
+
+// Eq. 2 for one sequence. The product and the sum are two separately
+// rounded IEEE double operations (the volatile store keeps the compiler from
+// fusing them), exactly as written: floor(alpha * n + 1e-9), clipped to
+// [tau, n] (never above n).
+int32_t keep_count_impl(int32_t n, double alpha, int32_t tau) {
+  volatile double prod = alpha * static_cast<double>(n);
+  const double v = prod + 1e-9;
+  int64_t k = static_cast<int64_t>(floor(v));
+  if (k < tau) k = tau;
+  if (k > n) k = n;
+  return static_cast<int32_t>(k);
+}
+
+int check_rate(double a) {
+  if (!(a >= 0.0 && a <= 1.0))  // also rejects NaN
+    return fail(ZSA_EINVAL, "keep rate %g is NaN or outside [0, 1]", a);
+  return ZSA_OK;
+}
+
+// validate packed sequence offsets; returns total rows and the longest length
+int check_seqs(int32_t batch, const int32_t* cu_host, const int32_t* cu_dev, int32_t* total,
+               int32_t* max_len) {
+  if (batch < 0) return fail(ZSA_EINVAL, "batch %d < 0", batch);
+  if (cu_host == nullptr || cu_dev == nullptr) return fail(ZSA_EINVAL, "cu_host / cu_dev is NULL");
+  if (cu_host[0] != 0) return fail(ZSA_ESHAPE, "cu[0] = %d, must be 0", cu_host[0]);
+  int32_t ml = 0;
+  for (int b = 0; b < batch; ++b) {
+    const int32_t len = cu_host[b + 1] - cu_host[b];
+    if (len < 0) return fail(ZSA_ESHAPE, "cu not monotone at sequence %d", b);
+    if (len > ml) ml = len;
+  }
+  *total = cu_host[batch];
+  *max_len = ml;
+  return ZSA_OK;
+}
+
+int check_dtype(int32_t dtype) {
+  if (dtype != ZSA_F32 && dtype != ZSA_BF16) return fail(ZSA_EINVAL, "dtype %d unknown", dtype);
+  return ZSA_OK;
+}
+
+int check_ptr16(const void* p, const char* name, bool may_be_null = false) {
+  if (p == nullptr) {
+    if (may_be_null) return ZSA_OK;
+    return fail(ZSA_EINVAL, "%s is NULL", name);
+  }
+  if (!aligned16(p)) return fail(ZSA_EALIGN, "%s is not 16-byte aligned", name);
+  return ZSA_OK;
+}
+
+int check_width(int32_t dtype, int64_t width, const char* name) {
+  if (width <= 0) return fail(ZSA_ESHAPE, "%s = %lld must be positive", name, (long long)width);
+  if ((width * static_cast<int64_t>(esize(dtype))) % 16 != 0)
+    return fail(ZSA_EALIGN, "%s = %lld rows are not a multiple of 16 bytes", name, (long long)width);
+  return ZSA_OK;
+}
+
+int check_head_dim(int32_t hd) {
+  if (hd != 16 && hd != 32 && hd != 64 && hd != 128)
+    return fail(ZSA_EUNSUPPORTED, "head_dim %d (supported: 16, 32, 64, 128)", hd);
+  return ZSA_OK;
+}
+
+int check_cfg(const zsa_layer_cfg* c) {
+  if (c == nullptr) return fail(ZSA_EINVAL, "cfg is NULL");
+  if (c->kind != ZSA_ENCODER && c->kind != ZSA_DECODER) return fail(ZSA_EINVAL, "kind %d", c->kind);
+  CHECK(check_dtype(c->dtype));
+  if (c->n_heads <= 0 || c->head_dim <= 0 || c->n_heads * c->head_dim != c->d_model)
+    return fail(ZSA_ESHAPE, "n_heads %d * head_dim %d != d_model %d", c->n_heads, c->head_dim,
+                c->d_model);
+  CHECK(check_head_dim(c->head_dim));
+  CHECK(check_width(c->dtype, c->d_model, "d_model"));
+  CHECK(check_width(c->dtype, c->d_ff, "d_ff"));
+  if (c->d_model % 8 != 0 || c->d_ff % 8 != 0)
+    return fail(ZSA_EUNSUPPORTED, "d_model and d_ff must be multiples of 8");
+  if (c->d_model > (c->dtype == ZSA_BF16 ? 8192 : 4096))
+    return fail(ZSA_EUNSUPPORTED, "d_model %d above the row-norm limit", c->d_model);
+  if (c->tau < 1) return fail(ZSA_EINVAL, "tau %d < 1", c->tau);
+  if (!(c->norm_eps >= 0.f)) return fail(ZSA_EINVAL, "norm_eps must be >= 0");
+  if (c->kind == ZSA_DECODER && !(c->rope_theta > 0.f)) return fail(ZSA_EINVAL, "rope_theta <= 0");
+  return ZSA_OK;
+}
+
+int check_weights(const zsa_layer_cfg* c, const zsa_layer_weights* w) {
+  if (w == nullptr) return fail(ZSA_EINVAL, "weights are NULL");
+  CHECK(check_ptr16(w->norm1_w, "norm1_w"));
+  CHECK(check_ptr16(w->w_qkv, "w_qkv"));
+  CHECK(check_ptr16(w->w_o, "w_o"));
+  CHECK(check_ptr16(w->norm2_w, "norm2_w"));
+  CHECK(check_ptr16(w->w_up, "w_up"));
+  CHECK(check_ptr16(w->w_down, "w_down"));
+  CHECK(check_ptr16(w->b_qkv, "b_qkv", true));
+  CHECK(check_ptr16(w->b_o, "b_o", true));
+  CHECK(check_ptr16(w->b_up, "b_up", true));
+  CHECK(check_ptr16(w->b_down, "b_down", true));
+  if (c->kind == ZSA_ENCODER) {
+    CHECK(check_ptr16(w->norm1_b, "norm1_b", true));
+    CHECK(check_ptr16(w->norm2_b, "norm2_b", true));
+  }
+  return ZSA_OK;
+}
+
+// ---------------------------------------------------------------------------
+// workspace layout
+// ---------------------------------------------------------------------------
+struct LayerBufs {
+  void* h;
+  void* qkv;
+  void* o;
+  void* f;
+  void* xg;
+  void* og;
+  float* lse;
+  float* partials;
+  int32_t* kept;
+};
+
+struct Carver {
+  size_t off = 0;
+  size_t take(size_t bytes) {
+    const size_t o = off;
+    off += round256(bytes);
+    return o;
+  }
+};
+
+struct LayerLayout {
+  size_t h, qkv, o, f, xg, og, lse, partials, kept, end;
+};
+
+LayerLayout layer_layout(const zsa_layer_cfg* c, int64_t T, Carver& cv) {
+  const size_t e = esize(c->dtype);
+  const int64_t d = c->d_model, F = c->d_ff;
+  // a later (shorter) layer may pick more head groups; H is the upper bound
+  const int G = c->n_heads;
+  LayerLayout L;
+  L.h = cv.take(T * d * e);
+  L.qkv = cv.take(T * 3 * d * e);
+  L.o = cv.take(T * d * e);
+  L.f = cv.take(T * F * e);
+  L.xg = cv.take(T * d * e);
+  L.og = cv.take(T * d * e);
+  L.lse = cv.take(static_cast<size_t>(c->n_heads) * T * 4);
+  L.partials = cv.take(static_cast<size_t>(G) * T * 4);
+  L.kept = cv.take(T * 4);
+  L.end = cv.off;
+  return L;
+}
+
+LayerBufs carve_layer(const LayerLayout& L, void* ws) {
+  char* base = static_cast<char*>(ws);
+  LayerBufs b;
+  b.h = base + L.h;
+  b.qkv = base + L.qkv;
+  b.o = base + L.o;
+  b.f = base + L.f;
+  b.xg = base + L.xg;
+  b.og = base + L.og;
+  b.lse = reinterpret_cast<float*>(base + L.lse);
+  b.partials = reinterpret_cast<float*>(base + L.partials);
+  b.kept = reinterpret_cast<int32_t*>(base + L.kept);
+  return b;
+}
+
+// ---------------------------------------------------------------------------
+// one block
+// ---------------------------------------------------------------------------
+struct RowSet {
+  int32_t B;
+  const int32_t* cu_host;
+  const int32_t* cu_dev;
+  int32_t T;
+  int32_t max_len;
+};
+
+void fill_rope(zsa::EpiParams& ep, int hd, float theta) {
+  for (int i = 0; i < zsa::kMaxHalfHead; ++i)
+    ep.inv_freq[i] = i < hd / 2 ? pow(static_cast<double>(theta), -2.0 * i / hd) : 0.0;
+}
+
+int run_layer(hipStream_t s, const zsa_layer_cfg& c, const zsa_layer_weights& w,
+              const void* x_in, const int32_t* pos_in, const RowSet& in, bool prune,
+              const RowSet& out, void* x_out, int32_t* pos_out, float* scores_out,
+              int32_t* kept_out, const LayerBufs& wb) {
+  using namespace zsa;
+  const int dt = c.dtype;
+  const size_t e = esize(dt);
+  const int d = c.d_model, H = c.n_heads, hd = c.head_dim, F = c.d_ff;
+  const bool dec = c.kind == ZSA_DECODER;
+  const int norm_kind = dec ? ZSA_NORM_RMS : ZSA_NORM_LAYER;
+  const float scale = 1.0f / sqrtf(static_cast<float>(hd));
+
+  HIP_TRY(launch_norm(s, dt, norm_kind, x_in, w.norm1_w, dec ? nullptr : w.norm1_b, in.T, d,
+                      c.norm_eps, wb.h),
+          "norm1");
+  {
+    EpiParams ep{};
+    ep.epi = dec ? EPI_ROPE : EPI_NONE;
+    ep.bias = w.b_qkv;
+    ep.y = wb.qkv;
+    ep.ldy = 3 * d;
+    ep.pos = pos_in;
+    ep.head_dim = hd;
+    ep.rope_cols = dec ? 2 * d : 0;
+    if (dec) fill_rope(ep, hd, c.rope_theta);
+    HIP_TRY(launch_gemm(s, dt, wb.h, in.T, d, w.w_qkv, 3 * d, ep), "qkv projection");
+  }
+  const char* qkv = static_cast<const char*>(wb.qkv);
+  const void* q = qkv;
+  const void* k = qkv + d * e;
+  const void* v = qkv + 2 * d * e;
+  HIP_TRY(launch_attention(s, dt, q, k, v, 3 * d, H, hd, c.causal, scale, in.B, in.max_len, in.T,
+                           in.cu_dev, wb.o, d, wb.lse),
+          "attention");
+  const void* xr = x_in;
+  const void* orows = wb.o;
+  int rows = in.T;
+  if (prune) {
+    const int G = score_groups(dt, H, hd, in.T);
+    HIP_TRY(launch_score(s, dt, q, k, 3 * d, wb.lse, H, hd, c.causal, scale, in.B, in.max_len,
+                         in.T, in.cu_dev, wb.partials, G),
+            "score");
+    int32_t* kept = kept_out != nullptr ? kept_out : wb.kept;
+    HIP_TRY(launch_select(s, wb.partials, G, in.T, in.B, in.max_len, in.cu_dev, out.cu_dev, kept,
+                          scores_out),
+            "select");
+    HIP_TRY(launch_gather(s, dt, d, in.T, kept, out.T, x_in, wb.xg, wb.o, wb.og, pos_in, pos_out),
+            "gather");
+    xr = wb.xg;
+    orows = wb.og;
+    rows = out.T;
+  }
+  {
+    EpiParams ep{};
+    ep.epi = EPI_RESIDUAL;
+    ep.bias = w.b_o;
+    ep.residual = xr;
+    ep.y = x_out;
+    ep.ldy = d;
+    HIP_TRY(launch_gemm(s, dt, orows, rows, d, w.w_o, d, ep), "output projection");
+  }
+  HIP_TRY(launch_norm(s, dt, norm_kind, x_out, w.norm2_w, dec ? nullptr : w.norm2_b, rows, d,
+                      c.norm_eps, wb.h),
+          "norm2");
+  {
+    EpiParams ep{};
+    ep.epi = dec ? EPI_SWIGLU : EPI_GELU;
+    ep.bias = w.b_up;
+    ep.y = wb.f;
+    ep.ldy = F;
+    HIP_TRY(launch_gemm(s, dt, wb.h, rows, d, w.w_up, dec ? 2 * F : F, ep), "up projection");
+  }
+  {
+    EpiParams ep{};
+    ep.epi = EPI_RESIDUAL;
+    ep.bias = w.b_down;
+    ep.residual = x_out;
+    ep.y = x_out;
+    ep.ldy = d;
+    HIP_TRY(launch_gemm(s, dt, wb.f, rows, F, w.w_down, d, ep), "down projection");
+  }
+  return ZSA_OK;
+}
+
+// ---------------------------------------------------------------------------
+// timing hook
+// ---------------------------------------------------------------------------
+struct TimingState {
+  bool armed = false;
+  int used = 0;
+  std::vector<hipEvent_t> start, stop;
+};
+TimingState g_timing[zsa::K_NCLASS];
+
+}  // namespace
+
+namespace zsa {
+bool timing_take(int kclass, hipEvent_t* start, hipEvent_t* stop) {
+  if (kclass < 0 || kclass >= K_NCLASS) return false;
+  TimingState& t = g_timing[kclass];
+  if (!t.armed || t.used >= static_cast<int>(t.start.size())) return false;
+  *start = t.start[t.used];
+  *stop = t.stop[t.used];
+  ++t.used;
+  return true;
+}
+}  // namespace zsa
+
+// ===========================================================================
+// exported entry points
+// ===========================================================================
+extern "C" {
+
+const char* zsa_last_error(void) { return g_err.c_str(); }
+const char* zsa_version(void) { return "zsa 0.1 gfx950"; }
+
+int zsa_keep_count(int32_t n, double keep_rate, int32_t tau, int32_t* k_out) {
+  if (k_out == nullptr) return fail(ZSA_EINVAL, "k_out is NULL");
+  CHECK(check_rate(keep_rate));
+  if (tau < 1) return fail(ZSA_EINVAL, "tau %d < 1", tau);
+  if (n < 0) return fail(ZSA_EINVAL, "n %d < 0", n);
+  *k_out = keep_count_impl(n, keep_rate, tau);
+  return ZSA_OK;
+}
+
+int zsa_keep_schedule(int32_t batch, const int32_t* lengths, const double* keep_rate, int32_t tau,
+                      int32_t n_points, int32_t* counts_out) {
+  if (batch < 0 || n_points < 0) return fail(ZSA_EINVAL, "negative batch or n_points");
+  if (batch > 0 && (lengths == nullptr || keep_rate == nullptr || counts_out == nullptr))
+    return fail(ZSA_EINVAL, "NULL array");
+  if (tau < 1) return fail(ZSA_EINVAL, "tau %d < 1", tau);
+  for (int b = 0; b < batch; ++b) {
+    CHECK(check_rate(keep_rate[b]));
+    if (lengths[b] < 0) return fail(ZSA_EINVAL, "length %d < 0", lengths[b]);
+  }
+  for (int b = 0; b < batch; ++b) {
+    int32_t cur = lengths[b];
+    for (int p = 0; p < n_points; ++p) {
+      cur = keep_count_impl(cur, keep_rate[b], tau);
+      counts_out[p * batch + b] = cur;
+    }
+  }
+  return ZSA_OK;
+}
+
+int zsa_norm(void* stream, int32_t dtype, int32_t kind, const void* x, const void* gain,
+             const void* shift, int32_t rows, int32_t d, float eps, void* y) {
+  CHECK(check_dtype(dtype));
+  if (kind != ZSA_NORM_LAYER && kind != ZSA_NORM_RMS) return fail(ZSA_EINVAL, "norm kind %d", kind);
+  if (rows < 0) return fail(ZSA_EINVAL, "rows < 0");
+  CHECK(check_width(dtype, d, "d"));
+  if (d > (dtype == ZSA_BF16 ? 8192 : 4096)) return fail(ZSA_EUNSUPPORTED, "d %d too wide", d);
+  CHECK(check_ptr16(x, "x"));
+  CHECK(check_ptr16(gain, "gain"));
+  CHECK(check_ptr16(y, "y"));
+  CHECK(check_ptr16(shift, "shift", true));
+  HIP_TRY(zsa::launch_norm(static_cast<hipStream_t>(stream), dtype, kind, x, gain,
+                           kind == ZSA_NORM_LAYER ? shift : nullptr, rows, d, eps, y),
+          "norm");
+  return ZSA_OK;
+}
+
+int zsa_linear(void* stream, int32_t dtype, const void* x, int32_t m, int32_t k, const void* w,
+               int32_t n, const void* bias, int32_t epilogue, const void* residual,
+               const int32_t* pos, int32_t head_dim, int32_t rope_cols, float rope_theta,
+               void* y) {
+  CHECK(check_dtype(dtype));
+  if (m < 0) return fail(ZSA_EINVAL, "m < 0");
+  CHECK(check_width(dtype, k, "k"));
+  if (n <= 0 || n % 8 != 0) return fail(ZSA_ESHAPE, "n %d must be a positive multiple of 8", n);
+  if (epilogue < ZSA_EPI_NONE || epilogue > ZSA_EPI_ROPE) return fail(ZSA_EINVAL, "epilogue %d", epilogue);
+  if (epilogue == ZSA_EPI_SWIGLU && n % 16 != 0)
+    return fail(ZSA_ESHAPE, "SwiGLU needs n %% 16 == 0 (n = %d)", n);
+  CHECK(check_ptr16(x, "x"));
+  CHECK(check_ptr16(w, "w"));
+  CHECK(check_ptr16(y, "y"));
+  CHECK(check_ptr16(bias, "bias", true));
+  if (epilogue == ZSA_EPI_RESIDUAL) CHECK(check_ptr16(residual, "residual"));
+  zsa::EpiParams ep{};
+  ep.epi = epilogue;
+  ep.bias = bias;
+  ep.residual = residual;
+  ep.y = y;
+  ep.ldy = epilogue == ZSA_EPI_SWIGLU ? n / 2 : n;
+  if (epilogue == ZSA_EPI_ROPE) {
+    if (head_dim != 16 && head_dim != 32 && head_dim != 64 && head_dim != 128)
+      return fail(ZSA_EUNSUPPORTED, "rotary head_dim %d", head_dim);
+    if (rope_cols < 0 || rope_cols % head_dim != 0 || rope_cols > n)
+      return fail(ZSA_ESHAPE, "rope_cols %d", rope_cols);
+    if (pos == nullptr && m > 0) return fail(ZSA_EINVAL, "pos is NULL");
+    if (!(rope_theta > 0.f)) return fail(ZSA_EINVAL, "rope_theta <= 0");
+    ep.pos = pos;
+    ep.head_dim = head_dim;
+    ep.rope_cols = rope_cols;
+    fill_rope(ep, head_dim, rope_theta);
+  }
+  HIP_TRY(zsa::launch_gemm(static_cast<hipStream_t>(stream), dtype, x, m, k, w, n, ep), "linear");
+  return ZSA_OK;
+}
+
+size_t zsa_attention_workspace_size(int32_t n_heads, int32_t total_rows, int32_t want_scores) {
+  if (n_heads <= 0 || total_rows < 0) return 0;
+  size_t b = round256(static_cast<size_t>(n_heads) * total_rows * 4);  // lse scratch
+  if (want_scores) b += round256(static_cast<size_t>(n_heads) * total_rows * 4);  // partials
+  return b;
+}
+
+int zsa_attention_with_scores(void* stream, int32_t dtype, const void* q, const void* k,
+                              const void* v, int64_t row_stride, int32_t n_heads,
+                              int32_t head_dim, int32_t causal, float scale, int32_t batch,
+                              const int32_t* cu_host, const int32_t* cu_dev, void* out,
+                              int64_t out_stride, float* lse, float* scores, void* ws,
+                              size_t ws_bytes) {
+  CHECK(check_dtype(dtype));
+  CHECK(check_head_dim(head_dim));
+  if (n_heads <= 0) return fail(ZSA_EINVAL, "n_heads %d", n_heads);
+  int32_t T, max_len;
+  CHECK(check_seqs(batch, cu_host, cu_dev, &T, &max_len));
+  CHECK(check_ptr16(q, "q"));
+  CHECK(check_ptr16(k, "k"));
+  CHECK(check_ptr16(v, "v"));
+  CHECK(check_ptr16(out, "out"));
+  CHECK(check_width(dtype, row_stride, "row_stride"));
+  CHECK(check_width(dtype, out_stride, "out_stride"));
+  if (row_stride < static_cast<int64_t>(n_heads) * head_dim || out_stride < static_cast<int64_t>(n_heads) * head_dim)
+    return fail(ZSA_ESHAPE, "row stride shorter than n_heads * head_dim");
+  if (!(scale > 0.f)) return fail(ZSA_EINVAL, "scale must be positive");
+  const size_t need = zsa_attention_workspace_size(n_heads, T, scores != nullptr);
+  if (scores != nullptr || lse == nullptr) {
+    if (ws_bytes < need || (need > 0 && ws == nullptr))
+      return fail(ZSA_EWORKSPACE, "workspace %zu bytes < %zu", ws_bytes, need);
+  }
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  char* base = static_cast<char*>(ws);
+  float* lse_buf = lse != nullptr ? lse : reinterpret_cast<float*>(base);
+  HIP_TRY(zsa::launch_attention(s, dtype, q, k, v, row_stride, n_heads, head_dim, causal, scale,
+                                batch, max_len, T, cu_dev, out, out_stride, lse_buf),
+          "attention");
+  if (scores != nullptr) {
+    float* partials = reinterpret_cast<float*>(base + round256(static_cast<size_t>(n_heads) * T * 4));
+    const int G = zsa::score_groups(dtype, n_heads, head_dim, T);
+    HIP_TRY(zsa::launch_score(s, dtype, q, k, row_stride, lse_buf, n_heads, head_dim, causal, scale,
+                              batch, max_len, T, cu_dev, partials, G),
+            "score");
+    HIP_TRY(zsa::launch_score_finalize(s, partials, G, T, scores), "score finalize");
+  }
+  return ZSA_OK;
+}
+
+size_t zsa_score_workspace_size(int32_t n_heads, int32_t total_rows) {
+  if (n_heads <= 0 || total_rows < 0) return 0;
+  return round256(static_cast<size_t>(n_heads) * total_rows * 4);
+}
+
+int zsa_score_positions(void* stream, int32_t dtype, const void* q, const void* k,
+                        int64_t row_stride, const float* lse, int32_t n_heads, int32_t head_dim,
+                        int32_t causal, float scale, int32_t batch, const int32_t* cu_host,
+                        const int32_t* cu_dev, float* scores, void* ws, size_t ws_bytes) {
+  CHECK(check_dtype(dtype));
+  CHECK(check_head_dim(head_dim));
+  if (n_heads <= 0) return fail(ZSA_EINVAL, "n_heads %d", n_heads);
+  int32_t T, max_len;
+  CHECK(check_seqs(batch, cu_host, cu_dev, &T, &max_len));
+  CHECK(check_ptr16(q, "q"));
+  CHECK(check_ptr16(k, "k"));
+  if (lse == nullptr || scores == nullptr) return fail(ZSA_EINVAL, "lse / scores is NULL");
+  CHECK(check_width(dtype, row_stride, "row_stride"));
+  if (row_stride < static_cast<int64_t>(n_heads) * head_dim)
+    return fail(ZSA_ESHAPE, "row stride shorter than n_heads * head_dim");
+  if (!(scale > 0.f)) return fail(ZSA_EINVAL, "scale must be positive");
+  const size_t need = zsa_score_workspace_size(n_heads, T);
+  if (ws_bytes < need || (need > 0 && ws == nullptr))
+    return fail(ZSA_EWORKSPACE, "workspace %zu bytes < %zu", ws_bytes, need);
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  const int G = zsa::score_groups(dtype, n_heads, head_dim, T);
+  float* partials = static_cast<float*>(ws);
+  HIP_TRY(zsa::launch_score(s, dtype, q, k, row_stride, lse, n_heads, head_dim, causal, scale,
+                            batch, max_len, T, cu_dev, partials, G),
+          "score");
+  HIP_TRY(zsa::launch_score_finalize(s, partials, G, T, scores), "score finalize");
+  return ZSA_OK;
+}
+
+size_t zsa_select_workspace_size(int32_t batch) {
+  return batch < 0 ? 0 : round256(static_cast<size_t>(batch + 1) * 4);
+}
+
+int zsa_select_topk(void* stream, const float* scores, int32_t batch, const int32_t* cu_host,
+                    const int32_t* cu_dev, const int32_t* k_host, int32_t* kept_rows, void* ws,
+                    size_t ws_bytes) {
+  int32_t T, max_len;
+  CHECK(check_seqs(batch, cu_host, cu_dev, &T, &max_len));
+  if (batch > 0 && k_host == nullptr) return fail(ZSA_EINVAL, "k_host is NULL");
+  std::vector<int32_t> cu_out(batch + 1, 0);
+  for (int b = 0; b < batch; ++b) {
+    const int32_t n = cu_host[b + 1] - cu_host[b];
+    if (k_host[b] < 0 || k_host[b] > n)
+      return fail(ZSA_ESHAPE, "k[%d] = %d outside [0, %d]", b, k_host[b], n);
+    cu_out[b + 1] = cu_out[b] + k_host[b];
+  }
+  if (T > 0 && scores == nullptr) return fail(ZSA_EINVAL, "scores is NULL");
+  if (cu_out[batch] > 0 && kept_rows == nullptr) return fail(ZSA_EINVAL, "kept_rows is NULL");
+  const size_t need = zsa_select_workspace_size(batch);
+  if (ws_bytes < need || ws == nullptr) return fail(ZSA_EWORKSPACE, "workspace %zu < %zu", ws_bytes, need);
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  int32_t* cu_out_dev = static_cast<int32_t*>(ws);
+  HIP_TRY(zsa::launch_upload_i32(s, cu_out_dev, cu_out.data(), batch + 1), "upload");
+  HIP_TRY(zsa::launch_select(s, scores, 1, T, batch, max_len, cu_dev, cu_out_dev, kept_rows, nullptr),
+          "select");
+  return ZSA_OK;
+}
+
+int zsa_compact_gather(void* stream, int32_t dtype, const void* hidden, int32_t d,
+                       const int32_t* pos, int32_t t_in, const int32_t* kept_rows, int32_t t_out,
+                       void* hidden_out, int32_t* pos_out) {
+  CHECK(check_dtype(dtype));
+  CHECK(check_width(dtype, d, "d"));
+  if (t_in < 0 || t_out < 0) return fail(ZSA_EINVAL, "negative row count");
+  if ((pos == nullptr) != (pos_out == nullptr)) return fail(ZSA_EINVAL, "pos and pos_out must both be set or both NULL");
+  if (t_out > 0) {
+    CHECK(check_ptr16(hidden, "hidden"));
+    CHECK(check_ptr16(hidden_out, "hidden_out"));
+    if (kept_rows == nullptr) return fail(ZSA_EINVAL, "kept_rows is NULL");
+  }
+  HIP_TRY(zsa::launch_gather(static_cast<hipStream_t>(stream), dtype, d, t_in, kept_rows, t_out,
+                             hidden, hidden_out, nullptr, nullptr, pos, pos_out),
+          "gather");
+  return ZSA_OK;
+}
+
+size_t zsa_layer_workspace_size(const zsa_layer_cfg* cfg, int32_t total_rows, int32_t batch) {
+  if (cfg == nullptr || total_rows < 0 || batch < 0) return 0;
+  Carver cv;
+  layer_layout(cfg, total_rows, cv);
+  return cv.off;
+}
+
+int zsa_layer_forward(void* stream, const zsa_layer_cfg* cfg, const zsa_layer_weights* w,
+                      const void* hidden_in, const int32_t* pos_in, int32_t batch,
+                      const int32_t* cu_host, const int32_t* cu_dev, const double* keep_rate,
+                      void* hidden_out, int32_t* pos_out, int32_t* cu_out_host,
+                      int32_t* cu_out_dev, float* scores_out, int32_t* kept_rows_out, void* ws,
+                      size_t ws_bytes) {
+  CHECK(check_cfg(cfg));
+  CHECK(check_weights(cfg, w));
+  int32_t T, max_len;
+  CHECK(check_seqs(batch, cu_host, cu_dev, &T, &max_len));
+  if (T > 0) {
+    CHECK(check_ptr16(hidden_in, "hidden_in"));
+    CHECK(check_ptr16(hidden_out, "hidden_out"));
+    if (pos_in == nullptr || pos_out == nullptr) return fail(ZSA_EINVAL, "pos_in / pos_out is NULL");
+  }
+  if (cu_out_host == nullptr || cu_out_dev == nullptr) return fail(ZSA_EINVAL, "cu_out is NULL");
+  const bool prune = keep_rate != nullptr;
+  std::vector<int32_t> cu_out(batch + 1, 0);
+  int32_t max_out = 0;
+  for (int b = 0; b < batch; ++b) {
+    const int32_t n = cu_host[b + 1] - cu_host[b];
+    int32_t kb = n;
+    if (prune) {
+      CHECK(check_rate(keep_rate[b]));
+      kb = keep_count_impl(n, keep_rate[b], cfg->tau);
+    }
+    cu_out[b + 1] = cu_out[b] + kb;
+    if (kb > max_out) max_out = kb;
+  }
+  const size_t need = zsa_layer_workspace_size(cfg, T, batch);
+  if (ws_bytes < need || ws == nullptr) return fail(ZSA_EWORKSPACE, "workspace %zu < %zu", ws_bytes, need);
+
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  Carver cv;
+  const LayerBufs wb = carve_layer(layer_layout(cfg, T, cv), ws);
+  HIP_TRY(zsa::launch_upload_i32(s, cu_out_dev, cu_out.data(), batch + 1), "upload");
+  const RowSet in{batch, cu_host, cu_dev, T, max_len};
+  const RowSet out{batch, cu_out.data(), cu_out_dev, cu_out[batch], max_out};
+  if (T > 0) {
+    CHECK(run_layer(s, *cfg, *w, hidden_in, pos_in, in, prune, out, hidden_out, pos_out,
+                    scores_out, kept_rows_out, wb));
+    if (!prune) HIP_TRY(zsa::launch_copy_i32(s, pos_out, pos_in, T), "pos copy");
+  }
+  memcpy(cu_out_host, cu_out.data(), sizeof(int32_t) * (batch + 1));
+  return ZSA_OK;
+}
+
+size_t zsa_stack_workspace_size(const zsa_layer_cfg* cfg, int32_t total_rows, int32_t batch,
+                                int32_t n_prune) {
+  if (cfg == nullptr || total_rows < 0 || batch < 0 || n_prune < 0) return 0;
+  Carver cv;
+  layer_layout(cfg, total_rows, cv);
+  const size_t xb = static_cast<size_t>(total_rows) * cfg->d_model * esize(cfg->dtype);
+  cv.take(xb);
+  cv.take(xb);
+  cv.take(static_cast<size_t>(total_rows) * 4);
+  cv.take(static_cast<size_t>(total_rows) * 4);
+  cv.take(static_cast<size_t>(n_prune) * (batch + 1) * 4);
+  return cv.off;
+}
+
+int zsa_stack_forward(void* stream, const zsa_layer_cfg* cfg, const zsa_layer_weights* w,
+                      int32_t n_layers, const int32_t* prune_after, int32_t n_prune,
+                      const double* keep_rate, const void* hidden_in, const int32_t* pos_in,
+                      int32_t batch, const int32_t* cu_host, const int32_t* cu_dev,
+                      void* hidden_out, int32_t* pos_out, int32_t* cu_out_host,
+                      int32_t* cu_out_dev, int32_t* counts_out_host, float* scores_dbg,
+                      int32_t* pos_dbg, void* ws, size_t ws_bytes) {
+  CHECK(check_cfg(cfg));
+  if (n_layers < 1) return fail(ZSA_EINVAL, "n_layers %d < 1", n_layers);
+  if (w == nullptr) return fail(ZSA_EINVAL, "weights are NULL");
+  for (int l = 0; l < n_layers; ++l) {
+    const int rc = check_weights(cfg, &w[l]);
+    if (rc != ZSA_OK) return fail(rc, "layer %d: %s", l + 1, g_err.c_str());
+  }
+  if (n_prune < 0 || (n_prune > 0 && prune_after == nullptr)) return fail(ZSA_EINVAL, "prune_after");
+  for (int p = 0; p < n_prune; ++p) {
+    if (prune_after[p] < 1 || prune_after[p] > n_layers)
+      return fail(ZSA_EINVAL, "prune_after[%d] = %d outside 1..%d", p, prune_after[p], n_layers);
+    if (p > 0 && prune_after[p] <= prune_after[p - 1])
+      return fail(ZSA_EINVAL, "prune_after must be strictly ascending");
+  }
+  int32_t T0, max_len0;
+  CHECK(check_seqs(batch, cu_host, cu_dev, &T0, &max_len0));
+  if (n_prune > 0 && batch > 0 && keep_rate == nullptr) return fail(ZSA_EINVAL, "keep_rate is NULL");
+  for (int b = 0; n_prune > 0 && b < batch; ++b) CHECK(check_rate(keep_rate[b]));
+  if (T0 > 0) {
+    CHECK(check_ptr16(hidden_in, "hidden_in"));
+    CHECK(check_ptr16(hidden_out, "hidden_out"));
+    if (pos_in == nullptr || pos_out == nullptr) return fail(ZSA_EINVAL, "pos_in / pos_out is NULL");
+  }
+  if (cu_out_host == nullptr || cu_out_dev == nullptr) return fail(ZSA_EINVAL, "cu_out is NULL");
+  const size_t need = zsa_stack_workspace_size(cfg, T0, batch, n_prune);
+  if (ws_bytes < need || ws == nullptr) return fail(ZSA_EWORKSPACE, "workspace %zu < %zu", ws_bytes, need);
+
+  // the whole schedule is known on the host before any launch
+  std::vector<std::vector<int32_t>> cus(n_prune + 1, std::vector<int32_t>(batch + 1, 0));
+  std::vector<int32_t> maxl(n_prune + 1, 0);
+  for (int b = 0; b <= batch; ++b) cus[0][b] = cu_host[b];
+  maxl[0] = max_len0;
+  for (int p = 1; p <= n_prune; ++p) {
+    for (int b = 0; b < batch; ++b) {
+      const int32_t n = cus[p - 1][b + 1] - cus[p - 1][b];
+      const int32_t kb = keep_count_impl(n, keep_rate[b], cfg->tau);
+      cus[p][b + 1] = cus[p][b] + kb;
+      if (kb > maxl[p]) maxl[p] = kb;
+      if (counts_out_host != nullptr) counts_out_host[(p - 1) * batch + b] = kb;
+    }
+  }
+
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  Carver cv;
+  const LayerBufs wb = carve_layer(layer_layout(cfg, T0, cv), ws);
+  char* base = static_cast<char*>(ws);
+  const size_t xb = static_cast<size_t>(T0) * cfg->d_model * esize(cfg->dtype);
+  void* xbuf[2] = {base + cv.take(xb), base + cv.take(xb)};
+  int32_t* posbuf[2] = {reinterpret_cast<int32_t*>(base + cv.take(static_cast<size_t>(T0) * 4)),
+                        reinterpret_cast<int32_t*>(base + cv.take(static_cast<size_t>(T0) * 4))};
+  int32_t* meta = reinterpret_cast<int32_t*>(base + cv.take(static_cast<size_t>(n_prune) * (batch + 1) * 4));
+
+  std::vector<int32_t> flat;
+  for (int p = 1; p <= n_prune; ++p) flat.insert(flat.end(), cus[p].begin(), cus[p].end());
+  if (!flat.empty()) HIP_TRY(zsa::launch_upload_i32(s, meta, flat.data(), static_cast<int>(flat.size())), "upload");
+  HIP_TRY(zsa::launch_upload_i32(s, cu_out_dev, cus[n_prune].data(), batch + 1), "upload");
+
+  const void* cur_x = hidden_in;
+  const int32_t* cur_pos = pos_in;
+  RowSet cur{batch, cus[0].data(), cu_dev, T0, max_len0};
+  int point = 0;
+  size_t score_off = 0, pos_off = 0;
+  for (int l = 1; l <= n_layers && T0 > 0; ++l) {
+    const bool last = l == n_layers;
+    const bool prune = point < n_prune && prune_after[point] == l;
+    void* x_out = last ? hidden_out : xbuf[(l - 1) & 1];
+    if (prune) {
+      const RowSet nxt{batch, cus[point + 1].data(), meta + static_cast<size_t>(point) * (batch + 1),
+                       cus[point + 1][batch], maxl[point + 1]};
+      int32_t* pos_next = last ? pos_out : posbuf[point & 1];
+      float* sdbg = scores_dbg != nullptr ? scores_dbg + score_off : nullptr;
+      CHECK(run_layer(s, *cfg, w[l - 1], cur_x, cur_pos, cur, true, nxt, x_out, pos_next, sdbg,
+                      nullptr, wb));
+      if (pos_dbg != nullptr)
+        HIP_TRY(zsa::launch_copy_i32(s, pos_dbg + pos_off, pos_next, nxt.T), "pos debug copy");
+      score_off += cur.T;
+      pos_off += nxt.T;
+      cur_pos = pos_next;
+      cur = nxt;
+      ++point;
+    } else {
+      CHECK(run_layer(s, *cfg, w[l - 1], cur_x, cur_pos, cur, false, cur, x_out, nullptr, nullptr,
+                      nullptr, wb));
+    }
+    cur_x = x_out;
+  }
+  if (T0 > 0 && cur_pos != pos_out) HIP_TRY(zsa::launch_copy_i32(s, pos_out, cur_pos, cur.T), "pos copy");
+  memcpy(cu_out_host, cus[n_prune].data(), sizeof(int32_t) * (batch + 1));
+  return ZSA_OK;
+}
+
+int zsa_timing_arm(int32_t kclass, int32_t capacity) {
+  if (kclass < 0 || kclass >= zsa::K_NCLASS) return fail(ZSA_EINVAL, "kernel class %d", kclass);
+  if (capacity < 1) return fail(ZSA_EINVAL, "capacity %d", capacity);
+  TimingState& t = g_timing[kclass];
+  while (static_cast<int>(t.start.size()) < capacity) {
+    hipEvent_t a, b;
+    HIP_TRY(hipEventCreate(&a), "event create");
+    HIP_TRY(hipEventCreate(&b), "event create");
+    t.start.push_back(a);
+    t.stop.push_back(b);
+  }
+  t.armed = true;
+  t.used = 0;
+  return ZSA_OK;
+}
+
+int zsa_timing_read(int32_t kclass, int32_t* launches, double* total_ms) {
+  if (kclass < 0 || kclass >= zsa::K_NCLASS) return fail(ZSA_EINVAL, "kernel class %d", kclass);
+  if (launches == nullptr || total_ms == nullptr) return fail(ZSA_EINVAL, "NULL output");
+  TimingState& t = g_timing[kclass];
+  double sum = 0.0;
+  for (int i = 0; i < t.used; ++i) {
+    HIP_TRY(hipEventSynchronize(t.stop[i]), "event sync");
+    float ms = 0.f;
+    HIP_TRY(hipEventElapsedTime(&ms, t.start[i], t.stop[i]), "event time");
+    sum += ms;
+  }
+  *launches = t.used;
+  *total_ms = sum;
+  t.armed = false;
+  t.used = 0;
+  return ZSA_OK;
+}
+
+}  // extern "C"

@@ -1,0 +1,149 @@
+// Internal declarations shared by the HIP kernels and the C-ABI layer.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <hip/hip_ext.h>
+#include <stddef.h>
+#include <stdint.h>
+
+#include <utility>
+
+namespace zsa {
+
+typedef uint16_t bf16_t;
+
+// ---------------------------------------------------------------------------
+// storage conversions (fp32 compute, f32 or bf16 storage)
+// ---------------------------------------------------------------------------
+__device__ __forceinline__ float to_f32(float x) { return x; }
+__device__ __forceinline__ float to_f32(bf16_t h) {
+  return __uint_as_float(static_cast<uint32_t>(h) << 16);
+}
+
+// fp32 -> bf16, round to nearest even; NaN stays a (quiet) NaN
+__device__ __forceinline__ bf16_t f32_to_bf16(float f) {
+  uint32_t u = __float_as_uint(f);
+  if ((u & 0x7fffffffu) > 0x7f800000u) return static_cast<bf16_t>((u >> 16) | 0x0040u);
+  u += 0x7fffu + ((u >> 16) & 1u);
+  return static_cast<bf16_t>(u >> 16);
+}
+
+template <typename T>
+__device__ __forceinline__ T from_f32(float x);
+template <>
+__device__ __forceinline__ float from_f32<float>(float x) { return x; }
+template <>
+__device__ __forceinline__ bf16_t from_f32<bf16_t>(float x) { return f32_to_bf16(x); }
+
+// 16-byte vector of storage elements
+template <typename T>
+struct Vec16 {
+  static constexpr int N = 16 / sizeof(T);
+};
+
+__device__ __forceinline__ void unpack16(const uint4& v, float* out, float) {
+  out[0] = __uint_as_float(v.x); out[1] = __uint_as_float(v.y);
+  out[2] = __uint_as_float(v.z); out[3] = __uint_as_float(v.w);
+}
+__device__ __forceinline__ void unpack16(const uint4& v, float* out, bf16_t) {
+  const uint32_t w[4] = {v.x, v.y, v.z, v.w};
+#pragma unroll
+  for (int i = 0; i < 4; ++i) {
+    out[2 * i] = __uint_as_float(w[i] << 16);
+    out[2 * i + 1] = __uint_as_float(w[i] & 0xffff0000u);
+  }
+}
+__device__ __forceinline__ uint4 pack16(const float* in, float) {
+  return make_uint4(__float_as_uint(in[0]), __float_as_uint(in[1]), __float_as_uint(in[2]),
+                    __float_as_uint(in[3]));
+}
+__device__ __forceinline__ uint4 pack16(const float* in, bf16_t) {
+  uint32_t w[4];
+#pragma unroll
+  for (int i = 0; i < 4; ++i)
+    w[i] = static_cast<uint32_t>(f32_to_bf16(in[2 * i])) |
+           (static_cast<uint32_t>(f32_to_bf16(in[2 * i + 1])) << 16);
+  return make_uint4(w[0], w[1], w[2], w[3]);
+}
+
+// ---------------------------------------------------------------------------
+// launch helper with the optional per-class timing hook
+// ---------------------------------------------------------------------------
+enum KClass { K_GEMM = 0, K_ATTENTION = 1, K_SCORE = 2, K_SELECT = 3, K_GATHER = 4,
+              K_NORM = 5, K_MISC = 6, K_NCLASS = 7 };
+
+// returns true and a (start, stop) pair if the next launch of this class is timed
+bool timing_take(int kclass, hipEvent_t* start, hipEvent_t* stop);
+
+template <typename... KArgs, typename... Args>
+inline hipError_t launch(int kclass, void (*kernel)(KArgs...), dim3 grid, dim3 block,
+                         size_t shmem, hipStream_t stream, Args... args) {
+  hipEvent_t e0 = nullptr, e1 = nullptr;
+  if (timing_take(kclass, &e0, &e1)) {
+    hipExtLaunchKernelGGL(kernel, grid, block, static_cast<uint32_t>(shmem), stream, e0, e1, 0,
+                          static_cast<KArgs>(args)...);
+  } else {
+    hipLaunchKernelGGL(kernel, grid, block, static_cast<uint32_t>(shmem), stream,
+                       static_cast<KArgs>(args)...);
+  }
+  return hipGetLastError();
+}
+
+// ---------------------------------------------------------------------------
+// GEMM epilogue parameters (shared by the MFMA and the vector-ALU GEMMs)
+// ---------------------------------------------------------------------------
+enum Epi { EPI_NONE = 0, EPI_GELU = 1, EPI_SWIGLU = 2, EPI_RESIDUAL = 3, EPI_ROPE = 4 };
+
+constexpr int kMaxHalfHead = 64;  // head_dim <= 128 for the rotary epilogue
+
+struct EpiParams {
+  int epi;
+  const void* bias;      // [N] or null
+  const void* residual;  // [M, ldy] or null
+  void* y;               // output
+  int ldy;               // output row stride (elements)
+  const int32_t* pos;    // [M] rotary positions
+  int head_dim;
+  int rope_cols;
+  double inv_freq[kMaxHalfHead];  // theta^(-2i/hd), computed on the host in double
+};
+
+// ---------------------------------------------------------------------------
+// kernel launchers (one translation unit each)
+// ---------------------------------------------------------------------------
+hipError_t launch_norm(hipStream_t s, int dtype, int kind, const void* x, const void* g,
+                       const void* b, int rows, int d, float eps, void* y);
+
+// y = epi(x[a_rows] W^T + bias); x [*, K] (row-gathered through a_rows if non-null)
+hipError_t launch_gemm(hipStream_t s, int dtype, const void* x, int M, int K, const void* w,
+                       int N, const EpiParams& ep);
+
+hipError_t launch_attention(hipStream_t s, int dtype, const void* q, const void* k,
+                            const void* v, int64_t row_stride, int H, int hd, int causal,
+                            float scale, int B, int max_len, int T, const int32_t* cu_dev,
+                            void* out, int64_t out_stride, float* lse);
+
+// writes G partial score vectors [G][T] (G = head groups); returns G via *groups
+hipError_t launch_score(hipStream_t s, int dtype, const void* q, const void* k,
+                        int64_t row_stride, const float* lse, int H, int hd, int causal,
+                        float scale, int B, int max_len, int T, const int32_t* cu_dev,
+                        float* partials, int groups);
+int score_groups(int dtype, int H, int hd, int T);
+
+hipError_t launch_score_finalize(hipStream_t s, const float* partials, int groups, int T,
+                                 float* scores);
+
+// per-sequence top-k over sum_g partials[g*T + row]; cu_out gives output offsets
+hipError_t launch_select(hipStream_t s, const float* partials, int groups, int T, int B,
+                         int max_len, const int32_t* cu_in_dev, const int32_t* cu_out_dev,
+                         int32_t* kept_rows, float* scores_out);
+
+// row gather of up to two [*, d] arrays plus pos
+hipError_t launch_gather(hipStream_t s, int dtype, int d, int t_in, const int32_t* kept,
+                         int t_out, const void* src0, void* dst0, const void* src1, void* dst1,
+                         const int32_t* pos, int32_t* pos_out);
+
+hipError_t launch_upload_i32(hipStream_t s, int32_t* dst, const int32_t* host_vals, int n);
+hipError_t launch_copy_i32(hipStream_t s, int32_t* dst, const int32_t* src, int n);
+
+}  // namespace zsa

@@ -1,0 +1,134 @@
+"""The C-ABI library on the CPU: it loads, exports every symbol the header
+declares, its host-only Eq. 2 schedule agrees with the oracle's, and its
+argument validation rejects bad calls before touching the GPU."""
+import ctypes
+import os
+import re
+
+import numpy as np
+import pytest
+
+from oracle import zsa_oracle as O
+from paper_2509_01190_amd import zsa
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "zsa.h")
+
+
+def _declared():
+    text = open(HEADER).read()
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    return sorted(set(re.findall(r"\b(zsa_[a-z_0-9]+)\s*\(", text)))
+
+
+def test_library_exports_every_declared_symbol():
+    lib = zsa.lib()
+    names = _declared()
+    assert len(names) >= 15
+    for n in names:
+        assert hasattr(lib, n), n
+    assert set(names) == set(zsa.EXPORTED)
+
+
+def test_version_and_error_text():
+    assert "gfx950" in zsa.version()
+    with pytest.raises(zsa.ZsaError) as e:
+        zsa.keep_count(10, 1.5, 5)
+    assert e.value.code == zsa.EINVAL
+    assert "keep rate" in zsa.lib().zsa_last_error().decode()
+
+
+def test_keep_count_matches_oracle():
+    rng = np.random.default_rng(0)
+    rates = list(np.linspace(0, 1, 201)) + list(rng.uniform(0, 1, 300)) + \
+        [0.57, 0.29, 0.09, 0.7, 0.3, 0.1, 0.99, 0.98, 0.97, 0.96]
+    for n in [0, 1, 3, 5, 7, 40, 64, 100, 128, 512, 2048, 4096, 9999]:
+        for a in rates:
+            for tau in (1, 5):
+                assert zsa.keep_count(n, float(a), tau) == O.keep_count(n, float(a), tau), (n, a, tau)
+
+
+def test_keep_schedule_matches_oracle():
+    rng = np.random.default_rng(1)
+    lens = rng.integers(0, 5000, 64)
+    rates = rng.uniform(0.0, 1.0, 64)
+    got = zsa.keep_schedule(lens, rates, 5, 4)
+    ref = O.keep_schedule(list(lens), list(rates), 5, 4)
+    assert np.array_equal(got, np.array(ref))
+
+
+@pytest.mark.parametrize("bad", [float("nan"), -1e-12, 1.0000001, float("inf")])
+def test_keep_schedule_rejects_bad_rates(bad):
+    with pytest.raises(zsa.ZsaError) as e:
+        zsa.keep_schedule([10, 10], [0.5, bad], 5, 1)
+    assert e.value.code == zsa.EINVAL
+
+
+def test_validation_happens_before_any_launch():
+    lib = zsa.lib()
+    # unknown dtype
+    assert lib.zsa_norm(None, 7, 0, None, None, None, 4, 64, 1e-5, None) == zsa.EINVAL
+    # misaligned pointer
+    assert lib.zsa_norm(None, zsa.F32, 0, ctypes.c_void_p(0x1004), ctypes.c_void_p(0x2000), None, 4,
+                        64, 1e-5, ctypes.c_void_p(0x3000)) == zsa.EALIGN
+    # row length not a multiple of 16 bytes
+    assert lib.zsa_norm(None, zsa.BF16, 0, ctypes.c_void_p(0x1000), ctypes.c_void_p(0x2000), None,
+                        4, 12, 1e-5, ctypes.c_void_p(0x3000)) == zsa.EALIGN
+    # unsupported head_dim
+    cu = np.array([0, 8], dtype=np.int32)
+    rc = lib.zsa_attention_with_scores(None, zsa.BF16, ctypes.c_void_p(0x1000),
+                                       ctypes.c_void_p(0x1000), ctypes.c_void_p(0x1000), 96, 2, 48,
+                                       0, 0.1, 1, cu.ctypes.data_as(zsa._pi32),
+                                       ctypes.c_void_p(0x4000), ctypes.c_void_p(0x5000), 96, None,
+                                       None, None, 0)
+    assert rc == zsa.EUNSUPPORTED
+    # cu not monotone
+    cu = np.array([0, 8, 4], dtype=np.int32)
+    rc = lib.zsa_select_topk(None, ctypes.c_void_p(0x1000), 2, cu.ctypes.data_as(zsa._pi32),
+                             ctypes.c_void_p(0x2000), cu.ctypes.data_as(zsa._pi32),
+                             ctypes.c_void_p(0x3000), ctypes.c_void_p(0x4000), 1024)
+    assert rc == zsa.ESHAPE
+    # k > n
+    cu = np.array([0, 8], dtype=np.int32)
+    k = np.array([9], dtype=np.int32)
+    rc = lib.zsa_select_topk(None, ctypes.c_void_p(0x1000), 1, cu.ctypes.data_as(zsa._pi32),
+                             ctypes.c_void_p(0x2000), k.ctypes.data_as(zsa._pi32),
+                             ctypes.c_void_p(0x3000), ctypes.c_void_p(0x4000), 1024)
+    assert rc == zsa.ESHAPE
+    # workspace too small
+    k = np.array([4], dtype=np.int32)
+    rc = lib.zsa_select_topk(None, ctypes.c_void_p(0x1000), 1, cu.ctypes.data_as(zsa._pi32),
+                             ctypes.c_void_p(0x2000), k.ctypes.data_as(zsa._pi32),
+                             ctypes.c_void_p(0x3000), ctypes.c_void_p(0x4000), 4)
+    assert rc == zsa.EWORKSPACE
+
+
+def test_layer_config_validation():
+    lib = zsa.lib()
+    cfg = zsa.make_cfg(zsa.ENCODER, 768, 12, 3072, False, zsa.BF16)
+    cfg.tau = 0
+    cu = np.array([0, 16], dtype=np.int32)
+    w = zsa.LayerWeights(*([0x1000] * 12))
+    rc = lib.zsa_layer_forward(None, ctypes.byref(cfg), ctypes.byref(w), ctypes.c_void_p(0x1000),
+                               ctypes.c_void_p(0x2000), 1, cu.ctypes.data_as(zsa._pi32),
+                               ctypes.c_void_p(0x3000), None, ctypes.c_void_p(0x4000),
+                               ctypes.c_void_p(0x5000), cu.ctypes.data_as(zsa._pi32),
+                               ctypes.c_void_p(0x6000), None, None, ctypes.c_void_p(0x7000), 1)
+    assert rc == zsa.EINVAL
+    cfg = zsa.make_cfg(zsa.ENCODER, 768, 10, 3072, False, zsa.BF16)   # 768 / 10 is not integral
+    assert lib.zsa_layer_workspace_size(ctypes.byref(cfg), 16, 1) > 0
+    rc = lib.zsa_layer_forward(None, ctypes.byref(cfg), ctypes.byref(w), ctypes.c_void_p(0x1000),
+                               ctypes.c_void_p(0x2000), 1, cu.ctypes.data_as(zsa._pi32),
+                               ctypes.c_void_p(0x3000), None, ctypes.c_void_p(0x4000),
+                               ctypes.c_void_p(0x5000), cu.ctypes.data_as(zsa._pi32),
+                               ctypes.c_void_p(0x6000), None, None, ctypes.c_void_p(0x7000), 1)
+    assert rc == zsa.ESHAPE
+
+
+def test_workspace_sizes_grow_with_rows():
+    cfg = zsa.make_cfg(zsa.DECODER, 4096, 32, 11008, True, zsa.BF16)
+    lib = zsa.lib()
+    a = lib.zsa_stack_workspace_size(ctypes.byref(cfg), 1024, 4, 1)
+    b = lib.zsa_stack_workspace_size(ctypes.byref(cfg), 16384, 4, 1)
+    assert 0 < a < b
+    assert b < 4 << 30   # a 7B-shaped 16k-row slice needs well under 4 GiB of scratch

@@ -1,0 +1,226 @@
+"""Kernel-level parity of the HIP path against the CPU oracle, through the
+C-ABI (select, gather, norms, projections with every epilogue, attention,
+contribution scores)."""
+import math
+
+import numpy as np
+import pytest
+import torch
+
+from oracle import zsa_oracle as O
+from paper_2509_01190_amd import workloads as W
+from paper_2509_01190_amd import zsa
+from tests.helpers import assert_close, dev, f64, to_dev
+
+pytestmark = pytest.mark.gpu
+
+
+# ------------------------------------------------------------------ top-k
+@pytest.mark.parametrize("case", ["ragged_ties", "long_rows", "edges"])
+def test_select_topk_bit_exact(case):
+    if case == "ragged_ties":
+        lens = W.lengths(W.PRESETS["ragged"], 0)
+    elif case == "long_rows":
+        lens = [20000, 16384, 16385, 3, 4097]
+    else:
+        lens = [0, 1, 5, 6, 64, 1000, 2]
+    g = np.random.default_rng(3)
+    scores = W.injected_scores(lens, seed=1)
+    ks = []
+    for b, n in enumerate(lens):
+        if b % 5 == 3:
+            ks.append(0)
+        elif b % 5 == 4:
+            ks.append(n)
+        else:
+            ks.append(O.keep_count(n, float(g.uniform(0.0, 1.0)), 5))
+    seqs = zsa.Seqs(lens, dev())
+    kept = zsa.select_topk(torch.from_numpy(scores).to(dev()), seqs, ks)
+    torch.cuda.synchronize()
+    got = kept.cpu().numpy()
+    ref = []
+    for b, n in enumerate(lens):
+        lo = int(seqs.host[b])
+        ref.append(O.select_topk(scores[lo:lo + n].astype(np.float64), ks[b]) + lo)
+    ref = np.concatenate(ref) if ref else np.zeros(0)
+    assert np.array_equal(got, ref)
+
+
+def test_select_topk_deterministic():
+    lens = [4096, 777, 3000]
+    scores = np.random.default_rng(4).standard_normal(sum(lens)).astype(np.float32)
+    seqs = zsa.Seqs(lens, dev())
+    s = torch.from_numpy(scores).to(dev())
+    a = zsa.select_topk(s, seqs, [100, 300, 2999]).cpu()
+    b = zsa.select_topk(s, seqs, [100, 300, 2999]).cpu()
+    assert torch.equal(a, b)
+
+
+# ------------------------------------------------------------------ gather
+@pytest.mark.parametrize("dtype,d", [("bf16", 768), ("bf16", 4096), ("f32", 128)])
+def test_compact_gather_bit_exact(dtype, d):
+    g = np.random.default_rng(5)
+    t_in = 1000
+    x = g.standard_normal((t_in, d)).astype(np.float32)
+    pos = g.integers(0, 5000, t_in).astype(np.int32)
+    kept = np.sort(g.choice(t_in, 333, replace=False)).astype(np.int32)
+    kept = np.concatenate([kept, np.array([-1, t_in], dtype=np.int32)])   # out-of-range rows
+    xd = to_dev(x, dtype)
+    out, pos_out = zsa.compact_gather(xd, torch.from_numpy(pos).to(dev()),
+                                      torch.from_numpy(kept).to(dev()))
+    torch.cuda.synchronize()
+    ref = xd.cpu()
+    assert torch.equal(out[:333].cpu(), ref[kept[:333]])
+    assert torch.equal(out[333:].cpu(), torch.zeros_like(out[333:].cpu()))
+    assert np.array_equal(pos_out.cpu().numpy(), np.concatenate([pos[kept[:333]], [-1, -1]]))
+
+
+# ------------------------------------------------------------------ norms
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
+@pytest.mark.parametrize("kind", [zsa.NORM_LAYER, zsa.NORM_RMS])
+@pytest.mark.parametrize("d", [128, 768, 4096])
+def test_norm(dtype, kind, d):
+    g = np.random.default_rng(6)
+    rows = 37
+    x = (g.standard_normal((rows, d)) * 2 + 0.5).astype(np.float32)
+    w = (1 + 0.1 * g.standard_normal(d)).astype(np.float32)
+    b = (0.1 * g.standard_normal(d)).astype(np.float32)
+    xd, wd, bd = to_dev(x, dtype), to_dev(w, dtype), to_dev(b, dtype)
+    y = zsa.norm(xd, wd, bd, kind, 1e-5)
+    torch.cuda.synchronize()
+    x64, w64, b64 = f64(xd), f64(wd), f64(bd)
+    ref = O.layer_norm(x64, w64, b64, 1e-5) if kind == zsa.NORM_LAYER else O.rms_norm(x64, w64, 1e-5)
+    assert_close(f64(y), ref, 1e-2 if dtype == "bf16" else 1e-5, f"norm {kind}")
+
+
+# ------------------------------------------------------------------ projections
+EPIS = [zsa.EPI_NONE, zsa.EPI_GELU, zsa.EPI_SWIGLU, zsa.EPI_RESIDUAL, zsa.EPI_ROPE]
+
+
+@pytest.mark.parametrize("dtype,k", [("bf16", 256), ("bf16", 136), ("f32", 200)])
+@pytest.mark.parametrize("epi", EPIS)
+def test_linear_epilogues(dtype, k, epi):
+    g = np.random.default_rng(7 + epi)
+    m, n, hd = 300, 384, 64
+    x = g.standard_normal((m, k)).astype(np.float32)
+    w = (g.standard_normal((n, k)) / math.sqrt(k)).astype(np.float32)
+    bias = (0.1 * g.standard_normal(n)).astype(np.float32)
+    xd, wd, bd = to_dev(x, dtype), to_dev(w, dtype), to_dev(bias, dtype)
+    res = to_dev(g.standard_normal((m, n)).astype(np.float32), dtype) if epi == zsa.EPI_RESIDUAL else None
+    pos = g.integers(0, 4096, m).astype(np.int32)
+    posd = torch.from_numpy(pos).to(dev())
+    rope_cols = 256
+    y = zsa.linear(xd, wd, bd, epi, residual=res, pos=posd if epi == zsa.EPI_ROPE else None,
+                   head_dim=hd, rope_cols=rope_cols, rope_theta=10000.0)
+    torch.cuda.synchronize()
+    z = f64(xd) @ f64(wd).T + f64(bd)
+    if epi == zsa.EPI_NONE:
+        ref = z
+    elif epi == zsa.EPI_GELU:
+        ref = O.gelu(z)
+    elif epi == zsa.EPI_SWIGLU:
+        ref = O.silu(z[:, 0::2]) * z[:, 1::2]
+    elif epi == zsa.EPI_RESIDUAL:
+        ref = f64(res) + z
+    else:
+        ref = z.copy()
+        ref[:, :rope_cols] = O.rope(z[:, :rope_cols], pos.astype(np.int64), rope_cols // hd, 1e4)
+    assert_close(f64(y), ref, 1e-2 if dtype == "bf16" else 2e-5, f"epilogue {epi}")
+
+
+def test_linear_in_place_residual():
+    g = np.random.default_rng(8)
+    m, k, n = 129, 128, 256
+    xd = to_dev(g.standard_normal((m, k)).astype(np.float32), "bf16")
+    wd = to_dev((g.standard_normal((n, k)) / 11).astype(np.float32), "bf16")
+    yd = to_dev(g.standard_normal((m, n)).astype(np.float32), "bf16")
+    ref = f64(yd) + f64(xd) @ f64(wd).T
+    zsa.linear(xd, wd, None, zsa.EPI_RESIDUAL, residual=yd, out=yd)
+    torch.cuda.synchronize()
+    assert_close(f64(yd), ref, 1e-2, "in-place residual")
+
+
+# ------------------------------------------------------------------ attention + scores
+def _qkv(lens, H, hd, dtype, seed, sharp=1.5):
+    g = np.random.default_rng(seed)
+    T = sum(lens)
+    d = H * hd
+    qkv = g.standard_normal((T, 3 * d)).astype(np.float32)
+    qkv[:, :d] *= sharp
+    t = to_dev(qkv, dtype)
+    return t, t[:, :d], t[:, d:2 * d], t[:, 2 * d:]
+
+
+ATT_CASES = [("bf16", 64), ("bf16", 128), ("f32", 32), ("f32", 64), ("bf16", 32)]
+
+
+@pytest.mark.parametrize("dtype,hd", ATT_CASES)
+@pytest.mark.parametrize("causal", [False, True])
+def test_attention_with_scores(dtype, hd, causal):
+    lens = [1, 17, 130, 300, 64]
+    H = 4
+    qkv, q, k, v = _qkv(lens, H, hd, dtype, seed=hd + causal)
+    seqs = zsa.Seqs(lens, dev())
+    out, lse, scores = zsa.attention_with_scores(q, k, v, H, seqs, causal)
+    torch.cuda.synchronize()
+    q64, k64, v64 = f64(q), f64(k), f64(v)
+    o_ref, lse_ref, s_ref = [], [], []
+    for b, n in enumerate(lens):
+        lo = int(seqs.host[b])
+        o, l, s = O.attention(q64[lo:lo + n], k64[lo:lo + n], v64[lo:lo + n], np.arange(n), H,
+                              causal)
+        o_ref.append(o)
+        lse_ref.append(l)
+        s_ref.append(s)
+    o_ref = np.concatenate(o_ref)
+    lse_ref = np.concatenate(lse_ref, axis=1)
+    s_ref = np.concatenate(s_ref)
+    assert_close(f64(out), o_ref, 1e-2 if dtype == "bf16" else 1e-5, "attention output")
+    assert np.max(np.abs(lse.cpu().numpy() - lse_ref)) <= 2e-5 * max(1.0, np.abs(lse_ref).max())
+    assert np.max(np.abs(scores.cpu().numpy() - s_ref) / s_ref) <= 1e-4
+    assert abs(scores.cpu().double().sum() - H * sum(lens)) <= 1e-4 * H * sum(lens)
+
+
+@pytest.mark.parametrize("dtype,hd", [("bf16", 64), ("bf16", 128), ("f32", 32)])
+@pytest.mark.parametrize("causal", [False, True])
+def test_score_positions_from_oracle_lse(dtype, hd, causal):
+    lens = [300, 9, 64, 129]
+    H = 3
+    qkv, q, k, v = _qkv(lens, H, hd, dtype, seed=11 + hd, sharp=2.0)
+    seqs = zsa.Seqs(lens, dev())
+    q64, k64, v64 = f64(q), f64(k), f64(v)
+    lse_ref, s_ref = [], []
+    for b, n in enumerate(lens):
+        lo = int(seqs.host[b])
+        _, l, s = O.attention(q64[lo:lo + n], k64[lo:lo + n], v64[lo:lo + n], np.arange(n), H, causal)
+        lse_ref.append(l)
+        s_ref.append(s)
+    lse_ref = np.concatenate(lse_ref, axis=1)
+    s_ref = np.concatenate(s_ref)
+    lse_d = torch.from_numpy(lse_ref.astype(np.float32)).to(dev())
+    s = zsa.score_positions(q, k, lse_d, H, seqs, causal)
+    torch.cuda.synchronize()
+    assert np.max(np.abs(s.cpu().numpy() - s_ref) / s_ref) <= 1e-4
+    s2 = zsa.score_positions(q, k, lse_d, H, seqs, causal)
+    assert torch.equal(s, s2)   # fixed reduction order: bitwise reproducible
+
+
+def test_uniform_attention_scores_closed_form():
+    # all-zero queries: every row spreads its mass uniformly over the rows it sees
+    lens = [50, 7, 200]
+    H, hd = 4, 64
+    qkv, q, k, v = _qkv(lens, H, hd, "bf16", seed=2)
+    q.zero_()
+    seqs = zsa.Seqs(lens, dev())
+    for causal in (False, True):
+        _, _, s = zsa.attention_with_scores(q, k, v, H, seqs, causal)
+        torch.cuda.synchronize()
+        s = s.cpu().double().numpy()
+        for b, n in enumerate(lens):
+            lo = int(seqs.host[b])
+            if causal:
+                harm = np.concatenate([[0.0], np.cumsum(1.0 / np.arange(1, n + 1))])
+                expect = H * (harm[n] - harm[np.arange(n)])
+            else:
+                expect = np.full(n, float(H))
+            assert np.allclose(s[lo:lo + n], expect, rtol=1e-5)

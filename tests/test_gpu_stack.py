@@ -1,0 +1,164 @@
+"""The whole pruned stack through zsa_stack_forward against the oracle:
+the small fp32 encoder exactly (kept positions identical), small bf16
+encoder/decoder stacks under the margin protocol, determinism and the
+keep_rate = 1 identity."""
+import numpy as np
+import pytest
+import torch
+
+from oracle import zsa_oracle as O
+from paper_2509_01190_amd import workloads as W
+from paper_2509_01190_amd import zsa
+from tests.helpers import (assert_close, assert_rel_l2, check_kept_sets, dev, dev_weights, f64,
+                           modes, to_dev, weights_f64)
+
+pytestmark = pytest.mark.gpu
+
+
+def build(p, seed, lens=None, norm_jitter=True, sharp=1.0):
+    lens = W.lengths(p, seed) if lens is None else lens
+    ws = W.stack_weights(p, seed, norm_jitter=norm_jitter)
+    for w in ws:
+        w["w_qkv"] = (w["w_qkv"] * np.float32(sharp)).astype(np.float32)
+    dws = [dev_weights(w, p.dtype) for w in ws]
+    cfg = zsa.make_cfg(p.kind, p.d_model, p.n_heads, p.d_ff, p.causal,
+                       zsa.BF16 if p.dtype == "bf16" else zsa.F32, p.tau, p.norm_eps, p.rope_theta)
+    stack = zsa.Stack(cfg, dws)
+    x = W.hidden(p, seed, lens)
+    xd = to_dev(x, p.dtype)
+    posd = torch.from_numpy(W.positions(lens)).to(dev())
+    ocfg = O.LayerCfg(p.kind, p.d_model, p.n_heads, p.d_ff, p.causal, p.norm_eps, p.rope_theta,
+                      p.tau)
+    return lens, stack, xd, posd, dws, ocfg
+
+
+def compare_stack(p, lens, stack, xd, posd, dws, ocfg, rates, seqs_check=None, tol=None,
+                  eps=None):
+    """Run the stack on the GPU (with debug outputs) and check it against the
+    oracle, sequence by sequence (sequences are independent), continuing the
+    oracle on the GPU's kept sets. Returns the number of kept-set swaps."""
+    seqs = zsa.Seqs(lens, dev())
+    out = stack.forward(xd, posd, seqs, p.prune_after, rates, debug=True)
+    torch.cuda.synchronize()
+    bf16 = p.dtype == "bf16"
+    tol = tol if tol is not None else (2e-2 if bf16 else 1e-4)
+    eps = eps if eps is not None else (5e-3 if bf16 else 1e-5)
+    rows_in = out["rows_in"]
+    n_pts = len(p.prune_after)
+    # split the debug outputs per pruning point
+    s_dbg = out["scores_dbg"].cpu().numpy()
+    pos_dbg = out["pos_dbg"].cpu().numpy()
+    cus = [seqs.host.astype(np.int64)]
+    for pt in range(n_pts):
+        c = np.zeros(len(lens) + 1, dtype=np.int64)
+        c[1:] = np.cumsum(out["counts"][pt])
+        cus.append(c)
+    s_off = np.concatenate([[0], np.cumsum(rows_in[:n_pts])])
+    p_off = np.concatenate([[0], np.cumsum(rows_in[1:n_pts + 1])])
+    assert np.array_equal(out["cu_host"], cus[-1])
+    sched = O.keep_schedule(lens, list(rates), p.tau, n_pts)
+    assert np.array_equal(out["counts"], np.array(sched).reshape(n_pts, len(lens)))
+    x_all = f64(xd)
+    ws64 = [weights_f64(w) for w in dws]
+    x_fin = f64(out["x"][: out["t_final"]])
+    pos_fin = out["pos"][: out["t_final"]].cpu().numpy()
+    swaps = 0
+    check = range(len(lens)) if seqs_check is None else seqs_check
+    for b in check:
+        n = lens[b]
+        lo = int(seqs.host[b])
+        xb = x_all[lo:lo + n]
+        posb = np.arange(n)
+        override = {}
+        for pt, layer in enumerate(p.prune_after):
+            # GPU kept original positions -> local indices among the rows entering this point
+            prev_pos = posb if pt == 0 else pos_dbg[p_off[pt - 1] + cus[pt][b]:p_off[pt - 1] + cus[pt][b + 1]]
+            kept_pos = pos_dbg[p_off[pt] + cus[pt + 1][b]:p_off[pt] + cus[pt + 1][b + 1]]
+            override[layer] = [np.searchsorted(prev_pos, kept_pos)]
+        # oracle continuing on the GPU's kept sets: exact (hidden-state L2) and
+        # rounding at the GPU's storage points (scores, kept sets, elementwise)
+        m_l2, m_el = modes(p.dtype)
+        ref = O.stack_forward(xb, posb, [0, n], ws64, ocfg, p.prune_after, [rates[b]],
+                              mode=m_l2, kept_override=override)
+        ref_e = ref if m_el == m_l2 else O.stack_forward(
+            xb, posb, [0, n], ws64, ocfg, p.prune_after, [rates[b]], mode=m_el,
+            kept_override=override)
+        for pt, layer in enumerate(p.prune_after):
+            s_gpu = s_dbg[s_off[pt] + cus[pt][b]:s_off[pt] + cus[pt][b + 1]]
+            s_ref = ref_e["points"][pt]["scores"]
+            k = ref["points"][pt]["k"][0]
+            kg = override[layer][0]
+            # the oracle's own choice given identical inputs to this point
+            kr = O.select_topk(s_ref, k)
+            swaps += check_kept_sets(s_gpu, s_ref, k, kg, kr, eps, f"seq {b} point {pt}")
+        fo, fe = out["cu_host"][b], out["cu_host"][b + 1]
+        assert np.array_equal(pos_fin[fo:fe], ref["pos"])
+        assert_rel_l2(x_fin[fo:fe], ref["x"], tol, f"seq {b} final rows")
+        assert_close(x_fin[fo:fe], ref_e["x"], tol, f"seq {b} final rows")
+    return swaps
+
+
+def test_tiny_encoder_exact():
+    p = W.PRESETS["tiny"]
+    lens, stack, xd, posd, dws, ocfg = build(p, 0)
+    rates = W.keep_rates(p, 0, 0.5)
+    assert compare_stack(p, lens, stack, xd, posd, dws, ocfg, rates) == 0
+
+
+@pytest.mark.parametrize("kind", [W.ENCODER, W.DECODER])
+def test_small_bf16_stack(kind):
+    causal = kind == W.DECODER
+    p = W.shrink(W.PRESETS["bert"], kind=kind, causal=causal, n_layers=4, d_model=256, n_heads=4,
+                 d_ff=512, batch=5, prune_after=(1, 3))
+    lens = [300, 64, 129, 17, 512]
+    lens, stack, xd, posd, dws, ocfg = build(p, 1, lens, sharp=3.0)
+    rates = [0.5, 0.7, 0.3, 0.9, 0.1]
+    compare_stack(p, lens, stack, xd, posd, dws, ocfg, rates)
+
+
+def test_stack_deterministic_and_keep_one():
+    p = W.shrink(W.PRESETS["dec1b"], n_layers=3, d_model=256, n_heads=4, d_ff=256, batch=3,
+                 prune_after=(1, 2))
+    lens = [200, 33, 450]
+    lens, stack, xd, posd, dws, ocfg = build(p, 2, lens, sharp=8.0)
+    seqs = zsa.Seqs(lens, dev())
+    a = stack.forward(xd, posd, seqs, p.prune_after, [0.4, 0.6, 0.25], debug=True)
+    a_x = a["x"].clone()
+    a_s = a["scores_dbg"].clone()
+    b = stack.forward(xd, posd, seqs, p.prune_after, [0.4, 0.6, 0.25], debug=True)
+    torch.cuda.synchronize()
+    assert torch.equal(a_x, b["x"])
+    assert torch.equal(a_s, b["scores_dbg"])
+    one = stack.forward(xd, posd, seqs, p.prune_after, [1.0] * 3)
+    none = stack.forward(xd, posd, seqs, (), [1.0] * 3)
+    torch.cuda.synchronize()
+    assert torch.equal(one["x"][: one["t_final"]], none["x"][: none["t_final"]])
+    assert torch.equal(one["pos"][: one["t_final"]], none["pos"][: none["t_final"]])
+
+
+def test_graph_replay_matches_eager():
+    p = W.shrink(W.PRESETS["bert"], n_layers=3, d_model=256, n_heads=4, d_ff=512, batch=4,
+                 prune_after=(1, 2))
+    lens = [128, 300, 77, 512]
+    lens, stack, xd, posd, dws, ocfg = build(p, 3, lens, sharp=8.0)
+    seqs = zsa.Seqs(lens, dev())
+    rates = [0.5, 0.3, 0.8, 0.6]
+    eager = stack.forward(xd, posd, seqs, p.prune_after, rates)
+    ref_x = eager["x"].clone()
+    ref_pos = eager["pos"].clone()
+    out = stack.forward(xd, posd, seqs, p.prune_after, rates)
+    torch.cuda.synchronize()
+    g = torch.cuda.CUDAGraph()
+    s = torch.cuda.Stream()
+    s.wait_stream(torch.cuda.current_stream())
+    with torch.cuda.stream(s):
+        with torch.cuda.graph(g, stream=s):
+            stack.forward(xd, posd, seqs, p.prune_after, rates, out=out)
+    torch.cuda.current_stream().wait_stream(s)
+    for i in range(3):
+        out["x"].zero_()
+        torch.cuda.synchronize()
+        g.replay()
+        torch.cuda.synchronize()
+        assert torch.equal(out["x"], ref_x), f"replay {i}"
+        assert torch.equal(out["pos"], ref_pos), f"replay {i}"
