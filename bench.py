@@ -1,0 +1,238 @@
+#!/usr/bin/env python3
+"""Throughput of the pruned layer-stack forward on one MI355X.
+
+Workload: a 12-layer BERT-base-shaped encoder (d = 768, 12 heads, FFN 3072,
+exact GELU, pre-LN), 32 sequences x 512 rows, bf16 storage, random-init
+N(0, 0.02) weights and N(0, 1) hidden rows (synthetic), pruned after
+layers 3, 6 and 9. One step = one whole stack forward over the batch
+(norms, projections, attention, contribution scores, top-k, compaction),
+replayed as a HIP graph with every input already in HBM.
+
+The keep rate is swept over 1.0, 0.7, 0.5, 0.3, 0.1; `value` is the
+throughput at keep rate 0.5 (input tokens per second), the other points go
+to `sweep` with their speedup over keep rate 1.
+
+`roofline` is reported for the kernel class with the largest share of GPU
+time (the projection GEMM): algorithmic FLOPs (2 * rows * out * in per
+launch) over the summed launch durations measured with HIP events on the
+launch stream, against the 2.5 PFLOP/s dense bf16 MFMA peak.
+`cpu_baseline` times the float64 CPU oracle on a bounded sample of the same
+workload.
+"""
+import argparse
+import json
+import os
+import sys
+import time
+
+import numpy as np
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+if ROOT not in sys.path:
+    sys.path.insert(0, ROOT)
+
+METRIC = "tokens/sec of pruned layer-stack forward vs keep_rate (1 GPU) + roofline %"
+PEAK_BF16_TFLOPS = 2500.0
+PEAK_HBM_GBS = 8000.0
+HEADLINE_RATE = 0.5
+
+
+def parse():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=20)
+    ap.add_argument("--warmup", type=int, default=5)
+    ap.add_argument("--workload", default="bert")
+    ap.add_argument("--keep-rates", default=None, help="comma-separated sweep")
+    ap.add_argument("--seed", type=int, default=0)
+    ap.add_argument("--no-graph", action="store_true", help="time eager launches instead")
+    ap.add_argument("--cpu-seconds", type=float, default=15.0,
+                    help="target wall time of the CPU-oracle sample (0 disables it)")
+    return ap.parse_args()
+
+
+def gemm_flops(p, rows_in, rows_after):
+    """Algorithmic FLOPs of the projections of each layer: 2 * M * N * K,
+    with M the rows the GEMM processes (the pruned rows after the pruning
+    layer's attention)."""
+    d, F = p.d_model, p.d_ff
+    up_n = 2 * F if p.kind == 1 else F
+    total = 0
+    for l in range(p.n_layers):
+        t_in, t_out = rows_in[l], rows_after[l]
+        total += 2 * t_in * 3 * d * d          # QKV
+        total += 2 * t_out * d * d             # output projection
+        total += 2 * t_out * up_n * d          # up (or gate|up)
+        total += 2 * t_out * d * F             # down
+    return total
+
+
+def layer_rows(p, plan):
+    rows_in, rows_after = [], []
+    cur = plan["rows_in"][0]
+    point = 0
+    for l in range(1, p.n_layers + 1):
+        rows_in.append(cur)
+        if point < len(p.prune_after) and p.prune_after[point] == l:
+            cur = plan["rows_in"][point + 1]
+            point += 1
+        rows_after.append(cur)
+    return rows_in, rows_after
+
+
+def cpu_baseline(p, ws_np, x_np, lens, rate, budget_s):
+    """The float64 oracle (as it stands) on a bounded sample of sequences."""
+    from oracle import zsa_oracle as O
+    from paper_2509_01190_amd import workloads as W
+    try:
+        from threadpoolctl import threadpool_info
+        threads = max([i.get("num_threads", 1) for i in threadpool_info()] or [1])
+    except Exception:  # pragma: no cover
+        threads = 1
+    ocfg = O.LayerCfg(p.kind, p.d_model, p.n_heads, p.d_ff, p.causal, p.norm_eps, p.rope_theta,
+                      p.tau)
+    ows = [{k: (None if v is None else W.as_f64(W.to_storage(v, p.dtype))) for k, v in w.items()}
+           for w in ws_np]
+    x64 = W.as_f64(W.to_storage(x_np, p.dtype))
+    cu = W.cu_seqlens(lens)
+    done_rows, elapsed, nseq = 0, 0.0, 0
+    while nseq < len(lens) and (elapsed < budget_s * 0.5 or nseq == 0):
+        b = nseq
+        n = lens[b]
+        xb = x64[cu[b]:cu[b + 1]]
+        t0 = time.perf_counter()
+        O.stack_forward(xb, np.arange(n), [0, n], ows, ocfg, p.prune_after, [rate])
+        elapsed += time.perf_counter() - t0
+        done_rows += n
+        nseq += 1
+        per = elapsed / nseq
+        if elapsed + per > budget_s:
+            break
+    return {"value": done_rows / elapsed, "unit": "tokens/s", "cores": int(threads),
+            "kind": "oracle",
+            "sample": f"{nseq} of {len(lens)} sequences x {lens[0]} rows, keep_rate {rate}, "
+                      f"float64 exact mode, {elapsed:.1f} s"}
+
+
+def main():
+    args = parse()
+    if args.gpus != 1:
+        print(f"bench.py runs on one GPU only (asked for --gpus {args.gpus}); the pruned stack "
+              f"is measured on a single MI355X and this build has no multi-GPU path.",
+              file=sys.stderr)
+        sys.exit(2)
+
+    import torch
+
+    from paper_2509_01190_amd import workloads as W
+    from paper_2509_01190_amd import zsa
+
+    if not torch.cuda.is_available():
+        print("bench.py needs a GPU", file=sys.stderr)
+        sys.exit(1)
+    dev = torch.device("cuda:0")
+    p = W.PRESETS[args.workload]
+    rates = [float(r) for r in args.keep_rates.split(",")] if args.keep_rates else list(p.keep_rates)
+    if HEADLINE_RATE not in rates:
+        rates.append(HEADLINE_RATE)
+    lens = W.lengths(p, args.seed)
+    ws_np = W.stack_weights(p, args.seed)
+    x_np = W.hidden(p, args.seed, lens)
+    dws = [{k: (None if v is None else W.to_storage(v, p.dtype).to(dev)) for k, v in w.items()}
+           for w in ws_np]
+    cfg = zsa.make_cfg(p.kind, p.d_model, p.n_heads, p.d_ff, p.causal,
+                       zsa.BF16 if p.dtype == "bf16" else zsa.F32, p.tau, p.norm_eps, p.rope_theta)
+    stack = zsa.Stack(cfg, dws)
+    seqs = zsa.Seqs(lens, dev)
+    xd = W.to_storage(x_np, p.dtype).to(dev)
+    posd = torch.from_numpy(W.positions(lens)).to(dev)
+    tokens = int(sum(lens))
+
+    results = {}
+    for rate in rates:
+        kr = W.keep_rates(p, args.seed, rate)
+        outs = stack.forward(xd, posd, seqs, p.prune_after, kr)   # allocates outputs once
+        torch.cuda.synchronize()
+        if args.no_graph:
+            def step():
+                stack.forward(xd, posd, seqs, p.prune_after, kr, out=outs)
+        else:
+            g = torch.cuda.CUDAGraph()
+            s = torch.cuda.Stream()
+            s.wait_stream(torch.cuda.current_stream())
+            with torch.cuda.stream(s):
+                with torch.cuda.graph(g, stream=s):
+                    stack.forward(xd, posd, seqs, p.prune_after, kr, out=outs)
+            torch.cuda.current_stream().wait_stream(s)
+            step = g.replay
+        for _ in range(args.warmup):
+            step()
+        torch.cuda.synchronize()
+        t0 = time.perf_counter()
+        for _ in range(args.steps):
+            step()
+        torch.cuda.synchronize()
+        ms = (time.perf_counter() - t0) * 1e3 / args.steps
+
+        # per-class launch durations of one eager forward (HIP events on the stream)
+        for c in range(len(zsa.KCLASS_NAMES)):
+            zsa.timing_arm(c, 1024)
+        stack.forward(xd, posd, seqs, p.prune_after, kr, out=outs)
+        torch.cuda.synchronize()
+        cls = {}
+        for c, name in enumerate(zsa.KCLASS_NAMES):
+            n, t = zsa.timing_read(c)
+            cls[name] = {"launches": n, "ms": t}
+        plan = stack.plan(seqs, p.prune_after, kr)
+        rows_in, rows_after = layer_rows(p, plan)
+        results[rate] = {"ms": ms, "tok_s": tokens / (ms * 1e-3), "classes": cls,
+                         "gemm_flops": gemm_flops(p, rows_in, rows_after),
+                         "kept_rows_final": plan["final_rows"]}
+
+    base = results.get(1.0)
+    sweep = []
+    for rate in rates:
+        r = results[rate]
+        sweep.append({"keep_rate": rate, "tokens_per_s": round(r["tok_s"], 1),
+                      "ms_per_step": round(r["ms"], 4),
+                      "speedup_vs_keep_rate_1": None if base is None else round(base["ms"] / r["ms"], 3),
+                      "rows_after_last_prune": r["kept_rows_final"]})
+
+    # dominant kernel class over the whole sweep (every rate runs the same
+    # number of steps, so this is also the mix a profiler sees)
+    tot = {name: sum(results[r]["classes"][name]["ms"] for r in rates) for name in zsa.KCLASS_NAMES}
+    dom = max(tot, key=tot.get)
+    g_ms = sum(results[r]["classes"]["gemm"]["ms"] for r in rates)
+    g_n = sum(results[r]["classes"]["gemm"]["launches"] for r in rates)
+    g_flops = sum(results[r]["gemm_flops"] for r in rates)
+    achieved = g_flops / (g_ms * 1e-3) / 1e12 if g_ms > 0 else 0.0
+    roofline = {"kernel": "gemm_bf16_mfma_kernel (all projection GEMMs)", "bound": "mfma",
+                "achieved": round(achieved, 1), "peak": PEAK_BF16_TFLOPS, "unit": "TFLOP/s",
+                "frac": round(achieved / PEAK_BF16_TFLOPS, 4), "traffic": None,
+                "avg_launch_us": round(g_ms * 1e3 / max(g_n, 1), 2), "launches": g_n,
+                "dominant_class": dom}
+    head = results[HEADLINE_RATE]
+    phases = {name: round(v["ms"], 4) for name, v in head["classes"].items() if v["launches"]}
+
+    cpu = None
+    if args.cpu_seconds > 0:
+        cpu = cpu_baseline(p, ws_np, x_np, lens, HEADLINE_RATE, args.cpu_seconds)
+
+    line = {
+        "metric": METRIC, "value": round(head["tok_s"], 1), "unit": "tokens/s", "n_gpus": 1,
+        "steps": args.steps, "warmup": args.warmup, "ms_per_step": round(head["ms"], 4),
+        "higher_is_better": True, "scaling": "weak", "vs_baseline": None, "dtype": p.dtype,
+        "data": "synthetic (seeded N(0,0.02) weights, N(0,1) hidden rows)",
+        "config": {"workload": f"{p.name}: {p.n_layers}-layer encoder d{p.d_model} H{p.n_heads} "
+                               f"FFN{p.d_ff}, {p.batch}x{p.seq_len} rows, pruned after layers "
+                               f"{'/'.join(map(str, p.prune_after))}",
+                   "keep_rate": HEADLINE_RATE, "global_batch": p.batch, "seq_len": p.seq_len,
+                   "graph": not args.no_graph},
+        "sweep": sweep, "phases_ms_at_headline": phases, "roofline": roofline,
+        "cpu_baseline": cpu,
+    }
+    print(json.dumps(line))
+
+
+if __name__ == "__main__":
+    main()

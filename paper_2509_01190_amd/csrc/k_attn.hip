@@ -59,14 +59,13 @@ __global__ __launch_bounds__(256) void attn_mfma_kernel(
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int half = lane >> 5, l32 = lane & 31;
   const int qrow = q0 + wave * 32 + l32;
-  const uint4 zero = make_uint4(0, 0, 0, 0);
-
   bf16x8_t qf[HD / 16];
 #pragma unroll
   for (int kk = 0; kk < HD / 16; ++kk) {
-    const uint4 v = qrow < n ? *reinterpret_cast<const uint4*>(
-                                   Q + static_cast<int64_t>(lo + qrow) * rs + h * HD + kk * 16 + half * 8)
-                             : zero;
+    const int qr = min(qrow, n - 1);
+    const uint4 v = keep16(*reinterpret_cast<const uint4*>(
+                               Q + static_cast<int64_t>(lo + qr) * rs + h * HD + kk * 16 + half * 8),
+                           qrow < n);
     qf[kk] = __builtin_bit_cast(bf16x8_t, v);
   }
 
@@ -83,17 +82,19 @@ __global__ __launch_bounds__(256) void attn_mfma_kernel(
     for (int c = tid; c < BKEY * HD / 8; c += 256) {
       const int r = c / (HD / 8), ch = (c % (HD / 8)) * 8;
       const int jr = j0 + r;
-      *reinterpret_cast<uint4*>(Ks + r * KLD + ch) =
-          jr < n ? *reinterpret_cast<const uint4*>(K + static_cast<int64_t>(lo + jr) * rs + h * HD + ch)
-                 : zero;
+      *reinterpret_cast<uint4*>(Ks + r * KLD + ch) = keep16(
+          *reinterpret_cast<const uint4*>(K + static_cast<int64_t>(lo + min(jr, n - 1)) * rs + h * HD + ch),
+          jr < n);
     }
     for (int c = tid; c < (BKEY / 2) * (HD / 8); c += 256) {
       const int rp = c / (HD / 8), ch = (c % (HD / 8)) * 8;
       const int jr = j0 + 2 * rp;
-      const uint4 v0 = jr < n ? *reinterpret_cast<const uint4*>(V + static_cast<int64_t>(lo + jr) * rs + h * HD + ch)
-                              : zero;
-      const uint4 v1 = jr + 1 < n ? *reinterpret_cast<const uint4*>(V + static_cast<int64_t>(lo + jr + 1) * rs + h * HD + ch)
-                                  : zero;
+      const uint4 v0 = keep16(*reinterpret_cast<const uint4*>(
+                                  V + static_cast<int64_t>(lo + min(jr, n - 1)) * rs + h * HD + ch),
+                              jr < n);
+      const uint4 v1 = keep16(*reinterpret_cast<const uint4*>(
+                                  V + static_cast<int64_t>(lo + min(jr + 1, n - 1)) * rs + h * HD + ch),
+                              jr + 1 < n);
 #pragma unroll
       for (int e = 0; e < 8; ++e)
         *reinterpret_cast<uint32_t*>(Vt + (ch + e) * VLD + 2 * rp) = bf16_at(v0, e) | (bf16_at(v1, e) << 16);

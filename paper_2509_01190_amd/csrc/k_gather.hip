@@ -26,9 +26,13 @@ __global__ __launch_bounds__(256) void gather_rows_kernel(
     const bool ok = src >= 0 && src < t_in;
     const int64_t so = static_cast<int64_t>(src) * chunks_per_row + c;
     const int64_t d_o = static_cast<int64_t>(r) * chunks_per_row + c;
-    const uint4 zero = make_uint4(0, 0, 0, 0);
-    dst0[d_o] = ok ? src0[so] : zero;
-    if (src1 != nullptr) dst1[d_o] = ok ? src1[so] : zero;
+    uint4 v0 = make_uint4(0u, 0u, 0u, 0u), v1 = v0;
+    if (ok) {
+      v0 = src0[so];
+      if (src1 != nullptr) v1 = src1[so];
+    }
+    dst0[d_o] = v0;
+    if (src1 != nullptr) dst1[d_o] = v1;
     if (c == 0 && pos_out != nullptr) pos_out[r] = ok ? pos[src] : -1;
   }
 }

@@ -17,6 +17,7 @@
 // the rotary rotation of head channel pairs (i, i+hd/2), which needs the
 // partner column of the same row) and stores them as one 16-byte vector.
 #include <math.h>
+#include <stdlib.h>
 
 #include "zsa_internal.h"
 
@@ -152,60 +153,70 @@ __device__ void epilogue_tile(const float* tile, int ldt, int m0, int n0, int M,
 // ---------------------------------------------------------------------------
 // bf16 MFMA GEMM
 // ---------------------------------------------------------------------------
-constexpr int kBM = 128, kBN = 128, kBK = 64, kLDK = kBK + 8;
-constexpr int kMfmaLds = 2 * (kBM + kBN) * kLDK * 2;  // bytes, double-buffered A and B
-constexpr int kTileLd = kBN + 4;
-static_assert(kBM * kTileLd * 4 <= kMfmaLds, "epilogue tile must fit in the operand buffers");
+constexpr int kBK = 64, kLDK = kBK + 8;  // K step; padded LDS row (bf16)
+constexpr int kTileLd = 128 + 4;         // fp32 epilogue tile row stride (128 columns)
 
-__global__ __launch_bounds__(256) void gemm_bf16_mfma_kernel(const bf16_t* __restrict__ X,
-                                                             const bf16_t* __restrict__ W,
-                                                             int M, int N, int K, EpiParams ep) {
+template <int BM, int BN>
+constexpr int mfma_lds_bytes() {
+  return 2 * (BM + BN) * kLDK * 2 > 128 * kTileLd * 4 ? 2 * (BM + BN) * kLDK * 2
+                                                       : 128 * kTileLd * 4;
+}
+
+// BM x BN output tile, WM x WN waves, each wave (BM/WM) x (BN/WN) made of
+// 32x32 MFMA tiles. The operand staging arrays are indexed only by
+// unrolled constants so they stay in VGPRs, and the next K step's global
+// loads are issued before this step's MFMAs so their latency is hidden.
+template <int BM, int BN, int WM, int WN>
+__global__ __launch_bounds__(WM * WN * 64) void gemm_bf16_mfma_kernel(
+    const bf16_t* __restrict__ X, const bf16_t* __restrict__ W, int M, int N, int K,
+    EpiParams ep) {
+  static_assert(BN == 128, "the epilogue stages 128-column tiles");
+  constexpr int NT = WM * WN * 64;
+  constexpr int WTM = BM / WM, WTN = BN / WN;
+  constexpr int TM = WTM / 32, TN = WTN / 32;
+  constexpr int RPP = NT / 8;                 // rows covered by one pass of 16-byte chunks
+  constexpr int ACH = BM / RPP, BCH = BN / RPP;
   extern __shared__ __align__(16) unsigned char smem[];
-  bf16_t* As = reinterpret_cast<bf16_t*>(smem);  // [2][kBM][kLDK]
-  bf16_t* Bs = As + 2 * kBM * kLDK;              // [2][kBN][kLDK]
+  bf16_t* As = reinterpret_cast<bf16_t*>(smem);  // [2][BM][kLDK]
+  bf16_t* Bs = As + 2 * BM * kLDK;               // [2][BN][kLDK]
   const int tid = threadIdx.x;
   const int lane = tid & 63;
   const int wave = tid >> 6;
-  const int wm = wave >> 1, wn = wave & 1;
-  const int m0 = blockIdx.x * kBM;
-  const int n0 = blockIdx.y * kBN;
-  constexpr int TM = kBM / 2 / 32, TN = kBN / 2 / 32;
-  constexpr int ACH = kBM * kBK / 8 / 256, BCH = kBN * kBK / 8 / 256;
+  const int wm = wave / WN, wn = wave % WN;
+  const int m0 = blockIdx.x * BM;
+  const int n0 = blockIdx.y * BN;
+  const int lrow = tid >> 3, lkc = (tid & 7) * 8;
 
+  const bf16_t* xp[ACH];
+  bool xv[ACH];
+#pragma unroll
+  for (int i = 0; i < ACH; ++i) {
+    const int gm = m0 + lrow + i * RPP;
+    xv[i] = gm < M;
+    xp[i] = X + static_cast<int64_t>(xv[i] ? gm : M - 1) * K + lkc;
+  }
+  const bf16_t* wp[BCH];
+  bool wv[BCH];
+#pragma unroll
+  for (int i = 0; i < BCH; ++i) {
+    const int gn = n0 + lrow + i * RPP;
+    wv[i] = gn < N;
+    wp[i] = W + static_cast<int64_t>(wv[i] ? gn : N - 1) * K + lkc;
+  }
   uint4 ra[ACH], rb[BCH];
-  const uint4 zero = make_uint4(0, 0, 0, 0);
-  auto gload = [&](int k0) {
-#pragma unroll
-    for (int i = 0; i < ACH; ++i) {
-      const int c = tid + i * 256;
-      const int r = c >> 3, kc = (c & 7) * 8;
-      const int gm = m0 + r;
-      ra[i] = gm < M ? *reinterpret_cast<const uint4*>(X + static_cast<int64_t>(gm) * K + k0 + kc)
-                     : zero;
-    }
-#pragma unroll
-    for (int i = 0; i < BCH; ++i) {
-      const int c = tid + i * 256;
-      const int r = c >> 3, kc = (c & 7) * 8;
-      const int gn = n0 + r;
-      rb[i] = gn < N ? *reinterpret_cast<const uint4*>(W + static_cast<int64_t>(gn) * K + k0 + kc)
-                     : zero;
-    }
-  };
-  auto sstore = [&](int buf) {
-#pragma unroll
-    for (int i = 0; i < ACH; ++i) {
-      const int c = tid + i * 256;
-      const int r = c >> 3, kc = (c & 7) * 8;
-      *reinterpret_cast<uint4*>(As + (buf * kBM + r) * kLDK + kc) = ra[i];
-    }
-#pragma unroll
-    for (int i = 0; i < BCH; ++i) {
-      const int c = tid + i * 256;
-      const int r = c >> 3, kc = (c & 7) * 8;
-      *reinterpret_cast<uint4*>(Bs + (buf * kBN + r) * kLDK + kc) = rb[i];
-    }
-  };
+
+#define ZSA_GLOAD(k0)                                                              \
+  _Pragma("unroll") for (int i = 0; i < ACH; ++i) {                                \
+    ra[i] = keep16(*reinterpret_cast<const uint4*>(xp[i] + (k0)), xv[i]);          \
+  }                                                                                \
+  _Pragma("unroll") for (int i = 0; i < BCH; ++i) {                                \
+    rb[i] = keep16(*reinterpret_cast<const uint4*>(wp[i] + (k0)), wv[i]);          \
+  }
+#define ZSA_SSTORE(buf)                                                            \
+  _Pragma("unroll") for (int i = 0; i < ACH; ++i)                                  \
+    *reinterpret_cast<uint4*>(As + ((buf) * BM + lrow + i * RPP) * kLDK + lkc) = ra[i]; \
+  _Pragma("unroll") for (int i = 0; i < BCH; ++i)                                  \
+    *reinterpret_cast<uint4*>(Bs + ((buf) * BN + lrow + i * RPP) * kLDK + lkc) = rb[i];
 
   f32x16_t acc[TM][TN];
 #pragma unroll
@@ -216,14 +227,17 @@ __global__ __launch_bounds__(256) void gemm_bf16_mfma_kernel(const bf16_t* __res
       for (int r = 0; r < 16; ++r) acc[i][j][r] = 0.f;
 
   const int KT = K / kBK;
-  gload(0);
-  sstore(0);
+  ZSA_GLOAD(0)
+  ZSA_SSTORE(0)
   __syncthreads();
   for (int kt = 0; kt < KT; ++kt) {
     const int buf = kt & 1;
-    if (kt + 1 < KT) gload((kt + 1) * kBK);
-    const bf16_t* Ab = As + (buf * kBM + wm * (kBM / 2) + (lane & 31)) * kLDK + (lane >> 5) * 8;
-    const bf16_t* Bb = Bs + (buf * kBN + wn * (kBN / 2) + (lane & 31)) * kLDK + (lane >> 5) * 8;
+    const bool more = kt + 1 < KT;
+    if (more) {
+      ZSA_GLOAD((kt + 1) * kBK)
+    }
+    const bf16_t* Ab = As + (buf * BM + wm * WTM + (lane & 31)) * kLDK + (lane >> 5) * 8;
+    const bf16_t* Bb = Bs + (buf * BN + wn * WTN + (lane & 31)) * kLDK + (lane >> 5) * 8;
 #pragma unroll
     for (int kk = 0; kk < kBK / 16; ++kk) {
       bf16x8_t a[TM], b[TN];
@@ -241,25 +255,36 @@ __global__ __launch_bounds__(256) void gemm_bf16_mfma_kernel(const bf16_t* __res
         for (int j = 0; j < TN; ++j)
           acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a[i], b[j], acc[i][j], 0, 0, 0);
     }
-    if (kt + 1 < KT) sstore(buf ^ 1);
+    if (more) {
+      ZSA_SSTORE(buf ^ 1)
+    }
     __syncthreads();
   }
+#undef ZSA_GLOAD
+#undef ZSA_SSTORE
 
   // accumulator layout of a 32x32 MFMA tile: lane l, register r holds
-  // row 8*(r/4) + 4*(l/32) + r%4, column l%32
+  // row 8*(r/4) + 4*(l/32) + r%4, column l%32. The fp32 tile is staged
+  // through LDS 128 rows at a time.
   float* tile = reinterpret_cast<float*>(smem);
 #pragma unroll
-  for (int i = 0; i < TM; ++i)
+  for (int pass = 0; pass < BM / 128; ++pass) {
+    if (pass > 0) __syncthreads();
+    if ((wm * WTM) / 128 == pass) {
 #pragma unroll
-    for (int j = 0; j < TN; ++j)
+      for (int i = 0; i < TM; ++i)
 #pragma unroll
-      for (int r = 0; r < 16; ++r) {
-        const int row = wm * (kBM / 2) + i * 32 + (r >> 2) * 8 + (lane >> 5) * 4 + (r & 3);
-        const int col = wn * (kBN / 2) + j * 32 + (lane & 31);
-        tile[row * kTileLd + col] = acc[i][j][r];
-      }
-  __syncthreads();
-  epilogue_tile<bf16_t, kBM, kBN, 256>(tile, kTileLd, m0, n0, M, N, ep);
+        for (int j = 0; j < TN; ++j)
+#pragma unroll
+          for (int r = 0; r < 16; ++r) {
+            const int row = wm * WTM - pass * 128 + i * 32 + (r >> 2) * 8 + (lane >> 5) * 4 + (r & 3);
+            const int col = wn * WTN + j * 32 + (lane & 31);
+            tile[row * kTileLd + col] = acc[i][j][r];
+          }
+    }
+    __syncthreads();
+    epilogue_tile<bf16_t, 128, BN, NT>(tile, kTileLd, m0 + pass * 128, n0, M, N, ep);
+  }
 }
 
 // ---------------------------------------------------------------------------
@@ -320,22 +345,45 @@ __global__ __launch_bounds__(256) void gemm_valu_kernel(const T* __restrict__ X,
   epilogue_tile<T, vBM, vBN, 256>(tile, vBN + 4, m0, n0, M, N, ep);
 }
 
+
+template <int BM, int BN, int WM, int WN>
+hipError_t launch_mfma(hipStream_t s, const void* x, int M, int K, const void* w, int N,
+                       const EpiParams& ep) {
+  constexpr int lds = mfma_lds_bytes<BM, BN>();
+  static bool lds_raised = false;  // more than 64 KiB of dynamic LDS per workgroup
+  if (!lds_raised) {
+    const hipError_t e = hipFuncSetAttribute(
+        reinterpret_cast<const void*>(gemm_bf16_mfma_kernel<BM, BN, WM, WN>),
+        hipFuncAttributeMaxDynamicSharedMemorySize, lds);
+    if (e != hipSuccess) return e;
+    lds_raised = true;
+  }
+  const dim3 grid((M + BM - 1) / BM, (N + BN - 1) / BN);
+  return launch(K_GEMM, gemm_bf16_mfma_kernel<BM, BN, WM, WN>, grid, dim3(WM * WN * 64), lds, s,
+                static_cast<const bf16_t*>(x), static_cast<const bf16_t*>(w), M, N, K, ep);
+}
+
 }  // namespace
+
+// Tile choice: by shape, unless ZSA_GEMM_TILE=128 or =256 pins one (tuning aid).
+static int gemm_tile_override() {
+  static const int v = [] {
+    const char* e = getenv("ZSA_GEMM_TILE");
+    return e == nullptr ? 0 : atoi(e);
+  }();
+  return v;
+}
 
 hipError_t launch_gemm(hipStream_t s, int dtype, const void* x, int M, int K, const void* w,
                        int N, const EpiParams& ep) {
   if (M == 0 || N == 0) return hipSuccess;
   if (dtype == 1 && K % kBK == 0) {
-    static bool lds_raised = false;  // > 64 KiB of dynamic LDS per workgroup
-    if (!lds_raised) {
-      const hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void*>(gemm_bf16_mfma_kernel),
-                                               hipFuncAttributeMaxDynamicSharedMemorySize, kMfmaLds);
-      if (e != hipSuccess) return e;
-      lds_raised = true;
-    }
-    const dim3 grid((M + kBM - 1) / kBM, (N + kBN - 1) / kBN);
-    return launch(K_GEMM, gemm_bf16_mfma_kernel, grid, dim3(256), kMfmaLds, s,
-                  static_cast<const bf16_t*>(x), static_cast<const bf16_t*>(w), M, N, K, ep);
+    const int gemm_variant = gemm_tile_override() == 256 ? 2 : gemm_tile_override() == 128 ? 1 : 0;
+    // 256x128 (one wave per SIMD) measured slower than 128x128 on every
+    // projection shape here; it stays selectable for tuning
+    const bool big = gemm_variant == 2;
+    if (big) return launch_mfma<256, 128, 2, 2>(s, x, M, K, w, N, ep);
+    return launch_mfma<128, 128, 2, 2>(s, x, M, K, w, N, ep);
   }
   const dim3 grid((M + vBM - 1) / vBM, (N + vBN - 1) / vBN);
   if (dtype == 1)

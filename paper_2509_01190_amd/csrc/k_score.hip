@@ -48,7 +48,6 @@ __global__ __launch_bounds__(256) void score_mfma_kernel(
   if (j0 >= n) return;
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int half = lane >> 5, l32 = lane & 31;
-  const uint4 zero = make_uint4(0, 0, 0, 0);
   float colsum[2] = {0.f, 0.f};
 
   const int qs = causal ? (j0 & ~31) : 0;
@@ -57,9 +56,9 @@ __global__ __launch_bounds__(256) void score_mfma_kernel(
     for (int c = tid; c < 64 * HD / 8; c += 256) {
       const int r = c / (HD / 8), ch = (c % (HD / 8)) * 8;
       const int jr = j0 + r;
-      *reinterpret_cast<uint4*>(Ks + r * KLD + ch) =
-          jr < n ? *reinterpret_cast<const uint4*>(K + static_cast<int64_t>(lo + jr) * rs + h * HD + ch)
-                 : zero;
+      *reinterpret_cast<uint4*>(Ks + r * KLD + ch) = keep16(
+          *reinterpret_cast<const uint4*>(K + static_cast<int64_t>(lo + min(jr, n - 1)) * rs + h * HD + ch),
+          jr < n);
     }
     __syncthreads();
     bf16x8_t kf[2][HD / 16];
@@ -82,9 +81,9 @@ __global__ __launch_bounds__(256) void score_mfma_kernel(
 #pragma unroll
         for (int kk = 0; kk < HD / 16; ++kk)
           qa[kk] = __builtin_bit_cast(
-              bf16x8_t, qr < n ? *reinterpret_cast<const uint4*>(
-                                     Q + static_cast<int64_t>(lo + qr) * rs + h * HD + kk * 16 + half * 8)
-                               : zero);
+              bf16x8_t, keep16(*reinterpret_cast<const uint4*>(
+                                   Q + static_cast<int64_t>(lo + min(qr, n - 1)) * rs + h * HD + kk * 16 + half * 8),
+                               qr < n));
 #pragma unroll
         for (int ks = 0; ks < 2; ++ks) {
           f32x16_t acc;

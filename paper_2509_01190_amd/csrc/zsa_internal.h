@@ -66,6 +66,13 @@ __device__ __forceinline__ uint4 pack16(const float* in, bf16_t) {
   return make_uint4(w[0], w[1], w[2], w[3]);
 }
 
+// keep a 16-byte value or zero it, without a select between two uint4 objects
+// (which the compiler lowers through a stack slot)
+__device__ __forceinline__ uint4 keep16(const uint4& v, bool keep) {
+  const uint32_t m = keep ? 0xffffffffu : 0u;
+  return make_uint4(v.x & m, v.y & m, v.z & m, v.w & m);
+}
+
 // ---------------------------------------------------------------------------
 // launch helper with the optional per-class timing hook
 // ---------------------------------------------------------------------------
