@@ -48,6 +48,21 @@ def assert_rel_l2(got: np.ndarray, ref: np.ndarray, tol: float, what: str = "") 
     assert e <= tol, f"{what}: relative L2 error {e:.3e} > {tol:.1e}"
 
 
+def assert_rows_close(got: np.ndarray, ref: np.ndarray, tol: float, what: str = "") -> None:
+    """Every row's relative L2 error <= tol (a row that went to the wrong
+    place, or was rotated with the wrong position, is off by O(1))."""
+    got = np.asarray(got, dtype=np.float64)
+    ref = np.asarray(ref, dtype=np.float64)
+    assert got.shape == ref.shape, (what, got.shape, ref.shape)
+    if ref.size == 0:
+        return
+    num = np.linalg.norm(got - ref, axis=1)
+    den = np.maximum(np.linalg.norm(ref, axis=1), 1e-30)
+    worst = int(np.argmax(num / den))
+    assert num[worst] / den[worst] <= tol, \
+        f"{what}: row {worst} relative error {num[worst] / den[worst]:.3e} > {tol:.1e}"
+
+
 def modes(dtype: str):
     """(mode for hidden-state L2 tolerance, mode for scores / kept sets and
     the elementwise check): bf16 storage is judged in L2 against the exact
