@@ -62,11 +62,10 @@ __global__ __launch_bounds__(256) void attn_mfma_kernel(
   bf16x8_t qf[HD / 16];
 #pragma unroll
   for (int kk = 0; kk < HD / 16; ++kk) {
+    // rows past the sequence are clamped, not zeroed: their outputs are not stored
     const int qr = min(qrow, n - 1);
-    const uint4 v = keep16(*reinterpret_cast<const uint4*>(
-                               Q + static_cast<int64_t>(lo + qr) * rs + h * HD + kk * 16 + half * 8),
-                           qrow < n);
-    qf[kk] = __builtin_bit_cast(bf16x8_t, v);
+    qf[kk] = __builtin_bit_cast(bf16x8_t, *reinterpret_cast<const uint4*>(
+                                              Q + static_cast<int64_t>(lo + qr) * rs + h * HD + kk * 16 + half * 8));
   }
 
   float m_run = -INFINITY, l_run = 0.f;
@@ -82,19 +81,18 @@ __global__ __launch_bounds__(256) void attn_mfma_kernel(
     for (int c = tid; c < BKEY * HD / 8; c += 256) {
       const int r = c / (HD / 8), ch = (c % (HD / 8)) * 8;
       const int jr = j0 + r;
-      *reinterpret_cast<uint4*>(Ks + r * KLD + ch) = keep16(
-          *reinterpret_cast<const uint4*>(K + static_cast<int64_t>(lo + min(jr, n - 1)) * rs + h * HD + ch),
-          jr < n);
+      // keys past the sequence repeat the last row: they are masked to
+      // probability 0, and the repeated V rows are finite
+      *reinterpret_cast<uint4*>(Ks + r * KLD + ch) =
+          *reinterpret_cast<const uint4*>(K + static_cast<int64_t>(lo + min(jr, n - 1)) * rs + h * HD + ch);
     }
     for (int c = tid; c < (BKEY / 2) * (HD / 8); c += 256) {
       const int rp = c / (HD / 8), ch = (c % (HD / 8)) * 8;
       const int jr = j0 + 2 * rp;
-      const uint4 v0 = keep16(*reinterpret_cast<const uint4*>(
-                                  V + static_cast<int64_t>(lo + min(jr, n - 1)) * rs + h * HD + ch),
-                              jr < n);
-      const uint4 v1 = keep16(*reinterpret_cast<const uint4*>(
-                                  V + static_cast<int64_t>(lo + min(jr + 1, n - 1)) * rs + h * HD + ch),
-                              jr + 1 < n);
+      const uint4 v0 = *reinterpret_cast<const uint4*>(
+          V + static_cast<int64_t>(lo + min(jr, n - 1)) * rs + h * HD + ch);
+      const uint4 v1 = *reinterpret_cast<const uint4*>(
+          V + static_cast<int64_t>(lo + min(jr + 1, n - 1)) * rs + h * HD + ch);
 #pragma unroll
       for (int e = 0; e < 8; ++e)
         *reinterpret_cast<uint32_t*>(Vt + (ch + e) * VLD + 2 * rp) = bf16_at(v0, e) | (bf16_at(v1, e) << 16);

@@ -154,12 +154,12 @@ __device__ void epilogue_tile(const float* tile, int ldt, int m0, int n0, int M,
 // bf16 MFMA GEMM
 // ---------------------------------------------------------------------------
 constexpr int kBK = 64, kLDK = kBK + 8;  // K step; padded LDS row (bf16)
-constexpr int kTileLd = 128 + 4;         // fp32 epilogue tile row stride (128 columns)
 
+// fp32 epilogue tile: 128 rows of BN columns, row stride BN + 4
 template <int BM, int BN>
 constexpr int mfma_lds_bytes() {
-  return 2 * (BM + BN) * kLDK * 2 > 128 * kTileLd * 4 ? 2 * (BM + BN) * kLDK * 2
-                                                       : 128 * kTileLd * 4;
+  return 2 * (BM + BN) * kLDK * 2 > 128 * (BN + 4) * 4 ? 2 * (BM + BN) * kLDK * 2
+                                                        : 128 * (BN + 4) * 4;
 }
 
 // BM x BN output tile, WM x WN waves, each wave (BM/WM) x (BN/WN) made of
@@ -170,8 +170,9 @@ template <int BM, int BN, int WM, int WN>
 __global__ __launch_bounds__(WM * WN * 64) void gemm_bf16_mfma_kernel(
     const bf16_t* __restrict__ X, const bf16_t* __restrict__ W, int M, int N, int K,
     EpiParams ep) {
-  static_assert(BN == 128, "the epilogue stages 128-column tiles");
+  static_assert(BM % 128 == 0 && (BN == 128 || BN == 256), "tile shape");
   constexpr int NT = WM * WN * 64;
+  constexpr int kTileLd = BN + 4;
   constexpr int WTM = BM / WM, WTN = BN / WN;
   constexpr int TM = WTM / 32, TN = WTN / 32;
   constexpr int RPP = NT / 8;                 // rows covered by one pass of 16-byte chunks
@@ -187,36 +188,31 @@ __global__ __launch_bounds__(WM * WN * 64) void gemm_bf16_mfma_kernel(
   const int n0 = blockIdx.y * BN;
   const int lrow = tid >> 3, lkc = (tid & 7) * 8;
 
+  // Rows past M (or N) are clamped to the last row instead of zeroed: they
+  // only feed output rows (columns) that are never stored, and a mask
+  // applied at load time would make the loads wait before the MFMAs.
   const bf16_t* xp[ACH];
-  bool xv[ACH];
 #pragma unroll
-  for (int i = 0; i < ACH; ++i) {
-    const int gm = m0 + lrow + i * RPP;
-    xv[i] = gm < M;
-    xp[i] = X + static_cast<int64_t>(xv[i] ? gm : M - 1) * K + lkc;
-  }
+  for (int i = 0; i < ACH; ++i)
+    xp[i] = X + static_cast<int64_t>(min(m0 + lrow + i * RPP, M - 1)) * K + lkc;
   const bf16_t* wp[BCH];
-  bool wv[BCH];
 #pragma unroll
-  for (int i = 0; i < BCH; ++i) {
-    const int gn = n0 + lrow + i * RPP;
-    wv[i] = gn < N;
-    wp[i] = W + static_cast<int64_t>(wv[i] ? gn : N - 1) * K + lkc;
-  }
-  uint4 ra[ACH], rb[BCH];
+  for (int i = 0; i < BCH; ++i)
+    wp[i] = W + static_cast<int64_t>(min(n0 + lrow + i * RPP, N - 1)) * K + lkc;
+  u32x4 ra[ACH], rb[BCH];
 
 #define ZSA_GLOAD(k0)                                                              \
   _Pragma("unroll") for (int i = 0; i < ACH; ++i) {                                \
-    ra[i] = keep16(*reinterpret_cast<const uint4*>(xp[i] + (k0)), xv[i]);          \
+    ra[i] = *reinterpret_cast<const u32x4*>(xp[i] + (k0));                         \
   }                                                                                \
   _Pragma("unroll") for (int i = 0; i < BCH; ++i) {                                \
-    rb[i] = keep16(*reinterpret_cast<const uint4*>(wp[i] + (k0)), wv[i]);          \
+    rb[i] = *reinterpret_cast<const u32x4*>(wp[i] + (k0));                         \
   }
 #define ZSA_SSTORE(buf)                                                            \
   _Pragma("unroll") for (int i = 0; i < ACH; ++i)                                  \
-    *reinterpret_cast<uint4*>(As + ((buf) * BM + lrow + i * RPP) * kLDK + lkc) = ra[i]; \
+    *reinterpret_cast<u32x4*>(As + ((buf) * BM + lrow + i * RPP) * kLDK + lkc) = ra[i]; \
   _Pragma("unroll") for (int i = 0; i < BCH; ++i)                                  \
-    *reinterpret_cast<uint4*>(Bs + ((buf) * BN + lrow + i * RPP) * kLDK + lkc) = rb[i];
+    *reinterpret_cast<u32x4*>(Bs + ((buf) * BN + lrow + i * RPP) * kLDK + lkc) = rb[i];
 
   f32x16_t acc[TM][TN];
 #pragma unroll
@@ -244,11 +240,11 @@ __global__ __launch_bounds__(WM * WN * 64) void gemm_bf16_mfma_kernel(
 #pragma unroll
       for (int i = 0; i < TM; ++i)
         a[i] = __builtin_bit_cast(bf16x8_t,
-                                  *reinterpret_cast<const uint4*>(Ab + i * 32 * kLDK + kk * 16));
+                                  *reinterpret_cast<const u32x4*>(Ab + i * 32 * kLDK + kk * 16));
 #pragma unroll
       for (int j = 0; j < TN; ++j)
         b[j] = __builtin_bit_cast(bf16x8_t,
-                                  *reinterpret_cast<const uint4*>(Bb + j * 32 * kLDK + kk * 16));
+                                  *reinterpret_cast<const u32x4*>(Bb + j * 32 * kLDK + kk * 16));
 #pragma unroll
       for (int i = 0; i < TM; ++i)
 #pragma unroll
@@ -383,6 +379,10 @@ hipError_t launch_gemm(hipStream_t s, int dtype, const void* x, int M, int K, co
     // projection shape here; it stays selectable for tuning
     const bool big = gemm_variant == 2;
     if (big) return launch_mfma<256, 128, 2, 2>(s, x, M, K, w, N, ep);
+    if (gemm_tile_override() == 2564) return launch_mfma<256, 256, 2, 2>(s, x, M, K, w, N, ep);
+    const long tiles256 = static_cast<long>((M + 255) / 256) * ((N + 255) / 256);
+    if (gemm_tile_override() == 2568 || (gemm_tile_override() == 0 && tiles256 >= 512))
+      return launch_mfma<256, 256, 2, 4>(s, x, M, K, w, N, ep);
     return launch_mfma<128, 128, 2, 2>(s, x, M, K, w, N, ep);
   }
   const dim3 grid((M + vBM - 1) / vBM, (N + vBN - 1) / vBN);

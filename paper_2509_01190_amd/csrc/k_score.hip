@@ -56,9 +56,9 @@ __global__ __launch_bounds__(256) void score_mfma_kernel(
     for (int c = tid; c < 64 * HD / 8; c += 256) {
       const int r = c / (HD / 8), ch = (c % (HD / 8)) * 8;
       const int jr = j0 + r;
-      *reinterpret_cast<uint4*>(Ks + r * KLD + ch) = keep16(
-          *reinterpret_cast<const uint4*>(K + static_cast<int64_t>(lo + min(jr, n - 1)) * rs + h * HD + ch),
-          jr < n);
+      // keys past the sequence repeat the last row; their columns are not written
+      *reinterpret_cast<uint4*>(Ks + r * KLD + ch) =
+          *reinterpret_cast<const uint4*>(K + static_cast<int64_t>(lo + min(jr, n - 1)) * rs + h * HD + ch);
     }
     __syncthreads();
     bf16x8_t kf[2][HD / 16];
@@ -80,10 +80,9 @@ __global__ __launch_bounds__(256) void score_mfma_kernel(
         const int qr = i0 + l32;
 #pragma unroll
         for (int kk = 0; kk < HD / 16; ++kk)
-          qa[kk] = __builtin_bit_cast(
-              bf16x8_t, keep16(*reinterpret_cast<const uint4*>(
-                                   Q + static_cast<int64_t>(lo + min(qr, n - 1)) * rs + h * HD + kk * 16 + half * 8),
-                               qr < n));
+          qa[kk] = __builtin_bit_cast(  // rows past the sequence are clamped and masked below
+              bf16x8_t, *reinterpret_cast<const uint4*>(
+                            Q + static_cast<int64_t>(lo + min(qr, n - 1)) * rs + h * HD + kk * 16 + half * 8));
 #pragma unroll
         for (int ks = 0; ks < 2; ++ks) {
           f32x16_t acc;

@@ -66,6 +66,10 @@ __device__ __forceinline__ uint4 pack16(const float* in, bf16_t) {
   return make_uint4(w[0], w[1], w[2], w[3]);
 }
 
+// native 16-byte vector (first-class in LLVM, so arrays of it stay in
+// registers; HIP's uint4 is a struct whose copies can end up on the stack)
+typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
+
 // keep a 16-byte value or zero it, without a select between two uint4 objects
 // (which the compiler lowers through a stack slot)
 __device__ __forceinline__ uint4 keep16(const uint4& v, bool keep) {
