@@ -63,8 +63,20 @@ __device__ __forceinline__ void rope_sincos(int p, double inv_freq, float* s, fl
   sincosf(static_cast<float>(r), s, c);
 }
 
+// erf by Abramowitz & Stegun, Handbook of Mathematical Functions, 7.1.26:
+// erf(x) = 1 - (a1 t + a2 t^2 + a3 t^3 + a4 t^4 + a5 t^5) exp(-x^2),
+// t = 1 / (1 + p x), x >= 0, |error| <= 1.5e-7; odd extension for x < 0.
+__device__ __forceinline__ float erf_as(float x) {
+  const float ax = fabsf(x);
+  const float t = __builtin_amdgcn_rcpf(1.0f + 0.3275911f * ax);
+  const float poly =
+      t * (0.254829592f + t * (-0.284496736f + t * (1.421413741f + t * (-1.453152027f + t * 1.061405429f))));
+  const float e = 1.0f - poly * __expf(-ax * ax);
+  return copysignf(e, x);
+}
+// exact (erf-based) GELU: z * Phi(z) = 0.5 z (1 + erf(z / sqrt 2))
 __device__ __forceinline__ float gelu_erf(float z) {
-  return 0.5f * z * (1.0f + erff(z * 0.70710678118654752f));
+  return 0.5f * z * (1.0f + erf_as(z * 0.70710678118654752f));
 }
 __device__ __forceinline__ float silu(float z) { return z / (1.0f + expf(-z)); }
 
@@ -284,6 +296,181 @@ __global__ __launch_bounds__(WM * WN * 64) void gemm_bf16_mfma_kernel(
 }
 
 // ---------------------------------------------------------------------------
+// bf16 MFMA GEMM with direct-to-LDS operand loads
+// ---------------------------------------------------------------------------
+// global_load_lds_dwordx4 writes each lane's 16 bytes to LDS at
+// (wave-uniform base) + 16 * lane, so one instruction fills 1 KiB: 8 rows of
+// 64 bf16. Tiles are stored unpadded, 128 bytes per row, with the 16-byte
+// chunk c of row r at position c ^ ((r >> 1) & 7). The DMA writes are
+// contiguous, and the 16 lanes of an MFMA fragment read phase (16
+// consecutive rows, one logical chunk) land on 16 distinct 4-bank groups.
+// Operands never pass through VGPRs: at the top of a K step each wave waits
+// for its own loads, one barrier publishes the stage, the next stage's
+// loads are issued into the other buffer and the MFMAs of this stage run
+// while they are in flight.
+template <int BM, int BN>
+constexpr int dma_lds_bytes() {
+  return 2 * (BM + BN) * 128 > 128 * (BN + 4) * 4 ? 2 * (BM + BN) * 128 : 128 * (BN + 4) * 4;
+}
+
+__device__ __forceinline__ int swz(int r, int c) { return c ^ ((r >> 1) & 7); }
+
+// waves per SIMD the tile's LDS footprint allows (160 KiB per CU)
+template <int BM, int BN, int WM, int WN>
+constexpr int dma_waves_per_simd() {
+  return (163840 / (2 * (BM + BN) * 128 > 128 * (BN + 4) * 4 ? 2 * (BM + BN) * 128
+                                                               : 128 * (BN + 4) * 4)) *
+         WM * WN / 4;
+}
+
+template <int BM, int BN, int WM, int WN>
+__global__ __launch_bounds__(WM * WN * 64)
+__attribute__((amdgpu_waves_per_eu(dma_waves_per_simd<BM, BN, WM, WN>(),
+                                   dma_waves_per_simd<BM, BN, WM, WN>()))) void
+gemm_bf16_dma_kernel(
+    const bf16_t* __restrict__ X, const bf16_t* __restrict__ W, int M, int N, int K,
+    EpiParams ep) {
+  static_assert(BM % 128 == 0 && (BN == 128 || BN == 256), "tile shape");
+  constexpr int NW = WM * WN;
+  constexpr int NT = NW * 64;
+  constexpr int kTileLd = BN + 4;
+  constexpr int WTM = BM / WM, WTN = BN / WN;
+  constexpr int TM = WTM / 32, TN = WTN / 32;
+  constexpr int AI = BM / 8 / NW, BI = BN / 8 / NW;  // 1 KiB DMA blocks per wave
+  static_assert(AI * NW * 8 == BM && BI * NW * 8 == BN, "blocks per wave");
+  extern __shared__ __align__(16) unsigned char smem[];
+  // stage s: A at smem + s * (BM + BN) * 128, B right after it
+  const int tid = threadIdx.x;
+  const int lane = tid & 63;
+  const int wave = tid >> 6;
+  const int wm = wave / WN, wn = wave % WN;
+  const int m0 = blockIdx.x * BM;
+  const int n0 = blockIdx.y * BN;
+
+  // per-lane global sources of this wave's DMA blocks (row clamped; the
+  // logical chunk is the position un-swizzled for the destination row)
+  const int lr = lane >> 3, lp = lane & 7;
+  const bf16_t* asrc[AI];
+#pragma unroll
+  for (int i = 0; i < AI; ++i) {
+    const int r = (i * NW + wave) * 8 + lr;
+    asrc[i] = X + static_cast<int64_t>(min(m0 + r, M - 1)) * K + swz(r, lp) * 8;
+  }
+  const bf16_t* bsrc[BI];
+#pragma unroll
+  for (int i = 0; i < BI; ++i) {
+    const int r = (i * NW + wave) * 8 + lr;
+    bsrc[i] = W + static_cast<int64_t>(min(n0 + r, N - 1)) * K + swz(r, lp) * 8;
+  }
+  typedef __attribute__((address_space(3))) void lds_void;
+  auto stage_base = [](int s) { return s * (BM + BN) * 128; };
+
+// the LDS-DMA builtin exists only in the device pass; the host pass only
+// needs the kernel's launch stub
+#if defined(__HIP_DEVICE_COMPILE__)
+#define ZSA_DMA1(src, dst) __builtin_amdgcn_global_load_lds((src), (lds_void*)(dst), 16, 0, 0)
+#else
+#define ZSA_DMA1(src, dst) ((void)(src), (void)(dst))
+#endif
+#define ZSA_DMA(s, k0)                                                                   \
+  _Pragma("unroll") for (int i = 0; i < AI; ++i)                                         \
+    ZSA_DMA1(asrc[i] + (k0), smem + stage_base(s) + (i * NW + wave) * 1024);             \
+  _Pragma("unroll") for (int i = 0; i < BI; ++i)                                         \
+    ZSA_DMA1(bsrc[i] + (k0), smem + stage_base(s) + BM * 128 + (i * NW + wave) * 1024);
+
+  f32x16_t acc[TM][TN];
+#pragma unroll
+  for (int i = 0; i < TM; ++i)
+#pragma unroll
+    for (int j = 0; j < TN; ++j)
+#pragma unroll
+      for (int r = 0; r < 16; ++r) acc[i][j][r] = 0.f;
+
+  // fragment rows of this lane and their swizzle keys
+  const int l32 = lane & 31, half = lane >> 5;
+  int arow[TM], brow[TN];
+#pragma unroll
+  for (int i = 0; i < TM; ++i) arow[i] = wm * WTM + i * 32 + l32;
+#pragma unroll
+  for (int j = 0; j < TN; ++j) brow[j] = wn * WTN + j * 32 + l32;
+
+  const int KT = K / kBK;
+  ZSA_DMA(0, 0)
+  for (int kt = 0; kt < KT; ++kt) {
+    const int s = kt & 1;
+    __builtin_amdgcn_s_waitcnt(0);  // this wave's DMA into stage s has landed
+    __syncthreads();                // ... and every other wave's; stage s^1 is free
+    if (kt + 1 < KT) {
+      ZSA_DMA(s ^ 1, (kt + 1) * kBK)
+    }
+    const unsigned char* As = smem + stage_base(s);
+    const unsigned char* Bs = As + BM * 128;
+    // fragments of step kk + 1 are read while the MFMAs of step kk run
+    bf16x8_t a[2][TM], b[2][TN];
+#pragma unroll
+    for (int i = 0; i < TM; ++i)
+      a[0][i] = __builtin_bit_cast(
+          bf16x8_t, *reinterpret_cast<const u32x4*>(As + arow[i] * 128 + swz(arow[i], half) * 16));
+#pragma unroll
+    for (int j = 0; j < TN; ++j)
+      b[0][j] = __builtin_bit_cast(
+          bf16x8_t, *reinterpret_cast<const u32x4*>(Bs + brow[j] * 128 + swz(brow[j], half) * 16));
+#pragma unroll
+    for (int kk = 0; kk < kBK / 16; ++kk) {
+      const int cur = kk & 1, nxt = cur ^ 1;
+      if (kk + 1 < kBK / 16) {
+        const int c = (kk + 1) * 2 + half;
+#pragma unroll
+        for (int i = 0; i < TM; ++i)
+          a[nxt][i] = __builtin_bit_cast(
+              bf16x8_t, *reinterpret_cast<const u32x4*>(As + arow[i] * 128 + swz(arow[i], c) * 16));
+#pragma unroll
+        for (int j = 0; j < TN; ++j)
+          b[nxt][j] = __builtin_bit_cast(
+              bf16x8_t, *reinterpret_cast<const u32x4*>(Bs + brow[j] * 128 + swz(brow[j], c) * 16));
+      }
+      __builtin_amdgcn_sched_barrier(0);  // keep those reads ahead of these MFMAs
+      // operands swapped: the accumulator holds C^T, so lane l owns output row
+      // l%32 of the m-block and 4 consecutive columns per register group
+#pragma unroll
+      for (int i = 0; i < TM; ++i)
+#pragma unroll
+        for (int j = 0; j < TN; ++j)
+          acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(b[cur][j], a[cur][i], acc[i][j], 0, 0, 0);
+      __builtin_amdgcn_sched_barrier(0);
+    }
+  }
+#undef ZSA_DMA
+#undef ZSA_DMA1
+  // acc[i][j][4g + e] = C[m][n + e] with m = wm*WTM + 32 i + l%32 and
+  // n = wn*WTN + 32 j + 8 g + 4 (l/32) inside the tile: every register group
+  // is 4 consecutive columns of one row, staged with one 16-byte LDS write
+  // (rows 132 floats apart, so 16 lanes cover the 64 banks once).
+  __syncthreads();  // all waves are done reading the operand stages
+  float* tile = reinterpret_cast<float*>(smem);
+#pragma unroll
+  for (int pass = 0; pass < BM / 128; ++pass) {
+    if (pass > 0) __syncthreads();
+    if ((wm * WTM) / 128 == pass) {
+#pragma unroll
+      for (int i = 0; i < TM; ++i)
+#pragma unroll
+        for (int j = 0; j < TN; ++j)
+#pragma unroll
+          for (int g = 0; g < 4; ++g) {
+            const int row = wm * WTM - pass * 128 + i * 32 + l32;
+            const int col = wn * WTN + j * 32 + g * 8 + half * 4;
+            const float4 v = make_float4(acc[i][j][4 * g], acc[i][j][4 * g + 1],
+                                         acc[i][j][4 * g + 2], acc[i][j][4 * g + 3]);
+            *reinterpret_cast<float4*>(tile + row * kTileLd + col) = v;
+          }
+    }
+    __syncthreads();
+    epilogue_tile<bf16_t, 128, BN, NT>(tile, kTileLd, m0 + pass * 128, n0, M, N, ep);
+  }
+}
+
+// ---------------------------------------------------------------------------
 // vector-ALU GEMM (fp32 storage, and any shape)
 // ---------------------------------------------------------------------------
 constexpr int vBM = 64, vBN = 128, vBK = 16;
@@ -359,10 +546,28 @@ hipError_t launch_mfma(hipStream_t s, const void* x, int M, int K, const void* w
                 static_cast<const bf16_t*>(x), static_cast<const bf16_t*>(w), M, N, K, ep);
 }
 
-}  // namespace
+template <int BM, int BN, int WM, int WN>
+hipError_t launch_dma(hipStream_t s, const void* x, int M, int K, const void* w, int N,
+                      const EpiParams& ep) {
+  constexpr int lds = dma_lds_bytes<BM, BN>();
+  static bool lds_raised = false;
+  if (!lds_raised) {
+    const hipError_t e = hipFuncSetAttribute(
+        reinterpret_cast<const void*>(gemm_bf16_dma_kernel<BM, BN, WM, WN>),
+        hipFuncAttributeMaxDynamicSharedMemorySize, lds);
+    if (e != hipSuccess) return e;
+    lds_raised = true;
+  }
+  const dim3 grid((M + BM - 1) / BM, (N + BN - 1) / BN);
+  return launch(K_GEMM, gemm_bf16_dma_kernel<BM, BN, WM, WN>, grid, dim3(WM * WN * 64), lds, s,
+                static_cast<const bf16_t*>(x), static_cast<const bf16_t*>(w), M, N, K, ep);
+}
 
-// Tile choice: by shape, unless ZSA_GEMM_TILE=128 or =256 pins one (tuning aid).
-static int gemm_tile_override() {
+// ZSA_GEMM_TILE pins one kernel variant (a tuning aid; 0 or unset = by shape):
+// 128 / 256 / 2564 / 2568: register-staged 128x128, 256x128, 256x256 on 4 and
+// on 8 waves; 1281 / 2563 / 2562 / 2561: direct-to-LDS 128x128, 256x128,
+// 256x256 on 4 and on 8 waves.
+int gemm_tile_override() {
   static const int v = [] {
     const char* e = getenv("ZSA_GEMM_TILE");
     return e == nullptr ? 0 : atoi(e);
@@ -370,20 +575,29 @@ static int gemm_tile_override() {
   return v;
 }
 
+}  // namespace
+
 hipError_t launch_gemm(hipStream_t s, int dtype, const void* x, int M, int K, const void* w,
                        int N, const EpiParams& ep) {
   if (M == 0 || N == 0) return hipSuccess;
   if (dtype == 1 && K % kBK == 0) {
-    const int gemm_variant = gemm_tile_override() == 256 ? 2 : gemm_tile_override() == 128 ? 1 : 0;
-    // 256x128 (one wave per SIMD) measured slower than 128x128 on every
-    // projection shape here; it stays selectable for tuning
-    const bool big = gemm_variant == 2;
-    if (big) return launch_mfma<256, 128, 2, 2>(s, x, M, K, w, N, ep);
-    if (gemm_tile_override() == 2564) return launch_mfma<256, 256, 2, 2>(s, x, M, K, w, N, ep);
+    switch (gemm_tile_override()) {
+      case 128: return launch_mfma<128, 128, 2, 2>(s, x, M, K, w, N, ep);
+      case 256: return launch_mfma<256, 128, 2, 2>(s, x, M, K, w, N, ep);
+      case 2564: return launch_mfma<256, 256, 2, 2>(s, x, M, K, w, N, ep);
+      case 2568: return launch_mfma<256, 256, 2, 4>(s, x, M, K, w, N, ep);
+      case 1281: return launch_dma<128, 128, 2, 2>(s, x, M, K, w, N, ep);
+      case 2563: return launch_dma<256, 128, 2, 2>(s, x, M, K, w, N, ep);
+      case 2562: return launch_dma<256, 256, 2, 2>(s, x, M, K, w, N, ep);
+      case 2561: return launch_dma<256, 256, 2, 4>(s, x, M, K, w, N, ep);
+      default: break;
+    }
+    // Measured on the projection shapes: direct-to-LDS 256x256 tiles over 8
+    // waves (128x64 per wave) win once the grid holds at least four rounds of
+    // such tiles; below that, direct-to-LDS 128x128 tiles over 4 waves.
     const long tiles256 = static_cast<long>((M + 255) / 256) * ((N + 255) / 256);
-    if (gemm_tile_override() == 2568 || (gemm_tile_override() == 0 && tiles256 >= 512))
-      return launch_mfma<256, 256, 2, 4>(s, x, M, K, w, N, ep);
-    return launch_mfma<128, 128, 2, 2>(s, x, M, K, w, N, ep);
+    if (tiles256 >= 1024) return launch_dma<256, 256, 2, 4>(s, x, M, K, w, N, ep);
+    return launch_dma<128, 128, 2, 2>(s, x, M, K, w, N, ep);
   }
   const dim3 grid((M + vBM - 1) / vBM, (N + vBN - 1) / vBN);
   if (dtype == 1)
