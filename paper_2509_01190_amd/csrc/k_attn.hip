@@ -149,8 +149,7 @@ __global__ __launch_bounds__(256) void attn_mfma_kernel(
         uint32_t pw[4];
 #pragma unroll
         for (int t = 0; t < 4; ++t)
-          pw[t] = static_cast<uint32_t>(f32_to_bf16(s[ks][rb + 2 * t])) |
-                  (static_cast<uint32_t>(f32_to_bf16(s[ks][rb + 2 * t + 1])) << 16);
+          pw[t] = pack_bf16x2(s[ks][rb + 2 * t], s[ks][rb + 2 * t + 1]);
         const bf16x8_t pb = __builtin_bit_cast(bf16x8_t, make_uint4(pw[0], pw[1], pw[2], pw[3]));
         const int base = ks * 32 + (g & 1) * 16 + 4 * half;
 #pragma unroll

@@ -342,7 +342,9 @@ gemm_bf16_dma_kernel(
   // stage s: A at smem + s * (BM + BN) * 128, B right after it
   const int tid = threadIdx.x;
   const int lane = tid & 63;
-  const int wave = tid >> 6;
+  // wave index as a scalar: the DMA destinations derived from it are then
+  // wave-uniform scalars (M0) instead of per-lane values read back each time
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int wm = wave / WN, wn = wave % WN;
   const int m0 = blockIdx.x * BM;
   const int n0 = blockIdx.y * BN;
@@ -386,60 +388,66 @@ gemm_bf16_dma_kernel(
 #pragma unroll
       for (int r = 0; r < 16; ++r) acc[i][j][r] = 0.f;
 
-  // fragment rows of this lane and their swizzle keys
+  // byte offsets (within a stage) of this lane's fragments for each k-substep
   const int l32 = lane & 31, half = lane >> 5;
-  int arow[TM], brow[TN];
+  int aoff[TM][kBK / 16], boff[TN][kBK / 16];
 #pragma unroll
-  for (int i = 0; i < TM; ++i) arow[i] = wm * WTM + i * 32 + l32;
+  for (int i = 0; i < TM; ++i) {
+    const int r = wm * WTM + i * 32 + l32;
 #pragma unroll
-  for (int j = 0; j < TN; ++j) brow[j] = wn * WTN + j * 32 + l32;
-
-  const int KT = K / kBK;
-  ZSA_DMA(0, 0)
-  for (int kt = 0; kt < KT; ++kt) {
-    const int s = kt & 1;
-    __builtin_amdgcn_s_waitcnt(0);  // this wave's DMA into stage s has landed
-    __syncthreads();                // ... and every other wave's; stage s^1 is free
-    if (kt + 1 < KT) {
-      ZSA_DMA(s ^ 1, (kt + 1) * kBK)
-    }
-    const unsigned char* As = smem + stage_base(s);
-    const unsigned char* Bs = As + BM * 128;
-    // fragments of step kk + 1 are read while the MFMAs of step kk run
-    bf16x8_t a[2][TM], b[2][TN];
-#pragma unroll
-    for (int i = 0; i < TM; ++i)
-      a[0][i] = __builtin_bit_cast(
-          bf16x8_t, *reinterpret_cast<const u32x4*>(As + arow[i] * 128 + swz(arow[i], half) * 16));
-#pragma unroll
-    for (int j = 0; j < TN; ++j)
-      b[0][j] = __builtin_bit_cast(
-          bf16x8_t, *reinterpret_cast<const u32x4*>(Bs + brow[j] * 128 + swz(brow[j], half) * 16));
-#pragma unroll
-    for (int kk = 0; kk < kBK / 16; ++kk) {
-      const int cur = kk & 1, nxt = cur ^ 1;
-      if (kk + 1 < kBK / 16) {
-        const int c = (kk + 1) * 2 + half;
-#pragma unroll
-        for (int i = 0; i < TM; ++i)
-          a[nxt][i] = __builtin_bit_cast(
-              bf16x8_t, *reinterpret_cast<const u32x4*>(As + arow[i] * 128 + swz(arow[i], c) * 16));
-#pragma unroll
-        for (int j = 0; j < TN; ++j)
-          b[nxt][j] = __builtin_bit_cast(
-              bf16x8_t, *reinterpret_cast<const u32x4*>(Bs + brow[j] * 128 + swz(brow[j], c) * 16));
-      }
-      __builtin_amdgcn_sched_barrier(0);  // keep those reads ahead of these MFMAs
-      // operands swapped: the accumulator holds C^T, so lane l owns output row
-      // l%32 of the m-block and 4 consecutive columns per register group
-#pragma unroll
-      for (int i = 0; i < TM; ++i)
-#pragma unroll
-        for (int j = 0; j < TN; ++j)
-          acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(b[cur][j], a[cur][i], acc[i][j], 0, 0, 0);
-      __builtin_amdgcn_sched_barrier(0);
-    }
+    for (int kk = 0; kk < kBK / 16; ++kk) aoff[i][kk] = r * 128 + swz(r, kk * 2 + half) * 16;
   }
+#pragma unroll
+  for (int j = 0; j < TN; ++j) {
+    const int r = wn * WTN + j * 32 + l32;
+#pragma unroll
+    for (int kk = 0; kk < kBK / 16; ++kk) boff[j][kk] = BM * 128 + r * 128 + swz(r, kk * 2 + half) * 16;
+  }
+
+  // one K step on stage S (a compile-time constant, so every LDS address is
+  // a register plus an immediate): wait for this wave's DMA, publish the
+  // stage with one barrier, start the next step's DMA into the other stage,
+  // then run the MFMAs, reading the next k-substep's fragments ahead.
+#define ZSA_STEP(S, KT)                                                                  \
+  {                                                                                      \
+    __builtin_amdgcn_s_waitcnt(0);                                                       \
+    __syncthreads();                                                                     \
+    if ((KT) + 1 < KTOT) {                                                               \
+      ZSA_DMA((S) ^ 1, ((KT) + 1) * kBK)                                                 \
+    }                                                                                    \
+    const unsigned char* st = smem + stage_base(S);                                      \
+    bf16x8_t a[2][TM], b[2][TN];                                                         \
+    _Pragma("unroll") for (int i = 0; i < TM; ++i)                                       \
+      a[0][i] = __builtin_bit_cast(bf16x8_t, *reinterpret_cast<const u32x4*>(st + aoff[i][0])); \
+    _Pragma("unroll") for (int j = 0; j < TN; ++j)                                       \
+      b[0][j] = __builtin_bit_cast(bf16x8_t, *reinterpret_cast<const u32x4*>(st + boff[j][0])); \
+    _Pragma("unroll") for (int kk = 0; kk < kBK / 16; ++kk) {                            \
+      const int cur = kk & 1, nxt = cur ^ 1;                                             \
+      if (kk + 1 < kBK / 16) {                                                           \
+        _Pragma("unroll") for (int i = 0; i < TM; ++i)                                   \
+          a[nxt][i] = __builtin_bit_cast(bf16x8_t, *reinterpret_cast<const u32x4*>(st + aoff[i][kk + 1])); \
+        _Pragma("unroll") for (int j = 0; j < TN; ++j)                                   \
+          b[nxt][j] = __builtin_bit_cast(bf16x8_t, *reinterpret_cast<const u32x4*>(st + boff[j][kk + 1])); \
+      }                                                                                  \
+      __builtin_amdgcn_sched_barrier(0);                                                 \
+      _Pragma("unroll") for (int i = 0; i < TM; ++i)                                     \
+        _Pragma("unroll") for (int j = 0; j < TN; ++j)                                   \
+          acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(b[cur][j], a[cur][i], acc[i][j], 0, 0, 0); \
+      __builtin_amdgcn_sched_barrier(0);                                                 \
+    }                                                                                    \
+  }
+
+  // operands swapped in the MFMA: the accumulator holds C^T, so lane l owns
+  // output row l%32 of an m-block and 4 consecutive columns per register group
+  const int KTOT = K / kBK;
+  ZSA_DMA(0, 0)
+  int kt = 0;
+  for (; kt + 1 < KTOT; kt += 2) {
+    ZSA_STEP(0, kt)
+    ZSA_STEP(1, kt + 1)
+  }
+  if (kt < KTOT) ZSA_STEP(0, kt)
+#undef ZSA_STEP
 #undef ZSA_DMA
 #undef ZSA_DMA1
   // acc[i][j][4g + e] = C[m][n + e] with m = wm*WTM + 32 i + l%32 and
