@@ -48,7 +48,78 @@ def parse():
     ap.add_argument("--no-graph", action="store_true", help="time eager launches instead")
     ap.add_argument("--cpu-seconds", type=float, default=15.0,
                     help="target wall time of the CPU-oracle sample (0 disables it)")
+    ap.add_argument("--copy-calibration", type=int, default=0, metavar="BYTES",
+                    help="only run one plain device copy of BYTES bytes (profiled under "
+                         "rocprofv3 --pmc to scale FETCH_SIZE / WRITE_SIZE) and exit")
+    ap.add_argument("--summarize-pmc", nargs=4, default=None,
+                    metavar=("FETCH_CSV", "WRITE_CSV", "COPY_FETCH_CSV", "COPY_WRITE_CSV"),
+                    help="turn rocprofv3 --pmc counter CSVs of this bench and of the copy "
+                         "calibration into " + "profiles/gemm_traffic.json and exit")
+    ap.add_argument("--copy-bytes", type=int, default=256 << 20)
     return ap.parse_args()
+
+
+GEMM_SRC = os.path.join(ROOT, "paper_2509_01190_amd", "csrc", "k_gemm.hip")
+TRAFFIC_FILE = os.path.join(ROOT, "profiles", "gemm_traffic.json")
+GEMM_KERNEL_TAG = "gemm_bf16_"
+
+
+def gemm_source_hash():
+    import hashlib
+    with open(GEMM_SRC, "rb") as f:
+        return hashlib.sha256(f.read()).hexdigest()[:16]
+
+
+def pmc_mean(csv_path, counter, name_filter):
+    """Mean per-dispatch value (KiB for FETCH_SIZE / WRITE_SIZE) of a counter
+    over the dispatches whose kernel name contains name_filter."""
+    import csv
+    import collections
+    per = collections.defaultdict(float)
+    with open(csv_path) as f:
+        for r in csv.DictReader(f):
+            if r["Counter_Name"] == counter and name_filter in r["Kernel_Name"]:
+                per[r["Dispatch_Id"]] += float(r["Counter_Value"])
+    if not per:
+        raise SystemExit(f"no {counter} rows for kernels matching {name_filter!r} in {csv_path}")
+    return sum(per.values()) / len(per), len(per)
+
+
+def summarize_pmc(args):
+    """FETCH_SIZE / WRITE_SIZE (KiB per dispatch) of the GEMM launches of a bench
+    run, scaled by the ratio of true to counted bytes of a plain copy kernel."""
+    f_csv, w_csv, cf_csv, cw_csv = args.summarize_pmc
+    fetch_kib, n_f = pmc_mean(f_csv, "FETCH_SIZE", GEMM_KERNEL_TAG)
+    write_kib, n_w = pmc_mean(w_csv, "WRITE_SIZE", GEMM_KERNEL_TAG)
+    copy_f, _ = pmc_mean(cf_csv, "FETCH_SIZE", "copyBuffer")
+    copy_w, _ = pmc_mean(cw_csv, "WRITE_SIZE", "copyBuffer")
+    f_scale = args.copy_bytes / (copy_f * 1024.0)
+    w_scale = args.copy_bytes / (copy_w * 1024.0)
+    out = {
+        "kernel": "gemm_bf16_* (all projection GEMM launches of one bench run)",
+        "gemm_source_sha256_16": gemm_source_hash(),
+        "dispatches": [n_f, n_w],
+        "fetch_kib_per_dispatch": fetch_kib, "write_kib_per_dispatch": write_kib,
+        "copy_bytes": args.copy_bytes, "copy_fetch_kib": copy_f, "copy_write_kib": copy_w,
+        "fetch_scale": f_scale, "write_scale": w_scale,
+        "hbm_bytes_per_launch": fetch_kib * 1024.0 * f_scale + write_kib * 1024.0 * w_scale,
+    }
+    with open(TRAFFIC_FILE, "w") as f:
+        json.dump(out, f, indent=1)
+    print(json.dumps(out))
+
+
+def measured_traffic():
+    """HBM bytes per GEMM launch from the committed counter summary, or None
+    when the GEMM source changed since the counters were taken."""
+    try:
+        with open(TRAFFIC_FILE) as f:
+            t = json.load(f)
+    except (OSError, ValueError):
+        return None
+    if t.get("gemm_source_sha256_16") != gemm_source_hash():
+        return None
+    return t.get("hbm_bytes_per_launch")
 
 
 def gemm_flops(p, rows_in, rows_after):
@@ -116,6 +187,9 @@ def cpu_baseline(p, ws_np, x_np, lens, rate, budget_s):
 
 def main():
     args = parse()
+    if args.summarize_pmc:
+        summarize_pmc(args)
+        return
     if args.gpus != 1:
         print(f"bench.py runs on one GPU only (asked for --gpus {args.gpus}); the pruned stack "
               f"is measured on a single MI355X and this build has no multi-GPU path.",
@@ -131,6 +205,14 @@ def main():
         print("bench.py needs a GPU", file=sys.stderr)
         sys.exit(1)
     dev = torch.device("cuda:0")
+    if args.copy_calibration:
+        src = torch.empty(args.copy_calibration, dtype=torch.uint8, device=dev).fill_(1)
+        dst = torch.empty_like(src)
+        torch.cuda.synchronize()
+        dst.copy_(src)
+        torch.cuda.synchronize()
+        print(json.dumps({"copy_bytes": args.copy_calibration}))
+        return
     p = W.PRESETS[args.workload]
     rates = [float(r) for r in args.keep_rates.split(",")] if args.keep_rates else list(p.keep_rates)
     if HEADLINE_RATE not in rates:
@@ -206,9 +288,12 @@ def main():
     g_n = sum(results[r]["classes"]["gemm"]["launches"] for r in rates)
     g_flops = sum(results[r]["gemm_flops"] for r in rates)
     achieved = g_flops / (g_ms * 1e-3) / 1e12 if g_ms > 0 else 0.0
-    roofline = {"kernel": "gemm_bf16_mfma_kernel (all projection GEMMs)", "bound": "mfma",
+    traffic = measured_traffic()
+    roofline = {"kernel": "gemm_bf16_* (all projection GEMM launches)", "bound": "mfma",
                 "achieved": round(achieved, 1), "peak": PEAK_BF16_TFLOPS, "unit": "TFLOP/s",
-                "frac": round(achieved / PEAK_BF16_TFLOPS, 4), "traffic": None,
+                "frac": round(achieved / PEAK_BF16_TFLOPS, 4),
+                "traffic": None if traffic is None else round(traffic),
+                "traffic_unit": "HBM bytes per launch (FETCH_SIZE + WRITE_SIZE, copy-scaled)",
                 "avg_launch_us": round(g_ms * 1e3 / max(g_n, 1), 2), "launches": g_n,
                 "dominant_class": dom}
     head = results[HEADLINE_RATE]
