@@ -296,6 +296,43 @@ __global__ __launch_bounds__(WM * WN * 64) void gemm_bf16_mfma_kernel(
 }
 
 // ---------------------------------------------------------------------------
+// XCD-aware tile order
+// ---------------------------------------------------------------------------
+// Workgroups are handed to the 8 XCDs round-robin by linear id, and every XCD
+// has its own L2. Workgroup L therefore runs on XCD k = L % 8 as that XCD's
+// j-th workgroup (j = L / 8). XCD k is given a contiguous, balanced stripe of
+// the M-tiles and walks it in groups of kXcdGroup M-tiles: for each N-tile,
+// the group's M-tiles. The A rows of a group and the W tiles in flight then
+// fit one L2, so A is fetched from memory about once and W once per group
+// and XCD, instead of once per N-tile. The grid is 8 x (largest stripe x
+// N-tiles) one-dimensional workgroups; the ones past their stripe exit.
+constexpr int kXcds = 8;
+constexpr int kXcdGroup = 8;
+
+template <int BM, int BN>
+__device__ __forceinline__ bool xcd_tile(int M, int N, int* mt, int* nt) {
+  const int nM = (M + BM - 1) / BM, nN = (N + BN - 1) / BN;
+  const int k = blockIdx.x % kXcds, j = blockIdx.x / kXcds;
+  const int base = nM / kXcds, extra = nM % kXcds;
+  const int rows = base + (k < extra ? 1 : 0);
+  const int m_lo = k * base + (k < extra ? k : extra);
+  if (j >= rows * nN) return false;
+  const int g = j / (kXcdGroup * nN);
+  const int gm0 = g * kXcdGroup;
+  const int gsz = min(kXcdGroup, rows - gm0);
+  const int r = j - g * kXcdGroup * nN;
+  *nt = r / gsz;
+  *mt = m_lo + gm0 + r % gsz;
+  return true;
+}
+
+inline dim3 xcd_grid(int M, int N, int BM, int BN) {
+  const int nM = (M + BM - 1) / BM, nN = (N + BN - 1) / BN;
+  const int rows = (nM + kXcds - 1) / kXcds;
+  return dim3(static_cast<unsigned>(kXcds * rows * nN));
+}
+
+// ---------------------------------------------------------------------------
 // bf16 MFMA GEMM with direct-to-LDS operand loads
 // ---------------------------------------------------------------------------
 // global_load_lds_dwordx4 writes each lane's 16 bytes to LDS at
@@ -346,8 +383,10 @@ gemm_bf16_dma_kernel(
   // wave-uniform scalars (M0) instead of per-lane values read back each time
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int wm = wave / WN, wn = wave % WN;
-  const int m0 = blockIdx.x * BM;
-  const int n0 = blockIdx.y * BN;
+  int mt, nt;
+  if (!xcd_tile<BM, BN>(M, N, &mt, &nt)) return;
+  const int m0 = mt * BM;
+  const int n0 = nt * BN;
 
   // per-lane global sources of this wave's DMA blocks (row clamped; the
   // logical chunk is the position un-swizzled for the destination row)
@@ -566,7 +605,7 @@ hipError_t launch_dma(hipStream_t s, const void* x, int M, int K, const void* w,
     if (e != hipSuccess) return e;
     lds_raised = true;
   }
-  const dim3 grid((M + BM - 1) / BM, (N + BN - 1) / BN);
+  const dim3 grid = xcd_grid(M, N, BM, BN);
   return launch(K_GEMM, gemm_bf16_dma_kernel<BM, BN, WM, WN>, grid, dim3(WM * WN * 64), lds, s,
                 static_cast<const bf16_t*>(x), static_cast<const bf16_t*>(w), M, N, K, ep);
 }
