@@ -44,10 +44,12 @@ __global__ __launch_bounds__(256) void attn_mfma_kernel(
   constexpr int VLD = BKEY + 8;  // V^T tile row stride (bf16)
   constexpr int OLD = HD + 8;    // output staging row stride
   constexpr int KBYTES = BKEY * KLD * 2, VBYTES = HD * VLD * 2;
-  constexpr int SBYTES = KBYTES + VBYTES > 4 * 32 * OLD * 2 ? KBYTES + VBYTES : 4 * 32 * OLD * 2;
+  constexpr int BUF = KBYTES + VBYTES;
+  constexpr int SBYTES = 2 * BUF > 4 * 32 * OLD * 2 ? 2 * BUF : 4 * 32 * OLD * 2;
+  constexpr int KCH = BKEY * HD / 8 / 256;        // 16-byte K chunks per thread
+  constexpr int VPR = (BKEY / 2) * (HD / 8) / 256;  // V row-pair chunks per thread
+  static_assert(KCH >= 1 && VPR >= 1, "tile split");
   __shared__ __align__(16) unsigned char smem[SBYTES];
-  bf16_t* Ks = reinterpret_cast<bf16_t*>(smem);
-  bf16_t* Vt = reinterpret_cast<bf16_t*>(smem + KBYTES);
 
   const int b = blockIdx.z, h = blockIdx.y;
   const int lo = cu[b];
@@ -64,11 +66,57 @@ __global__ __launch_bounds__(256) void attn_mfma_kernel(
   for (int kk = 0; kk < HD / 16; ++kk) {
     // rows past the sequence are clamped, not zeroed: their outputs are not stored
     const int qr = min(qrow, n - 1);
-    qf[kk] = __builtin_bit_cast(bf16x8_t, *reinterpret_cast<const uint4*>(
+    qf[kk] = __builtin_bit_cast(bf16x8_t, *reinterpret_cast<const u32x4*>(
                                               Q + static_cast<int64_t>(lo + qr) * rs + h * HD + kk * 16 + half * 8));
   }
 
-  float m_run = -INFINITY, l_run = 0.f;
+  // K/V tiles of the next key block are prefetched into registers while the
+  // current block is computed; LDS is double-buffered, one barrier per block.
+  // Keys past the sequence repeat the last row: they are masked to
+  // probability 0 and the repeated V rows are finite.
+  const bf16_t* kbase = K + static_cast<int64_t>(lo) * rs + h * HD;
+  const bf16_t* vbase = V + static_cast<int64_t>(lo) * rs + h * HD;
+  u32x4 kreg[KCH], vreg[VPR][2];
+  auto load_tile = [&](int j0) {
+#pragma unroll
+    for (int i = 0; i < KCH; ++i) {
+      const int c = tid + i * 256;
+      const int r = c / (HD / 8), ch = (c % (HD / 8)) * 8;
+      kreg[i] = *reinterpret_cast<const u32x4*>(kbase + static_cast<int64_t>(min(j0 + r, n - 1)) * rs + ch);
+    }
+#pragma unroll
+    for (int i = 0; i < VPR; ++i) {
+      const int c = tid + i * 256;
+      const int rp = c / (HD / 8), ch = (c % (HD / 8)) * 8;
+      const int jr = j0 + 2 * rp;
+      vreg[i][0] = *reinterpret_cast<const u32x4*>(vbase + static_cast<int64_t>(min(jr, n - 1)) * rs + ch);
+      vreg[i][1] = *reinterpret_cast<const u32x4*>(vbase + static_cast<int64_t>(min(jr + 1, n - 1)) * rs + ch);
+    }
+  };
+  auto store_tile = [&](int buf) {
+    bf16_t* Ks = reinterpret_cast<bf16_t*>(smem + buf * BUF);
+    bf16_t* Vt = reinterpret_cast<bf16_t*>(smem + buf * BUF + KBYTES);
+#pragma unroll
+    for (int i = 0; i < KCH; ++i) {
+      const int c = tid + i * 256;
+      const int r = c / (HD / 8), ch = (c % (HD / 8)) * 8;
+      *reinterpret_cast<u32x4*>(Ks + r * KLD + ch) = kreg[i];
+    }
+#pragma unroll
+    for (int i = 0; i < VPR; ++i) {
+      const int c = tid + i * 256;
+      const int rp = c / (HD / 8), ch = (c % (HD / 8)) * 8;
+#pragma unroll
+      for (int e = 0; e < 8; ++e) {
+        const uint32_t w0 = vreg[i][0][e >> 1], w1 = vreg[i][1][e >> 1];
+        const uint32_t x0 = (e & 1) ? (w0 >> 16) : (w0 & 0xffffu);
+        const uint32_t x1 = (e & 1) ? (w1 & 0xffff0000u) : (w1 << 16);
+        *reinterpret_cast<uint32_t*>(Vt + (ch + e) * VLD + 2 * rp) = x0 | x1;
+      }
+    }
+  };
+
+  float m_run = -INFINITY, l_run = 0.f;  // running max in raw score units
   f32x16_t o[HD / 32];
 #pragma unroll
   for (int ct = 0; ct < HD / 32; ++ct)
@@ -76,29 +124,21 @@ __global__ __launch_bounds__(256) void attn_mfma_kernel(
     for (int r = 0; r < 16; ++r) o[ct][r] = 0.f;
 
   const int kend = causal ? min(n, q0 + BQ) : n;
-  const int wave_qmax = q0 + wave * 32 + 31;
-  for (int j0 = 0; j0 < kend; j0 += BKEY) {
-    for (int c = tid; c < BKEY * HD / 8; c += 256) {
-      const int r = c / (HD / 8), ch = (c % (HD / 8)) * 8;
-      const int jr = j0 + r;
-      // keys past the sequence repeat the last row: they are masked to
-      // probability 0, and the repeated V rows are finite
-      *reinterpret_cast<uint4*>(Ks + r * KLD + ch) =
-          *reinterpret_cast<const uint4*>(K + static_cast<int64_t>(lo + min(jr, n - 1)) * rs + h * HD + ch);
+  const int wave_q0 = q0 + wave * 32;
+  load_tile(0);
+  store_tile(0);
+  if (BKEY < kend) load_tile(BKEY);
+  __syncthreads();
+  int t = 0;
+  for (int j0 = 0; j0 < kend; j0 += BKEY, ++t) {
+    const int buf = t & 1;
+    if (j0 + BKEY < kend) {
+      store_tile(buf ^ 1);  // the other buffer was last read before the previous barrier
+      if (j0 + 2 * BKEY < kend) load_tile(j0 + 2 * BKEY);
     }
-    for (int c = tid; c < (BKEY / 2) * (HD / 8); c += 256) {
-      const int rp = c / (HD / 8), ch = (c % (HD / 8)) * 8;
-      const int jr = j0 + 2 * rp;
-      const uint4 v0 = *reinterpret_cast<const uint4*>(
-          V + static_cast<int64_t>(lo + min(jr, n - 1)) * rs + h * HD + ch);
-      const uint4 v1 = *reinterpret_cast<const uint4*>(
-          V + static_cast<int64_t>(lo + min(jr + 1, n - 1)) * rs + h * HD + ch);
-#pragma unroll
-      for (int e = 0; e < 8; ++e)
-        *reinterpret_cast<uint32_t*>(Vt + (ch + e) * VLD + 2 * rp) = bf16_at(v0, e) | (bf16_at(v1, e) << 16);
-    }
-    __syncthreads();
-    if (!causal || j0 <= wave_qmax) {
+    const bf16_t* Ks = reinterpret_cast<const bf16_t*>(smem + buf * BUF);
+    const bf16_t* Vt = reinterpret_cast<const bf16_t*>(smem + buf * BUF + KBYTES);
+    if (!causal || j0 <= wave_q0 + 31) {
       f32x16_t s[2];
 #pragma unroll
       for (int ks = 0; ks < 2; ++ks) {
@@ -107,32 +147,37 @@ __global__ __launch_bounds__(256) void attn_mfma_kernel(
 #pragma unroll
         for (int kk = 0; kk < HD / 16; ++kk) {
           const bf16x8_t a = __builtin_bit_cast(
-              bf16x8_t, *reinterpret_cast<const uint4*>(Ks + (ks * 32 + l32) * KLD + kk * 16 + half * 8));
+              bf16x8_t, *reinterpret_cast<const u32x4*>(Ks + (ks * 32 + l32) * KLD + kk * 16 + half * 8));
           s[ks] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, qf[kk], s[ks], 0, 0, 0);
         }
       }
-      // s[ks][r]: query qrow, key j0 + 32 ks + 8 (r/4) + 4 half + r%4
+      // s[ks][r]: query qrow, key j0 + 32 ks + 8 (r/4) + 4 half + r%4 (raw q.k)
+      // masks only on the tiles that cross the sequence end or the diagonal
+      if (j0 + BKEY > n || (causal && j0 + BKEY - 1 > wave_q0)) {
+#pragma unroll
+        for (int ks = 0; ks < 2; ++ks)
+#pragma unroll
+          for (int r = 0; r < 16; ++r) {
+            const int j = j0 + ks * 32 + 8 * (r >> 2) + 4 * half + (r & 3);
+            if (j >= n || (causal && j > qrow)) s[ks][r] = -INFINITY;
+          }
+      }
       float mloc = -INFINITY;
 #pragma unroll
       for (int ks = 0; ks < 2; ++ks)
 #pragma unroll
-        for (int r = 0; r < 16; ++r) {
-          const int j = j0 + ks * 32 + 8 * (r >> 2) + 4 * half + (r & 3);
-          float x = s[ks][r] * scale_log2;
-          if (j >= n || (causal && j > qrow)) x = -INFINITY;
-          s[ks][r] = x;
-          mloc = fmaxf(mloc, x);
-        }
+        for (int r = 0; r < 16; ++r) mloc = fmaxf(mloc, s[ks][r]);
       mloc = fmaxf(mloc, __shfl_xor(mloc, 32, 64));
       const float m_new = fmaxf(m_run, mloc);
-      const float m_use = m_new == -INFINITY ? 0.f : m_new;
-      const float alpha = exp2f(m_run - m_use);
+      // scale > 0, so the max of the scaled scores is the scaled max
+      const float m_use = m_new == -INFINITY ? 0.f : m_new * scale_log2;
+      const float alpha = __builtin_amdgcn_exp2f(m_run * scale_log2 - m_use);
       float rsum = 0.f;
 #pragma unroll
       for (int ks = 0; ks < 2; ++ks)
 #pragma unroll
         for (int r = 0; r < 16; ++r) {
-          const float p = exp2f(s[ks][r] - m_use);
+          const float p = __builtin_amdgcn_exp2f(fmaf(s[ks][r], scale_log2, -m_use));
           s[ks][r] = p;
           rsum += p;
         }
@@ -146,19 +191,17 @@ __global__ __launch_bounds__(256) void attn_mfma_kernel(
 #pragma unroll
       for (int g = 0; g < 4; ++g) {
         const int ks = g >> 1, rb = (g & 1) * 8;
-        uint32_t pw[4];
-#pragma unroll
-        for (int t = 0; t < 4; ++t)
-          pw[t] = pack_bf16x2(s[ks][rb + 2 * t], s[ks][rb + 2 * t + 1]);
-        const bf16x8_t pb = __builtin_bit_cast(bf16x8_t, make_uint4(pw[0], pw[1], pw[2], pw[3]));
+        const u32x4 pw = {pack_bf16x2(s[ks][rb], s[ks][rb + 1]), pack_bf16x2(s[ks][rb + 2], s[ks][rb + 3]),
+                          pack_bf16x2(s[ks][rb + 4], s[ks][rb + 5]), pack_bf16x2(s[ks][rb + 6], s[ks][rb + 7])};
+        const bf16x8_t pb = __builtin_bit_cast(bf16x8_t, pw);
         const int base = ks * 32 + (g & 1) * 16 + 4 * half;
 #pragma unroll
         for (int ct = 0; ct < HD / 32; ++ct) {
           const bf16_t* vr = Vt + (ct * 32 + l32) * VLD + base;
           const uint2 lo4 = *reinterpret_cast<const uint2*>(vr);
           const uint2 hi4 = *reinterpret_cast<const uint2*>(vr + 8);
-          const bf16x8_t a = __builtin_bit_cast(bf16x8_t, make_uint4(lo4.x, lo4.y, hi4.x, hi4.y));
-          o[ct] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, pb, o[ct], 0, 0, 0);
+          const u32x4 av = {lo4.x, lo4.y, hi4.x, hi4.y};
+          o[ct] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(__builtin_bit_cast(bf16x8_t, av), pb, o[ct], 0, 0, 0);
         }
       }
     }
@@ -180,11 +223,11 @@ __global__ __launch_bounds__(256) void attn_mfma_kernel(
     const int r = c / (HD / 8), ch = (c % (HD / 8)) * 8;
     const int qr = q0 + wave * 32 + r;
     if (qr < n)
-      *reinterpret_cast<uint4*>(O + static_cast<int64_t>(lo + qr) * os + h * HD + ch) =
-          *reinterpret_cast<const uint4*>(Os + r * OLD + ch);
+      *reinterpret_cast<u32x4*>(O + static_cast<int64_t>(lo + qr) * os + h * HD + ch) =
+          *reinterpret_cast<const u32x4*>(Os + r * OLD + ch);
   }
   if (lse != nullptr && half == 0 && qrow < n)
-    lse[static_cast<int64_t>(h) * T + lo + qrow] = (m_run + log2f(l_run)) * kLn2;
+    lse[static_cast<int64_t>(h) * T + lo + qrow] = (m_run * scale_log2 + log2f(l_run)) * kLn2;
 }
 
 template <typename T, int HD>
