@@ -45,6 +45,9 @@ def parse():
     ap.add_argument("--workload", default="bert")
     ap.add_argument("--keep-rates", default=None, help="comma-separated sweep")
     ap.add_argument("--seed", type=int, default=0)
+    ap.add_argument("--also", default="gpt2",
+                    help="comma-separated presets whose keep-rate sweeps are reported beside "
+                         "the headline workload")
     ap.add_argument("--no-graph", action="store_true", help="time eager launches instead")
     ap.add_argument("--cpu-seconds", type=float, default=15.0,
                     help="target wall time of the CPU-oracle sample (0 disables it)")
@@ -138,6 +141,44 @@ def gemm_flops(p, rows_in, rows_after):
     return total
 
 
+def class_work(p, lens, plan, rows_in, rows_after):
+    """Algorithmic work per kernel class for one forward: FLOPs for the MFMA
+    classes, bytes for the memory-bound ones (the per-row or per-pair figure
+    times the rows or pairs each launch processes)."""
+    d, H, hd, F = p.d_model, p.n_heads, p.d_model // p.n_heads, p.d_ff
+    e = 2 if p.dtype == "bf16" else 4
+    attn_flops = 0.0
+    score_flops = 0.0
+    norm_bytes = 0.0
+    # per-sequence lengths through the schedule
+    counts = [list(lens)] + [list(c) for c in plan["counts"]]
+    point = 0
+    cur = counts[0]
+    for l in range(1, p.n_layers + 1):
+        # Eq. 1 attention: QK^T and PV, 2*n*hd each per query and head
+        # (half of that under the causal mask)
+        frac = 0.5 if p.causal else 1.0
+        attn_flops += sum(4.0 * n * n * hd * H * frac for n in cur)
+        norm_bytes += 2.0 * rows_in[l - 1] * d * e + 2.0 * rows_after[l - 1] * d * e
+        if point < len(p.prune_after) and p.prune_after[point] == l:
+            score_flops += sum(2.0 * n * n * hd * H * frac for n in cur)
+            point += 1
+            cur = counts[point]
+    gather_bytes = 0.0
+    select_bytes = 0.0
+    for pt in range(len(p.prune_after)):
+        t_in = plan["rows_in"][pt]
+        t_out = plan["rows_in"][pt + 1]
+        # two row arrays (residual, attention output) read and written, plus
+        # index and position words
+        gather_bytes += 2 * 2.0 * t_out * d * e + 12.0 * t_out
+        # scores (one partial per head group; counted as one vector) and kept rows
+        select_bytes += 4.0 * t_in + 4.0 * t_out
+    return {"attention": ("TFLOP/s", attn_flops), "score": ("TFLOP/s", score_flops),
+            "norm": ("GB/s", norm_bytes), "gather": ("GB/s", gather_bytes),
+            "select": ("GB/s", select_bytes)}
+
+
 def layer_rows(p, plan):
     rows_in, rows_after = [], []
     cur = plan["rows_in"][0]
@@ -185,38 +226,9 @@ def cpu_baseline(p, ws_np, x_np, lens, rate, budget_s):
                       f"float64 exact mode, {elapsed:.1f} s"}
 
 
-def main():
-    args = parse()
-    if args.summarize_pmc:
-        summarize_pmc(args)
-        return
-    if args.gpus != 1:
-        print(f"bench.py runs on one GPU only (asked for --gpus {args.gpus}); the pruned stack "
-              f"is measured on a single MI355X and this build has no multi-GPU path.",
-              file=sys.stderr)
-        sys.exit(2)
-
-    import torch
-
-    from paper_2509_01190_amd import workloads as W
-    from paper_2509_01190_amd import zsa
-
-    if not torch.cuda.is_available():
-        print("bench.py needs a GPU", file=sys.stderr)
-        sys.exit(1)
-    dev = torch.device("cuda:0")
-    if args.copy_calibration:
-        src = torch.empty(args.copy_calibration, dtype=torch.uint8, device=dev).fill_(1)
-        dst = torch.empty_like(src)
-        torch.cuda.synchronize()
-        dst.copy_(src)
-        torch.cuda.synchronize()
-        print(json.dumps({"copy_bytes": args.copy_calibration}))
-        return
-    p = W.PRESETS[args.workload]
-    rates = [float(r) for r in args.keep_rates.split(",")] if args.keep_rates else list(p.keep_rates)
-    if HEADLINE_RATE not in rates:
-        rates.append(HEADLINE_RATE)
+def measure(p, rates, args, torch, W, zsa, dev, timing):
+    """Graph-replayed step time of preset ``p`` at every keep rate (and, with
+    ``timing``, per-class launch durations of one eager forward)."""
     lens = W.lengths(p, args.seed)
     ws_np = W.stack_weights(p, args.seed)
     x_np = W.hidden(p, args.seed, lens)
@@ -255,30 +267,84 @@ def main():
             step()
         torch.cuda.synchronize()
         ms = (time.perf_counter() - t0) * 1e3 / args.steps
-
-        # per-class launch durations of one eager forward (HIP events on the stream)
-        for c in range(len(zsa.KCLASS_NAMES)):
-            zsa.timing_arm(c, 1024)
-        stack.forward(xd, posd, seqs, p.prune_after, kr, out=outs)
-        torch.cuda.synchronize()
-        cls = {}
-        for c, name in enumerate(zsa.KCLASS_NAMES):
-            n, t = zsa.timing_read(c)
-            cls[name] = {"launches": n, "ms": t}
         plan = stack.plan(seqs, p.prune_after, kr)
-        rows_in, rows_after = layer_rows(p, plan)
-        results[rate] = {"ms": ms, "tok_s": tokens / (ms * 1e-3), "classes": cls,
-                         "gemm_flops": gemm_flops(p, rows_in, rows_after),
-                         "kept_rows_final": plan["final_rows"]}
+        r = {"ms": ms, "tok_s": tokens / (ms * 1e-3), "kept_rows_final": plan["final_rows"]}
+        if timing:
+            # per-class launch durations of one eager forward (HIP events on the stream)
+            for c in range(len(zsa.KCLASS_NAMES)):
+                zsa.timing_arm(c, 1024)
+            stack.forward(xd, posd, seqs, p.prune_after, kr, out=outs)
+            torch.cuda.synchronize()
+            cls = {}
+            for c, name in enumerate(zsa.KCLASS_NAMES):
+                n, t = zsa.timing_read(c)
+                cls[name] = {"launches": n, "ms": t}
+            rows_in, rows_after = layer_rows(p, plan)
+            r.update({"classes": cls, "gemm_flops": gemm_flops(p, rows_in, rows_after),
+                      "work": class_work(p, lens, plan, rows_in, rows_after)})
+        results[rate] = r
+        if not args.no_graph:
+            del g
+    return lens, ws_np, x_np, results
 
+
+def sweep_of(results, rates):
     base = results.get(1.0)
-    sweep = []
+    out = []
     for rate in rates:
         r = results[rate]
-        sweep.append({"keep_rate": rate, "tokens_per_s": round(r["tok_s"], 1),
-                      "ms_per_step": round(r["ms"], 4),
-                      "speedup_vs_keep_rate_1": None if base is None else round(base["ms"] / r["ms"], 3),
-                      "rows_after_last_prune": r["kept_rows_final"]})
+        out.append({"keep_rate": rate, "tokens_per_s": round(r["tok_s"], 1),
+                    "ms_per_step": round(r["ms"], 4),
+                    "speedup_vs_keep_rate_1": None if base is None else round(base["ms"] / r["ms"], 3),
+                    "rows_after_last_prune": r["kept_rows_final"]})
+    return out
+
+
+def describe(p):
+    kind = "decoder (RMSNorm, SwiGLU, RoPE)" if p.kind == 1 else "pre-LN block (LayerNorm, GELU, biases)"
+    mask = "causal" if p.causal else "bidirectional"
+    if len(p.prune_after) == p.n_layers:
+        where = "after every layer"
+    else:
+        where = "after layers " + "/".join(map(str, p.prune_after))
+    return (f"{p.name}: {p.n_layers}-layer {mask} {kind} d{p.d_model} H{p.n_heads} FFN{p.d_ff}, "
+            f"{p.batch}x{p.seq_len} rows, pruned {where} (tau {p.tau})")
+
+
+def main():
+    args = parse()
+    if args.summarize_pmc:
+        summarize_pmc(args)
+        return
+    if args.gpus != 1:
+        print(f"bench.py runs on one GPU only (asked for --gpus {args.gpus}); the pruned stack "
+              f"is measured on a single MI355X and this build has no multi-GPU path.",
+              file=sys.stderr)
+        sys.exit(2)
+
+    import torch
+
+    from paper_2509_01190_amd import workloads as W
+    from paper_2509_01190_amd import zsa
+
+    if not torch.cuda.is_available():
+        print("bench.py needs a GPU", file=sys.stderr)
+        sys.exit(1)
+    dev = torch.device("cuda:0")
+    if args.copy_calibration:
+        src = torch.empty(args.copy_calibration, dtype=torch.uint8, device=dev).fill_(1)
+        dst = torch.empty_like(src)
+        torch.cuda.synchronize()
+        dst.copy_(src)
+        torch.cuda.synchronize()
+        print(json.dumps({"copy_bytes": args.copy_calibration}))
+        return
+    p = W.PRESETS[args.workload]
+    rates = [float(r) for r in args.keep_rates.split(",")] if args.keep_rates else list(p.keep_rates)
+    if HEADLINE_RATE not in rates:
+        rates.append(HEADLINE_RATE)
+    lens, ws_np, x_np, results = measure(p, rates, args, torch, W, zsa, dev, timing=True)
+    sweep = sweep_of(results, rates)
 
     # dominant kernel class over the whole sweep (every rate runs the same
     # number of steps, so this is also the mix a profiler sees)
@@ -298,6 +364,29 @@ def main():
                 "dominant_class": dom}
     head = results[HEADLINE_RATE]
     phases = {name: round(v["ms"], 4) for name, v in head["classes"].items() if v["launches"]}
+    # every kernel class against its own roofline, at the headline keep rate
+    per_class = {"gemm": {"bound": "mfma", "achieved": round(
+        head["gemm_flops"] / (head["classes"]["gemm"]["ms"] * 1e-3) / 1e12, 1), "unit": "TFLOP/s",
+        "peak": PEAK_BF16_TFLOPS}}
+    for name, (unit, amount) in head["work"].items():
+        t = head["classes"][name]["ms"] * 1e-3
+        if t <= 0:
+            continue
+        if unit == "TFLOP/s":
+            ach, peak, bound = amount / t / 1e12, PEAK_BF16_TFLOPS, "mfma"
+        else:
+            ach, peak, bound = amount / t / 1e9, PEAK_HBM_GBS, "hbm"
+        per_class[name] = {"bound": bound, "achieved": round(ach, 1), "unit": unit,
+                           "peak": peak}
+    for v in per_class.values():
+        v["frac"] = round(v["achieved"] / v["peak"], 4)
+
+    # the paper's every-layer schedule on a GPT-2-small-shaped causal stack
+    others = {}
+    for name in [w for w in args.also.split(",") if w and w != p.name]:
+        q = W.PRESETS[name]
+        _, _, _, res = measure(q, list(q.keep_rates), args, torch, W, zsa, dev, timing=False)
+        others[name] = {"workload": describe(q), "sweep": sweep_of(res, list(q.keep_rates))}
 
     cpu = None
     if args.cpu_seconds > 0:
@@ -308,12 +397,11 @@ def main():
         "steps": args.steps, "warmup": args.warmup, "ms_per_step": round(head["ms"], 4),
         "higher_is_better": True, "scaling": "weak", "vs_baseline": None, "dtype": p.dtype,
         "data": "synthetic (seeded N(0,0.02) weights, N(0,1) hidden rows)",
-        "config": {"workload": f"{p.name}: {p.n_layers}-layer encoder d{p.d_model} H{p.n_heads} "
-                               f"FFN{p.d_ff}, {p.batch}x{p.seq_len} rows, pruned after layers "
-                               f"{'/'.join(map(str, p.prune_after))}",
+        "config": {"workload": describe(p),
                    "keep_rate": HEADLINE_RATE, "global_batch": p.batch, "seq_len": p.seq_len,
                    "graph": not args.no_graph},
         "sweep": sweep, "phases_ms_at_headline": phases, "roofline": roofline,
+        "roofline_by_class_at_headline": per_class, "other_workloads": others,
         "cpu_baseline": cpu,
     }
     print(json.dumps(line))

@@ -79,6 +79,11 @@ PRESETS: Dict[str, Preset] = {
     # 7B-shaped decoder prefill, a 4-layer slice at real width, pruned after layer 1
     "dec7b": Preset("dec7b", DECODER, 4, 4096, 32, 11008, 4, 4096, "bf16", True, (1,),
                     (0.5, 0.2, 0.09)),
+    # the paper's own schedule: Eq. 2 after every layer (tau = 5) on a
+    # GPT-2-small-shaped causal stack (pre-LN, GELU, biases, no rotary; the
+    # learned position embeddings are part of the synthetic input rows)
+    "gpt2": Preset("gpt2", ENCODER, 12, 768, 12, 3072, 32, 512, "bf16", True,
+                   tuple(range(1, 13)), (1.0, 0.9, 0.8, 0.7, 0.5, 0.3, 0.1, 0.02)),
     # one 7B-shaped layer over a ragged batch with per-sequence keep rates
     "ragged": Preset("ragged", DECODER, 1, 4096, 32, 11008, 64, 4096, "bf16", True, (1,), (),
                      ragged=True, min_len=128, per_seq_rates=True, rate_lo=0.05, rate_hi=1.0),

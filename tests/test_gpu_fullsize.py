@@ -44,3 +44,11 @@ def test_ragged_full():
     order = np.argsort(lens)
     compare_stack(p, lens, stack, xd, posd, dws, ocfg, rates,
                   seqs_check=[int(order[0]), int(order[-1])])
+
+
+@pytest.mark.parametrize("rate", [0.7, 0.3])
+def test_gpt2_every_layer_full(rate):
+    p = W.PRESETS["gpt2"]
+    lens, stack, xd, posd, dws, ocfg = build(p, 0, norm_jitter=False)
+    rates = W.keep_rates(p, 0, rate)
+    compare_stack(p, lens, stack, xd, posd, dws, ocfg, rates, seqs_check=[3])

@@ -167,3 +167,14 @@ def test_graph_replay_matches_eager():
         torch.cuda.synchronize()
         assert torch.equal(out["x"], ref_x), f"replay {i}"
         assert torch.equal(out["pos"], ref_pos), f"replay {i}"
+
+
+def test_small_every_layer_schedule():
+    # the paper's default: Eq. 2 after every layer, tau = 5, causal GPT-2-like
+    # blocks, down to the tau floor
+    p = W.shrink(W.PRESETS["gpt2"], n_layers=5, d_model=256, n_heads=4, d_ff=512, batch=4,
+                 prune_after=(1, 2, 3, 4, 5))
+    lens = [300, 64, 129, 17]
+    lens, stack, xd, posd, dws, ocfg = build(p, 4, lens, sharp=3.0)
+    for rates in ([0.5, 0.7, 0.3, 0.9], [0.02, 0.1, 0.05, 1.0]):
+        compare_stack(p, lens, stack, xd, posd, dws, ocfg, rates)
