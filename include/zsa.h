@@ -149,11 +149,21 @@ int zsa_norm(void* stream, int32_t dtype, int32_t kind, const void* x, const voi
  * (a multiple of head_dim) in head_dim blocks: channels i and i + hd/2
  * rotate by pos[row] * rope_theta^(-2i/hd); pos [m] int32 device.
  * bf16 uses MFMA tiles; fp32 uses vector ALU tiles.
+ * ws (device, 16-byte aligned, caller-owned) or NULL: room for split-K
+ * partial sums. When the output tiles of a bf16 product are too few to
+ * fill the GPU, K is split into slices whose fp32 partials are summed in a
+ * fixed slice order before the epilogue (results are reproducible; they
+ * may differ from the unsplit sum in the last bits). With ws NULL the
+ * product is never split. ws_bytes below zsa_linear_workspace_size()
+ * returns ZSA_EWORKSPACE.
  */
 int zsa_linear(void* stream, int32_t dtype, const void* x, int32_t m, int32_t k, const void* w,
                int32_t n, const void* bias, int32_t epilogue, const void* residual,
                const int32_t* pos, int32_t head_dim, int32_t rope_cols, float rope_theta,
-               void* y);
+               void* y, void* ws, size_t ws_bytes);
+
+/* Bytes of split-K workspace zsa_linear uses for this shape (0: none). */
+size_t zsa_linear_workspace_size(int32_t dtype, int32_t m, int32_t n, int32_t k);
 
 /* ---------------------------------------------------------------------
  * Attention of Eq. 1, per sequence and head, over packed varlen rows, and

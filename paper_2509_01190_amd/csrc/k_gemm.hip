@@ -19,6 +19,8 @@
 #include <math.h>
 #include <stdlib.h>
 
+#include <algorithm>
+
 #include "zsa_internal.h"
 
 namespace zsa {
@@ -166,6 +168,8 @@ __device__ void epilogue_tile(const float* tile, int ldt, int m0, int n0, int M,
 // bf16 MFMA GEMM
 // ---------------------------------------------------------------------------
 constexpr int kBK = 64, kLDK = kBK + 8;  // K step; padded LDS row (bf16)
+constexpr int kMinSplitSteps = 4;          // K steps per split-K slice, at least
+constexpr int kMinSplitK = 1024;           // shortest K that is split
 
 // fp32 epilogue tile: 128 rows of BN columns, row stride BN + 4
 template <int BM, int BN>
@@ -336,47 +340,69 @@ inline dim3 xcd_grid(int M, int N, int BM, int BN) {
 // bf16 MFMA GEMM with direct-to-LDS operand loads
 // ---------------------------------------------------------------------------
 // global_load_lds_dwordx4 writes each lane's 16 bytes to LDS at
-// (wave-uniform base) + 16 * lane, so one instruction fills 1 KiB: 8 rows of
-// 64 bf16. Tiles are stored unpadded, 128 bytes per row, with the 16-byte
-// chunk c of row r at position c ^ ((r >> 1) & 7). The DMA writes are
-// contiguous, and the 16 lanes of an MFMA fragment read phase (16
-// consecutive rows, one logical chunk) land on 16 distinct 4-bank groups.
-// Operands never pass through VGPRs: at the top of a K step each wave waits
-// for its own loads, one barrier publishes the stage, the next stage's
-// loads are issued into the other buffer and the MFMAs of this stage run
-// while they are in flight.
-template <int BM, int BN>
-constexpr int dma_lds_bytes() {
-  return 2 * (BM + BN) * 128 > 128 * (BN + 4) * 4 ? 2 * (BM + BN) * 128 : 128 * (BN + 4) * 4;
+// (wave-uniform base) + 16 * lane, so one instruction fills 1 KiB of a tile
+// whose rows are one K slice of KB bf16 (RB = 2 KB bytes): 1024 / RB rows.
+// Tiles are stored unpadded with the 16-byte chunk c of row r at position
+// c ^ ((r / RPP) & (CPR - 1)), where CPR = RB / 16 chunks make a row and
+// RPP = 256 / RB rows share one 256-byte span of the 64 banks. The DMA
+// writes stay contiguous, and the 16 lanes of an MFMA fragment read phase
+// (16 consecutive rows, one logical chunk) land on 16 distinct 4-bank
+// groups. Operands never pass through VGPRs.
+//
+// NS stages form a ring: the loads of K slice t + NS - 1 are issued at the
+// top of step t, so NS - 1 slices are in flight while the MFMAs of slice t
+// run. Each wave waits only for its own loads of slice t (vmcnt counts the
+// later slices' loads as still outstanding), one barrier publishes the
+// slice to the workgroup and also retires the stage the new loads reuse.
+// The fp32 output tile is staged through LDS in passes of ER rows.
+template <int KB>
+struct Slice {
+  static constexpr int RB = KB * 2;      // bytes per tile row
+  static constexpr int CPR = RB / 16;    // 16-byte chunks per row
+  static constexpr int RPD = 1024 / RB;  // rows per 1 KiB load instruction
+  static constexpr int RPP = 256 / RB;   // rows per 256-byte bank span
+};
+
+template <int KB>
+__device__ __forceinline__ int swz(int r, int c) {
+  return c ^ ((r / Slice<KB>::RPP) & (Slice<KB>::CPR - 1));
 }
 
-__device__ __forceinline__ int swz(int r, int c) { return c ^ ((r >> 1) & 7); }
+template <int BM, int BN, int KB, int NS, int ER>
+constexpr int dma_lds_bytes() {
+  return NS * (BM + BN) * Slice<KB>::RB > ER * (BN + 4) * 4 ? NS * (BM + BN) * Slice<KB>::RB
+                                                             : ER * (BN + 4) * 4;
+}
 
 // waves per SIMD the tile's LDS footprint allows (160 KiB per CU)
-template <int BM, int BN, int WM, int WN>
+template <int BM, int BN, int WM, int WN, int KB, int NS, int ER>
 constexpr int dma_waves_per_simd() {
-  return (163840 / (2 * (BM + BN) * 128 > 128 * (BN + 4) * 4 ? 2 * (BM + BN) * 128
-                                                               : 128 * (BN + 4) * 4)) *
-         WM * WN / 4;
+  return (163840 / dma_lds_bytes<BM, BN, KB, NS, ER>()) * WM * WN / 4;
 }
 
-template <int BM, int BN, int WM, int WN>
+// s_waitcnt immediate: vector-memory count <= n, LDS/scalar and export counts 0
+__device__ __forceinline__ constexpr int vmcnt_imm(int n) { return (n & 15) | ((n >> 4) << 14); }
+
+template <int BM, int BN, int WM, int WN, int KB, int NS, int ER>
 __global__ __launch_bounds__(WM * WN * 64)
-__attribute__((amdgpu_waves_per_eu(dma_waves_per_simd<BM, BN, WM, WN>(),
-                                   dma_waves_per_simd<BM, BN, WM, WN>()))) void
+__attribute__((amdgpu_waves_per_eu(dma_waves_per_simd<BM, BN, WM, WN, KB, NS, ER>(),
+                                   dma_waves_per_simd<BM, BN, WM, WN, KB, NS, ER>()))) void
 gemm_bf16_dma_kernel(
     const bf16_t* __restrict__ X, const bf16_t* __restrict__ W, int M, int N, int K,
-    EpiParams ep) {
+    EpiParams ep, int kchunk, float* __restrict__ part) {
   static_assert(BM % 128 == 0 && (BN == 128 || BN == 256), "tile shape");
+  static_assert((KB == 32 || KB == 64) && NS >= 2 && ER % 32 == 0 && BM % ER == 0, "pipeline");
+  using SL = Slice<KB>;
   constexpr int NW = WM * WN;
   constexpr int NT = NW * 64;
   constexpr int kTileLd = BN + 4;
   constexpr int WTM = BM / WM, WTN = BN / WN;
   constexpr int TM = WTM / 32, TN = WTN / 32;
-  constexpr int AI = BM / 8 / NW, BI = BN / 8 / NW;  // 1 KiB DMA blocks per wave
-  static_assert(AI * NW * 8 == BM && BI * NW * 8 == BN, "blocks per wave");
+  constexpr int AI = BM / SL::RPD / NW, BI = BN / SL::RPD / NW;  // 1 KiB loads per wave
+  static_assert(AI * NW * SL::RPD == BM && BI * NW * SL::RPD == BN, "loads per wave");
+  constexpr int SB = (BM + BN) * SL::RB;  // bytes per stage: A rows, then B rows
+  constexpr int KS = KB / 16;              // MFMA k-substeps per slice
   extern __shared__ __align__(16) unsigned char smem[];
-  // stage s: A at smem + s * (BM + BN) * 128, B right after it
   const int tid = threadIdx.x;
   const int lane = tid & 63;
   // wave index as a scalar: the DMA destinations derived from it are then
@@ -388,23 +414,26 @@ gemm_bf16_dma_kernel(
   const int m0 = mt * BM;
   const int n0 = nt * BN;
 
-  // per-lane global sources of this wave's DMA blocks (row clamped; the
-  // logical chunk is the position un-swizzled for the destination row)
-  const int lr = lane >> 3, lp = lane & 7;
+  // split K: workgroup row y covers K columns [y * kchunk, y * kchunk + kchunk)
+  const int kbeg = blockIdx.y * kchunk;
+  const int KTOT = min(kchunk, K - kbeg) / KB;
+
+  // per-lane global sources of this wave's loads (row clamped; the logical
+  // chunk is the position un-swizzled for the destination row)
+  const int lr = lane / SL::CPR, lp = lane % SL::CPR;
   const bf16_t* asrc[AI];
 #pragma unroll
   for (int i = 0; i < AI; ++i) {
-    const int r = (i * NW + wave) * 8 + lr;
-    asrc[i] = X + static_cast<int64_t>(min(m0 + r, M - 1)) * K + swz(r, lp) * 8;
+    const int r = (i * NW + wave) * SL::RPD + lr;
+    asrc[i] = X + static_cast<int64_t>(min(m0 + r, M - 1)) * K + kbeg + swz<KB>(r, lp) * 8;
   }
   const bf16_t* bsrc[BI];
 #pragma unroll
   for (int i = 0; i < BI; ++i) {
-    const int r = (i * NW + wave) * 8 + lr;
-    bsrc[i] = W + static_cast<int64_t>(min(n0 + r, N - 1)) * K + swz(r, lp) * 8;
+    const int r = (i * NW + wave) * SL::RPD + lr;
+    bsrc[i] = W + static_cast<int64_t>(min(n0 + r, N - 1)) * K + kbeg + swz<KB>(r, lp) * 8;
   }
   typedef __attribute__((address_space(3))) void lds_void;
-  auto stage_base = [](int s) { return s * (BM + BN) * 128; };
 
 // the LDS-DMA builtin exists only in the device pass; the host pass only
 // needs the kernel's launch stub
@@ -415,9 +444,9 @@ gemm_bf16_dma_kernel(
 #endif
 #define ZSA_DMA(s, k0)                                                                   \
   _Pragma("unroll") for (int i = 0; i < AI; ++i)                                         \
-    ZSA_DMA1(asrc[i] + (k0), smem + stage_base(s) + (i * NW + wave) * 1024);             \
+    ZSA_DMA1(asrc[i] + (k0), smem + (s) * SB + (i * NW + wave) * 1024);                  \
   _Pragma("unroll") for (int i = 0; i < BI; ++i)                                         \
-    ZSA_DMA1(bsrc[i] + (k0), smem + stage_base(s) + BM * 128 + (i * NW + wave) * 1024);
+    ZSA_DMA1(bsrc[i] + (k0), smem + (s) * SB + BM * SL::RB + (i * NW + wave) * 1024);
 
   f32x16_t acc[TM][TN];
 #pragma unroll
@@ -429,40 +458,46 @@ gemm_bf16_dma_kernel(
 
   // byte offsets (within a stage) of this lane's fragments for each k-substep
   const int l32 = lane & 31, half = lane >> 5;
-  int aoff[TM][kBK / 16], boff[TN][kBK / 16];
+  int aoff[TM][KS], boff[TN][KS];
 #pragma unroll
   for (int i = 0; i < TM; ++i) {
     const int r = wm * WTM + i * 32 + l32;
 #pragma unroll
-    for (int kk = 0; kk < kBK / 16; ++kk) aoff[i][kk] = r * 128 + swz(r, kk * 2 + half) * 16;
+    for (int kk = 0; kk < KS; ++kk) aoff[i][kk] = r * SL::RB + swz<KB>(r, kk * 2 + half) * 16;
   }
 #pragma unroll
   for (int j = 0; j < TN; ++j) {
     const int r = wn * WTN + j * 32 + l32;
 #pragma unroll
-    for (int kk = 0; kk < kBK / 16; ++kk) boff[j][kk] = BM * 128 + r * 128 + swz(r, kk * 2 + half) * 16;
+    for (int kk = 0; kk < KS; ++kk)
+      boff[j][kk] = BM * SL::RB + r * SL::RB + swz<KB>(r, kk * 2 + half) * 16;
   }
 
   // one K step on stage S (a compile-time constant, so every LDS address is
-  // a register plus an immediate): wait for this wave's DMA, publish the
-  // stage with one barrier, start the next step's DMA into the other stage,
-  // then run the MFMAs, reading the next k-substep's fragments ahead.
-#define ZSA_STEP(S, KT)                                                                  \
+  // a register plus an immediate): wait for this wave's loads of slice T,
+  // publish it with one barrier, start the loads of slice T + NS - 1 into the
+  // stage slice T - 1 used, then run the MFMAs, reading the next k-substep's
+  // fragments ahead. Near the end fewer later slices are in flight, so the
+  // wait there is for all of them.
+#define ZSA_STEP(S, T)                                                                   \
   {                                                                                      \
-    __builtin_amdgcn_s_waitcnt(0);                                                       \
+    if (KTOT - 1 - (T) >= NS - 2)                                                        \
+      __builtin_amdgcn_s_waitcnt(vmcnt_imm((NS - 2) * (AI + BI)));                       \
+    else                                                                                 \
+      __builtin_amdgcn_s_waitcnt(0);                                                     \
     __syncthreads();                                                                     \
-    if ((KT) + 1 < KTOT) {                                                               \
-      ZSA_DMA((S) ^ 1, ((KT) + 1) * kBK)                                                 \
+    if ((T) + NS - 1 < KTOT) {                                                           \
+      ZSA_DMA(((S) + NS - 1) % NS, ((T) + NS - 1) * KB)                                  \
     }                                                                                    \
-    const unsigned char* st = smem + stage_base(S);                                      \
+    const unsigned char* st = smem + (S) * SB;                                           \
     bf16x8_t a[2][TM], b[2][TN];                                                         \
     _Pragma("unroll") for (int i = 0; i < TM; ++i)                                       \
       a[0][i] = __builtin_bit_cast(bf16x8_t, *reinterpret_cast<const u32x4*>(st + aoff[i][0])); \
     _Pragma("unroll") for (int j = 0; j < TN; ++j)                                       \
       b[0][j] = __builtin_bit_cast(bf16x8_t, *reinterpret_cast<const u32x4*>(st + boff[j][0])); \
-    _Pragma("unroll") for (int kk = 0; kk < kBK / 16; ++kk) {                            \
+    _Pragma("unroll") for (int kk = 0; kk < KS; ++kk) {                                  \
       const int cur = kk & 1, nxt = cur ^ 1;                                             \
-      if (kk + 1 < kBK / 16) {                                                           \
+      if (kk + 1 < KS) {                                                                 \
         _Pragma("unroll") for (int i = 0; i < TM; ++i)                                   \
           a[nxt][i] = __builtin_bit_cast(bf16x8_t, *reinterpret_cast<const u32x4*>(st + aoff[i][kk + 1])); \
         _Pragma("unroll") for (int j = 0; j < TN; ++j)                                   \
@@ -478,43 +513,110 @@ gemm_bf16_dma_kernel(
 
   // operands swapped in the MFMA: the accumulator holds C^T, so lane l owns
   // output row l%32 of an m-block and 4 consecutive columns per register group
-  const int KTOT = K / kBK;
-  ZSA_DMA(0, 0)
+#pragma unroll
+  for (int s = 0; s < NS - 1; ++s)
+    if (s < KTOT) {
+      ZSA_DMA(s, s * KB)
+    }
   int kt = 0;
-  for (; kt + 1 < KTOT; kt += 2) {
-    ZSA_STEP(0, kt)
-    ZSA_STEP(1, kt + 1)
+  for (; kt + NS <= KTOT; kt += NS) {
+#pragma unroll
+    for (int s = 0; s < NS; ++s) ZSA_STEP(s, kt + s)
   }
-  if (kt < KTOT) ZSA_STEP(0, kt)
+  // kt is a multiple of NS here, so slice kt + s sits in stage s
+#pragma unroll
+  for (int s = 0; s < NS - 1; ++s)
+    if (kt + s < KTOT) ZSA_STEP(s, kt + s)
 #undef ZSA_STEP
 #undef ZSA_DMA
 #undef ZSA_DMA1
   // acc[i][j][4g + e] = C[m][n + e] with m = wm*WTM + 32 i + l%32 and
   // n = wn*WTN + 32 j + 8 g + 4 (l/32) inside the tile: every register group
   // is 4 consecutive columns of one row, staged with one 16-byte LDS write
-  // (rows 132 floats apart, so 16 lanes cover the 64 banks once).
-  __syncthreads();  // all waves are done reading the operand stages
+  // (rows BN + 4 floats apart, so 16 lanes cover the 64 banks once). The
+  // 32-row blocks are aligned, so each lies in one pass of ER rows.
+  if (part != nullptr) {
+    // split K: the raw fp32 partial tile goes to slice y of part [S][M][N]
+    // (N is a multiple of 8, so a 4-column group is inside or outside whole)
+    float* dst = part + static_cast<int64_t>(blockIdx.y) * M * N;
+#pragma unroll
+    for (int i = 0; i < TM; ++i)
+#pragma unroll
+      for (int j = 0; j < TN; ++j)
+#pragma unroll
+        for (int g = 0; g < 4; ++g) {
+          const int m = m0 + wm * WTM + i * 32 + l32;
+          const int n = n0 + wn * WTN + j * 32 + g * 8 + half * 4;
+          if (m < M && n < N)
+            *reinterpret_cast<float4*>(dst + static_cast<int64_t>(m) * N + n) =
+                make_float4(acc[i][j][4 * g], acc[i][j][4 * g + 1], acc[i][j][4 * g + 2],
+                            acc[i][j][4 * g + 3]);
+        }
+    return;
+  }
   float* tile = reinterpret_cast<float*>(smem);
 #pragma unroll
-  for (int pass = 0; pass < BM / 128; ++pass) {
-    if (pass > 0) __syncthreads();
-    if ((wm * WTM) / 128 == pass) {
+  for (int pass = 0; pass < BM / ER; ++pass) {
+    __syncthreads();  // operand stages (pass 0) or the previous pass's tile are free
 #pragma unroll
-      for (int i = 0; i < TM; ++i)
+    for (int i = 0; i < TM; ++i) {
+      if ((wm * WTM + i * 32) / ER != pass) continue;
 #pragma unroll
-        for (int j = 0; j < TN; ++j)
+      for (int j = 0; j < TN; ++j)
 #pragma unroll
-          for (int g = 0; g < 4; ++g) {
-            const int row = wm * WTM - pass * 128 + i * 32 + l32;
-            const int col = wn * WTN + j * 32 + g * 8 + half * 4;
-            const float4 v = make_float4(acc[i][j][4 * g], acc[i][j][4 * g + 1],
-                                         acc[i][j][4 * g + 2], acc[i][j][4 * g + 3]);
-            *reinterpret_cast<float4*>(tile + row * kTileLd + col) = v;
-          }
+        for (int g = 0; g < 4; ++g) {
+          const int row = wm * WTM + i * 32 - pass * ER + l32;
+          const int col = wn * WTN + j * 32 + g * 8 + half * 4;
+          const float4 v = make_float4(acc[i][j][4 * g], acc[i][j][4 * g + 1],
+                                       acc[i][j][4 * g + 2], acc[i][j][4 * g + 3]);
+          *reinterpret_cast<float4*>(tile + row * kTileLd + col) = v;
+        }
     }
     __syncthreads();
-    epilogue_tile<bf16_t, 128, BN, NT>(tile, kTileLd, m0 + pass * 128, n0, M, N, ep);
+    epilogue_tile<bf16_t, ER, BN, NT>(tile, kTileLd, m0 + pass * ER, n0, M, N, ep);
   }
+}
+
+// Split-K finish: sums the S partial tiles of an 8 x 128 output block in
+// slice order (fixed, so the result is reproducible), then applies the
+// epilogue exactly as the unsplit kernel does. One float4 per thread; the
+// slice loads are issued in groups of four before their (ordered) adds.
+constexpr int kRedRows = 8, kRedCols = 128;
+
+__global__ __launch_bounds__(256) void splitk_reduce_kernel(const float* __restrict__ part,
+                                                            int S, int M, int N, EpiParams ep) {
+  __shared__ __align__(16) float tile[kRedRows * (kRedCols + 4)];
+  const int m0 = blockIdx.x * kRedRows, n0 = blockIdx.y * kRedCols;
+  const int64_t slice = static_cast<int64_t>(M) * N;
+  const int r = threadIdx.x / (kRedCols / 4), c = (threadIdx.x % (kRedCols / 4)) * 4;
+  const int m = m0 + r, n = n0 + c;
+  float4 v = make_float4(0.f, 0.f, 0.f, 0.f);
+  if (m < M && n < N) {
+    const float* src = part + static_cast<int64_t>(m) * N + n;
+    int y = 0;
+    for (; y + 4 <= S; y += 4) {
+      float4 t[4];
+#pragma unroll
+      for (int u = 0; u < 4; ++u) t[u] = *reinterpret_cast<const float4*>(src + (y + u) * slice);
+#pragma unroll
+      for (int u = 0; u < 4; ++u) {
+        v.x += t[u].x;
+        v.y += t[u].y;
+        v.z += t[u].z;
+        v.w += t[u].w;
+      }
+    }
+    for (; y < S; ++y) {
+      const float4 t = *reinterpret_cast<const float4*>(src + y * slice);
+      v.x += t.x;
+      v.y += t.y;
+      v.z += t.z;
+      v.w += t.w;
+    }
+  }
+  *reinterpret_cast<float4*>(tile + r * (kRedCols + 4) + c) = v;
+  __syncthreads();
+  epilogue_tile<bf16_t, kRedRows, kRedCols, 256>(tile, kRedCols + 4, m0, n0, M, N, ep);
 }
 
 // ---------------------------------------------------------------------------
@@ -593,21 +695,23 @@ hipError_t launch_mfma(hipStream_t s, const void* x, int M, int K, const void* w
                 static_cast<const bf16_t*>(x), static_cast<const bf16_t*>(w), M, N, K, ep);
 }
 
-template <int BM, int BN, int WM, int WN>
+template <int BM, int BN, int WM, int WN, int KB, int NS, int ER>
 hipError_t launch_dma(hipStream_t s, const void* x, int M, int K, const void* w, int N,
-                      const EpiParams& ep) {
-  constexpr int lds = dma_lds_bytes<BM, BN>();
+                      const EpiParams& ep, int S = 1, int kchunk = 0, float* part = nullptr) {
+  constexpr int lds = dma_lds_bytes<BM, BN, KB, NS, ER>();
   static bool lds_raised = false;
   if (!lds_raised) {
     const hipError_t e = hipFuncSetAttribute(
-        reinterpret_cast<const void*>(gemm_bf16_dma_kernel<BM, BN, WM, WN>),
+        reinterpret_cast<const void*>(gemm_bf16_dma_kernel<BM, BN, WM, WN, KB, NS, ER>),
         hipFuncAttributeMaxDynamicSharedMemorySize, lds);
     if (e != hipSuccess) return e;
     lds_raised = true;
   }
-  const dim3 grid = xcd_grid(M, N, BM, BN);
-  return launch(K_GEMM, gemm_bf16_dma_kernel<BM, BN, WM, WN>, grid, dim3(WM * WN * 64), lds, s,
-                static_cast<const bf16_t*>(x), static_cast<const bf16_t*>(w), M, N, K, ep);
+  dim3 grid = xcd_grid(M, N, BM, BN);
+  grid.y = S;
+  return launch(K_GEMM, gemm_bf16_dma_kernel<BM, BN, WM, WN, KB, NS, ER>, grid,
+                dim3(WM * WN * 64), lds, s, static_cast<const bf16_t*>(x),
+                static_cast<const bf16_t*>(w), M, N, K, ep, S > 1 ? kchunk : K, part);
 }
 
 // ZSA_GEMM_TILE pins one kernel variant (a tuning aid; 0 or unset = by shape):
@@ -624,27 +728,87 @@ int gemm_tile_override() {
 
 }  // namespace
 
+// Split K when the 128 x 128 output tiles cannot fill the chip (fewer than
+// 256, under one round at two workgroups per CU) and K is long (at least
+// kMinSplitK): S slices of at least kMinSplitSteps K steps, S x tiles <= 512
+// workgroups (one round, no tail). Every slice is non-empty and all but the
+// last have kchunk columns.
+void splitk_plan(int M, int N, int K, int* S, int* kchunk) {
+  *S = 1;
+  *kchunk = K;
+  if (K % kBK != 0 || K < kMinSplitK) return;
+  const long tiles = static_cast<long>((M + 127) / 128) * ((N + 127) / 128);
+  const int steps = K / kBK;
+  if (tiles >= 256) return;
+  const int want = std::min(static_cast<int>(512 / tiles), steps / kMinSplitSteps);
+  if (want < 2) return;
+  const int per = (steps + want - 1) / want;
+  *S = (steps + per - 1) / per;
+  *kchunk = per * kBK;
+}
+
+size_t splitk_bytes(int S, int M, int N) {
+  return S > 1 ? static_cast<size_t>(S) * M * N * sizeof(float) : 0;
+}
+
+size_t gemm_workspace_bytes(int dtype, int M, int N, int K) {
+  if (dtype != 1) return 0;
+  int S, kchunk;
+  splitk_plan(M, N, K, &S, &kchunk);
+  return splitk_bytes(S, M, N);
+}
+
+size_t gemm_workspace_bound(int dtype, int max_rows, int N, int K) {
+  size_t b = 0;
+  // within a 128-row bucket the plan is fixed and the need grows with M, so
+  // the largest M of each bucket bounds it
+  for (int mt = 1; (mt - 1) * 128 < max_rows; ++mt) {
+    const int m = std::min(mt * 128, max_rows);
+    b = std::max(b, gemm_workspace_bytes(dtype, m, N, K));
+  }
+  return b;
+}
+
 hipError_t launch_gemm(hipStream_t s, int dtype, const void* x, int M, int K, const void* w,
-                       int N, const EpiParams& ep) {
+                       int N, const EpiParams& ep, void* ws, size_t ws_bytes) {
   if (M == 0 || N == 0) return hipSuccess;
   if (dtype == 1 && K % kBK == 0) {
+    int S = 1, kchunk = K;
+    splitk_plan(M, N, K, &S, &kchunk);
+    if (S > 1 && ws != nullptr && ws_bytes >= splitk_bytes(S, M, N)) {
+      float* part = static_cast<float*>(ws);
+      const hipError_t e =
+          launch_dma<128, 128, 2, 2, 64, 2, 128>(s, x, M, K, w, N, ep, S, kchunk, part);
+      if (e != hipSuccess) return e;
+      return launch(K_GEMM, splitk_reduce_kernel,
+                    dim3((M + kRedRows - 1) / kRedRows, (N + kRedCols - 1) / kRedCols), dim3(256),
+                    0, s, static_cast<const float*>(part), S, M, N, ep);
+    }
     switch (gemm_tile_override()) {
       case 128: return launch_mfma<128, 128, 2, 2>(s, x, M, K, w, N, ep);
       case 256: return launch_mfma<256, 128, 2, 2>(s, x, M, K, w, N, ep);
       case 2564: return launch_mfma<256, 256, 2, 2>(s, x, M, K, w, N, ep);
       case 2568: return launch_mfma<256, 256, 2, 4>(s, x, M, K, w, N, ep);
-      case 1281: return launch_dma<128, 128, 2, 2>(s, x, M, K, w, N, ep);
-      case 2563: return launch_dma<256, 128, 2, 2>(s, x, M, K, w, N, ep);
-      case 2562: return launch_dma<256, 256, 2, 2>(s, x, M, K, w, N, ep);
-      case 2561: return launch_dma<256, 256, 2, 4>(s, x, M, K, w, N, ep);
+      case 1281: return launch_dma<128, 128, 2, 2, 64, 2, 128>(s, x, M, K, w, N, ep);
+      case 2563: return launch_dma<256, 128, 2, 2, 64, 2, 128>(s, x, M, K, w, N, ep);
+      case 2562: return launch_dma<256, 256, 2, 2, 64, 2, 128>(s, x, M, K, w, N, ep);
+      case 2561: return launch_dma<256, 256, 2, 4, 64, 2, 128>(s, x, M, K, w, N, ep);
+      case 3241: return launch_dma<128, 128, 2, 2, 32, 4, 64>(s, x, M, K, w, N, ep);
+      case 3231: return launch_dma<128, 128, 2, 2, 32, 3, 64>(s, x, M, K, w, N, ep);
+      case 3251: return launch_dma<128, 128, 2, 2, 32, 5, 64>(s, x, M, K, w, N, ep);
+      case 6431: return launch_dma<128, 128, 2, 2, 64, 3, 64>(s, x, M, K, w, N, ep);
+      case 6421: return launch_dma<128, 128, 2, 2, 64, 2, 64>(s, x, M, K, w, N, ep);
+      case 3243: return launch_dma<256, 128, 2, 2, 32, 4, 64>(s, x, M, K, w, N, ep);
+      case 3233: return launch_dma<256, 128, 2, 2, 32, 3, 64>(s, x, M, K, w, N, ep);
+      case 3245: return launch_dma<256, 256, 2, 4, 32, 4, 64>(s, x, M, K, w, N, ep);
       default: break;
     }
     // Measured on the projection shapes: direct-to-LDS 256x256 tiles over 8
     // waves (128x64 per wave) win once the grid holds at least four rounds of
     // such tiles; below that, direct-to-LDS 128x128 tiles over 4 waves.
     const long tiles256 = static_cast<long>((M + 255) / 256) * ((N + 255) / 256);
-    if (tiles256 >= 1024) return launch_dma<256, 256, 2, 4>(s, x, M, K, w, N, ep);
-    return launch_dma<128, 128, 2, 2>(s, x, M, K, w, N, ep);
+    if (tiles256 >= 1024) return launch_dma<256, 256, 2, 4, 64, 2, 128>(s, x, M, K, w, N, ep);
+    return launch_dma<128, 128, 2, 2, 64, 2, 128>(s, x, M, K, w, N, ep);
   }
   const dim3 grid((M + vBM - 1) / vBM, (N + vBN - 1) / vBN);
   if (dtype == 1)

@@ -3,6 +3,7 @@
 // Everything here runs on the host and only enqueues work on the caller's
 // stream; no call synchronises, allocates device memory or copies from host
 // memory (host values reach kernels as launch arguments).
+#include <algorithm>
 #include <math.h>
 #include <stdarg.h>
 #include <stdio.h>
@@ -163,6 +164,8 @@ struct LayerBufs {
   float* lse;
   float* partials;
   int32_t* kept;
+  void* splitk;
+  size_t splitk_bytes;
 };
 
 struct Carver {
@@ -175,7 +178,7 @@ struct Carver {
 };
 
 struct LayerLayout {
-  size_t h, qkv, o, f, xg, og, lse, partials, kept, end;
+  size_t h, qkv, o, f, xg, og, lse, partials, kept, splitk, splitk_bytes, end;
 };
 
 LayerLayout layer_layout(const zsa_layer_cfg* c, int64_t T, Carver& cv) {
@@ -193,6 +196,15 @@ LayerLayout layer_layout(const zsa_layer_cfg* c, int64_t T, Carver& cv) {
   L.lse = cv.take(static_cast<size_t>(c->n_heads) * T * 4);
   L.partials = cv.take(static_cast<size_t>(G) * T * 4);
   L.kept = cv.take(T * 4);
+  // split-K partials of the projections, for any row count up to T
+  const int dt = c->dtype;
+  const int up_n = c->kind == ZSA_DECODER ? 2 * F : F;
+  const int rows = static_cast<int>(T);
+  L.splitk_bytes = std::max({zsa::gemm_workspace_bound(dt, rows, 3 * d, d),
+                             zsa::gemm_workspace_bound(dt, rows, d, d),
+                             zsa::gemm_workspace_bound(dt, rows, up_n, d),
+                             zsa::gemm_workspace_bound(dt, rows, d, F)});
+  L.splitk = cv.take(L.splitk_bytes);
   L.end = cv.off;
   return L;
 }
@@ -209,6 +221,8 @@ LayerBufs carve_layer(const LayerLayout& L, void* ws) {
   b.lse = reinterpret_cast<float*>(base + L.lse);
   b.partials = reinterpret_cast<float*>(base + L.partials);
   b.kept = reinterpret_cast<int32_t*>(base + L.kept);
+  b.splitk = L.splitk_bytes ? base + L.splitk : nullptr;
+  b.splitk_bytes = L.splitk_bytes;
   return b;
 }
 
@@ -253,7 +267,8 @@ int run_layer(hipStream_t s, const zsa_layer_cfg& c, const zsa_layer_weights& w,
     ep.head_dim = hd;
     ep.rope_cols = dec ? 2 * d : 0;
     if (dec) fill_rope(ep, hd, c.rope_theta);
-    HIP_TRY(launch_gemm(s, dt, wb.h, in.T, d, w.w_qkv, 3 * d, ep), "qkv projection");
+    HIP_TRY(launch_gemm(s, dt, wb.h, in.T, d, w.w_qkv, 3 * d, ep, wb.splitk, wb.splitk_bytes),
+            "qkv projection");
   }
   const char* qkv = static_cast<const char*>(wb.qkv);
   const void* q = qkv;
@@ -287,7 +302,8 @@ int run_layer(hipStream_t s, const zsa_layer_cfg& c, const zsa_layer_weights& w,
     ep.residual = xr;
     ep.y = x_out;
     ep.ldy = d;
-    HIP_TRY(launch_gemm(s, dt, orows, rows, d, w.w_o, d, ep), "output projection");
+    HIP_TRY(launch_gemm(s, dt, orows, rows, d, w.w_o, d, ep, wb.splitk, wb.splitk_bytes),
+            "output projection");
   }
   HIP_TRY(launch_norm(s, dt, norm_kind, x_out, w.norm2_w, dec ? nullptr : w.norm2_b, rows, d,
                       c.norm_eps, wb.h),
@@ -298,7 +314,9 @@ int run_layer(hipStream_t s, const zsa_layer_cfg& c, const zsa_layer_weights& w,
     ep.bias = w.b_up;
     ep.y = wb.f;
     ep.ldy = F;
-    HIP_TRY(launch_gemm(s, dt, wb.h, rows, d, w.w_up, dec ? 2 * F : F, ep), "up projection");
+    HIP_TRY(launch_gemm(s, dt, wb.h, rows, d, w.w_up, dec ? 2 * F : F, ep, wb.splitk,
+                        wb.splitk_bytes),
+            "up projection");
   }
   {
     EpiParams ep{};
@@ -307,7 +325,8 @@ int run_layer(hipStream_t s, const zsa_layer_cfg& c, const zsa_layer_weights& w,
     ep.residual = x_out;
     ep.y = x_out;
     ep.ldy = d;
-    HIP_TRY(launch_gemm(s, dt, wb.f, rows, F, w.w_down, d, ep), "down projection");
+    HIP_TRY(launch_gemm(s, dt, wb.f, rows, F, w.w_down, d, ep, wb.splitk, wb.splitk_bytes),
+            "down projection");
   }
   return ZSA_OK;
 }
@@ -390,10 +409,15 @@ int zsa_norm(void* stream, int32_t dtype, int32_t kind, const void* x, const voi
   return ZSA_OK;
 }
 
+size_t zsa_linear_workspace_size(int32_t dtype, int32_t m, int32_t n, int32_t k) {
+  if (m <= 0 || n <= 0 || k <= 0) return 0;
+  return zsa::gemm_workspace_bytes(dtype, m, n, k);
+}
+
 int zsa_linear(void* stream, int32_t dtype, const void* x, int32_t m, int32_t k, const void* w,
                int32_t n, const void* bias, int32_t epilogue, const void* residual,
                const int32_t* pos, int32_t head_dim, int32_t rope_cols, float rope_theta,
-               void* y) {
+               void* y, void* ws, size_t ws_bytes) {
   CHECK(check_dtype(dtype));
   if (m < 0) return fail(ZSA_EINVAL, "m < 0");
   CHECK(check_width(dtype, k, "k"));
@@ -424,7 +448,15 @@ int zsa_linear(void* stream, int32_t dtype, const void* x, int32_t m, int32_t k,
     ep.rope_cols = rope_cols;
     fill_rope(ep, head_dim, rope_theta);
   }
-  HIP_TRY(zsa::launch_gemm(static_cast<hipStream_t>(stream), dtype, x, m, k, w, n, ep), "linear");
+  if (ws != nullptr) {
+    CHECK(check_ptr16(ws, "ws"));
+    const size_t need = zsa_linear_workspace_size(dtype, m, n, k);
+    if (ws_bytes < need)
+      return fail(ZSA_EWORKSPACE, "linear workspace %zu < %zu bytes", ws_bytes, need);
+  }
+  HIP_TRY(zsa::launch_gemm(static_cast<hipStream_t>(stream), dtype, x, m, k, w, n, ep, ws,
+                           ws_bytes),
+          "linear");
   return ZSA_OK;
 }
 

@@ -127,9 +127,16 @@ struct EpiParams {
 hipError_t launch_norm(hipStream_t s, int dtype, int kind, const void* x, const void* g,
                        const void* b, int rows, int d, float eps, void* y);
 
-// y = epi(x[a_rows] W^T + bias); x [*, K] (row-gathered through a_rows if non-null)
+// y = epi(x W^T + bias); x [M, K], W [N, K]. ws (may be NULL) holds split-K
+// partials; the bf16 path splits K for small grids when ws_bytes covers it.
 hipError_t launch_gemm(hipStream_t s, int dtype, const void* x, int M, int K, const void* w,
-                       int N, const EpiParams& ep);
+                       int N, const EpiParams& ep, void* ws, size_t ws_bytes);
+// split-K plan of the bf16 path and its workspace (0 when K is not split)
+void splitk_plan(int M, int N, int K, int* S, int* kchunk);
+size_t splitk_bytes(int S, int M, int N);
+size_t gemm_workspace_bytes(int dtype, int M, int N, int K);
+// the most any M <= max_rows needs
+size_t gemm_workspace_bound(int dtype, int max_rows, int N, int K);
 
 hipError_t launch_attention(hipStream_t s, int dtype, const void* q, const void* k,
                             const void* v, int64_t row_stride, int H, int hd, int causal,

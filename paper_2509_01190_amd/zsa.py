@@ -63,7 +63,8 @@ _SIGS = {
     "zsa_keep_schedule": (ctypes.c_int, [_i32, _pi32, _pf64, _i32, _i32, _pi32]),
     "zsa_norm": (ctypes.c_int, [_vp, _i32, _i32, _vp, _vp, _vp, _i32, _i32, _f32, _vp]),
     "zsa_linear": (ctypes.c_int, [_vp, _i32, _vp, _i32, _i32, _vp, _i32, _vp, _i32, _vp, _vp,
-                                  _i32, _i32, _f32, _vp]),
+                                  _i32, _i32, _f32, _vp, _vp, _sz]),
+    "zsa_linear_workspace_size": (_sz, [_i32, _i32, _i32, _i32]),
     "zsa_attention_with_scores": (ctypes.c_int, [_vp, _i32, _vp, _vp, _vp, _i64, _i32, _i32,
                                                  _i32, _f32, _i32, _pi32, _vp, _vp, _i64, _vp,
                                                  _vp, _vp, _sz]),
@@ -202,10 +203,18 @@ def norm(x: torch.Tensor, gain: torch.Tensor, shift: Optional[torch.Tensor], kin
     return y
 
 
+def linear_workspace_size(dtype: int, m: int, n: int, k: int) -> int:
+    return int(lib().zsa_linear_workspace_size(dtype, m, n, k))
+
+
 def linear(x: torch.Tensor, w: torch.Tensor, bias: Optional[torch.Tensor] = None,
            epilogue: int = EPI_NONE, residual: Optional[torch.Tensor] = None,
            pos: Optional[torch.Tensor] = None, head_dim: int = 0, rope_cols: int = 0,
-           rope_theta: float = 10000.0, out: Optional[torch.Tensor] = None) -> torch.Tensor:
+           rope_theta: float = 10000.0, out: Optional[torch.Tensor] = None,
+           split: bool = True, ws: Optional[torch.Tensor] = None) -> torch.Tensor:
+    """y = epilogue(x w^T + bias). With ``split`` (and no ``ws``) a split-K
+    workspace is allocated when the shape asks for one; ``split=False``
+    never splits K."""
     _require_cuda(x, w, bias, residual, pos)
     m, k = x.shape
     n, k2 = w.shape
@@ -213,9 +222,14 @@ def linear(x: torch.Tensor, w: torch.Tensor, bias: Optional[torch.Tensor] = None
         raise ValueError("inner dimensions differ")
     ncols = n // 2 if epilogue == EPI_SWIGLU else n
     y = torch.empty((m, ncols), dtype=x.dtype, device=x.device) if out is None else out
+    if ws is None and split:
+        need = linear_workspace_size(_dtype_code(x), m, n, k)
+        if need:
+            ws = torch.empty(need, dtype=torch.uint8, device=x.device)
+    ws_bytes = 0 if ws is None else ws.numel() * ws.element_size()
     _check(lib().zsa_linear(_stream(x.device), _dtype_code(x), _p(x), m, k, _p(w), n, _p(bias),
                             epilogue, _p(residual), _p(pos), head_dim, rope_cols, rope_theta,
-                            _p(y)))
+                            _p(y), _p(ws), ws_bytes))
     return y
 
 

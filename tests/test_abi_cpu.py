@@ -132,3 +132,27 @@ def test_workspace_sizes_grow_with_rows():
     b = lib.zsa_stack_workspace_size(ctypes.byref(cfg), 16384, 4, 1)
     assert 0 < a < b
     assert b < 4 << 30   # a 7B-shaped 16k-row slice needs well under 4 GiB of scratch
+
+
+def test_linear_split_k_workspace():
+    ws = zsa.linear_workspace_size
+    # a 160-row down projection (12 output tiles) is split; 12 slices of K
+    assert ws(zsa.BF16, 160, 768, 3072) == 12 * 160 * 768 * 4
+    # grids that fill the GPU, fp32, and K too short to split are not
+    assert ws(zsa.BF16, 16384, 2304, 768) == 0
+    assert ws(zsa.F32, 160, 768, 3072) == 0
+    assert ws(zsa.BF16, 160, 768, 256) == 0
+    assert ws(zsa.BF16, 160, 768, 768) == 0
+    # 96 tiles of a 2048-row down projection: 5 slices (one round of 480 workgroups)
+    assert ws(zsa.BF16, 2048, 768, 3072) == 5 * 2048 * 768 * 4
+    assert ws(zsa.BF16, 0, 768, 3072) == 0
+    # a workspace below the need is refused before any launch
+    lib = zsa.lib()
+    rc = lib.zsa_linear(None, zsa.BF16, ctypes.c_void_p(0x1000), 160, 3072, ctypes.c_void_p(0x2000),
+                        768, None, zsa.EPI_NONE, None, None, 0, 0, 1e4, ctypes.c_void_p(0x3000),
+                        ctypes.c_void_p(0x4000), 1024)
+    assert rc == zsa.EWORKSPACE
+    # the layer workspace covers the split of every projection at any row count
+    cfg = zsa.make_cfg(zsa.ENCODER, 768, 12, 3072, False, zsa.BF16)
+    small = lib.zsa_layer_workspace_size(ctypes.byref(cfg), 160, 32)
+    assert small >= ws(zsa.BF16, 160, 768, 3072)
