@@ -65,6 +65,7 @@ def parse():
 GEMM_SRC = os.path.join(ROOT, "paper_2509_01190_amd", "csrc", "k_gemm.hip")
 TRAFFIC_FILE = os.path.join(ROOT, "profiles", "gemm_traffic.json")
 GEMM_KERNEL_TAG = "gemm_bf16_"
+REDUCE_KERNEL_TAG = "splitk_reduce"
 
 
 def gemm_source_hash():
@@ -73,9 +74,9 @@ def gemm_source_hash():
         return hashlib.sha256(f.read()).hexdigest()[:16]
 
 
-def pmc_mean(csv_path, counter, name_filter):
-    """Mean per-dispatch value (KiB for FETCH_SIZE / WRITE_SIZE) of a counter
-    over the dispatches whose kernel name contains name_filter."""
+def pmc_sum(csv_path, counter, name_filter):
+    """Sum over dispatches (KiB for FETCH_SIZE / WRITE_SIZE) of a counter for
+    the kernels whose name contains name_filter, and the dispatch count."""
     import csv
     import collections
     per = collections.defaultdict(float)
@@ -83,29 +84,39 @@ def pmc_mean(csv_path, counter, name_filter):
         for r in csv.DictReader(f):
             if r["Counter_Name"] == counter and name_filter in r["Kernel_Name"]:
                 per[r["Dispatch_Id"]] += float(r["Counter_Value"])
-    if not per:
-        raise SystemExit(f"no {counter} rows for kernels matching {name_filter!r} in {csv_path}")
-    return sum(per.values()) / len(per), len(per)
+    return sum(per.values()), len(per)
 
 
 def summarize_pmc(args):
-    """FETCH_SIZE / WRITE_SIZE (KiB per dispatch) of the GEMM launches of a bench
-    run, scaled by the ratio of true to counted bytes of a plain copy kernel."""
+    """FETCH_SIZE / WRITE_SIZE of the projections of a bench run (the GEMM
+    kernel and, where K is split, its reduce kernel), per projection (one
+    GEMM dispatch each), scaled by the ratio of true to counted bytes of a
+    plain copy kernel."""
     f_csv, w_csv, cf_csv, cw_csv = args.summarize_pmc
-    fetch_kib, n_f = pmc_mean(f_csv, "FETCH_SIZE", GEMM_KERNEL_TAG)
-    write_kib, n_w = pmc_mean(w_csv, "WRITE_SIZE", GEMM_KERNEL_TAG)
-    copy_f, _ = pmc_mean(cf_csv, "FETCH_SIZE", "copyBuffer")
-    copy_w, _ = pmc_mean(cw_csv, "WRITE_SIZE", "copyBuffer")
+    fetch_g, n_f = pmc_sum(f_csv, "FETCH_SIZE", GEMM_KERNEL_TAG)
+    write_g, n_w = pmc_sum(w_csv, "WRITE_SIZE", GEMM_KERNEL_TAG)
+    fetch_r, n_fr = pmc_sum(f_csv, "FETCH_SIZE", REDUCE_KERNEL_TAG)
+    write_r, n_wr = pmc_sum(w_csv, "WRITE_SIZE", REDUCE_KERNEL_TAG)
+    if not n_f or not n_w:
+        raise SystemExit("no GEMM dispatches in the counter files")
+    copy_f, n_cf = pmc_sum(cf_csv, "FETCH_SIZE", "copyBuffer")
+    copy_w, n_cw = pmc_sum(cw_csv, "WRITE_SIZE", "copyBuffer")
+    copy_f, copy_w = copy_f / max(n_cf, 1), copy_w / max(n_cw, 1)
     f_scale = args.copy_bytes / (copy_f * 1024.0)
     w_scale = args.copy_bytes / (copy_w * 1024.0)
+    fetch_kib = (fetch_g + fetch_r) / n_f
+    write_kib = (write_g + write_r) / n_w
     out = {
-        "kernel": "gemm_bf16_* (all projection GEMM launches of one bench run)",
+        "kernel": "projections: gemm_bf16_* plus splitk_reduce_kernel where K is split "
+                  "(one bench run, headline workload)",
         "gemm_source_sha256_16": gemm_source_hash(),
-        "dispatches": [n_f, n_w],
-        "fetch_kib_per_dispatch": fetch_kib, "write_kib_per_dispatch": write_kib,
+        "gemm_dispatches": [n_f, n_w], "reduce_dispatches": [n_fr, n_wr],
+        "fetch_kib_per_projection": fetch_kib, "write_kib_per_projection": write_kib,
+        "reduce_share_of_bytes": (fetch_r * f_scale + write_r * w_scale)
+                                 / ((fetch_g + fetch_r) * f_scale + (write_g + write_r) * w_scale),
         "copy_bytes": args.copy_bytes, "copy_fetch_kib": copy_f, "copy_write_kib": copy_w,
         "fetch_scale": f_scale, "write_scale": w_scale,
-        "hbm_bytes_per_launch": fetch_kib * 1024.0 * f_scale + write_kib * 1024.0 * w_scale,
+        "hbm_bytes_per_projection": fetch_kib * 1024.0 * f_scale + write_kib * 1024.0 * w_scale,
     }
     with open(TRAFFIC_FILE, "w") as f:
         json.dump(out, f, indent=1)
@@ -113,7 +124,7 @@ def summarize_pmc(args):
 
 
 def measured_traffic():
-    """HBM bytes per GEMM launch from the committed counter summary, or None
+    """HBM bytes per projection from the committed counter summary, or None
     when the GEMM source changed since the counters were taken."""
     try:
         with open(TRAFFIC_FILE) as f:
@@ -122,7 +133,7 @@ def measured_traffic():
         return None
     if t.get("gemm_source_sha256_16") != gemm_source_hash():
         return None
-    return t.get("hbm_bytes_per_launch")
+    return t.get("hbm_bytes_per_projection")
 
 
 def gemm_flops(p, rows_in, rows_after):
@@ -138,6 +149,25 @@ def gemm_flops(p, rows_in, rows_after):
         total += 2 * t_out * d * d             # output projection
         total += 2 * t_out * up_n * d          # up (or gate|up)
         total += 2 * t_out * d * F             # down
+    return total
+
+
+def gemm_bytes(p, results, rates):
+    """Algorithmic HBM bytes of the projections over the sweep: each operand
+    read once, the output written once, the residual read once."""
+    d, F = p.d_model, p.d_ff
+    e = 2 if p.dtype == "bf16" else 4
+    up_n = 2 * F if p.kind == 1 else F
+    up_out = F
+    total = 0
+    for r in rates:
+        rows_in, rows_after = results[r]["rows"]
+        for l in range(p.n_layers):
+            t_in, t_out = rows_in[l], rows_after[l]
+            total += e * (t_in * d + 3 * d * d + t_in * 3 * d)                  # QKV
+            total += e * (t_out * d + d * d + 2 * t_out * d)                    # O + residual
+            total += e * (t_out * d + up_n * d + t_out * up_out)                # up
+            total += e * (t_out * F + d * F + 2 * t_out * d)                    # down + residual
     return total
 
 
@@ -281,6 +311,7 @@ def measure(p, rates, args, torch, W, zsa, dev, timing):
                 cls[name] = {"launches": n, "ms": t}
             rows_in, rows_after = layer_rows(p, plan)
             r.update({"classes": cls, "gemm_flops": gemm_flops(p, rows_in, rows_after),
+                      "rows": (rows_in, rows_after),
                       "work": class_work(p, lens, plan, rows_in, rows_after)})
         results[rate] = r
         if not args.no_graph:
@@ -352,16 +383,18 @@ def main():
     dom = max(tot, key=tot.get)
     g_ms = sum(results[r]["classes"]["gemm"]["ms"] for r in rates)
     g_n = sum(results[r]["classes"]["gemm"]["launches"] for r in rates)
+    n_proj = 4 * p.n_layers * len(rates)      # QKV, output, up, down per layer
     g_flops = sum(results[r]["gemm_flops"] for r in rates)
     achieved = g_flops / (g_ms * 1e-3) / 1e12 if g_ms > 0 else 0.0
     traffic = measured_traffic()
-    roofline = {"kernel": "gemm_bf16_* (all projection GEMM launches)", "bound": "mfma",
-                "achieved": round(achieved, 1), "peak": PEAK_BF16_TFLOPS, "unit": "TFLOP/s",
-                "frac": round(achieved / PEAK_BF16_TFLOPS, 4),
+    roofline = {"kernel": "projections (gemm_bf16_* and, where K is split, splitk_reduce_kernel)",
+                "bound": "mfma", "achieved": round(achieved, 1), "peak": PEAK_BF16_TFLOPS,
+                "unit": "TFLOP/s", "frac": round(achieved / PEAK_BF16_TFLOPS, 4),
                 "traffic": None if traffic is None else round(traffic),
-                "traffic_unit": "HBM bytes per launch (FETCH_SIZE + WRITE_SIZE, copy-scaled)",
-                "avg_launch_us": round(g_ms * 1e3 / max(g_n, 1), 2), "launches": g_n,
-                "dominant_class": dom}
+                "traffic_unit": "HBM bytes per projection (FETCH_SIZE + WRITE_SIZE, copy-scaled)",
+                "algorithmic_bytes_per_projection": round(gemm_bytes(p, results, rates) / n_proj),
+                "avg_us_per_projection": round(g_ms * 1e3 / n_proj, 2), "projections": n_proj,
+                "launches": g_n, "dominant_class": dom}
     head = results[HEADLINE_RATE]
     phases = {name: round(v["ms"], 4) for name, v in head["classes"].items() if v["launches"]}
     # every kernel class against its own roofline, at the headline keep rate
