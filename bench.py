@@ -10,12 +10,18 @@ replayed as a HIP graph with every input already in HBM.
 
 The keep rate is swept over 1.0, 0.7, 0.5, 0.3, 0.1; `value` is the
 throughput at keep rate 0.5 (input tokens per second), the other points go
-to `sweep` with their speedup over keep rate 1.
+to `sweep` with their speedup over keep rate 1. `other_workloads` adds the
+same sweep for the paper's own schedule (Eq. 2 after every layer, tau = 5)
+on a GPT-2-small-shaped causal stack at 128, 512 and 1024 rows per sequence.
 
 `roofline` is reported for the kernel class with the largest share of GPU
-time (the projection GEMM): algorithmic FLOPs (2 * rows * out * in per
-launch) over the summed launch durations measured with HIP events on the
-launch stream, against the 2.5 PFLOP/s dense bf16 MFMA peak.
+time, the projections: algorithmic FLOPs (2 * rows * out * in per
+projection) over the summed durations of the projection kernels (the GEMM
+and, where K is split, its reduce), measured with HIP events on the launch
+stream, against the 2.5 PFLOP/s dense bf16 MFMA peak; `traffic` is the
+counter-measured HBM bytes per projection. `roofline_by_class_at_headline`
+puts every kernel class against its own bound, and `measured_ceilings`
+gives what the GPU sustains on a plain copy and a vendor bf16 GEMM.
 `cpu_baseline` times the float64 CPU oracle on a bounded sample of the same
 workload.
 """
@@ -45,7 +51,7 @@ def parse():
     ap.add_argument("--workload", default="bert")
     ap.add_argument("--keep-rates", default=None, help="comma-separated sweep")
     ap.add_argument("--seed", type=int, default=0)
-    ap.add_argument("--also", default="gpt2",
+    ap.add_argument("--also", default="gpt2,gpt2_n128,gpt2_n1024",
                     help="comma-separated presets whose keep-rate sweeps are reported beside "
                          "the headline workload")
     ap.add_argument("--no-graph", action="store_true", help="time eager launches instead")
@@ -319,6 +325,39 @@ def measure(p, rates, args, torch, W, zsa, dev, timing):
     return lens, ws_np, x_np, results
 
 
+def ceilings(torch, dev):
+    """What this GPU sustains: a 1 GiB device-to-device copy (read + write
+    bytes over time) and a large bf16 product through the vendor library
+    (hipBLASLt), for reading the rooflines beside the published peaks."""
+    out = {}
+    n = 1 << 30
+    src = torch.empty(n, dtype=torch.uint8, device=dev).fill_(1)
+    dst = torch.empty_like(src)
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    for _ in range(2):
+        dst.copy_(src)
+    e0.record()
+    for _ in range(5):
+        dst.copy_(src)
+    e1.record()
+    torch.cuda.synchronize()
+    out["hbm_copy_GBs"] = round(2.0 * n * 5 / (e0.elapsed_time(e1) * 1e-3) / 1e9, 1)
+    del src, dst
+    m = 8192
+    a = torch.randn(m, m, device=dev, dtype=torch.bfloat16)
+    b = torch.randn(m, m, device=dev, dtype=torch.bfloat16)
+    for _ in range(2):
+        torch.matmul(a, b)
+    e0.record()
+    for _ in range(5):
+        torch.matmul(a, b)
+    e1.record()
+    torch.cuda.synchronize()
+    out["bf16_gemm_8192_hipblaslt_TFLOPs"] = round(2.0 * m ** 3 * 5 / (e0.elapsed_time(e1) * 1e-3)
+                                                  / 1e12, 1)
+    return out
+
+
 def sweep_of(results, rates):
     base = results.get(1.0)
     out = []
@@ -421,6 +460,8 @@ def main():
         _, _, _, res = measure(q, list(q.keep_rates), args, torch, W, zsa, dev, timing=False)
         others[name] = {"workload": describe(q), "sweep": sweep_of(res, list(q.keep_rates))}
 
+    ceil = ceilings(torch, dev)
+
     cpu = None
     if args.cpu_seconds > 0:
         cpu = cpu_baseline(p, ws_np, x_np, lens, HEADLINE_RATE, args.cpu_seconds)
@@ -434,7 +475,8 @@ def main():
                    "keep_rate": HEADLINE_RATE, "global_batch": p.batch, "seq_len": p.seq_len,
                    "graph": not args.no_graph},
         "sweep": sweep, "phases_ms_at_headline": phases, "roofline": roofline,
-        "roofline_by_class_at_headline": per_class, "other_workloads": others,
+        "roofline_by_class_at_headline": per_class, "measured_ceilings": ceil,
+        "other_workloads": others,
         "cpu_baseline": cpu,
     }
     print(json.dumps(line))

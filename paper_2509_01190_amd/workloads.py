@@ -16,7 +16,7 @@ the oracle consume the same numbers.
 The presets follow the paper's two attention forms (bidirectional encoder,
 causal decoder; Sec. 3.2) and the backbone features it lists as shared by
 current models (pre-norm residual, GELU/SwiGLU, RoPE; Appendix A, Table 1),
-at the sizes of the five workloads this library is measured on.
+at the sizes of the workloads this library is measured on.
 """
 from __future__ import annotations
 
@@ -84,6 +84,11 @@ PRESETS: Dict[str, Preset] = {
     # learned position embeddings are part of the synthetic input rows)
     "gpt2": Preset("gpt2", ENCODER, 12, 768, 12, 3072, 32, 512, "bf16", True,
                    tuple(range(1, 13)), (1.0, 0.9, 0.8, 0.7, 0.5, 0.3, 0.1, 0.02)),
+    # ... the same stack at the other sequence lengths, 16384 rows per batch
+    "gpt2_n128": Preset("gpt2_n128", ENCODER, 12, 768, 12, 3072, 128, 128, "bf16", True,
+                        tuple(range(1, 13)), (1.0, 0.9, 0.8, 0.7, 0.5, 0.3, 0.1, 0.02)),
+    "gpt2_n1024": Preset("gpt2_n1024", ENCODER, 12, 768, 12, 3072, 16, 1024, "bf16", True,
+                         tuple(range(1, 13)), (1.0, 0.9, 0.8, 0.7, 0.5, 0.3, 0.1, 0.02)),
     # one 7B-shaped layer over a ragged batch with per-sequence keep rates
     "ragged": Preset("ragged", DECODER, 1, 4096, 32, 11008, 64, 4096, "bf16", True, (1,), (),
                      ragged=True, min_len=128, per_seq_rates=True, rate_lo=0.05, rate_hi=1.0),

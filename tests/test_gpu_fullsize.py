@@ -52,3 +52,11 @@ def test_gpt2_every_layer_full(rate):
     lens, stack, xd, posd, dws, ocfg = build(p, 0, norm_jitter=False)
     rates = W.keep_rates(p, 0, rate)
     compare_stack(p, lens, stack, xd, posd, dws, ocfg, rates, seqs_check=[3])
+
+
+@pytest.mark.parametrize("name,rate,seq", [("gpt2_n128", 0.3, 100), ("gpt2_n1024", 0.5, 9)])
+def test_gpt2_every_layer_other_lengths(name, rate, seq):
+    p = W.PRESETS[name]
+    lens, stack, xd, posd, dws, ocfg = build(p, 0, norm_jitter=False)
+    rates = W.keep_rates(p, 0, rate)
+    compare_stack(p, lens, stack, xd, posd, dws, ocfg, rates, seqs_check=[seq])
