@@ -717,7 +717,9 @@ hipError_t launch_dma(hipStream_t s, const void* x, int M, int K, const void* w,
 // ZSA_GEMM_TILE pins one kernel variant (a tuning aid; 0 or unset = by shape):
 // 128 / 256 / 2564 / 2568: register-staged 128x128, 256x128, 256x256 on 4 and
 // on 8 waves; 1281 / 2563 / 2562 / 2561: direct-to-LDS 128x128, 256x128,
-// 256x256 on 4 and on 8 waves.
+// 256x256 on 4 and on 8 waves (64-wide K slices, 2 stages); 3241: 128x128
+// with 32-wide slices in 4 stages; 6431: 128x128 with 3 stages; 2542:
+// 256x256 on 4 waves (128x128 per wave) with 64-row epilogue passes.
 int gemm_tile_override() {
   static const int v = [] {
     const char* e = getenv("ZSA_GEMM_TILE");
@@ -794,13 +796,8 @@ hipError_t launch_gemm(hipStream_t s, int dtype, const void* x, int M, int K, co
       case 2562: return launch_dma<256, 256, 2, 2, 64, 2, 128>(s, x, M, K, w, N, ep);
       case 2561: return launch_dma<256, 256, 2, 4, 64, 2, 128>(s, x, M, K, w, N, ep);
       case 3241: return launch_dma<128, 128, 2, 2, 32, 4, 64>(s, x, M, K, w, N, ep);
-      case 3231: return launch_dma<128, 128, 2, 2, 32, 3, 64>(s, x, M, K, w, N, ep);
-      case 3251: return launch_dma<128, 128, 2, 2, 32, 5, 64>(s, x, M, K, w, N, ep);
       case 6431: return launch_dma<128, 128, 2, 2, 64, 3, 64>(s, x, M, K, w, N, ep);
-      case 6421: return launch_dma<128, 128, 2, 2, 64, 2, 64>(s, x, M, K, w, N, ep);
-      case 3243: return launch_dma<256, 128, 2, 2, 32, 4, 64>(s, x, M, K, w, N, ep);
-      case 3233: return launch_dma<256, 128, 2, 2, 32, 3, 64>(s, x, M, K, w, N, ep);
-      case 3245: return launch_dma<256, 256, 2, 4, 32, 4, 64>(s, x, M, K, w, N, ep);
+      case 2542: return launch_dma<256, 256, 2, 2, 64, 2, 64>(s, x, M, K, w, N, ep);
       default: break;
     }
     // Measured on the projection shapes: direct-to-LDS 256x256 tiles over 8
