@@ -37,8 +37,9 @@ __global__ __launch_bounds__(256) void score_mfma_kernel(
     const float* __restrict__ lse, int H, int causal, float scale_log2,
     const int32_t* __restrict__ cu, int T, int groups, float* __restrict__ partials) {
   constexpr int KLD = HD + 8;
+  constexpr int KK = HD / 16;
   __shared__ __align__(16) bf16_t Ks[64 * KLD];
-  __shared__ float Ls[kLseChunk];
+  __shared__ __align__(16) float Ls[kLseChunk];
   __shared__ float red[4][64];
 
   const int b = blockIdx.z, g = blockIdx.y;
@@ -61,44 +62,76 @@ __global__ __launch_bounds__(256) void score_mfma_kernel(
           *reinterpret_cast<const uint4*>(K + static_cast<int64_t>(lo + min(jr, n - 1)) * rs + h * HD + ch);
     }
     __syncthreads();
-    bf16x8_t kf[2][HD / 16];
+    bf16x8_t kf[2][KK];
 #pragma unroll
     for (int ks = 0; ks < 2; ++ks)
 #pragma unroll
-      for (int kk = 0; kk < HD / 16; ++kk)
+      for (int kk = 0; kk < KK; ++kk)
         kf[ks][kk] = __builtin_bit_cast(
             bf16x8_t, *reinterpret_cast<const uint4*>(Ks + (ks * 32 + l32) * KLD + kk * 16 + half * 8));
 
+    const bf16_t* qh = Q + static_cast<int64_t>(lo) * rs + h * HD + half * 8;
     for (int c0 = qs; c0 < n; c0 += kLseChunk) {
       const int cend = min(n, c0 + kLseChunk);
       __syncthreads();
       for (int i = c0 + tid; i < cend; i += 256)
         Ls[i - c0] = lse[static_cast<int64_t>(h) * T + lo + i] * kLog2e;
       __syncthreads();
-      for (int i0 = c0 + wave * 32; i0 < cend; i0 += 128) {
-        bf16x8_t qa[HD / 16];
-        const int qr = i0 + l32;
+      // query tiles of 32 rows, strided over the 4 waves; the next tile's Q
+      // fragments are loaded while this tile's products and exps run. Rows
+      // past the sequence are clamped and masked.
+      int i0 = c0 + wave * 32;
+      u32x4 qn[KK];
+      if (i0 < cend) {
 #pragma unroll
-        for (int kk = 0; kk < HD / 16; ++kk)
-          qa[kk] = __builtin_bit_cast(  // rows past the sequence are clamped and masked below
-              bf16x8_t, *reinterpret_cast<const uint4*>(
-                            Q + static_cast<int64_t>(lo + min(qr, n - 1)) * rs + h * HD + kk * 16 + half * 8));
+        for (int kk = 0; kk < KK; ++kk)
+          qn[kk] = *reinterpret_cast<const u32x4*>(qh + static_cast<int64_t>(min(i0 + l32, n - 1)) * rs + kk * 16);
+      }
+      for (; i0 < cend; i0 += 128) {
+        bf16x8_t qa[KK];
+#pragma unroll
+        for (int kk = 0; kk < KK; ++kk) qa[kk] = __builtin_bit_cast(bf16x8_t, qn[kk]);
+        const int inext = i0 + 128;
+        if (inext < cend) {
+#pragma unroll
+          for (int kk = 0; kk < KK; ++kk)
+            qn[kk] = *reinterpret_cast<const u32x4*>(qh + static_cast<int64_t>(min(inext + l32, n - 1)) * rs + kk * 16);
+        }
+        // this lane's 16 query rows: i0 + 8 (r/4) + 4 half + r%4, four runs of 4
+        float4 lq[4];
+#pragma unroll
+        for (int q4 = 0; q4 < 4; ++q4)
+          lq[q4] = *reinterpret_cast<const float4*>(Ls + (i0 - c0) + 8 * q4 + 4 * half);
+        // masks matter only where the tile crosses the sequence end or, under
+        // the causal mask, reaches keys after some of its queries
+        const bool edge = i0 + 32 > cend || (causal && j0 + 63 > i0);
 #pragma unroll
         for (int ks = 0; ks < 2; ++ks) {
           f32x16_t acc;
 #pragma unroll
           for (int r = 0; r < 16; ++r) acc[r] = 0.f;
 #pragma unroll
-          for (int kk = 0; kk < HD / 16; ++kk)
+          for (int kk = 0; kk < KK; ++kk)
             acc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(qa[kk], kf[ks][kk], acc, 0, 0, 0);
           // acc[r]: query i0 + 8 (r/4) + 4 half + r%4, key j0 + 32 ks + l32
-          const int j = j0 + ks * 32 + l32;
           float tsum = 0.f;
+          if (!edge) {
 #pragma unroll
-          for (int r = 0; r < 16; ++r) {
-            const int i = i0 + 8 * (r >> 2) + 4 * half + (r & 3);
-            const bool ok = i < cend && (!causal || j <= i);
-            tsum += ok ? exp2f(acc[r] * scale_log2 - Ls[ok ? i - c0 : 0]) : 0.f;
+            for (int r = 0; r < 16; ++r) {
+              const float4 l4 = lq[r >> 2];
+              const float L = (r & 3) == 0 ? l4.x : (r & 3) == 1 ? l4.y : (r & 3) == 2 ? l4.z : l4.w;
+              tsum += __builtin_amdgcn_exp2f(fmaf(acc[r], scale_log2, -L));
+            }
+          } else {
+            const int j = j0 + ks * 32 + l32;
+#pragma unroll
+            for (int r = 0; r < 16; ++r) {
+              const int i = i0 + 8 * (r >> 2) + 4 * half + (r & 3);
+              const float4 l4 = lq[r >> 2];
+              const float L = (r & 3) == 0 ? l4.x : (r & 3) == 1 ? l4.y : (r & 3) == 2 ? l4.z : l4.w;
+              const bool ok = i < cend && (!causal || j <= i);
+              tsum += ok ? __builtin_amdgcn_exp2f(fmaf(acc[r], scale_log2, -L)) : 0.f;
+            }
           }
           colsum[ks] += tsum;
         }
