@@ -40,6 +40,9 @@ if ROOT not in sys.path:
 METRIC = "tokens/sec of pruned layer-stack forward vs keep_rate (1 GPU) + roofline %"
 PEAK_BF16_TFLOPS = 2500.0
 PEAK_HBM_GBS = 8000.0
+# exp throughput: v_exp_f32 is a quarter-rate VALU op, so a wave64 takes 16
+# cycles: 256 CUs x 4 SIMDs x 4 exp per clock x 2.4 GHz
+PEAK_EXP_PER_S = 256 * 4 * 4 * 2.4e9
 HEADLINE_RATE = 0.5
 
 
@@ -452,6 +455,16 @@ def main():
                            "peak": peak}
     for v in per_class.values():
         v["frac"] = round(v["achieved"] / v["peak"], 4)
+    # attention and the score sweep take one exp per (query, key, head) pair:
+    # their second bound is the exp rate
+    hd = p.d_model // p.n_heads
+    for name, flop_per_exp in (("attention", 4 * hd), ("score", 2 * hd)):
+        if name in per_class:
+            t = head["classes"][name]["ms"] * 1e-3
+            rate = head["work"][name][1] / flop_per_exp / t
+            per_class[name]["exp_bound"] = {"achieved_exp_per_s": float(f"{rate:.4g}"),
+                                            "peak_exp_per_s": PEAK_EXP_PER_S,
+                                            "frac": round(rate / PEAK_EXP_PER_S, 4)}
 
     # the paper's every-layer schedule on a GPT-2-small-shaped causal stack
     others = {}

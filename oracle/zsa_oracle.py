@@ -29,6 +29,15 @@ constants the paper leaves open (eps = 1e-5, RoPE theta = 1e4 with
 rotate-half pairing (i, i + hd/2), SwiGLU gate/up rows interleaved) are
 readings shared with the library's documented interface.
 
+Grouped-query attention (the LLaMA 3 / Gemma 2 backbones of Table 1):
+query head h reads key/value head h // (H / H_kv); H_kv = H is ordinary
+multi-head attention and H_kv = 1 multi-query attention. The score still
+sums the soft-score matrices of all H query heads.
+
+``force_keep_last`` (a reading for generation, where the first new token is
+predicted from the last input row): that row is always kept and the other
+k - 1 rows are chosen by score as above.
+
 ``mode="exact"`` keeps everything in float64. ``mode="bf16"`` rounds to
 bfloat16 (nearest-even) exactly where the GPU path stores bfloat16: norm
 outputs, Q/K/V (after RoPE), attention output, MLP intermediate and the
@@ -159,18 +168,24 @@ def rope(x: np.ndarray, pos: np.ndarray, n_heads: int, theta: float) -> np.ndarr
 # Eq. 1 attention and the soft-score contribution of each position
 # ---------------------------------------------------------------------------
 def attention(q: np.ndarray, k: np.ndarray, v: np.ndarray, pos: np.ndarray, n_heads: int,
-              causal: bool, want_scores: bool = True):
+              causal: bool, want_scores: bool = True, n_kv_heads: Optional[int] = None):
     """Eq. 1 for one sequence, per head, plus the column sums of the
     soft-score matrix (Sec. 3.2-3.3).
 
-    q, k, v: [n, n_heads*hd]. pos: [n] original positions; under the causal
-    mask, row i may attend to row j iff pos[j] <= pos[i].
+    q: [n, n_heads*hd]; k, v: [n, n_kv_heads*hd] (n_kv_heads divides
+    n_heads; None means n_heads), query head h reading key/value head
+    h // (n_heads // n_kv_heads). pos: [n] original positions; under the
+    causal mask, row i may attend to row j iff pos[j] <= pos[i].
     Returns (o [n, d], lse [n_heads, n], s [n] or None) where lse is the
     natural-log log-sum-exp of each scaled, masked score row and
     s[j] = sum_h sum_i P_h[i, j].
     """
     n, d = q.shape
     hd = d // n_heads
+    hkv = n_heads if n_kv_heads is None else int(n_kv_heads)
+    if hkv <= 0 or n_heads % hkv != 0 or k.shape[1] != hkv * hd or v.shape[1] != hkv * hd:
+        raise ValueError("key/value heads do not divide the query heads")
+    group = n_heads // hkv
     scale = 1.0 / math.sqrt(hd)
     o = np.zeros((n, d))
     lse = np.zeros((n_heads, n))
@@ -180,30 +195,36 @@ def attention(q: np.ndarray, k: np.ndarray, v: np.ndarray, pos: np.ndarray, n_he
     future = pos[None, :] > pos[:, None]      # [i, j]: j is after i
     for h in range(n_heads):
         cols = slice(h * hd, (h + 1) * hd)
-        S = (q[:, cols] @ k[:, cols].T) * scale
+        kv = slice((h // group) * hd, (h // group + 1) * hd)
+        S = (q[:, cols] @ k[:, kv].T) * scale
         if causal:
             S = np.where(future, -np.inf, S)   # M of Eq. 1
         row_max = S.max(axis=1, keepdims=True)
         E = np.exp(S - row_max)
         Z = E.sum(axis=1, keepdims=True)
         P = E / Z                               # the soft-score matrix of head h
-        o[:, cols] = P @ v[:, cols]
+        o[:, cols] = P @ v[:, kv]
         lse[h] = row_max[:, 0] + np.log(Z[:, 0])
         if want_scores:
             s += P.sum(axis=0)                  # weight each V row receives
     return o, lse, s
 
 
-def select_topk(s: np.ndarray, k: int) -> np.ndarray:
+def select_topk(s: np.ndarray, k: int, keep_last: bool = False) -> np.ndarray:
     """Indices of the k highest scores, ties going to the lower index
     (total order: score descending, then index ascending), returned in
-    ascending index order. -0.0 and +0.0 compare equal. NaN is rejected."""
+    ascending index order. -0.0 and +0.0 compare equal. NaN is rejected.
+    With ``keep_last`` the last index is always kept (if k >= 1) and the
+    other k - 1 are the highest of the remaining scores."""
     s = np.asarray(s, dtype=np.float64)
     if np.isnan(s).any():
         raise ValueError("NaN score")
     n = s.shape[0]
     if not (0 <= k <= n):
         raise ValueError("k out of range")
+    if keep_last and 1 <= k < n:
+        rest = select_topk(s[:n - 1], k - 1)
+        return np.concatenate([rest, [n - 1]]).astype(np.int64)
     idx = np.arange(n)
     order = np.lexsort((idx, -s))              # primary -s, secondary index
     return np.sort(order[:k])
@@ -222,6 +243,12 @@ class LayerCfg:
     norm_eps: float = 1e-5
     rope_theta: float = 10000.0
     tau: int = 5
+    n_kv_heads: int = 0          # key/value heads (0: n_heads)
+    force_keep_last: bool = False
+
+    @property
+    def kv_heads(self) -> int:
+        return self.n_heads if self.n_kv_heads == 0 else self.n_kv_heads
 
 
 def _linear(x, w, b):
@@ -242,12 +269,13 @@ def sequence_layer(x: np.ndarray, pos: np.ndarray, w: Dict[str, Optional[np.ndar
     else:
         h = r(rms_norm(x, w["norm1_w"], cfg.norm_eps))
     qkv = _linear(h, w["w_qkv"], w["b_qkv"])
-    q, k, v = qkv[:, :d], qkv[:, d:2 * d], qkv[:, 2 * d:]
+    kvd = cfg.kv_heads * (d // cfg.n_heads)
+    q, k, v = qkv[:, :d], qkv[:, d:d + kvd], qkv[:, d + kvd:d + 2 * kvd]
     if cfg.kind == DECODER:
         q = rope(q, pos, cfg.n_heads, cfg.rope_theta)
-        k = rope(k, pos, cfg.n_heads, cfg.rope_theta)
+        k = rope(k, pos, cfg.kv_heads, cfg.rope_theta)
     q, k, v = r(q), r(k), r(v)
-    o, lse, s = attention(q, k, v, pos, cfg.n_heads, cfg.causal, want_scores)
+    o, lse, s = attention(q, k, v, pos, cfg.n_heads, cfg.causal, want_scores, cfg.kv_heads)
     o = r(o)
     x1 = r(x + _linear(o, w["w_o"], w["b_o"]))
     if cfg.kind == ENCODER:
@@ -289,7 +317,7 @@ def layer_forward(x: np.ndarray, pos: np.ndarray, cu: Sequence[int], w: Dict,
             if kept_override is not None:
                 kept = np.asarray(kept_override[b], dtype=np.int64)
             else:
-                kept = select_topk(res["scores"], kb)
+                kept = select_topk(res["scores"], kb, cfg.force_keep_last)
             ss.append(res["scores"])
             ks.append(kb)
             kept_all.append(kept + lo)

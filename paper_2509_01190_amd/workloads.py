@@ -61,10 +61,16 @@ class Preset:
     rate_hi: float = 1.0
     norm_eps: float = 1e-5
     rope_theta: float = 10000.0
+    n_kv_heads: int = 0       # key/value heads (grouped-query attention); 0: n_heads
+    force_keep_last: bool = False
 
     @property
     def head_dim(self) -> int:
         return self.d_model // self.n_heads
+
+    @property
+    def kv_heads(self) -> int:
+        return self.n_heads if self.n_kv_heads == 0 else self.n_kv_heads
 
 
 PRESETS: Dict[str, Preset] = {
@@ -148,13 +154,15 @@ def layer_weights(p: Preset, layer: int, seed: int = 0, norm_jitter: bool = Fals
                   zero_wq: bool = False) -> Dict[str, Optional[np.ndarray]]:
     """Weights of one layer (PyTorch Linear layout [out, in], float32).
 
-    w_qkv rows are [q; k; v], each d_model rows with head h at rows
-    h*head_dim .. (h+1)*head_dim. For the decoder, w_up has 2*d_ff rows that
+    w_qkv rows are [q; k; v]: d_model query rows, then kv_heads*head_dim key
+    rows and as many value rows, head h at rows h*head_dim ..
+    (h+1)*head_dim of its block. For the decoder, w_up has 2*d_ff rows that
     interleave gate and up projections: row 2f is gate f, row 2f+1 is up f.
     ``zero_wq`` zeroes the query rows (and their bias): every query is then
     the zero vector, which makes attention exactly uniform.
     """
     d, f = p.d_model, p.d_ff
+    qkv = d + 2 * p.kv_heads * p.head_dim
 
     def normal(name, shape, std=0.02):
         return (_rng(seed, layer, _TID[name]).standard_normal(shape, dtype=np.float32)
@@ -174,8 +182,8 @@ def layer_weights(p: Preset, layer: int, seed: int = 0, norm_jitter: bool = Fals
     if p.kind == ENCODER:
         w["norm1_w"] = gain("norm1_w", (d,))
         w["norm1_b"] = shift("norm1_b", (d,))
-        w["w_qkv"] = normal("w_qkv", (3 * d, d))
-        w["b_qkv"] = normal("b_qkv", (3 * d,))
+        w["w_qkv"] = normal("w_qkv", (qkv, d))
+        w["b_qkv"] = normal("b_qkv", (qkv,))
         w["w_o"] = normal("w_o", (d, d))
         w["b_o"] = normal("b_o", (d,))
         w["norm2_w"] = gain("norm2_w", (d,))
@@ -187,7 +195,7 @@ def layer_weights(p: Preset, layer: int, seed: int = 0, norm_jitter: bool = Fals
     else:
         w["norm1_w"] = gain("norm1_w", (d,))
         w["norm1_b"] = None
-        w["w_qkv"] = normal("w_qkv", (3 * d, d))
+        w["w_qkv"] = normal("w_qkv", (qkv, d))
         w["b_qkv"] = None
         w["w_o"] = normal("w_o", (d, d))
         w["b_o"] = None

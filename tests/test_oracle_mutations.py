@@ -13,12 +13,13 @@ from oracle import zsa_oracle as O
 from tests import test_oracle_pins as P
 
 
-def _attention_no_scale(q, k, v, pos, n_heads, causal, want_scores=True):
+def _attention_no_scale(q, k, v, pos, n_heads, causal, want_scores=True, n_kv_heads=None):
     return _orig_attention(q * math.sqrt(q.shape[1] // n_heads), k, v, pos, n_heads, causal,
-                           want_scores)
+                           want_scores, n_kv_heads)
 
 
-def _attention_mask_excludes_diagonal(q, k, v, pos, n_heads, causal, want_scores=True):
+def _attention_mask_excludes_diagonal(q, k, v, pos, n_heads, causal, want_scores=True,
+                                      n_kv_heads=None):
     return _attention_shifted(q, k, v, pos, n_heads, want_scores)
 
 
@@ -42,14 +43,26 @@ def _attention_shifted(q, k, v, pos, n_heads, want_scores):
     return o, lse, s
 
 
-def _attention_row_sums(q, k, v, pos, n_heads, causal, want_scores=True):
-    o, lse, s = _orig_attention(q, k, v, pos, n_heads, causal, want_scores)
+def _attention_row_sums(q, k, v, pos, n_heads, causal, want_scores=True, n_kv_heads=None):
+    o, lse, s = _orig_attention(q, k, v, pos, n_heads, causal, want_scores, n_kv_heads)
     if s is not None:
         s = np.full_like(s, float(n_heads))   # what summing each row (axis 1) gives
     return o, lse, s
 
 
-def _select_ties_high(s, k):
+def _attention_kv_modulo(q, k, v, pos, n_heads, causal, want_scores=True, n_kv_heads=None):
+    # query head h reads key/value head h % H_kv instead of h // (H / H_kv)
+    hkv = n_heads if n_kv_heads is None else n_kv_heads
+    hd = q.shape[1] // n_heads
+    idx = np.concatenate([np.arange((h % hkv) * hd, (h % hkv + 1) * hd) for h in range(n_heads)])
+    return _orig_attention(q, k[:, idx], v[:, idx], pos, n_heads, causal, want_scores)
+
+
+def _select_ignores_keep_last(s, k, keep_last=False):
+    return _orig_select(s, k)
+
+
+def _select_ties_high(s, k, keep_last=False):
     s = np.asarray(s, dtype=np.float64)
     idx = np.arange(s.shape[0])
     order = np.lexsort((-idx, -s))
@@ -91,13 +104,16 @@ def _bf16_truncate(x):
 
 
 _orig_attention = O.attention
+_orig_select = O.select_topk
 
 MUTANTS = [
     ("attention", _attention_no_scale, lambda: P.test_attention_brute_force(False)),
     ("attention", _attention_mask_excludes_diagonal, lambda: P.test_attention_brute_force(True)),
     ("attention", _attention_row_sums,
      lambda: P.test_scores_closed_form_uniform_attention(P.W.DECODER)),
+    ("attention", _attention_kv_modulo, lambda: P.test_gqa_vs_torch_sdpa(True, 2)),
     ("select_topk", _select_ties_high, P.test_select_topk_brute_force),
+    ("select_topk", _select_ignores_keep_last, P.test_select_topk_keep_last),
     ("keep_count", _keep_count_round, P.test_keep_schedule_golden),
     ("rope", _rope_adjacent, P.test_rope_hand_example),
     ("layer_norm", _layer_norm_unbiased, P.test_layer_norm_vs_torch),

@@ -6,6 +6,7 @@ invariants, and independent library routines (torch CPU float64). They are
 chosen so that a dropped term, a wrong sign or index, a transposed operand or
 a wrong mask in the oracle fails at least one of them.
 """
+import dataclasses
 import itertools
 import json
 import math
@@ -191,6 +192,30 @@ def test_attention_brute_force(causal):
     assert np.allclose(s, bs, rtol=1e-12, atol=1e-12)
 
 
+@pytest.mark.parametrize("hkv", [1, 2, 3, 6])
+@pytest.mark.parametrize("causal", [False, True])
+def test_gqa_vs_torch_sdpa(causal, hkv):
+    # grouped-query attention against torch's float64 SDPA (enable_gqa: query
+    # head h reads key/value head h // (H / H_kv)); scores and LSE from torch
+    # on the key/value heads repeated to H
+    g = np.random.default_rng(40 + hkv + 10 * causal)
+    n, H, hd = 23, 6, 8
+    q = g.standard_normal((n, H * hd)) * 2.0
+    k = g.standard_normal((n, hkv * hd))
+    v = g.standard_normal((n, hkv * hd))
+    o, lse, s = O.attention(q, k, v, np.arange(n), H, causal, True, hkv)
+    tq = torch.from_numpy(q).view(n, H, hd).transpose(0, 1).contiguous()
+    tk, tv = (torch.from_numpy(a).view(n, hkv, hd).transpose(0, 1).contiguous() for a in (k, v))
+    ref = F.scaled_dot_product_attention(tq, tk, tv, is_causal=causal, enable_gqa=True)
+    assert np.allclose(o, ref.transpose(0, 1).reshape(n, H * hd).numpy(), rtol=1e-11, atol=1e-12)
+    kk = tk.repeat_interleave(H // hkv, dim=0)
+    logits = (tq @ kk.transpose(1, 2)) / math.sqrt(hd)
+    if causal:
+        logits = logits.masked_fill(torch.ones(n, n, dtype=torch.bool).triu(1), float("-inf"))
+    assert np.allclose(lse, torch.logsumexp(logits, dim=-1).numpy(), rtol=1e-12, atol=1e-12)
+    assert np.allclose(s, torch.softmax(logits, dim=-1).sum(dim=(0, 1)).numpy(), rtol=1e-12)
+
+
 @pytest.mark.parametrize("causal", [False, True])
 def test_attention_vs_torch_sdpa(causal):
     g = np.random.default_rng(12)
@@ -281,6 +306,25 @@ def test_select_topk_brute_force():
             assert got == _brute_topk(list(vals), k), (vals, k)
 
 
+def test_select_topk_keep_last():
+    # the last row is always kept; the rest is the plain top-k (pinned by
+    # brute force above) when that already holds the last row, else the
+    # plain top-(k-1)
+    g = np.random.default_rng(21)
+    for _ in range(150):
+        n = int(g.integers(1, 11))
+        s = g.integers(0, 4, n).astype(np.float64)
+        for k in range(n + 1):
+            got = O.select_topk(s, k, keep_last=True)
+            assert len(got) == k and np.all(np.diff(got) > 0)
+            if k == 0:
+                continue
+            assert got[-1] == n - 1
+            plain = _brute_topk(s, k)
+            want = set(plain) if (n - 1) in set(plain) else set(_brute_topk(s, k - 1)) | {n - 1}
+            assert set(got.tolist()) == want
+
+
 def test_select_topk_reject_nan():
     with pytest.raises(ValueError):
         O.select_topk(np.array([1.0, np.nan]), 1)
@@ -320,9 +364,12 @@ def test_encoder_layer_vs_torch_transformer_layer():
     assert np.allclose(got, ref, rtol=1e-10, atol=1e-10)
 
 
-def test_decoder_layer_vs_torch_composition():
-    # RMSNorm, causal SDPA and SiLU from torch; RoPE from the oracle (pinned above)
-    p = W.shrink(W.PRESETS["tiny"], kind=W.DECODER, causal=True, n_layers=1, batch=1, seq_len=21)
+@pytest.mark.parametrize("hkv", [4, 2, 1])
+def test_decoder_layer_vs_torch_composition(hkv):
+    # RMSNorm, causal SDPA (grouped-query when hkv < H) and SiLU from torch;
+    # RoPE from the oracle (pinned above)
+    p = W.shrink(W.PRESETS["tiny"], kind=W.DECODER, causal=True, n_layers=1, batch=1, seq_len=21,
+                 n_kv_heads=hkv)
     w = {k: (None if v is None else v.astype(np.float64))
          for k, v in W.layer_weights(p, 0, 5, norm_jitter=True).items()}
     w["w_qkv"] *= 25.0
@@ -334,16 +381,18 @@ def test_decoder_layer_vs_torch_composition():
     t = torch.from_numpy
     h = F.rms_norm(t(x), (d,), t(w["norm1_w"]), 1e-5)
     qkv = h @ t(w["w_qkv"]).T
+    kvd = hkv * hd
     q = t(O.rope(qkv[:, :d].numpy(), pos, H, 1e4))
-    k = t(O.rope(qkv[:, d:2 * d].numpy(), pos, H, 1e4))
-    v = qkv[:, 2 * d:]
-    heads = lambda a: a.view(n, H, hd).transpose(0, 1).contiguous()
-    o = F.scaled_dot_product_attention(heads(q), heads(k), heads(v), is_causal=True)
+    k = t(O.rope(qkv[:, d:d + kvd].numpy(), pos, hkv, 1e4))
+    v = qkv[:, d + kvd:]
+    heads = lambda a, m: a.reshape(n, m, hd).transpose(0, 1).contiguous()
+    o = F.scaled_dot_product_attention(heads(q, H), heads(k, hkv), heads(v, hkv), is_causal=True,
+                                       enable_gqa=True)
     x1 = t(x) + o.transpose(0, 1).reshape(n, d) @ t(w["w_o"]).T
     h2 = F.rms_norm(x1, (d,), t(w["norm2_w"]), 1e-5)
     z = h2 @ t(w["w_up"]).T
     ref = (x1 + (F.silu(z[:, 0::2]) * z[:, 1::2]) @ t(w["w_down"]).T).numpy()
-    cfg = O.LayerCfg(W.DECODER, d, H, Fd, True)
+    cfg = O.LayerCfg(W.DECODER, d, H, Fd, True, n_kv_heads=hkv)
     got = O.sequence_layer(x, pos, w, cfg)["x"]
     assert np.allclose(got, ref, rtol=1e-10, atol=1e-10)
 
@@ -452,3 +501,18 @@ def test_bf16_mode_rounds_storage_points():
     ex = O.sequence_layer(x, pos, ws[0], cfg, "exact")["x"]
     assert not np.array_equal(ex, res["x"])
     assert np.allclose(ex, res["x"], rtol=0.05, atol=0.05)
+
+
+def test_stack_force_keep_last_keeps_every_last_row():
+    # every-layer schedule down to tau: the last input row of every sequence
+    # survives every pruning point, and each point keeps the Eq. 2 count
+    lens = [40, 9, 23]
+    x, pos, cu, ws, cfg = _stack_inputs(W.DECODER, lens, 7, n_layers=4)
+    cfg = dataclasses.replace(cfg, force_keep_last=True)
+    out = O.stack_forward(x, pos, cu, ws, cfg, (1, 2, 3, 4), [0.3, 0.5, 0.2])
+    for pt in out["points"]:
+        c = pt["cu"]
+        for b, n in enumerate(lens):
+            assert pt["pos"][c[b + 1] - 1] == n - 1
+    sched = O.keep_schedule(lens, [0.3, 0.5, 0.2], cfg.tau, 4)
+    assert [list(pt["k"]) for pt in out["points"]] == [list(r) for r in sched]
