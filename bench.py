@@ -54,7 +54,7 @@ def parse():
     ap.add_argument("--workload", default="bert")
     ap.add_argument("--keep-rates", default=None, help="comma-separated sweep")
     ap.add_argument("--seed", type=int, default=0)
-    ap.add_argument("--also", default="gpt2,gpt2_n128,gpt2_n1024",
+    ap.add_argument("--also", default="gpt2,gpt2_n128,gpt2_n1024,llama3_8b",
                     help="comma-separated presets whose keep-rate sweeps are reported beside "
                          "the headline workload")
     ap.add_argument("--no-graph", action="store_true", help="time eager launches instead")
@@ -145,6 +145,11 @@ def measured_traffic():
     return t.get("hbm_bytes_per_projection")
 
 
+def qkv_n(p):
+    """Output width of the fused [q | k | v] projection."""
+    return p.d_model + 2 * p.kv_heads * (p.d_model // p.n_heads)
+
+
 def gemm_flops(p, rows_in, rows_after):
     """Algorithmic FLOPs of the projections of each layer: 2 * M * N * K,
     with M the rows the GEMM processes (the pruned rows after the pruning
@@ -154,7 +159,7 @@ def gemm_flops(p, rows_in, rows_after):
     total = 0
     for l in range(p.n_layers):
         t_in, t_out = rows_in[l], rows_after[l]
-        total += 2 * t_in * 3 * d * d          # QKV
+        total += 2 * t_in * qkv_n(p) * d       # QKV (fused; grouped-query k/v)
         total += 2 * t_out * d * d             # output projection
         total += 2 * t_out * up_n * d          # up (or gate|up)
         total += 2 * t_out * d * F             # down
@@ -173,7 +178,7 @@ def gemm_bytes(p, results, rates):
         rows_in, rows_after = results[r]["rows"]
         for l in range(p.n_layers):
             t_in, t_out = rows_in[l], rows_after[l]
-            total += e * (t_in * d + 3 * d * d + t_in * 3 * d)                  # QKV
+            total += e * (t_in * d + qkv_n(p) * d + t_in * qkv_n(p))            # QKV
             total += e * (t_out * d + d * d + 2 * t_out * d)                    # O + residual
             total += e * (t_out * d + up_n * d + t_out * up_out)                # up
             total += e * (t_out * F + d * F + 2 * t_out * d)                    # down + residual
@@ -274,7 +279,8 @@ def measure(p, rates, args, torch, W, zsa, dev, timing):
     dws = [{k: (None if v is None else W.to_storage(v, p.dtype).to(dev)) for k, v in w.items()}
            for w in ws_np]
     cfg = zsa.make_cfg(p.kind, p.d_model, p.n_heads, p.d_ff, p.causal,
-                       zsa.BF16 if p.dtype == "bf16" else zsa.F32, p.tau, p.norm_eps, p.rope_theta)
+                       zsa.BF16 if p.dtype == "bf16" else zsa.F32, p.tau, p.norm_eps, p.rope_theta,
+                       p.n_kv_heads, p.force_keep_last)
     stack = zsa.Stack(cfg, dws)
     seqs = zsa.Seqs(lens, dev)
     xd = W.to_storage(x_np, p.dtype).to(dev)
@@ -380,8 +386,10 @@ def describe(p):
         where = "after every layer"
     else:
         where = "after layers " + "/".join(map(str, p.prune_after))
-    return (f"{p.name}: {p.n_layers}-layer {mask} {kind} d{p.d_model} H{p.n_heads} FFN{p.d_ff}, "
-            f"{p.batch}x{p.seq_len} rows, pruned {where} (tau {p.tau})")
+    heads = f"H{p.n_heads}" + (f"/KV{p.kv_heads}" if p.kv_heads != p.n_heads else "")
+    last = ", last row always kept" if p.force_keep_last else ""
+    return (f"{p.name}: {p.n_layers}-layer {mask} {kind} d{p.d_model} {heads} FFN{p.d_ff}, "
+            f"{p.batch}x{p.seq_len} rows, pruned {where} (tau {p.tau}){last}")
 
 
 def main():

@@ -97,11 +97,19 @@ typedef struct zsa_layer_cfg {
   int32_t tau;        /* floor of Eq. 2 (the paper fixes it at 5, Sec. 4.2) */
   float norm_eps;     /* LayerNorm / RMSNorm epsilon */
   float rope_theta;   /* rotary base (decoder) */
+  int32_t n_kv_heads; /* key/value heads, dividing n_heads (grouped-query
+                         attention of the LLaMA 3 / Gemma 2 backbones, Table 1);
+                         0 means n_heads, 1 is multi-query attention */
+  int32_t force_keep_last; /* nonzero: every pruning point keeps the last row
+                              of each sequence (the row the first generated
+                              token is predicted from) and chooses the other
+                              k - 1 rows by score */
 } zsa_layer_cfg;
 
 /* Weights of one block, device pointers in the storage dtype, PyTorch
  * Linear layout [out, in] (row-major, the input dimension contiguous).
- *   w_qkv  [3d, d]  rows q | k | v, head h at rows h*hd .. h*hd+hd-1 of each
+ *   w_qkv  [d + 2*kv*hd, d]  rows q (d) | k (kv*hd) | v (kv*hd), head h at
+ *          rows h*hd .. h*hd+hd-1 of its block (kv = key/value heads)
  *   w_o    [d, d]
  *   w_up   encoder [F, d]; decoder [2F, d] with row 2f = gate f, 2f+1 = up f
  *   w_down [d, F]
@@ -171,8 +179,11 @@ size_t zsa_linear_workspace_size(int32_t dtype, int32_t m, int32_t n, int32_t k)
  *     scores[j] = sum over heads h, query rows i of P_h[i, j],
  * P_h = softmax(Q_h K_h^T * scale + M) the normalised soft-score matrix.
  * P is never written to memory.
- *   q, k, v  device, dtype; row r of head h starts at q + r*row_stride + h*hd
- *            (same for k and v); row_stride in elements
+ *   q, k, v  device, dtype; row r of query head h starts at
+ *            q + r*row_stride + h*hd, row r of key/value head g at
+ *            k + r*row_stride + g*hd (and v); row_stride in elements
+ *   n_kv_heads  key/value heads (divides n_heads; 0 means n_heads): query
+ *            head h reads key/value head h / (n_heads / n_kv_heads)
  *   out      [T, n_heads*hd] dtype, row stride out_stride (elements)
  *   lse      [n_heads, T] fp32: natural-log log-sum-exp of each scaled,
  *            masked score row; NULL if not wanted
@@ -185,9 +196,9 @@ size_t zsa_linear_workspace_size(int32_t dtype, int32_t m, int32_t n, int32_t k)
  */
 int zsa_attention_with_scores(void* stream, int32_t dtype, const void* q, const void* k,
                               const void* v, int64_t row_stride, int32_t n_heads,
-                              int32_t head_dim, int32_t causal, float scale, int32_t batch,
-                              const int32_t* cu_host, const int32_t* cu_dev, void* out,
-                              int64_t out_stride, float* lse, float* scores, void* ws,
+                              int32_t n_kv_heads, int32_t head_dim, int32_t causal, float scale,
+                              int32_t batch, const int32_t* cu_host, const int32_t* cu_dev,
+                              void* out, int64_t out_stride, float* lse, float* scores, void* ws,
                               size_t ws_bytes);
 size_t zsa_attention_workspace_size(int32_t n_heads, int32_t total_rows, int32_t want_scores);
 
@@ -197,9 +208,10 @@ size_t zsa_attention_workspace_size(int32_t n_heads, int32_t total_rows, int32_t
  * reduction order, no atomics). Arguments as in zsa_attention_with_scores;
  * lse [n_heads, T] fp32 device. ws >= zsa_score_workspace_size(n_heads, T). */
 int zsa_score_positions(void* stream, int32_t dtype, const void* q, const void* k,
-                        int64_t row_stride, const float* lse, int32_t n_heads, int32_t head_dim,
-                        int32_t causal, float scale, int32_t batch, const int32_t* cu_host,
-                        const int32_t* cu_dev, float* scores, void* ws, size_t ws_bytes);
+                        int64_t row_stride, const float* lse, int32_t n_heads,
+                        int32_t n_kv_heads, int32_t head_dim, int32_t causal, float scale,
+                        int32_t batch, const int32_t* cu_host, const int32_t* cu_dev,
+                        float* scores, void* ws, size_t ws_bytes);
 size_t zsa_score_workspace_size(int32_t n_heads, int32_t total_rows);
 
 /* ---------------------------------------------------------------------
@@ -209,11 +221,13 @@ size_t zsa_score_workspace_size(int32_t n_heads, int32_t total_rows);
  * [sum k] device int32, the global row ids (into the packed input) of the
  * kept rows, sequence by sequence, ascending within each sequence.
  *   scores [T] fp32 device; k_host [batch] host, 0 <= k_host[b] <= n_b
+ *   force_keep_last  nonzero: the last row of every sequence is kept
+ *            (when k_host[b] >= 1) and the other k - 1 are chosen by score
  *   ws >= zsa_select_workspace_size(batch)
  */
 int zsa_select_topk(void* stream, const float* scores, int32_t batch, const int32_t* cu_host,
-                    const int32_t* cu_dev, const int32_t* k_host, int32_t* kept_rows, void* ws,
-                    size_t ws_bytes);
+                    const int32_t* cu_dev, const int32_t* k_host, int32_t force_keep_last,
+                    int32_t* kept_rows, void* ws, size_t ws_bytes);
 size_t zsa_select_workspace_size(int32_t batch);
 
 /* Compaction after pruning (Sec. 3.3: pruned rows take no part in later

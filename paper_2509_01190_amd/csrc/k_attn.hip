@@ -1,4 +1,5 @@
-// Attention of Eq. 1, softmax(Q K^T * scale + M) V, per sequence and head,
+// Attention of Eq. 1, softmax(Q K^T * scale + M) V, per sequence and head
+// (query head h reads key/value head h / kv_group: grouped-query attention),
 // over packed variable-length rows; also writes the natural-log
 // log-sum-exp of every score row (used by the contribution scores).
 //
@@ -37,7 +38,7 @@ __device__ __forceinline__ uint32_t bf16_at(const uint4& v, int e) {
 template <int HD>
 __global__ __launch_bounds__(256) void attn_mfma_kernel(
     const bf16_t* __restrict__ Q, const bf16_t* __restrict__ K, const bf16_t* __restrict__ V,
-    int64_t rs, int causal, float scale_log2, const int32_t* __restrict__ cu,
+    int64_t rs, int kv_group, int causal, float scale_log2, const int32_t* __restrict__ cu,
     bf16_t* __restrict__ O, int64_t os, float* __restrict__ lse, int T) {
   constexpr int BQ = 128, BKEY = 64;
   constexpr int KLD = HD + 8;    // K tile row stride (bf16)
@@ -74,8 +75,10 @@ __global__ __launch_bounds__(256) void attn_mfma_kernel(
   // current block is computed; LDS is double-buffered, one barrier per block.
   // Keys past the sequence repeat the last row: they are masked to
   // probability 0 and the repeated V rows are finite.
-  const bf16_t* kbase = K + static_cast<int64_t>(lo) * rs + h * HD;
-  const bf16_t* vbase = V + static_cast<int64_t>(lo) * rs + h * HD;
+  // grouped-query attention: query head h reads key/value head h / kv_group
+  const int hk = h / kv_group;
+  const bf16_t* kbase = K + static_cast<int64_t>(lo) * rs + hk * HD;
+  const bf16_t* vbase = V + static_cast<int64_t>(lo) * rs + hk * HD;
   u32x4 kreg[KCH], vreg[VPR][2];
   auto load_tile = [&](int j0) {
 #pragma unroll
@@ -234,7 +237,7 @@ template <typename T, int HD>
 __global__ __launch_bounds__(64) void attn_valu_kernel(const T* __restrict__ Q,
                                                        const T* __restrict__ K,
                                                        const T* __restrict__ V, int64_t rs,
-                                                       int causal, float scale,
+                                                       int kv_group, int causal, float scale,
                                                        const int32_t* __restrict__ cu,
                                                        T* __restrict__ O, int64_t os,
                                                        float* __restrict__ lse, int Tn) {
@@ -260,8 +263,8 @@ __global__ __launch_bounds__(64) void attn_valu_kernel(const T* __restrict__ Q,
     for (int e = threadIdx.x; e < BKEY * HD; e += 64) {
       const int r = e / HD, c = e % HD;
       const int j = j0 + r;
-      Ks[r][c] = j < n ? to_f32(K[static_cast<int64_t>(lo + j) * rs + h * HD + c]) : 0.f;
-      Vs[r][c] = j < n ? to_f32(V[static_cast<int64_t>(lo + j) * rs + h * HD + c]) : 0.f;
+      Ks[r][c] = j < n ? to_f32(K[static_cast<int64_t>(lo + j) * rs + (h / kv_group) * HD + c]) : 0.f;
+      Vs[r][c] = j < n ? to_f32(V[static_cast<int64_t>(lo + j) * rs + (h / kv_group) * HD + c]) : 0.f;
     }
     __syncthreads();
     if (active) {
@@ -297,7 +300,7 @@ __global__ __launch_bounds__(64) void attn_valu_kernel(const T* __restrict__ Q,
 
 template <typename T>
 hipError_t valu_dispatch(hipStream_t s, const void* q, const void* k, const void* v, int64_t rs,
-                         int H, int hd, int causal, float scale, int B, int max_len, int Trows,
+                         int H, int kvg, int hd, int causal, float scale, int B, int max_len, int Trows,
                          const int32_t* cu, void* out, int64_t os, float* lse) {
   const dim3 grid((max_len + 63) / 64, H, B), block(64);
   const T* qp = static_cast<const T*>(q);
@@ -305,10 +308,10 @@ hipError_t valu_dispatch(hipStream_t s, const void* q, const void* k, const void
   const T* vp = static_cast<const T*>(v);
   T* op = static_cast<T*>(out);
   switch (hd) {
-    case 16: return launch(K_ATTENTION, attn_valu_kernel<T, 16>, grid, block, 0, s, qp, kp, vp, rs, causal, scale, cu, op, os, lse, Trows);
-    case 32: return launch(K_ATTENTION, attn_valu_kernel<T, 32>, grid, block, 0, s, qp, kp, vp, rs, causal, scale, cu, op, os, lse, Trows);
-    case 64: return launch(K_ATTENTION, attn_valu_kernel<T, 64>, grid, block, 0, s, qp, kp, vp, rs, causal, scale, cu, op, os, lse, Trows);
-    case 128: return launch(K_ATTENTION, attn_valu_kernel<T, 128>, grid, block, 0, s, qp, kp, vp, rs, causal, scale, cu, op, os, lse, Trows);
+    case 16: return launch(K_ATTENTION, attn_valu_kernel<T, 16>, grid, block, 0, s, qp, kp, vp, rs, kvg, causal, scale, cu, op, os, lse, Trows);
+    case 32: return launch(K_ATTENTION, attn_valu_kernel<T, 32>, grid, block, 0, s, qp, kp, vp, rs, kvg, causal, scale, cu, op, os, lse, Trows);
+    case 64: return launch(K_ATTENTION, attn_valu_kernel<T, 64>, grid, block, 0, s, qp, kp, vp, rs, kvg, causal, scale, cu, op, os, lse, Trows);
+    case 128: return launch(K_ATTENTION, attn_valu_kernel<T, 128>, grid, block, 0, s, qp, kp, vp, rs, kvg, causal, scale, cu, op, os, lse, Trows);
     default: return hipErrorInvalidValue;
   }
 }
@@ -316,9 +319,9 @@ hipError_t valu_dispatch(hipStream_t s, const void* q, const void* k, const void
 }  // namespace
 
 hipError_t launch_attention(hipStream_t s, int dtype, const void* q, const void* k,
-                            const void* v, int64_t row_stride, int H, int hd, int causal,
-                            float scale, int B, int max_len, int T, const int32_t* cu_dev,
-                            void* out, int64_t out_stride, float* lse) {
+                            const void* v, int64_t row_stride, int H, int kv_group, int hd,
+                            int causal, float scale, int B, int max_len, int T,
+                            const int32_t* cu_dev, void* out, int64_t out_stride, float* lse) {
   if (B == 0 || max_len == 0) return hipSuccess;
   if (dtype == 1 && (hd == 64 || hd == 128)) {
     const dim3 grid((max_len + 127) / 128, H, B), block(256);
@@ -329,15 +332,15 @@ hipError_t launch_attention(hipStream_t s, int dtype, const void* q, const void*
     const float sl = scale * kLog2e;
     if (hd == 64)
       return launch(K_ATTENTION, attn_mfma_kernel<64>, grid, block, 0, s, qp, kp, vp, row_stride,
-                    causal, sl, cu_dev, op, out_stride, lse, T);
+                    kv_group, causal, sl, cu_dev, op, out_stride, lse, T);
     return launch(K_ATTENTION, attn_mfma_kernel<128>, grid, block, 0, s, qp, kp, vp, row_stride,
-                  causal, sl, cu_dev, op, out_stride, lse, T);
+                  kv_group, causal, sl, cu_dev, op, out_stride, lse, T);
   }
   if (dtype == 1)
-    return valu_dispatch<bf16_t>(s, q, k, v, row_stride, H, hd, causal, scale, B, max_len, T,
-                                 cu_dev, out, out_stride, lse);
-  return valu_dispatch<float>(s, q, k, v, row_stride, H, hd, causal, scale, B, max_len, T,
-                              cu_dev, out, out_stride, lse);
+    return valu_dispatch<bf16_t>(s, q, k, v, row_stride, H, kv_group, hd, causal, scale, B,
+                                 max_len, T, cu_dev, out, out_stride, lse);
+  return valu_dispatch<float>(s, q, k, v, row_stride, H, kv_group, hd, causal, scale, B, max_len,
+                              T, cu_dev, out, out_stride, lse);
 }
 
 }  // namespace zsa

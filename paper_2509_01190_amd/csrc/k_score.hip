@@ -34,7 +34,7 @@ constexpr int kLseChunk = 2048;
 template <int HD>
 __global__ __launch_bounds__(256) void score_mfma_kernel(
     const bf16_t* __restrict__ Q, const bf16_t* __restrict__ K, int64_t rs,
-    const float* __restrict__ lse, int H, int causal, float scale_log2,
+    const float* __restrict__ lse, int H, int kv_group, int causal, float scale_log2,
     const int32_t* __restrict__ cu, int T, int groups, float* __restrict__ partials) {
   constexpr int KLD = HD + 8;
   constexpr int KK = HD / 16;
@@ -59,7 +59,8 @@ __global__ __launch_bounds__(256) void score_mfma_kernel(
       const int jr = j0 + r;
       // keys past the sequence repeat the last row; their columns are not written
       *reinterpret_cast<uint4*>(Ks + r * KLD + ch) =
-          *reinterpret_cast<const uint4*>(K + static_cast<int64_t>(lo + min(jr, n - 1)) * rs + h * HD + ch);
+          *reinterpret_cast<const uint4*>(K + static_cast<int64_t>(lo + min(jr, n - 1)) * rs +
+                                          (h / kv_group) * HD + ch);
     }
     __syncthreads();
     bf16x8_t kf[2][KK];
@@ -156,7 +157,7 @@ template <typename T, int HD>
 __global__ __launch_bounds__(64) void score_valu_kernel(const T* __restrict__ Q,
                                                         const T* __restrict__ K, int64_t rs,
                                                         const float* __restrict__ lse, int H,
-                                                        int causal, float scale,
+                                                        int kv_group, int causal, float scale,
                                                         const int32_t* __restrict__ cu, int Tn,
                                                         int groups, float* __restrict__ partials) {
   __shared__ float Qs[32][HD];
@@ -172,7 +173,7 @@ __global__ __launch_bounds__(64) void score_valu_kernel(const T* __restrict__ Q,
     float kv[HD];
 #pragma unroll
     for (int c = 0; c < HD; ++c)
-      kv[c] = j < n ? to_f32(K[static_cast<int64_t>(lo + j) * rs + h * HD + c]) * scale : 0.f;
+      kv[c] = j < n ? to_f32(K[static_cast<int64_t>(lo + j) * rs + (h / kv_group) * HD + c]) * scale : 0.f;
     const int qstart = causal ? jbase : 0;
     for (int i0 = qstart; i0 < n; i0 += 32) {
       __syncthreads();
@@ -203,17 +204,17 @@ __global__ __launch_bounds__(64) void score_valu_kernel(const T* __restrict__ Q,
 
 template <typename T>
 hipError_t valu_dispatch(hipStream_t s, const void* q, const void* k, int64_t rs,
-                         const float* lse, int H, int hd, int causal, float scale, int B,
+                         const float* lse, int H, int kvg, int hd, int causal, float scale, int B,
                          int max_len, int Trows, const int32_t* cu, float* partials,
                          int groups) {
   const dim3 grid((max_len + 63) / 64, groups, B), block(64);
   const T* qp = static_cast<const T*>(q);
   const T* kp = static_cast<const T*>(k);
   switch (hd) {
-    case 16: return launch(K_SCORE, score_valu_kernel<T, 16>, grid, block, 0, s, qp, kp, rs, lse, H, causal, scale, cu, Trows, groups, partials);
-    case 32: return launch(K_SCORE, score_valu_kernel<T, 32>, grid, block, 0, s, qp, kp, rs, lse, H, causal, scale, cu, Trows, groups, partials);
-    case 64: return launch(K_SCORE, score_valu_kernel<T, 64>, grid, block, 0, s, qp, kp, rs, lse, H, causal, scale, cu, Trows, groups, partials);
-    case 128: return launch(K_SCORE, score_valu_kernel<T, 128>, grid, block, 0, s, qp, kp, rs, lse, H, causal, scale, cu, Trows, groups, partials);
+    case 16: return launch(K_SCORE, score_valu_kernel<T, 16>, grid, block, 0, s, qp, kp, rs, lse, H, kvg, causal, scale, cu, Trows, groups, partials);
+    case 32: return launch(K_SCORE, score_valu_kernel<T, 32>, grid, block, 0, s, qp, kp, rs, lse, H, kvg, causal, scale, cu, Trows, groups, partials);
+    case 64: return launch(K_SCORE, score_valu_kernel<T, 64>, grid, block, 0, s, qp, kp, rs, lse, H, kvg, causal, scale, cu, Trows, groups, partials);
+    case 128: return launch(K_SCORE, score_valu_kernel<T, 128>, grid, block, 0, s, qp, kp, rs, lse, H, kvg, causal, scale, cu, Trows, groups, partials);
     default: return hipErrorInvalidValue;
   }
 }
@@ -231,7 +232,7 @@ int score_groups(int dtype, int H, int hd, int T) {
 }
 
 hipError_t launch_score(hipStream_t s, int dtype, const void* q, const void* k,
-                        int64_t row_stride, const float* lse, int H, int hd, int causal,
+                        int64_t row_stride, const float* lse, int H, int kv_group, int hd, int causal,
                         float scale, int B, int max_len, int T, const int32_t* cu_dev,
                         float* partials, int groups) {
   if (B == 0 || max_len == 0) return hipSuccess;
@@ -242,15 +243,15 @@ hipError_t launch_score(hipStream_t s, int dtype, const void* q, const void* k,
     const float sl = scale * kLog2e;
     if (hd == 64)
       return launch(K_SCORE, score_mfma_kernel<64>, grid, block, 0, s, qp, kp, row_stride, lse,
-                    H, causal, sl, cu_dev, T, groups, partials);
+                    H, kv_group, causal, sl, cu_dev, T, groups, partials);
     return launch(K_SCORE, score_mfma_kernel<128>, grid, block, 0, s, qp, kp, row_stride, lse, H,
-                  causal, sl, cu_dev, T, groups, partials);
+                  kv_group, causal, sl, cu_dev, T, groups, partials);
   }
   if (dtype == 1)
-    return valu_dispatch<bf16_t>(s, q, k, row_stride, lse, H, hd, causal, scale, B, max_len, T,
-                                 cu_dev, partials, groups);
-  return valu_dispatch<float>(s, q, k, row_stride, lse, H, hd, causal, scale, B, max_len, T,
-                              cu_dev, partials, groups);
+    return valu_dispatch<bf16_t>(s, q, k, row_stride, lse, H, kv_group, hd, causal, scale, B,
+                                 max_len, T, cu_dev, partials, groups);
+  return valu_dispatch<float>(s, q, k, row_stride, lse, H, kv_group, hd, causal, scale, B, max_len,
+                              T, cu_dev, partials, groups);
 }
 
 }  // namespace zsa

@@ -1,5 +1,6 @@
 // Per-sequence top-k of the contribution scores (keep the k highest, ties to
-// the lower row, output in ascending row order).
+// the lower row, output in ascending row order; optionally the last row of
+// every sequence is always kept and the other k - 1 are chosen by score).
 //
 // One 1024-thread workgroup (16 waves) per sequence. The score of a row is
 // first finalised as the fixed-order sum of the per-head-group partial sums
@@ -37,7 +38,7 @@ __device__ __forceinline__ float finalise(const float* __restrict__ partials, in
 __global__ __launch_bounds__(kSelThreads) void select_kernel(
     const float* __restrict__ partials, int groups, int T, const int32_t* __restrict__ cu_in,
     const int32_t* __restrict__ cu_out, int32_t* __restrict__ kept,
-    float* __restrict__ scores_out, int lds_cap) {
+    float* __restrict__ scores_out, int lds_cap, int keep_last) {
   extern __shared__ uint32_t keys[];
   __shared__ uint32_t hist[256];
   __shared__ uint32_t wave_cnt[kSelWaves];
@@ -53,10 +54,12 @@ __global__ __launch_bounds__(kSelThreads) void select_kernel(
   const int wave = tid >> 6;
   const bool staged = n <= lds_cap;
 
+  // with keep_last the sequence's last row takes the largest key, above
+  // every finite or infinite score, so it is always among the k kept
   for (int i = tid; i < n; i += kSelThreads) {
     const float s = finalise(partials, groups, T, lo + i);
     if (scores_out != nullptr) scores_out[lo + i] = s;
-    if (staged) keys[i] = order_key(s);
+    if (staged) keys[i] = (keep_last && i == n - 1) ? 0xffffffffu : order_key(s);
   }
   if (k <= 0 || n <= 0) return;
   if (k >= n) {
@@ -66,7 +69,8 @@ __global__ __launch_bounds__(kSelThreads) void select_kernel(
   __syncthreads();
 
   auto key_at = [&](int i) -> uint32_t {
-    return staged ? keys[i] : order_key(finalise(partials, groups, T, lo + i));
+    if (staged) return keys[i];
+    return (keep_last && i == n - 1) ? 0xffffffffu : order_key(finalise(partials, groups, T, lo + i));
   };
 
   uint32_t prefix = 0u;
@@ -170,12 +174,12 @@ __global__ void finalize_kernel(const float* __restrict__ partials, int groups, 
 
 hipError_t launch_select(hipStream_t s, const float* partials, int groups, int T, int B,
                          int max_len, const int32_t* cu_in_dev, const int32_t* cu_out_dev,
-                         int32_t* kept_rows, float* scores_out) {
+                         int32_t* kept_rows, float* scores_out, int keep_last) {
   if (B == 0) return hipSuccess;
   const int cap = max_len < kSelLdsCap ? max_len : kSelLdsCap;
   const size_t shmem = static_cast<size_t>(cap > 0 ? cap : 1) * sizeof(uint32_t);
   return launch(K_SELECT, select_kernel, dim3(B), dim3(kSelThreads), shmem, s, partials, groups,
-                T, cu_in_dev, cu_out_dev, kept_rows, scores_out, cap);
+                T, cu_in_dev, cu_out_dev, kept_rows, scores_out, cap, keep_last);
 }
 
 hipError_t launch_score_finalize(hipStream_t s, const float* partials, int groups, int T,

@@ -129,7 +129,16 @@ int check_cfg(const zsa_layer_cfg* c) {
   if (c->tau < 1) return fail(ZSA_EINVAL, "tau %d < 1", c->tau);
   if (!(c->norm_eps >= 0.f)) return fail(ZSA_EINVAL, "norm_eps must be >= 0");
   if (c->kind == ZSA_DECODER && !(c->rope_theta > 0.f)) return fail(ZSA_EINVAL, "rope_theta <= 0");
+  if (c->n_kv_heads < 0 || (c->n_kv_heads > 0 && c->n_heads % c->n_kv_heads != 0))
+    return fail(ZSA_ESHAPE, "n_kv_heads %d must divide n_heads %d", c->n_kv_heads, c->n_heads);
   return ZSA_OK;
+}
+
+// key/value heads (grouped-query attention; 0 in the config means n_heads)
+int kv_heads(const zsa_layer_cfg& c) { return c.n_kv_heads == 0 ? c.n_heads : c.n_kv_heads; }
+// width of the fused [q | k | v] projection output
+int64_t qkv_width(const zsa_layer_cfg& c) {
+  return c.d_model + 2 * static_cast<int64_t>(kv_heads(c)) * c.head_dim;
 }
 
 int check_weights(const zsa_layer_cfg* c, const zsa_layer_weights* w) {
@@ -188,7 +197,7 @@ LayerLayout layer_layout(const zsa_layer_cfg* c, int64_t T, Carver& cv) {
   const int G = c->n_heads;
   LayerLayout L;
   L.h = cv.take(T * d * e);
-  L.qkv = cv.take(T * 3 * d * e);
+  L.qkv = cv.take(T * qkv_width(*c) * e);
   L.o = cv.take(T * d * e);
   L.f = cv.take(T * F * e);
   L.xg = cv.take(T * d * e);
@@ -200,7 +209,7 @@ LayerLayout layer_layout(const zsa_layer_cfg* c, int64_t T, Carver& cv) {
   const int dt = c->dtype;
   const int up_n = c->kind == ZSA_DECODER ? 2 * F : F;
   const int rows = static_cast<int>(T);
-  L.splitk_bytes = std::max({zsa::gemm_workspace_bound(dt, rows, 3 * d, d),
+  L.splitk_bytes = std::max({zsa::gemm_workspace_bound(dt, rows, static_cast<int>(qkv_width(*c)), d),
                              zsa::gemm_workspace_bound(dt, rows, d, d),
                              zsa::gemm_workspace_bound(dt, rows, up_n, d),
                              zsa::gemm_workspace_bound(dt, rows, d, F)});
@@ -250,6 +259,9 @@ int run_layer(hipStream_t s, const zsa_layer_cfg& c, const zsa_layer_weights& w,
   const int dt = c.dtype;
   const size_t e = esize(dt);
   const int d = c.d_model, H = c.n_heads, hd = c.head_dim, F = c.d_ff;
+  const int kvd = kv_heads(c) * hd;     // key (and value) columns
+  const int qw = d + 2 * kvd;           // row width of the fused [q | k | v] output
+  const int kvg = H / kv_heads(c);      // query heads per key/value head
   const bool dec = c.kind == ZSA_DECODER;
   const int norm_kind = dec ? ZSA_NORM_RMS : ZSA_NORM_LAYER;
   const float scale = 1.0f / sqrtf(static_cast<float>(hd));
@@ -262,19 +274,19 @@ int run_layer(hipStream_t s, const zsa_layer_cfg& c, const zsa_layer_weights& w,
     ep.epi = dec ? EPI_ROPE : EPI_NONE;
     ep.bias = w.b_qkv;
     ep.y = wb.qkv;
-    ep.ldy = 3 * d;
+    ep.ldy = qw;
     ep.pos = pos_in;
     ep.head_dim = hd;
-    ep.rope_cols = dec ? 2 * d : 0;
+    ep.rope_cols = dec ? d + kvd : 0;
     if (dec) fill_rope(ep, hd, c.rope_theta);
-    HIP_TRY(launch_gemm(s, dt, wb.h, in.T, d, w.w_qkv, 3 * d, ep, wb.splitk, wb.splitk_bytes),
+    HIP_TRY(launch_gemm(s, dt, wb.h, in.T, d, w.w_qkv, qw, ep, wb.splitk, wb.splitk_bytes),
             "qkv projection");
   }
   const char* qkv = static_cast<const char*>(wb.qkv);
   const void* q = qkv;
   const void* k = qkv + d * e;
-  const void* v = qkv + 2 * d * e;
-  HIP_TRY(launch_attention(s, dt, q, k, v, 3 * d, H, hd, c.causal, scale, in.B, in.max_len, in.T,
+  const void* v = qkv + (d + kvd) * e;
+  HIP_TRY(launch_attention(s, dt, q, k, v, qw, H, kvg, hd, c.causal, scale, in.B, in.max_len, in.T,
                            in.cu_dev, wb.o, d, wb.lse),
           "attention");
   const void* xr = x_in;
@@ -282,12 +294,12 @@ int run_layer(hipStream_t s, const zsa_layer_cfg& c, const zsa_layer_weights& w,
   int rows = in.T;
   if (prune) {
     const int G = score_groups(dt, H, hd, in.T);
-    HIP_TRY(launch_score(s, dt, q, k, 3 * d, wb.lse, H, hd, c.causal, scale, in.B, in.max_len,
+    HIP_TRY(launch_score(s, dt, q, k, qw, wb.lse, H, kvg, hd, c.causal, scale, in.B, in.max_len,
                          in.T, in.cu_dev, wb.partials, G),
             "score");
     int32_t* kept = kept_out != nullptr ? kept_out : wb.kept;
     HIP_TRY(launch_select(s, wb.partials, G, in.T, in.B, in.max_len, in.cu_dev, out.cu_dev, kept,
-                          scores_out),
+                          scores_out, c.force_keep_last != 0),
             "select");
     HIP_TRY(launch_gather(s, dt, d, in.T, kept, out.T, x_in, wb.xg, wb.o, wb.og, pos_in, pos_out),
             "gather");
@@ -467,15 +479,25 @@ size_t zsa_attention_workspace_size(int32_t n_heads, int32_t total_rows, int32_t
   return b;
 }
 
+int check_kv_heads(int32_t n_heads, int32_t n_kv_heads, int* group) {
+  if (n_heads <= 0) return fail(ZSA_EINVAL, "n_heads %d", n_heads);
+  const int32_t hkv = n_kv_heads == 0 ? n_heads : n_kv_heads;
+  if (hkv < 0 || n_heads % hkv != 0)
+    return fail(ZSA_ESHAPE, "n_kv_heads %d must divide n_heads %d", n_kv_heads, n_heads);
+  *group = n_heads / hkv;
+  return ZSA_OK;
+}
+
 int zsa_attention_with_scores(void* stream, int32_t dtype, const void* q, const void* k,
                               const void* v, int64_t row_stride, int32_t n_heads,
-                              int32_t head_dim, int32_t causal, float scale, int32_t batch,
-                              const int32_t* cu_host, const int32_t* cu_dev, void* out,
-                              int64_t out_stride, float* lse, float* scores, void* ws,
+                              int32_t n_kv_heads, int32_t head_dim, int32_t causal, float scale,
+                              int32_t batch, const int32_t* cu_host, const int32_t* cu_dev,
+                              void* out, int64_t out_stride, float* lse, float* scores, void* ws,
                               size_t ws_bytes) {
   CHECK(check_dtype(dtype));
   CHECK(check_head_dim(head_dim));
-  if (n_heads <= 0) return fail(ZSA_EINVAL, "n_heads %d", n_heads);
+  int kvg = 1;
+  CHECK(check_kv_heads(n_heads, n_kv_heads, &kvg));
   int32_t T, max_len;
   CHECK(check_seqs(batch, cu_host, cu_dev, &T, &max_len));
   CHECK(check_ptr16(q, "q"));
@@ -495,14 +517,14 @@ int zsa_attention_with_scores(void* stream, int32_t dtype, const void* q, const 
   hipStream_t s = static_cast<hipStream_t>(stream);
   char* base = static_cast<char*>(ws);
   float* lse_buf = lse != nullptr ? lse : reinterpret_cast<float*>(base);
-  HIP_TRY(zsa::launch_attention(s, dtype, q, k, v, row_stride, n_heads, head_dim, causal, scale,
-                                batch, max_len, T, cu_dev, out, out_stride, lse_buf),
+  HIP_TRY(zsa::launch_attention(s, dtype, q, k, v, row_stride, n_heads, kvg, head_dim, causal,
+                                scale, batch, max_len, T, cu_dev, out, out_stride, lse_buf),
           "attention");
   if (scores != nullptr) {
     float* partials = reinterpret_cast<float*>(base + round256(static_cast<size_t>(n_heads) * T * 4));
     const int G = zsa::score_groups(dtype, n_heads, head_dim, T);
-    HIP_TRY(zsa::launch_score(s, dtype, q, k, row_stride, lse_buf, n_heads, head_dim, causal, scale,
-                              batch, max_len, T, cu_dev, partials, G),
+    HIP_TRY(zsa::launch_score(s, dtype, q, k, row_stride, lse_buf, n_heads, kvg, head_dim, causal,
+                              scale, batch, max_len, T, cu_dev, partials, G),
             "score");
     HIP_TRY(zsa::launch_score_finalize(s, partials, G, T, scores), "score finalize");
   }
@@ -515,12 +537,14 @@ size_t zsa_score_workspace_size(int32_t n_heads, int32_t total_rows) {
 }
 
 int zsa_score_positions(void* stream, int32_t dtype, const void* q, const void* k,
-                        int64_t row_stride, const float* lse, int32_t n_heads, int32_t head_dim,
-                        int32_t causal, float scale, int32_t batch, const int32_t* cu_host,
-                        const int32_t* cu_dev, float* scores, void* ws, size_t ws_bytes) {
+                        int64_t row_stride, const float* lse, int32_t n_heads,
+                        int32_t n_kv_heads, int32_t head_dim, int32_t causal, float scale,
+                        int32_t batch, const int32_t* cu_host, const int32_t* cu_dev,
+                        float* scores, void* ws, size_t ws_bytes) {
   CHECK(check_dtype(dtype));
   CHECK(check_head_dim(head_dim));
-  if (n_heads <= 0) return fail(ZSA_EINVAL, "n_heads %d", n_heads);
+  int kvg = 1;
+  CHECK(check_kv_heads(n_heads, n_kv_heads, &kvg));
   int32_t T, max_len;
   CHECK(check_seqs(batch, cu_host, cu_dev, &T, &max_len));
   CHECK(check_ptr16(q, "q"));
@@ -536,8 +560,8 @@ int zsa_score_positions(void* stream, int32_t dtype, const void* q, const void* 
   hipStream_t s = static_cast<hipStream_t>(stream);
   const int G = zsa::score_groups(dtype, n_heads, head_dim, T);
   float* partials = static_cast<float*>(ws);
-  HIP_TRY(zsa::launch_score(s, dtype, q, k, row_stride, lse, n_heads, head_dim, causal, scale,
-                            batch, max_len, T, cu_dev, partials, G),
+  HIP_TRY(zsa::launch_score(s, dtype, q, k, row_stride, lse, n_heads, kvg, head_dim, causal,
+                            scale, batch, max_len, T, cu_dev, partials, G),
           "score");
   HIP_TRY(zsa::launch_score_finalize(s, partials, G, T, scores), "score finalize");
   return ZSA_OK;
@@ -548,8 +572,8 @@ size_t zsa_select_workspace_size(int32_t batch) {
 }
 
 int zsa_select_topk(void* stream, const float* scores, int32_t batch, const int32_t* cu_host,
-                    const int32_t* cu_dev, const int32_t* k_host, int32_t* kept_rows, void* ws,
-                    size_t ws_bytes) {
+                    const int32_t* cu_dev, const int32_t* k_host, int32_t force_keep_last,
+                    int32_t* kept_rows, void* ws, size_t ws_bytes) {
   int32_t T, max_len;
   CHECK(check_seqs(batch, cu_host, cu_dev, &T, &max_len));
   if (batch > 0 && k_host == nullptr) return fail(ZSA_EINVAL, "k_host is NULL");
@@ -567,7 +591,8 @@ int zsa_select_topk(void* stream, const float* scores, int32_t batch, const int3
   hipStream_t s = static_cast<hipStream_t>(stream);
   int32_t* cu_out_dev = static_cast<int32_t*>(ws);
   HIP_TRY(zsa::launch_upload_i32(s, cu_out_dev, cu_out.data(), batch + 1), "upload");
-  HIP_TRY(zsa::launch_select(s, scores, 1, T, batch, max_len, cu_dev, cu_out_dev, kept_rows, nullptr),
+  HIP_TRY(zsa::launch_select(s, scores, 1, T, batch, max_len, cu_dev, cu_out_dev, kept_rows, nullptr,
+                             force_keep_last != 0),
           "select");
   return ZSA_OK;
 }

@@ -138,25 +138,27 @@ size_t gemm_workspace_bytes(int dtype, int M, int N, int K);
 // the most any M <= max_rows needs
 size_t gemm_workspace_bound(int dtype, int max_rows, int N, int K);
 
+// query head h reads key/value head h / kv_group (kv_group = H / H_kv)
 hipError_t launch_attention(hipStream_t s, int dtype, const void* q, const void* k,
-                            const void* v, int64_t row_stride, int H, int hd, int causal,
-                            float scale, int B, int max_len, int T, const int32_t* cu_dev,
-                            void* out, int64_t out_stride, float* lse);
+                            const void* v, int64_t row_stride, int H, int kv_group, int hd,
+                            int causal, float scale, int B, int max_len, int T,
+                            const int32_t* cu_dev, void* out, int64_t out_stride, float* lse);
 
 // writes G partial score vectors [G][T] (G = head groups); returns G via *groups
 hipError_t launch_score(hipStream_t s, int dtype, const void* q, const void* k,
-                        int64_t row_stride, const float* lse, int H, int hd, int causal,
-                        float scale, int B, int max_len, int T, const int32_t* cu_dev,
-                        float* partials, int groups);
+                        int64_t row_stride, const float* lse, int H, int kv_group, int hd,
+                        int causal, float scale, int B, int max_len, int T,
+                        const int32_t* cu_dev, float* partials, int groups);
 int score_groups(int dtype, int H, int hd, int T);
 
 hipError_t launch_score_finalize(hipStream_t s, const float* partials, int groups, int T,
                                  float* scores);
 
-// per-sequence top-k over sum_g partials[g*T + row]; cu_out gives output offsets
+// per-sequence top-k over sum_g partials[g*T + row]; cu_out gives output
+// offsets; keep_last always keeps each sequence's last row
 hipError_t launch_select(hipStream_t s, const float* partials, int groups, int T, int B,
                          int max_len, const int32_t* cu_in_dev, const int32_t* cu_out_dev,
-                         int32_t* kept_rows, float* scores_out);
+                         int32_t* kept_rows, float* scores_out, int keep_last);
 
 // row gather of up to two [*, d] arrays plus pos
 hipError_t launch_gather(hipStream_t s, int dtype, int d, int t_in, const int32_t* kept,

@@ -95,6 +95,12 @@ PRESETS: Dict[str, Preset] = {
                         tuple(range(1, 13)), (1.0, 0.9, 0.8, 0.7, 0.5, 0.3, 0.1, 0.02)),
     "gpt2_n1024": Preset("gpt2_n1024", ENCODER, 12, 768, 12, 3072, 16, 1024, "bf16", True,
                          tuple(range(1, 13)), (1.0, 0.9, 0.8, 0.7, 0.5, 0.3, 0.1, 0.02)),
+    # LLaMA-3-8B-shaped prefill slice: grouped-query attention (32 query heads
+    # over 8 key/value heads), FFN 14336; the last input row always survives
+    # (the first generated token is predicted from it)
+    "llama3_8b": Preset("llama3_8b", DECODER, 4, 4096, 32, 14336, 4, 4096, "bf16", True, (1,),
+                        (1.0, 0.5, 0.2, 0.09), rope_theta=500000.0, n_kv_heads=8,
+                        force_keep_last=True),
     # one 7B-shaped layer over a ragged batch with per-sequence keep rates
     "ragged": Preset("ragged", DECODER, 1, 4096, 32, 11008, 64, 4096, "bf16", True, (1,), (),
                      ragged=True, min_len=128, per_seq_rates=True, rate_lo=0.05, rate_hi=1.0),

@@ -45,7 +45,8 @@ class ZsaError(RuntimeError):
 class LayerCfg(ctypes.Structure):
     _fields_ = [("kind", _i32), ("d_model", _i32), ("n_heads", _i32), ("head_dim", _i32),
                 ("d_ff", _i32), ("causal", _i32), ("dtype", _i32), ("tau", _i32),
-                ("norm_eps", _f32), ("rope_theta", _f32)]
+                ("norm_eps", _f32), ("rope_theta", _f32), ("n_kv_heads", _i32),
+                ("force_keep_last", _i32)]
 
 
 WEIGHT_NAMES = ["norm1_w", "norm1_b", "w_qkv", "b_qkv", "w_o", "b_o",
@@ -66,13 +67,13 @@ _SIGS = {
                                   _i32, _i32, _f32, _vp, _vp, _sz]),
     "zsa_linear_workspace_size": (_sz, [_i32, _i32, _i32, _i32]),
     "zsa_attention_with_scores": (ctypes.c_int, [_vp, _i32, _vp, _vp, _vp, _i64, _i32, _i32,
-                                                 _i32, _f32, _i32, _pi32, _vp, _vp, _i64, _vp,
-                                                 _vp, _vp, _sz]),
+                                                 _i32, _i32, _f32, _i32, _pi32, _vp, _vp, _i64,
+                                                 _vp, _vp, _vp, _sz]),
     "zsa_attention_workspace_size": (_sz, [_i32, _i32, _i32]),
     "zsa_score_positions": (ctypes.c_int, [_vp, _i32, _vp, _vp, _i64, _vp, _i32, _i32, _i32,
-                                           _f32, _i32, _pi32, _vp, _vp, _vp, _sz]),
+                                           _i32, _f32, _i32, _pi32, _vp, _vp, _vp, _sz]),
     "zsa_score_workspace_size": (_sz, [_i32, _i32]),
-    "zsa_select_topk": (ctypes.c_int, [_vp, _vp, _i32, _pi32, _vp, _pi32, _vp, _vp, _sz]),
+    "zsa_select_topk": (ctypes.c_int, [_vp, _vp, _i32, _pi32, _vp, _pi32, _i32, _vp, _vp, _sz]),
     "zsa_select_workspace_size": (_sz, [_i32]),
     "zsa_compact_gather": (ctypes.c_int, [_vp, _i32, _vp, _i32, _vp, _i32, _vp, _i32, _vp, _vp]),
     "zsa_layer_forward": (ctypes.c_int, [_vp, ctypes.POINTER(LayerCfg),
@@ -235,9 +236,12 @@ def linear(x: torch.Tensor, w: torch.Tensor, bias: Optional[torch.Tensor] = None
 
 def attention_with_scores(q: torch.Tensor, k: torch.Tensor, v: torch.Tensor, n_heads: int,
                           seqs: Seqs, causal: bool, want_lse: bool = True,
-                          want_scores: bool = True, scale: Optional[float] = None):
-    """q, k, v: [T, n_heads*hd] views that may share a row stride (e.g.
-    slices of one [T, 3d] tensor). Returns (out, lse or None, scores or None)."""
+                          want_scores: bool = True, scale: Optional[float] = None,
+                          n_kv_heads: int = 0):
+    """q: [T, n_heads*hd], k, v: [T, n_kv_heads*hd] views sharing one row
+    stride (e.g. slices of one fused [T, (n_heads + 2 n_kv_heads) hd]
+    tensor); n_kv_heads 0 means n_heads. Returns (out, lse or None, scores
+    or None)."""
     _require_cuda(q, k, v)
     T, width = q.shape
     hd = width // n_heads
@@ -252,14 +256,15 @@ def attention_with_scores(q: torch.Tensor, k: torch.Tensor, v: torch.Tensor, n_h
     wsz = lib().zsa_attention_workspace_size(n_heads, T, int(want_scores))
     ws = torch.empty(max(int(wsz), 1), dtype=torch.uint8, device=q.device)
     _check(lib().zsa_attention_with_scores(
-        _stream(q.device), _dtype_code(q), _p(q), _p(k), _p(v), rs, n_heads, hd, int(causal),
-        scale, seqs.batch, _hp32(seqs.host), _p(seqs.dev), _p(out), width, _p(lse), _p(scores),
-        _p(ws), wsz))
+        _stream(q.device), _dtype_code(q), _p(q), _p(k), _p(v), rs, n_heads, n_kv_heads, hd,
+        int(causal), scale, seqs.batch, _hp32(seqs.host), _p(seqs.dev), _p(out), width, _p(lse),
+        _p(scores), _p(ws), wsz))
     return out, lse, scores
 
 
 def score_positions(q: torch.Tensor, k: torch.Tensor, lse: torch.Tensor, n_heads: int,
-                    seqs: Seqs, causal: bool, scale: Optional[float] = None) -> torch.Tensor:
+                    seqs: Seqs, causal: bool, scale: Optional[float] = None,
+                    n_kv_heads: int = 0) -> torch.Tensor:
     _require_cuda(q, k, lse)
     T, width = q.shape
     hd = width // n_heads
@@ -272,20 +277,20 @@ def score_positions(q: torch.Tensor, k: torch.Tensor, lse: torch.Tensor, n_heads
     wsz = lib().zsa_score_workspace_size(n_heads, T)
     ws = torch.empty(max(int(wsz), 1), dtype=torch.uint8, device=q.device)
     _check(lib().zsa_score_positions(
-        _stream(q.device), _dtype_code(q), _p(q), _p(k), rs, _p(lse), n_heads, hd, int(causal),
-        scale, seqs.batch, _hp32(seqs.host), _p(seqs.dev), _p(scores), _p(ws), wsz))
+        _stream(q.device), _dtype_code(q), _p(q), _p(k), rs, _p(lse), n_heads, n_kv_heads, hd,
+        int(causal), scale, seqs.batch, _hp32(seqs.host), _p(seqs.dev), _p(scores), _p(ws), wsz))
     return scores
 
 
-def select_topk(scores: torch.Tensor, seqs: Seqs, k) -> torch.Tensor:
+def select_topk(scores: torch.Tensor, seqs: Seqs, k, keep_last: bool = False) -> torch.Tensor:
     _require_cuda(scores)
     kh = _host_i32(k)
     kept = torch.empty(max(int(kh.sum()), 1), dtype=torch.int32, device=scores.device)
     wsz = lib().zsa_select_workspace_size(seqs.batch)
     ws = torch.empty(max(int(wsz), 1), dtype=torch.uint8, device=scores.device)
     _check(lib().zsa_select_topk(_stream(scores.device), _p(scores), seqs.batch,
-                                 _hp32(seqs.host), _p(seqs.dev), _hp32(kh), _p(kept), _p(ws),
-                                 wsz))
+                                 _hp32(seqs.host), _p(seqs.dev), _hp32(kh), int(keep_last),
+                                 _p(kept), _p(ws), wsz))
     return kept[: int(kh.sum())]
 
 
@@ -303,9 +308,37 @@ def compact_gather(hidden: torch.Tensor, pos: Optional[torch.Tensor],
 
 # ------------------------------------------------------------------ blocks
 def make_cfg(kind: int, d_model: int, n_heads: int, d_ff: int, causal: bool, dtype: int,
-             tau: int = 5, norm_eps: float = 1e-5, rope_theta: float = 10000.0) -> LayerCfg:
+             tau: int = 5, norm_eps: float = 1e-5, rope_theta: float = 10000.0,
+             n_kv_heads: int = 0, force_keep_last: bool = False) -> LayerCfg:
     return LayerCfg(kind, d_model, n_heads, d_model // n_heads, d_ff, int(causal), dtype, tau,
-                    norm_eps, rope_theta)
+                    norm_eps, rope_theta, n_kv_heads, int(force_keep_last))
+
+
+def weight_shapes(cfg: LayerCfg) -> Dict[str, tuple]:
+    """Shape of every weight of one block under ``cfg`` (PyTorch Linear
+    layout; the fused projection is [q | k | v] with grouped-query k/v)."""
+    d, hd, F = cfg.d_model, cfg.head_dim, cfg.d_ff
+    kv = cfg.n_kv_heads or cfg.n_heads
+    qkv = d + 2 * kv * hd
+    up = 2 * F if cfg.kind == DECODER else F
+    return {"norm1_w": (d,), "norm1_b": (d,), "w_qkv": (qkv, d), "b_qkv": (qkv,),
+            "w_o": (d, d), "b_o": (d,), "norm2_w": (d,), "norm2_b": (d,),
+            "w_up": (up, d), "b_up": (up,), "w_down": (d, F), "b_down": (d,)}
+
+
+def _check_weight_shapes(cfg: LayerCfg, w: Dict[str, Optional[torch.Tensor]], layer: int) -> None:
+    # the library takes raw pointers: a wrongly sized weight would be read out
+    # of bounds, so shapes are checked here, before any launch
+    required = {"norm1_w", "w_qkv", "w_o", "norm2_w", "w_up", "w_down"}
+    for name, shape in weight_shapes(cfg).items():
+        t = w.get(name)
+        if t is None:
+            if name in required:
+                raise ValueError(f"layer {layer}: {name} is missing")
+            continue
+        if tuple(t.shape) != shape or not t.is_contiguous():
+            raise ValueError(f"layer {layer}: {name} has shape {tuple(t.shape)}, "
+                             f"expected contiguous {shape}")
 
 
 def _weights_struct(w: Dict[str, Optional[torch.Tensor]]) -> LayerWeights:
@@ -319,6 +352,8 @@ class Stack:
     device tensors in the storage dtype."""
 
     def __init__(self, cfg: LayerCfg, weights: List[Dict[str, Optional[torch.Tensor]]]):
+        for l, w in enumerate(weights):
+            _check_weight_shapes(cfg, w, l)
         self.cfg = cfg
         self.weights = weights
         self._wstructs = (LayerWeights * len(weights))(*[_weights_struct(w) for w in weights])

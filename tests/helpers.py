@@ -79,7 +79,8 @@ def dev_weights(w_np, dtype):
     return {k: (None if v is None else to_dev(v, dtype)) for k, v in w_np.items()}
 
 
-def check_kept_sets(gpu_scores, ref_scores, k, kept_gpu, kept_ref, eps, what=""):
+def check_kept_sets(gpu_scores, ref_scores, k, kept_gpu, kept_ref, eps, what="",
+                    keep_last=False):
     """Kept-set agreement for one sequence.
 
     Exact: the GPU kept set is the oracle's top-k of the GPU's own scores.
@@ -91,7 +92,7 @@ def check_kept_sets(gpu_scores, ref_scores, k, kept_gpu, kept_ref, eps, what="")
     ref_scores = np.asarray(ref_scores, dtype=np.float64)
     kept_gpu = np.asarray(kept_gpu, dtype=np.int64)
     kept_ref = np.asarray(kept_ref, dtype=np.int64)
-    own = O.select_topk(gpu_scores, k)
+    own = O.select_topk(gpu_scores, k, keep_last)
     assert np.array_equal(kept_gpu, own), f"{what}: GPU kept set is not the top-k of its own scores"
     scale = np.maximum(np.abs(ref_scores), 1e-30)
     rel = np.max(np.abs(gpu_scores - ref_scores) / scale) if ref_scores.size else 0.0
@@ -99,7 +100,10 @@ def check_kept_sets(gpu_scores, ref_scores, k, kept_gpu, kept_ref, eps, what="")
     diff = np.setxor1d(kept_gpu, kept_ref)
     if diff.size == 0 or k == 0:
         return 0
-    s_star = np.sort(ref_scores)[::-1][k - 1]
+    # with keep_last the last row is fixed and k - 1 are chosen among the rest
+    cand, kk = (ref_scores[:-1], k - 1) if keep_last else (ref_scores, k)
+    assert kk > 0, f"{what}: kept sets differ where only the last row is kept"
+    s_star = np.sort(cand)[::-1][kk - 1]
     amb = np.abs(ref_scores[diff] - s_star) <= 2 * eps * abs(s_star)
     assert amb.all(), f"{what}: kept sets differ at unambiguous rows {diff[~amb]}"
     return int(diff.size // 2)

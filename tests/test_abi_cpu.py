@@ -77,28 +77,35 @@ def test_validation_happens_before_any_launch():
     # unsupported head_dim
     cu = np.array([0, 8], dtype=np.int32)
     rc = lib.zsa_attention_with_scores(None, zsa.BF16, ctypes.c_void_p(0x1000),
-                                       ctypes.c_void_p(0x1000), ctypes.c_void_p(0x1000), 96, 2, 48,
-                                       0, 0.1, 1, cu.ctypes.data_as(zsa._pi32),
+                                       ctypes.c_void_p(0x1000), ctypes.c_void_p(0x1000), 96, 2, 0,
+                                       48, 0, 0.1, 1, cu.ctypes.data_as(zsa._pi32),
                                        ctypes.c_void_p(0x4000), ctypes.c_void_p(0x5000), 96, None,
                                        None, None, 0)
     assert rc == zsa.EUNSUPPORTED
+    # key/value heads that do not divide the query heads
+    rc = lib.zsa_attention_with_scores(None, zsa.BF16, ctypes.c_void_p(0x1000),
+                                       ctypes.c_void_p(0x1000), ctypes.c_void_p(0x1000), 384, 6, 4,
+                                       64, 0, 0.1, 1, cu.ctypes.data_as(zsa._pi32),
+                                       ctypes.c_void_p(0x4000), ctypes.c_void_p(0x5000), 384, None,
+                                       None, None, 0)
+    assert rc == zsa.ESHAPE
     # cu not monotone
     cu = np.array([0, 8, 4], dtype=np.int32)
     rc = lib.zsa_select_topk(None, ctypes.c_void_p(0x1000), 2, cu.ctypes.data_as(zsa._pi32),
-                             ctypes.c_void_p(0x2000), cu.ctypes.data_as(zsa._pi32),
+                             ctypes.c_void_p(0x2000), cu.ctypes.data_as(zsa._pi32), 0,
                              ctypes.c_void_p(0x3000), ctypes.c_void_p(0x4000), 1024)
     assert rc == zsa.ESHAPE
     # k > n
     cu = np.array([0, 8], dtype=np.int32)
     k = np.array([9], dtype=np.int32)
     rc = lib.zsa_select_topk(None, ctypes.c_void_p(0x1000), 1, cu.ctypes.data_as(zsa._pi32),
-                             ctypes.c_void_p(0x2000), k.ctypes.data_as(zsa._pi32),
+                             ctypes.c_void_p(0x2000), k.ctypes.data_as(zsa._pi32), 0,
                              ctypes.c_void_p(0x3000), ctypes.c_void_p(0x4000), 1024)
     assert rc == zsa.ESHAPE
     # workspace too small
     k = np.array([4], dtype=np.int32)
     rc = lib.zsa_select_topk(None, ctypes.c_void_p(0x1000), 1, cu.ctypes.data_as(zsa._pi32),
-                             ctypes.c_void_p(0x2000), k.ctypes.data_as(zsa._pi32),
+                             ctypes.c_void_p(0x2000), k.ctypes.data_as(zsa._pi32), 1,
                              ctypes.c_void_p(0x3000), ctypes.c_void_p(0x4000), 4)
     assert rc == zsa.EWORKSPACE
 
@@ -115,6 +122,18 @@ def test_layer_config_validation():
                                ctypes.c_void_p(0x5000), cu.ctypes.data_as(zsa._pi32),
                                ctypes.c_void_p(0x6000), None, None, ctypes.c_void_p(0x7000), 1)
     assert rc == zsa.EINVAL
+    cfg = zsa.make_cfg(zsa.DECODER, 768, 12, 3072, True, zsa.BF16, n_kv_heads=5)  # 5 does not divide 12
+    rc = lib.zsa_layer_forward(None, ctypes.byref(cfg), ctypes.byref(w), ctypes.c_void_p(0x1000),
+                               ctypes.c_void_p(0x2000), 1, cu.ctypes.data_as(zsa._pi32),
+                               ctypes.c_void_p(0x3000), None, ctypes.c_void_p(0x4000),
+                               ctypes.c_void_p(0x5000), cu.ctypes.data_as(zsa._pi32),
+                               ctypes.c_void_p(0x6000), None, None, ctypes.c_void_p(0x7000), 1)
+    assert rc == zsa.ESHAPE
+    # grouped-query attention shrinks the fused projection (and its workspace)
+    mha = zsa.make_cfg(zsa.DECODER, 4096, 32, 14336, True, zsa.BF16)
+    gqa = zsa.make_cfg(zsa.DECODER, 4096, 32, 14336, True, zsa.BF16, n_kv_heads=8)
+    assert lib.zsa_layer_workspace_size(ctypes.byref(gqa), 4096, 1) < \
+        lib.zsa_layer_workspace_size(ctypes.byref(mha), 4096, 1)
     cfg = zsa.make_cfg(zsa.ENCODER, 768, 10, 3072, False, zsa.BF16)   # 768 / 10 is not integral
     assert lib.zsa_layer_workspace_size(ctypes.byref(cfg), 16, 1) > 0
     rc = lib.zsa_layer_forward(None, ctypes.byref(cfg), ctypes.byref(w), ctypes.c_void_p(0x1000),
@@ -156,3 +175,21 @@ def test_linear_split_k_workspace():
     cfg = zsa.make_cfg(zsa.ENCODER, 768, 12, 3072, False, zsa.BF16)
     small = lib.zsa_layer_workspace_size(ctypes.byref(cfg), 160, 32)
     assert small >= ws(zsa.BF16, 160, 768, 3072)
+
+
+def test_stack_rejects_misshaped_weights():
+    import torch
+    from paper_2509_01190_amd import workloads as W
+    p = W.shrink(W.PRESETS["dec1b"], n_layers=1, d_model=256, n_heads=4, d_ff=256, n_kv_heads=2)
+    cfg = zsa.make_cfg(p.kind, p.d_model, p.n_heads, p.d_ff, True, zsa.BF16, n_kv_heads=2)
+    good = {k: (None if v is None else torch.from_numpy(v)) for k, v in W.layer_weights(p, 0).items()}
+    assert tuple(good["w_qkv"].shape) == (256 + 2 * 2 * 64, 256)
+    zsa.Stack(cfg, [good])
+    bad = dict(good)
+    bad["w_qkv"] = torch.zeros(3 * 256, 256)        # the MHA shape under a GQA config
+    with pytest.raises(ValueError):
+        zsa.Stack(cfg, [bad])
+    bad = dict(good)
+    bad["w_down"] = None
+    with pytest.raises(ValueError):
+        zsa.Stack(cfg, [bad])

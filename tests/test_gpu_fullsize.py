@@ -60,3 +60,10 @@ def test_gpt2_every_layer_other_lengths(name, rate, seq):
     lens, stack, xd, posd, dws, ocfg = build(p, 0, norm_jitter=False)
     rates = W.keep_rates(p, 0, rate)
     compare_stack(p, lens, stack, xd, posd, dws, ocfg, rates, seqs_check=[seq])
+
+
+def test_llama3_gqa_keep_last_full():
+    p = W.PRESETS["llama3_8b"]
+    lens, stack, xd, posd, dws, ocfg = build(p, 0, norm_jitter=False)
+    rates = W.keep_rates(p, 0, 0.2)
+    compare_stack(p, lens, stack, xd, posd, dws, ocfg, rates, seqs_check=[1])

@@ -46,6 +46,22 @@ def test_select_topk_bit_exact(case):
     assert np.array_equal(got, ref)
 
 
+def test_select_topk_keep_last_bit_exact():
+    lens = [1, 2, 5, 6, 64, 1000, 20000, 777]
+    g = np.random.default_rng(13)
+    scores = W.injected_scores(lens, seed=2)
+    ks = [O.keep_count(n, float(g.uniform(0.0, 1.0)), 5) for n in lens]
+    ks[3] = 1
+    seqs = zsa.Seqs(lens, dev())
+    kept = zsa.select_topk(torch.from_numpy(scores).to(dev()), seqs, ks, keep_last=True)
+    torch.cuda.synchronize()
+    ref = []
+    for b, n in enumerate(lens):
+        lo = int(seqs.host[b])
+        ref.append(O.select_topk(scores[lo:lo + n].astype(np.float64), ks[b], keep_last=True) + lo)
+    assert np.array_equal(kept.cpu().numpy(), np.concatenate(ref))
+
+
 def test_select_topk_deterministic():
     lens = [4096, 777, 3000]
     scores = np.random.default_rng(4).standard_normal(sum(lens)).astype(np.float32)
@@ -220,6 +236,40 @@ def test_attention_with_scores(dtype, hd, causal):
     assert np.max(np.abs(lse.cpu().numpy() - lse_ref)) <= 2e-5 * max(1.0, np.abs(lse_ref).max())
     assert np.max(np.abs(scores.cpu().numpy() - s_ref) / s_ref) <= 1e-4
     assert abs(scores.cpu().double().sum() - H * sum(lens)) <= 1e-4 * H * sum(lens)
+
+
+@pytest.mark.parametrize("dtype,hd,hkv", [("bf16", 64, 2), ("bf16", 128, 1), ("f32", 32, 2),
+                                          ("bf16", 64, 4)])
+@pytest.mark.parametrize("causal", [False, True])
+def test_attention_with_scores_gqa(dtype, hd, hkv, causal):
+    """Grouped-query (hkv < H) and multi-query (hkv = 1) attention from one
+    fused [q | k | v] buffer."""
+    lens = [1, 17, 130, 300, 64]
+    H = 4
+    d, kvd = H * hd, hkv * hd
+    g = np.random.default_rng(30 + hd + hkv + causal)
+    fused = g.standard_normal((sum(lens), d + 2 * kvd)).astype(np.float32)
+    fused[:, :d] *= 1.5
+    t = to_dev(fused, dtype)
+    q, k, v = t[:, :d], t[:, d:d + kvd], t[:, d + kvd:]
+    seqs = zsa.Seqs(lens, dev())
+    out, lse, scores = zsa.attention_with_scores(q, k, v, H, seqs, causal, n_kv_heads=hkv)
+    torch.cuda.synchronize()
+    q64, k64, v64 = f64(q), f64(k), f64(v)
+    o_ref, lse_ref, s_ref = [], [], []
+    for b, n in enumerate(lens):
+        lo = int(seqs.host[b])
+        o, l, s = O.attention(q64[lo:lo + n], k64[lo:lo + n], v64[lo:lo + n], np.arange(n), H,
+                              causal, True, hkv)
+        o_ref.append(o)
+        lse_ref.append(l)
+        s_ref.append(s)
+    o_ref = np.concatenate(o_ref)
+    lse_ref = np.concatenate(lse_ref, axis=1)
+    s_ref = np.concatenate(s_ref)
+    assert_close(f64(out), o_ref, 1e-2 if dtype == "bf16" else 1e-5, "attention output")
+    assert np.max(np.abs(lse.cpu().numpy() - lse_ref)) <= 2e-5 * max(1.0, np.abs(lse_ref).max())
+    assert np.max(np.abs(scores.cpu().numpy() - s_ref) / s_ref) <= 1e-4
 
 
 @pytest.mark.parametrize("dtype,hd", [("bf16", 64), ("bf16", 128), ("f32", 32)])

@@ -22,13 +22,14 @@ def build(p, seed, lens=None, norm_jitter=True, sharp=1.0):
         w["w_qkv"] = (w["w_qkv"] * np.float32(sharp)).astype(np.float32)
     dws = [dev_weights(w, p.dtype) for w in ws]
     cfg = zsa.make_cfg(p.kind, p.d_model, p.n_heads, p.d_ff, p.causal,
-                       zsa.BF16 if p.dtype == "bf16" else zsa.F32, p.tau, p.norm_eps, p.rope_theta)
+                       zsa.BF16 if p.dtype == "bf16" else zsa.F32, p.tau, p.norm_eps, p.rope_theta,
+                       p.n_kv_heads, p.force_keep_last)
     stack = zsa.Stack(cfg, dws)
     x = W.hidden(p, seed, lens)
     xd = to_dev(x, p.dtype)
     posd = torch.from_numpy(W.positions(lens)).to(dev())
     ocfg = O.LayerCfg(p.kind, p.d_model, p.n_heads, p.d_ff, p.causal, p.norm_eps, p.rope_theta,
-                      p.tau)
+                      p.tau, p.n_kv_heads, p.force_keep_last)
     return lens, stack, xd, posd, dws, ocfg
 
 
@@ -89,8 +90,9 @@ def compare_stack(p, lens, stack, xd, posd, dws, ocfg, rates, seqs_check=None, t
             k = ref["points"][pt]["k"][0]
             kg = override[layer][0]
             # the oracle's own choice given identical inputs to this point
-            kr = O.select_topk(s_ref, k)
-            swaps += check_kept_sets(s_gpu, s_ref, k, kg, kr, eps, f"seq {b} point {pt}")
+            kr = O.select_topk(s_ref, k, ocfg.force_keep_last)
+            swaps += check_kept_sets(s_gpu, s_ref, k, kg, kr, eps, f"seq {b} point {pt}",
+                                     ocfg.force_keep_last)
         fo, fe = out["cu_host"][b], out["cu_host"][b + 1]
         assert np.array_equal(pos_fin[fo:fe], ref["pos"])
         assert_rel_l2(x_fin[fo:fe], ref["x"], tol, f"seq {b} final rows")
@@ -178,3 +180,20 @@ def test_small_every_layer_schedule():
     lens, stack, xd, posd, dws, ocfg = build(p, 4, lens, sharp=3.0)
     for rates in ([0.5, 0.7, 0.3, 0.9], [0.02, 0.1, 0.05, 1.0]):
         compare_stack(p, lens, stack, xd, posd, dws, ocfg, rates)
+
+
+@pytest.mark.parametrize("hkv", [2, 1])
+def test_small_gqa_stack_keep_last(hkv):
+    # grouped-query (and multi-query) decoder, every-layer schedule, the last
+    # row of each sequence forced to survive every pruning point
+    p = W.shrink(W.PRESETS["dec1b"], n_layers=3, d_model=256, n_heads=4, d_ff=256, batch=4,
+                 prune_after=(1, 2, 3), n_kv_heads=hkv, force_keep_last=True)
+    lens = [300, 64, 129, 17]
+    lens, stack, xd, posd, dws, ocfg = build(p, 5, lens, sharp=3.0)
+    rates = [0.5, 0.3, 0.7, 0.1]
+    compare_stack(p, lens, stack, xd, posd, dws, ocfg, rates)
+    out = stack.forward(xd, posd, zsa.Seqs(lens, dev()), p.prune_after, rates)
+    torch.cuda.synchronize()
+    pos = out["pos"][: out["t_final"]].cpu().numpy()
+    cu = out["cu_host"]
+    assert [int(pos[cu[b + 1] - 1]) for b in range(len(lens))] == [n - 1 for n in lens]
