@@ -293,7 +293,7 @@ def sequence_layer(x: np.ndarray, pos: np.ndarray, w: Dict[str, Optional[np.ndar
 def layer_forward(x: np.ndarray, pos: np.ndarray, cu: Sequence[int], w: Dict,
                   cfg: LayerCfg, keep_rate: Optional[Sequence[float]] = None,
                   mode: str = "exact", kept_override: Optional[Sequence[np.ndarray]] = None,
-                  keep_intermediates: bool = False) -> Dict:
+                  keep_intermediates: bool = False, want_kv: bool = False) -> Dict:
     """One layer over a packed batch ([T, d] rows, sequence b at rows
     cu[b]..cu[b+1]). With ``keep_rate`` (one rate per sequence) the layer is
     a pruning layer: its output rows are cut down to the Eq. 2 count by
@@ -303,7 +303,7 @@ def layer_forward(x: np.ndarray, pos: np.ndarray, cu: Sequence[int], w: Dict,
     cu = [int(c) for c in cu]
     B = len(cu) - 1
     prune = keep_rate is not None
-    xs, ps, ss, kept_all, ks, lses, inter = [], [], [], [], [], [], []
+    xs, ps, ss, kept_all, ks, lses, inter, kvs = [], [], [], [], [], [], [], []
     cu_out = [0]
     for b in range(B):
         lo, hi = cu[b], cu[b + 1]
@@ -311,6 +311,8 @@ def layer_forward(x: np.ndarray, pos: np.ndarray, cu: Sequence[int], w: Dict,
         lses.append(res["lse"])
         if keep_intermediates:
             inter.append(res)
+        if want_kv:
+            kvs.append((res["k"], res["v"]))
         if prune:
             n = hi - lo
             kb = keep_count(n, float(keep_rate[b]), cfg.tau)
@@ -341,6 +343,8 @@ def layer_forward(x: np.ndarray, pos: np.ndarray, cu: Sequence[int], w: Dict,
         out["k"] = ks
     if keep_intermediates:
         out["per_seq"] = inter
+    if want_kv:
+        out["kv"] = kvs
     return out
 
 
@@ -348,24 +352,105 @@ def stack_forward(x: np.ndarray, pos: np.ndarray, cu: Sequence[int], weights: Se
                   cfg: LayerCfg, prune_after: Sequence[int], keep_rate: Sequence[float],
                   mode: str = "exact",
                   kept_override: Optional[Dict[int, Sequence[np.ndarray]]] = None,
-                  record: bool = False) -> Dict:
+                  record: bool = False, want_kv: bool = False) -> Dict:
     """The layer stack: layers 1..L in order; after each layer listed in
     ``prune_after`` (1-based) the output is pruned at the per-sequence keep
     rates. Returns the final rows, their original positions and row offsets,
     and per pruning point the scores, counts and kept positions.
     ``kept_override`` maps a 1-based layer index to per-sequence kept local
-    indices. With ``record`` every layer's output is kept too."""
+    indices. With ``record`` every layer's output is kept too. With
+    ``want_kv`` the result holds, per layer and sequence, the keys and values
+    (after RoPE) of the rows that entered that layer: the cache a decode step
+    attends to."""
     prune_set = set(int(p) for p in prune_after)
     cur_x, cur_pos, cur_cu = x, pos, np.asarray(cu, dtype=np.int64)
-    points, layers = [], []
+    points, layers, kv = [], [], []
     for l, w in enumerate(weights, start=1):
         pr = l in prune_set
         ov = kept_override.get(l) if (kept_override and pr) else None
-        res = layer_forward(cur_x, cur_pos, cur_cu, w, cfg, keep_rate if pr else None, mode, ov)
+        res = layer_forward(cur_x, cur_pos, cur_cu, w, cfg, keep_rate if pr else None, mode, ov,
+                            want_kv=want_kv)
+        if want_kv:
+            kv.append(res["kv"])
         if pr:
             points.append({"layer": l, "scores": res["scores"], "k": res["k"],
                            "kept_rows": res["kept_rows"], "pos": res["pos"], "cu": res["cu"]})
         cur_x, cur_pos, cur_cu = res["x"], res["pos"], res["cu"]
         if record:
             layers.append({"x": cur_x, "pos": cur_pos, "cu": cur_cu})
-    return {"x": cur_x, "pos": cur_pos, "cu": cur_cu, "points": points, "layers": layers}
+    return {"x": cur_x, "pos": cur_pos, "cu": cur_cu, "points": points, "layers": layers,
+            "kv": kv}
+
+
+# ---------------------------------------------------------------------------
+# generation after a pruned prefill
+# ---------------------------------------------------------------------------
+def decode_attention(q: np.ndarray, k: np.ndarray, v: np.ndarray, n_heads: int,
+                     n_kv_heads: Optional[int] = None) -> np.ndarray:
+    """Eq. 1 for one new query row over m cached rows (all of them earlier
+    positions, so the causal mask removes nothing): q [n_heads*hd], k, v
+    [m, n_kv_heads*hd]; query head h reads key/value head
+    h // (n_heads // n_kv_heads). Returns o [n_heads*hd]."""
+    d = q.shape[0]
+    hd = d // n_heads
+    hkv = n_heads if n_kv_heads is None else int(n_kv_heads)
+    group = n_heads // hkv
+    o = np.zeros(d)
+    for h in range(n_heads):
+        g = h // group
+        S = k[:, g * hd:(g + 1) * hd] @ q[h * hd:(h + 1) * hd] / math.sqrt(hd)
+        P = np.exp(S - S.max())
+        P /= P.sum()
+        o[h * hd:(h + 1) * hd] = P @ v[:, g * hd:(g + 1) * hd]
+    return o
+
+
+def decode_step(x_new: np.ndarray, pos_new: np.ndarray, cache: List[List[tuple]],
+                weights: Sequence[Dict], cfg: LayerCfg, mode: str = "exact") -> Dict:
+    """One generated token per sequence through the stack (causal models).
+
+    Reading: generated rows are never pruned; at layer l the new row of
+    sequence b attends to the keys and values of the rows that entered
+    layer l in the (pruned) prefill, plus every earlier generated row, plus
+    itself. ``cache[l][b]`` = (k, v) of those earlier rows ([m, kvd] each,
+    after RoPE); it is not modified. x_new [B, d], pos_new [B] (original
+    position of the new row). Returns the new rows' outputs "x" [B, d] and,
+    per layer and sequence, the (k, v) rows to append ("kv")."""
+    if not cfg.causal:
+        raise ValueError("decoding needs the causal mask")
+    r = _rounder(mode)
+    d = cfg.d_model
+    kvd = cfg.kv_heads * (d // cfg.n_heads)
+    x = np.asarray(x_new, dtype=np.float64)
+    appended = []
+    for l, w in enumerate(weights):
+        x1s, new_kv = [], []
+        for b in range(x.shape[0]):
+            xb = x[b:b + 1]
+            pb = np.asarray([pos_new[b]])
+            if cfg.kind == ENCODER:
+                h = r(layer_norm(xb, w["norm1_w"], w["norm1_b"], cfg.norm_eps))
+            else:
+                h = r(rms_norm(xb, w["norm1_w"], cfg.norm_eps))
+            qkv = _linear(h, w["w_qkv"], w["b_qkv"])
+            q, k, v = qkv[:, :d], qkv[:, d:d + kvd], qkv[:, d + kvd:d + 2 * kvd]
+            if cfg.kind == DECODER:
+                q = rope(q, pb, cfg.n_heads, cfg.rope_theta)
+                k = rope(k, pb, cfg.kv_heads, cfg.rope_theta)
+            q, k, v = r(q), r(k), r(v)
+            ck, cv = cache[l][b]
+            o = r(decode_attention(q[0], np.concatenate([ck, k]), np.concatenate([cv, v]),
+                                   cfg.n_heads, cfg.kv_heads))
+            x1s.append(r(xb[0] + _linear(o[None, :], w["w_o"], w["b_o"])[0]))
+            new_kv.append((k, v))
+        x1 = np.stack(x1s)
+        if cfg.kind == ENCODER:
+            h2 = r(layer_norm(x1, w["norm2_w"], w["norm2_b"], cfg.norm_eps))
+            f = r(gelu(_linear(h2, w["w_up"], w["b_up"])))
+        else:
+            h2 = r(rms_norm(x1, w["norm2_w"], cfg.norm_eps))
+            z = _linear(h2, w["w_up"], w["b_up"])
+            f = r(silu(z[:, 0::2]) * z[:, 1::2])
+        x = r(x1 + _linear(f, w["w_down"], w["b_down"]))
+        appended.append(new_kv)
+    return {"x": x, "kv": appended}

@@ -105,6 +105,12 @@ def _bf16_truncate(x):
 
 _orig_attention = O.attention
 _orig_select = O.select_topk
+_orig_decode_attention = O.decode_attention
+
+
+def _decode_attention_skips_self(q, k, v, n_heads, n_kv_heads=None):
+    # the new row does not attend to its own key/value
+    return _orig_decode_attention(q, k[:-1], v[:-1], n_heads, n_kv_heads)
 
 MUTANTS = [
     ("attention", _attention_no_scale, lambda: P.test_attention_brute_force(False)),
@@ -114,6 +120,8 @@ MUTANTS = [
     ("attention", _attention_kv_modulo, lambda: P.test_gqa_vs_torch_sdpa(True, 2)),
     ("select_topk", _select_ties_high, P.test_select_topk_brute_force),
     ("select_topk", _select_ignores_keep_last, P.test_select_topk_keep_last),
+    ("decode_attention", _decode_attention_skips_self,
+     lambda: P.test_decode_equals_forward_on_the_extended_sequence(P.W.DECODER, 2)),
     ("keep_count", _keep_count_round, P.test_keep_schedule_golden),
     ("rope", _rope_adjacent, P.test_rope_hand_example),
     ("layer_norm", _layer_norm_unbiased, P.test_layer_norm_vs_torch),

@@ -516,3 +516,68 @@ def test_stack_force_keep_last_keeps_every_last_row():
             assert pt["pos"][c[b + 1] - 1] == n - 1
     sched = O.keep_schedule(lens, [0.3, 0.5, 0.2], cfg.tau, 4)
     assert [list(pt["k"]) for pt in out["points"]] == [list(r) for r in sched]
+
+
+# ---------------------------------------------------------------- generation
+def _decode_setup(kind, lens, seed, hkv=0, n_layers=3):
+    p = W.shrink(W.PRESETS["tiny"], kind=kind, causal=True, n_layers=n_layers, batch=len(lens),
+                 d_model=64, n_heads=4, d_ff=128, n_kv_heads=hkv)
+    ws = [{k: (None if v is None else v.astype(np.float64)) for k, v in wd.items()}
+          for wd in W.stack_weights(p, seed, norm_jitter=True)]
+    for wd in ws:
+        wd["w_qkv"] *= 10.0
+    cfg = O.LayerCfg(kind, p.d_model, p.n_heads, p.d_ff, True, n_kv_heads=hkv)
+    return p, ws, cfg
+
+
+@pytest.mark.parametrize("kind,hkv", [(W.DECODER, 0), (W.DECODER, 2), (W.ENCODER, 0)])
+def test_decode_equals_forward_on_the_extended_sequence(kind, hkv):
+    # without pruning, a causal model's output for a new last row is the
+    # last output row of the forward over the sequence with that row appended;
+    # two steps in a row are the forward with two rows appended
+    lens = [11, 6, 1]
+    p, ws, cfg = _decode_setup(kind, lens, 3, hkv)
+    full = [n + 2 for n in lens]
+    cuf = W.cu_seqlens(full)
+    xf = W.hidden(p, 3, full).astype(np.float64)
+    xp = np.concatenate([xf[cuf[b]:cuf[b] + n] for b, n in enumerate(lens)])
+    pre = O.stack_forward(xp, W.positions(lens).astype(np.int64), W.cu_seqlens(lens), ws, cfg, (),
+                          [1.0] * 3, want_kv=True)
+    ref = O.stack_forward(xf, W.positions(full).astype(np.int64), cuf, ws, cfg, (), [1.0] * 3)
+    cache = pre["kv"]
+    for step in range(2):
+        xn = np.stack([xf[cuf[b] + n + step] for b, n in enumerate(lens)])
+        dec = O.decode_step(xn, np.array(lens) + step, cache, ws, cfg)
+        want = np.stack([ref["x"][cuf[b] + n + step] for b, n in enumerate(lens)])
+        assert np.allclose(dec["x"], want, rtol=1e-11, atol=1e-12)
+        cache = [[(np.concatenate([ck, nk]), np.concatenate([cv, nv]))
+                  for (ck, cv), (nk, nv) in zip(cache[l], dec["kv"][l])] for l in range(len(ws))]
+
+
+def test_decode_after_pruned_prefill():
+    # with pruning, the prefill's first n rows do not see the new row (causal),
+    # so the decode output equals the forward over n + 1 rows whose pruning
+    # points keep the prefill's kept rows plus the new (last) row
+    lens = [30, 12]
+    p, ws, cfg = _decode_setup(W.DECODER, lens, 9, hkv=2)
+    prune, rates = (1, 2), [0.4, 0.5]
+    full = [n + 1 for n in lens]
+    cuf = W.cu_seqlens(full)
+    xf = W.hidden(p, 9, full).astype(np.float64)
+    for b, n in enumerate(lens):
+        xp = xf[cuf[b]:cuf[b] + n]
+        pre = O.stack_forward(xp, np.arange(n), [0, n], ws, cfg, prune, [rates[b]], want_kv=True)
+        override = {}
+        m = n
+        for pt in pre["points"]:
+            kept = pt["kept_rows"]                 # local indices among the m rows entering
+            override[pt["layer"]] = [np.concatenate([kept, [m]])]
+            m = len(kept)
+        ext = O.stack_forward(xf[cuf[b]:cuf[b + 1]], np.arange(n + 1), [0, n + 1], ws, cfg, prune,
+                              [rates[b]], kept_override=override)
+        cache = [[layer_kv[0]] for layer_kv in pre["kv"]]
+        dec = O.decode_step(xf[cuf[b] + n][None, :], np.array([n]), cache, ws, cfg)
+        assert np.allclose(dec["x"][0], ext["x"][-1], rtol=1e-11, atol=1e-12)
+        # and the cache it used holds exactly the rows entering each layer
+        sizes = [n] + [len(pt["kept_rows"]) for pt in pre["points"]]
+        assert [pre["kv"][l][0][0].shape[0] for l in range(3)] == [sizes[0], sizes[1], sizes[2]]
