@@ -274,6 +274,13 @@ size_t zsa_layer_workspace_size(const zsa_layer_cfg* cfg, int32_t total_rows, in
  *   scores_dbg fp32 device or NULL: the scores at each pruning point,
  *     concatenated (point p occupies the rows entering that block)
  *   pos_dbg int32 device or NULL: pos after each pruning point, concatenated
+ *   kv_cache device or NULL (causal stacks only): the key/value cache a
+ *     decode step attends to (see zsa_decode_step). Block l writes the k
+ *     (after RoPE) and v of the rows that entered it, sequence b's row r at
+ *     ((l * batch + b) * kv_capacity + r) * 2*kvd elements, k in the first
+ *     kvd = kv_heads*head_dim and v in the next kvd, dtype. kv_capacity >=
+ *     the longest input sequence. The rows a sequence has at block l are
+ *     its count after the last pruning point before l.
  *   ws >= zsa_stack_workspace_size(cfg, T, batch, n_prune)
  * No host synchronisation: every shape follows from cu_host and keep_rate.
  */
@@ -283,9 +290,30 @@ int zsa_stack_forward(void* stream, const zsa_layer_cfg* cfg, const zsa_layer_we
                       int32_t batch, const int32_t* cu_host, const int32_t* cu_dev,
                       void* hidden_out, int32_t* pos_out, int32_t* cu_out_host,
                       int32_t* cu_out_dev, int32_t* counts_out_host, float* scores_dbg,
-                      int32_t* pos_dbg, void* ws, size_t ws_bytes);
+                      int32_t* pos_dbg, void* kv_cache, int32_t kv_capacity, void* ws,
+                      size_t ws_bytes);
 size_t zsa_stack_workspace_size(const zsa_layer_cfg* cfg, int32_t total_rows, int32_t batch,
                                 int32_t n_prune);
+
+/* ---------------------------------------------------------------------
+ * One generated row per sequence through the stack, after a prefill that
+ * filled kv_cache (zsa_stack_forward). Generated rows are never pruned: at
+ * block l the new row of sequence b attends (Eq. 1) to the kv_len_host[l *
+ * batch + b] rows already in that block's cache (the rows that entered
+ * block l in the pruned prefill, then earlier generated rows) and to
+ * itself; its own k / v are appended at that row of the cache. The caller
+ * adds 1 to every kv_len after the call.
+ *   x_in, x_out [batch, d] dtype device (may alias); pos_host [batch] the
+ *   original position of each new row (RoPE); kv_len_host [n_layers*batch]
+ *   host, each < kv_capacity; ws >= zsa_decode_workspace_size(cfg, batch,
+ *   kv_capacity). Causal stacks, bf16, head_dim 64 or 128, 1/2/4/8 query
+ *   heads per key/value head; otherwise ZSA_EUNSUPPORTED.
+ */
+int zsa_decode_step(void* stream, const zsa_layer_cfg* cfg, const zsa_layer_weights* w,
+                    int32_t n_layers, int32_t batch, const void* x_in, const int32_t* pos_host,
+                    void* kv_cache, int32_t kv_capacity, const int32_t* kv_len_host, void* x_out,
+                    void* ws, size_t ws_bytes);
+size_t zsa_decode_workspace_size(const zsa_layer_cfg* cfg, int32_t batch, int32_t kv_capacity);
 
 /* ---------------------------------------------------------------------
  * Timing hook (profiling aid, not thread-safe): while armed, the next

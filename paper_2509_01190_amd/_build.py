@@ -27,6 +27,7 @@ SOURCES = [
     "k_score.hip",
     "k_select.hip",
     "k_gather.hip",
+    "k_decode.hip",
 ]
 
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")

@@ -254,7 +254,7 @@ void fill_rope(zsa::EpiParams& ep, int hd, float theta) {
 int run_layer(hipStream_t s, const zsa_layer_cfg& c, const zsa_layer_weights& w,
               const void* x_in, const int32_t* pos_in, const RowSet& in, bool prune,
               const RowSet& out, void* x_out, int32_t* pos_out, float* scores_out,
-              int32_t* kept_out, const LayerBufs& wb) {
+              int32_t* kept_out, const LayerBufs& wb, void* kv_layer = nullptr, int kv_cap = 0) {
   using namespace zsa;
   const int dt = c.dtype;
   const size_t e = esize(dt);
@@ -282,6 +282,10 @@ int run_layer(hipStream_t s, const zsa_layer_cfg& c, const zsa_layer_weights& w,
     HIP_TRY(launch_gemm(s, dt, wb.h, in.T, d, w.w_qkv, qw, ep, wb.splitk, wb.splitk_bytes),
             "qkv projection");
   }
+  if (kv_layer != nullptr)  // the rows entering this layer, for generation
+    HIP_TRY(launch_kv_store(s, dt, wb.qkv, qw, d, kvd, in.B, in.max_len, in.cu_dev, nullptr,
+                            kv_layer, kv_cap),
+            "kv cache");
   const char* qkv = static_cast<const char*>(wb.qkv);
   const void* q = qkv;
   const void* k = qkv + d * e;
@@ -689,7 +693,8 @@ int zsa_stack_forward(void* stream, const zsa_layer_cfg* cfg, const zsa_layer_we
                       int32_t batch, const int32_t* cu_host, const int32_t* cu_dev,
                       void* hidden_out, int32_t* pos_out, int32_t* cu_out_host,
                       int32_t* cu_out_dev, int32_t* counts_out_host, float* scores_dbg,
-                      int32_t* pos_dbg, void* ws, size_t ws_bytes) {
+                      int32_t* pos_dbg, void* kv_cache, int32_t kv_capacity, void* ws,
+                      size_t ws_bytes) {
   CHECK(check_cfg(cfg));
   if (n_layers < 1) return fail(ZSA_EINVAL, "n_layers %d < 1", n_layers);
   if (w == nullptr) return fail(ZSA_EINVAL, "weights are NULL");
@@ -714,6 +719,12 @@ int zsa_stack_forward(void* stream, const zsa_layer_cfg* cfg, const zsa_layer_we
     if (pos_in == nullptr || pos_out == nullptr) return fail(ZSA_EINVAL, "pos_in / pos_out is NULL");
   }
   if (cu_out_host == nullptr || cu_out_dev == nullptr) return fail(ZSA_EINVAL, "cu_out is NULL");
+  if (kv_cache != nullptr) {
+    if (!cfg->causal) return fail(ZSA_EINVAL, "a key/value cache needs the causal mask");
+    CHECK(check_ptr16(kv_cache, "kv_cache"));
+    if (kv_capacity < max_len0)
+      return fail(ZSA_ESHAPE, "kv_capacity %d below the longest sequence %d", kv_capacity, max_len0);
+  }
   const size_t need = zsa_stack_workspace_size(cfg, T0, batch, n_prune);
   if (ws_bytes < need || ws == nullptr) return fail(ZSA_EWORKSPACE, "workspace %zu < %zu", ws_bytes, need);
 
@@ -756,13 +767,18 @@ int zsa_stack_forward(void* stream, const zsa_layer_cfg* cfg, const zsa_layer_we
     const bool last = l == n_layers;
     const bool prune = point < n_prune && prune_after[point] == l;
     void* x_out = last ? hidden_out : xbuf[(l - 1) & 1];
+    void* kv_layer = kv_cache == nullptr
+                         ? nullptr
+                         : static_cast<char*>(kv_cache) + static_cast<size_t>(l - 1) * batch *
+                                                              kv_capacity * 2 * kv_heads(*cfg) *
+                                                              cfg->head_dim * esize(cfg->dtype);
     if (prune) {
       const RowSet nxt{batch, cus[point + 1].data(), meta + static_cast<size_t>(point) * (batch + 1),
                        cus[point + 1][batch], maxl[point + 1]};
       int32_t* pos_next = last ? pos_out : posbuf[point & 1];
       float* sdbg = scores_dbg != nullptr ? scores_dbg + score_off : nullptr;
       CHECK(run_layer(s, *cfg, w[l - 1], cur_x, cur_pos, cur, true, nxt, x_out, pos_next, sdbg,
-                      nullptr, wb));
+                      nullptr, wb, kv_layer, kv_capacity));
       if (pos_dbg != nullptr)
         HIP_TRY(zsa::launch_copy_i32(s, pos_dbg + pos_off, pos_next, nxt.T), "pos debug copy");
       score_off += cur.T;
@@ -772,12 +788,174 @@ int zsa_stack_forward(void* stream, const zsa_layer_cfg* cfg, const zsa_layer_we
       ++point;
     } else {
       CHECK(run_layer(s, *cfg, w[l - 1], cur_x, cur_pos, cur, false, cur, x_out, nullptr, nullptr,
-                      nullptr, wb));
+                      nullptr, wb, kv_layer, kv_capacity));
     }
     cur_x = x_out;
   }
   if (T0 > 0 && cur_pos != pos_out) HIP_TRY(zsa::launch_copy_i32(s, pos_out, cur_pos, cur.T), "pos copy");
   memcpy(cu_out_host, cus[n_prune].data(), sizeof(int32_t) * (batch + 1));
+  return ZSA_OK;
+}
+
+// ---------------------------------------------------------------------------
+// generation after a pruned prefill
+// ---------------------------------------------------------------------------
+struct DecodeLayout {
+  size_t h, qkv, o, f, m, l, op, pos, cu, len, splitk, splitk_bytes, end;
+};
+
+DecodeLayout decode_layout(const zsa_layer_cfg* c, int32_t batch, int32_t cap) {
+  const size_t e = esize(c->dtype);
+  const int64_t d = c->d_model, F = c->d_ff, qw = qkv_width(*c);
+  const int S = zsa::decode_splits(cap);
+  const size_t part = static_cast<size_t>(batch) * c->n_heads * S;
+  Carver cv;
+  DecodeLayout L;
+  L.h = cv.take(batch * d * e);
+  L.qkv = cv.take(batch * qw * e);
+  L.o = cv.take(batch * d * e);
+  L.f = cv.take(batch * F * e);
+  L.m = cv.take(part * 4);
+  L.l = cv.take(part * 4);
+  L.op = cv.take(part * c->head_dim * 4);
+  L.pos = cv.take(static_cast<size_t>(batch) * 4);
+  L.cu = cv.take(static_cast<size_t>(batch + 1) * 4);
+  L.len = cv.take(static_cast<size_t>(2 * batch) * 4);
+  const int dt = c->dtype;
+  const int up_n = c->kind == ZSA_DECODER ? 2 * c->d_ff : c->d_ff;
+  L.splitk_bytes = std::max({zsa::gemm_workspace_bound(dt, batch, static_cast<int>(qw), c->d_model),
+                             zsa::gemm_workspace_bound(dt, batch, c->d_model, c->d_model),
+                             zsa::gemm_workspace_bound(dt, batch, up_n, c->d_model),
+                             zsa::gemm_workspace_bound(dt, batch, c->d_model, c->d_ff)});
+  L.splitk = cv.take(L.splitk_bytes);
+  L.end = cv.off;
+  return L;
+}
+
+size_t zsa_decode_workspace_size(const zsa_layer_cfg* cfg, int32_t batch, int32_t kv_capacity) {
+  if (cfg == nullptr || batch < 0 || kv_capacity < 1) return 0;
+  return decode_layout(cfg, batch, kv_capacity).end;
+}
+
+int zsa_decode_step(void* stream, const zsa_layer_cfg* cfg, const zsa_layer_weights* w,
+                    int32_t n_layers, int32_t batch, const void* x_in, const int32_t* pos_host,
+                    void* kv_cache, int32_t kv_capacity, const int32_t* kv_len_host, void* x_out,
+                    void* ws, size_t ws_bytes) {
+  using namespace zsa;
+  CHECK(check_cfg(cfg));
+  const zsa_layer_cfg& c = *cfg;
+  const int d = c.d_model, H = c.n_heads, hd = c.head_dim, F = c.d_ff;
+  const int kvd = kv_heads(c) * hd, qw = static_cast<int>(qkv_width(c)), kvg = H / kv_heads(c);
+  if (!c.causal) return fail(ZSA_EINVAL, "decoding needs the causal mask");
+  if (!decode_supported(c.dtype, hd, kvg))
+    return fail(ZSA_EUNSUPPORTED, "decode: bf16 with head_dim 64 or 128 and 1, 2, 4 or 8 query "
+                                  "heads per key/value head");
+  if (n_layers < 1 || w == nullptr) return fail(ZSA_EINVAL, "n_layers %d / weights", n_layers);
+  if (batch < 0) return fail(ZSA_EINVAL, "batch %d", batch);
+  if (batch == 0) return ZSA_OK;
+  if (kv_capacity < 1) return fail(ZSA_EINVAL, "kv_capacity %d", kv_capacity);
+  CHECK(check_ptr16(x_in, "x_in"));
+  CHECK(check_ptr16(x_out, "x_out"));
+  CHECK(check_ptr16(kv_cache, "kv_cache"));
+  if (pos_host == nullptr || kv_len_host == nullptr) return fail(ZSA_EINVAL, "pos / kv_len is NULL");
+  for (int i = 0; i < n_layers * batch; ++i)
+    if (kv_len_host[i] < 0 || kv_len_host[i] >= kv_capacity)
+      return fail(ZSA_ESHAPE, "kv_len[%d] = %d leaves no room below kv_capacity %d", i,
+                  kv_len_host[i], kv_capacity);
+  const DecodeLayout L = decode_layout(cfg, batch, kv_capacity);
+  if (ws == nullptr || ws_bytes < L.end)
+    return fail(ZSA_EWORKSPACE, "workspace %zu < %zu", ws_bytes, L.end);
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  char* base = static_cast<char*>(ws);
+  void* h = base + L.h;
+  void* qkv = base + L.qkv;
+  void* o = base + L.o;
+  void* f = base + L.f;
+  int32_t* pos_dev = reinterpret_cast<int32_t*>(base + L.pos);
+  int32_t* cu_dev = reinterpret_cast<int32_t*>(base + L.cu);
+  int32_t* len_dev = reinterpret_cast<int32_t*>(base + L.len);
+  void* splitk = L.splitk_bytes ? base + L.splitk : nullptr;
+  const bool dec = c.kind == ZSA_DECODER;
+  const int norm_kind = dec ? ZSA_NORM_RMS : ZSA_NORM_LAYER;
+  const size_t e = esize(c.dtype);
+  const size_t layer_bytes = static_cast<size_t>(batch) * kv_capacity * 2 * kvd * e;
+
+  std::vector<int32_t> unit(batch + 1);
+  for (int b = 0; b <= batch; ++b) unit[b] = b;
+  HIP_TRY(launch_upload_i32(s, pos_dev, pos_host, batch), "upload");
+  HIP_TRY(launch_upload_i32(s, cu_dev, unit.data(), batch + 1), "upload");
+  std::vector<int32_t> lens(2 * batch);
+  for (int l = 0; l < n_layers; ++l) {
+    const zsa_layer_weights& wl = w[l];
+    const void* xin = l == 0 ? x_in : x_out;
+    void* cache_l = static_cast<char*>(kv_cache) + l * layer_bytes;
+    int max_n = 0;
+    for (int b = 0; b < batch; ++b) {
+      lens[b] = kv_len_host[l * batch + b];          // where the new row goes
+      lens[batch + b] = lens[b] + 1;                 // rows attended, the new one included
+      max_n = std::max(max_n, lens[batch + b]);
+    }
+    HIP_TRY(launch_upload_i32(s, len_dev, lens.data(), 2 * batch), "upload");
+    HIP_TRY(launch_norm(s, c.dtype, norm_kind, xin, wl.norm1_w, dec ? nullptr : wl.norm1_b, batch,
+                        d, c.norm_eps, h),
+            "norm1");
+    {
+      EpiParams ep{};
+      ep.epi = dec ? EPI_ROPE : EPI_NONE;
+      ep.bias = wl.b_qkv;
+      ep.y = qkv;
+      ep.ldy = qw;
+      ep.pos = pos_dev;
+      ep.head_dim = hd;
+      ep.rope_cols = dec ? d + kvd : 0;
+      if (dec) fill_rope(ep, hd, c.rope_theta);
+      HIP_TRY(launch_gemm(s, c.dtype, h, batch, d, wl.w_qkv, qw, ep, splitk, L.splitk_bytes),
+              "qkv projection");
+    }
+    HIP_TRY(launch_kv_store(s, c.dtype, qkv, qw, d, kvd, batch, 1, cu_dev, len_dev, cache_l,
+                            kv_capacity),
+            "kv append");
+    HIP_TRY(launch_decode_attention(s, qkv, qw, cache_l, kv_capacity, hd, H, kv_heads(c),
+                                    len_dev + batch, batch, decode_splits(max_n),
+                                    1.0f / sqrtf(static_cast<float>(hd)),
+                                    reinterpret_cast<float*>(base + L.m),
+                                    reinterpret_cast<float*>(base + L.l),
+                                    reinterpret_cast<float*>(base + L.op), o, d),
+            "decode attention");
+    {
+      EpiParams ep{};
+      ep.epi = EPI_RESIDUAL;
+      ep.bias = wl.b_o;
+      ep.residual = xin;
+      ep.y = x_out;
+      ep.ldy = d;
+      HIP_TRY(launch_gemm(s, c.dtype, o, batch, d, wl.w_o, d, ep, splitk, L.splitk_bytes),
+              "output projection");
+    }
+    HIP_TRY(launch_norm(s, c.dtype, norm_kind, x_out, wl.norm2_w, dec ? nullptr : wl.norm2_b,
+                        batch, d, c.norm_eps, h),
+            "norm2");
+    {
+      EpiParams ep{};
+      ep.epi = dec ? EPI_SWIGLU : EPI_GELU;
+      ep.bias = wl.b_up;
+      ep.y = f;
+      ep.ldy = F;
+      HIP_TRY(launch_gemm(s, c.dtype, h, batch, d, wl.w_up, dec ? 2 * F : F, ep, splitk,
+                          L.splitk_bytes),
+              "up projection");
+    }
+    {
+      EpiParams ep{};
+      ep.epi = EPI_RESIDUAL;
+      ep.bias = wl.b_down;
+      ep.residual = x_out;
+      ep.y = x_out;
+      ep.ldy = d;
+      HIP_TRY(launch_gemm(s, c.dtype, f, batch, F, wl.w_down, d, ep, splitk, L.splitk_bytes),
+              "down projection");
+    }
+  }
   return ZSA_OK;
 }
 

@@ -160,6 +160,19 @@ hipError_t launch_select(hipStream_t s, const float* partials, int groups, int T
                          int max_len, const int32_t* cu_in_dev, const int32_t* cu_out_dev,
                          int32_t* kept_rows, float* scores_out, int keep_last);
 
+// generation: key/value cache rows and the attention of one new row per
+// sequence (cache layout [batch][cap][k | v] per layer, kvd = H_kv * hd)
+hipError_t launch_kv_store(hipStream_t s, int dtype, const void* src, int64_t src_stride,
+                           int src_col, int kvd, int B, int max_rows, const int32_t* cu_dev,
+                           const int32_t* start_dev, void* cache_layer, int cap);
+hipError_t launch_decode_attention(hipStream_t s, const void* q, int64_t q_stride,
+                                   const void* cache_layer, int cap, int hd, int H, int Hkv,
+                                   const int32_t* len_dev, int B, int S, float scale,
+                                   float* m_part, float* l_part, float* o_part, void* out,
+                                   int64_t out_stride);
+int decode_splits(int max_len);
+bool decode_supported(int dtype, int hd, int group);
+
 // row gather of up to two [*, d] arrays plus pos
 hipError_t launch_gather(hipStream_t s, int dtype, int d, int t_in, const int32_t* kept,
                          int t_out, const void* src0, void* dst0, const void* src1, void* dst1,

@@ -83,7 +83,10 @@ _SIGS = {
     "zsa_stack_forward": (ctypes.c_int, [_vp, ctypes.POINTER(LayerCfg),
                                          ctypes.POINTER(LayerWeights), _i32, _pi32, _i32, _pf64,
                                          _vp, _vp, _i32, _pi32, _vp, _vp, _vp, _pi32, _vp, _pi32,
-                                         _vp, _vp, _vp, _sz]),
+                                         _vp, _vp, _vp, _i32, _vp, _sz]),
+    "zsa_decode_step": (ctypes.c_int, [_vp, ctypes.POINTER(LayerCfg), ctypes.POINTER(LayerWeights),
+                                       _i32, _i32, _vp, _pi32, _vp, _i32, _pi32, _vp, _vp, _sz]),
+    "zsa_decode_workspace_size": (_sz, [ctypes.POINTER(LayerCfg), _i32, _i32]),
     "zsa_stack_workspace_size": (_sz, [ctypes.POINTER(LayerCfg), _i32, _i32, _i32]),
     "zsa_timing_arm": (ctypes.c_int, [_i32, _i32]),
     "zsa_timing_read": (ctypes.c_int, [_i32, _pi32, ctypes.POINTER(ctypes.c_double)]),
@@ -415,12 +418,59 @@ class Stack:
         rows_in = [seqs.total] + [int(c.sum()) for c in counts]
         return {"counts": counts, "final_rows": final, "rows_in": rows_in}
 
+    def kv_cache(self, batch: int, capacity: int, device) -> torch.Tensor:
+        """An empty key/value cache [layers, batch, capacity, 2 * kvd]."""
+        kvd = (self.cfg.n_kv_heads or self.cfg.n_heads) * self.cfg.head_dim
+        dtype = torch.bfloat16 if self.cfg.dtype == BF16 else torch.float32
+        return torch.empty((self.n_layers, batch, capacity, 2 * kvd), dtype=dtype, device=device)
+
+    def kv_lengths(self, seqs: Seqs, prune_after: Sequence[int], keep_rate) -> np.ndarray:
+        """Rows each sequence has in each layer's cache after a prefill:
+        [layers, batch] int32 (the count after the last pruning point before
+        the layer)."""
+        counts = self.plan(seqs, prune_after, keep_rate)["counts"]
+        cur = np.asarray(seqs.lengths, dtype=np.int32)
+        out = np.zeros((self.n_layers, seqs.batch), dtype=np.int32)
+        pset = list(prune_after)
+        point = 0
+        for l in range(1, self.n_layers + 1):
+            out[l - 1] = cur
+            if point < len(pset) and pset[point] == l:
+                cur = np.asarray(counts[point], dtype=np.int32)
+                point += 1
+        return out
+
+    def decode_step(self, x_new: torch.Tensor, pos_new, kv_cache: torch.Tensor,
+                    kv_len: np.ndarray, out: Optional[torch.Tensor] = None) -> torch.Tensor:
+        """One generated row per sequence (x_new [batch, d]) at original
+        positions pos_new; appends its k / v to kv_cache at rows kv_len
+        ([layers, batch] host, incremented in place) and returns the
+        outputs [batch, d]."""
+        _require_cuda(x_new, kv_cache)
+        batch = x_new.shape[0]
+        if kv_cache.shape[:2] != (self.n_layers, batch) or not kv_cache.is_contiguous():
+            raise ValueError("kv_cache must be a contiguous [layers, batch, capacity, 2*kvd] tensor")
+        cap = kv_cache.shape[2]
+        lens = np.ascontiguousarray(kv_len, dtype=np.int32)
+        if lens.shape != (self.n_layers, batch):
+            raise ValueError("kv_len must be [layers, batch]")
+        y = torch.empty_like(x_new) if out is None else out
+        wsz = int(lib().zsa_decode_workspace_size(ctypes.byref(self.cfg), batch, cap))
+        ws = torch.empty(max(wsz, 1), dtype=torch.uint8, device=x_new.device)
+        _check(lib().zsa_decode_step(_stream(x_new.device), ctypes.byref(self.cfg), self._wstructs,
+                                     self.n_layers, batch, _p(x_new), _hp32(_host_i32(pos_new)),
+                                     _p(kv_cache), cap, _hp32(lens), _p(y), _p(ws), wsz))
+        kv_len += 1
+        return y
+
     def forward(self, hidden: torch.Tensor, pos: torch.Tensor, seqs: Seqs,
                 prune_after: Sequence[int], keep_rate, debug: bool = False,
-                out: Optional[Dict] = None) -> Dict:
+                out: Optional[Dict] = None, kv_cache: Optional[torch.Tensor] = None) -> Dict:
         """The whole stack. With ``out`` (a dict from a previous call with the
         same shapes) the outputs are written into its tensors again, so the
-        call allocates nothing and may be captured in a HIP graph."""
+        call allocates nothing and may be captured in a HIP graph. With
+        ``kv_cache`` (from ``kv_cache()``) every layer's keys and values are
+        stored for decoding."""
         _require_cuda(hidden, pos)
         dev = hidden.device
         pa = _host_i32(prune_after)
@@ -451,7 +501,8 @@ class Stack:
             seqs.batch, _hp32(seqs.host), _p(seqs.dev), _p(out["x"]), _p(out["pos"]),
             _hp32(out["cu_host"]), _p(out["cu_dev"]),
             _hp32(out["counts"]) if len(out["pa"]) else None,
-            _p(out.get("scores_dbg")), _p(out.get("pos_dbg")), _p(ws), ws.numel()))
+            _p(out.get("scores_dbg")), _p(out.get("pos_dbg")), _p(kv_cache),
+            0 if kv_cache is None else kv_cache.shape[2], _p(ws), ws.numel()))
         return out
 
 

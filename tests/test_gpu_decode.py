@@ -1,0 +1,90 @@
+"""Generation after a pruned prefill: the key/value cache the stack writes
+and the decode step over it, against the oracle continued on the GPU's kept
+sets (generated rows are never pruned)."""
+import numpy as np
+import pytest
+import torch
+
+from oracle import zsa_oracle as O
+from paper_2509_01190_amd import workloads as W
+from paper_2509_01190_amd import zsa
+from tests.helpers import assert_rel_l2, assert_rows_close, dev, f64, to_dev, weights_f64
+from tests.test_gpu_stack import build, gpu_kept_overrides
+
+pytestmark = pytest.mark.gpu
+
+
+CASES = [
+    # kind, kv heads, pruning points, force_keep_last, head_dim
+    (W.DECODER, 2, (1, 2), True, 64),
+    (W.DECODER, 1, (2,), False, 128),
+    (W.ENCODER, 0, (1,), True, 64),
+    (W.DECODER, 4, (), False, 64),
+]
+
+
+@pytest.mark.parametrize("kind,hkv,prune,keep_last,hd", CASES)
+def test_prefill_cache_and_decode(kind, hkv, prune, keep_last, hd):
+    H = 4
+    p = W.shrink(W.PRESETS["dec1b"], kind=kind, causal=True, n_layers=3, d_model=H * hd,
+                 n_heads=H, d_ff=256, batch=3, prune_after=prune, n_kv_heads=hkv,
+                 force_keep_last=keep_last)
+    lens = [200, 33, 129]
+    lens, stack, xd, posd, dws, ocfg = build(p, 6, lens, sharp=3.0)
+    seqs = zsa.Seqs(lens, dev())
+    rates = [0.5, 0.3, 0.7]
+    cap = max(lens) + 3
+    cache = stack.kv_cache(len(lens), cap, dev())
+    out = stack.forward(xd, posd, seqs, p.prune_after, rates, debug=True, kv_cache=cache)
+    torch.cuda.synchronize()
+    kv_len = stack.kv_lengths(seqs, p.prune_after, rates)
+    overrides = gpu_kept_overrides(p, lens, seqs, out) if prune else [{} for _ in lens]
+    x_all = f64(xd)
+    ws64 = [weights_f64(w) for w in dws]
+    kvd = p.kv_heads * hd
+    caches = {"exact": [], "bf16": []}
+    for b, n in enumerate(lens):
+        lo = int(seqs.host[b])
+        for mode in caches:
+            ref = O.stack_forward(x_all[lo:lo + n], np.arange(n), [0, n], ws64, ocfg, p.prune_after,
+                                  [rates[b]], mode=mode, kept_override=overrides[b], want_kv=True)
+            caches[mode].append([ref["kv"][l][0] for l in range(p.n_layers)])
+    # the cache rows the prefill stored
+    gc = f64(cache)
+    for l in range(p.n_layers):
+        for b in range(len(lens)):
+            k_ref, v_ref = caches["bf16"][b][l]
+            m = int(kv_len[l, b])
+            assert m == k_ref.shape[0]
+            got = gc[l, b, :m]
+            assert_rows_close(got[:, :kvd], k_ref, 5e-2, f"layer {l} seq {b} k")
+            assert_rows_close(got[:, kvd:], v_ref, 5e-2, f"layer {l} seq {b} v")
+    # two generated rows per sequence
+    g = np.random.default_rng(17)
+    ocache = {mode: [[caches[mode][b][l] for b in range(len(lens))] for l in range(p.n_layers)]
+              for mode in caches}
+    for step in range(2):
+        x_new = to_dev(g.standard_normal((len(lens), p.d_model)).astype(np.float32), "bf16")
+        pos_new = [n + step for n in lens]
+        before = kv_len.copy()
+        y = stack.decode_step(x_new, pos_new, cache, kv_len)
+        y2 = stack.decode_step(x_new, pos_new, cache, before.copy())   # same rows again
+        torch.cuda.synchronize()
+        assert torch.equal(y, y2)
+        assert np.array_equal(kv_len, before + 1)
+        x64 = f64(x_new)
+        res = {mode: O.decode_step(x64, np.array(pos_new), ocache[mode], ws64, ocfg, mode=mode)
+               for mode in ocache}
+        assert_rel_l2(f64(y), res["exact"]["x"], 2e-2, f"decode step {step}")
+        assert_rows_close(f64(y), res["bf16"]["x"], 5e-2, f"decode step {step}")
+        gc = f64(cache)
+        for l in range(p.n_layers):
+            for b in range(len(lens)):
+                nk, nv = res["bf16"]["kv"][l][b]
+                row = gc[l, b, before[l, b]]
+                assert_rows_close(row[None, :kvd], nk, 5e-2, f"appended k, layer {l} seq {b}")
+                assert_rows_close(row[None, kvd:], nv, 5e-2, f"appended v, layer {l} seq {b}")
+        for mode in ocache:
+            ocache[mode] = [[(np.concatenate([ocache[mode][l][b][0], res[mode]["kv"][l][b][0]]),
+                              np.concatenate([ocache[mode][l][b][1], res[mode]["kv"][l][b][1]]))
+                             for b in range(len(lens))] for l in range(p.n_layers)]

@@ -33,6 +33,30 @@ def build(p, seed, lens=None, norm_jitter=True, sharp=1.0):
     return lens, stack, xd, posd, dws, ocfg
 
 
+def gpu_kept_overrides(p, lens, seqs, out):
+    """Per sequence, the GPU's kept sets at every pruning point as local row
+    indices among the rows entering that point (for kept_override)."""
+    n_pts = len(p.prune_after)
+    rows_in = out["rows_in"]
+    pos_dbg = out["pos_dbg"].cpu().numpy()
+    cus = [seqs.host.astype(np.int64)]
+    for pt in range(n_pts):
+        c = np.zeros(len(lens) + 1, dtype=np.int64)
+        c[1:] = np.cumsum(out["counts"][pt])
+        cus.append(c)
+    p_off = np.concatenate([[0], np.cumsum(rows_in[1:n_pts + 1])])
+    overrides = []
+    for b, n in enumerate(lens):
+        posb = np.arange(n)
+        override = {}
+        for pt, layer in enumerate(p.prune_after):
+            prev_pos = posb if pt == 0 else pos_dbg[p_off[pt - 1] + cus[pt][b]:p_off[pt - 1] + cus[pt][b + 1]]
+            kept_pos = pos_dbg[p_off[pt] + cus[pt + 1][b]:p_off[pt] + cus[pt + 1][b + 1]]
+            override[layer] = [np.searchsorted(prev_pos, kept_pos)]
+        overrides.append(override)
+    return overrides
+
+
 def compare_stack(p, lens, stack, xd, posd, dws, ocfg, rates, seqs_check=None, tol=None,
                   eps=None, exact_only=False):
     """Run the stack on the GPU (with debug outputs) and check it against the
