@@ -314,6 +314,8 @@ def measure(p, rates, args, torch, W, zsa, dev, timing):
         ms = (time.perf_counter() - t0) * 1e3 / args.steps
         plan = stack.plan(seqs, p.prune_after, kr)
         r = {"ms": ms, "tok_s": tokens / (ms * 1e-3), "kept_rows_final": plan["final_rows"]}
+        if p.causal and p.force_keep_last:
+            r["decode_ms"] = decode_ms(p, stack, xd, posd, seqs, kr, lens, outs, args, torch, dev)
         if timing:
             # per-class launch durations of one eager forward (HIP events on the stream)
             for c in range(len(zsa.KCLASS_NAMES)):
@@ -367,6 +369,35 @@ def ceilings(torch, dev):
     return out
 
 
+def decode_ms(p, stack, xd, posd, seqs, kr, lens, outs, args, torch, dev):
+    """Time of one generated row per sequence after the pruned prefill at
+    this keep rate (the cache then holds each layer's kept rows), as a
+    replayed HIP graph at a fixed cache length."""
+    cap = max(lens) + 8
+    cache = stack.kv_cache(seqs.batch, cap, dev)
+    stack.forward(xd, posd, seqs, p.prune_after, kr, out=outs, kv_cache=cache)
+    lens0 = stack.kv_lengths(seqs, p.prune_after, kr)
+    g = torch.Generator().manual_seed(args.seed)
+    x_new = torch.randn(seqs.batch, p.d_model, generator=g).to(torch.bfloat16).to(dev)
+    y = stack.decode_step(x_new, lens, cache, lens0.copy())
+    torch.cuda.synchronize()
+    graph = torch.cuda.CUDAGraph()
+    s = torch.cuda.Stream()
+    s.wait_stream(torch.cuda.current_stream())
+    with torch.cuda.stream(s):
+        with torch.cuda.graph(graph, stream=s):
+            stack.decode_step(x_new, lens, cache, lens0.copy(), out=y)
+    torch.cuda.current_stream().wait_stream(s)
+    for _ in range(args.warmup):
+        graph.replay()
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for _ in range(args.steps):
+        graph.replay()
+    torch.cuda.synchronize()
+    return (time.perf_counter() - t0) * 1e3 / args.steps
+
+
 def sweep_of(results, rates):
     base = results.get(1.0)
     out = []
@@ -376,6 +407,12 @@ def sweep_of(results, rates):
                     "ms_per_step": round(r["ms"], 4),
                     "speedup_vs_keep_rate_1": None if base is None else round(base["ms"] / r["ms"], 3),
                     "rows_after_last_prune": r["kept_rows_final"]})
+        if "decode_ms" in r:
+            out[-1]["decode_ms_per_step"] = round(r["decode_ms"], 4)
+            out[-1]["ttft_ms"] = round(r["ms"] + r["decode_ms"], 4)
+            if base is not None and "decode_ms" in base:
+                out[-1]["ttft_speedup_vs_keep_rate_1"] = round(
+                    (base["ms"] + base["decode_ms"]) / (r["ms"] + r["decode_ms"]), 3)
     return out
 
 

@@ -304,12 +304,15 @@ __global__ __launch_bounds__(WM * WN * 64) void gemm_bf16_mfma_kernel(
 // ---------------------------------------------------------------------------
 // Workgroups are handed to the 8 XCDs round-robin by linear id, and every XCD
 // has its own L2. Workgroup L therefore runs on XCD k = L % 8 as that XCD's
-// j-th workgroup (j = L / 8). XCD k is given a contiguous, balanced stripe of
-// the M-tiles and walks it in groups of kXcdGroup M-tiles: for each N-tile,
-// the group's M-tiles. The A rows of a group and the W tiles in flight then
-// fit one L2, so A is fetched from memory about once and W once per group
-// and XCD, instead of once per N-tile. The grid is 8 x (largest stripe x
-// N-tiles) one-dimensional workgroups; the ones past their stripe exit.
+// j-th workgroup (j = L / 8). The output tiles are put in a grouped order --
+// groups of kXcdGroup M-tiles, and within a group every N-tile with the
+// group's M-tiles inner -- and XCD k takes a contiguous, balanced range of
+// that order. Neighbouring tiles of the order share A rows or W columns, so
+// a range's operands are fetched from memory about once into its XCD's L2;
+// and since the ranges split the tiles, not the M-tiles, all 8 XCDs work
+// even when there is a single M-tile (short inputs, decoding). The grid is
+// 8 x (largest range) one-dimensional workgroups; the ones past their range
+// exit.
 constexpr int kXcds = 8;
 constexpr int kXcdGroup = 8;
 
@@ -317,23 +320,22 @@ template <int BM, int BN>
 __device__ __forceinline__ bool xcd_tile(int M, int N, int* mt, int* nt) {
   const int nM = (M + BM - 1) / BM, nN = (N + BN - 1) / BN;
   const int k = blockIdx.x % kXcds, j = blockIdx.x / kXcds;
-  const int base = nM / kXcds, extra = nM % kXcds;
-  const int rows = base + (k < extra ? 1 : 0);
-  const int m_lo = k * base + (k < extra ? k : extra);
-  if (j >= rows * nN) return false;
-  const int g = j / (kXcdGroup * nN);
+  const int tiles = nM * nN;
+  const int per = tiles / kXcds, extra = tiles % kXcds;
+  if (j >= per + (k < extra ? 1 : 0)) return false;
+  const int t = k * per + min(k, extra) + j;  // position in the grouped order
+  const int g = t / (kXcdGroup * nN);
   const int gm0 = g * kXcdGroup;
-  const int gsz = min(kXcdGroup, rows - gm0);
-  const int r = j - g * kXcdGroup * nN;
+  const int gsz = min(kXcdGroup, nM - gm0);
+  const int r = t - g * kXcdGroup * nN;
   *nt = r / gsz;
-  *mt = m_lo + gm0 + r % gsz;
+  *mt = gm0 + r % gsz;
   return true;
 }
 
 inline dim3 xcd_grid(int M, int N, int BM, int BN) {
-  const int nM = (M + BM - 1) / BM, nN = (N + BN - 1) / BN;
-  const int rows = (nM + kXcds - 1) / kXcds;
-  return dim3(static_cast<unsigned>(kXcds * rows * nN));
+  const int tiles = ((M + BM - 1) / BM) * ((N + BN - 1) / BN);
+  return dim3(static_cast<unsigned>(kXcds * ((tiles + kXcds - 1) / kXcds)));
 }
 
 // ---------------------------------------------------------------------------
