@@ -38,6 +38,13 @@ sums the soft-score matrices of all H query heads.
 predicted from the last input row): that row is always kept and the other
 k - 1 rows are chosen by score as above.
 
+``mark_only`` (the visualisation mode of Appendix B: rows "pruned but not
+removed"): every row continues through every layer, so the hidden states
+are those of the unpruned stack; each pruning point ranks all current rows
+by score and marks the Eq. 2 count, compounded on the previous point's
+marked count, as kept. A row marked pruned at one point can be marked kept
+again later (reactivated).
+
 ``mode="exact"`` keeps everything in float64. ``mode="bf16"`` rounds to
 bfloat16 (nearest-even) exactly where the GPU path stores bfloat16: norm
 outputs, Q/K/V (after RoPE), attention output, MLP intermediate and the
@@ -293,7 +300,8 @@ def sequence_layer(x: np.ndarray, pos: np.ndarray, w: Dict[str, Optional[np.ndar
 def layer_forward(x: np.ndarray, pos: np.ndarray, cu: Sequence[int], w: Dict,
                   cfg: LayerCfg, keep_rate: Optional[Sequence[float]] = None,
                   mode: str = "exact", kept_override: Optional[Sequence[np.ndarray]] = None,
-                  keep_intermediates: bool = False, want_kv: bool = False) -> Dict:
+                  keep_intermediates: bool = False, want_kv: bool = False,
+                  want_scores: bool = False) -> Dict:
     """One layer over a packed batch ([T, d] rows, sequence b at rows
     cu[b]..cu[b+1]). With ``keep_rate`` (one rate per sequence) the layer is
     a pruning layer: its output rows are cut down to the Eq. 2 count by
@@ -307,9 +315,9 @@ def layer_forward(x: np.ndarray, pos: np.ndarray, cu: Sequence[int], w: Dict,
     cu_out = [0]
     for b in range(B):
         lo, hi = cu[b], cu[b + 1]
-        res = sequence_layer(x[lo:hi], pos[lo:hi], w, cfg, mode, want_scores=prune)
+        res = sequence_layer(x[lo:hi], pos[lo:hi], w, cfg, mode, want_scores=prune or want_scores)
         lses.append(res["lse"])
-        if keep_intermediates:
+        if keep_intermediates or (want_scores and not prune):
             inter.append(res)
         if want_kv:
             kvs.append((res["k"], res["v"]))
@@ -337,6 +345,8 @@ def layer_forward(x: np.ndarray, pos: np.ndarray, cu: Sequence[int], w: Dict,
         "cu": np.asarray(cu_out, dtype=np.int64),
         "lse": np.concatenate(lses, axis=1) if lses else np.zeros((cfg.n_heads, 0)),
     }
+    if want_scores and not prune:
+        out["scores"] = np.concatenate([r["scores"] for r in inter]) if inter else np.zeros(0)
     if prune:
         out["scores"] = np.concatenate(ss) if ss else np.zeros(0)
         out["kept_rows"] = np.concatenate(kept_all) if kept_all else np.zeros(0, dtype=np.int64)
@@ -352,7 +362,7 @@ def stack_forward(x: np.ndarray, pos: np.ndarray, cu: Sequence[int], weights: Se
                   cfg: LayerCfg, prune_after: Sequence[int], keep_rate: Sequence[float],
                   mode: str = "exact",
                   kept_override: Optional[Dict[int, Sequence[np.ndarray]]] = None,
-                  record: bool = False, want_kv: bool = False) -> Dict:
+                  record: bool = False, want_kv: bool = False, mark_only: bool = False) -> Dict:
     """The layer stack: layers 1..L in order; after each layer listed in
     ``prune_after`` (1-based) the output is pruned at the per-sequence keep
     rates. Returns the final rows, their original positions and row offsets,
@@ -361,10 +371,39 @@ def stack_forward(x: np.ndarray, pos: np.ndarray, cu: Sequence[int], weights: Se
     indices. With ``record`` every layer's output is kept too. With
     ``want_kv`` the result holds, per layer and sequence, the keys and values
     (after RoPE) of the rows that entered that layer: the cache a decode step
-    attends to."""
+    attends to. With ``mark_only`` nothing is removed: each pruning point
+    marks its kept rows (``points``) and every row continues."""
     prune_set = set(int(p) for p in prune_after)
     cur_x, cur_pos, cur_cu = x, pos, np.asarray(cu, dtype=np.int64)
     points, layers, kv = [], [], []
+    if mark_only:
+        active = [int(cur_cu[b + 1] - cur_cu[b]) for b in range(len(cur_cu) - 1)]
+        for l, w in enumerate(weights, start=1):
+            pr = l in prune_set
+            res = layer_forward(cur_x, cur_pos, cur_cu, w, cfg, None, mode, want_kv=want_kv,
+                                want_scores=pr)
+            if want_kv:
+                kv.append(res["kv"])
+            if pr:
+                ks, kept_all, cu_k = [], [], [0]
+                for b in range(len(active)):
+                    lo, hi = int(cur_cu[b]), int(cur_cu[b + 1])
+                    kb = keep_count(active[b], float(keep_rate[b]), cfg.tau)
+                    ov = kept_override.get(l) if kept_override else None
+                    kept = (np.asarray(ov[b], dtype=np.int64) if ov is not None else
+                            select_topk(res["scores"][lo:hi], kb, cfg.force_keep_last))
+                    active[b] = kb
+                    ks.append(kb)
+                    kept_all.append(kept + lo)
+                    cu_k.append(cu_k[-1] + len(kept))
+                kr = np.concatenate(kept_all) if kept_all else np.zeros(0, dtype=np.int64)
+                points.append({"layer": l, "scores": res["scores"], "k": ks, "kept_rows": kr,
+                               "pos": cur_pos[kr], "cu": np.asarray(cu_k, dtype=np.int64)})
+            cur_x = res["x"]
+            if record:
+                layers.append({"x": cur_x, "pos": cur_pos, "cu": cur_cu})
+        return {"x": cur_x, "pos": cur_pos, "cu": cur_cu, "points": points, "layers": layers,
+                "kv": kv}
     for l, w in enumerate(weights, start=1):
         pr = l in prune_set
         ov = kept_override.get(l) if (kept_override and pr) else None

@@ -294,6 +294,17 @@ def _brute_topk(s, k):
     return found[0]
 
 
+def _is_topk(s, kept, k):
+    """kept (ascending) has k members and each beats every non-member under
+    (score desc, index asc) -- the defining property, checked pairwise."""
+    kept = [int(i) for i in kept]
+    if len(kept) != k or kept != sorted(set(kept)):
+        return False
+    inside = set(kept)
+    beats = lambda a, b: s[a] > s[b] or (s[a] == s[b] and a < b)
+    return all(beats(a, b) for a in inside for b in range(len(s)) if b not in inside)
+
+
 def test_select_topk_brute_force():
     g = np.random.default_rng(5)
     for trial in range(60):
@@ -581,3 +592,31 @@ def test_decode_after_pruned_prefill():
         # and the cache it used holds exactly the rows entering each layer
         sizes = [n] + [len(pt["kept_rows"]) for pt in pre["points"]]
         assert [pre["kv"][l][0][0].shape[0] for l in range(3)] == [sizes[0], sizes[1], sizes[2]]
+
+
+# ---------------------------------------------------------------- mark-only mode
+def test_mark_only_mode():
+    # rows are marked, not removed: the hidden states are the unpruned stack's;
+    # the first point marks exactly the compacting mode's first kept set (same
+    # scores), counts follow the compounded Eq. 2 schedule, and later points
+    # rank all rows (a row can come back)
+    lens = [40, 17]
+    x, pos, cu, ws, cfg = _stack_inputs(W.DECODER, lens, 11, n_layers=3)
+    prune, rates = (1, 2, 3), [0.5, 0.4]
+    mark = O.stack_forward(x, pos, cu, ws, cfg, prune, rates, mark_only=True)
+    plain = O.stack_forward(x, pos, cu, ws, cfg, (), rates)
+    comp = O.stack_forward(x, pos, cu, ws, cfg, prune, rates)
+    assert np.array_equal(mark["x"], plain["x"]) and np.array_equal(mark["pos"], pos)
+    assert np.array_equal(mark["points"][0]["kept_rows"], comp["points"][0]["kept_rows"])
+    sched = O.keep_schedule(lens, rates, cfg.tau, 3)
+    assert [list(pt["k"]) for pt in mark["points"]] == [list(r) for r in sched]
+    rec = O.stack_forward(x, pos, cu, ws, cfg, (), rates, record=True)
+    for i, pt in enumerate(mark["points"]):
+        # the scores a point ranks are those of all rows at that layer
+        assert pt["scores"].shape[0] == sum(lens)
+        for b in range(len(lens)):
+            lo, hi = int(cu[b]), int(cu[b + 1])
+            kept = pt["kept_rows"][pt["cu"][b]:pt["cu"][b + 1]] - lo
+            assert _is_topk(pt["scores"][lo:hi], kept, sched[i][b])
+    # in this example some rows marked pruned at point 1 are marked kept at point 2
+    assert set(mark["points"][1]["kept_rows"]) - set(mark["points"][0]["kept_rows"])
