@@ -270,9 +270,29 @@ def cpu_baseline(p, ws_np, x_np, lens, rate, budget_s):
                       f"float64 exact mode, {elapsed:.1f} s"}
 
 
+def graph_ms(fn, args, torch):
+    """Mean time of fn replayed as a HIP graph (after warm-up replays)."""
+    g = torch.cuda.CUDAGraph()
+    s = torch.cuda.Stream()
+    s.wait_stream(torch.cuda.current_stream())
+    with torch.cuda.stream(s):
+        with torch.cuda.graph(g, stream=s):
+            fn()
+    torch.cuda.current_stream().wait_stream(s)
+    for _ in range(args.warmup):
+        g.replay()
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for _ in range(args.steps):
+        g.replay()
+    torch.cuda.synchronize()
+    return (time.perf_counter() - t0) * 1e3 / args.steps
+
+
 def measure(p, rates, args, torch, W, zsa, dev, timing):
     """Graph-replayed step time of preset ``p`` at every keep rate (and, with
-    ``timing``, per-class launch durations of one eager forward)."""
+    ``timing``, per-class launch durations of one eager forward and the same
+    stack in mark-only mode, rows marked instead of removed)."""
     lens = W.lengths(p, args.seed)
     ws_np = W.stack_weights(p, args.seed)
     x_np = W.hidden(p, args.seed, lens)
@@ -282,6 +302,10 @@ def measure(p, rates, args, torch, W, zsa, dev, timing):
                        zsa.BF16 if p.dtype == "bf16" else zsa.F32, p.tau, p.norm_eps, p.rope_theta,
                        p.n_kv_heads, p.force_keep_last)
     stack = zsa.Stack(cfg, dws)
+    mcfg = zsa.make_cfg(p.kind, p.d_model, p.n_heads, p.d_ff, p.causal,
+                        zsa.BF16 if p.dtype == "bf16" else zsa.F32, p.tau, p.norm_eps,
+                        p.rope_theta, p.n_kv_heads, p.force_keep_last, mark_only=True)
+    mstack = zsa.Stack(mcfg, dws)
     seqs = zsa.Seqs(lens, dev)
     xd = W.to_storage(x_np, p.dtype).to(dev)
     posd = torch.from_numpy(W.positions(lens)).to(dev)
@@ -327,6 +351,9 @@ def measure(p, rates, args, torch, W, zsa, dev, timing):
                 n, t = zsa.timing_read(c)
                 cls[name] = {"launches": n, "ms": t}
             rows_in, rows_after = layer_rows(p, plan)
+            mouts = mstack.forward(xd, posd, seqs, p.prune_after, kr)
+            r["mark_ms"] = graph_ms(
+                lambda: mstack.forward(xd, posd, seqs, p.prune_after, kr, out=mouts), args, torch)
             r.update({"classes": cls, "gemm_flops": gemm_flops(p, rows_in, rows_after),
                       "rows": (rows_in, rows_after),
                       "work": class_work(p, lens, plan, rows_in, rows_after)})
@@ -407,6 +434,11 @@ def sweep_of(results, rates):
                     "ms_per_step": round(r["ms"], 4),
                     "speedup_vs_keep_rate_1": None if base is None else round(base["ms"] / r["ms"], 3),
                     "rows_after_last_prune": r["kept_rows_final"]})
+        if "mark_ms" in r:
+            # the same stack with rows marked instead of removed (Appendix B):
+            # the ratio is the part of the speedup that compaction delivers
+            out[-1]["mark_mode_ms_per_step"] = round(r["mark_ms"], 4)
+            out[-1]["compaction_speedup_vs_mark_mode"] = round(r["mark_ms"] / r["ms"], 3)
         if "decode_ms" in r:
             out[-1]["decode_ms_per_step"] = round(r["decode_ms"], 4)
             out[-1]["ttft_ms"] = round(r["ms"] + r["decode_ms"], 4)

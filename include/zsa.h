@@ -104,6 +104,13 @@ typedef struct zsa_layer_cfg {
                               of each sequence (the row the first generated
                               token is predicted from) and chooses the other
                               k - 1 rows by score */
+  int32_t mark_only;  /* nonzero: the visualisation mode of Appendix B --
+                         pruning points mark their kept rows (kept_rows_out,
+                         pos_dbg) but remove none, so every row continues
+                         and the outputs are those of the unpruned stack;
+                         each point ranks all rows and marks the Eq. 2 count
+                         of the previous point's marked count (a row can be
+                         marked again after being passed over) */
 } zsa_layer_cfg;
 
 /* Weights of one block, device pointers in the storage dtype, PyTorch
@@ -251,7 +258,8 @@ int zsa_compact_gather(void* stream, int32_t dtype, const void* hidden, int32_t 
  * running the whole block and then compacting.
  *   hidden_in [T, d], pos_in [T] int32, cu_host/cu_dev [batch+1]
  *   hidden_out [T', d], pos_out [T'], T' = sum of the kept counts
- *   (zsa_keep_schedule with one point) or T when keep_rate is NULL
+ *   (zsa_keep_schedule with one point) or T when keep_rate is NULL or
+ *   cfg->mark_only is set (then kept_rows_out lists the marked rows)
  *   cu_out_host [batch+1] host, cu_out_dev [batch+1] device: written
  *   scores_out [T] fp32 / kept_rows_out [T'] int32 device, may be NULL
  *   ws >= zsa_layer_workspace_size(cfg, T, batch)
@@ -270,6 +278,8 @@ size_t zsa_layer_workspace_size(const zsa_layer_cfg* cfg, int32_t total_rows, in
  * pruned at keep_rate[b] (host [batch]) as in zsa_layer_forward, each count
  * relative to the rows entering that block (Eq. 2 compounded).
  *   hidden_out [T_final, d], pos_out [T_final], cu_out_host/dev [batch+1]
+ *   (T_final = T with cfg->mark_only: the rows are marked, not removed;
+ *   pos_dbg then lists the positions each point marks)
  *   counts_out_host [n_prune * batch] host or NULL: rows kept per point
  *   scores_dbg fp32 device or NULL: the scores at each pruning point,
  *     concatenated (point p occupies the rows entering that block)

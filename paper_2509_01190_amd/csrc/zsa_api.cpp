@@ -254,7 +254,8 @@ void fill_rope(zsa::EpiParams& ep, int hd, float theta) {
 int run_layer(hipStream_t s, const zsa_layer_cfg& c, const zsa_layer_weights& w,
               const void* x_in, const int32_t* pos_in, const RowSet& in, bool prune,
               const RowSet& out, void* x_out, int32_t* pos_out, float* scores_out,
-              int32_t* kept_out, const LayerBufs& wb, void* kv_layer = nullptr, int kv_cap = 0) {
+              int32_t* kept_out, const LayerBufs& wb, void* kv_layer = nullptr, int kv_cap = 0,
+              int32_t* marks_pos = nullptr) {
   using namespace zsa;
   const int dt = c.dtype;
   const size_t e = esize(dt);
@@ -305,11 +306,20 @@ int run_layer(hipStream_t s, const zsa_layer_cfg& c, const zsa_layer_weights& w,
     HIP_TRY(launch_select(s, wb.partials, G, in.T, in.B, in.max_len, in.cu_dev, out.cu_dev, kept,
                           scores_out, c.force_keep_last != 0),
             "select");
-    HIP_TRY(launch_gather(s, dt, d, in.T, kept, out.T, x_in, wb.xg, wb.o, wb.og, pos_in, pos_out),
-            "gather");
-    xr = wb.xg;
-    orows = wb.og;
-    rows = out.T;
+    if (c.mark_only != 0) {
+      // rows are marked, not removed: only the marked positions are gathered
+      if (marks_pos != nullptr)
+        HIP_TRY(launch_gather(s, dt, d, in.T, kept, out.T, nullptr, nullptr, nullptr, nullptr,
+                              pos_in, marks_pos),
+                "mark positions");
+    } else {
+      HIP_TRY(launch_gather(s, dt, d, in.T, kept, out.T, x_in, wb.xg, wb.o, wb.og, pos_in,
+                            pos_out),
+              "gather");
+      xr = wb.xg;
+      orows = wb.og;
+      rows = out.T;
+    }
   }
   {
     EpiParams ep{};
@@ -623,6 +633,7 @@ size_t zsa_layer_workspace_size(const zsa_layer_cfg* cfg, int32_t total_rows, in
   if (cfg == nullptr || total_rows < 0 || batch < 0) return 0;
   Carver cv;
   layer_layout(cfg, total_rows, cv);
+  cv.take(static_cast<size_t>(batch + 1) * 4);   // kept-list offsets (mark-only)
   return cv.off;
 }
 
@@ -661,15 +672,21 @@ int zsa_layer_forward(void* stream, const zsa_layer_cfg* cfg, const zsa_layer_we
   hipStream_t s = static_cast<hipStream_t>(stream);
   Carver cv;
   const LayerBufs wb = carve_layer(layer_layout(cfg, T, cv), ws);
-  HIP_TRY(zsa::launch_upload_i32(s, cu_out_dev, cu_out.data(), batch + 1), "upload");
+  // mark-only: the output keeps every row; the kept lists get offsets of their own
+  const bool mark = prune && cfg->mark_only != 0;
+  int32_t* marks_cu = reinterpret_cast<int32_t*>(static_cast<char*>(ws) +
+                                                 cv.take(static_cast<size_t>(batch + 1) * 4));
   const RowSet in{batch, cu_host, cu_dev, T, max_len};
-  const RowSet out{batch, cu_out.data(), cu_out_dev, cu_out[batch], max_out};
+  int32_t* sel_cu = mark ? marks_cu : cu_out_dev;
+  const RowSet sel{batch, cu_out.data(), sel_cu, cu_out[batch], max_out};
+  HIP_TRY(zsa::launch_upload_i32(s, sel_cu, cu_out.data(), batch + 1), "upload");
+  if (mark) HIP_TRY(zsa::launch_upload_i32(s, cu_out_dev, cu_host, batch + 1), "upload");
   if (T > 0) {
-    CHECK(run_layer(s, *cfg, *w, hidden_in, pos_in, in, prune, out, hidden_out, pos_out,
+    CHECK(run_layer(s, *cfg, *w, hidden_in, pos_in, in, prune, sel, hidden_out, pos_out,
                     scores_out, kept_rows_out, wb));
-    if (!prune) HIP_TRY(zsa::launch_copy_i32(s, pos_out, pos_in, T), "pos copy");
+    if (!prune || mark) HIP_TRY(zsa::launch_copy_i32(s, pos_out, pos_in, T), "pos copy");
   }
-  memcpy(cu_out_host, cu_out.data(), sizeof(int32_t) * (batch + 1));
+  memcpy(cu_out_host, mark ? cu_host : cu_out.data(), sizeof(int32_t) * (batch + 1));
   return ZSA_OK;
 }
 
@@ -756,7 +773,10 @@ int zsa_stack_forward(void* stream, const zsa_layer_cfg* cfg, const zsa_layer_we
   std::vector<int32_t> flat;
   for (int p = 1; p <= n_prune; ++p) flat.insert(flat.end(), cus[p].begin(), cus[p].end());
   if (!flat.empty()) HIP_TRY(zsa::launch_upload_i32(s, meta, flat.data(), static_cast<int>(flat.size())), "upload");
-  HIP_TRY(zsa::launch_upload_i32(s, cu_out_dev, cus[n_prune].data(), batch + 1), "upload");
+  const bool mark = cfg->mark_only != 0;
+  HIP_TRY(zsa::launch_upload_i32(s, cu_out_dev, mark ? cus[0].data() : cus[n_prune].data(),
+                                 batch + 1),
+          "upload");
 
   const void* cur_x = hidden_in;
   const int32_t* cur_pos = pos_in;
@@ -772,7 +792,18 @@ int zsa_stack_forward(void* stream, const zsa_layer_cfg* cfg, const zsa_layer_we
                          : static_cast<char*>(kv_cache) + static_cast<size_t>(l - 1) * batch *
                                                               kv_capacity * 2 * kv_heads(*cfg) *
                                                               cfg->head_dim * esize(cfg->dtype);
-    if (prune) {
+    if (prune && mark) {
+      // every row continues; the point's marked rows (Eq. 2 count) are listed
+      const RowSet sel{batch, cus[point + 1].data(), meta + static_cast<size_t>(point) * (batch + 1),
+                       cus[point + 1][batch], maxl[point + 1]};
+      float* sdbg = scores_dbg != nullptr ? scores_dbg + score_off : nullptr;
+      int32_t* mpos = pos_dbg != nullptr ? pos_dbg + pos_off : nullptr;
+      CHECK(run_layer(s, *cfg, w[l - 1], cur_x, cur_pos, cur, true, sel, x_out, nullptr, sdbg,
+                      nullptr, wb, kv_layer, kv_capacity, mpos));
+      score_off += cur.T;
+      pos_off += sel.T;
+      ++point;
+    } else if (prune) {
       const RowSet nxt{batch, cus[point + 1].data(), meta + static_cast<size_t>(point) * (batch + 1),
                        cus[point + 1][batch], maxl[point + 1]};
       int32_t* pos_next = last ? pos_out : posbuf[point & 1];
@@ -793,7 +824,7 @@ int zsa_stack_forward(void* stream, const zsa_layer_cfg* cfg, const zsa_layer_we
     cur_x = x_out;
   }
   if (T0 > 0 && cur_pos != pos_out) HIP_TRY(zsa::launch_copy_i32(s, pos_out, cur_pos, cur.T), "pos copy");
-  memcpy(cu_out_host, cus[n_prune].data(), sizeof(int32_t) * (batch + 1));
+  memcpy(cu_out_host, mark ? cus[0].data() : cus[n_prune].data(), sizeof(int32_t) * (batch + 1));
   return ZSA_OK;
 }
 

@@ -63,6 +63,7 @@ class Preset:
     rope_theta: float = 10000.0
     n_kv_heads: int = 0       # key/value heads (grouped-query attention); 0: n_heads
     force_keep_last: bool = False
+    mark_only: bool = False   # pruning points mark rows instead of removing them
 
     @property
     def head_dim(self) -> int:

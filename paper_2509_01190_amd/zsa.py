@@ -46,7 +46,7 @@ class LayerCfg(ctypes.Structure):
     _fields_ = [("kind", _i32), ("d_model", _i32), ("n_heads", _i32), ("head_dim", _i32),
                 ("d_ff", _i32), ("causal", _i32), ("dtype", _i32), ("tau", _i32),
                 ("norm_eps", _f32), ("rope_theta", _f32), ("n_kv_heads", _i32),
-                ("force_keep_last", _i32)]
+                ("force_keep_last", _i32), ("mark_only", _i32)]
 
 
 WEIGHT_NAMES = ["norm1_w", "norm1_b", "w_qkv", "b_qkv", "w_o", "b_o",
@@ -312,9 +312,10 @@ def compact_gather(hidden: torch.Tensor, pos: Optional[torch.Tensor],
 # ------------------------------------------------------------------ blocks
 def make_cfg(kind: int, d_model: int, n_heads: int, d_ff: int, causal: bool, dtype: int,
              tau: int = 5, norm_eps: float = 1e-5, rope_theta: float = 10000.0,
-             n_kv_heads: int = 0, force_keep_last: bool = False) -> LayerCfg:
+             n_kv_heads: int = 0, force_keep_last: bool = False,
+             mark_only: bool = False) -> LayerCfg:
     return LayerCfg(kind, d_model, n_heads, d_model // n_heads, d_ff, int(causal), dtype, tau,
-                    norm_eps, rope_theta, n_kv_heads, int(force_keep_last))
+                    norm_eps, rope_theta, n_kv_heads, int(force_keep_last), int(mark_only))
 
 
 def weight_shapes(cfg: LayerCfg) -> Dict[str, tuple]:
@@ -380,20 +381,21 @@ class Stack:
         _require_cuda(hidden, pos)
         dev = hidden.device
         T = seqs.total
+        t_kept = T
         if keep_rate is not None:
             kr = _host_f64(keep_rate)
             counts = keep_schedule(seqs.lengths, kr, self.cfg.tau, 1)[0]
-            t_out = int(counts.sum())
+            t_kept = int(counts.sum())
             kr_p = _hpf64(kr)
         else:
             kr_p = None
-            t_out = T
+        t_out = T if self.cfg.mark_only else t_kept     # mark-only keeps every row
         x_out = torch.empty((max(t_out, 1), self.cfg.d_model), dtype=hidden.dtype, device=dev)
         pos_out = torch.empty(max(t_out, 1), dtype=torch.int32, device=dev)
         cu_out = np.zeros(seqs.batch + 1, dtype=np.int32)
         cu_out_dev = torch.empty(seqs.batch + 1, dtype=torch.int32, device=dev)
         scores = torch.empty(max(T, 1), dtype=torch.float32, device=dev) if want_scores else None
-        kept = torch.empty(max(t_out, 1), dtype=torch.int32, device=dev) if want_kept else None
+        kept = torch.empty(max(t_kept, 1), dtype=torch.int32, device=dev) if want_kept else None
         wsz = int(lib().zsa_layer_workspace_size(ctypes.byref(self.cfg), T, seqs.batch))
         ws = torch.empty(max(wsz, 1), dtype=torch.uint8, device=dev)
         w = _weights_struct(self.weights[layer])
@@ -407,16 +409,20 @@ class Stack:
         if want_scores:
             res["scores"] = scores[:T]
         if want_kept:
-            res["kept_rows"] = kept[:t_out]
+            res["kept_rows"] = kept[:t_kept]
         return res
 
     def plan(self, seqs: Seqs, prune_after: Sequence[int], keep_rate) -> Dict:
         """Host-side shapes of a stack call (the Eq. 2 schedule)."""
         kr = _host_f64(keep_rate)
         counts = keep_schedule(seqs.lengths, kr, self.cfg.tau, len(prune_after))
-        final = int(counts[-1].sum()) if len(prune_after) else seqs.total
-        rows_in = [seqs.total] + [int(c.sum()) for c in counts]
-        return {"counts": counts, "final_rows": final, "rows_in": rows_in}
+        marked = [int(c.sum()) for c in counts]
+        if self.cfg.mark_only:        # rows are marked, not removed
+            return {"counts": counts, "final_rows": seqs.total, "marked": marked,
+                    "rows_in": [seqs.total] * (len(marked) + 1)}
+        final = marked[-1] if len(prune_after) else seqs.total
+        rows_in = [seqs.total] + marked
+        return {"counts": counts, "final_rows": final, "rows_in": rows_in, "marked": marked}
 
     def kv_cache(self, batch: int, capacity: int, device) -> torch.Tensor:
         """An empty key/value cache [layers, batch, capacity, 2 * kvd]."""
@@ -490,7 +496,7 @@ class Stack:
             }
             if debug:
                 sc_rows = sum(plan["rows_in"][:len(pa)])
-                pos_rows = sum(plan["rows_in"][1:])
+                pos_rows = sum(plan["marked"])
                 out["scores_dbg"] = torch.empty(max(sc_rows, 1), dtype=torch.float32, device=dev)
                 out["pos_dbg"] = torch.empty(max(pos_rows, 1), dtype=torch.int32, device=dev)
                 out["rows_in"] = plan["rows_in"]

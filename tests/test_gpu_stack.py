@@ -23,7 +23,7 @@ def build(p, seed, lens=None, norm_jitter=True, sharp=1.0):
     dws = [dev_weights(w, p.dtype) for w in ws]
     cfg = zsa.make_cfg(p.kind, p.d_model, p.n_heads, p.d_ff, p.causal,
                        zsa.BF16 if p.dtype == "bf16" else zsa.F32, p.tau, p.norm_eps, p.rope_theta,
-                       p.n_kv_heads, p.force_keep_last)
+                       p.n_kv_heads, p.force_keep_last, p.mark_only)
     stack = zsa.Stack(cfg, dws)
     x = W.hidden(p, seed, lens)
     xd = to_dev(x, p.dtype)
@@ -221,3 +221,50 @@ def test_small_gqa_stack_keep_last(hkv):
     pos = out["pos"][: out["t_final"]].cpu().numpy()
     cu = out["cu_host"]
     assert [int(pos[cu[b + 1] - 1]) for b in range(len(lens))] == [n - 1 for n in lens]
+
+
+@pytest.mark.parametrize("kind", [W.ENCODER, W.DECODER])
+def test_mark_only_stack(kind):
+    # rows are marked, not removed: the outputs are the unpruned stack's, and
+    # every point marks the Eq. 2 count (compounded on the marked counts) by
+    # the scores of all rows at that layer
+    causal = kind == W.DECODER
+    p = W.shrink(W.PRESETS["bert"], kind=kind, causal=causal, n_layers=3, d_model=256, n_heads=4,
+                 d_ff=512, batch=3, prune_after=(1, 2, 3), mark_only=True)
+    lens = [300, 64, 129]
+    lens, stack, xd, posd, dws, ocfg = build(p, 8, lens, sharp=3.0)
+    seqs = zsa.Seqs(lens, dev())
+    rates = [0.5, 0.3, 0.7]
+    out = stack.forward(xd, posd, seqs, p.prune_after, rates, debug=True)
+    torch.cuda.synchronize()
+    T = sum(lens)
+    assert out["t_final"] == T and np.array_equal(out["cu_host"], seqs.host)
+    assert torch.equal(out["pos"][:T], posd)
+    sched = O.keep_schedule(lens, rates, p.tau, 3)
+    assert np.array_equal(out["counts"], np.array(sched).reshape(3, len(lens)))
+    x_all = f64(xd)
+    ws64 = [weights_f64(w) for w in dws]
+    s_dbg = out["scores_dbg"].cpu().numpy()
+    pos_dbg = out["pos_dbg"].cpu().numpy()
+    x_fin = f64(out["x"][:T])
+    m_off = np.concatenate([[0], np.cumsum([int(np.sum(c)) for c in sched])])
+    for b, n in enumerate(lens):
+        lo = int(seqs.host[b])
+        ref = O.stack_forward(x_all[lo:lo + n], np.arange(n), [0, n], ws64, ocfg, p.prune_after,
+                              [rates[b]], mode="exact", mark_only=True)
+        ref_e = O.stack_forward(x_all[lo:lo + n], np.arange(n), [0, n], ws64, ocfg, p.prune_after,
+                                [rates[b]], mode="bf16", mark_only=True)
+        assert_rel_l2(x_fin[lo:lo + n], ref["x"], 2e-2, f"seq {b} final rows")
+        assert_rows_close(x_fin[lo:lo + n], ref_e["x"], 5e-2, f"seq {b} final rows")
+        for pt in range(3):
+            k = sched[pt][b]
+            c0 = m_off[pt] + int(np.sum(sched[pt][:b]))
+            kept_gpu = pos_dbg[c0:c0 + k]                 # positions = local indices here
+            s_gpu = s_dbg[pt * T + lo:pt * T + lo + n]
+            s_ref = ref_e["points"][pt]["scores"]
+            # every row stays through all three layers here, including the last
+            # causal rows whose column sums are small; their bf16 relative score
+            # error (about 2 * 2^-9 * |logit|) needs a wider eps than the
+            # compacted stacks, where those rows are mostly gone by point 2
+            check_kept_sets(s_gpu, s_ref, k, kept_gpu, ref_e["points"][pt]["kept_rows"], 1e-2,
+                            f"seq {b} point {pt}")
