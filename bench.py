@@ -351,6 +351,13 @@ def measure(p, rates, args, torch, W, zsa, dev, timing):
                 n, t = zsa.timing_read(c)
                 cls[name] = {"launches": n, "ms": t}
             rows_in, rows_after = layer_rows(p, plan)
+            if p.dtype == "bf16" and p.d_model // p.n_heads in (64, 128):
+                # the training step's backward (forward recomputed inside), as a graph
+                g = torch.Generator().manual_seed(args.seed)
+                dy = torch.randn(plan["final_rows"], p.d_model, generator=g).to(torch.bfloat16).to(dev)
+                stack.backward(xd, posd, seqs, p.prune_after, kr, dy)
+                r["backward_ms"] = graph_ms(
+                    lambda: stack.backward(xd, posd, seqs, p.prune_after, kr, dy), args, torch)
             mouts = mstack.forward(xd, posd, seqs, p.prune_after, kr)
             r["mark_ms"] = graph_ms(
                 lambda: mstack.forward(xd, posd, seqs, p.prune_after, kr, out=mouts), args, torch)
@@ -439,6 +446,9 @@ def sweep_of(results, rates):
             # the ratio is the part of the speedup that compaction delivers
             out[-1]["mark_mode_ms_per_step"] = round(r["mark_ms"], 4)
             out[-1]["compaction_speedup_vs_mark_mode"] = round(r["mark_ms"] / r["ms"], 3)
+        if "backward_ms" in r:
+            out[-1]["backward_ms_per_step"] = round(r["backward_ms"], 4)
+            out[-1]["train_step_ms"] = round(r["ms"] + r["backward_ms"], 4)
         if "decode_ms" in r:
             out[-1]["decode_ms_per_step"] = round(r["decode_ms"], 4)
             out[-1]["ttft_ms"] = round(r["ms"] + r["decode_ms"], 4)

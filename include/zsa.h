@@ -306,6 +306,37 @@ size_t zsa_stack_workspace_size(const zsa_layer_cfg* cfg, int32_t total_rows, in
                                 int32_t n_prune);
 
 /* ---------------------------------------------------------------------
+ * Gradients of one block's weights: fp32 device pointers, the shapes of
+ * zsa_layer_weights. norm*_b and the biases may be NULL (not wanted or not
+ * present); the others are required.
+ */
+typedef struct zsa_layer_grads {
+  float *norm1_w, *norm1_b, *w_qkv, *b_qkv, *w_o, *b_o;
+  float *norm2_w, *norm2_b, *w_up, *b_up, *w_down, *b_down;
+} zsa_layer_grads;
+
+/* Backward pass through the pruned stack (the step the fine-tuning of Eq. 3
+ * trains with): for the loss sum(hidden_out * dy), with hidden_out the
+ * output of zsa_stack_forward under the same arguments, writes dx [T, d]
+ * (the gradient of hidden_in, dtype) and every weight gradient (fp32,
+ * overwritten). Every pruning point's kept rows are taken as constants
+ * (the selection is not differentiable): rows it drops still receive
+ * gradient through that layer's keys and values and the layers before it.
+ * The forward is recomputed inside (it is deterministic), layer by layer.
+ *   dy [T_final, d] dtype device; grads[n_layers];
+ *   ws >= zsa_stack_backward_workspace_size(cfg, T, batch, n_layers, n_prune)
+ * bf16 with head_dim 64 or 128, compacting mode; otherwise ZSA_EUNSUPPORTED.
+ */
+int zsa_stack_backward(void* stream, const zsa_layer_cfg* cfg, const zsa_layer_weights* w,
+                       const zsa_layer_grads* grads, int32_t n_layers, const int32_t* prune_after,
+                       int32_t n_prune, const double* keep_rate, const void* hidden_in,
+                       const int32_t* pos_in, int32_t batch, const int32_t* cu_host,
+                       const int32_t* cu_dev, const void* dy, void* dx, void* ws,
+                       size_t ws_bytes);
+size_t zsa_stack_backward_workspace_size(const zsa_layer_cfg* cfg, int32_t total_rows,
+                                         int32_t batch, int32_t n_layers, int32_t n_prune);
+
+/* ---------------------------------------------------------------------
  * One generated row per sequence through the stack, after a prefill that
  * filled kv_cache (zsa_stack_forward). Generated rows are never pruned: at
  * block l the new row of sequence b attends (Eq. 1) to the kv_len_host[l *

@@ -28,6 +28,7 @@ SOURCES = [
     "k_select.hip",
     "k_gather.hip",
     "k_decode.hip",
+    "k_backward.hip",
 ]
 
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")

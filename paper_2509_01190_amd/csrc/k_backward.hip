@@ -1,0 +1,753 @@
+// Backward pass through the pruned block (the fine-tuning step of Eq. 3
+// trains through the pruned forward; the kept rows are constants).
+//
+// Row-wise pieces: transposes (so both products of a projection's backward
+// run on the forward's NT GEMM), column sums (bias / gain gradients, in a
+// fixed order), LayerNorm / RMSNorm backward, GELU / SwiGLU backward, the
+// scatter that undoes compaction (dropped rows get zero gradient), the
+// per-row dot D_i = dO_i . O_i, and the inverse rotary rotation.
+//
+// Attention backward (bf16, head_dim 64 / 128, MFMA), with P recomputed
+// from the forward's log-sum-exp:
+//     dV = P^T dO,  dP = dO V^T,  dS = P o (dP - D),  dK = scale dS^T Q,
+//     dQ = scale dS K.
+// attn_bwd_dkdv: one workgroup per (key block, key/value head, sequence);
+// every wave walks 32-query tiles, computes S = Q K^T and dP = dO V^T in the
+// layout where a lane owns one key, packs P and dS as MFMA A operands and
+// multiplies them with transposed Q / dO tiles staged in its own LDS; the
+// four waves' partial dK / dV are added in wave order (no atomics). For
+// grouped-query attention the workgroup also loops over the query heads
+// that read its key/value head.
+// attn_bwd_dq: one workgroup per (128-query block, head, sequence), laid out
+// like the forward attention: S^T and dP^T with a lane owning one query, dS
+// packed as the B operand of dQ^T += K^T dS^T, K^T staged in LDS.
+#include <math.h>
+
+#include "zsa_internal.h"
+
+namespace zsa {
+namespace {
+
+typedef __bf16 bf16x8_t __attribute__((ext_vector_type(8)));
+typedef float f32x16_t __attribute__((ext_vector_type(16)));
+constexpr float kLog2e = 1.4426950408889634f;
+
+// ---------------------------------------------------------------------------
+// transpose: out[c][r] = in[r][c] for r < R, 0 for R <= r < Rpad
+// ---------------------------------------------------------------------------
+template <typename T>
+__global__ __launch_bounds__(256) void transpose_kernel(const T* __restrict__ in, int R, int C,
+                                                        int64_t ldi, T* __restrict__ out,
+                                                        int Rpad) {
+  __shared__ T tile[32][33];
+  const int r0 = blockIdx.y * 32, c0 = blockIdx.x * 32;
+  const int tx = threadIdx.x & 31, ty = threadIdx.x >> 5;  // 8 rows per pass
+  for (int k = ty; k < 32; k += 8) {
+    const int r = r0 + k, c = c0 + tx;
+    tile[k][tx] = (r < R && c < C) ? in[static_cast<int64_t>(r) * ldi + c] : T(0.f);
+  }
+  __syncthreads();
+  for (int k = ty; k < 32; k += 8) {
+    const int c = c0 + k, r = r0 + tx;
+    if (c < C && r < Rpad) out[static_cast<int64_t>(c) * Rpad + r] = tile[tx][k];
+  }
+}
+
+// ---------------------------------------------------------------------------
+// column sums in a fixed order: stage 1 sums row chunks, stage 2 the chunks
+// ---------------------------------------------------------------------------
+constexpr int kColRows = 256;  // rows per stage-1 chunk
+
+// sum over rows of a[r][c] (or of a[r][c] * xhat[r][c] when x is given, with
+// xhat = (x - mean_r) * rstd_r from stats [R][2])
+template <typename T>
+__global__ __launch_bounds__(256) void colsum_stage1(const T* __restrict__ a, int64_t lda,
+                                                     const T* __restrict__ x, int64_t ldx,
+                                                     const float* __restrict__ stats, int R,
+                                                     int C, float* __restrict__ part) {
+  const int c = blockIdx.x * 256 + threadIdx.x;
+  const int r0 = blockIdx.y * kColRows;
+  if (c >= C) return;
+  float s = 0.f;
+  const int r1 = min(R, r0 + kColRows);
+  for (int r = r0; r < r1; ++r) {
+    float v = to_f32(a[static_cast<int64_t>(r) * lda + c]);
+    if (x != nullptr)
+      v *= (to_f32(x[static_cast<int64_t>(r) * ldx + c]) - stats[2 * r]) * stats[2 * r + 1];
+    s += v;
+  }
+  part[static_cast<int64_t>(blockIdx.y) * C + c] = s;
+}
+
+__global__ __launch_bounds__(256) void colsum_stage2(const float* __restrict__ part, int chunks,
+                                                     int C, float* __restrict__ out) {
+  const int c = blockIdx.x * 256 + threadIdx.x;
+  if (c >= C) return;
+  float s = 0.f;
+  for (int k = 0; k < chunks; ++k) s += part[static_cast<int64_t>(k) * C + c];
+  out[c] = s;
+}
+
+// ---------------------------------------------------------------------------
+// norm backward: one wave per row.
+//   LN:  dx = rstd (g dh - mean(g dh) - xhat mean(g dh xhat))
+//   RMS: dx = rstd (g dh - xhat mean(g dh xhat))
+// out = res + dx (res may alias out, or be NULL); stats[r] = (mean, rstd)
+// (mean 0 for RMS) for the gain / shift gradients.
+// ---------------------------------------------------------------------------
+template <typename T, int RMS>
+__global__ __launch_bounds__(256) void norm_bwd_kernel(const T* __restrict__ x,
+                                                       const T* __restrict__ g,
+                                                       const T* __restrict__ dh, const T* res,
+                                                       T* out, int R, int d, float eps,
+                                                       float* __restrict__ stats) {
+  const int row = blockIdx.x * 4 + (threadIdx.x >> 6);
+  const int lane = threadIdx.x & 63;
+  if (row >= R) return;
+  const T* xr = x + static_cast<int64_t>(row) * d;
+  const T* dr = dh + static_cast<int64_t>(row) * d;
+  float mean = 0.f;
+  if (!RMS) {
+    float s = 0.f;
+    for (int c = lane; c < d; c += 64) s += to_f32(xr[c]);
+    for (int o = 32; o > 0; o >>= 1) s += __shfl_xor(s, o, 64);
+    mean = s / d;
+  }
+  float ss = 0.f;
+  for (int c = lane; c < d; c += 64) {
+    const float v = to_f32(xr[c]) - mean;
+    ss += v * v;
+  }
+  for (int o = 32; o > 0; o >>= 1) ss += __shfl_xor(ss, o, 64);
+  const float rstd = 1.0f / sqrtf(ss / d + eps);
+  float s1 = 0.f, s2 = 0.f;  // sum(g dh), sum(g dh xhat)
+  for (int c = lane; c < d; c += 64) {
+    const float gd = to_f32(g[c]) * to_f32(dr[c]);
+    s1 += gd;
+    s2 += gd * (to_f32(xr[c]) - mean) * rstd;
+  }
+  for (int o = 32; o > 0; o >>= 1) {
+    s1 += __shfl_xor(s1, o, 64);
+    s2 += __shfl_xor(s2, o, 64);
+  }
+  const float m1 = RMS ? 0.f : s1 / d, m2 = s2 / d;
+  for (int c = lane; c < d; c += 64) {
+    const float xh = (to_f32(xr[c]) - mean) * rstd;
+    float v = rstd * (to_f32(g[c]) * to_f32(dr[c]) - m1 - xh * m2);
+    if (res != nullptr) v += to_f32(res[static_cast<int64_t>(row) * d + c]);
+    out[static_cast<int64_t>(row) * d + c] = from_f32<T>(v);
+  }
+  if (lane == 0) {
+    stats[2 * row] = mean;
+    stats[2 * row + 1] = rstd;
+  }
+}
+
+// ---------------------------------------------------------------------------
+// activation backward. GELU: du = dF (Phi(u) + u phi(u)). SwiGLU on
+// interleaved columns (2f gate, 2f+1 up): dgate = dF up silu'(gate),
+// dup = dF silu(gate), silu'(z) = s (1 + z (1 - s)), s = sigmoid(z).
+// ---------------------------------------------------------------------------
+template <typename T>
+__global__ __launch_bounds__(256) void act_bwd_kernel(const T* __restrict__ dF,
+                                                      const T* __restrict__ u, T* __restrict__ du,
+                                                      int64_t rows, int F, int swiglu) {
+  const int64_t i = static_cast<int64_t>(blockIdx.x) * 256 + threadIdx.x;
+  if (i >= rows * F) return;
+  const int64_t r = i / F;
+  const int f = static_cast<int>(i - r * F);
+  const float g = to_f32(dF[i]);
+  if (swiglu) {
+    const float z = to_f32(u[r * 2 * F + 2 * f]);
+    const float up = to_f32(u[r * 2 * F + 2 * f + 1]);
+    const float s = 1.0f / (1.0f + expf(-z));
+    du[r * 2 * F + 2 * f] = from_f32<T>(g * up * s * (1.0f + z * (1.0f - s)));
+    du[r * 2 * F + 2 * f + 1] = from_f32<T>(g * z * s);
+  } else {
+    const float z = to_f32(u[i]);
+    const float cdf = 0.5f * (1.0f + erff(z * 0.70710678118654752f));
+    const float pdf = 0.39894228040143268f * expf(-0.5f * z * z);
+    du[i] = from_f32<T>(g * (cdf + z * pdf));
+  }
+}
+
+// the activation itself from the pre-activation u (GELU, or SwiGLU on
+// interleaved gate / up columns): the backward's recomputed forward
+template <typename T>
+__global__ __launch_bounds__(256) void act_fwd_kernel(const T* __restrict__ u, T* __restrict__ f,
+                                                      int64_t rows, int F, int swiglu) {
+  const int64_t i = static_cast<int64_t>(blockIdx.x) * 256 + threadIdx.x;
+  if (i >= rows * F) return;
+  const int64_t r = i / F;
+  const int c = static_cast<int>(i - r * F);
+  if (swiglu) {
+    const float z = to_f32(u[r * 2 * F + 2 * c]);
+    const float up = to_f32(u[r * 2 * F + 2 * c + 1]);
+    f[i] = from_f32<T>(z / (1.0f + expf(-z)) * up);
+  } else {
+    const float z = to_f32(u[i]);
+    f[i] = from_f32<T>(0.5f * z * (1.0f + erff(z * 0.70710678118654752f)));
+  }
+}
+
+// ---------------------------------------------------------------------------
+// undo compaction: dst[r] = src[inv[r]] for kept rows, 0 for dropped ones
+// ---------------------------------------------------------------------------
+__global__ void inverse_index_kernel(const int32_t* __restrict__ kept, int t_out, int t_in,
+                                     int32_t* __restrict__ inv) {
+  // one pass per row of the input: rows not found stay -1 (filled first)
+  const int i = blockIdx.x * blockDim.x + threadIdx.x;
+  if (i < t_out) {
+    const int r = kept[i];
+    if (r >= 0 && r < t_in) inv[r] = i;
+  }
+}
+
+__global__ void fill_i32_kernel(int32_t* __restrict__ p, int n, int v) {
+  const int i = blockIdx.x * blockDim.x + threadIdx.x;
+  if (i < n) p[i] = v;
+}
+
+__global__ __launch_bounds__(256) void scatter_rows_kernel(const uint4* __restrict__ src,
+                                                           const int32_t* __restrict__ inv,
+                                                           int t_in, int cpr,
+                                                           uint4* __restrict__ dst) {
+  const int64_t i = static_cast<int64_t>(blockIdx.x) * 256 + threadIdx.x;
+  if (i >= static_cast<int64_t>(t_in) * cpr) return;
+  const int r = static_cast<int>(i / cpr), c = static_cast<int>(i % cpr);
+  const int s = inv[r];
+  dst[i] = s >= 0 ? src[static_cast<int64_t>(s) * cpr + c] : make_uint4(0u, 0u, 0u, 0u);
+}
+
+// D[h][r] = sum_c dO[r][h hd + c] O[r][h hd + c]
+template <typename T>
+__global__ __launch_bounds__(256) void rowdot_kernel(const T* __restrict__ dO,
+                                                     const T* __restrict__ O, int64_t ld, int T_,
+                                                     int H, int hd, float* __restrict__ D) {
+  const int64_t i = static_cast<int64_t>(blockIdx.x) * 256 + threadIdx.x;
+  if (i >= static_cast<int64_t>(T_) * H) return;
+  const int r = static_cast<int>(i / H), h = static_cast<int>(i % H);
+  float s = 0.f;
+  for (int c = 0; c < hd; ++c)
+    s = fmaf(to_f32(dO[static_cast<int64_t>(r) * ld + h * hd + c]),
+             to_f32(O[static_cast<int64_t>(r) * ld + h * hd + c]), s);
+  D[static_cast<int64_t>(h) * T_ + r] = s;
+}
+
+// inverse rotary rotation of the gradient, in place, on the first `cols`
+// columns (whole heads) of rows of a [rows, ld] array
+template <typename T>
+__global__ __launch_bounds__(256) void rope_bwd_kernel(T* __restrict__ g, int64_t ld, int rows,
+                                                       int cols, int hd,
+                                                       const int32_t* __restrict__ pos,
+                                                       EpiParams ep) {
+  const int half = hd / 2;
+  const int64_t i = static_cast<int64_t>(blockIdx.x) * 256 + threadIdx.x;
+  const int pairs = cols / 2;
+  if (i >= static_cast<int64_t>(rows) * pairs) return;
+  const int r = static_cast<int>(i / pairs);
+  const int pr = static_cast<int>(i % pairs);
+  const int head = pr / half, k = pr % half;
+  const int64_t a = static_cast<int64_t>(r) * ld + head * hd + k;
+  float sn, cs;
+  rope_angle(pos[r], ep.inv_freq[k], &sn, &cs);
+  const float x = to_f32(g[a]), y = to_f32(g[a + half]);
+  g[a] = from_f32<T>(x * cs + y * sn);
+  g[a + half] = from_f32<T>(y * cs - x * sn);
+}
+
+// ---------------------------------------------------------------------------
+// attention backward, dK and dV
+// ---------------------------------------------------------------------------
+__device__ __forceinline__ float pick4(const float4& v, int i) {
+  return i == 0 ? v.x : i == 1 ? v.y : i == 2 ? v.z : v.w;
+}
+
+template <int HD, int NKS>
+__global__ __launch_bounds__(256) void attn_bwd_dkdv_kernel(
+    const bf16_t* __restrict__ Q, const bf16_t* __restrict__ K, const bf16_t* __restrict__ V,
+    int64_t rs, const bf16_t* __restrict__ dO, int64_t ors, const float* __restrict__ lse,
+    const float* __restrict__ Dv, int T, int H, int kv_group, int causal, float scale,
+    float scale_log2, const int32_t* __restrict__ cu, bf16_t* __restrict__ dK,
+    bf16_t* __restrict__ dV, int64_t grs) {
+  constexpr int KW = 32 * NKS;    // keys per workgroup
+  constexpr int KK = HD / 16;
+  constexpr int CT = HD / 32;
+  constexpr int TLD = 32 + 8;     // transposed tile row stride (bf16)
+  constexpr int WAVE_BYTES = 2 * HD * TLD * 2;
+  constexpr int RED_BYTES = 4 * KW * HD * 4;
+  constexpr int SMEM = 4 * WAVE_BYTES > RED_BYTES ? 4 * WAVE_BYTES : RED_BYTES;
+  __shared__ __align__(16) unsigned char smem[SMEM];
+  const int b = blockIdx.z, g = blockIdx.y;
+  const int lo = cu[b];
+  const int n = cu[b + 1] - lo;
+  const int j0 = blockIdx.x * KW;
+  if (j0 >= n) return;
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int half = lane >> 5, l32 = lane & 31;
+  bf16_t* Qt = reinterpret_cast<bf16_t*>(smem + wave * WAVE_BYTES);
+  bf16_t* Dt = Qt + HD * TLD;
+
+  bf16x8_t kf[NKS][KK], vf[NKS][KK];
+#pragma unroll
+  for (int ks = 0; ks < NKS; ++ks) {
+    const int jr = lo + min(j0 + ks * 32 + l32, n - 1);
+#pragma unroll
+    for (int kk = 0; kk < KK; ++kk) {
+      kf[ks][kk] = __builtin_bit_cast(bf16x8_t, *reinterpret_cast<const u32x4*>(
+                                                    K + static_cast<int64_t>(jr) * rs + g * HD + kk * 16 + half * 8));
+      vf[ks][kk] = __builtin_bit_cast(bf16x8_t, *reinterpret_cast<const u32x4*>(
+                                                    V + static_cast<int64_t>(jr) * rs + g * HD + kk * 16 + half * 8));
+    }
+  }
+  f32x16_t dk[NKS][CT], dv[NKS][CT];
+#pragma unroll
+  for (int ks = 0; ks < NKS; ++ks)
+#pragma unroll
+    for (int ct = 0; ct < CT; ++ct)
+#pragma unroll
+      for (int r = 0; r < 16; ++r) {
+        dk[ks][ct][r] = 0.f;
+        dv[ks][ct][r] = 0.f;
+      }
+
+  const int qs = causal ? (j0 & ~31) : 0;
+  // the four waves take the query tiles base + 32 wave in lockstep (a wave
+  // past the sequence idles), so block barriers order the LDS staging
+  for (int e = 0; e < kv_group; ++e) {
+    const int h = g * kv_group + e;
+    for (int base = qs; base < n; base += 128) {
+      const int i0 = base + wave * 32;
+      const bool active = i0 < n;
+      __syncthreads();  // the previous round's reads of the staged tiles are done
+      if (active) {
+      // this tile's Q and dO, transposed into the wave's LDS (query pairs packed)
+      for (int task = lane; task < 16 * (HD / 8); task += 64) {
+        const int rp = task / (HD / 8), ch = (task % (HD / 8)) * 8;
+        const int r0 = lo + min(i0 + 2 * rp, n - 1), r1 = lo + min(i0 + 2 * rp + 1, n - 1);
+        const u32x4 q0 = *reinterpret_cast<const u32x4*>(Q + static_cast<int64_t>(r0) * rs + h * HD + ch);
+        const u32x4 q1 = *reinterpret_cast<const u32x4*>(Q + static_cast<int64_t>(r1) * rs + h * HD + ch);
+        const u32x4 d0 = *reinterpret_cast<const u32x4*>(dO + static_cast<int64_t>(r0) * ors + h * HD + ch);
+        const u32x4 d1 = *reinterpret_cast<const u32x4*>(dO + static_cast<int64_t>(r1) * ors + h * HD + ch);
+#pragma unroll
+        for (int c = 0; c < 8; ++c) {
+          const uint32_t a0 = q0[c >> 1], a1 = q1[c >> 1], b0 = d0[c >> 1], b1 = d1[c >> 1];
+          const uint32_t qlo = (c & 1) ? (a0 >> 16) : (a0 & 0xffffu);
+          const uint32_t qhi = (c & 1) ? (a1 & 0xffff0000u) : (a1 << 16);
+          const uint32_t dlo = (c & 1) ? (b0 >> 16) : (b0 & 0xffffu);
+          const uint32_t dhi = (c & 1) ? (b1 & 0xffff0000u) : (b1 << 16);
+          *reinterpret_cast<uint32_t*>(Qt + (ch + c) * TLD + 2 * rp) = qlo | qhi;
+          *reinterpret_cast<uint32_t*>(Dt + (ch + c) * TLD + 2 * rp) = dlo | dhi;
+        }
+      }
+      }
+      __syncthreads();
+      if (!active) continue;
+      const int qr = lo + min(i0 + l32, n - 1);
+      bf16x8_t qa[KK], da[KK];
+#pragma unroll
+      for (int kk = 0; kk < KK; ++kk) {
+        qa[kk] = __builtin_bit_cast(bf16x8_t, *reinterpret_cast<const u32x4*>(
+                                                  Q + static_cast<int64_t>(qr) * rs + h * HD + kk * 16 + half * 8));
+        da[kk] = __builtin_bit_cast(bf16x8_t, *reinterpret_cast<const u32x4*>(
+                                                  dO + static_cast<int64_t>(qr) * ors + h * HD + kk * 16 + half * 8));
+      }
+      // this lane's 16 query rows: i0 + 8 (r/4) + 4 half + r%4
+      float L[16], Dd[16];
+#pragma unroll
+      for (int r = 0; r < 16; ++r) {
+        const int i = min(i0 + 8 * (r >> 2) + 4 * half + (r & 3), n - 1);
+        L[r] = lse[static_cast<int64_t>(h) * T + lo + i] * kLog2e;
+        Dd[r] = Dv[static_cast<int64_t>(h) * T + lo + i];
+      }
+      const bool edge = i0 + 32 > n || (causal && j0 + KW - 1 > i0);
+#pragma unroll
+      for (int ks = 0; ks < NKS; ++ks) {
+        f32x16_t s, dp;
+#pragma unroll
+        for (int r = 0; r < 16; ++r) {
+          s[r] = 0.f;
+          dp[r] = 0.f;
+        }
+#pragma unroll
+        for (int kk = 0; kk < KK; ++kk) {
+          s = __builtin_amdgcn_mfma_f32_32x32x16_bf16(qa[kk], kf[ks][kk], s, 0, 0, 0);
+          dp = __builtin_amdgcn_mfma_f32_32x32x16_bf16(da[kk], vf[ks][kk], dp, 0, 0, 0);
+        }
+        // s[r], dp[r]: query i0 + 8 (r/4) + 4 half + r%4, key j0 + 32 ks + l32
+        const int j = j0 + ks * 32 + l32;
+#pragma unroll
+        for (int r = 0; r < 16; ++r) {
+          float p = __builtin_amdgcn_exp2f(fmaf(s[r], scale_log2, -L[r]));
+          if (edge) {
+            const int i = i0 + 8 * (r >> 2) + 4 * half + (r & 3);
+            if (i >= n || j >= n || (causal && j > i)) p = 0.f;
+          }
+          s[r] = p;
+          dp[r] = p * (dp[r] - Dd[r]);
+        }
+#pragma unroll
+        for (int g4 = 0; g4 < 2; ++g4) {
+          const int rb = 8 * g4;
+          const u32x4 pw = {pack_bf16x2(s[rb], s[rb + 1]), pack_bf16x2(s[rb + 2], s[rb + 3]),
+                            pack_bf16x2(s[rb + 4], s[rb + 5]), pack_bf16x2(s[rb + 6], s[rb + 7])};
+          const u32x4 sw = {pack_bf16x2(dp[rb], dp[rb + 1]), pack_bf16x2(dp[rb + 2], dp[rb + 3]),
+                            pack_bf16x2(dp[rb + 4], dp[rb + 5]), pack_bf16x2(dp[rb + 6], dp[rb + 7])};
+          const bf16x8_t pa = __builtin_bit_cast(bf16x8_t, pw);
+          const bf16x8_t sa = __builtin_bit_cast(bf16x8_t, sw);
+          const int base = 16 * g4 + 4 * half;  // queries base..+3, base+8..+11
+#pragma unroll
+          for (int ct = 0; ct < CT; ++ct) {
+            const bf16_t* dr = Dt + (ct * 32 + l32) * TLD + base;
+            const bf16_t* qrw = Qt + (ct * 32 + l32) * TLD + base;
+            const uint2 d_lo = *reinterpret_cast<const uint2*>(dr);
+            const uint2 d_hi = *reinterpret_cast<const uint2*>(dr + 8);
+            const uint2 q_lo = *reinterpret_cast<const uint2*>(qrw);
+            const uint2 q_hi = *reinterpret_cast<const uint2*>(qrw + 8);
+            const u32x4 bd = {d_lo.x, d_lo.y, d_hi.x, d_hi.y};
+            const u32x4 bq = {q_lo.x, q_lo.y, q_hi.x, q_hi.y};
+            dv[ks][ct] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(
+                pa, __builtin_bit_cast(bf16x8_t, bd), dv[ks][ct], 0, 0, 0);
+            dk[ks][ct] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(
+                sa, __builtin_bit_cast(bf16x8_t, bq), dk[ks][ct], 0, 0, 0);
+          }
+        }
+      }
+    }
+  }
+  // acc[ks][ct][r]: key j0 + 32 ks + 8 (r/4) + 4 half + r%4, channel ct*32 + l32.
+  // The waves' partial sums are added in wave order through LDS.
+  float* red = reinterpret_cast<float*>(smem);
+#pragma unroll
+  for (int pass = 0; pass < 2; ++pass) {
+    __syncthreads();
+#pragma unroll
+    for (int ks = 0; ks < NKS; ++ks)
+#pragma unroll
+      for (int ct = 0; ct < CT; ++ct)
+#pragma unroll
+        for (int r = 0; r < 16; ++r) {
+          const int key = ks * 32 + 8 * (r >> 2) + 4 * half + (r & 3);
+          red[(wave * KW + key) * HD + ct * 32 + l32] = pass == 0 ? dv[ks][ct][r] : dk[ks][ct][r];
+        }
+    __syncthreads();
+    bf16_t* dst = pass == 0 ? dV : dK;
+    const float mul = pass == 0 ? 1.0f : scale;
+    for (int e2 = tid; e2 < KW * HD; e2 += 256) {
+      const int key = e2 / HD, c = e2 % HD;
+      if (j0 + key >= n) continue;
+      const float v = ((red[(0 * KW + key) * HD + c] + red[(1 * KW + key) * HD + c]) +
+                       red[(2 * KW + key) * HD + c]) + red[(3 * KW + key) * HD + c];
+      dst[static_cast<int64_t>(lo + j0 + key) * grs + g * HD + c] = f32_to_bf16(v * mul);
+    }
+  }
+}
+
+// ---------------------------------------------------------------------------
+// attention backward, dQ
+// ---------------------------------------------------------------------------
+template <int HD>
+__global__ __launch_bounds__(256) void attn_bwd_dq_kernel(
+    const bf16_t* __restrict__ Q, const bf16_t* __restrict__ K, const bf16_t* __restrict__ V,
+    int64_t rs, const bf16_t* __restrict__ dO, int64_t ors, const float* __restrict__ lse,
+    const float* __restrict__ Dv, int T, int kv_group, int causal, float scale, float scale_log2,
+    const int32_t* __restrict__ cu, bf16_t* __restrict__ dQ, int64_t grs) {
+  constexpr int BQ = 128, BKEY = 64;
+  constexpr int KLD = HD + 8, TLD = BKEY + 8, OLD = HD + 8;
+  constexpr int KK = HD / 16, CT = HD / 32;
+  constexpr int KB = BKEY * KLD * 2, TB = HD * TLD * 2;
+  constexpr int SMEM = 2 * KB + TB > 4 * 32 * OLD * 2 ? 2 * KB + TB : 4 * 32 * OLD * 2;
+  __shared__ __align__(16) unsigned char smem[SMEM];
+  bf16_t* Ks = reinterpret_cast<bf16_t*>(smem);
+  bf16_t* Vs = reinterpret_cast<bf16_t*>(smem + KB);
+  bf16_t* Kt = reinterpret_cast<bf16_t*>(smem + 2 * KB);
+
+  const int b = blockIdx.z, h = blockIdx.y;
+  const int lo = cu[b];
+  const int n = cu[b + 1] - lo;
+  const int q0 = blockIdx.x * BQ;
+  if (q0 >= n) return;
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int half = lane >> 5, l32 = lane & 31;
+  const int qrow = q0 + wave * 32 + l32;
+  const int qr = lo + min(qrow, n - 1);
+  const int hk = h / kv_group;
+  bf16x8_t qf[KK], df[KK];
+#pragma unroll
+  for (int kk = 0; kk < KK; ++kk) {
+    qf[kk] = __builtin_bit_cast(bf16x8_t, *reinterpret_cast<const u32x4*>(
+                                              Q + static_cast<int64_t>(qr) * rs + h * HD + kk * 16 + half * 8));
+    df[kk] = __builtin_bit_cast(bf16x8_t, *reinterpret_cast<const u32x4*>(
+                                              dO + static_cast<int64_t>(qr) * ors + h * HD + kk * 16 + half * 8));
+  }
+  const float Lq = lse[static_cast<int64_t>(h) * T + qr] * kLog2e;
+  const float Dq = Dv[static_cast<int64_t>(h) * T + qr];
+  f32x16_t acc[CT];
+#pragma unroll
+  for (int ct = 0; ct < CT; ++ct)
+#pragma unroll
+    for (int r = 0; r < 16; ++r) acc[ct][r] = 0.f;
+
+  const int kend = causal ? min(n, q0 + BQ) : n;
+  const int wave_q0 = q0 + wave * 32;
+  for (int j0 = 0; j0 < kend; j0 += BKEY) {
+    __syncthreads();
+    for (int c = tid; c < BKEY * HD / 8; c += 256) {
+      const int r = c / (HD / 8), ch = (c % (HD / 8)) * 8;
+      const int64_t row = lo + min(j0 + r, n - 1);
+      *reinterpret_cast<u32x4*>(Ks + r * KLD + ch) =
+          *reinterpret_cast<const u32x4*>(K + row * rs + hk * HD + ch);
+      *reinterpret_cast<u32x4*>(Vs + r * KLD + ch) =
+          *reinterpret_cast<const u32x4*>(V + row * rs + hk * HD + ch);
+    }
+    // K^T with key pairs packed
+    for (int c = tid; c < (BKEY / 2) * (HD / 8); c += 256) {
+      const int rp = c / (HD / 8), ch = (c % (HD / 8)) * 8;
+      const int64_t r0 = lo + min(j0 + 2 * rp, n - 1), r1 = lo + min(j0 + 2 * rp + 1, n - 1);
+      const u32x4 k0 = *reinterpret_cast<const u32x4*>(K + r0 * rs + hk * HD + ch);
+      const u32x4 k1 = *reinterpret_cast<const u32x4*>(K + r1 * rs + hk * HD + ch);
+#pragma unroll
+      for (int e = 0; e < 8; ++e) {
+        const uint32_t w0 = k0[e >> 1], w1 = k1[e >> 1];
+        const uint32_t x0 = (e & 1) ? (w0 >> 16) : (w0 & 0xffffu);
+        const uint32_t x1 = (e & 1) ? (w1 & 0xffff0000u) : (w1 << 16);
+        *reinterpret_cast<uint32_t*>(Kt + (ch + e) * TLD + 2 * rp) = x0 | x1;
+      }
+    }
+    __syncthreads();
+    if (causal && j0 > wave_q0 + 31) continue;
+#pragma unroll
+    for (int ks = 0; ks < 2; ++ks) {
+      f32x16_t s, dp;
+#pragma unroll
+      for (int r = 0; r < 16; ++r) {
+        s[r] = 0.f;
+        dp[r] = 0.f;
+      }
+#pragma unroll
+      for (int kk = 0; kk < KK; ++kk) {
+        const bf16x8_t ka = __builtin_bit_cast(
+            bf16x8_t, *reinterpret_cast<const u32x4*>(Ks + (ks * 32 + l32) * KLD + kk * 16 + half * 8));
+        const bf16x8_t va = __builtin_bit_cast(
+            bf16x8_t, *reinterpret_cast<const u32x4*>(Vs + (ks * 32 + l32) * KLD + kk * 16 + half * 8));
+        s = __builtin_amdgcn_mfma_f32_32x32x16_bf16(ka, qf[kk], s, 0, 0, 0);
+        dp = __builtin_amdgcn_mfma_f32_32x32x16_bf16(va, df[kk], dp, 0, 0, 0);
+      }
+      // s[r], dp[r]: key j0 + 32 ks + 8 (r/4) + 4 half + r%4, query qrow
+      const bool edge = j0 + BKEY > n || (causal && j0 + BKEY - 1 > wave_q0);
+#pragma unroll
+      for (int r = 0; r < 16; ++r) {
+        float p = __builtin_amdgcn_exp2f(fmaf(s[r], scale_log2, -Lq));
+        if (edge) {
+          const int j = j0 + ks * 32 + 8 * (r >> 2) + 4 * half + (r & 3);
+          if (j >= n || qrow >= n || (causal && j > qrow)) p = 0.f;
+        }
+        s[r] = p * (dp[r] - Dq);  // dS
+      }
+#pragma unroll
+      for (int g4 = 0; g4 < 2; ++g4) {
+        const int rb = 8 * g4;
+        const u32x4 sw = {pack_bf16x2(s[rb], s[rb + 1]), pack_bf16x2(s[rb + 2], s[rb + 3]),
+                          pack_bf16x2(s[rb + 4], s[rb + 5]), pack_bf16x2(s[rb + 6], s[rb + 7])};
+        const bf16x8_t sb = __builtin_bit_cast(bf16x8_t, sw);
+        const int base = ks * 32 + 16 * g4 + 4 * half;
+#pragma unroll
+        for (int ct = 0; ct < CT; ++ct) {
+          const bf16_t* kr = Kt + (ct * 32 + l32) * TLD + base;
+          const uint2 a_lo = *reinterpret_cast<const uint2*>(kr);
+          const uint2 a_hi = *reinterpret_cast<const uint2*>(kr + 8);
+          const u32x4 av = {a_lo.x, a_lo.y, a_hi.x, a_hi.y};
+          acc[ct] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(__builtin_bit_cast(bf16x8_t, av), sb,
+                                                             acc[ct], 0, 0, 0);
+        }
+      }
+    }
+  }
+  // acc[ct][r] = dQ^T[channel ct*32 + 8 (r/4) + 4 half + r%4][query qrow] / scale
+  __syncthreads();
+  bf16_t* Os = reinterpret_cast<bf16_t*>(smem) + wave * 32 * OLD;
+#pragma unroll
+  for (int ct = 0; ct < CT; ++ct)
+#pragma unroll
+    for (int r = 0; r < 16; ++r) {
+      const int c = ct * 32 + 8 * (r >> 2) + 4 * half + (r & 3);
+      Os[l32 * OLD + c] = f32_to_bf16(acc[ct][r] * scale);
+    }
+  __syncthreads();
+  for (int c = lane; c < 32 * HD / 8; c += 64) {
+    const int r = c / (HD / 8), ch = (c % (HD / 8)) * 8;
+    const int q = q0 + wave * 32 + r;
+    if (q < n)
+      *reinterpret_cast<u32x4*>(dQ + static_cast<int64_t>(lo + q) * grs + h * HD + ch) =
+          *reinterpret_cast<const u32x4*>(Os + r * OLD + ch);
+  }
+}
+
+template <typename T>
+hipError_t transpose_t(hipStream_t s, const void* in, int R, int C, int64_t ldi, void* out,
+                       int Rpad) {
+  const dim3 grid((C + 31) / 32, (Rpad + 31) / 32);
+  return launch(K_MISC, transpose_kernel<T>, grid, dim3(256), 0, s, static_cast<const T*>(in), R,
+                C, ldi, static_cast<T*>(out), Rpad);
+}
+
+}  // namespace
+
+bool backward_supported(int dtype, int hd) { return dtype == 1 && (hd == 64 || hd == 128); }
+
+hipError_t launch_transpose(hipStream_t s, int dtype, const void* in, int R, int C, int64_t ldi,
+                            void* out, int Rpad) {
+  if (C == 0 || Rpad == 0) return hipSuccess;
+  return dtype == 1 ? transpose_t<bf16_t>(s, in, R, C, ldi, out, Rpad)
+                    : transpose_t<float>(s, in, R, C, ldi, out, Rpad);
+}
+
+size_t colsum_scratch_floats(int R, int C) {
+  return static_cast<size_t>((R + kColRows - 1) / kColRows + 1) * C;
+}
+
+hipError_t launch_colsum(hipStream_t s, int dtype, const void* a, int64_t lda, const void* x,
+                         int64_t ldx, const float* stats, int R, int C, float* scratch,
+                         float* out) {
+  if (C == 0) return hipSuccess;
+  const int chunks = R > 0 ? (R + kColRows - 1) / kColRows : 0;
+  hipError_t e = hipSuccess;
+  if (chunks > 0) {
+    const dim3 grid((C + 255) / 256, chunks);
+    e = dtype == 1 ? launch(K_MISC, colsum_stage1<bf16_t>, grid, dim3(256), 0, s,
+                            static_cast<const bf16_t*>(a), lda, static_cast<const bf16_t*>(x),
+                            ldx, stats, R, C, scratch)
+                   : launch(K_MISC, colsum_stage1<float>, grid, dim3(256), 0, s,
+                            static_cast<const float*>(a), lda, static_cast<const float*>(x), ldx,
+                            stats, R, C, scratch);
+    if (e != hipSuccess) return e;
+  }
+  return launch(K_MISC, colsum_stage2, dim3((C + 255) / 256), dim3(256), 0, s, scratch, chunks, C,
+                out);
+}
+
+hipError_t launch_norm_bwd(hipStream_t s, int dtype, int kind, const void* x, const void* g,
+                           const void* dh, const void* res, void* out, int R, int d, float eps,
+                           float* stats) {
+  if (R == 0) return hipSuccess;
+  const dim3 grid((R + 3) / 4), block(256);
+  if (dtype == 1) {
+    auto* xp = static_cast<const bf16_t*>(x);
+    auto* gp = static_cast<const bf16_t*>(g);
+    auto* dp = static_cast<const bf16_t*>(dh);
+    auto* rp = static_cast<const bf16_t*>(res);
+    auto* op = static_cast<bf16_t*>(out);
+    return kind == 1 ? launch(K_NORM, norm_bwd_kernel<bf16_t, 1>, grid, block, 0, s, xp, gp, dp, rp, op, R, d, eps, stats)
+                     : launch(K_NORM, norm_bwd_kernel<bf16_t, 0>, grid, block, 0, s, xp, gp, dp, rp, op, R, d, eps, stats);
+  }
+  auto* xp = static_cast<const float*>(x);
+  auto* gp = static_cast<const float*>(g);
+  auto* dp = static_cast<const float*>(dh);
+  auto* rp = static_cast<const float*>(res);
+  auto* op = static_cast<float*>(out);
+  return kind == 1 ? launch(K_NORM, norm_bwd_kernel<float, 1>, grid, block, 0, s, xp, gp, dp, rp, op, R, d, eps, stats)
+                   : launch(K_NORM, norm_bwd_kernel<float, 0>, grid, block, 0, s, xp, gp, dp, rp, op, R, d, eps, stats);
+}
+
+hipError_t launch_act_bwd(hipStream_t s, int dtype, const void* dF, const void* u, void* du,
+                          int rows, int F, int swiglu) {
+  const int64_t total = static_cast<int64_t>(rows) * F;
+  if (total == 0) return hipSuccess;
+  const dim3 grid(static_cast<unsigned>((total + 255) / 256));
+  if (dtype == 1)
+    return launch(K_MISC, act_bwd_kernel<bf16_t>, grid, dim3(256), 0, s,
+                  static_cast<const bf16_t*>(dF), static_cast<const bf16_t*>(u),
+                  static_cast<bf16_t*>(du), static_cast<int64_t>(rows), F, swiglu);
+  return launch(K_MISC, act_bwd_kernel<float>, grid, dim3(256), 0, s,
+                static_cast<const float*>(dF), static_cast<const float*>(u),
+                static_cast<float*>(du), static_cast<int64_t>(rows), F, swiglu);
+}
+
+hipError_t launch_act_fwd(hipStream_t s, int dtype, const void* u, void* f, int rows, int F,
+                          int swiglu) {
+  const int64_t total = static_cast<int64_t>(rows) * F;
+  if (total == 0) return hipSuccess;
+  const dim3 grid(static_cast<unsigned>((total + 255) / 256));
+  if (dtype == 1)
+    return launch(K_MISC, act_fwd_kernel<bf16_t>, grid, dim3(256), 0, s,
+                  static_cast<const bf16_t*>(u), static_cast<bf16_t*>(f),
+                  static_cast<int64_t>(rows), F, swiglu);
+  return launch(K_MISC, act_fwd_kernel<float>, grid, dim3(256), 0, s, static_cast<const float*>(u),
+                static_cast<float*>(f), static_cast<int64_t>(rows), F, swiglu);
+}
+
+hipError_t launch_scatter_rows(hipStream_t s, int dtype, int d, const void* src,
+                               const int32_t* kept, int t_out, int t_in, int32_t* inv,
+                               void* dst) {
+  if (t_in == 0) return hipSuccess;
+  hipError_t e = launch(K_MISC, fill_i32_kernel, dim3((t_in + 255) / 256), dim3(256), 0, s, inv,
+                        t_in, -1);
+  if (e != hipSuccess) return e;
+  if (t_out > 0) {
+    e = launch(K_MISC, inverse_index_kernel, dim3((t_out + 255) / 256), dim3(256), 0, s, kept,
+               t_out, t_in, inv);
+    if (e != hipSuccess) return e;
+  }
+  const int cpr = d * (dtype == 1 ? 2 : 4) / 16;
+  const int64_t total = static_cast<int64_t>(t_in) * cpr;
+  return launch(K_MISC, scatter_rows_kernel, dim3(static_cast<unsigned>((total + 255) / 256)),
+                dim3(256), 0, s, static_cast<const uint4*>(src), inv, t_in, cpr,
+                static_cast<uint4*>(dst));
+}
+
+hipError_t launch_rowdot(hipStream_t s, int dtype, const void* dO, const void* O, int64_t ld,
+                         int T, int H, int hd, float* D) {
+  const int64_t total = static_cast<int64_t>(T) * H;
+  if (total == 0) return hipSuccess;
+  const dim3 grid(static_cast<unsigned>((total + 255) / 256));
+  if (dtype == 1)
+    return launch(K_MISC, rowdot_kernel<bf16_t>, grid, dim3(256), 0, s,
+                  static_cast<const bf16_t*>(dO), static_cast<const bf16_t*>(O), ld, T, H, hd, D);
+  return launch(K_MISC, rowdot_kernel<float>, grid, dim3(256), 0, s, static_cast<const float*>(dO),
+                static_cast<const float*>(O), ld, T, H, hd, D);
+}
+
+hipError_t launch_rope_bwd(hipStream_t s, int dtype, void* g, int64_t ld, int rows, int cols,
+                           int hd, const int32_t* pos, const EpiParams& ep) {
+  const int64_t total = static_cast<int64_t>(rows) * (cols / 2);
+  if (total == 0) return hipSuccess;
+  const dim3 grid(static_cast<unsigned>((total + 255) / 256));
+  if (dtype == 1)
+    return launch(K_MISC, rope_bwd_kernel<bf16_t>, grid, dim3(256), 0, s, static_cast<bf16_t*>(g),
+                  ld, rows, cols, hd, pos, ep);
+  return launch(K_MISC, rope_bwd_kernel<float>, grid, dim3(256), 0, s, static_cast<float*>(g), ld,
+                rows, cols, hd, pos, ep);
+}
+
+hipError_t launch_attention_bwd(hipStream_t s, const void* q, const void* k, const void* v,
+                                int64_t rs, const void* dO, int64_t ors, const float* lse,
+                                const float* D, int H, int kv_group, int hd, int causal,
+                                float scale, int B, int max_len, int T, const int32_t* cu_dev,
+                                void* dq, void* dk, void* dv, int64_t grs) {
+  if (B == 0 || max_len == 0) return hipSuccess;
+  const float sl = scale * kLog2e;
+  auto* qp = static_cast<const bf16_t*>(q);
+  auto* kp = static_cast<const bf16_t*>(k);
+  auto* vp = static_cast<const bf16_t*>(v);
+  auto* dp = static_cast<const bf16_t*>(dO);
+  const int Hkv = H / kv_group;
+  hipError_t e;
+  if (hd == 64) {
+    e = launch(K_ATTENTION, attn_bwd_dkdv_kernel<64, 2>, dim3((max_len + 63) / 64, Hkv, B),
+               dim3(256), 0, s, qp, kp, vp, rs, dp, ors, lse, D, T, H, kv_group, causal, scale, sl,
+               cu_dev, static_cast<bf16_t*>(dk), static_cast<bf16_t*>(dv), grs);
+    if (e != hipSuccess) return e;
+    return launch(K_ATTENTION, attn_bwd_dq_kernel<64>, dim3((max_len + 127) / 128, H, B),
+                  dim3(256), 0, s, qp, kp, vp, rs, dp, ors, lse, D, T, kv_group, causal, scale, sl,
+                  cu_dev, static_cast<bf16_t*>(dq), grs);
+  }
+  e = launch(K_ATTENTION, attn_bwd_dkdv_kernel<128, 1>, dim3((max_len + 31) / 32, Hkv, B),
+             dim3(256), 0, s, qp, kp, vp, rs, dp, ors, lse, D, T, H, kv_group, causal, scale, sl,
+             cu_dev, static_cast<bf16_t*>(dk), static_cast<bf16_t*>(dv), grs);
+  if (e != hipSuccess) return e;
+  return launch(K_ATTENTION, attn_bwd_dq_kernel<128>, dim3((max_len + 127) / 128, H, B),
+                dim3(256), 0, s, qp, kp, vp, rs, dp, ors, lse, D, T, kv_group, causal, scale, sl,
+                cu_dev, static_cast<bf16_t*>(dq), grs);
+}
+
+}  // namespace zsa

@@ -52,19 +52,6 @@ __device__ __forceinline__ void store8<float>(float* p, const float* v) {
   reinterpret_cast<uint4*>(p)[1] = pack16(v + 4, 0.f);
 }
 
-// angle reduction for the rotary epilogue: the angle pos * inv_freq is
-// formed in double and reduced to [-pi, pi] with a two-constant
-// (Cody-Waite) subtraction of multiples of 2*pi before the fp32 sincos.
-__device__ __forceinline__ void rope_sincos(int p, double inv_freq, float* s, float* c) {
-  const double two_pi_hi = 6.283185307179586;       // nearest double to 2*pi
-  const double two_pi_lo = 2.4492935982947064e-16;  // 2*pi - two_pi_hi
-  const double a = static_cast<double>(p) * inv_freq;
-  const double q = rint(a * 0.15915494309189535);   // a / (2*pi)
-  double r = fma(-q, two_pi_hi, a);
-  r = fma(-q, two_pi_lo, r);
-  sincosf(static_cast<float>(r), s, c);
-}
-
 // erf by Abramowitz & Stegun, Handbook of Mathematical Functions, 7.1.26:
 // erf(x) = 1 - (a1 t + a2 t^2 + a3 t^3 + a4 t^4 + a5 t^5) exp(-x^2),
 // t = 1 / (1 + p x), x >= 0, |error| <= 1.5e-7; odd extension for x < 0.
@@ -156,7 +143,7 @@ __device__ void epilogue_tile(const float* tile, int ldt, int m0, int n0, int M,
         const float zp = tile[r * ldt + pcol + e] + pb[e];
         const int i = (c0 + e) - (lower ? 0 : half);
         float sn, cs;
-        rope_sincos(p, ep.inv_freq[i], &sn, &cs);
+        rope_angle(p, ep.inv_freq[i], &sn, &cs);
         z[e] = lower ? (z[e] * cs - zp * sn) : (z[e] * cs + zp * sn);
       }
     }
@@ -771,6 +758,16 @@ size_t gemm_workspace_bound(int dtype, int max_rows, int N, int K) {
     b = std::max(b, gemm_workspace_bytes(dtype, m, N, K));
   }
   return b;
+}
+
+// out[M][N] = x W^T in fp32 (no epilogue): the weight gradients of the
+// backward pass; bf16 operands with K a multiple of 64
+hipError_t launch_gemm_f32(hipStream_t s, const void* x, int M, int K, const void* w, int N,
+                           float* out) {
+  if (M == 0 || N == 0) return hipSuccess;
+  if (K % kBK != 0) return hipErrorInvalidValue;
+  EpiParams ep{};
+  return launch_dma<128, 128, 2, 2, 64, 2, 128>(s, x, M, K, w, N, ep, 1, K, out);
 }
 
 hipError_t launch_gemm(hipStream_t s, int dtype, const void* x, int M, int K, const void* w,

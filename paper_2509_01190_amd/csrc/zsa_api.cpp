@@ -829,6 +829,340 @@ int zsa_stack_forward(void* stream, const zsa_layer_cfg* cfg, const zsa_layer_we
 }
 
 // ---------------------------------------------------------------------------
+// backward through the pruned stack
+// ---------------------------------------------------------------------------
+namespace {
+
+int64_t round64(int64_t v) { return (v + 63) / 64 * 64; }
+
+// buffers of one layer's backward, for up to T rows
+struct BwdLayout {
+  size_t h1, x1, h2, u, dF, du, dh2, dx1, dog, dofull, dxr, dqkv, dh1, D, stats, inv, wT, aT, bT,
+      col, splitk, splitk_bytes, end;
+};
+
+BwdLayout bwd_layout(const zsa_layer_cfg* c, int64_t T, Carver& cv) {
+  const size_t e = esize(c->dtype);
+  const int64_t d = c->d_model, F = c->d_ff, qw = qkv_width(*c);
+  const int64_t up_n = c->kind == ZSA_DECODER ? 2 * F : F;
+  const int64_t maxc = std::max({d, qw, up_n, F});
+  BwdLayout B;
+  B.h1 = cv.take(T * d * e);
+  B.x1 = cv.take(T * d * e);
+  B.h2 = cv.take(T * d * e);
+  B.u = cv.take(T * up_n * e);
+  B.dF = cv.take(T * F * e);
+  B.du = cv.take(T * up_n * e);
+  B.dh2 = cv.take(T * d * e);
+  B.dx1 = cv.take(T * d * e);
+  B.dog = cv.take(T * d * e);
+  B.dofull = cv.take(T * d * e);
+  B.dxr = cv.take(T * d * e);
+  B.dqkv = cv.take(T * qw * e);
+  B.dh1 = cv.take(T * d * e);
+  B.D = cv.take(static_cast<size_t>(c->n_heads) * T * 4);
+  B.stats = cv.take(static_cast<size_t>(T) * 2 * 4);
+  B.inv = cv.take(static_cast<size_t>(T) * 4);
+  B.wT = cv.take(static_cast<size_t>(d) * maxc * e);
+  B.aT = cv.take(static_cast<size_t>(round64(T)) * maxc * e);
+  B.bT = cv.take(static_cast<size_t>(round64(T)) * maxc * e);
+  B.col = cv.take(zsa::colsum_scratch_floats(static_cast<int>(T), static_cast<int>(maxc)) * 4);
+  // split-K room for the backward's input-gradient products at any row count
+  const int dt = c->dtype, rows = static_cast<int>(T);
+  B.splitk_bytes = std::max({zsa::gemm_workspace_bound(dt, rows, static_cast<int>(F), static_cast<int>(d)),
+                             zsa::gemm_workspace_bound(dt, rows, static_cast<int>(d), static_cast<int>(up_n)),
+                             zsa::gemm_workspace_bound(dt, rows, static_cast<int>(d), static_cast<int>(d)),
+                             zsa::gemm_workspace_bound(dt, rows, static_cast<int>(d), static_cast<int>(qw))});
+  B.splitk = cv.take(B.splitk_bytes);
+  B.end = cv.off;
+  return B;
+}
+
+// one block's backward: recompute its forward, then dL/dx and dL/dW
+int layer_backward(hipStream_t s, const zsa_layer_cfg& c, const zsa_layer_weights& w,
+                   const zsa_layer_grads& gr, const void* x_in, const int32_t* pos_in,
+                   const RowSet& in, bool prune, const RowSet& out, const int32_t* kept,
+                   const void* dy, void* dx, const LayerBufs& wb, char* base, const BwdLayout& B) {
+  using namespace zsa;
+  const int dt = c.dtype;
+  const size_t e = esize(dt);
+  const int d = c.d_model, H = c.n_heads, hd = c.head_dim, F = c.d_ff;
+  const int kvd = kv_heads(c) * hd, qw = static_cast<int>(qkv_width(c)), kvg = H / kv_heads(c);
+  const bool dec = c.kind == ZSA_DECODER;
+  const int norm_kind = dec ? ZSA_NORM_RMS : ZSA_NORM_LAYER;
+  const int up_n = dec ? 2 * F : F;
+  const float scale = 1.0f / sqrtf(static_cast<float>(hd));
+  const int T = in.T, To = prune ? out.T : in.T;
+  const int Tp = static_cast<int>(round64(T)), Top = static_cast<int>(round64(To));
+  auto P = [&](size_t off) { return static_cast<void*>(base + off); };
+  float* stats = reinterpret_cast<float*>(base + B.stats);
+  float* col = reinterpret_cast<float*>(base + B.col);
+  void* sk = B.splitk_bytes ? P(B.splitk) : nullptr;
+  auto gemm = [&](const void* x, int M, int K, const void* wt, int N, void* y) {
+    EpiParams ep{};
+    ep.epi = EPI_NONE;
+    ep.y = y;
+    ep.ldy = N;
+    return launch_gemm(s, dt, x, M, K, wt, N, ep, sk, B.splitk_bytes);
+  };
+  // dW = a^T b over `rows` rows: a [rows, na], b [rows, nb] -> out [na, nb]
+  auto wgrad = [&](const void* a, int na, const void* b, int nb, int rows, int rows_p,
+                   float* out) -> hipError_t {
+    hipError_t er = launch_transpose(s, dt, a, rows, na, na, P(B.aT), rows_p);
+    if (er != hipSuccess) return er;
+    er = launch_transpose(s, dt, b, rows, nb, nb, P(B.bT), rows_p);
+    if (er != hipSuccess) return er;
+    return launch_gemm_f32(s, P(B.aT), na, rows_p, P(B.bT), nb, out);
+  };
+  // y = x W for W [n_out_w, n_in_w] stored as a Linear weight: x [rows, n_out_w]
+  auto xgrad = [&](const void* x, int rows, const void* W, int wn, int wk, void* y) -> hipError_t {
+    hipError_t er = launch_transpose(s, dt, W, wn, wk, wk, P(B.wT), wn);  // W^T [wk, wn]
+    if (er != hipSuccess) return er;
+    return gemm(x, rows, wn, P(B.wT), wk, y);
+  };
+  auto colsum = [&](const void* a, int rows, int cols, const void* x, float* outp) -> hipError_t {
+    if (outp == nullptr) return hipSuccess;
+    return launch_colsum(s, dt, a, cols, x, cols, x != nullptr ? stats : nullptr, rows, cols, col,
+                         outp);
+  };
+
+  // ---- the layer's forward again (deterministic: the same values)
+  HIP_TRY(launch_norm(s, dt, norm_kind, x_in, w.norm1_w, dec ? nullptr : w.norm1_b, T, d,
+                      c.norm_eps, P(B.h1)),
+          "norm1");
+  EpiParams rope{};
+  if (dec) fill_rope(rope, hd, c.rope_theta);
+  {
+    EpiParams ep = rope;
+    ep.epi = dec ? EPI_ROPE : EPI_NONE;
+    ep.bias = w.b_qkv;
+    ep.y = wb.qkv;
+    ep.ldy = qw;
+    ep.pos = pos_in;
+    ep.head_dim = hd;
+    ep.rope_cols = dec ? d + kvd : 0;
+    HIP_TRY(launch_gemm(s, dt, P(B.h1), T, d, w.w_qkv, qw, ep, wb.splitk, wb.splitk_bytes),
+            "qkv projection");
+  }
+  const char* qkv = static_cast<const char*>(wb.qkv);
+  const void* q = qkv;
+  const void* k = qkv + d * e;
+  const void* v = qkv + (d + kvd) * e;
+  HIP_TRY(launch_attention(s, dt, q, k, v, qw, H, kvg, hd, c.causal, scale, in.B, in.max_len, T,
+                           in.cu_dev, wb.o, d, wb.lse),
+          "attention");
+  const void* xr = x_in;
+  const void* og = wb.o;
+  if (prune) {
+    HIP_TRY(launch_gather(s, dt, d, T, kept, To, x_in, wb.xg, wb.o, wb.og, nullptr, nullptr),
+            "gather");
+    xr = wb.xg;
+    og = wb.og;
+  }
+  {
+    EpiParams ep{};
+    ep.epi = EPI_RESIDUAL;
+    ep.bias = w.b_o;
+    ep.residual = xr;
+    ep.y = P(B.x1);
+    ep.ldy = d;
+    HIP_TRY(launch_gemm(s, dt, og, To, d, w.w_o, d, ep, wb.splitk, wb.splitk_bytes),
+            "output projection");
+  }
+  HIP_TRY(launch_norm(s, dt, norm_kind, P(B.x1), w.norm2_w, dec ? nullptr : w.norm2_b, To, d,
+                      c.norm_eps, P(B.h2)),
+          "norm2");
+  {
+    EpiParams ep{};
+    ep.epi = EPI_NONE;
+    ep.bias = w.b_up;
+    ep.y = P(B.u);
+    ep.ldy = up_n;
+    HIP_TRY(launch_gemm(s, dt, P(B.h2), To, d, w.w_up, up_n, ep, wb.splitk, wb.splitk_bytes),
+            "up projection");
+  }
+  HIP_TRY(launch_act_fwd(s, dt, P(B.u), wb.f, To, F, dec), "activation");
+
+  // ---- backward: MLP
+  HIP_TRY(wgrad(dy, d, wb.f, F, To, Top, gr.w_down), "down weight gradient");
+  HIP_TRY(colsum(dy, To, d, nullptr, gr.b_down), "down bias gradient");
+  HIP_TRY(xgrad(dy, To, w.w_down, d, F, P(B.dF)), "down input gradient");
+  HIP_TRY(launch_act_bwd(s, dt, P(B.dF), P(B.u), P(B.du), To, F, dec), "activation gradient");
+  HIP_TRY(wgrad(P(B.du), up_n, P(B.h2), d, To, Top, gr.w_up), "up weight gradient");
+  HIP_TRY(colsum(P(B.du), To, up_n, nullptr, gr.b_up), "up bias gradient");
+  HIP_TRY(xgrad(P(B.du), To, w.w_up, up_n, d, P(B.dh2)), "up input gradient");
+  HIP_TRY(launch_norm_bwd(s, dt, norm_kind, P(B.x1), w.norm2_w, P(B.dh2), dy, P(B.dx1), To, d,
+                          c.norm_eps, stats),
+          "norm2 gradient");
+  HIP_TRY(colsum(P(B.dh2), To, d, P(B.x1), gr.norm2_w), "norm2 gain gradient");
+  if (!dec) HIP_TRY(colsum(P(B.dh2), To, d, nullptr, gr.norm2_b), "norm2 shift gradient");
+  // ---- output projection
+  HIP_TRY(wgrad(P(B.dx1), d, og, d, To, Top, gr.w_o), "output weight gradient");
+  HIP_TRY(colsum(P(B.dx1), To, d, nullptr, gr.b_o), "output bias gradient");
+  HIP_TRY(xgrad(P(B.dx1), To, w.w_o, d, d, P(B.dog)), "output input gradient");
+  // ---- undo compaction: dropped rows get no gradient from the rows after them
+  const void* dof = P(B.dog);
+  const void* dxr = P(B.dx1);
+  if (prune) {
+    int32_t* inv = reinterpret_cast<int32_t*>(base + B.inv);
+    HIP_TRY(launch_scatter_rows(s, dt, d, P(B.dog), kept, To, T, inv, P(B.dofull)), "scatter");
+    HIP_TRY(launch_scatter_rows(s, dt, d, P(B.dx1), kept, To, T, inv, P(B.dxr)), "scatter");
+    dof = P(B.dofull);
+    dxr = P(B.dxr);
+  }
+  // ---- attention
+  float* Dv = reinterpret_cast<float*>(base + B.D);
+  HIP_TRY(launch_rowdot(s, dt, dof, wb.o, d, T, H, hd, Dv), "rowdot");
+  char* dqkv = base + B.dqkv;
+  HIP_TRY(launch_attention_bwd(s, q, k, v, qw, dof, d, wb.lse, Dv, H, kvg, hd, c.causal, scale,
+                               in.B, in.max_len, T, in.cu_dev, dqkv, dqkv + d * e,
+                               dqkv + (d + kvd) * e, qw),
+          "attention gradient");
+  if (dec) HIP_TRY(launch_rope_bwd(s, dt, dqkv, qw, T, d + kvd, hd, pos_in, rope), "rope gradient");
+  // ---- qkv projection and norm1
+  HIP_TRY(wgrad(dqkv, qw, P(B.h1), d, T, Tp, gr.w_qkv), "qkv weight gradient");
+  HIP_TRY(colsum(dqkv, T, qw, nullptr, gr.b_qkv), "qkv bias gradient");
+  HIP_TRY(xgrad(dqkv, T, w.w_qkv, qw, d, P(B.dh1)), "qkv input gradient");
+  HIP_TRY(launch_norm_bwd(s, dt, norm_kind, x_in, w.norm1_w, P(B.dh1), dxr, dx, T, d, c.norm_eps,
+                          stats),
+          "norm1 gradient");
+  HIP_TRY(colsum(P(B.dh1), T, d, x_in, gr.norm1_w), "norm1 gain gradient");
+  if (!dec) HIP_TRY(colsum(P(B.dh1), T, d, nullptr, gr.norm1_b), "norm1 shift gradient");
+  return ZSA_OK;
+}
+
+}  // namespace
+
+size_t zsa_stack_backward_workspace_size(const zsa_layer_cfg* cfg, int32_t total_rows,
+                                         int32_t batch, int32_t n_layers, int32_t n_prune) {
+  if (cfg == nullptr || total_rows < 0 || batch < 0 || n_layers < 1 || n_prune < 0) return 0;
+  const size_t T = static_cast<size_t>(total_rows);
+  Carver cv;
+  layer_layout(cfg, total_rows, cv);
+  bwd_layout(cfg, total_rows, cv);
+  cv.take(static_cast<size_t>(n_layers) * T * cfg->d_model * esize(cfg->dtype));  // layer inputs
+  cv.take(static_cast<size_t>(n_layers) * T * 4);                                // positions
+  cv.take(static_cast<size_t>(n_prune) * T * 4);                                 // kept rows
+  cv.take(static_cast<size_t>(n_prune) * (batch + 1) * 4);                       // offsets
+  cv.take(2 * T * cfg->d_model * esize(cfg->dtype));                             // gradients
+  return cv.off;
+}
+
+int zsa_stack_backward(void* stream, const zsa_layer_cfg* cfg, const zsa_layer_weights* w,
+                       const zsa_layer_grads* grads, int32_t n_layers, const int32_t* prune_after,
+                       int32_t n_prune, const double* keep_rate, const void* hidden_in,
+                       const int32_t* pos_in, int32_t batch, const int32_t* cu_host,
+                       const int32_t* cu_dev, const void* dy, void* dx, void* ws,
+                       size_t ws_bytes) {
+  CHECK(check_cfg(cfg));
+  if (!zsa::backward_supported(cfg->dtype, cfg->head_dim))
+    return fail(ZSA_EUNSUPPORTED, "backward: bf16 with head_dim 64 or 128");
+  if (cfg->mark_only) return fail(ZSA_EUNSUPPORTED, "backward of the mark-only mode");
+  if (n_layers < 1 || w == nullptr || grads == nullptr)
+    return fail(ZSA_EINVAL, "n_layers %d / weights / grads", n_layers);
+  for (int l = 0; l < n_layers; ++l) {
+    const zsa_layer_grads& g = grads[l];
+    if (g.w_qkv == nullptr || g.w_o == nullptr || g.w_up == nullptr || g.w_down == nullptr ||
+        g.norm1_w == nullptr || g.norm2_w == nullptr)
+      return fail(ZSA_EINVAL, "layer %d: a weight gradient pointer is NULL", l + 1);
+  }
+  if (n_prune < 0 || (n_prune > 0 && prune_after == nullptr)) return fail(ZSA_EINVAL, "prune_after");
+  for (int p = 0; p < n_prune; ++p) {
+    if (prune_after[p] < 1 || prune_after[p] > n_layers || (p > 0 && prune_after[p] <= prune_after[p - 1]))
+      return fail(ZSA_EINVAL, "prune_after must be strictly ascending in 1..%d", n_layers);
+  }
+  int32_t T0, max_len0;
+  CHECK(check_seqs(batch, cu_host, cu_dev, &T0, &max_len0));
+  if (n_prune > 0 && batch > 0 && keep_rate == nullptr) return fail(ZSA_EINVAL, "keep_rate is NULL");
+  for (int b = 0; n_prune > 0 && b < batch; ++b) CHECK(check_rate(keep_rate[b]));
+  if (T0 > 0) {
+    CHECK(check_ptr16(hidden_in, "hidden_in"));
+    CHECK(check_ptr16(dy, "dy"));
+    CHECK(check_ptr16(dx, "dx"));
+    if (pos_in == nullptr) return fail(ZSA_EINVAL, "pos_in is NULL");
+  }
+  const size_t need = zsa_stack_backward_workspace_size(cfg, T0, batch, n_layers, n_prune);
+  if (ws == nullptr || ws_bytes < need) return fail(ZSA_EWORKSPACE, "workspace %zu < %zu", ws_bytes, need);
+  if (T0 == 0) return ZSA_OK;
+
+  // the schedule, as in the forward
+  std::vector<std::vector<int32_t>> cus(n_prune + 1, std::vector<int32_t>(batch + 1, 0));
+  std::vector<int32_t> maxl(n_prune + 1, 0);
+  for (int b = 0; b <= batch; ++b) cus[0][b] = cu_host[b];
+  maxl[0] = max_len0;
+  for (int p = 1; p <= n_prune; ++p)
+    for (int b = 0; b < batch; ++b) {
+      const int32_t n = cus[p - 1][b + 1] - cus[p - 1][b];
+      const int32_t kb = keep_count_impl(n, keep_rate[b], cfg->tau);
+      cus[p][b + 1] = cus[p][b] + kb;
+      maxl[p] = std::max(maxl[p], kb);
+    }
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  char* base = static_cast<char*>(ws);
+  Carver cv;
+  const LayerBufs wb = carve_layer(layer_layout(cfg, T0, cv), ws);
+  const BwdLayout B = bwd_layout(cfg, T0, cv);
+  const size_t e = esize(cfg->dtype);
+  const size_t xrow = static_cast<size_t>(cfg->d_model) * e;
+  char* xs = base + cv.take(static_cast<size_t>(n_layers) * T0 * xrow);
+  int32_t* ps = reinterpret_cast<int32_t*>(base + cv.take(static_cast<size_t>(n_layers) * T0 * 4));
+  int32_t* kept = reinterpret_cast<int32_t*>(base + cv.take(static_cast<size_t>(n_prune) * T0 * 4));
+  int32_t* meta = reinterpret_cast<int32_t*>(base + cv.take(static_cast<size_t>(n_prune) * (batch + 1) * 4));
+  char* gbuf = base + cv.take(2 * static_cast<size_t>(T0) * xrow);
+  std::vector<int32_t> flat;
+  for (int p = 1; p <= n_prune; ++p) flat.insert(flat.end(), cus[p].begin(), cus[p].end());
+  if (!flat.empty()) HIP_TRY(zsa::launch_upload_i32(s, meta, flat.data(), static_cast<int>(flat.size())), "upload");
+
+  // forward, keeping every layer's input rows, positions and kept rows
+  std::vector<const void*> xin(n_layers + 1);
+  std::vector<const int32_t*> pin(n_layers + 1);
+  std::vector<RowSet> rin(n_layers + 1);
+  std::vector<int> pt_of(n_layers + 1, -1);
+  xin[1] = hidden_in;
+  pin[1] = pos_in;
+  rin[1] = RowSet{batch, cus[0].data(), cu_dev, T0, max_len0};
+  int point = 0;
+  for (int l = 1; l <= n_layers; ++l) {
+    const bool prune = point < n_prune && prune_after[point] == l;
+    RowSet nxt = rin[l];
+    if (prune) {
+      nxt = RowSet{batch, cus[point + 1].data(), meta + static_cast<size_t>(point) * (batch + 1),
+                   cus[point + 1][batch], maxl[point + 1]};
+      pt_of[l] = point;
+    }
+    if (l < n_layers) {
+      void* x_out = xs + static_cast<size_t>(l) * T0 * xrow;
+      int32_t* p_out = prune ? ps + static_cast<size_t>(l) * T0 : nullptr;
+      CHECK(run_layer(s, *cfg, w[l - 1], xin[l], pin[l], rin[l], prune, nxt, x_out, p_out,
+                      nullptr, prune ? kept + static_cast<size_t>(point) * T0 : nullptr, wb));
+      xin[l + 1] = x_out;
+      pin[l + 1] = prune ? p_out : pin[l];
+      rin[l + 1] = nxt;
+    } else if (prune) {
+      // the last layer's kept rows, for its backward
+      CHECK(run_layer(s, *cfg, w[l - 1], xin[l], pin[l], rin[l], true, nxt, gbuf, ps, nullptr,
+                      kept + static_cast<size_t>(point) * T0, wb));
+    }
+    if (prune) ++point;
+  }
+  // backward, last layer first
+  const void* g_in = dy;
+  for (int l = n_layers; l >= 1; --l) {
+    const bool prune = pt_of[l] >= 0;
+    const RowSet out = prune ? RowSet{batch, cus[pt_of[l] + 1].data(),
+                                      meta + static_cast<size_t>(pt_of[l]) * (batch + 1),
+                                      cus[pt_of[l] + 1][batch], maxl[pt_of[l] + 1]}
+                             : rin[l];
+    void* g_out = l == 1 ? dx : gbuf + static_cast<size_t>(l & 1) * T0 * xrow;
+    CHECK(layer_backward(s, *cfg, w[l - 1], grads[l - 1], xin[l], pin[l], rin[l], prune, out,
+                         prune ? kept + static_cast<size_t>(pt_of[l]) * T0 : nullptr, g_in, g_out,
+                         wb, base, B));
+    g_in = g_out;
+  }
+  return ZSA_OK;
+}
+
+// ---------------------------------------------------------------------------
 // generation after a pruned prefill
 // ---------------------------------------------------------------------------
 struct DecodeLayout {

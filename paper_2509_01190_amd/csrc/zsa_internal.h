@@ -109,6 +109,19 @@ enum Epi { EPI_NONE = 0, EPI_GELU = 1, EPI_SWIGLU = 2, EPI_RESIDUAL = 3, EPI_ROP
 
 constexpr int kMaxHalfHead = 64;  // head_dim <= 128 for the rotary epilogue
 
+// sine and cosine of the rotary angle pos * inv_freq: the angle is formed in
+// double and reduced to [-pi, pi] with a two-constant (Cody-Waite)
+// subtraction of multiples of 2*pi before the fp32 sincos
+__device__ __forceinline__ void rope_angle(int p, double inv_freq, float* s, float* c) {
+  const double two_pi_hi = 6.283185307179586;       // nearest double to 2*pi
+  const double two_pi_lo = 2.4492935982947064e-16;  // 2*pi - two_pi_hi
+  const double a = static_cast<double>(p) * inv_freq;
+  const double q = rint(a * 0.15915494309189535);   // a / (2*pi)
+  double r = fma(-q, two_pi_hi, a);
+  r = fma(-q, two_pi_lo, r);
+  sincosf(static_cast<float>(r), s, c);
+}
+
 struct EpiParams {
   int epi;
   const void* bias;      // [N] or null
@@ -172,6 +185,36 @@ hipError_t launch_decode_attention(hipStream_t s, const void* q, int64_t q_strid
                                    int64_t out_stride);
 int decode_splits(int max_len);
 bool decode_supported(int dtype, int hd, int group);
+
+// backward pass (bf16, head_dim 64 / 128 for the attention part)
+bool backward_supported(int dtype, int hd);
+hipError_t launch_gemm_f32(hipStream_t s, const void* x, int M, int K, const void* w, int N,
+                           float* out);
+hipError_t launch_transpose(hipStream_t s, int dtype, const void* in, int R, int C, int64_t ldi,
+                            void* out, int Rpad);
+size_t colsum_scratch_floats(int R, int C);
+hipError_t launch_colsum(hipStream_t s, int dtype, const void* a, int64_t lda, const void* x,
+                         int64_t ldx, const float* stats, int R, int C, float* scratch,
+                         float* out);
+hipError_t launch_norm_bwd(hipStream_t s, int dtype, int kind, const void* x, const void* g,
+                           const void* dh, const void* res, void* out, int R, int d, float eps,
+                           float* stats);
+hipError_t launch_act_fwd(hipStream_t s, int dtype, const void* u, void* f, int rows, int F,
+                          int swiglu);
+hipError_t launch_act_bwd(hipStream_t s, int dtype, const void* dF, const void* u, void* du,
+                          int rows, int F, int swiglu);
+hipError_t launch_scatter_rows(hipStream_t s, int dtype, int d, const void* src,
+                               const int32_t* kept, int t_out, int t_in, int32_t* inv,
+                               void* dst);
+hipError_t launch_rowdot(hipStream_t s, int dtype, const void* dO, const void* O, int64_t ld,
+                         int T, int H, int hd, float* D);
+hipError_t launch_rope_bwd(hipStream_t s, int dtype, void* g, int64_t ld, int rows, int cols,
+                           int hd, const int32_t* pos, const EpiParams& ep);
+hipError_t launch_attention_bwd(hipStream_t s, const void* q, const void* k, const void* v,
+                                int64_t rs, const void* dO, int64_t ors, const float* lse,
+                                const float* D, int H, int kv_group, int hd, int causal,
+                                float scale, int B, int max_len, int T, const int32_t* cu_dev,
+                                void* dq, void* dk, void* dv, int64_t grs);
 
 // row gather of up to two [*, d] arrays plus pos
 hipError_t launch_gather(hipStream_t s, int dtype, int d, int t_in, const int32_t* kept,

@@ -57,6 +57,10 @@ class LayerWeights(ctypes.Structure):
     _fields_ = [(n, _vp) for n in WEIGHT_NAMES]
 
 
+class LayerGrads(ctypes.Structure):
+    _fields_ = [(n, _vp) for n in WEIGHT_NAMES]
+
+
 _SIGS = {
     "zsa_last_error": (ctypes.c_char_p, []),
     "zsa_version": (ctypes.c_char_p, []),
@@ -87,6 +91,11 @@ _SIGS = {
     "zsa_decode_step": (ctypes.c_int, [_vp, ctypes.POINTER(LayerCfg), ctypes.POINTER(LayerWeights),
                                        _i32, _i32, _vp, _pi32, _vp, _i32, _pi32, _vp, _vp, _sz]),
     "zsa_decode_workspace_size": (_sz, [ctypes.POINTER(LayerCfg), _i32, _i32]),
+    "zsa_stack_backward": (ctypes.c_int, [_vp, ctypes.POINTER(LayerCfg),
+                                          ctypes.POINTER(LayerWeights), ctypes.POINTER(LayerGrads),
+                                          _i32, _pi32, _i32, _pf64, _vp, _vp, _i32, _pi32, _vp,
+                                          _vp, _vp, _vp, _sz]),
+    "zsa_stack_backward_workspace_size": (_sz, [ctypes.POINTER(LayerCfg), _i32, _i32, _i32, _i32]),
     "zsa_stack_workspace_size": (_sz, [ctypes.POINTER(LayerCfg), _i32, _i32, _i32]),
     "zsa_timing_arm": (ctypes.c_int, [_i32, _i32]),
     "zsa_timing_read": (ctypes.c_int, [_i32, _pi32, ctypes.POINTER(ctypes.c_double)]),
@@ -445,6 +454,34 @@ class Stack:
                 cur = np.asarray(counts[point], dtype=np.int32)
                 point += 1
         return out
+
+    def backward(self, hidden: torch.Tensor, pos: torch.Tensor, seqs: Seqs,
+                 prune_after: Sequence[int], keep_rate, dy: torch.Tensor):
+        """Gradients of sum(forward(...)["x"] * dy): returns (dx, grads) with
+        grads[l][name] fp32 tensors shaped like the weights (None where the
+        weight is absent). The kept rows are constants."""
+        _require_cuda(hidden, pos, dy)
+        dev = hidden.device
+        pa = _host_i32(prune_after)
+        kr = _host_f64(keep_rate)
+        shapes = weight_shapes(self.cfg)
+        grads = []
+        for w in self.weights:
+            grads.append({n: (None if w.get(n) is None else
+                              torch.empty(shapes[n], dtype=torch.float32, device=dev))
+                          for n in WEIGHT_NAMES})
+        gstructs = (LayerGrads * len(grads))(
+            *[LayerGrads(*[None if g[n] is None else g[n].data_ptr() for n in WEIGHT_NAMES])
+              for g in grads])
+        dx = torch.empty_like(hidden)
+        wsz = int(lib().zsa_stack_backward_workspace_size(ctypes.byref(self.cfg), seqs.total,
+                                                          seqs.batch, self.n_layers, len(pa)))
+        ws = torch.empty(max(wsz, 1), dtype=torch.uint8, device=dev)
+        _check(lib().zsa_stack_backward(
+            _stream(dev), ctypes.byref(self.cfg), self._wstructs, gstructs, self.n_layers,
+            _hp32(pa), len(pa), _hpf64(kr), _p(hidden), _p(pos), seqs.batch, _hp32(seqs.host),
+            _p(seqs.dev), _p(dy), _p(dx), _p(ws), wsz))
+        return dx, grads
 
     def decode_step(self, x_new: torch.Tensor, pos_new, kv_cache: torch.Tensor,
                     kv_len: np.ndarray, out: Optional[torch.Tensor] = None) -> torch.Tensor:
