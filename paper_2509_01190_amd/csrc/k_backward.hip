@@ -32,6 +32,29 @@ typedef __bf16 bf16x8_t __attribute__((ext_vector_type(8)));
 typedef float f32x16_t __attribute__((ext_vector_type(16)));
 constexpr float kLog2e = 1.4426950408889634f;
 
+template <typename T>
+__device__ __forceinline__ void load8(const T* p, float* v);
+template <>
+__device__ __forceinline__ void load8<bf16_t>(const bf16_t* p, float* v) {
+  unpack16(*reinterpret_cast<const uint4*>(p), v, bf16_t());
+}
+template <>
+__device__ __forceinline__ void load8<float>(const float* p, float* v) {
+  unpack16(reinterpret_cast<const uint4*>(p)[0], v, 0.f);
+  unpack16(reinterpret_cast<const uint4*>(p)[1], v + 4, 0.f);
+}
+template <typename T>
+__device__ __forceinline__ void store8(T* p, const float* v);
+template <>
+__device__ __forceinline__ void store8<bf16_t>(bf16_t* p, const float* v) {
+  *reinterpret_cast<uint4*>(p) = pack16(v, bf16_t());
+}
+template <>
+__device__ __forceinline__ void store8<float>(float* p, const float* v) {
+  reinterpret_cast<uint4*>(p)[0] = pack16(v, 0.f);
+  reinterpret_cast<uint4*>(p)[1] = pack16(v + 4, 0.f);
+}
+
 // ---------------------------------------------------------------------------
 // transpose: out[c][r] = in[r][c] for r < R, 0 for R <= r < Rpad
 // ---------------------------------------------------------------------------
@@ -53,39 +76,102 @@ __global__ __launch_bounds__(256) void transpose_kernel(const T* __restrict__ in
   }
 }
 
+// bf16, 64 x 64 tiles with 16-byte loads and stores (C, R multiples of 8 for
+// the vector paths; edges fall back to element accesses)
+__global__ __launch_bounds__(256) void transpose64_kernel(const bf16_t* __restrict__ in, int R,
+                                                          int C, int64_t ldi,
+                                                          bf16_t* __restrict__ out, int Rpad) {
+  __shared__ bf16_t tile[64][64 + 2];
+  const int r0 = blockIdx.y * 64, c0 = blockIdx.x * 64;
+  const int t = threadIdx.x;
+  for (int k = t; k < 64 * 8; k += 256) {
+    const int r = k / 8, ch = (k % 8) * 8;
+    const int gr = r0 + r, gc = c0 + ch;
+    if (gr < R && gc + 8 <= C) {
+      const uint4 v = *reinterpret_cast<const uint4*>(in + static_cast<int64_t>(gr) * ldi + gc);
+      const bf16_t* e = reinterpret_cast<const bf16_t*>(&v);
+#pragma unroll
+      for (int j = 0; j < 8; ++j) tile[r][ch + j] = e[j];
+    } else {
+#pragma unroll
+      for (int j = 0; j < 8; ++j)
+        tile[r][ch + j] = (gr < R && gc + j < C) ? in[static_cast<int64_t>(gr) * ldi + gc + j]
+                                                 : bf16_t(0.f);
+    }
+  }
+  __syncthreads();
+  for (int k = t; k < 64 * 8; k += 256) {
+    const int c = k / 8, rh = (k % 8) * 8;   // output row c0 + c, columns r0 + rh ..
+    const int gc = c0 + c, gr = r0 + rh;
+    if (gc >= C) continue;
+    if (gr + 8 <= Rpad) {
+      uint4 v;
+      bf16_t* e = reinterpret_cast<bf16_t*>(&v);
+#pragma unroll
+      for (int j = 0; j < 8; ++j) e[j] = tile[rh + j][c];
+      *reinterpret_cast<uint4*>(out + static_cast<int64_t>(gc) * Rpad + gr) = v;
+    } else {
+      for (int j = 0; j < 8 && gr + j < Rpad; ++j)
+        out[static_cast<int64_t>(gc) * Rpad + gr + j] = tile[rh + j][c];
+    }
+  }
+}
+
 // ---------------------------------------------------------------------------
-// column sums in a fixed order: stage 1 sums row chunks, stage 2 the chunks
+// column sums in a fixed order: stage 1 sums chunks of kColRows rows (each
+// thread 8 consecutive columns with 16-byte loads, 8 row lanes per block
+// added in lane order), stage 2 adds the chunks in chunk order
 // ---------------------------------------------------------------------------
-constexpr int kColRows = 256;  // rows per stage-1 chunk
+constexpr int kColRows = 64;   // rows per stage-1 chunk
+constexpr int kColLanes = 8;   // row lanes per block
 
 // sum over rows of a[r][c] (or of a[r][c] * xhat[r][c] when x is given, with
-// xhat = (x - mean_r) * rstd_r from stats [R][2])
+// xhat = (x - mean_r) * rstd_r from stats [R][2]); C a multiple of 8
 template <typename T>
 __global__ __launch_bounds__(256) void colsum_stage1(const T* __restrict__ a, int64_t lda,
                                                      const T* __restrict__ x, int64_t ldx,
                                                      const float* __restrict__ stats, int R,
                                                      int C, float* __restrict__ part) {
-  const int c = blockIdx.x * 256 + threadIdx.x;
+  __shared__ float red[kColLanes][32 * 8 + 4];
+  const int cg = threadIdx.x & 31, lane_r = threadIdx.x >> 5;
+  const int c0 = (blockIdx.x * 32 + cg) * 8;
   const int r0 = blockIdx.y * kColRows;
-  if (c >= C) return;
-  float s = 0.f;
-  const int r1 = min(R, r0 + kColRows);
-  for (int r = r0; r < r1; ++r) {
-    float v = to_f32(a[static_cast<int64_t>(r) * lda + c]);
-    if (x != nullptr)
-      v *= (to_f32(x[static_cast<int64_t>(r) * ldx + c]) - stats[2 * r]) * stats[2 * r + 1];
-    s += v;
+  float s[8];
+#pragma unroll
+  for (int e = 0; e < 8; ++e) s[e] = 0.f;
+  if (c0 < C) {
+    const int r1 = min(R, r0 + kColRows);
+    for (int r = r0 + lane_r; r < r1; r += kColLanes) {
+      float v[8];
+      load8<T>(a + static_cast<int64_t>(r) * lda + c0, v);
+      if (x != nullptr) {
+        float xv[8];
+        load8<T>(x + static_cast<int64_t>(r) * ldx + c0, xv);
+        const float mu = stats[2 * r], rs = stats[2 * r + 1];
+#pragma unroll
+        for (int e = 0; e < 8; ++e) v[e] *= (xv[e] - mu) * rs;
+      }
+#pragma unroll
+      for (int e = 0; e < 8; ++e) s[e] += v[e];
+    }
   }
-  part[static_cast<int64_t>(blockIdx.y) * C + c] = s;
+#pragma unroll
+  for (int e = 0; e < 8; ++e) red[lane_r][cg * 8 + e] = s[e];
+  __syncthreads();
+  if (lane_r == 0 && c0 < C) {
+#pragma unroll
+    for (int e = 0; e < 8; ++e) {
+      float v = red[0][cg * 8 + e];
+#pragma unroll
+      for (int k = 1; k < kColLanes; ++k) v += red[k][cg * 8 + e];
+      part[static_cast<int64_t>(blockIdx.y) * C + c0 + e] = v;
+    }
+  }
 }
 
-__global__ __launch_bounds__(256) void colsum_stage2(const float* __restrict__ part, int chunks,
-                                                     int C, float* __restrict__ out) {
-  const int c = blockIdx.x * 256 + threadIdx.x;
-  if (c >= C) return;
-  float s = 0.f;
-  for (int k = 0; k < chunks; ++k) s += part[static_cast<int64_t>(k) * C + c];
-  out[c] = s;
+__global__ void zero_f32_kernel(float* __restrict__ p, int n) {
+  const int i = blockIdx.x * blockDim.x + threadIdx.x;
+  if (i < n) p[i] = 0.f;
 }
 
 // ---------------------------------------------------------------------------
@@ -152,22 +238,38 @@ template <typename T>
 __global__ __launch_bounds__(256) void act_bwd_kernel(const T* __restrict__ dF,
                                                       const T* __restrict__ u, T* __restrict__ du,
                                                       int64_t rows, int F, int swiglu) {
-  const int64_t i = static_cast<int64_t>(blockIdx.x) * 256 + threadIdx.x;
+  // 8 consecutive outputs f..f+7 of one row per thread
+  const int64_t i = (static_cast<int64_t>(blockIdx.x) * 256 + threadIdx.x) * 8;
   if (i >= rows * F) return;
   const int64_t r = i / F;
   const int f = static_cast<int>(i - r * F);
-  const float g = to_f32(dF[i]);
+  float g[8];
+  load8<T>(dF + i, g);
   if (swiglu) {
-    const float z = to_f32(u[r * 2 * F + 2 * f]);
-    const float up = to_f32(u[r * 2 * F + 2 * f + 1]);
-    const float s = 1.0f / (1.0f + expf(-z));
-    du[r * 2 * F + 2 * f] = from_f32<T>(g * up * s * (1.0f + z * (1.0f - s)));
-    du[r * 2 * F + 2 * f + 1] = from_f32<T>(g * z * s);
+    float u0[8], u1[8], o0[8], o1[8];
+    load8<T>(u + r * 2 * F + 2 * f, u0);       // gate, up of outputs f .. f+3
+    load8<T>(u + r * 2 * F + 2 * f + 8, u1);   // ... of f+4 .. f+7
+#pragma unroll
+    for (int e = 0; e < 4; ++e) {
+      const float z0 = u0[2 * e], up0 = u0[2 * e + 1], s0 = 1.0f / (1.0f + expf(-z0));
+      const float z1 = u1[2 * e], up1 = u1[2 * e + 1], s1 = 1.0f / (1.0f + expf(-z1));
+      o0[2 * e] = g[e] * up0 * s0 * (1.0f + z0 * (1.0f - s0));
+      o0[2 * e + 1] = g[e] * z0 * s0;
+      o1[2 * e] = g[4 + e] * up1 * s1 * (1.0f + z1 * (1.0f - s1));
+      o1[2 * e + 1] = g[4 + e] * z1 * s1;
+    }
+    store8<T>(du + r * 2 * F + 2 * f, o0);
+    store8<T>(du + r * 2 * F + 2 * f + 8, o1);
   } else {
-    const float z = to_f32(u[i]);
-    const float cdf = 0.5f * (1.0f + erff(z * 0.70710678118654752f));
-    const float pdf = 0.39894228040143268f * expf(-0.5f * z * z);
-    du[i] = from_f32<T>(g * (cdf + z * pdf));
+    float z[8], o[8];
+    load8<T>(u + i, z);
+#pragma unroll
+    for (int e = 0; e < 8; ++e) {
+      const float cdf = 0.5f * (1.0f + erff(z[e] * 0.70710678118654752f));
+      const float pdf = 0.39894228040143268f * __expf(-0.5f * z[e] * z[e]);
+      o[e] = g[e] * (cdf + z[e] * pdf);
+    }
+    store8<T>(du + i, o);
   }
 }
 
@@ -176,18 +278,27 @@ __global__ __launch_bounds__(256) void act_bwd_kernel(const T* __restrict__ dF,
 template <typename T>
 __global__ __launch_bounds__(256) void act_fwd_kernel(const T* __restrict__ u, T* __restrict__ f,
                                                       int64_t rows, int F, int swiglu) {
-  const int64_t i = static_cast<int64_t>(blockIdx.x) * 256 + threadIdx.x;
+  const int64_t i = (static_cast<int64_t>(blockIdx.x) * 256 + threadIdx.x) * 8;
   if (i >= rows * F) return;
   const int64_t r = i / F;
   const int c = static_cast<int>(i - r * F);
+  float o[8];
   if (swiglu) {
-    const float z = to_f32(u[r * 2 * F + 2 * c]);
-    const float up = to_f32(u[r * 2 * F + 2 * c + 1]);
-    f[i] = from_f32<T>(z / (1.0f + expf(-z)) * up);
+    float u0[8], u1[8];
+    load8<T>(u + r * 2 * F + 2 * c, u0);
+    load8<T>(u + r * 2 * F + 2 * c + 8, u1);
+#pragma unroll
+    for (int e = 0; e < 4; ++e) {
+      o[e] = u0[2 * e] / (1.0f + expf(-u0[2 * e])) * u0[2 * e + 1];
+      o[4 + e] = u1[2 * e] / (1.0f + expf(-u1[2 * e])) * u1[2 * e + 1];
+    }
   } else {
-    const float z = to_f32(u[i]);
-    f[i] = from_f32<T>(0.5f * z * (1.0f + erff(z * 0.70710678118654752f)));
+    float z[8];
+    load8<T>(u + i, z);
+#pragma unroll
+    for (int e = 0; e < 8; ++e) o[e] = 0.5f * z[e] * (1.0f + erff(z[e] * 0.70710678118654752f));
   }
+  store8<T>(f + i, o);
 }
 
 // ---------------------------------------------------------------------------
@@ -219,7 +330,7 @@ __global__ __launch_bounds__(256) void scatter_rows_kernel(const uint4* __restri
   dst[i] = s >= 0 ? src[static_cast<int64_t>(s) * cpr + c] : make_uint4(0u, 0u, 0u, 0u);
 }
 
-// D[h][r] = sum_c dO[r][h hd + c] O[r][h hd + c]
+// D[h][r] = sum_c dO[r][h hd + c] O[r][h hd + c] (hd a multiple of 8)
 template <typename T>
 __global__ __launch_bounds__(256) void rowdot_kernel(const T* __restrict__ dO,
                                                      const T* __restrict__ O, int64_t ld, int T_,
@@ -227,10 +338,16 @@ __global__ __launch_bounds__(256) void rowdot_kernel(const T* __restrict__ dO,
   const int64_t i = static_cast<int64_t>(blockIdx.x) * 256 + threadIdx.x;
   if (i >= static_cast<int64_t>(T_) * H) return;
   const int r = static_cast<int>(i / H), h = static_cast<int>(i % H);
+  const T* a = dO + static_cast<int64_t>(r) * ld + h * hd;
+  const T* b = O + static_cast<int64_t>(r) * ld + h * hd;
   float s = 0.f;
-  for (int c = 0; c < hd; ++c)
-    s = fmaf(to_f32(dO[static_cast<int64_t>(r) * ld + h * hd + c]),
-             to_f32(O[static_cast<int64_t>(r) * ld + h * hd + c]), s);
+  for (int c = 0; c < hd; c += 8) {
+    float va[8], vb[8];
+    load8<T>(a + c, va);
+    load8<T>(b + c, vb);
+#pragma unroll
+    for (int e = 0; e < 8; ++e) s = fmaf(va[e], vb[e], s);
+  }
   D[static_cast<int64_t>(h) * T_ + r] = s;
 }
 
@@ -598,32 +715,57 @@ bool backward_supported(int dtype, int hd) { return dtype == 1 && (hd == 64 || h
 hipError_t launch_transpose(hipStream_t s, int dtype, const void* in, int R, int C, int64_t ldi,
                             void* out, int Rpad) {
   if (C == 0 || Rpad == 0) return hipSuccess;
+  if (dtype == 1 && ldi % 8 == 0 && Rpad % 8 == 0)
+    return launch(K_MISC, transpose64_kernel, dim3((C + 63) / 64, (Rpad + 63) / 64), dim3(256), 0,
+                  s, static_cast<const bf16_t*>(in), R, C, ldi, static_cast<bf16_t*>(out), Rpad);
   return dtype == 1 ? transpose_t<bf16_t>(s, in, R, C, ldi, out, Rpad)
                     : transpose_t<float>(s, in, R, C, ldi, out, Rpad);
 }
 
 size_t colsum_scratch_floats(int R, int C) {
-  return static_cast<size_t>((R + kColRows - 1) / kColRows + 1) * C;
+  size_t f = 0;
+  for (int rows = R; rows > kColRows;) {
+    rows = (rows + kColRows - 1) / kColRows;
+    f += static_cast<size_t>(rows) * C;
+  }
+  return f + C;
 }
 
+// passes of 64x row reduction (fixed order) until one row is left; the
+// first pass reads the input (times xhat when x is given), the others the
+// fp32 partial rows of the previous pass
 hipError_t launch_colsum(hipStream_t s, int dtype, const void* a, int64_t lda, const void* x,
                          int64_t ldx, const float* stats, int R, int C, float* scratch,
                          float* out) {
   if (C == 0) return hipSuccess;
-  const int chunks = R > 0 ? (R + kColRows - 1) / kColRows : 0;
-  hipError_t e = hipSuccess;
-  if (chunks > 0) {
-    const dim3 grid((C + 255) / 256, chunks);
-    e = dtype == 1 ? launch(K_MISC, colsum_stage1<bf16_t>, grid, dim3(256), 0, s,
-                            static_cast<const bf16_t*>(a), lda, static_cast<const bf16_t*>(x),
-                            ldx, stats, R, C, scratch)
-                   : launch(K_MISC, colsum_stage1<float>, grid, dim3(256), 0, s,
-                            static_cast<const float*>(a), lda, static_cast<const float*>(x), ldx,
-                            stats, R, C, scratch);
-    if (e != hipSuccess) return e;
+  if (R == 0)
+    return launch(K_MISC, zero_f32_kernel, dim3((C + 255) / 256), dim3(256), 0, s, out, C);
+  const dim3 block(256);
+  int rows = R;
+  bool first = true;
+  const float* src = nullptr;
+  float* dst = scratch;
+  while (true) {
+    const int chunks = (rows + kColRows - 1) / kColRows;
+    float* target = chunks == 1 ? out : dst;
+    const dim3 grid((C + 255) / 256, chunks);  // 32 column groups of 8 per block
+    hipError_t e;
+    if (first && dtype == 1)
+      e = launch(K_MISC, colsum_stage1<bf16_t>, grid, block, 0, s, static_cast<const bf16_t*>(a),
+                 lda, static_cast<const bf16_t*>(x), ldx, stats, rows, C, target);
+    else if (first)
+      e = launch(K_MISC, colsum_stage1<float>, grid, block, 0, s, static_cast<const float*>(a),
+                 lda, static_cast<const float*>(x), ldx, stats, rows, C, target);
+    else
+      e = launch(K_MISC, colsum_stage1<float>, grid, block, 0, s, src, static_cast<int64_t>(C),
+                 static_cast<const float*>(nullptr), static_cast<int64_t>(0), nullptr, rows, C,
+                 target);
+    if (e != hipSuccess || chunks == 1) return e;
+    first = false;
+    src = dst;
+    dst += static_cast<size_t>(chunks) * C;
+    rows = chunks;
   }
-  return launch(K_MISC, colsum_stage2, dim3((C + 255) / 256), dim3(256), 0, s, scratch, chunks, C,
-                out);
 }
 
 hipError_t launch_norm_bwd(hipStream_t s, int dtype, int kind, const void* x, const void* g,
@@ -653,7 +795,7 @@ hipError_t launch_act_bwd(hipStream_t s, int dtype, const void* dF, const void* 
                           int rows, int F, int swiglu) {
   const int64_t total = static_cast<int64_t>(rows) * F;
   if (total == 0) return hipSuccess;
-  const dim3 grid(static_cast<unsigned>((total + 255) / 256));
+  const dim3 grid(static_cast<unsigned>((total / 8 + 255) / 256));  // F % 8 == 0
   if (dtype == 1)
     return launch(K_MISC, act_bwd_kernel<bf16_t>, grid, dim3(256), 0, s,
                   static_cast<const bf16_t*>(dF), static_cast<const bf16_t*>(u),
@@ -667,7 +809,7 @@ hipError_t launch_act_fwd(hipStream_t s, int dtype, const void* u, void* f, int 
                           int swiglu) {
   const int64_t total = static_cast<int64_t>(rows) * F;
   if (total == 0) return hipSuccess;
-  const dim3 grid(static_cast<unsigned>((total + 255) / 256));
+  const dim3 grid(static_cast<unsigned>((total / 8 + 255) / 256));  // F % 8 == 0
   if (dtype == 1)
     return launch(K_MISC, act_fwd_kernel<bf16_t>, grid, dim3(256), 0, s,
                   static_cast<const bf16_t*>(u), static_cast<bf16_t*>(f),

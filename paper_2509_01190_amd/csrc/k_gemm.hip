@@ -608,6 +608,23 @@ __global__ __launch_bounds__(256) void splitk_reduce_kernel(const float* __restr
   epilogue_tile<bf16_t, kRedRows, kRedCols, 256>(tile, kRedCols + 4, m0, n0, M, N, ep);
 }
 
+// fp32 sum of the S slices [S][total4] (float4 units), in slice order
+__global__ __launch_bounds__(256) void splitk_sum_f32_kernel(const float4* __restrict__ part,
+                                                             int S, int64_t total4,
+                                                             float4* __restrict__ out) {
+  const int64_t i = static_cast<int64_t>(blockIdx.x) * 256 + threadIdx.x;
+  if (i >= total4) return;
+  float4 v = part[i];
+  for (int y = 1; y < S; ++y) {
+    const float4 t = part[y * total4 + i];
+    v.x += t.x;
+    v.y += t.y;
+    v.z += t.z;
+    v.w += t.w;
+  }
+  out[i] = v;
+}
+
 // ---------------------------------------------------------------------------
 // vector-ALU GEMM (fp32 storage, and any shape)
 // ---------------------------------------------------------------------------
@@ -761,13 +778,32 @@ size_t gemm_workspace_bound(int dtype, int max_rows, int N, int K) {
 }
 
 // out[M][N] = x W^T in fp32 (no epilogue): the weight gradients of the
-// backward pass; bf16 operands with K a multiple of 64
+// backward pass (few output tiles, K = the rows of the batch); bf16
+// operands with K a multiple of 64. Small grids split K as the forward
+// does, and the slices are added in slice order.
 hipError_t launch_gemm_f32(hipStream_t s, const void* x, int M, int K, const void* w, int N,
-                           float* out) {
+                           float* out, void* ws, size_t ws_bytes) {
   if (M == 0 || N == 0) return hipSuccess;
   if (K % kBK != 0) return hipErrorInvalidValue;
   EpiParams ep{};
+  int S = 1, kchunk = K;
+  splitk_plan(M, N, K, &S, &kchunk);
+  if (S > 1 && ws != nullptr && ws_bytes >= splitk_bytes(S, M, N)) {
+    float* part = static_cast<float*>(ws);
+    const hipError_t e = launch_dma<128, 128, 2, 2, 64, 2, 128>(s, x, M, K, w, N, ep, S, kchunk, part);
+    if (e != hipSuccess) return e;
+    const int64_t total4 = static_cast<int64_t>(M) * N / 4;
+    return launch(K_GEMM, splitk_sum_f32_kernel, dim3(static_cast<unsigned>((total4 + 255) / 256)),
+                  dim3(256), 0, s, static_cast<const float4*>(ws), S, total4,
+                  reinterpret_cast<float4*>(out));
+  }
   return launch_dma<128, 128, 2, 2, 64, 2, 128>(s, x, M, K, w, N, ep, 1, K, out);
+}
+
+size_t gemm_f32_workspace_bound(int M, int N, int K) {
+  int S, kchunk;
+  splitk_plan(M, N, K, &S, &kchunk);
+  return splitk_bytes(S, M, N);
 }
 
 hipError_t launch_gemm(hipStream_t s, int dtype, const void* x, int M, int K, const void* w,

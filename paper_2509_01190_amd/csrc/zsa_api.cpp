@@ -873,6 +873,13 @@ BwdLayout bwd_layout(const zsa_layer_cfg* c, int64_t T, Carver& cv) {
                              zsa::gemm_workspace_bound(dt, rows, static_cast<int>(d), static_cast<int>(up_n)),
                              zsa::gemm_workspace_bound(dt, rows, static_cast<int>(d), static_cast<int>(d)),
                              zsa::gemm_workspace_bound(dt, rows, static_cast<int>(d), static_cast<int>(qw))});
+  // ... and for the weight-gradient products (K = the rows, padded to 64)
+  const int kp = static_cast<int>(round64(T));
+  B.splitk_bytes = std::max({B.splitk_bytes,
+                             zsa::gemm_f32_workspace_bound(static_cast<int>(d), static_cast<int>(F), kp),
+                             zsa::gemm_f32_workspace_bound(static_cast<int>(up_n), static_cast<int>(d), kp),
+                             zsa::gemm_f32_workspace_bound(static_cast<int>(d), static_cast<int>(d), kp),
+                             zsa::gemm_f32_workspace_bound(static_cast<int>(qw), static_cast<int>(d), kp)});
   B.splitk = cv.take(B.splitk_bytes);
   B.end = cv.off;
   return B;
@@ -912,7 +919,7 @@ int layer_backward(hipStream_t s, const zsa_layer_cfg& c, const zsa_layer_weight
     if (er != hipSuccess) return er;
     er = launch_transpose(s, dt, b, rows, nb, nb, P(B.bT), rows_p);
     if (er != hipSuccess) return er;
-    return launch_gemm_f32(s, P(B.aT), na, rows_p, P(B.bT), nb, out);
+    return launch_gemm_f32(s, P(B.aT), na, rows_p, P(B.bT), nb, out, sk, B.splitk_bytes);
   };
   // y = x W for W [n_out_w, n_in_w] stored as a Linear weight: x [rows, n_out_w]
   auto xgrad = [&](const void* x, int rows, const void* W, int wn, int wk, void* y) -> hipError_t {

@@ -189,7 +189,8 @@ bool decode_supported(int dtype, int hd, int group);
 // backward pass (bf16, head_dim 64 / 128 for the attention part)
 bool backward_supported(int dtype, int hd);
 hipError_t launch_gemm_f32(hipStream_t s, const void* x, int M, int K, const void* w, int N,
-                           float* out);
+                           float* out, void* ws, size_t ws_bytes);
+size_t gemm_f32_workspace_bound(int M, int N, int K);
 hipError_t launch_transpose(hipStream_t s, int dtype, const void* in, int R, int C, int64_t ldi,
                             void* out, int Rpad);
 size_t colsum_scratch_floats(int R, int C);
