@@ -11,13 +11,14 @@
 // from the forward's log-sum-exp:
 //     dV = P^T dO,  dP = dO V^T,  dS = P o (dP - D),  dK = scale dS^T Q,
 //     dQ = scale dS K.
-// attn_bwd_dkdv: one workgroup per (key block, key/value head, sequence);
-// every wave walks 32-query tiles, computes S = Q K^T and dP = dO V^T in the
-// layout where a lane owns one key, packs P and dS as MFMA A operands and
-// multiplies them with transposed Q / dO tiles staged in its own LDS; the
-// four waves' partial dK / dV are added in wave order (no atomics). For
-// grouped-query attention the workgroup also loops over the query heads
-// that read its key/value head.
+// attn_bwd_dkdv: one workgroup per (128-key block, key/value head,
+// sequence), 32 keys per wave; the waves walk the 32-query tiles together
+// from one double-buffered LDS stage (Q and dO in rows and transposed),
+// compute S = Q K^T and dP = dO V^T in the layout where a lane owns one key,
+// and multiply P and dS, packed as MFMA A operands, with the transposed
+// tiles. Each key's dK / dV is summed by one wave in query order (no
+// atomics). For grouped-query attention the workgroup also loops over the
+// query heads that read its key/value head.
 // attn_bwd_dq: one workgroup per (128-query block, head, sequence), laid out
 // like the forward attention: S^T and dP^T with a lane owning one query, dS
 // packed as the B operand of dQ^T += K^T dS^T, K^T staged in LDS.
@@ -181,47 +182,83 @@ __global__ void zero_f32_kernel(float* __restrict__ p, int n) {
 // out = res + dx (res may alias out, or be NULL); stats[r] = (mean, rstd)
 // (mean 0 for RMS) for the gain / shift gradients.
 // ---------------------------------------------------------------------------
-template <typename T, int RMS>
+template <typename T, int RMS, int NC>
 __global__ __launch_bounds__(256) void norm_bwd_kernel(const T* __restrict__ x,
                                                        const T* __restrict__ g,
                                                        const T* __restrict__ dh, const T* res,
                                                        T* out, int R, int d, float eps,
                                                        float* __restrict__ stats) {
+  // one wave per row; lane owns the 8-column chunks lane, lane + 64, ...
+  // (NC of them, d <= NC * 512), held in registers across the passes
   const int row = blockIdx.x * 4 + (threadIdx.x >> 6);
   const int lane = threadIdx.x & 63;
   if (row >= R) return;
-  const T* xr = x + static_cast<int64_t>(row) * d;
-  const T* dr = dh + static_cast<int64_t>(row) * d;
+  const int64_t base = static_cast<int64_t>(row) * d;
+  float xv[NC][8], gd[NC][8];
+  float s = 0.f;
+#pragma unroll
+  for (int k = 0; k < NC; ++k) {
+    const int c = (k * 64 + lane) * 8;
+    if (c < d) {
+      float gv[8];
+      load8<T>(x + base + c, xv[k]);
+      load8<T>(g + c, gv);
+      load8<T>(dh + base + c, gd[k]);
+#pragma unroll
+      for (int e = 0; e < 8; ++e) {
+        gd[k][e] *= gv[e];
+        s += xv[k][e];
+      }
+    } else {
+#pragma unroll
+      for (int e = 0; e < 8; ++e) xv[k][e] = gd[k][e] = 0.f;
+    }
+  }
   float mean = 0.f;
   if (!RMS) {
-    float s = 0.f;
-    for (int c = lane; c < d; c += 64) s += to_f32(xr[c]);
     for (int o = 32; o > 0; o >>= 1) s += __shfl_xor(s, o, 64);
     mean = s / d;
   }
   float ss = 0.f;
-  for (int c = lane; c < d; c += 64) {
-    const float v = to_f32(xr[c]) - mean;
-    ss += v * v;
+#pragma unroll
+  for (int k = 0; k < NC; ++k) {
+    if ((k * 64 + lane) * 8 < d) {
+#pragma unroll
+      for (int e = 0; e < 8; ++e) {
+        const float v = xv[k][e] - mean;
+        ss += v * v;
+      }
+    }
   }
   for (int o = 32; o > 0; o >>= 1) ss += __shfl_xor(ss, o, 64);
   const float rstd = 1.0f / sqrtf(ss / d + eps);
   float s1 = 0.f, s2 = 0.f;  // sum(g dh), sum(g dh xhat)
-  for (int c = lane; c < d; c += 64) {
-    const float gd = to_f32(g[c]) * to_f32(dr[c]);
-    s1 += gd;
-    s2 += gd * (to_f32(xr[c]) - mean) * rstd;
+#pragma unroll
+  for (int k = 0; k < NC; ++k) {
+#pragma unroll
+    for (int e = 0; e < 8; ++e) {
+      s1 += gd[k][e];
+      s2 += gd[k][e] * (xv[k][e] - mean) * rstd;  // zero on chunks past d
+    }
   }
   for (int o = 32; o > 0; o >>= 1) {
     s1 += __shfl_xor(s1, o, 64);
     s2 += __shfl_xor(s2, o, 64);
   }
   const float m1 = RMS ? 0.f : s1 / d, m2 = s2 / d;
-  for (int c = lane; c < d; c += 64) {
-    const float xh = (to_f32(xr[c]) - mean) * rstd;
-    float v = rstd * (to_f32(g[c]) * to_f32(dr[c]) - m1 - xh * m2);
-    if (res != nullptr) v += to_f32(res[static_cast<int64_t>(row) * d + c]);
-    out[static_cast<int64_t>(row) * d + c] = from_f32<T>(v);
+#pragma unroll
+  for (int k = 0; k < NC; ++k) {
+    const int c = (k * 64 + lane) * 8;
+    if (c < d) {
+      float o[8], rv[8];
+      if (res != nullptr) load8<T>(res + base + c, rv);
+#pragma unroll
+      for (int e = 0; e < 8; ++e) {
+        const float xh = (xv[k][e] - mean) * rstd;
+        o[e] = rstd * (gd[k][e] - m1 - xh * m2) + (res != nullptr ? rv[e] : 0.f);
+      }
+      store8<T>(out + base + c, o);
+    }
   }
   if (lane == 0) {
     stats[2 * row] = mean;
@@ -330,25 +367,30 @@ __global__ __launch_bounds__(256) void scatter_rows_kernel(const uint4* __restri
   dst[i] = s >= 0 ? src[static_cast<int64_t>(s) * cpr + c] : make_uint4(0u, 0u, 0u, 0u);
 }
 
-// D[h][r] = sum_c dO[r][h hd + c] O[r][h hd + c] (hd a multiple of 8)
+// D[h][r] = sum_c dO[r][h hd + c] O[r][h hd + c]: each thread takes 8
+// consecutive columns, the L = hd / 8 threads of one head (L a power of two
+// up to 64, adjacent lanes of one wave) add theirs in a fixed butterfly
 template <typename T>
 __global__ __launch_bounds__(256) void rowdot_kernel(const T* __restrict__ dO,
                                                      const T* __restrict__ O, int64_t ld, int T_,
                                                      int H, int hd, float* __restrict__ D) {
+  const int L = hd / 8, per_row = H * L;
   const int64_t i = static_cast<int64_t>(blockIdx.x) * 256 + threadIdx.x;
-  if (i >= static_cast<int64_t>(T_) * H) return;
-  const int r = static_cast<int>(i / H), h = static_cast<int>(i % H);
-  const T* a = dO + static_cast<int64_t>(r) * ld + h * hd;
-  const T* b = O + static_cast<int64_t>(r) * ld + h * hd;
+  const bool live = i < static_cast<int64_t>(T_) * per_row;
+  const int r = live ? static_cast<int>(i / per_row) : 0;
+  const int c8 = live ? static_cast<int>(i - static_cast<int64_t>(r) * per_row) : 0;
   float s = 0.f;
-  for (int c = 0; c < hd; c += 8) {
+  if (live) {
     float va[8], vb[8];
-    load8<T>(a + c, va);
-    load8<T>(b + c, vb);
+    load8<T>(dO + static_cast<int64_t>(r) * ld + c8 * 8, va);
+    load8<T>(O + static_cast<int64_t>(r) * ld + c8 * 8, vb);
 #pragma unroll
     for (int e = 0; e < 8; ++e) s = fmaf(va[e], vb[e], s);
   }
-  D[static_cast<int64_t>(h) * T_ + r] = s;
+  // groups of L lanes start at multiples of L within the wave (64 % L == 0
+  // and each block is 256 threads), so the butterfly stays inside one head
+  for (int o = 1; o < L; o <<= 1) s += __shfl_xor(s, o, 64);
+  if (live && (c8 & (L - 1)) == 0) D[static_cast<int64_t>(c8 / L) * T_ + r] = s;
 }
 
 // inverse rotary rotation of the gradient, in place, on the first `cols`
@@ -380,21 +422,35 @@ __device__ __forceinline__ float pick4(const float4& v, int i) {
   return i == 0 ? v.x : i == 1 ? v.y : i == 2 ? v.z : v.w;
 }
 
-template <int HD, int NKS>
+// Each workgroup owns 128 consecutive keys of one kv head, 32 per wave. The
+// waves sweep the query tiles of 32 together: each tile of Q and dO (with
+// the rows' log-sum-exp and D) is staged once per workgroup into LDS, in
+// rows (the A operands of S = Q K^T and dP = dO V^T) and transposed (the B
+// operands of dV += P^T dO and dK += dS^T Q), double-buffered so the next
+// tile's global loads overlap this tile's MFMAs. P and dS leave the
+// accumulators with the keys on the lanes and the queries in the registers,
+// so they are the A operands of the dV and dK products as they are; each
+// wave keeps its keys' dK and dV and writes them once.
+template <int HD>
 __global__ __launch_bounds__(256) void attn_bwd_dkdv_kernel(
     const bf16_t* __restrict__ Q, const bf16_t* __restrict__ K, const bf16_t* __restrict__ V,
     int64_t rs, const bf16_t* __restrict__ dO, int64_t ors, const float* __restrict__ lse,
-    const float* __restrict__ Dv, int T, int H, int kv_group, int causal, float scale,
+    const float* __restrict__ Dv, int T, int kv_group, int causal, float scale,
     float scale_log2, const int32_t* __restrict__ cu, bf16_t* __restrict__ dK,
     bf16_t* __restrict__ dV, int64_t grs) {
-  constexpr int KW = 32 * NKS;    // keys per workgroup
-  constexpr int KK = HD / 16;
-  constexpr int CT = HD / 32;
-  constexpr int TLD = 32 + 8;     // transposed tile row stride (bf16)
-  constexpr int WAVE_BYTES = 2 * HD * TLD * 2;
-  constexpr int RED_BYTES = 4 * KW * HD * 4;
-  constexpr int SMEM = 4 * WAVE_BYTES > RED_BYTES ? 4 * WAVE_BYTES : RED_BYTES;
-  __shared__ __align__(16) unsigned char smem[SMEM];
+  constexpr int KW = 128, QT = 32;
+  constexpr int KK = HD / 16, CT = HD / 32;
+  constexpr int RLD = HD + 8;            // row tile stride (bf16)
+  constexpr int TLD = QT + 4;            // transposed tile stride (bf16), 18 dwords
+  constexpr int ROW_E = QT * RLD, TR_E = HD * TLD;
+  constexpr int BUF = 4 * ROW_E + 4 * TR_E + 2 * QT * 4;  // bytes of one stage
+  constexpr int TASKS = 2 * (QT / 2) * (HD / 8);          // (tensor, query pair, chunk)
+  constexpr int NT = TASKS / 256;
+  static_assert(NT >= 1 && NT * 256 == TASKS, "staging tasks must fill the block");
+  static_assert(BUF % 16 == 0, "stage size");
+  static_assert(8 * 32 * RLD * 2 <= 2 * BUF, "output staging fits the stages");
+  __shared__ __align__(16) unsigned char smem[2 * BUF];
+
   const int b = blockIdx.z, g = blockIdx.y;
   const int lo = cu[b];
   const int n = cu[b + 1] - lo;
@@ -402,161 +458,175 @@ __global__ __launch_bounds__(256) void attn_bwd_dkdv_kernel(
   if (j0 >= n) return;
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int half = lane >> 5, l32 = lane & 31;
-  bf16_t* Qt = reinterpret_cast<bf16_t*>(smem + wave * WAVE_BYTES);
-  bf16_t* Dt = Qt + HD * TLD;
+  const int jw = j0 + wave * 32;  // the wave's first key
+  const bool wave_live = jw < n;
 
-  bf16x8_t kf[NKS][KK], vf[NKS][KK];
-#pragma unroll
-  for (int ks = 0; ks < NKS; ++ks) {
-    const int jr = lo + min(j0 + ks * 32 + l32, n - 1);
+  bf16x8_t kf[KK], vf[KK];
+  {
+    const int jr = lo + min(jw + l32, n - 1);
 #pragma unroll
     for (int kk = 0; kk < KK; ++kk) {
-      kf[ks][kk] = __builtin_bit_cast(bf16x8_t, *reinterpret_cast<const u32x4*>(
-                                                    K + static_cast<int64_t>(jr) * rs + g * HD + kk * 16 + half * 8));
-      vf[ks][kk] = __builtin_bit_cast(bf16x8_t, *reinterpret_cast<const u32x4*>(
-                                                    V + static_cast<int64_t>(jr) * rs + g * HD + kk * 16 + half * 8));
+      kf[kk] = __builtin_bit_cast(bf16x8_t, *reinterpret_cast<const u32x4*>(
+                                                K + static_cast<int64_t>(jr) * rs + g * HD + kk * 16 + half * 8));
+      vf[kk] = __builtin_bit_cast(bf16x8_t, *reinterpret_cast<const u32x4*>(
+                                                V + static_cast<int64_t>(jr) * rs + g * HD + kk * 16 + half * 8));
     }
   }
-  f32x16_t dk[NKS][CT], dv[NKS][CT];
+  f32x16_t dk[CT], dv[CT];
 #pragma unroll
-  for (int ks = 0; ks < NKS; ++ks)
+  for (int ct = 0; ct < CT; ++ct)
 #pragma unroll
-    for (int ct = 0; ct < CT; ++ct)
+    for (int r = 0; r < 16; ++r) {
+      dk[ct][r] = 0.f;
+      dv[ct][r] = 0.f;
+    }
+
+  // queries before the first key see none of the keys (causal)
+  const int qs = causal ? j0 : 0;
+  const int ntile = (n - qs + QT - 1) / QT;
+  const int rounds = ntile * kv_group;
+
+  u32x4 st[NT][2];
+  float stl = 0.f;
+  auto fetch = [&](int t) {
+    const int e = t / ntile, i0 = qs + (t - e * ntile) * QT, h = g * kv_group + e;
+#pragma unroll
+    for (int k = 0; k < NT; ++k) {
+      const int task = tid + 256 * k;
+      const int tensor = task / (TASKS / 2), rem = task % (TASKS / 2);
+      const int rp = rem / (HD / 8), ch = (rem % (HD / 8)) * 8;
+      const int r0 = lo + min(i0 + 2 * rp, n - 1), r1 = lo + min(i0 + 2 * rp + 1, n - 1);
+      const bf16_t* src = tensor ? dO : Q;
+      const int64_t ld = tensor ? ors : rs;
+      st[k][0] = *reinterpret_cast<const u32x4*>(src + static_cast<int64_t>(r0) * ld + h * HD + ch);
+      st[k][1] = *reinterpret_cast<const u32x4*>(src + static_cast<int64_t>(r1) * ld + h * HD + ch);
+    }
+    if (tid < 2 * QT) {
+      const int64_t i = static_cast<int64_t>(h) * T + lo + min(i0 + (tid & (QT - 1)), n - 1);
+      stl = tid < QT ? lse[i] * kLog2e : Dv[i];
+    }
+  };
+  auto stash = [&](int buf) {
+    bf16_t* rowQ = reinterpret_cast<bf16_t*>(smem + buf * BUF);
+    bf16_t* trQ = rowQ + 2 * ROW_E;
+    float* LD = reinterpret_cast<float*>(trQ + 2 * TR_E);
+#pragma unroll
+    for (int k = 0; k < NT; ++k) {
+      const int task = tid + 256 * k;
+      const int tensor = task / (TASKS / 2), rem = task % (TASKS / 2);
+      const int rp = rem / (HD / 8), ch = (rem % (HD / 8)) * 8;
+      bf16_t* rw = rowQ + tensor * ROW_E;
+      bf16_t* tr = trQ + tensor * TR_E;
+      *reinterpret_cast<u32x4*>(rw + (2 * rp) * RLD + ch) = st[k][0];
+      *reinterpret_cast<u32x4*>(rw + (2 * rp + 1) * RLD + ch) = st[k][1];
+#pragma unroll
+      for (int c = 0; c < 8; ++c) {
+        const uint32_t a0 = st[k][0][c >> 1], a1 = st[k][1][c >> 1];
+        const uint32_t lo16 = (c & 1) ? (a0 >> 16) : (a0 & 0xffffu);
+        const uint32_t hi16 = (c & 1) ? (a1 & 0xffff0000u) : (a1 << 16);
+        *reinterpret_cast<uint32_t*>(tr + (ch + c) * TLD + 2 * rp) = lo16 | hi16;
+      }
+    }
+    if (tid < 2 * QT) LD[tid] = stl;
+  };
+
+  fetch(0);
+  stash(0);
+  __syncthreads();
+  for (int t = 0; t < rounds; ++t) {
+    if (t + 1 < rounds) fetch(t + 1);
+    const int e = t / ntile, i0 = qs + (t - e * ntile) * QT;
+    // a wave whose keys all lie past this tile's last query sees none of it
+    if (wave_live && !(causal && jw > i0 + QT - 1)) {
+      const bf16_t* rowQ = reinterpret_cast<const bf16_t*>(smem + (t & 1) * BUF);
+      const bf16_t* rowD = rowQ + ROW_E;
+      const bf16_t* trQ = rowQ + 2 * ROW_E;
+      const bf16_t* trD = trQ + TR_E;
+      const float* LD = reinterpret_cast<const float*>(trQ + 2 * TR_E);
+      f32x16_t s, dp;
 #pragma unroll
       for (int r = 0; r < 16; ++r) {
-        dk[ks][ct][r] = 0.f;
-        dv[ks][ct][r] = 0.f;
+        s[r] = 0.f;
+        dp[r] = 0.f;
       }
-
-  const int qs = causal ? (j0 & ~31) : 0;
-  // the four waves take the query tiles base + 32 wave in lockstep (a wave
-  // past the sequence idles), so block barriers order the LDS staging
-  for (int e = 0; e < kv_group; ++e) {
-    const int h = g * kv_group + e;
-    for (int base = qs; base < n; base += 128) {
-      const int i0 = base + wave * 32;
-      const bool active = i0 < n;
-      __syncthreads();  // the previous round's reads of the staged tiles are done
-      if (active) {
-      // this tile's Q and dO, transposed into the wave's LDS (query pairs packed)
-      for (int task = lane; task < 16 * (HD / 8); task += 64) {
-        const int rp = task / (HD / 8), ch = (task % (HD / 8)) * 8;
-        const int r0 = lo + min(i0 + 2 * rp, n - 1), r1 = lo + min(i0 + 2 * rp + 1, n - 1);
-        const u32x4 q0 = *reinterpret_cast<const u32x4*>(Q + static_cast<int64_t>(r0) * rs + h * HD + ch);
-        const u32x4 q1 = *reinterpret_cast<const u32x4*>(Q + static_cast<int64_t>(r1) * rs + h * HD + ch);
-        const u32x4 d0 = *reinterpret_cast<const u32x4*>(dO + static_cast<int64_t>(r0) * ors + h * HD + ch);
-        const u32x4 d1 = *reinterpret_cast<const u32x4*>(dO + static_cast<int64_t>(r1) * ors + h * HD + ch);
-#pragma unroll
-        for (int c = 0; c < 8; ++c) {
-          const uint32_t a0 = q0[c >> 1], a1 = q1[c >> 1], b0 = d0[c >> 1], b1 = d1[c >> 1];
-          const uint32_t qlo = (c & 1) ? (a0 >> 16) : (a0 & 0xffffu);
-          const uint32_t qhi = (c & 1) ? (a1 & 0xffff0000u) : (a1 << 16);
-          const uint32_t dlo = (c & 1) ? (b0 >> 16) : (b0 & 0xffffu);
-          const uint32_t dhi = (c & 1) ? (b1 & 0xffff0000u) : (b1 << 16);
-          *reinterpret_cast<uint32_t*>(Qt + (ch + c) * TLD + 2 * rp) = qlo | qhi;
-          *reinterpret_cast<uint32_t*>(Dt + (ch + c) * TLD + 2 * rp) = dlo | dhi;
-        }
-      }
-      }
-      __syncthreads();
-      if (!active) continue;
-      const int qr = lo + min(i0 + l32, n - 1);
-      bf16x8_t qa[KK], da[KK];
 #pragma unroll
       for (int kk = 0; kk < KK; ++kk) {
-        qa[kk] = __builtin_bit_cast(bf16x8_t, *reinterpret_cast<const u32x4*>(
-                                                  Q + static_cast<int64_t>(qr) * rs + h * HD + kk * 16 + half * 8));
-        da[kk] = __builtin_bit_cast(bf16x8_t, *reinterpret_cast<const u32x4*>(
-                                                  dO + static_cast<int64_t>(qr) * ors + h * HD + kk * 16 + half * 8));
+        const bf16x8_t qa = __builtin_bit_cast(
+            bf16x8_t, *reinterpret_cast<const u32x4*>(rowQ + l32 * RLD + kk * 16 + half * 8));
+        const bf16x8_t da = __builtin_bit_cast(
+            bf16x8_t, *reinterpret_cast<const u32x4*>(rowD + l32 * RLD + kk * 16 + half * 8));
+        s = __builtin_amdgcn_mfma_f32_32x32x16_bf16(qa, kf[kk], s, 0, 0, 0);
+        dp = __builtin_amdgcn_mfma_f32_32x32x16_bf16(da, vf[kk], dp, 0, 0, 0);
       }
-      // this lane's 16 query rows: i0 + 8 (r/4) + 4 half + r%4
-      float L[16], Dd[16];
+      // s[r], dp[r]: query i0 + 8 (r/4) + 4 half + r%4, key jw + l32. Keys
+      // past the sequence only feed accumulator rows that are not written.
+      const int j = jw + l32;
+      const bool edge = i0 + QT > n || (causal && jw + 31 > i0);
 #pragma unroll
-      for (int r = 0; r < 16; ++r) {
-        const int i = min(i0 + 8 * (r >> 2) + 4 * half + (r & 3), n - 1);
-        L[r] = lse[static_cast<int64_t>(h) * T + lo + i] * kLog2e;
-        Dd[r] = Dv[static_cast<int64_t>(h) * T + lo + i];
-      }
-      const bool edge = i0 + 32 > n || (causal && j0 + KW - 1 > i0);
+      for (int a = 0; a < 4; ++a) {
+        const float4 L4 = *reinterpret_cast<const float4*>(LD + 8 * a + 4 * half);
+        const float4 D4 = *reinterpret_cast<const float4*>(LD + QT + 8 * a + 4 * half);
 #pragma unroll
-      for (int ks = 0; ks < NKS; ++ks) {
-        f32x16_t s, dp;
-#pragma unroll
-        for (int r = 0; r < 16; ++r) {
-          s[r] = 0.f;
-          dp[r] = 0.f;
-        }
-#pragma unroll
-        for (int kk = 0; kk < KK; ++kk) {
-          s = __builtin_amdgcn_mfma_f32_32x32x16_bf16(qa[kk], kf[ks][kk], s, 0, 0, 0);
-          dp = __builtin_amdgcn_mfma_f32_32x32x16_bf16(da[kk], vf[ks][kk], dp, 0, 0, 0);
-        }
-        // s[r], dp[r]: query i0 + 8 (r/4) + 4 half + r%4, key j0 + 32 ks + l32
-        const int j = j0 + ks * 32 + l32;
-#pragma unroll
-        for (int r = 0; r < 16; ++r) {
-          float p = __builtin_amdgcn_exp2f(fmaf(s[r], scale_log2, -L[r]));
+        for (int q = 0; q < 4; ++q) {
+          const int r = 4 * a + q;
+          float p = __builtin_amdgcn_exp2f(fmaf(s[r], scale_log2, -pick4(L4, q)));
           if (edge) {
-            const int i = i0 + 8 * (r >> 2) + 4 * half + (r & 3);
-            if (i >= n || j >= n || (causal && j > i)) p = 0.f;
+            const int i = i0 + 8 * a + 4 * half + q;
+            if (i >= n || (causal && j > i)) p = 0.f;
           }
           s[r] = p;
-          dp[r] = p * (dp[r] - Dd[r]);
+          dp[r] = p * (dp[r] - pick4(D4, q));
         }
+      }
 #pragma unroll
-        for (int g4 = 0; g4 < 2; ++g4) {
-          const int rb = 8 * g4;
-          const u32x4 pw = {pack_bf16x2(s[rb], s[rb + 1]), pack_bf16x2(s[rb + 2], s[rb + 3]),
-                            pack_bf16x2(s[rb + 4], s[rb + 5]), pack_bf16x2(s[rb + 6], s[rb + 7])};
-          const u32x4 sw = {pack_bf16x2(dp[rb], dp[rb + 1]), pack_bf16x2(dp[rb + 2], dp[rb + 3]),
-                            pack_bf16x2(dp[rb + 4], dp[rb + 5]), pack_bf16x2(dp[rb + 6], dp[rb + 7])};
-          const bf16x8_t pa = __builtin_bit_cast(bf16x8_t, pw);
-          const bf16x8_t sa = __builtin_bit_cast(bf16x8_t, sw);
-          const int base = 16 * g4 + 4 * half;  // queries base..+3, base+8..+11
+      for (int g4 = 0; g4 < 2; ++g4) {
+        const int rb = 8 * g4;
+        const u32x4 pw = {pack_bf16x2(s[rb], s[rb + 1]), pack_bf16x2(s[rb + 2], s[rb + 3]),
+                          pack_bf16x2(s[rb + 4], s[rb + 5]), pack_bf16x2(s[rb + 6], s[rb + 7])};
+        const u32x4 sw = {pack_bf16x2(dp[rb], dp[rb + 1]), pack_bf16x2(dp[rb + 2], dp[rb + 3]),
+                          pack_bf16x2(dp[rb + 4], dp[rb + 5]), pack_bf16x2(dp[rb + 6], dp[rb + 7])};
+        const bf16x8_t pa = __builtin_bit_cast(bf16x8_t, pw);
+        const bf16x8_t sa = __builtin_bit_cast(bf16x8_t, sw);
+        const int base = 16 * g4 + 4 * half;  // queries base..+3, base+8..+11
 #pragma unroll
-          for (int ct = 0; ct < CT; ++ct) {
-            const bf16_t* dr = Dt + (ct * 32 + l32) * TLD + base;
-            const bf16_t* qrw = Qt + (ct * 32 + l32) * TLD + base;
-            const uint2 d_lo = *reinterpret_cast<const uint2*>(dr);
-            const uint2 d_hi = *reinterpret_cast<const uint2*>(dr + 8);
-            const uint2 q_lo = *reinterpret_cast<const uint2*>(qrw);
-            const uint2 q_hi = *reinterpret_cast<const uint2*>(qrw + 8);
-            const u32x4 bd = {d_lo.x, d_lo.y, d_hi.x, d_hi.y};
-            const u32x4 bq = {q_lo.x, q_lo.y, q_hi.x, q_hi.y};
-            dv[ks][ct] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(
-                pa, __builtin_bit_cast(bf16x8_t, bd), dv[ks][ct], 0, 0, 0);
-            dk[ks][ct] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(
-                sa, __builtin_bit_cast(bf16x8_t, bq), dk[ks][ct], 0, 0, 0);
-          }
+        for (int ct = 0; ct < CT; ++ct) {
+          const bf16_t* dr = trD + (ct * 32 + l32) * TLD + base;
+          const bf16_t* qrw = trQ + (ct * 32 + l32) * TLD + base;
+          const uint2 d_lo = *reinterpret_cast<const uint2*>(dr);
+          const uint2 d_hi = *reinterpret_cast<const uint2*>(dr + 8);
+          const uint2 q_lo = *reinterpret_cast<const uint2*>(qrw);
+          const uint2 q_hi = *reinterpret_cast<const uint2*>(qrw + 8);
+          const u32x4 bd = {d_lo.x, d_lo.y, d_hi.x, d_hi.y};
+          const u32x4 bq = {q_lo.x, q_lo.y, q_hi.x, q_hi.y};
+          dv[ct] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(pa, __builtin_bit_cast(bf16x8_t, bd),
+                                                           dv[ct], 0, 0, 0);
+          dk[ct] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(sa, __builtin_bit_cast(bf16x8_t, bq),
+                                                           dk[ct], 0, 0, 0);
         }
       }
     }
+    if (t + 1 < rounds) stash((t + 1) & 1);
+    __syncthreads();
   }
-  // acc[ks][ct][r]: key j0 + 32 ks + 8 (r/4) + 4 half + r%4, channel ct*32 + l32.
-  // The waves' partial sums are added in wave order through LDS.
-  float* red = reinterpret_cast<float*>(smem);
+  // acc[ct][r]: key jw + 8 (r/4) + 4 half + r%4, channel ct*32 + l32; staged
+  // as bf16 rows in LDS (the wave's own region), then written 16 bytes a lane
+  bf16_t* ov = reinterpret_cast<bf16_t*>(smem) + wave * 2 * 32 * RLD;
+  bf16_t* okk = ov + 32 * RLD;
 #pragma unroll
-  for (int pass = 0; pass < 2; ++pass) {
-    __syncthreads();
+  for (int ct = 0; ct < CT; ++ct)
 #pragma unroll
-    for (int ks = 0; ks < NKS; ++ks)
-#pragma unroll
-      for (int ct = 0; ct < CT; ++ct)
-#pragma unroll
-        for (int r = 0; r < 16; ++r) {
-          const int key = ks * 32 + 8 * (r >> 2) + 4 * half + (r & 3);
-          red[(wave * KW + key) * HD + ct * 32 + l32] = pass == 0 ? dv[ks][ct][r] : dk[ks][ct][r];
-        }
-    __syncthreads();
-    bf16_t* dst = pass == 0 ? dV : dK;
-    const float mul = pass == 0 ? 1.0f : scale;
-    for (int e2 = tid; e2 < KW * HD; e2 += 256) {
-      const int key = e2 / HD, c = e2 % HD;
-      if (j0 + key >= n) continue;
-      const float v = ((red[(0 * KW + key) * HD + c] + red[(1 * KW + key) * HD + c]) +
-                       red[(2 * KW + key) * HD + c]) + red[(3 * KW + key) * HD + c];
-      dst[static_cast<int64_t>(lo + j0 + key) * grs + g * HD + c] = f32_to_bf16(v * mul);
+    for (int r = 0; r < 16; ++r) {
+      const int key = 8 * (r >> 2) + 4 * half + (r & 3);
+      ov[key * RLD + ct * 32 + l32] = f32_to_bf16(dv[ct][r]);
+      okk[key * RLD + ct * 32 + l32] = f32_to_bf16(dk[ct][r] * scale);
     }
+  __syncthreads();
+  for (int c = lane; c < 32 * (HD / 8); c += 64) {
+    const int key = c / (HD / 8), ch = (c % (HD / 8)) * 8;
+    if (jw + key >= n) continue;
+    const int64_t o = static_cast<int64_t>(lo + jw + key) * grs + g * HD + ch;
+    *reinterpret_cast<u32x4*>(dV + o) = *reinterpret_cast<const u32x4*>(ov + key * RLD + ch);
+    *reinterpret_cast<u32x4*>(dK + o) = *reinterpret_cast<const u32x4*>(okk + key * RLD + ch);
   }
 }
 
@@ -768,27 +838,33 @@ hipError_t launch_colsum(hipStream_t s, int dtype, const void* a, int64_t lda, c
   }
 }
 
+template <typename T, int RMS>
+static hipError_t norm_bwd_nc(hipStream_t s, const void* x, const void* g, const void* dh,
+                              const void* res, void* out, int R, int d, float eps, float* stats) {
+  const dim3 grid((R + 3) / 4), block(256);
+  auto* xp = static_cast<const T*>(x);
+  auto* gp = static_cast<const T*>(g);
+  auto* dp = static_cast<const T*>(dh);
+  auto* rp = static_cast<const T*>(res);
+  auto* op = static_cast<T*>(out);
+  const int nc = (d + 511) / 512;
+  if (nc <= 1) return launch(K_NORM, norm_bwd_kernel<T, RMS, 1>, grid, block, 0, s, xp, gp, dp, rp, op, R, d, eps, stats);
+  if (nc <= 2) return launch(K_NORM, norm_bwd_kernel<T, RMS, 2>, grid, block, 0, s, xp, gp, dp, rp, op, R, d, eps, stats);
+  if (nc <= 4) return launch(K_NORM, norm_bwd_kernel<T, RMS, 4>, grid, block, 0, s, xp, gp, dp, rp, op, R, d, eps, stats);
+  if (nc <= 8) return launch(K_NORM, norm_bwd_kernel<T, RMS, 8>, grid, block, 0, s, xp, gp, dp, rp, op, R, d, eps, stats);
+  return launch(K_NORM, norm_bwd_kernel<T, RMS, 16>, grid, block, 0, s, xp, gp, dp, rp, op, R, d, eps, stats);
+}
+
 hipError_t launch_norm_bwd(hipStream_t s, int dtype, int kind, const void* x, const void* g,
                            const void* dh, const void* res, void* out, int R, int d, float eps,
                            float* stats) {
   if (R == 0) return hipSuccess;
-  const dim3 grid((R + 3) / 4), block(256);
-  if (dtype == 1) {
-    auto* xp = static_cast<const bf16_t*>(x);
-    auto* gp = static_cast<const bf16_t*>(g);
-    auto* dp = static_cast<const bf16_t*>(dh);
-    auto* rp = static_cast<const bf16_t*>(res);
-    auto* op = static_cast<bf16_t*>(out);
-    return kind == 1 ? launch(K_NORM, norm_bwd_kernel<bf16_t, 1>, grid, block, 0, s, xp, gp, dp, rp, op, R, d, eps, stats)
-                     : launch(K_NORM, norm_bwd_kernel<bf16_t, 0>, grid, block, 0, s, xp, gp, dp, rp, op, R, d, eps, stats);
-  }
-  auto* xp = static_cast<const float*>(x);
-  auto* gp = static_cast<const float*>(g);
-  auto* dp = static_cast<const float*>(dh);
-  auto* rp = static_cast<const float*>(res);
-  auto* op = static_cast<float*>(out);
-  return kind == 1 ? launch(K_NORM, norm_bwd_kernel<float, 1>, grid, block, 0, s, xp, gp, dp, rp, op, R, d, eps, stats)
-                   : launch(K_NORM, norm_bwd_kernel<float, 0>, grid, block, 0, s, xp, gp, dp, rp, op, R, d, eps, stats);
+  if (d % 8 != 0 || d > 16 * 512) return hipErrorInvalidValue;
+  if (dtype == 1)
+    return kind == 1 ? norm_bwd_nc<bf16_t, 1>(s, x, g, dh, res, out, R, d, eps, stats)
+                     : norm_bwd_nc<bf16_t, 0>(s, x, g, dh, res, out, R, d, eps, stats);
+  return kind == 1 ? norm_bwd_nc<float, 1>(s, x, g, dh, res, out, R, d, eps, stats)
+                   : norm_bwd_nc<float, 0>(s, x, g, dh, res, out, R, d, eps, stats);
 }
 
 hipError_t launch_act_bwd(hipStream_t s, int dtype, const void* dF, const void* u, void* du,
@@ -839,7 +915,9 @@ hipError_t launch_scatter_rows(hipStream_t s, int dtype, int d, const void* src,
 
 hipError_t launch_rowdot(hipStream_t s, int dtype, const void* dO, const void* O, int64_t ld,
                          int T, int H, int hd, float* D) {
-  const int64_t total = static_cast<int64_t>(T) * H;
+  const int L = hd / 8;
+  if (hd % 8 != 0 || L > 64 || (L & (L - 1)) != 0) return hipErrorInvalidValue;
+  const int64_t total = static_cast<int64_t>(T) * H * L;
   if (total == 0) return hipSuccess;
   const dim3 grid(static_cast<unsigned>((total + 255) / 256));
   if (dtype == 1)
@@ -875,16 +953,16 @@ hipError_t launch_attention_bwd(hipStream_t s, const void* q, const void* k, con
   const int Hkv = H / kv_group;
   hipError_t e;
   if (hd == 64) {
-    e = launch(K_ATTENTION, attn_bwd_dkdv_kernel<64, 2>, dim3((max_len + 63) / 64, Hkv, B),
-               dim3(256), 0, s, qp, kp, vp, rs, dp, ors, lse, D, T, H, kv_group, causal, scale, sl,
+    e = launch(K_ATTENTION, attn_bwd_dkdv_kernel<64>, dim3((max_len + 127) / 128, Hkv, B),
+               dim3(256), 0, s, qp, kp, vp, rs, dp, ors, lse, D, T, kv_group, causal, scale, sl,
                cu_dev, static_cast<bf16_t*>(dk), static_cast<bf16_t*>(dv), grs);
     if (e != hipSuccess) return e;
     return launch(K_ATTENTION, attn_bwd_dq_kernel<64>, dim3((max_len + 127) / 128, H, B),
                   dim3(256), 0, s, qp, kp, vp, rs, dp, ors, lse, D, T, kv_group, causal, scale, sl,
                   cu_dev, static_cast<bf16_t*>(dq), grs);
   }
-  e = launch(K_ATTENTION, attn_bwd_dkdv_kernel<128, 1>, dim3((max_len + 31) / 32, Hkv, B),
-             dim3(256), 0, s, qp, kp, vp, rs, dp, ors, lse, D, T, H, kv_group, causal, scale, sl,
+  e = launch(K_ATTENTION, attn_bwd_dkdv_kernel<128>, dim3((max_len + 127) / 128, Hkv, B),
+             dim3(256), 0, s, qp, kp, vp, rs, dp, ors, lse, D, T, kv_group, causal, scale, sl,
              cu_dev, static_cast<bf16_t*>(dk), static_cast<bf16_t*>(dv), grs);
   if (e != hipSuccess) return e;
   return launch(K_ATTENTION, attn_bwd_dq_kernel<128>, dim3((max_len + 127) / 128, H, B),
