@@ -372,6 +372,20 @@ constexpr int dma_waves_per_simd() {
 // s_waitcnt immediate: vector-memory count <= n, LDS/scalar and export counts 0
 __device__ __forceinline__ constexpr int vmcnt_imm(int n) { return (n & 15) | ((n >> 4) << 14); }
 
+// Workgroup barrier for the K pipeline. __syncthreads() carries a
+// workgroup-scope release fence, for which the compiler waits on every
+// outstanding global operation -- including the K slices meant to stay in
+// flight. Here the DMA writes a wave depends on are covered by its explicit
+// vmcnt wait before the barrier, its own LDS reads by the lgkmcnt wait, the
+// asm memory clobber keeps the compiler from moving memory operations
+// across it, and the scheduling barriers keep every other instruction
+// (MFMAs included) on its side of it.
+__device__ __forceinline__ void barrier_lds() {
+  __builtin_amdgcn_sched_barrier(0);
+  asm volatile("s_waitcnt lgkmcnt(0)\n\ts_barrier" ::: "memory");
+  __builtin_amdgcn_sched_barrier(0);
+}
+
 template <int BM, int BN, int WM, int WN, int KB, int NS, int ER>
 __global__ __launch_bounds__(WM * WN * 64)
 __attribute__((amdgpu_waves_per_eu(dma_waves_per_simd<BM, BN, WM, WN, KB, NS, ER>(),
@@ -474,7 +488,7 @@ gemm_bf16_dma_kernel(
       __builtin_amdgcn_s_waitcnt(vmcnt_imm((NS - 2) * (AI + BI)));                       \
     else                                                                                 \
       __builtin_amdgcn_s_waitcnt(0);                                                     \
-    __syncthreads();                                                                     \
+    barrier_lds();                                                                       \
     if ((T) + NS - 1 < KTOT) {                                                           \
       ZSA_DMA(((S) + NS - 1) % NS, ((T) + NS - 1) * KB)                                  \
     }                                                                                    \
@@ -684,6 +698,553 @@ __global__ __launch_bounds__(256) void gemm_valu_kernel(const T* __restrict__ X,
 }
 
 
+// ---------------------------------------------------------------------------
+// persistent bf16 GEMM, epilogue in registers (bias, GELU, residual)
+// ---------------------------------------------------------------------------
+// Two workgroups per CU stay resident and each walks a strided share of its
+// XCD's range of 128 x 128 output tiles (the grouped order above). Between
+// two tiles nothing drains: once the last K slice of a tile has been read,
+// the first slice of the next tile is put in flight, and only then is the
+// finished tile's epilogue done -- in registers, from the accumulators
+// (which hold C^T: lane l owns row l%32 of a 32-row block and 4 consecutive
+// columns per register group), with raw buffer stores whose range check
+// drops the rows past M. The stores are not waited for; the next tile's
+// first wait counts them as the youngest operations in flight (vector
+// memory operations complete in issue order), so it waits for its slice
+// only. The bias is read with scalar loads; a residual is fetched during
+// the tile's last K step.
+//
+// Operand staging and the K pipeline are those of gemm_bf16_dma_kernel
+// (64-wide slices, 2 stages, swizzled direct-to-LDS loads). N must be a
+// multiple of 128; outputs and residual of fewer than 2^31 bytes.
+constexpr int kPersistWgPerCu = 2;
+
+template <int EPI>
+__global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2, 2))) void
+gemm_bf16_persist_kernel(const bf16_t* __restrict__ X, const bf16_t* __restrict__ W, int M, int N,
+                         int K, EpiParams ep) {
+  constexpr int BM = 128, BN = 128, KB = 64, NW = 4, WN = 2;
+  constexpr int WTM = 64, WTN = 64, TM = 2, TN = 2;
+  using SL = Slice<KB>;
+  constexpr int AI = BM / SL::RPD / NW, BI = BN / SL::RPD / NW;
+  constexpr int SB = (BM + BN) * SL::RB;
+  constexpr int KS = KB / 16;
+  constexpr int NSTORE = TM * TN * 4;  // buffer stores per wave per tile
+  extern __shared__ __align__(16) unsigned char smem[];
+  const int tid = threadIdx.x;
+  const int lane = tid & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+  const int wm = wave / WN, wn = wave % WN;
+  const int l32 = lane & 31, half = lane >> 5;
+
+  const int nM = (M + BM - 1) / BM, nN = N / BN;
+  const int tiles = nM * nN;
+  const int xcd = blockIdx.x % kXcds, slot = blockIdx.x / kXcds;
+  const int slots = gridDim.x / kXcds;
+  const int per = tiles / kXcds, extra = tiles % kXcds;
+  const int tbeg = xcd * per + min(xcd, extra);
+  const int tcount = per + (xcd < extra ? 1 : 0);
+  int k = slot;
+  if (k >= tcount) return;
+  auto tile_at = [&](int t, int* m0, int* n0) {
+    const int g = t / (kXcdGroup * nN);
+    const int gm0 = g * kXcdGroup;
+    const int gsz = min(kXcdGroup, nM - gm0);
+    const int r = t - g * kXcdGroup * nN;
+    *n0 = (r / gsz) * BN;
+    *m0 = (gm0 + r % gsz) * BM;
+  };
+  const int KTOT = K / KB;
+
+  const int lr = lane / SL::CPR, lp = lane % SL::CPR;
+  const bf16_t* asrc[AI];
+  const bf16_t* bsrc[BI];
+  auto set_sources = [&](int m0, int n0) {
+#pragma unroll
+    for (int i = 0; i < AI; ++i) {
+      const int r = (i * NW + wave) * SL::RPD + lr;
+      asrc[i] = X + static_cast<int64_t>(min(m0 + r, M - 1)) * K + swz<KB>(r, lp) * 8;
+    }
+#pragma unroll
+    for (int i = 0; i < BI; ++i) {
+      const int r = (i * NW + wave) * SL::RPD + lr;
+      bsrc[i] = W + static_cast<int64_t>(n0 + r) * K + swz<KB>(r, lp) * 8;
+    }
+  };
+  typedef __attribute__((address_space(3))) void lds_void;
+#if defined(__HIP_DEVICE_COMPILE__)
+#define ZSA_DMA1(src, dst) __builtin_amdgcn_global_load_lds((src), (lds_void*)(dst), 16, 0, 0)
+#else
+#define ZSA_DMA1(src, dst) ((void)(src), (void)(dst))
+#endif
+#define ZSA_DMA(s, k0)                                                                   \
+  _Pragma("unroll") for (int i = 0; i < AI; ++i)                                         \
+    ZSA_DMA1(asrc[i] + (k0), smem + (s) * SB + (i * NW + wave) * 1024);                  \
+  _Pragma("unroll") for (int i = 0; i < BI; ++i)                                         \
+    ZSA_DMA1(bsrc[i] + (k0), smem + (s) * SB + BM * SL::RB + (i * NW + wave) * 1024);
+
+  int aoff[TM][KS], boff[TN][KS];
+#pragma unroll
+  for (int i = 0; i < TM; ++i) {
+    const int r = wm * WTM + i * 32 + l32;
+#pragma unroll
+    for (int kk = 0; kk < KS; ++kk) aoff[i][kk] = r * SL::RB + swz<KB>(r, kk * 2 + half) * 16;
+  }
+#pragma unroll
+  for (int j = 0; j < TN; ++j) {
+    const int r = wn * WTN + j * 32 + l32;
+#pragma unroll
+    for (int kk = 0; kk < KS; ++kk)
+      boff[j][kk] = BM * SL::RB + r * SL::RB + swz<KB>(r, kk * 2 + half) * 16;
+  }
+
+  const int ybytes = M * ep.ldy * 2;
+  const __amdgpu_buffer_rsrc_t yres = __builtin_amdgcn_make_buffer_rsrc(ep.y, 0, ybytes, 0x00020000);
+  const __amdgpu_buffer_rsrc_t rres = __builtin_amdgcn_make_buffer_rsrc(
+      const_cast<void*>(EPI == EPI_RESIDUAL ? ep.residual : ep.y), 0, ybytes, 0x00020000);
+  const bf16_t* bias = static_cast<const bf16_t*>(ep.bias);
+
+  int m0, n0;
+  tile_at(tbeg + k, &m0, &n0);
+  set_sources(m0, n0);
+  ZSA_DMA(0, 0)
+  asm volatile("" ::: "memory");
+  __builtin_amdgcn_s_waitcnt(vmcnt_imm(0));
+  barrier_lds();
+  // Every wait below is straight-line code with a fixed count of younger
+  // vector memory operations, so the compiler's own waits agree with it:
+  // at the top of a tile slice 0 is in LDS and published.
+  while (true) {
+    f32x16_t acc[TM][TN];
+#pragma unroll
+    for (int i = 0; i < TM; ++i)
+#pragma unroll
+      for (int j = 0; j < TN; ++j)
+#pragma unroll
+        for (int r = 0; r < 16; ++r) acc[i][j][r] = 0.f;
+    uint32_t res[TM][TN][4][2];
+    uint2 bw[TN][4];
+#pragma unroll
+    for (int j = 0; j < TN; ++j)
+#pragma unroll
+      for (int g = 0; g < 4; ++g) bw[j][g] = make_uint2(0u, 0u);
+
+    // the work of K step T on stage S once slice T is published: start slice
+    // T + 1 into the other stage; one step before the last (in the only step
+    // when K is one slice) fetch the epilogue's bias and residual, which the
+    // last step's wait then covers; then the MFMAs
+#define ZSA_PBODY(S, T)                                                                  \
+  {                                                                                      \
+    if ((T) + 1 < KTOT) {                                                                \
+      ZSA_DMA(((S) + 1) & 1, ((T) + 1) * KB)                                             \
+    }                                                                                    \
+    if ((T) + 2 == KTOT || KTOT == 1) {                                                  \
+      if (bias != nullptr) {                                                             \
+        _Pragma("unroll") for (int j = 0; j < TN; ++j)                                   \
+          _Pragma("unroll") for (int g = 0; g < 4; ++g)                                  \
+            bw[j][g] = *reinterpret_cast<const uint2*>(                                  \
+                bias + n0 + wn * WTN + j * 32 + g * 8 + half * 4);                       \
+      }                                                                                  \
+      if (EPI == EPI_RESIDUAL) {                                                         \
+        _Pragma("unroll") for (int i = 0; i < TM; ++i)                                   \
+          _Pragma("unroll") for (int j = 0; j < TN; ++j)                                 \
+            _Pragma("unroll") for (int g = 0; g < 4; ++g) {                              \
+              const int m = m0 + wm * WTM + i * 32 + l32;                                \
+              const int n = n0 + wn * WTN + j * 32 + g * 8 + half * 4;                   \
+              const auto v = __builtin_amdgcn_raw_buffer_load_b64(                       \
+                  rres, (static_cast<uint32_t>(m) * ep.ldy + n) * 2u, 0, 0);             \
+              res[i][j][g][0] = v[0];                                                    \
+              res[i][j][g][1] = v[1];                                                    \
+            }                                                                            \
+      }                                                                                  \
+    }                                                                                    \
+    const unsigned char* st = smem + (S) * SB;                                           \
+    bf16x8_t a[2][TM], b[2][TN];                                                         \
+    _Pragma("unroll") for (int i = 0; i < TM; ++i)                                       \
+      a[0][i] = __builtin_bit_cast(bf16x8_t, *reinterpret_cast<const u32x4*>(st + aoff[i][0])); \
+    _Pragma("unroll") for (int j = 0; j < TN; ++j)                                       \
+      b[0][j] = __builtin_bit_cast(bf16x8_t, *reinterpret_cast<const u32x4*>(st + boff[j][0])); \
+    _Pragma("unroll") for (int kk = 0; kk < KS; ++kk) {                                  \
+      const int cur = kk & 1, nxt = cur ^ 1;                                             \
+      if (kk + 1 < KS) {                                                                 \
+        _Pragma("unroll") for (int i = 0; i < TM; ++i)                                   \
+          a[nxt][i] = __builtin_bit_cast(bf16x8_t, *reinterpret_cast<const u32x4*>(st + aoff[i][kk + 1])); \
+        _Pragma("unroll") for (int j = 0; j < TN; ++j)                                   \
+          b[nxt][j] = __builtin_bit_cast(bf16x8_t, *reinterpret_cast<const u32x4*>(st + boff[j][kk + 1])); \
+      }                                                                                  \
+      __builtin_amdgcn_sched_barrier(0);                                                 \
+      _Pragma("unroll") for (int i = 0; i < TM; ++i)                                     \
+        _Pragma("unroll") for (int j = 0; j < TN; ++j)                                   \
+          acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(b[cur][j], a[cur][i], acc[i][j], 0, 0, 0); \
+      __builtin_amdgcn_sched_barrier(0);                                                 \
+    }                                                                                    \
+  }
+    // K steps after the first: slice T is the only operation in flight
+#define ZSA_PSTEP(S, T)                                                                  \
+  {                                                                                      \
+    asm volatile("" ::: "memory");                                                       \
+    __builtin_amdgcn_s_waitcnt(vmcnt_imm(0));                                            \
+    barrier_lds();                                                                       \
+    ZSA_PBODY(S, T)                                                                      \
+  }
+
+    ZSA_PBODY(0, 0)
+    int kt = 1;
+    for (; kt + 2 <= KTOT; kt += 2) {
+      ZSA_PSTEP(1, kt)
+      ZSA_PSTEP(0, kt + 1)
+    }
+    if (kt < KTOT) ZSA_PSTEP(1, kt)
+#undef ZSA_PSTEP
+#undef ZSA_PBODY
+
+    // every wave is done reading the stages and nothing is in flight: put
+    // the next tile's first slice in flight before this tile's epilogue
+    const int knext = k + slots;
+    const bool more = knext < tcount;
+    int m0n = m0, n0n = n0;
+    asm volatile("" ::: "memory");
+    __builtin_amdgcn_s_waitcnt(vmcnt_imm(0));
+    barrier_lds();
+    if (more) {
+      tile_at(tbeg + knext, &m0n, &n0n);
+      set_sources(m0n, n0n);
+      ZSA_DMA(0, 0)
+    }
+#pragma unroll
+    for (int i = 0; i < TM; ++i)
+#pragma unroll
+      for (int j = 0; j < TN; ++j)
+#pragma unroll
+        for (int g = 0; g < 4; ++g) {
+          const int m = m0 + wm * WTM + i * 32 + l32;
+          const int n = n0 + wn * WTN + j * 32 + g * 8 + half * 4;
+          float z[4];
+          z[0] = acc[i][j][4 * g + 0] + __uint_as_float(bw[j][g].x << 16);
+          z[1] = acc[i][j][4 * g + 1] + __uint_as_float(bw[j][g].x & 0xffff0000u);
+          z[2] = acc[i][j][4 * g + 2] + __uint_as_float(bw[j][g].y << 16);
+          z[3] = acc[i][j][4 * g + 3] + __uint_as_float(bw[j][g].y & 0xffff0000u);
+          if (EPI == EPI_GELU) {
+#pragma unroll
+            for (int e = 0; e < 4; ++e) z[e] = gelu_erf(z[e]);
+          } else if (EPI == EPI_RESIDUAL) {
+            z[0] += __uint_as_float(res[i][j][g][0] << 16);
+            z[1] += __uint_as_float(res[i][j][g][0] & 0xffff0000u);
+            z[2] += __uint_as_float(res[i][j][g][1] << 16);
+            z[3] += __uint_as_float(res[i][j][g][1] & 0xffff0000u);
+          }
+          typedef uint32_t u32x2 __attribute__((ext_vector_type(2)));
+          const u32x2 v = {pack_bf16x2(z[0], z[1]), pack_bf16x2(z[2], z[3])};
+          __builtin_amdgcn_raw_buffer_store_b64(v, yres, (static_cast<uint32_t>(m) * ep.ldy + n) * 2u, 0, 0);
+        }
+    if (!more) break;
+    k = knext;
+    m0 = m0n;
+    n0 = n0n;
+    // the next tile's slice 0 (and this tile's stores) have completed
+    asm volatile("" ::: "memory");
+    __builtin_amdgcn_s_waitcnt(vmcnt_imm(0));
+    barrier_lds();
+  }
+#undef ZSA_DMA
+#undef ZSA_DMA1
+}
+
+
+// CUs of the current device (cached per device)
+int device_cus() {
+  static int cus[64] = {0};
+  int dev = 0;
+  if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= 64) return 256;
+  if (cus[dev] == 0) {
+    int n = 0;
+    if (hipDeviceGetAttribute(&n, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess || n <= 0)
+      n = 256;
+    cus[dev] = n;
+  }
+  return cus[dev];
+}
+
+// the persistent kernel takes bf16 products with N a multiple of 128, K a
+// multiple of 64, no rotary / SwiGLU epilogue, and buffers below 2^31 bytes
+bool persist_ok(int M, int N, int K, const EpiParams& ep) {
+  if (N % 128 != 0 || K % 64 != 0 || K < 64 || M <= 0) return false;
+  if (reinterpret_cast<uintptr_t>(ep.bias) % 8 != 0 || ep.ldy % 4 != 0) return false;
+  if (ep.epi != EPI_NONE && ep.epi != EPI_GELU && ep.epi != EPI_RESIDUAL) return false;
+  return static_cast<int64_t>(M + 128) * ep.ldy * 2 < (int64_t{1} << 31);
+}
+
+template <int EPI>
+hipError_t launch_persist(hipStream_t s, const void* x, int M, int K, const void* w, int N,
+                          const EpiParams& ep) {
+  constexpr int lds = 2 * (128 + 128) * 128;
+  static bool lds_raised = false;
+  if (!lds_raised) {
+    const hipError_t e = hipFuncSetAttribute(
+        reinterpret_cast<const void*>(gemm_bf16_persist_kernel<EPI>),
+        hipFuncAttributeMaxDynamicSharedMemorySize, lds);
+    if (e != hipSuccess) return e;
+    lds_raised = true;
+  }
+  const int tiles = ((M + 127) / 128) * (N / 128);
+  const int wgs = std::min(tiles, device_cus() * kPersistWgPerCu);
+  const int grid = kXcds * ((wgs + kXcds - 1) / kXcds);
+  return launch(K_GEMM, gemm_bf16_persist_kernel<EPI>, dim3(grid), dim3(256), lds, s,
+                static_cast<const bf16_t*>(x), static_cast<const bf16_t*>(w), M, N, K, ep);
+}
+
+// ---------------------------------------------------------------------------
+// bf16 GEMM, 8-wave ping-pong over BM x BN tiles, epilogue in registers
+// ---------------------------------------------------------------------------
+// Waves 0-3 (group 0) own the tile's upper BM/2 rows, waves 4-7 (group 1)
+// the lower ones; wave q of a group owns columns q*BN/4 .. +BN/4, and waves
+// q and q + 4 share a SIMD. K is walked in slices of 32: per slice a wave
+// has, per unit of 32, an R phase (read the unit's operand fragments from
+// LDS into registers) and a C phase (its MFMAs). Both groups run the same code with
+// a barrier after each phase, but group 1 passes one extra barrier first:
+// it runs one phase behind, so in every phase one wave of each SIMD issues
+// MFMAs while the other reads LDS, and the MFMA unit does not wait on LDS
+// reads or barriers. (The LDS traffic of the 128 x 64 per-wave tiles --
+// fragment reads plus the stage fills -- is close to what the LDS delivers
+// at the full MFMA rate, which bounds this design.)
+//
+// K slices of KB (32 or 64, one or two units of 32) live in a ring of NS
+// stages filled by buffer loads straight into
+// LDS (each wave loads 1/8 of a stage; the buffer range check turns rows
+// past M into zeros, whose outputs are dropped), in the swizzled layout of
+// gemm_bf16_dma_kernel. At the R phase of a slice's first unit a wave
+// starts its share of slice t + NS - 1, into the stage slice t - 1 used
+// (both groups have read it by then: group 1 one phase after group 0), and
+// at the R phase of the slice's last unit it waits for its share of slice
+// t + 1; group 1 does so one phase later, still before group 0 reads slice
+// t + 1. NS - 1 slices are in flight per wave.
+template <int BM, int BN, int KB, int NS, int EPI>
+__global__ __launch_bounds__(512) __attribute__((amdgpu_waves_per_eu(2, 2))) void
+gemm_bf16_pp_kernel(const bf16_t* __restrict__ X, const bf16_t* __restrict__ W, int M, int N,
+                    int K, EpiParams ep) {
+  using SL = Slice<KB>;
+  constexpr int UPS = KB / 32;                           // 32-wide units per slice
+  constexpr int WTM = BM / 2, WTN = BN / 4;
+  constexpr int TM = WTM / 32, TN = WTN / 32;
+  constexpr int SB = (BM + BN) * SL::RB;                 // bytes per stage
+  constexpr int LPW = (BM + BN) / SL::RPD / 8;           // 1 KiB loads per wave per stage
+  constexpr int ALD = BM / SL::RPD / 8;                  // of which A rows
+  static_assert(TM >= 1 && TN >= 1 && LPW * 8 * SL::RPD == BM + BN && ALD * 8 * SL::RPD == BM,
+                "tile shape");
+  static_assert((KB == 32 || KB == 64) && NS >= 2 && (NS - 2) * LPW < 64, "pipeline");
+  extern __shared__ __align__(16) unsigned char smem[];
+  const int tid = threadIdx.x;
+  const int lane = tid & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+  const int grp = wave >> 2, q = wave & 3;
+  const int l32 = lane & 31, half = lane >> 5;
+  int mt, nt;
+  if (!xcd_tile<BM, BN>(M, N, &mt, &nt)) return;
+  const int m0 = mt * BM, n0 = nt * BN;
+  const int KT = K / KB;
+
+  // loads: wave w moves row blocks (i * 8 + w) of the stage, RPD rows each;
+  // stage row r = RPD blk + lr has swizzle (r / RPP) & (CPR - 1), with
+  // RPD / RPP = 4: it depends on blk only through the wave's parity (for
+  // 64-wide slices; not at all for 32-wide ones; the B rows start at an even
+  // block), so the lane's byte offset is common to every block
+  const __amdgpu_buffer_rsrc_t xres =
+      __builtin_amdgcn_make_buffer_rsrc(const_cast<bf16_t*>(X), 0, M * K * 2, 0x00020000);
+  const __amdgpu_buffer_rsrc_t wres =
+      __builtin_amdgcn_make_buffer_rsrc(const_cast<bf16_t*>(W), 0, N * K * 2, 0x00020000);
+  const int lr = lane / SL::CPR, lp = lane % SL::CPR;
+  const uint32_t lane_off =
+      static_cast<uint32_t>(lr * K * 2 + swz<KB>((wave & 1) * SL::RPD + lr, lp) * 16);
+  typedef __attribute__((address_space(3))) void lds_void;
+  auto dma = [&](int s, int t) {
+#pragma unroll
+    for (int i = 0; i < LPW; ++i) {
+      const int blk = i * 8 + wave;
+      const uint32_t row0 = i < ALD ? static_cast<uint32_t>(m0 + blk * SL::RPD)
+                                    : static_cast<uint32_t>(n0 + blk * SL::RPD - BM);
+      const uint32_t off = (row0 * K + t * KB) * 2u + lane_off;
+      __builtin_amdgcn_raw_ptr_buffer_load_lds(i < ALD ? xres : wres,
+                                               (lds_void*)(smem + s * SB + blk * 1024), 16, off,
+                                               0, 0, 0);
+    }
+  };
+  // fragment addresses: row r (the lane's row of a 32-row block) and chunk
+  // c = 2 kk + half sit at r * RB + (c ^ ((r / RPP) & (CPR - 1))) * 16; the
+  // XOR term is (l32 / RPP) & (CPR - 1) for every block of the lane
+  const int sw = (l32 / SL::RPP) & (SL::CPR - 1);
+  int ab[KB / 16], bb[KB / 16];
+#pragma unroll
+  for (int kk = 0; kk < KB / 16; ++kk) {
+    const int ck = ((kk * 2 + half) ^ sw) * 16;
+    ab[kk] = (grp * WTM + l32) * SL::RB + ck;
+    bb[kk] = BM * SL::RB + (q * WTN + l32) * SL::RB + ck;
+  }
+  f32x16_t acc[TM][TN];
+#pragma unroll
+  for (int i = 0; i < TM; ++i)
+#pragma unroll
+    for (int j = 0; j < TN; ++j)
+#pragma unroll
+      for (int r = 0; r < 16; ++r) acc[i][j][r] = 0.f;
+  bf16x8_t fa[2][TM], fb[2][TN];
+
+  // prologue: slices 0 .. NS - 2 in flight, slice 0 landed and published
+  const int pre = min(NS - 1, KT);
+  for (int t = 0; t < pre; ++t) dma(t, t);
+  asm volatile("" ::: "memory");
+  if (pre == NS - 1)
+    __builtin_amdgcn_s_waitcnt(vmcnt_imm((NS - 2) * LPW));
+  else
+    __builtin_amdgcn_s_waitcnt(vmcnt_imm(0));
+  barrier_lds();
+  if (grp == 1) barrier_lds();
+  int s = 0;  // stage of slice t
+  for (int t = 0; t < KT; ++t) {
+    const int tn = t + NS - 1;
+#pragma unroll
+    for (int h = 0; h < UPS; ++h) {
+      // R phase of unit h of slice t
+      if (h == 0 && tn < KT) dma(s == 0 ? NS - 1 : s - 1, tn);
+      {
+        const unsigned char* st = smem + s * SB;
+#pragma unroll
+        for (int kk = 0; kk < 2; ++kk) {
+#pragma unroll
+          for (int i = 0; i < TM; ++i)
+            fa[kk][i] = __builtin_bit_cast(
+                bf16x8_t, *reinterpret_cast<const u32x4*>(st + ab[2 * h + kk] + i * 32 * SL::RB));
+#pragma unroll
+          for (int j = 0; j < TN; ++j)
+            fb[kk][j] = __builtin_bit_cast(
+                bf16x8_t, *reinterpret_cast<const u32x4*>(st + bb[2 * h + kk] + j * 32 * SL::RB));
+        }
+      }
+      if (h == UPS - 1) {
+        // this wave's share of slice t + 1 has landed (the slices after it
+        // that were issued may still be in flight)
+        asm volatile("" ::: "memory");
+        if (tn < KT)
+          __builtin_amdgcn_s_waitcnt(vmcnt_imm((NS - 2) * LPW));
+        else
+          __builtin_amdgcn_s_waitcnt(vmcnt_imm(0));
+      }
+      barrier_lds();
+      // C phase
+#pragma unroll
+      for (int kk = 0; kk < 2; ++kk)
+#pragma unroll
+        for (int i = 0; i < TM; ++i)
+#pragma unroll
+          for (int j = 0; j < TN; ++j)
+            acc[i][j] =
+                __builtin_amdgcn_mfma_f32_32x32x16_bf16(fb[kk][j], fa[kk][i], acc[i][j], 0, 0, 0);
+      barrier_lds();
+    }
+    s = s + 1 == NS ? 0 : s + 1;
+  }
+
+  // epilogue: acc[i][j][4g + e] = C[m][n + e], m = m0 + grp*WTM + 32 i + l32,
+  // n = n0 + q*WTN + 32 j + 8 g + 4 half
+  const int ybytes = M * ep.ldy * 2;
+  const __amdgpu_buffer_rsrc_t yres = __builtin_amdgcn_make_buffer_rsrc(ep.y, 0, ybytes, 0x00020000);
+  const bf16_t* bias = static_cast<const bf16_t*>(ep.bias);
+  uint2 bw[TN][4];
+#pragma unroll
+  for (int j = 0; j < TN; ++j)
+#pragma unroll
+    for (int g = 0; g < 4; ++g)
+      bw[j][g] = bias != nullptr
+                     ? *reinterpret_cast<const uint2*>(bias + n0 + q * WTN + j * 32 + g * 8 + half * 4)
+                     : make_uint2(0u, 0u);
+#pragma unroll
+  for (int i = 0; i < TM; ++i) {
+    uint32_t res[TN][4][2];
+    if (EPI == EPI_RESIDUAL) {
+      const __amdgpu_buffer_rsrc_t rres =
+          __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(ep.residual), 0, ybytes, 0x00020000);
+#pragma unroll
+      for (int j = 0; j < TN; ++j)
+#pragma unroll
+        for (int g = 0; g < 4; ++g) {
+          const int m = m0 + grp * WTM + i * 32 + l32;
+          const int n = n0 + q * WTN + j * 32 + g * 8 + half * 4;
+          const auto v = __builtin_amdgcn_raw_buffer_load_b64(
+              rres, (static_cast<uint32_t>(m) * ep.ldy + n) * 2u, 0, 0);
+          res[j][g][0] = v[0];
+          res[j][g][1] = v[1];
+        }
+    }
+#pragma unroll
+    for (int j = 0; j < TN; ++j)
+#pragma unroll
+      for (int g = 0; g < 4; ++g) {
+        const int m = m0 + grp * WTM + i * 32 + l32;
+        const int n = n0 + q * WTN + j * 32 + g * 8 + half * 4;
+        float z[4];
+        z[0] = acc[i][j][4 * g + 0] + __uint_as_float(bw[j][g].x << 16);
+        z[1] = acc[i][j][4 * g + 1] + __uint_as_float(bw[j][g].x & 0xffff0000u);
+        z[2] = acc[i][j][4 * g + 2] + __uint_as_float(bw[j][g].y << 16);
+        z[3] = acc[i][j][4 * g + 3] + __uint_as_float(bw[j][g].y & 0xffff0000u);
+        if (EPI == EPI_GELU) {
+#pragma unroll
+          for (int e = 0; e < 4; ++e) z[e] = gelu_erf(z[e]);
+        } else if (EPI == EPI_RESIDUAL) {
+          z[0] += __uint_as_float(res[j][g][0] << 16);
+          z[1] += __uint_as_float(res[j][g][0] & 0xffff0000u);
+          z[2] += __uint_as_float(res[j][g][1] << 16);
+          z[3] += __uint_as_float(res[j][g][1] & 0xffff0000u);
+        }
+        typedef uint32_t u32x2 __attribute__((ext_vector_type(2)));
+        const u32x2 v = {pack_bf16x2(z[0], z[1]), pack_bf16x2(z[2], z[3])};
+        __builtin_amdgcn_raw_buffer_store_b64(v, yres, (static_cast<uint32_t>(m) * ep.ldy + n) * 2u,
+                                              0, 0);
+      }
+  }
+  // group 0 passes its last barrier here, matching group 1's first one
+  if (grp == 0) barrier_lds();
+}
+
+template <int BM, int BN, int KB, int NS, int EPI>
+hipError_t launch_pp1(hipStream_t s, const void* x, int M, int K, const void* w, int N,
+                      const EpiParams& ep) {
+  constexpr int lds = NS * (BM + BN) * KB * 2;
+  static bool lds_raised = false;
+  if (!lds_raised) {
+    const hipError_t e = hipFuncSetAttribute(
+        reinterpret_cast<const void*>(gemm_bf16_pp_kernel<BM, BN, KB, NS, EPI>),
+        hipFuncAttributeMaxDynamicSharedMemorySize, lds);
+    if (e != hipSuccess) return e;
+    lds_raised = true;
+  }
+  return launch(K_GEMM, gemm_bf16_pp_kernel<BM, BN, KB, NS, EPI>, xcd_grid(M, N, BM, BN),
+                dim3(512), lds, s, static_cast<const bf16_t*>(x), static_cast<const bf16_t*>(w),
+                M, N, K, ep);
+}
+
+// the ping-pong kernel takes the products the persistent one takes, with N a
+// multiple of BN and both operands below 2^31 bytes (buffer range checks)
+bool pp_ok(int M, int N, int K, const EpiParams& ep, int BN) {
+  return persist_ok(M, N, K, ep) && N % BN == 0 &&
+         static_cast<int64_t>(M + 256) * K * 2 < (int64_t{1} << 31) &&
+         static_cast<int64_t>(N) * K * 2 < (int64_t{1} << 31);
+}
+
+template <int BM, int BN, int KB, int NS>
+hipError_t launch_pp(hipStream_t s, const void* x, int M, int K, const void* w, int N,
+                     const EpiParams& ep) {
+  if (ep.epi == EPI_GELU) return launch_pp1<BM, BN, KB, NS, EPI_GELU>(s, x, M, K, w, N, ep);
+  if (ep.epi == EPI_RESIDUAL)
+    return launch_pp1<BM, BN, KB, NS, EPI_RESIDUAL>(s, x, M, K, w, N, ep);
+  return launch_pp1<BM, BN, KB, NS, EPI_NONE>(s, x, M, K, w, N, ep);
+}
+
+hipError_t launch_persist_any(hipStream_t s, const void* x, int M, int K, const void* w, int N,
+                              const EpiParams& ep) {
+  if (ep.epi == EPI_GELU) return launch_persist<EPI_GELU>(s, x, M, K, w, N, ep);
+  if (ep.epi == EPI_RESIDUAL) return launch_persist<EPI_RESIDUAL>(s, x, M, K, w, N, ep);
+  return launch_persist<EPI_NONE>(s, x, M, K, w, N, ep);
+}
+
 template <int BM, int BN, int WM, int WN>
 hipError_t launch_mfma(hipStream_t s, const void* x, int M, int K, const void* w, int N,
                        const EpiParams& ep) {
@@ -833,11 +1394,36 @@ hipError_t launch_gemm(hipStream_t s, int dtype, const void* x, int M, int K, co
       case 3241: return launch_dma<128, 128, 2, 2, 32, 4, 64>(s, x, M, K, w, N, ep);
       case 6431: return launch_dma<128, 128, 2, 2, 64, 3, 64>(s, x, M, K, w, N, ep);
       case 2542: return launch_dma<256, 256, 2, 2, 64, 2, 64>(s, x, M, K, w, N, ep);
+      case 1289:
+        if (persist_ok(M, N, K, ep)) return launch_persist_any(s, x, M, K, w, N, ep);
+        break;
+      case 2589:
+        if (pp_ok(M, N, K, ep, 256)) return launch_pp<256, 256, 64, 2>(s, x, M, K, w, N, ep);
+        break;
+      case 2584:
+        if (pp_ok(M, N, K, ep, 256)) return launch_pp<256, 256, 32, 4>(s, x, M, K, w, N, ep);
+        break;
+      case 1259:
+        if (pp_ok(M, N, K, ep, 256)) return launch_pp<128, 256, 64, 2>(s, x, M, K, w, N, ep);
+        break;
+      case 1256:
+        if (pp_ok(M, N, K, ep, 256)) return launch_pp<128, 256, 32, 6>(s, x, M, K, w, N, ep);
+        break;
       default: break;
     }
-    // Measured on the projection shapes: direct-to-LDS 256x256 tiles over 8
-    // waves (128x64 per wave) win once the grid holds at least four rounds of
-    // such tiles; below that, direct-to-LDS 128x128 tiles over 4 waves.
+    // Measured on the projection shapes of the 768-wide stacks (N = 768,
+    // 2304, 3072; K = 768, 3072; M = 2048 .. 16384): with M >= 12288 the
+    // ping-pong 256x256 tiles win for the GELU and residual projections; up
+    // to 1536 tiles of 128x128 the persistent kernel wins; the largest
+    // grids without an epilogue op keep the 128x128 kernel. For longer K
+    // (the 4096-wide decoder): direct-to-LDS 256x256 tiles over 8 waves
+    // (128x64 per wave) once the grid holds at least four rounds of them.
+    const long tiles128 = static_cast<long>((M + 127) / 128) * ((N + 127) / 128);
+    if (K <= 3072 && persist_ok(M, N, K, ep)) {
+      if (M >= 12288 && ep.epi != EPI_NONE && pp_ok(M, N, K, ep, 256))
+        return launch_pp<256, 256, 64, 2>(s, x, M, K, w, N, ep);
+      if (tiles128 <= 1536) return launch_persist_any(s, x, M, K, w, N, ep);
+    }
     const long tiles256 = static_cast<long>((M + 255) / 256) * ((N + 255) / 256);
     if (tiles256 >= 1024) return launch_dma<256, 256, 2, 4, 64, 2, 128>(s, x, M, K, w, N, ep);
     return launch_dma<128, 128, 2, 2, 64, 2, 128>(s, x, M, K, w, N, ep);

@@ -185,6 +185,40 @@ def test_linear_split_k(m, n, k, epi):
     assert_close(f64(y0), ref, 1e-2, f"unsplit epilogue {epi}")
 
 
+@pytest.mark.parametrize("m,n,k,split", [(12289, 3072, 768, False),   # ping-pong 256x256 tiles
+                                         (12289, 768, 3072, False),
+                                         (1000, 768, 768, False),     # persistent 128x128
+                                         (4000, 768, 3072, False),
+                                         (16385, 2304, 768, False)])  # 128x128, largest grids
+@pytest.mark.parametrize("epi", [zsa.EPI_NONE, zsa.EPI_GELU, zsa.EPI_RESIDUAL])
+@pytest.mark.parametrize("with_bias", [True, False])
+def test_linear_kernel_regimes(m, n, k, split, epi, with_bias):
+    """Every GEMM the projection shapes dispatch to (by grid size and
+    epilogue), with ragged row counts, against the oracle on sampled rows
+    (the first and last 64 and 128 drawn at random), and reproducible."""
+    g = np.random.default_rng(m + n + k + epi + int(with_bias))
+    x = g.standard_normal((m, k)).astype(np.float32)
+    w = (g.standard_normal((n, k)) / math.sqrt(k)).astype(np.float32)
+    xd, wd = to_dev(x, "bf16"), to_dev(w, "bf16")
+    bd = to_dev((0.1 * g.standard_normal(n)).astype(np.float32), "bf16") if with_bias else None
+    res = to_dev(g.standard_normal((m, n)).astype(np.float32), "bf16") if epi == zsa.EPI_RESIDUAL else None
+    y1 = zsa.linear(xd, wd, bd, epi, residual=res, split=split)
+    y2 = zsa.linear(xd, wd, bd, epi, residual=res, split=split)
+    torch.cuda.synchronize()
+    assert torch.equal(y1, y2)
+    rows = np.unique(np.concatenate([np.arange(64), np.arange(m - 64, m),
+                                     g.integers(0, m, 128)]))
+    rt = torch.from_numpy(rows).to(dev())
+    z = f64(xd[rt]) @ f64(wd).T
+    if bd is not None:
+        z = z + f64(bd)
+    if epi == zsa.EPI_GELU:
+        z = O.gelu(z)
+    elif epi == zsa.EPI_RESIDUAL:
+        z = z + f64(res[rt])
+    assert_close(f64(y1[rt]), z, 1e-2, f"regime {m}x{n}x{k} epilogue {epi}")
+
+
 def test_linear_in_place_residual():
     g = np.random.default_rng(8)
     m, k, n = 129, 128, 256
