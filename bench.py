@@ -58,6 +58,8 @@ def parse():
                     help="comma-separated presets whose keep-rate sweeps are reported beside "
                          "the headline workload")
     ap.add_argument("--no-graph", action="store_true", help="time eager launches instead")
+    ap.add_argument("--forward-only", action="store_true",
+                    help="skip the decode, backward and mark-mode legs (counter runs of the forward)")
     ap.add_argument("--cpu-seconds", type=float, default=15.0,
                     help="target wall time of the CPU-oracle sample (0 disables it)")
     ap.add_argument("--copy-calibration", type=int, default=0, metavar="BYTES",
@@ -338,7 +340,7 @@ def measure(p, rates, args, torch, W, zsa, dev, timing):
         ms = (time.perf_counter() - t0) * 1e3 / args.steps
         plan = stack.plan(seqs, p.prune_after, kr)
         r = {"ms": ms, "tok_s": tokens / (ms * 1e-3), "kept_rows_final": plan["final_rows"]}
-        if p.causal and p.force_keep_last:
+        if p.causal and p.force_keep_last and not args.forward_only:
             r["decode_ms"] = decode_ms(p, stack, xd, posd, seqs, kr, lens, outs, args, torch, dev)
         if timing:
             # per-class launch durations of one eager forward (HIP events on the stream)
@@ -351,16 +353,18 @@ def measure(p, rates, args, torch, W, zsa, dev, timing):
                 n, t = zsa.timing_read(c)
                 cls[name] = {"launches": n, "ms": t}
             rows_in, rows_after = layer_rows(p, plan)
-            if p.dtype == "bf16" and p.d_model // p.n_heads in (64, 128):
+            if p.dtype == "bf16" and p.d_model // p.n_heads in (64, 128) and not args.forward_only:
                 # the training step's backward (forward recomputed inside), as a graph
                 g = torch.Generator().manual_seed(args.seed)
                 dy = torch.randn(plan["final_rows"], p.d_model, generator=g).to(torch.bfloat16).to(dev)
                 stack.backward(xd, posd, seqs, p.prune_after, kr, dy)
                 r["backward_ms"] = graph_ms(
                     lambda: stack.backward(xd, posd, seqs, p.prune_after, kr, dy), args, torch)
-            mouts = mstack.forward(xd, posd, seqs, p.prune_after, kr)
-            r["mark_ms"] = graph_ms(
-                lambda: mstack.forward(xd, posd, seqs, p.prune_after, kr, out=mouts), args, torch)
+            if not args.forward_only:
+                mouts = mstack.forward(xd, posd, seqs, p.prune_after, kr)
+                r["mark_ms"] = graph_ms(
+                    lambda: mstack.forward(xd, posd, seqs, p.prune_after, kr, out=mouts), args,
+                    torch)
             r.update({"classes": cls, "gemm_flops": gemm_flops(p, rows_in, rows_after),
                       "rows": (rows_in, rows_after),
                       "work": class_work(p, lens, plan, rows_in, rows_after)})
