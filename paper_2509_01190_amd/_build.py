@@ -47,9 +47,23 @@ FLAGS = [
 ]
 
 
+# MFMA results in VGPRs rather than the compiler's default choice of
+# accumulation registers: the attention, score and backward kernels run
+# softmax and scaling VALU work on their accumulators, and in AGPRs every
+# such use costs a v_accvgpr read and write (and the register total grows).
+# The GEMM file keeps the default: its 128x128-per-wave tiles need the AGPRs.
+VGPR_MFMA = ["-mllvm", "-amdgpu-mfma-vgpr-form"]
+EXTRA_FLAGS = {
+    "k_attn.hip": VGPR_MFMA,
+    "k_score.hip": VGPR_MFMA,
+    "k_backward.hip": VGPR_MFMA,
+    "k_decode.hip": VGPR_MFMA,
+}
+
+
 def _compile(src: str) -> str:
     obj = os.path.join(BUILD_DIR, os.path.splitext(src)[0] + ".o")
-    cmd = [HIPCC, *FLAGS, "-c", os.path.join(CSRC, src), "-o", obj]
+    cmd = [HIPCC, *FLAGS, *EXTRA_FLAGS.get(src, []), "-c", os.path.join(CSRC, src), "-o", obj]
     res = subprocess.run(cmd, capture_output=True, text=True)
     out = "\n".join(
         line for line in (res.stdout + res.stderr).splitlines()

@@ -42,7 +42,10 @@ __global__ __launch_bounds__(256) void attn_mfma_kernel(
     bf16_t* __restrict__ O, int64_t os, float* __restrict__ lse, int T) {
   constexpr int BQ = 128, BKEY = 64;
   constexpr int KLD = HD + 8;    // K tile row stride (bf16)
-  constexpr int VLD = BKEY + 8;  // V^T tile row stride (bf16)
+  // V^T tile row stride (bf16): 33 dwords, odd, so the transposing writes of
+  // a wave (8 row pairs x 8 channel blocks) and the fragment reads (32
+  // consecutive rows) each hit distinct banks; reads are then 4-byte aligned
+  constexpr int VLD = BKEY + 2;
   constexpr int OLD = HD + 8;    // output staging row stride
   constexpr int KBYTES = BKEY * KLD * 2, VBYTES = HD * VLD * 2;
   constexpr int BUF = KBYTES + VBYTES;
@@ -73,27 +76,41 @@ __global__ __launch_bounds__(256) void attn_mfma_kernel(
 
   // K/V tiles of the next key block are prefetched into registers while the
   // current block is computed; LDS is double-buffered, one barrier per block.
-  // Keys past the sequence repeat the last row: they are masked to
-  // probability 0 and the repeated V rows are finite.
+  // The loads go through a buffer resource spanning this sequence's rows,
+  // so keys past the sequence read as zeros (they are masked to probability
+  // 0); a thread's offsets within a tile are fixed, plus the tile's start.
   // grouped-query attention: query head h reads key/value head h / kv_group
   const int hk = h / kv_group;
-  const bf16_t* kbase = K + static_cast<int64_t>(lo) * rs + hk * HD;
-  const bf16_t* vbase = V + static_cast<int64_t>(lo) * rs + hk * HD;
+  const uint32_t seq_bytes = static_cast<uint32_t>(static_cast<int64_t>(n) * rs * 2);
+  const __amdgpu_buffer_rsrc_t kres = __builtin_amdgcn_make_buffer_rsrc(
+      const_cast<bf16_t*>(K + static_cast<int64_t>(lo) * rs + hk * HD), 0, seq_bytes, 0x00020000);
+  const __amdgpu_buffer_rsrc_t vres = __builtin_amdgcn_make_buffer_rsrc(
+      const_cast<bf16_t*>(V + static_cast<int64_t>(lo) * rs + hk * HD), 0, seq_bytes, 0x00020000);
+  uint32_t koff[KCH], voff[VPR];
+#pragma unroll
+  for (int i = 0; i < KCH; ++i) {
+    const int c = tid + i * 256;
+    koff[i] = static_cast<uint32_t>((c / (HD / 8)) * rs + (c % (HD / 8)) * 8) * 2u;
+  }
+#pragma unroll
+  for (int i = 0; i < VPR; ++i) {
+    const int c = tid + i * 256;
+    voff[i] = static_cast<uint32_t>((2 * (c / (HD / 8))) * rs + (c % (HD / 8)) * 8) * 2u;
+  }
+  const uint32_t row_bytes = static_cast<uint32_t>(rs * 2);
   u32x4 kreg[KCH], vreg[VPR][2];
   auto load_tile = [&](int j0) {
+    const uint32_t t0 = static_cast<uint32_t>(j0) * row_bytes;
+    // the whole offset goes in the vector operand, which the range check covers
 #pragma unroll
-    for (int i = 0; i < KCH; ++i) {
-      const int c = tid + i * 256;
-      const int r = c / (HD / 8), ch = (c % (HD / 8)) * 8;
-      kreg[i] = *reinterpret_cast<const u32x4*>(kbase + static_cast<int64_t>(min(j0 + r, n - 1)) * rs + ch);
-    }
+    for (int i = 0; i < KCH; ++i)
+      kreg[i] = __builtin_bit_cast(u32x4, __builtin_amdgcn_raw_buffer_load_b128(kres, koff[i] + t0, 0, 0));
 #pragma unroll
     for (int i = 0; i < VPR; ++i) {
-      const int c = tid + i * 256;
-      const int rp = c / (HD / 8), ch = (c % (HD / 8)) * 8;
-      const int jr = j0 + 2 * rp;
-      vreg[i][0] = *reinterpret_cast<const u32x4*>(vbase + static_cast<int64_t>(min(jr, n - 1)) * rs + ch);
-      vreg[i][1] = *reinterpret_cast<const u32x4*>(vbase + static_cast<int64_t>(min(jr + 1, n - 1)) * rs + ch);
+      vreg[i][0] = __builtin_bit_cast(
+          u32x4, __builtin_amdgcn_raw_buffer_load_b128(vres, voff[i] + t0, 0, 0));
+      vreg[i][1] = __builtin_bit_cast(
+          u32x4, __builtin_amdgcn_raw_buffer_load_b128(vres, voff[i] + t0 + row_bytes, 0, 0));
     }
   };
   auto store_tile = [&](int buf) {
@@ -187,10 +204,13 @@ __global__ __launch_bounds__(256) void attn_mfma_kernel(
       rsum += __shfl_xor(rsum, 32, 64);
       l_run = l_run * alpha + rsum;
       m_run = m_new;
+      // the accumulators change scale only when some lane's max moved
+      if (__builtin_amdgcn_ballot_w64(alpha != 1.0f) != 0) {
 #pragma unroll
-      for (int ct = 0; ct < HD / 32; ++ct)
+        for (int ct = 0; ct < HD / 32; ++ct)
 #pragma unroll
-        for (int r = 0; r < 16; ++r) o[ct][r] *= alpha;
+          for (int r = 0; r < 16; ++r) o[ct][r] *= alpha;
+      }
 #pragma unroll
       for (int g = 0; g < 4; ++g) {
         const int ks = g >> 1, rb = (g & 1) * 8;
@@ -200,10 +220,8 @@ __global__ __launch_bounds__(256) void attn_mfma_kernel(
         const int base = ks * 32 + (g & 1) * 16 + 4 * half;
 #pragma unroll
         for (int ct = 0; ct < HD / 32; ++ct) {
-          const bf16_t* vr = Vt + (ct * 32 + l32) * VLD + base;
-          const uint2 lo4 = *reinterpret_cast<const uint2*>(vr);
-          const uint2 hi4 = *reinterpret_cast<const uint2*>(vr + 8);
-          const u32x4 av = {lo4.x, lo4.y, hi4.x, hi4.y};
+          const uint32_t* vr = reinterpret_cast<const uint32_t*>(Vt + (ct * 32 + l32) * VLD + base);
+          const u32x4 av = {vr[0], vr[1], vr[4], vr[5]};
           o[ct] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(__builtin_bit_cast(bf16x8_t, av), pb, o[ct], 0, 0, 0);
         }
       }
