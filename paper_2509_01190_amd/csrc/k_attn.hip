@@ -42,10 +42,11 @@ __global__ __launch_bounds__(256) void attn_mfma_kernel(
     bf16_t* __restrict__ O, int64_t os, float* __restrict__ lse, int T) {
   constexpr int BQ = 128, BKEY = 64;
   constexpr int KLD = HD + 8;    // K tile row stride (bf16)
-  // V^T tile row stride (bf16): 33 dwords, odd, so the transposing writes of
-  // a wave (8 row pairs x 8 channel blocks) and the fragment reads (32
-  // consecutive rows) each hit distinct banks; reads are then 4-byte aligned
-  constexpr int VLD = BKEY + 2;
+  // V^T tile row stride (bf16): 34 dwords. The fragment reads (32
+  // consecutive rows, 8 bytes each) hit distinct bank pairs and stay 8-byte
+  // aligned, so they are ds_read_b64 with immediate offsets; the transposing
+  // writes of a wave (8 row pairs x 8 channel blocks) are at most 2-way.
+  constexpr int VLD = BKEY + 4;
   constexpr int OLD = HD + 8;    // output staging row stride
   constexpr int KBYTES = BKEY * KLD * 2, VBYTES = HD * VLD * 2;
   constexpr int BUF = KBYTES + VBYTES;
@@ -160,15 +161,14 @@ __global__ __launch_bounds__(256) void attn_mfma_kernel(
     const bf16_t* Vt = reinterpret_cast<const bf16_t*>(smem + buf * BUF + KBYTES);
     if (!causal || j0 <= wave_q0 + 31) {
       f32x16_t s[2];
+      const f32x16_t zero = {};
 #pragma unroll
       for (int ks = 0; ks < 2; ++ks) {
-#pragma unroll
-        for (int r = 0; r < 16; ++r) s[ks][r] = 0.f;
 #pragma unroll
         for (int kk = 0; kk < HD / 16; ++kk) {
           const bf16x8_t a = __builtin_bit_cast(
               bf16x8_t, *reinterpret_cast<const u32x4*>(Ks + (ks * 32 + l32) * KLD + kk * 16 + half * 8));
-          s[ks] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, qf[kk], s[ks], 0, 0, 0);
+          s[ks] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, qf[kk], kk == 0 ? zero : s[ks], 0, 0, 0);
         }
       }
       // s[ks][r]: query qrow, key j0 + 32 ks + 8 (r/4) + 4 half + r%4 (raw q.k)
@@ -187,7 +187,7 @@ __global__ __launch_bounds__(256) void attn_mfma_kernel(
       for (int ks = 0; ks < 2; ++ks)
 #pragma unroll
         for (int r = 0; r < 16; ++r) mloc = fmaxf(mloc, s[ks][r]);
-      mloc = fmaxf(mloc, __shfl_xor(mloc, 32, 64));
+      mloc = half_swap_max(mloc);
       const float m_new = fmaxf(m_run, mloc);
       // scale > 0, so the max of the scaled scores is the scaled max
       const float m_use = m_new == -INFINITY ? 0.f : m_new * scale_log2;
@@ -201,7 +201,7 @@ __global__ __launch_bounds__(256) void attn_mfma_kernel(
           s[ks][r] = p;
           rsum += p;
         }
-      rsum += __shfl_xor(rsum, 32, 64);
+      rsum = half_swap_sum(rsum);
       l_run = l_run * alpha + rsum;
       m_run = m_new;
       // the accumulators change scale only when some lane's max moved
@@ -220,8 +220,10 @@ __global__ __launch_bounds__(256) void attn_mfma_kernel(
         const int base = ks * 32 + (g & 1) * 16 + 4 * half;
 #pragma unroll
         for (int ct = 0; ct < HD / 32; ++ct) {
-          const uint32_t* vr = reinterpret_cast<const uint32_t*>(Vt + (ct * 32 + l32) * VLD + base);
-          const u32x4 av = {vr[0], vr[1], vr[4], vr[5]};
+          const bf16_t* vr = Vt + (ct * 32 + l32) * VLD + base;
+          const uint2 lo4 = *reinterpret_cast<const uint2*>(vr);
+          const uint2 hi4 = *reinterpret_cast<const uint2*>(vr + 8);
+          const u32x4 av = {lo4.x, lo4.y, hi4.x, hi4.y};
           o[ct] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(__builtin_bit_cast(bf16x8_t, av), pb, o[ct], 0, 0, 0);
         }
       }

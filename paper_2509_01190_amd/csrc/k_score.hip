@@ -140,7 +140,7 @@ __global__ __launch_bounds__(256) void score_mfma_kernel(
     }
   }
 #pragma unroll
-  for (int ks = 0; ks < 2; ++ks) colsum[ks] += __shfl_xor(colsum[ks], 32, 64);
+  for (int ks = 0; ks < 2; ++ks) colsum[ks] = half_swap_sum(colsum[ks]);
   if (half == 0) {
     red[wave][l32] = colsum[0];
     red[wave][32 + l32] = colsum[1];

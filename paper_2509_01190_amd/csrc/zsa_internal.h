@@ -30,6 +30,19 @@ __device__ __forceinline__ uint32_t pack_bf16x2(float lo, float hi) {
   const f32x2_t v = {lo, hi};
   return __builtin_bit_cast(uint32_t, __builtin_convertvector(v, bf16x2_t));
 }
+// the pair {x[l], x[l ^ 32]} of lane l in one VALU op (v_permlane32_swap:
+// the first result is x[l & 31], the second x[(l & 31) + 32] on every
+// lane), so combining the two gives the same value, in the same operand
+// order, on both halves of the wave -- without an LDS round trip
+__device__ __forceinline__ float half_swap_max(float x) {
+  const auto r = __builtin_amdgcn_permlane32_swap(__float_as_uint(x), __float_as_uint(x), false, false);
+  return fmaxf(__uint_as_float(r[0]), __uint_as_float(r[1]));
+}
+__device__ __forceinline__ float half_swap_sum(float x) {
+  const auto r = __builtin_amdgcn_permlane32_swap(__float_as_uint(x), __float_as_uint(x), false, false);
+  return __uint_as_float(r[0]) + __uint_as_float(r[1]);
+}
+
 __device__ __forceinline__ bf16_t f32_to_bf16(float f) {
   return static_cast<bf16_t>(pack_bf16x2(f, 0.f) & 0xffffu);
 }
