@@ -325,6 +325,68 @@ inline dim3 xcd_grid(int M, int N, int BM, int BN) {
   return dim3(static_cast<unsigned>(kXcds * ((tiles + kXcds - 1) / kXcds)));
 }
 
+// Epilogue from the accumulators of a wave whose block starts at row mb,
+// column nb: acc[i][j][4g + e] = C[m][n + e], m = mb + 32 i + l32,
+// n = nb + 32 j + 8 g + 4 half (the operand-swapped MFMA holds C^T); bias,
+// GELU or residual, then raw buffer stores, whose range check drops rows
+// past M. N is a multiple of the wave's column block.
+template <int TM, int TN, int EPI>
+__device__ __forceinline__ void reg_epilogue(const f32x16_t (&acc)[TM][TN], int mb, int nb, int M,
+                                             int l32, int half, const EpiParams& ep) {
+  const int ybytes = M * ep.ldy * 2;
+  const __amdgpu_buffer_rsrc_t yres = __builtin_amdgcn_make_buffer_rsrc(ep.y, 0, ybytes, 0x00020000);
+  const __amdgpu_buffer_rsrc_t rres = __builtin_amdgcn_make_buffer_rsrc(
+      const_cast<void*>(EPI == EPI_RESIDUAL ? ep.residual : ep.y), 0, ybytes, 0x00020000);
+  const bf16_t* bias = static_cast<const bf16_t*>(ep.bias);
+  // one 32 x 32 block at a time keeps the bias and residual registers few
+#pragma unroll
+  for (int j = 0; j < TN; ++j) {
+    uint2 bw[4];
+#pragma unroll
+    for (int g = 0; g < 4; ++g)
+      bw[g] = bias != nullptr
+                  ? *reinterpret_cast<const uint2*>(bias + nb + j * 32 + g * 8 + half * 4)
+                  : make_uint2(0u, 0u);
+#pragma unroll
+    for (int i = 0; i < TM; ++i) {
+      const int m = mb + i * 32 + l32;
+      uint32_t res[4][2];
+      if (EPI == EPI_RESIDUAL) {
+#pragma unroll
+        for (int g = 0; g < 4; ++g) {
+          const int n = nb + j * 32 + g * 8 + half * 4;
+          const auto v = __builtin_amdgcn_raw_buffer_load_b64(
+              rres, (static_cast<uint32_t>(m) * ep.ldy + n) * 2u, 0, 0);
+          res[g][0] = v[0];
+          res[g][1] = v[1];
+        }
+      }
+#pragma unroll
+      for (int g = 0; g < 4; ++g) {
+        const int n = nb + j * 32 + g * 8 + half * 4;
+        float z[4];
+        z[0] = acc[i][j][4 * g + 0] + __uint_as_float(bw[g].x << 16);
+        z[1] = acc[i][j][4 * g + 1] + __uint_as_float(bw[g].x & 0xffff0000u);
+        z[2] = acc[i][j][4 * g + 2] + __uint_as_float(bw[g].y << 16);
+        z[3] = acc[i][j][4 * g + 3] + __uint_as_float(bw[g].y & 0xffff0000u);
+        if (EPI == EPI_GELU) {
+#pragma unroll
+          for (int e = 0; e < 4; ++e) z[e] = gelu_erf(z[e]);
+        } else if (EPI == EPI_RESIDUAL) {
+          z[0] += __uint_as_float(res[g][0] << 16);
+          z[1] += __uint_as_float(res[g][0] & 0xffff0000u);
+          z[2] += __uint_as_float(res[g][1] << 16);
+          z[3] += __uint_as_float(res[g][1] & 0xffff0000u);
+        }
+        typedef uint32_t u32x2 __attribute__((ext_vector_type(2)));
+        const u32x2 v = {pack_bf16x2(z[0], z[1]), pack_bf16x2(z[2], z[3])};
+        __builtin_amdgcn_raw_buffer_store_b64(v, yres, (static_cast<uint32_t>(m) * ep.ldy + n) * 2u,
+                                              0, 0);
+      }
+    }
+  }
+}
+
 // ---------------------------------------------------------------------------
 // bf16 MFMA GEMM with direct-to-LDS operand loads
 // ---------------------------------------------------------------------------
@@ -993,70 +1055,6 @@ hipError_t launch_persist(hipStream_t s, const void* x, int M, int K, const void
                 static_cast<const bf16_t*>(x), static_cast<const bf16_t*>(w), M, N, K, ep);
 }
 
-// Epilogue of the ping-pong kernels from the accumulators:
-// acc[i][j][4g + e] = C[m][n + e], m = m0 + grp*WTM + 32 i + l32,
-// n = n0 + q*WTN + 32 j + 8 g + 4 half; raw buffer stores drop rows past M.
-template <int TM, int TN, int WTM, int WTN, int EPI>
-__device__ __forceinline__ void pp_epilogue(const f32x16_t (&acc)[TM][TN], int m0, int n0, int M,
-                                            int grp, int q, int l32, int half,
-                                            const EpiParams& ep) {
-  const int ybytes = M * ep.ldy * 2;
-  const __amdgpu_buffer_rsrc_t yres = __builtin_amdgcn_make_buffer_rsrc(ep.y, 0, ybytes, 0x00020000);
-  const bf16_t* bias = static_cast<const bf16_t*>(ep.bias);
-  uint2 bw[TN][4];
-#pragma unroll
-  for (int j = 0; j < TN; ++j)
-#pragma unroll
-    for (int g = 0; g < 4; ++g)
-      bw[j][g] = bias != nullptr
-                     ? *reinterpret_cast<const uint2*>(bias + n0 + q * WTN + j * 32 + g * 8 + half * 4)
-                     : make_uint2(0u, 0u);
-#pragma unroll
-  for (int i = 0; i < TM; ++i) {
-    uint32_t res[TN][4][2];
-    if (EPI == EPI_RESIDUAL) {
-      const __amdgpu_buffer_rsrc_t rres =
-          __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(ep.residual), 0, ybytes, 0x00020000);
-#pragma unroll
-      for (int j = 0; j < TN; ++j)
-#pragma unroll
-        for (int g = 0; g < 4; ++g) {
-          const int m = m0 + grp * WTM + i * 32 + l32;
-          const int n = n0 + q * WTN + j * 32 + g * 8 + half * 4;
-          const auto v = __builtin_amdgcn_raw_buffer_load_b64(
-              rres, (static_cast<uint32_t>(m) * ep.ldy + n) * 2u, 0, 0);
-          res[j][g][0] = v[0];
-          res[j][g][1] = v[1];
-        }
-    }
-#pragma unroll
-    for (int j = 0; j < TN; ++j)
-#pragma unroll
-      for (int g = 0; g < 4; ++g) {
-        const int m = m0 + grp * WTM + i * 32 + l32;
-        const int n = n0 + q * WTN + j * 32 + g * 8 + half * 4;
-        float z[4];
-        z[0] = acc[i][j][4 * g + 0] + __uint_as_float(bw[j][g].x << 16);
-        z[1] = acc[i][j][4 * g + 1] + __uint_as_float(bw[j][g].x & 0xffff0000u);
-        z[2] = acc[i][j][4 * g + 2] + __uint_as_float(bw[j][g].y << 16);
-        z[3] = acc[i][j][4 * g + 3] + __uint_as_float(bw[j][g].y & 0xffff0000u);
-        if (EPI == EPI_GELU) {
-#pragma unroll
-          for (int e = 0; e < 4; ++e) z[e] = gelu_erf(z[e]);
-        } else if (EPI == EPI_RESIDUAL) {
-          z[0] += __uint_as_float(res[j][g][0] << 16);
-          z[1] += __uint_as_float(res[j][g][0] & 0xffff0000u);
-          z[2] += __uint_as_float(res[j][g][1] << 16);
-          z[3] += __uint_as_float(res[j][g][1] & 0xffff0000u);
-        }
-        typedef uint32_t u32x2 __attribute__((ext_vector_type(2)));
-        const u32x2 v = {pack_bf16x2(z[0], z[1]), pack_bf16x2(z[2], z[3])};
-        __builtin_amdgcn_raw_buffer_store_b64(v, yres, (static_cast<uint32_t>(m) * ep.ldy + n) * 2u,
-                                              0, 0);
-      }
-  }
-}
-
 // ---------------------------------------------------------------------------
 // bf16 GEMM, 8-wave ping-pong over BM x BN tiles, epilogue in registers
 // ---------------------------------------------------------------------------
@@ -1207,7 +1205,7 @@ gemm_bf16_pp_kernel(const bf16_t* __restrict__ X, const bf16_t* __restrict__ W, 
     s = s + 1 == NS ? 0 : s + 1;
   }
 
-  pp_epilogue<TM, TN, WTM, WTN, EPI>(acc, m0, n0, M, grp, q, l32, half, ep);
+  reg_epilogue<TM, TN, EPI>(acc, m0 + grp * WTM, n0 + q * WTN, M, l32, half, ep);
   // group 0 passes its last barrier here, matching group 1's first one
   if (grp == 0) barrier_lds();
 }
