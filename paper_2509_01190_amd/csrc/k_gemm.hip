@@ -498,11 +498,10 @@ gemm_bf16_dma_kernel(
     const int r = (i * NW + wave) * SL::RPD + lr;
     bsrc[i] = W + static_cast<int64_t>(min(n0 + r, N - 1)) * K + kbeg + swz<KB>(r, lp) * 8;
   }
-  typedef __attribute__((address_space(3))) void lds_void;
-
 // the LDS-DMA builtin exists only in the device pass; the host pass only
 // needs the kernel's launch stub
 #if defined(__HIP_DEVICE_COMPILE__)
+  typedef __attribute__((address_space(3))) void lds_void;
 #define ZSA_DMA1(src, dst) __builtin_amdgcn_global_load_lds((src), (lds_void*)(dst), 16, 0, 0)
 #else
 #define ZSA_DMA1(src, dst) ((void)(src), (void)(dst))
@@ -791,7 +790,6 @@ gemm_bf16_persist_kernel(const bf16_t* __restrict__ X, const bf16_t* __restrict_
   constexpr int AI = BM / SL::RPD / NW, BI = BN / SL::RPD / NW;
   constexpr int SB = (BM + BN) * SL::RB;
   constexpr int KS = KB / 16;
-  constexpr int NSTORE = TM * TN * 4;  // buffer stores per wave per tile
   extern __shared__ __align__(16) unsigned char smem[];
   const int tid = threadIdx.x;
   const int lane = tid & 63;
@@ -833,8 +831,8 @@ gemm_bf16_persist_kernel(const bf16_t* __restrict__ X, const bf16_t* __restrict_
       bsrc[i] = W + static_cast<int64_t>(n0 + r) * K + swz<KB>(r, lp) * 8;
     }
   };
-  typedef __attribute__((address_space(3))) void lds_void;
 #if defined(__HIP_DEVICE_COMPILE__)
+  typedef __attribute__((address_space(3))) void lds_void;
 #define ZSA_DMA1(src, dst) __builtin_amdgcn_global_load_lds((src), (lds_void*)(dst), 16, 0, 0)
 #else
 #define ZSA_DMA1(src, dst) ((void)(src), (void)(dst))
