@@ -35,8 +35,9 @@ __device__ __forceinline__ uint32_t bf16_at(const uint4& v, int e) {
   return (e & 1) ? (w >> 16) : (w & 0xffffu);
 }
 
+// head dim 64 fits four waves per SIMD (128 registers), 128 two
 template <int HD>
-__global__ __launch_bounds__(256) void attn_mfma_kernel(
+__global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(HD == 64 ? 4 : 2))) void attn_mfma_kernel(
     const bf16_t* __restrict__ Q, const bf16_t* __restrict__ K, const bf16_t* __restrict__ V,
     int64_t rs, int kv_group, int causal, float scale_log2, const int32_t* __restrict__ cu,
     bf16_t* __restrict__ O, int64_t os, float* __restrict__ lse, int T) {
