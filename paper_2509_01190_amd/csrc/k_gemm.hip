@@ -776,15 +776,14 @@ __global__ __launch_bounds__(256) void gemm_valu_kernel(const T* __restrict__ X,
 // the tile's last K step.
 //
 // Operand staging and the K pipeline are those of gemm_bf16_dma_kernel
-// (64-wide slices, 2 stages, swizzled direct-to-LDS loads). N must be a
-// multiple of 128; outputs and residual of fewer than 2^31 bytes.
-constexpr int kPersistWgPerCu = 2;
-
-template <int EPI>
-__global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2, 2))) void
+// (KB-wide slices, 2 stages, swizzled direct-to-LDS loads; used with
+// 64-wide slices at two workgroups per CU). N must be a multiple of 128;
+// outputs and residual of fewer than 2^31 bytes.
+template <int EPI, int KB, int WPC>
+__global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(WPC, WPC))) void
 gemm_bf16_persist_kernel(const bf16_t* __restrict__ X, const bf16_t* __restrict__ W, int M, int N,
                          int K, EpiParams ep) {
-  constexpr int BM = 128, BN = 128, KB = 64, NW = 4, WN = 2;
+  constexpr int BM = 128, BN = 128, NW = 4, WN = 2;
   constexpr int WTM = 64, WTN = 64, TM = 2, TN = 2;
   using SL = Slice<KB>;
   constexpr int AI = BM / SL::RPD / NW, BI = BN / SL::RPD / NW;
@@ -1034,22 +1033,22 @@ bool persist_ok(int M, int N, int K, const EpiParams& ep) {
   return static_cast<int64_t>(M + 128) * ep.ldy * 2 < (int64_t{1} << 31);
 }
 
-template <int EPI>
+template <int EPI, int KB, int WPC>
 hipError_t launch_persist(hipStream_t s, const void* x, int M, int K, const void* w, int N,
                           const EpiParams& ep) {
-  constexpr int lds = 2 * (128 + 128) * 128;
+  constexpr int lds = 2 * (128 + 128) * KB * 2;
   static bool lds_raised = false;
   if (!lds_raised) {
     const hipError_t e = hipFuncSetAttribute(
-        reinterpret_cast<const void*>(gemm_bf16_persist_kernel<EPI>),
+        reinterpret_cast<const void*>(gemm_bf16_persist_kernel<EPI, KB, WPC>),
         hipFuncAttributeMaxDynamicSharedMemorySize, lds);
     if (e != hipSuccess) return e;
     lds_raised = true;
   }
   const int tiles = ((M + 127) / 128) * (N / 128);
-  const int wgs = std::min(tiles, device_cus() * kPersistWgPerCu);
+  const int wgs = std::min(tiles, device_cus() * WPC);
   const int grid = kXcds * ((wgs + kXcds - 1) / kXcds);
-  return launch(K_GEMM, gemm_bf16_persist_kernel<EPI>, dim3(grid), dim3(256), lds, s,
+  return launch(K_GEMM, gemm_bf16_persist_kernel<EPI, KB, WPC>, dim3(grid), dim3(256), lds, s,
                 static_cast<const bf16_t*>(x), static_cast<const bf16_t*>(w), M, N, K, ep);
 }
 
@@ -1242,11 +1241,12 @@ hipError_t launch_pp(hipStream_t s, const void* x, int M, int K, const void* w, 
   return launch_pp1<BM, BN, KB, NS, EPI_NONE>(s, x, M, K, w, N, ep);
 }
 
+template <int KB, int WPC>
 hipError_t launch_persist_any(hipStream_t s, const void* x, int M, int K, const void* w, int N,
                               const EpiParams& ep) {
-  if (ep.epi == EPI_GELU) return launch_persist<EPI_GELU>(s, x, M, K, w, N, ep);
-  if (ep.epi == EPI_RESIDUAL) return launch_persist<EPI_RESIDUAL>(s, x, M, K, w, N, ep);
-  return launch_persist<EPI_NONE>(s, x, M, K, w, N, ep);
+  if (ep.epi == EPI_GELU) return launch_persist<EPI_GELU, KB, WPC>(s, x, M, K, w, N, ep);
+  if (ep.epi == EPI_RESIDUAL) return launch_persist<EPI_RESIDUAL, KB, WPC>(s, x, M, K, w, N, ep);
+  return launch_persist<EPI_NONE, KB, WPC>(s, x, M, K, w, N, ep);
 }
 
 template <int BM, int BN, int WM, int WN>
@@ -1399,7 +1399,7 @@ hipError_t launch_gemm(hipStream_t s, int dtype, const void* x, int M, int K, co
       case 6431: return launch_dma<128, 128, 2, 2, 64, 3, 64>(s, x, M, K, w, N, ep);
       case 2542: return launch_dma<256, 256, 2, 2, 64, 2, 64>(s, x, M, K, w, N, ep);
       case 1289:
-        if (persist_ok(M, N, K, ep)) return launch_persist_any(s, x, M, K, w, N, ep);
+        if (persist_ok(M, N, K, ep)) return launch_persist_any<64, 2>(s, x, M, K, w, N, ep);
         break;
       case 2589:
         if (pp_ok(M, N, K, ep, 256)) return launch_pp<256, 256, 64, 2>(s, x, M, K, w, N, ep);
@@ -1426,7 +1426,7 @@ hipError_t launch_gemm(hipStream_t s, int dtype, const void* x, int M, int K, co
     if (K <= 3072 && persist_ok(M, N, K, ep)) {
       if (M >= 12288 && ep.epi != EPI_NONE && pp_ok(M, N, K, ep, 256))
         return launch_pp<256, 256, 64, 2>(s, x, M, K, w, N, ep);
-      if (tiles128 <= 1536) return launch_persist_any(s, x, M, K, w, N, ep);
+      if (tiles128 <= 1536) return launch_persist_any<64, 2>(s, x, M, K, w, N, ep);
     }
     const long tiles256 = static_cast<long>((M + 255) / 256) * ((N + 255) / 256);
     if (tiles256 >= 1024) return launch_dma<256, 256, 2, 4, 64, 2, 128>(s, x, M, K, w, N, ep);
