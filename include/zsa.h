@@ -168,9 +168,11 @@ int zsa_norm(void* stream, int32_t dtype, int32_t kind, const void* x, const voi
  * partial sums. When the output tiles of a bf16 product are too few to
  * fill the GPU, K is split into slices whose fp32 partials are summed in a
  * fixed slice order before the epilogue (results are reproducible; they
- * may differ from the unsplit sum in the last bits). With ws NULL the
- * product is never split. ws_bytes below zsa_linear_workspace_size()
- * returns ZSA_EWORKSPACE.
+ * may differ from the unsplit sum in the last bits). A bf16 product of at
+ * most 16 rows (k a multiple of 32) streams w into the matrix cores, one
+ * workgroup per 16 output columns whose waves split K and add their sums
+ * in a fixed order (no workspace). With ws NULL the product is never split.
+ * ws_bytes below zsa_linear_workspace_size() returns ZSA_EWORKSPACE.
  */
 int zsa_linear(void* stream, int32_t dtype, const void* x, int32_t m, int32_t k, const void* w,
                int32_t n, const void* bias, int32_t epilogue, const void* residual,
@@ -344,17 +346,21 @@ size_t zsa_stack_backward_workspace_size(const zsa_layer_cfg* cfg, int32_t total
  * block l in the pruned prefill, then earlier generated rows) and to
  * itself; its own k / v are appended at that row of the cache. The caller
  * adds 1 to every kv_len after the call.
- *   x_in, x_out [batch, d] dtype device (may alias); pos_host [batch] the
+ *   kv_cache [n_layers, batch, kv_capacity, 2 kvd] dtype device, 256-byte
+ *   aligned; x_in, x_out [batch, d] dtype device (may alias); pos_host [batch] the
  *   original position of each new row (RoPE); kv_len_host [n_layers*batch]
- *   host, each < kv_capacity; ws >= zsa_decode_workspace_size(cfg, batch,
- *   kv_capacity). Causal stacks, bf16, head_dim 64 or 128, 1/2/4/8 query
- *   heads per key/value head; otherwise ZSA_EUNSUPPORTED.
+ *   host, each < kv_capacity; ws >= zsa_decode_workspace_size(cfg,
+ *   n_layers, batch, kv_capacity), device, owned by the caller, contents
+ *   need not be preserved between calls. Causal stacks, bf16, head_dim 64
+ *   or 128, 1/2/4/8 query heads per key/value head; otherwise
+ *   ZSA_EUNSUPPORTED. Calls that share a workspace must not overlap.
  */
 int zsa_decode_step(void* stream, const zsa_layer_cfg* cfg, const zsa_layer_weights* w,
                     int32_t n_layers, int32_t batch, const void* x_in, const int32_t* pos_host,
                     void* kv_cache, int32_t kv_capacity, const int32_t* kv_len_host, void* x_out,
                     void* ws, size_t ws_bytes);
-size_t zsa_decode_workspace_size(const zsa_layer_cfg* cfg, int32_t batch, int32_t kv_capacity);
+size_t zsa_decode_workspace_size(const zsa_layer_cfg* cfg, int32_t n_layers, int32_t batch,
+                                 int32_t kv_capacity);
 
 /* ---------------------------------------------------------------------
  * Timing hook (profiling aid, not thread-safe): while armed, the next

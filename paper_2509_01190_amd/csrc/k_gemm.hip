@@ -28,6 +28,7 @@ namespace {
 
 typedef __bf16 bf16x8_t __attribute__((ext_vector_type(8)));
 typedef float f32x16_t __attribute__((ext_vector_type(16)));
+typedef float f32x4_t __attribute__((ext_vector_type(4)));
 
 template <typename T>
 __device__ __forceinline__ void load8(const T* p, float* v);
@@ -701,6 +702,213 @@ __global__ __launch_bounds__(256) void splitk_sum_f32_kernel(const float4* __res
 }
 
 // ---------------------------------------------------------------------------
+// Few-row products (generation: one new row per sequence)
+// ---------------------------------------------------------------------------
+// y = epi(x W^T) for M <= 16 rows of x: the whole cost is one read of W
+// (M multiply-adds per weight), so W goes straight from memory into MFMA
+// operands with no LDS staging. v_mfma_f32_16x16x32_bf16 takes A = 16 rows
+// of W (lane l: row l % 16, the 8 K values 8 (l / 16) .. + 7 of a 32-wide
+// step) and B = the x rows (lane l: row l % 16, zero past M); lane l then
+// holds outputs (row l % 16 of x, W rows 4 (l / 16) .. + 3).
+//
+// A workgroup owns 16 output columns over the whole of K: its 8 waves take
+// consecutive K ranges (256 K values, 8 KB of W per wave, per load round;
+// a round's steps past the range read zeros) and their 16 x 16 partial
+// sums are added in wave order through LDS, so no other workgroup is
+// involved and the result is reproducible. Loads go through buffer
+// resources: W rows past N, x rows past M and offsets set past the end
+// read as zeros.
+// For the rotary epilogue a workgroup's columns are 8 channels of a head
+// and their partners hd / 2 further on, so each rotation pair is local.
+constexpr int kSkCols = 16;   // output columns (W rows) per workgroup
+constexpr int kSkWaves = 8;   // K ranges per workgroup
+constexpr int kSkStep = 256;  // K values per load round
+constexpr int kSkMaxM = 16;   // rows of x
+
+// output column of tile column j in workgroup t (rope_half = hd / 2 for the
+// rotary epilogue, else 0)
+__device__ __forceinline__ int skinny_col(int t, int j, int rope_half) {
+  if (rope_half == 0) return t * kSkCols + j;
+  const int per_head = rope_half / 8;  // workgroups per head
+  const int h = t / per_head, i0 = (t % per_head) * 8;
+  return h * 2 * rope_half + i0 + (j & 7) + (j >> 3) * rope_half;
+}
+
+// CPL > 0: x is first normalised as the block's pre-norm does (LayerNorm,
+// or RMSNorm with mean 0): wave w takes row w (M <= 8), CPL 16-byte chunks
+// of it per lane, for the exact two-pass mean and centred sum of squares in
+// fp32; the gain (and shift) go to LDS; each x fragment then becomes
+// bf16((x - mean) * rstd * gain + shift) before its MFMA, the values the
+// separate normalisation would have stored.
+template <int CPL>
+__global__ __launch_bounds__(kSkWaves * 64) void gemm_skinny_kernel(
+    const bf16_t* __restrict__ X, const bf16_t* __restrict__ W, int M, int N, int K, int kc,
+    EpiParams ep, PreNorm pn) {
+  extern __shared__ __align__(16) uint4 gain_shift[];  // CPL > 0: gain [K / 8], shift [K / 8]
+  __shared__ float red[kSkWaves][kSkMaxM][kSkCols + 1];
+  __shared__ float tile[kSkMaxM][kSkCols + 1];
+  __shared__ float row_stat[2][kSkWaves];  // mean, rstd of each x row
+  const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63;
+  const int l16 = lane & 15, kg = lane >> 4;
+  const int t = blockIdx.x;
+  const int rope_half = ep.epi == EPI_ROPE ? ep.head_dim / 2 : 0;
+  const int k0 = wave * kc, k1 = min(K, k0 + kc);
+  const __amdgpu_buffer_rsrc_t xres = __builtin_amdgcn_make_buffer_rsrc(
+      const_cast<bf16_t*>(X), 0, static_cast<uint32_t>(M) * K * 2u, 0x00020000);
+  const __amdgpu_buffer_rsrc_t wres = __builtin_amdgcn_make_buffer_rsrc(
+      const_cast<bf16_t*>(W), 0, static_cast<uint32_t>(N) * K * 2u, 0x00020000);
+  const uint32_t woff = static_cast<uint32_t>(skinny_col(t, l16, rope_half)) * K * 2u + kg * 16u;
+  const uint32_t xoff = static_cast<uint32_t>(l16) * K * 2u + kg * 16u;
+  constexpr uint32_t kPast = 0x80000000u;  // beyond both buffers: reads zeros
+  constexpr int NF = kSkStep / 32;         // MFMA steps per round
+  const int C8 = K / 8;                    // 16-byte chunks of a row
+  // the normalisation's inputs are requested first, so waiting for them
+  // leaves the first round of W in flight
+  uint4 gs[2], rowc[CPL > 0 ? CPL : 1];  // gain / shift chunks: 2 K / 8 <= 2 x 512
+  if constexpr (CPL > 0) {
+#pragma unroll
+    for (int q = 0; q < 2; ++q) {
+      const int c = tid + q * kSkWaves * 64;
+      gs[q] = make_uint4(0u, 0u, 0u, 0u);
+      if (c < 2 * C8) {
+        const bf16_t* src = c < C8 ? pn.g + 8 * c : (pn.b != nullptr ? pn.b + 8 * (c - C8) : nullptr);
+        if (src != nullptr) gs[q] = *reinterpret_cast<const uint4*>(src);
+      }
+    }
+#pragma unroll
+    for (int i = 0; i < CPL; ++i) {
+      const int c = lane + 64 * i;
+      rowc[i] = __builtin_bit_cast(
+          uint4, __builtin_amdgcn_raw_buffer_load_b128(
+                     xres, wave < M && c < C8 ? (static_cast<uint32_t>(wave) * K + 8 * c) * 2u : kPast,
+                     0, 0));
+    }
+    __builtin_amdgcn_sched_barrier(0);
+  }
+  bf16x8_t a[NF], b[NF];
+  auto issue = [&](int k) {
+#pragma unroll
+    for (int j = 0; j < NF; ++j) {
+      const bool in = k + 32 * j < k1;
+      a[j] = __builtin_bit_cast(bf16x8_t, __builtin_amdgcn_raw_buffer_load_b128(
+                                              wres, in ? woff + (k + 32 * j) * 2u : kPast, 0, 0));
+    }
+#pragma unroll
+    for (int j = 0; j < NF; ++j) {
+      const bool in = k + 32 * j < k1;
+      b[j] = __builtin_bit_cast(bf16x8_t, __builtin_amdgcn_raw_buffer_load_b128(
+                                              xres, in ? xoff + (k + 32 * j) * 2u : kPast, 0, 0));
+    }
+  };
+  if (k0 < k1) issue(k0);
+  __builtin_amdgcn_sched_barrier(0);
+  float mean = 0.f, rstd = 0.f;
+  if constexpr (CPL > 0) {
+#pragma unroll
+    for (int q = 0; q < 2; ++q) {
+      const int c = tid + q * kSkWaves * 64;
+      if (c < 2 * C8) gain_shift[c] = gs[q];
+    }
+    const float inv_d = 1.0f / static_cast<float>(K);
+    float sum = 0.f, sq = 0.f, mu = 0.f;
+    if (!pn.rms) {
+#pragma unroll
+      for (int i = 0; i < CPL; ++i) {
+        float v[8];
+        unpack16(rowc[i], v, bf16_t());
+#pragma unroll
+        for (int e = 0; e < 8; ++e) sum += v[e];
+      }
+#pragma unroll
+      for (int off = 32; off > 0; off >>= 1) sum += __shfl_xor(sum, off, 64);
+      mu = sum * inv_d;
+    }
+#pragma unroll
+    for (int i = 0; i < CPL; ++i) {
+      if (lane + 64 * i < C8) {
+        float v[8];
+        unpack16(rowc[i], v, bf16_t());
+#pragma unroll
+        for (int e = 0; e < 8; ++e) {
+          const float d = v[e] - mu;
+          sq += d * d;
+        }
+      }
+    }
+#pragma unroll
+    for (int off = 32; off > 0; off >>= 1) sq += __shfl_xor(sq, off, 64);
+    if (lane == 0) {
+      row_stat[0][wave] = mu;
+      row_stat[1][wave] = 1.0f / sqrtf(sq * inv_d + pn.eps);
+    }
+    barrier_lds();
+    if (l16 < M) {
+      mean = row_stat[0][l16];
+      rstd = row_stat[1][l16];
+    }
+  }
+  f32x4_t acc = {0.f, 0.f, 0.f, 0.f};
+  for (int k = k0; k < k1; k += kSkStep) {
+    if (k != k0) issue(k);
+    // all of the round's loads in flight before the first MFMA waits on one
+    __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+    for (int j = 0; j < NF; ++j) {
+      bf16x8_t bj = b[j];
+      if constexpr (CPL > 0) {
+        const int c = min(k + 32 * j + 8 * kg, K - 8) / 8;
+        float v[8], g[8], sh[8], o[8];
+        unpack16(__builtin_bit_cast(uint4, b[j]), v, bf16_t());
+        unpack16(gain_shift[c], g, bf16_t());
+        unpack16(gain_shift[C8 + c], sh, bf16_t());
+#pragma unroll
+        for (int e = 0; e < 8; ++e) o[e] = (v[e] - mean) * rstd * g[e] + sh[e];
+        bj = __builtin_bit_cast(bf16x8_t, pack16(o, bf16_t()));
+      }
+      acc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a[j], bj, acc, 0, 0, 0);
+    }
+  }
+  if (l16 < M) {
+#pragma unroll
+    for (int r = 0; r < 4; ++r) red[wave][l16][4 * kg + r] = acc[r];
+  }
+  __syncthreads();
+  const int items = M * kSkCols;
+  if (tid < items) {
+    const int m = tid / kSkCols, j = tid % kSkCols;
+    float z = 0.f;
+#pragma unroll
+    for (int w = 0; w < kSkWaves; ++w) z += red[w][m][j];
+    const int c = skinny_col(t, j, rope_half);
+    if (ep.bias != nullptr && c < N) z += to_f32(static_cast<const bf16_t*>(ep.bias)[c]);
+    tile[m][j] = z;
+  }
+  __syncthreads();
+  if (tid >= items) return;
+  const int m = tid / kSkCols, j = tid % kSkCols;
+  const int c = skinny_col(t, j, rope_half);
+  if (c >= N) return;
+  bf16_t* y = static_cast<bf16_t*>(ep.y) + static_cast<int64_t>(m) * ep.ldy;
+  const float z = tile[m][j];
+  float v = z;
+  if (ep.epi == EPI_SWIGLU) {  // gate, up on columns 2f, 2f + 1
+    if (j & 1) return;
+    y[c / 2] = f32_to_bf16(silu(z) * tile[m][j + 1]);
+    return;
+  } else if (ep.epi == EPI_GELU) {
+    v = gelu_erf(z);
+  } else if (ep.epi == EPI_RESIDUAL) {
+    v = z + to_f32(static_cast<const bf16_t*>(ep.residual)[static_cast<int64_t>(m) * ep.ldy + c]);
+  } else if (ep.epi == EPI_ROPE && c < ep.rope_cols) {
+    const float zp = tile[m][j ^ 8];
+    float sn, cs;
+    rope_angle(ep.pos[m], ep.inv_freq[(c % ep.head_dim) % rope_half], &sn, &cs);
+    v = j < 8 ? z * cs - zp * sn : z * cs + zp * sn;
+  }
+  y[c] = f32_to_bf16(v);
+}
+
+// ---------------------------------------------------------------------------
 // vector-ALU GEMM (fp32 storage, and any shape)
 // ---------------------------------------------------------------------------
 constexpr int vBM = 64, vBN = 128, vBK = 16;
@@ -1318,6 +1526,48 @@ void splitk_plan(int M, int N, int K, int* S, int* kchunk) {
   const int per = (steps + want - 1) / want;
   *S = (steps + per - 1) / per;
   *kchunk = per * kBK;
+}
+
+int device_cu_count() { return device_cus(); }
+
+// Few-row products: one workgroup per 16 output columns; each of its waves
+// takes a K range of whole 32-wide steps.
+bool skinny_ok(int dtype, int M, int N, int K, const EpiParams& ep) {
+  if (dtype != 1 || M < 1 || M > kSkMaxM || K % 32 != 0 || K < 32) return false;
+  if (static_cast<int64_t>(N + kSkCols) * K * 2 >= (int64_t{1} << 31)) return false;
+  if (ep.epi == EPI_SWIGLU && N % 2 != 0) return false;
+  if (ep.epi == EPI_ROPE && (ep.head_dim < 16 || ep.head_dim % 16 != 0 || N % ep.head_dim != 0))
+    return false;
+  return true;
+}
+
+// Every workgroup normalises the x fragments it reads, so the folded norm
+// pays off only while the workgroups are few: at most two per CU (a q|k|v
+// projection; not a wide up-projection, where a separate normalisation is
+// cheaper than re-doing it in each of thousands of workgroups).
+bool skinny_norm_ok(int M, int N, int K) {
+  return M >= 1 && M <= kSkWaves && K % 32 == 0 && K <= 4096 &&
+         (N + kSkCols - 1) / kSkCols <= 2 * device_cus();
+}
+
+hipError_t launch_gemm_skinny(hipStream_t s, const void* x, int M, int K, const void* w, int N,
+                              const EpiParams& ep, const PreNorm* pn) {
+  if (M == 0 || N == 0) return hipSuccess;
+  const int kc = ((K + kSkWaves * 32 - 1) / (kSkWaves * 32)) * 32;
+  const dim3 grid((N + kSkCols - 1) / kSkCols), block(kSkWaves * 64);
+  const bf16_t* xp = static_cast<const bf16_t*>(x);
+  const bf16_t* wp = static_cast<const bf16_t*>(w);
+  if (pn == nullptr || pn->g == nullptr)
+    return launch(K_GEMM, gemm_skinny_kernel<0>, grid, block, 0, s, xp, wp, M, N, K, kc, ep,
+                  PreNorm{});
+  if (!skinny_norm_ok(M, N, K)) return hipErrorInvalidValue;
+  const size_t lds = static_cast<size_t>(K) / 8 * 2 * sizeof(uint4);
+  const int cpl = (K / 8 + 63) / 64;
+  if (cpl <= 2)
+    return launch(K_GEMM, gemm_skinny_kernel<2>, grid, block, lds, s, xp, wp, M, N, K, kc, ep, *pn);
+  if (cpl <= 4)
+    return launch(K_GEMM, gemm_skinny_kernel<4>, grid, block, lds, s, xp, wp, M, N, K, kc, ep, *pn);
+  return launch(K_GEMM, gemm_skinny_kernel<8>, grid, block, lds, s, xp, wp, M, N, K, kc, ep, *pn);
 }
 
 size_t splitk_bytes(int S, int M, int N) {

@@ -480,9 +480,12 @@ int zsa_linear(void* stream, int32_t dtype, const void* x, int32_t m, int32_t k,
     if (ws_bytes < need)
       return fail(ZSA_EWORKSPACE, "linear workspace %zu < %zu bytes", ws_bytes, need);
   }
-  HIP_TRY(zsa::launch_gemm(static_cast<hipStream_t>(stream), dtype, x, m, k, w, n, ep, ws,
-                           ws_bytes),
-          "linear");
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  if (m > 0 && zsa::skinny_ok(dtype, m, n, k, ep)) {
+    HIP_TRY(zsa::launch_gemm_skinny(s, x, m, k, w, n, ep), "linear");
+    return ZSA_OK;
+  }
+  HIP_TRY(zsa::launch_gemm(s, dtype, x, m, k, w, n, ep, ws, ws_bytes), "linear");
   return ZSA_OK;
 }
 
@@ -1173,13 +1176,24 @@ int zsa_stack_backward(void* stream, const zsa_layer_cfg* cfg, const zsa_layer_w
 // generation after a pruned prefill
 // ---------------------------------------------------------------------------
 struct DecodeLayout {
-  size_t h, qkv, o, f, m, l, op, pos, cu, len, splitk, splitk_bytes, end;
+  size_t h, qkv, o, f, m, l, op, pos, len, splitk, splitk_bytes, end;
 };
 
-DecodeLayout decode_layout(const zsa_layer_cfg* c, int32_t batch, int32_t cap) {
+// the four projections of a block: fused q|k|v, output, up, down (N, K)
+void decode_gemm_shapes(const zsa_layer_cfg& c, int nk[4][2]) {
+  const int d = c.d_model, F = c.d_ff, qw = static_cast<int>(qkv_width(c));
+  const int up_n = c.kind == ZSA_DECODER ? 2 * F : F;
+  const int shapes[4][2] = {{qw, d}, {d, d}, {up_n, d}, {d, F}};
+  for (int g = 0; g < 4; ++g) {
+    nk[g][0] = shapes[g][0];
+    nk[g][1] = shapes[g][1];
+  }
+}
+
+DecodeLayout decode_layout(const zsa_layer_cfg* c, int32_t batch, int32_t cap, int32_t n_layers) {
   const size_t e = esize(c->dtype);
   const int64_t d = c->d_model, F = c->d_ff, qw = qkv_width(*c);
-  const int S = zsa::decode_splits(cap);
+  const int S = zsa::decode_splits_bound(cap);
   const size_t part = static_cast<size_t>(batch) * c->n_heads * S;
   Carver cv;
   DecodeLayout L;
@@ -1190,23 +1204,26 @@ DecodeLayout decode_layout(const zsa_layer_cfg* c, int32_t batch, int32_t cap) {
   L.m = cv.take(part * 4);
   L.l = cv.take(part * 4);
   L.op = cv.take(part * c->head_dim * 4);
-  L.pos = cv.take(static_cast<size_t>(batch) * 4);
-  L.cu = cv.take(static_cast<size_t>(batch + 1) * 4);
-  L.len = cv.take(static_cast<size_t>(2 * batch) * 4);
-  const int dt = c->dtype;
-  const int up_n = c->kind == ZSA_DECODER ? 2 * c->d_ff : c->d_ff;
-  L.splitk_bytes = std::max({zsa::gemm_workspace_bound(dt, batch, static_cast<int>(qw), c->d_model),
-                             zsa::gemm_workspace_bound(dt, batch, c->d_model, c->d_model),
-                             zsa::gemm_workspace_bound(dt, batch, up_n, c->d_model),
-                             zsa::gemm_workspace_bound(dt, batch, c->d_model, c->d_ff)});
+  // host values of the step, uploaded together: pos [batch], then per layer
+  // the cache row of the new row and the rows attended [2 batch]
+  L.pos = cv.take(static_cast<size_t>(batch) * (1 + 2 * std::max(n_layers, 1)) * 4);
+  L.len = L.pos + static_cast<size_t>(batch) * 4;
+  // split-K partials of projections that do not take the few-row kernel
+  int nk[4][2];
+  decode_gemm_shapes(*c, nk);
+  L.splitk_bytes = 0;
+  for (int g = 0; g < 4; ++g)
+    L.splitk_bytes = std::max(L.splitk_bytes,
+                              zsa::gemm_workspace_bound(c->dtype, batch, nk[g][0], nk[g][1]));
   L.splitk = cv.take(L.splitk_bytes);
   L.end = cv.off;
   return L;
 }
 
-size_t zsa_decode_workspace_size(const zsa_layer_cfg* cfg, int32_t batch, int32_t kv_capacity) {
-  if (cfg == nullptr || batch < 0 || kv_capacity < 1) return 0;
-  return decode_layout(cfg, batch, kv_capacity).end;
+size_t zsa_decode_workspace_size(const zsa_layer_cfg* cfg, int32_t n_layers, int32_t batch,
+                                 int32_t kv_capacity) {
+  if (cfg == nullptr || n_layers < 1 || batch < 0 || kv_capacity < 1) return 0;
+  return decode_layout(cfg, batch, kv_capacity, n_layers).end;
 }
 
 int zsa_decode_step(void* stream, const zsa_layer_cfg* cfg, const zsa_layer_weights* w,
@@ -1229,12 +1246,14 @@ int zsa_decode_step(void* stream, const zsa_layer_cfg* cfg, const zsa_layer_weig
   CHECK(check_ptr16(x_in, "x_in"));
   CHECK(check_ptr16(x_out, "x_out"));
   CHECK(check_ptr16(kv_cache, "kv_cache"));
+  if (reinterpret_cast<uintptr_t>(kv_cache) % 256 != 0)
+    return fail(ZSA_EINVAL, "kv_cache must be 256-byte aligned");
   if (pos_host == nullptr || kv_len_host == nullptr) return fail(ZSA_EINVAL, "pos / kv_len is NULL");
   for (int i = 0; i < n_layers * batch; ++i)
     if (kv_len_host[i] < 0 || kv_len_host[i] >= kv_capacity)
       return fail(ZSA_ESHAPE, "kv_len[%d] = %d leaves no room below kv_capacity %d", i,
                   kv_len_host[i], kv_capacity);
-  const DecodeLayout L = decode_layout(cfg, batch, kv_capacity);
+  const DecodeLayout L = decode_layout(cfg, batch, kv_capacity, n_layers);
   if (ws == nullptr || ws_bytes < L.end)
     return fail(ZSA_EWORKSPACE, "workspace %zu < %zu", ws_bytes, L.end);
   hipStream_t s = static_cast<hipStream_t>(stream);
@@ -1244,7 +1263,6 @@ int zsa_decode_step(void* stream, const zsa_layer_cfg* cfg, const zsa_layer_weig
   void* o = base + L.o;
   void* f = base + L.f;
   int32_t* pos_dev = reinterpret_cast<int32_t*>(base + L.pos);
-  int32_t* cu_dev = reinterpret_cast<int32_t*>(base + L.cu);
   int32_t* len_dev = reinterpret_cast<int32_t*>(base + L.len);
   void* splitk = L.splitk_bytes ? base + L.splitk : nullptr;
   const bool dec = c.kind == ZSA_DECODER;
@@ -1252,25 +1270,44 @@ int zsa_decode_step(void* stream, const zsa_layer_cfg* cfg, const zsa_layer_weig
   const size_t e = esize(c.dtype);
   const size_t layer_bytes = static_cast<size_t>(batch) * kv_capacity * 2 * kvd * e;
 
-  std::vector<int32_t> unit(batch + 1);
-  for (int b = 0; b <= batch; ++b) unit[b] = b;
-  HIP_TRY(launch_upload_i32(s, pos_dev, pos_host, batch), "upload");
-  HIP_TRY(launch_upload_i32(s, cu_dev, unit.data(), batch + 1), "upload");
-  std::vector<int32_t> lens(2 * batch);
+  std::vector<int32_t> host_ints;
+  host_ints.reserve(static_cast<size_t>(batch) * (1 + 2 * n_layers));
+  host_ints.insert(host_ints.end(), pos_host, pos_host + batch);
+  std::vector<int> max_n(n_layers, 0);
+  for (int l = 0; l < n_layers; ++l) {
+    for (int b = 0; b < batch; ++b) host_ints.push_back(kv_len_host[l * batch + b]);  // new row
+    for (int b = 0; b < batch; ++b) {
+      host_ints.push_back(kv_len_host[l * batch + b] + 1);  // rows attended, the new one included
+      max_n[l] = std::max(max_n[l], kv_len_host[l * batch + b] + 1);
+    }
+  }
+  HIP_TRY(launch_upload_i32(s, pos_dev, host_ints.data(), static_cast<int>(host_ints.size())),
+          "upload");
+  // few-row projections stream W through the matrix cores; other shapes
+  // take the general GEMM
+  auto proj = [&](const void* x, int K, const void* wt, int N, const EpiParams& ep) -> hipError_t {
+    if (skinny_ok(c.dtype, batch, N, K, ep)) return launch_gemm_skinny(s, x, batch, K, wt, N, ep);
+    return launch_gemm(s, c.dtype, x, batch, K, wt, N, ep, splitk, L.splitk_bytes);
+  };
+  // the block's pre-norm and the projection that reads it: folded into the
+  // few-row kernel when it can take it, else normalised into h first
+  auto norm_proj = [&](const void* x, const void* g, const void* b, const void* wt, int N,
+                       const EpiParams& ep) -> hipError_t {
+    if (skinny_ok(c.dtype, batch, N, d, ep) && skinny_norm_ok(batch, N, d)) {
+      const PreNorm pn{static_cast<const bf16_t*>(g), dec ? nullptr : static_cast<const bf16_t*>(b),
+                       dec ? 1 : 0, c.norm_eps};
+      return launch_gemm_skinny(s, x, batch, d, wt, N, ep, &pn);
+    }
+    hipError_t e = launch_norm(s, c.dtype, norm_kind, x, g, dec ? nullptr : b, batch, d,
+                               c.norm_eps, h);
+    if (e != hipSuccess) return e;
+    return proj(h, d, wt, N, ep);
+  };
   for (int l = 0; l < n_layers; ++l) {
     const zsa_layer_weights& wl = w[l];
     const void* xin = l == 0 ? x_in : x_out;
     void* cache_l = static_cast<char*>(kv_cache) + l * layer_bytes;
-    int max_n = 0;
-    for (int b = 0; b < batch; ++b) {
-      lens[b] = kv_len_host[l * batch + b];          // where the new row goes
-      lens[batch + b] = lens[b] + 1;                 // rows attended, the new one included
-      max_n = std::max(max_n, lens[batch + b]);
-    }
-    HIP_TRY(launch_upload_i32(s, len_dev, lens.data(), 2 * batch), "upload");
-    HIP_TRY(launch_norm(s, c.dtype, norm_kind, xin, wl.norm1_w, dec ? nullptr : wl.norm1_b, batch,
-                        d, c.norm_eps, h),
-            "norm1");
+    int32_t* len_l = len_dev + 2 * batch * l;
     {
       EpiParams ep{};
       ep.epi = dec ? EPI_ROPE : EPI_NONE;
@@ -1281,14 +1318,10 @@ int zsa_decode_step(void* stream, const zsa_layer_cfg* cfg, const zsa_layer_weig
       ep.head_dim = hd;
       ep.rope_cols = dec ? d + kvd : 0;
       if (dec) fill_rope(ep, hd, c.rope_theta);
-      HIP_TRY(launch_gemm(s, c.dtype, h, batch, d, wl.w_qkv, qw, ep, splitk, L.splitk_bytes),
-              "qkv projection");
+      HIP_TRY(norm_proj(xin, wl.norm1_w, wl.norm1_b, wl.w_qkv, qw, ep), "norm1, qkv projection");
     }
-    HIP_TRY(launch_kv_store(s, c.dtype, qkv, qw, d, kvd, batch, 1, cu_dev, len_dev, cache_l,
-                            kv_capacity),
-            "kv append");
-    HIP_TRY(launch_decode_attention(s, qkv, qw, cache_l, kv_capacity, hd, H, kv_heads(c),
-                                    len_dev + batch, batch, decode_splits(max_n),
+    HIP_TRY(launch_decode_attention(s, qkv, qw, d, cache_l, kv_capacity, hd, H, kv_heads(c),
+                                    len_l + batch, batch, max_n[l],
                                     1.0f / sqrtf(static_cast<float>(hd)),
                                     reinterpret_cast<float*>(base + L.m),
                                     reinterpret_cast<float*>(base + L.l),
@@ -1301,21 +1334,16 @@ int zsa_decode_step(void* stream, const zsa_layer_cfg* cfg, const zsa_layer_weig
       ep.residual = xin;
       ep.y = x_out;
       ep.ldy = d;
-      HIP_TRY(launch_gemm(s, c.dtype, o, batch, d, wl.w_o, d, ep, splitk, L.splitk_bytes),
-              "output projection");
+      HIP_TRY(proj(o, d, wl.w_o, d, ep), "output projection");
     }
-    HIP_TRY(launch_norm(s, c.dtype, norm_kind, x_out, wl.norm2_w, dec ? nullptr : wl.norm2_b,
-                        batch, d, c.norm_eps, h),
-            "norm2");
     {
       EpiParams ep{};
       ep.epi = dec ? EPI_SWIGLU : EPI_GELU;
       ep.bias = wl.b_up;
       ep.y = f;
       ep.ldy = F;
-      HIP_TRY(launch_gemm(s, c.dtype, h, batch, d, wl.w_up, dec ? 2 * F : F, ep, splitk,
-                          L.splitk_bytes),
-              "up projection");
+      HIP_TRY(norm_proj(x_out, wl.norm2_w, wl.norm2_b, wl.w_up, dec ? 2 * F : F, ep),
+              "norm2, up projection");
     }
     {
       EpiParams ep{};
@@ -1324,8 +1352,7 @@ int zsa_decode_step(void* stream, const zsa_layer_cfg* cfg, const zsa_layer_weig
       ep.residual = x_out;
       ep.y = x_out;
       ep.ldy = d;
-      HIP_TRY(launch_gemm(s, c.dtype, f, batch, F, wl.w_down, d, ep, splitk, L.splitk_bytes),
-              "down projection");
+      HIP_TRY(proj(f, F, wl.w_down, d, ep), "down projection");
     }
   }
   return ZSA_OK;

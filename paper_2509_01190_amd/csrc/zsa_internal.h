@@ -164,6 +164,24 @@ size_t gemm_workspace_bytes(int dtype, int M, int N, int K);
 // the most any M <= max_rows needs
 size_t gemm_workspace_bound(int dtype, int max_rows, int N, int K);
 
+int device_cu_count();  // compute units of the current device
+
+// Few-row product (M <= 16 rows of x, bf16): W streamed into MFMA operands,
+// one workgroup per 16 output columns over the whole of K (no workspace).
+// With pn (gain non-null; skinny_norm_ok: M <= 8, K <= 4096, few output
+// tiles) x is first normalised as launch_norm would (LayerNorm with shift,
+// or RMSNorm).
+struct PreNorm {
+  const bf16_t* g;  // gain [K], or null: x is used as it is
+  const bf16_t* b;  // LayerNorm shift [K] or null
+  int rms;          // 1: RMSNorm, 0: LayerNorm
+  float eps;
+};
+bool skinny_ok(int dtype, int M, int N, int K, const EpiParams& ep);
+bool skinny_norm_ok(int M, int N, int K);
+hipError_t launch_gemm_skinny(hipStream_t s, const void* x, int M, int K, const void* w, int N,
+                              const EpiParams& ep, const PreNorm* pn = nullptr);
+
 // query head h reads key/value head h / kv_group (kv_group = H / H_kv)
 hipError_t launch_attention(hipStream_t s, int dtype, const void* q, const void* k,
                             const void* v, int64_t row_stride, int H, int kv_group, int hd,
@@ -191,12 +209,15 @@ hipError_t launch_select(hipStream_t s, const float* partials, int groups, int T
 hipError_t launch_kv_store(hipStream_t s, int dtype, const void* src, int64_t src_stride,
                            int src_col, int kvd, int B, int max_rows, const int32_t* cu_dev,
                            const int32_t* start_dev, void* cache_layer, int cap);
-hipError_t launch_decode_attention(hipStream_t s, const void* q, int64_t q_stride,
-                                   const void* cache_layer, int cap, int hd, int H, int Hkv,
-                                   const int32_t* len_dev, int B, int S, float scale,
+// qkv [B, q_stride]: query heads at column 0, the new row's k | v at kv_col;
+// appends them at cache row len - 1, then attends over len rows. Partials:
+// m, l [B][H][decode_splits_bound(cap)], o [...][hd]
+hipError_t launch_decode_attention(hipStream_t s, const void* qkv, int64_t q_stride, int kv_col,
+                                   void* cache_layer, int cap, int hd, int H, int Hkv,
+                                   const int32_t* len_dev, int B, int max_len, float scale,
                                    float* m_part, float* l_part, float* o_part, void* out,
                                    int64_t out_stride);
-int decode_splits(int max_len);
+int decode_splits_bound(int cap);
 bool decode_supported(int dtype, int hd, int group);
 
 // backward pass (bf16, head_dim 64 / 128 for the attention part)

@@ -90,7 +90,7 @@ _SIGS = {
                                          _vp, _vp, _vp, _i32, _vp, _sz]),
     "zsa_decode_step": (ctypes.c_int, [_vp, ctypes.POINTER(LayerCfg), ctypes.POINTER(LayerWeights),
                                        _i32, _i32, _vp, _pi32, _vp, _i32, _pi32, _vp, _vp, _sz]),
-    "zsa_decode_workspace_size": (_sz, [ctypes.POINTER(LayerCfg), _i32, _i32]),
+    "zsa_decode_workspace_size": (_sz, [ctypes.POINTER(LayerCfg), _i32, _i32, _i32]),
     "zsa_stack_backward": (ctypes.c_int, [_vp, ctypes.POINTER(LayerCfg),
                                           ctypes.POINTER(LayerWeights), ctypes.POINTER(LayerGrads),
                                           _i32, _pi32, _i32, _pf64, _vp, _vp, _i32, _pi32, _vp,
@@ -498,7 +498,8 @@ class Stack:
         if lens.shape != (self.n_layers, batch):
             raise ValueError("kv_len must be [layers, batch]")
         y = torch.empty_like(x_new) if out is None else out
-        wsz = int(lib().zsa_decode_workspace_size(ctypes.byref(self.cfg), batch, cap))
+        wsz = int(lib().zsa_decode_workspace_size(ctypes.byref(self.cfg), self.n_layers, batch,
+                                                  cap))
         ws = torch.empty(max(wsz, 1), dtype=torch.uint8, device=x_new.device)
         _check(lib().zsa_decode_step(_stream(x_new.device), ctypes.byref(self.cfg), self._wstructs,
                                      self.n_layers, batch, _p(x_new), _hp32(_host_i32(pos_new)),

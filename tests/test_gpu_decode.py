@@ -88,3 +88,65 @@ def test_prefill_cache_and_decode(kind, hkv, prune, keep_last, hd):
             ocache[mode] = [[(np.concatenate([ocache[mode][l][b][0], res[mode]["kv"][l][b][0]]),
                               np.concatenate([ocache[mode][l][b][1], res[mode]["kv"][l][b][1]]))
                              for b in range(len(lens))] for l in range(p.n_layers)]
+
+
+LONG_CASES = [
+    # kind, query heads, key/value heads, head_dim, rows in layer 0's cache per sequence
+    (W.DECODER, 8, 1, 128, [8500, 0, 300]),   # 8 query heads per cache head, 2 blocks per split
+    (W.DECODER, 8, 2, 64, [1030, 1, 257]),
+    (W.DECODER, 4, 4, 64, [700, 256, 255]),
+    (W.ENCODER, 4, 0, 128, [3000, 9, 511]),
+    (W.DECODER, 32, 8, 128, [600, 5, 0]),     # LLaMA-3-8B widths: d = 4096, 4 query heads per cache head
+    (W.ENCODER, 16, 0, 128, [400, 1, 70]),    # d = 2048, LayerNorm
+]
+
+
+@pytest.mark.parametrize("kind,H,hkv,hd,kv0", LONG_CASES)
+def test_decode_long_cache(kind, H, hkv, hd, kv0):
+    """Decode steps over long caches given directly (random k / v rows, a
+    second layer holding about half as many, as after pruning): several
+    splits per (sequence, head group) merged in-kernel, several row blocks
+    per split, splits past a short sequence's rows, and a cache holding
+    only the new row. Two steps against the oracle continued on the GPU's
+    cache, each step reproducible."""
+    B = len(kv0)
+    p = W.shrink(W.PRESETS["dec1b"], kind=kind, causal=True, n_layers=2, d_model=H * hd,
+                 n_heads=H, d_ff=512, batch=B, prune_after=(), n_kv_heads=hkv)
+    _, stack, _, _, dws, ocfg = build(p, 3, [8] * B, sharp=3.0)
+    kvd = p.kv_heads * hd
+    g = np.random.default_rng(sum(kv0) + hd)
+    kv_len = np.array([kv0, [n // 2 for n in kv0]], dtype=np.int32)
+    cap = int(kv_len.max()) + 3
+    host = np.zeros((2, B, cap, 2 * kvd), np.float32)
+    for l in range(2):
+        for b, n in enumerate(kv_len[l]):
+            host[l, b, :n, :kvd] = 2.0 * g.standard_normal((n, kvd))
+            host[l, b, :n, kvd:] = g.standard_normal((n, kvd))
+    cache = to_dev(host, "bf16").contiguous()
+    ws64 = [weights_f64(w) for w in dws]
+    for step in range(2):
+        gc = f64(cache)
+        ocache = [[(gc[l, b, :kv_len[l, b], :kvd], gc[l, b, :kv_len[l, b], kvd:])
+                   for b in range(B)] for l in range(2)]
+        x_new = to_dev(g.standard_normal((B, p.d_model)).astype(np.float32), "bf16")
+        pos_new = [int(n) + step for n in kv0]
+        before = kv_len.copy()
+        y = stack.decode_step(x_new, pos_new, cache, kv_len)
+        y2 = stack.decode_step(x_new, pos_new, cache, before.copy())
+        torch.cuda.synchronize()
+        assert torch.equal(y, y2)
+        x64 = f64(x_new)
+        res = {mode: O.decode_step(x64, np.array(pos_new), ocache, ws64, ocfg, mode=mode)
+               for mode in ("exact", "bf16")}
+        assert_rel_l2(f64(y), res["exact"]["x"], 2e-2, f"decode step {step}")
+        assert_rows_close(f64(y), res["bf16"]["x"], 5e-2, f"decode step {step}")
+        gc = f64(cache)
+        for l in range(2):
+            for b in range(B):
+                nk, nv = res["bf16"]["kv"][l][b]
+                row = gc[l, b, before[l, b]]
+                assert_rows_close(row[None, :kvd], nk, 5e-2, f"appended k, layer {l} seq {b}")
+                assert_rows_close(row[None, kvd:], nv, 5e-2, f"appended v, layer {l} seq {b}")
+                # rows before the new one are untouched
+                old = np.concatenate([ocache[l][b][0], ocache[l][b][1]], axis=1)
+                assert np.array_equal(gc[l, b, :before[l, b]], old)

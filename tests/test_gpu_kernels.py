@@ -219,6 +219,47 @@ def test_linear_kernel_regimes(m, n, k, split, epi, with_bias):
     assert_close(f64(y1[rt]), z, 1e-2, f"regime {m}x{n}x{k} epilogue {epi}")
 
 
+@pytest.mark.parametrize("m,n,k,hd", [(1, 384, 256, 64), (4, 6144, 4096, 128),
+                                      (4, 4096, 14336, 128), (16, 3072, 768, 64),
+                                      (3, 400, 512, 16), (7, 2304, 768, 64), (5, 512, 800, 64)])
+@pytest.mark.parametrize("epi", EPIS)
+def test_linear_few_rows(m, n, k, hd, epi):
+    """Products of at most 16 rows (one generated row per sequence): W
+    streamed into the matrix cores, one workgroup per 16 output columns
+    whose waves split K (k = 800: the last waves get a short range or
+    none) and add their sums in a fixed order. Every epilogue against the
+    oracle (the rotary one with each workgroup's columns paired across
+    half heads), results bit-identical over calls."""
+    g = np.random.default_rng(100 * m + n + k + epi)
+    x = g.standard_normal((m, k)).astype(np.float32)
+    w = (g.standard_normal((n, k)) / math.sqrt(k)).astype(np.float32)
+    bias = (0.1 * g.standard_normal(n)).astype(np.float32)
+    xd, wd, bd = to_dev(x, "bf16"), to_dev(w, "bf16"), to_dev(bias, "bf16")
+    res = to_dev(g.standard_normal((m, n)).astype(np.float32), "bf16") if epi == zsa.EPI_RESIDUAL else None
+    pos = g.integers(0, 4096, m).astype(np.int32)
+    posd = torch.from_numpy(pos).to(dev())
+    rope_cols = min(n, 8 * hd) // hd * hd
+    kw = dict(residual=res, pos=posd if epi == zsa.EPI_ROPE else None, head_dim=hd,
+              rope_cols=rope_cols, rope_theta=10000.0)
+    y1 = zsa.linear(xd, wd, bd, epi, **kw)
+    y2 = zsa.linear(xd, wd, bd, epi, **kw)
+    torch.cuda.synchronize()
+    assert torch.equal(y1, y2)
+    z = f64(xd) @ f64(wd).T + f64(bd)
+    if epi == zsa.EPI_NONE:
+        ref = z
+    elif epi == zsa.EPI_GELU:
+        ref = O.gelu(z)
+    elif epi == zsa.EPI_SWIGLU:
+        ref = O.silu(z[:, 0::2]) * z[:, 1::2]
+    elif epi == zsa.EPI_RESIDUAL:
+        ref = f64(res) + z
+    else:
+        ref = z.copy()
+        ref[:, :rope_cols] = O.rope(z[:, :rope_cols], pos.astype(np.int64), rope_cols // hd, 1e4)
+    assert_close(f64(y1), ref, 1e-2, f"few-row {m}x{n}x{k} epilogue {epi}")
+
+
 def test_linear_in_place_residual():
     g = np.random.default_rng(8)
     m, k, n = 129, 128, 256
