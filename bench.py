@@ -60,6 +60,8 @@ def parse():
     ap.add_argument("--no-graph", action="store_true", help="time eager launches instead")
     ap.add_argument("--forward-only", action="store_true",
                     help="skip the decode, backward and mark-mode legs (counter runs of the forward)")
+    ap.add_argument("--no-backward", action="store_true",
+                    help="skip the backward and mark-mode legs (traces of the forward and decode)")
     ap.add_argument("--cpu-seconds", type=float, default=15.0,
                     help="target wall time of the CPU-oracle sample (0 disables it)")
     ap.add_argument("--copy-calibration", type=int, default=0, metavar="BYTES",
@@ -353,14 +355,15 @@ def measure(p, rates, args, torch, W, zsa, dev, timing):
                 n, t = zsa.timing_read(c)
                 cls[name] = {"launches": n, "ms": t}
             rows_in, rows_after = layer_rows(p, plan)
-            if p.dtype == "bf16" and p.d_model // p.n_heads in (64, 128) and not args.forward_only:
+            if (p.dtype == "bf16" and p.d_model // p.n_heads in (64, 128) and not args.forward_only
+                    and not args.no_backward):
                 # the training step's backward (forward recomputed inside), as a graph
                 g = torch.Generator().manual_seed(args.seed)
                 dy = torch.randn(plan["final_rows"], p.d_model, generator=g).to(torch.bfloat16).to(dev)
                 stack.backward(xd, posd, seqs, p.prune_after, kr, dy)
                 r["backward_ms"] = graph_ms(
                     lambda: stack.backward(xd, posd, seqs, p.prune_after, kr, dy), args, torch)
-            if not args.forward_only:
+            if not args.forward_only and not args.no_backward:
                 mouts = mstack.forward(xd, posd, seqs, p.prune_after, kr)
                 r["mark_ms"] = graph_ms(
                     lambda: mstack.forward(xd, posd, seqs, p.prune_after, kr, out=mouts), args,
