@@ -1,21 +1,26 @@
 // Projections of the pre-norm block: y = epilogue(x W^T + bias).
 //
 // x [M, K] and W [N, K] are both K-contiguous ("NT" GEMM, PyTorch Linear
-// layout), so every MFMA operand fragment is one 16-byte load of 8
+// layout), so every MFMA operand fragment is one 16-byte run of 8
 // consecutive K values from a row of x or of W.
 //
-// bf16: 128x128 output tile per 256-thread workgroup (2x2 waves of 64x64),
-// K step 64, v_mfma_f32_32x32x16_bf16 with fp32 accumulation. Global tiles
-// are staged through registers into double-buffered, row-padded LDS (row
-// stride 72 bf16 = 144 bytes, so the 16 lanes of an LDS read phase hit 16
-// distinct 4-bank groups). One barrier per K step.
-// fp32: a 64x128 vector-ALU tile (4x8 outputs per thread).
+// bf16 kernels, fp32 accumulation, chosen by shape in launch_gemm:
+//  * gemm_bf16_dma_kernel: 128x128 tiles on 4 waves or 256x256 on 8, K
+//    slices loaded straight into swizzled LDS stages; split K for short
+//    grids, the slices summed in slice order by splitk_reduce_kernel;
+//  * gemm_bf16_persist_kernel: 128x128 tiles, two workgroups per CU walking
+//    their XCD's range of tiles, the epilogue from registers;
+//  * gemm_bf16_w4_kernel: 256x256 tiles on four waves of 128x128;
+//  * gemm_skinny_kernel: products of at most 16 rows (generation), W
+//    streamed into v_mfma_f32_16x16x32_bf16 operands;
+//  * gemm_bf16_mfma_kernel: the register-staged 128x128 original, kept as a
+//    tuning baseline (ZSA_GEMM_TILE).
+// The others use v_mfma_f32_32x32x16_bf16. fp32 storage: a 64x128
+// vector-ALU tile (4x8 outputs per thread).
 //
-// Both finish through the same epilogue: the fp32 accumulator tile is
-// written to LDS, then each thread produces 8 consecutive outputs of a row
-// (bias, exact GELU, SwiGLU on interleaved gate/up columns, residual add, or
-// the rotary rotation of head channel pairs (i, i+hd/2), which needs the
-// partner column of the same row) and stores them as one 16-byte vector.
+// Epilogues (all kernels, same order and precision): bias, exact GELU,
+// SwiGLU on interleaved gate/up columns, residual add, or the rotary
+// rotation of head channel pairs (i, i+hd/2).
 #include <math.h>
 #include <stdlib.h>
 
@@ -1261,192 +1266,170 @@ hipError_t launch_persist(hipStream_t s, const void* x, int M, int K, const void
 }
 
 // ---------------------------------------------------------------------------
-// bf16 GEMM, 8-wave ping-pong over BM x BN tiles, epilogue in registers
+// bf16 GEMM, 256x256 tiles on four waves of 128x128 (one wave per SIMD)
 // ---------------------------------------------------------------------------
-// Waves 0-3 (group 0) own the tile's upper BM/2 rows, waves 4-7 (group 1)
-// the lower ones; wave q of a group owns columns q*BN/4 .. +BN/4, and waves
-// q and q + 4 share a SIMD. K is walked in slices of 32: per slice a wave
-// has, per unit of 32, an R phase (read the unit's operand fragments from
-// LDS into registers) and a C phase (its MFMAs). Both groups run the same code with
-// a barrier after each phase, but group 1 passes one extra barrier first:
-// it runs one phase behind, so in every phase one wave of each SIMD issues
-// MFMAs while the other reads LDS, and the MFMA unit does not wait on LDS
-// reads or barriers. (The LDS traffic of the 128 x 64 per-wave tiles --
-// fragment reads plus the stage fills -- is close to what the LDS delivers
-// at the full MFMA rate, which bounds this design.)
-//
-// K slices of KB (32 or 64, one or two units of 32) live in a ring of NS
-// stages filled by buffer loads straight into
-// LDS (each wave loads 1/8 of a stage; the buffer range check turns rows
-// past M into zeros, whose outputs are dropped), in the swizzled layout of
-// gemm_bf16_dma_kernel. At the R phase of a slice's first unit a wave
-// starts its share of slice t + NS - 1, into the stage slice t - 1 used
-// (both groups have read it by then: group 1 one phase after group 0), and
-// at the R phase of the slice's last unit it waits for its share of slice
-// t + 1; group 1 does so one phase later, still before group 0 reads slice
-// t + 1. NS - 1 slices are in flight per wave.
-template <int BM, int BN, int KB, int NS, int EPI>
-__global__ __launch_bounds__(512) __attribute__((amdgpu_waves_per_eu(2, 2))) void
-gemm_bf16_pp_kernel(const bf16_t* __restrict__ X, const bf16_t* __restrict__ W, int M, int N,
-                    int K, EpiParams ep) {
+// Per 64-wide K slice a wave reads 32 fragments (32 KiB) for 64 MFMAs: two
+// thirds of the LDS reads per FLOP of four waves of 128x64. K slices of 64
+// (a stage row is one 128-byte line of a W or x row, so every 1 KiB load
+// fills 8 whole lines) live in two stages filled by buffer loads straight
+// into LDS, in the swizzled layout of gemm_bf16_dma_kernel (the buffer range
+// check turns rows past M into zeros, whose outputs are dropped). With one
+// wave per SIMD nothing else hides LDS latency or a barrier, so each slice
+// runs as two MFMA blocks and the work that would stall sits between their
+// MFMAs (the order is pinned with scheduling barriers):
+//   block A: MFMAs of the slice's first 32 K values, interleaved with the
+//            reads of its last 32 K values' fragments;
+//   wait for this wave's share of slice t + 1; barrier (publishes it, and
+//            every wave is done with the stage of slice t);
+//   block B: MFMAs of the last 32 K values, interleaved with the reads of
+//            slice t + 1's first fragments and the loads of slice t + 2 into
+//            the stage of slice t.
+// Loads past the last slice go to an offset past the buffers (they read
+// zeros into a stage that is not read again), so the loop body has no
+// branches and every wait count is fixed.
+template <int EPI>
+__global__ __launch_bounds__(256) void gemm_bf16_w4_kernel(const bf16_t* __restrict__ X,
+                                                          const bf16_t* __restrict__ W, int M,
+                                                          int N, int K, EpiParams ep) {
+  constexpr int BM = 256, BN = 256, KB = 64;
   using SL = Slice<KB>;
-  constexpr int UPS = KB / 32;                           // 32-wide units per slice
-  constexpr int WTM = BM / 2, WTN = BN / 4;
-  constexpr int TM = WTM / 32, TN = WTN / 32;
-  constexpr int SB = (BM + BN) * SL::RB;                 // bytes per stage
-  constexpr int LPW = (BM + BN) / SL::RPD / 8;           // 1 KiB loads per wave per stage
-  constexpr int ALD = BM / SL::RPD / 8;                  // of which A rows
-  static_assert(TM >= 1 && TN >= 1 && LPW * 8 * SL::RPD == BM + BN && ALD * 8 * SL::RPD == BM,
-                "tile shape");
-  static_assert((KB == 32 || KB == 64) && NS >= 2 && (NS - 2) * LPW < 64, "pipeline");
+  constexpr int SB = (BM + BN) * SL::RB;        // bytes per stage
+  constexpr int LPW = (BM + BN) / SL::RPD / 4;  // 1 KiB loads per wave per stage
+  constexpr int ALD = BM / SL::RPD / 4;         // of which A rows
+  static_assert(LPW == 16 && ALD == 8, "stage layout");
   extern __shared__ __align__(16) unsigned char smem[];
   const int tid = threadIdx.x;
   const int lane = tid & 63;
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
-  const int grp = wave >> 2, q = wave & 3;
+  const int wm = wave >> 1, wn = wave & 1;  // 2 x 2 waves of 128 x 128
   const int l32 = lane & 31, half = lane >> 5;
   int mt, nt;
   if (!xcd_tile<BM, BN>(M, N, &mt, &nt)) return;
   const int m0 = mt * BM, n0 = nt * BN;
   const int KT = K / KB;
-
-  // loads: wave w moves row blocks (i * 8 + w) of the stage, RPD rows each;
-  // stage row r = RPD blk + lr has swizzle (r / RPP) & (CPR - 1), with
-  // RPD / RPP = 4: it depends on blk only through the wave's parity (for
-  // 64-wide slices; not at all for 32-wide ones; the B rows start at an even
-  // block), so the lane's byte offset is common to every block
   const __amdgpu_buffer_rsrc_t xres =
       __builtin_amdgcn_make_buffer_rsrc(const_cast<bf16_t*>(X), 0, M * K * 2, 0x00020000);
   const __amdgpu_buffer_rsrc_t wres =
       __builtin_amdgcn_make_buffer_rsrc(const_cast<bf16_t*>(W), 0, N * K * 2, 0x00020000);
+  // wave w moves row blocks i * 4 + w (8 rows each; A rows, then B rows);
+  // stage row r = 8 blk + lr has swizzle (r / RPP) & (CPR - 1) =
+  // (4 blk + lr / 2) & 7, which depends on blk only through the wave's parity
   const int lr = lane / SL::CPR, lp = lane % SL::CPR;
   const uint32_t lane_off =
       static_cast<uint32_t>(lr * K * 2 + swz<KB>((wave & 1) * SL::RPD + lr, lp) * 16);
   typedef __attribute__((address_space(3))) void lds_void;
-  auto dma = [&](int s, int t) {
-#pragma unroll
-    for (int i = 0; i < LPW; ++i) {
-      const int blk = i * 8 + wave;
-      const uint32_t row0 = i < ALD ? static_cast<uint32_t>(m0 + blk * SL::RPD)
-                                    : static_cast<uint32_t>(n0 + blk * SL::RPD - BM);
-      const uint32_t off = (row0 * K + t * KB) * 2u + lane_off;
-      __builtin_amdgcn_raw_ptr_buffer_load_lds(i < ALD ? xres : wres,
-                                               (lds_void*)(smem + s * SB + blk * 1024), 16, off,
-                                               0, 0, 0);
-    }
+  auto dma1 = [&](int st, int t, int i) {
+    const int blk = i * 4 + wave;
+    const uint32_t row0 = i < ALD ? static_cast<uint32_t>(m0 + blk * SL::RPD)
+                                  : static_cast<uint32_t>(n0 + blk * SL::RPD - BM);
+    const uint32_t off = t < KT ? (row0 * K + t * KB) * 2u + lane_off : 0x80000000u;
+    __builtin_amdgcn_raw_ptr_buffer_load_lds(i < ALD ? xres : wres,
+                                             (lds_void*)(smem + st * SB + blk * 1024), 16, off, 0,
+                                             0, 0);
   };
-  // fragment addresses: row r (the lane's row of a 32-row block) and chunk
-  // c = 2 kk + half sit at r * RB + (c ^ ((r / RPP) & (CPR - 1))) * 16; the
-  // XOR term is (l32 / RPP) & (CPR - 1) for every block of the lane
+  // fragment q of k-substep kk: A block q (q < 4) or B block q - 4; row r of
+  // a 32-row block sits at r * RB, its chunk c at (c ^ ((r / RPP) & 7)) * 16
   const int sw = (l32 / SL::RPP) & (SL::CPR - 1);
-  int ab[KB / 16], bb[KB / 16];
+  int ab[4], bb[4];
 #pragma unroll
-  for (int kk = 0; kk < KB / 16; ++kk) {
-    const int ck = ((kk * 2 + half) ^ sw) * 16;
-    ab[kk] = (grp * WTM + l32) * SL::RB + ck;
-    bb[kk] = BM * SL::RB + (q * WTN + l32) * SL::RB + ck;
+  for (int kk = 0; kk < 4; ++kk) {
+    ab[kk] = (wm * 128 + l32) * SL::RB + ((kk * 2 + half) ^ sw) * 16;
+    bb[kk] = BM * SL::RB + (wn * 128 + l32) * SL::RB + ((kk * 2 + half) ^ sw) * 16;
   }
-  f32x16_t acc[TM][TN];
+  f32x16_t acc[4][4];
 #pragma unroll
-  for (int i = 0; i < TM; ++i)
+  for (int i = 0; i < 4; ++i)
 #pragma unroll
-    for (int j = 0; j < TN; ++j)
+    for (int j = 0; j < 4; ++j)
 #pragma unroll
       for (int r = 0; r < 16; ++r) acc[i][j][r] = 0.f;
-  bf16x8_t fa[2][TM], fb[2][TN];
-
-  // prologue: slices 0 .. NS - 2 in flight, slice 0 landed and published
-  const int pre = min(NS - 1, KT);
-  for (int t = 0; t < pre; ++t) dma(t, t);
+  // f0: fragments of k-substeps 0, 1 of a slice; f1: of k-substeps 2, 3
+  bf16x8_t f0[2][8], f1[2][8];
+  auto rd1 = [&](const unsigned char* st, int kk, bf16x8_t (&f)[8], int q) {
+    const int off = q < 4 ? ab[kk] + q * 32 * SL::RB : bb[kk] + (q - 4) * 32 * SL::RB;
+    f[q] = __builtin_bit_cast(bf16x8_t, *reinterpret_cast<const u32x4*>(st + off));
+  };
+  // MFMA p of a k-substep: output block (p / 4, p % 4), operands swapped so
+  // the accumulator holds C^T (four consecutive columns per register group)
+  auto mma1 = [&](bf16x8_t (&f)[8], int p) {
+    acc[p / 4][p % 4] =
+        __builtin_amdgcn_mfma_f32_32x32x16_bf16(f[4 + p % 4], f[p / 4], acc[p / 4][p % 4], 0, 0, 0);
+  };
+  // prologue: slices 0 and 1 in flight, slice 0 published, its first
+  // fragments read
+#pragma unroll
+  for (int i = 0; i < LPW; ++i) dma1(0, 0, i);
+#pragma unroll
+  for (int i = 0; i < LPW; ++i) dma1(1, 1, i);
   asm volatile("" ::: "memory");
-  if (pre == NS - 1)
-    __builtin_amdgcn_s_waitcnt(vmcnt_imm((NS - 2) * LPW));
-  else
-    __builtin_amdgcn_s_waitcnt(vmcnt_imm(0));
+  __builtin_amdgcn_s_waitcnt(vmcnt_imm(LPW));
   barrier_lds();
-  if (grp == 1) barrier_lds();
-  int s = 0;  // stage of slice t
-  for (int t = 0; t < KT; ++t) {
-    const int tn = t + NS - 1;
 #pragma unroll
-    for (int h = 0; h < UPS; ++h) {
-      // R phase of unit h of slice t
-      if (h == 0 && tn < KT) dma(s == 0 ? NS - 1 : s - 1, tn);
-      {
-        const unsigned char* st = smem + s * SB;
-#pragma unroll
-        for (int kk = 0; kk < 2; ++kk) {
-#pragma unroll
-          for (int i = 0; i < TM; ++i)
-            fa[kk][i] = __builtin_bit_cast(
-                bf16x8_t, *reinterpret_cast<const u32x4*>(st + ab[2 * h + kk] + i * 32 * SL::RB));
-#pragma unroll
-          for (int j = 0; j < TN; ++j)
-            fb[kk][j] = __builtin_bit_cast(
-                bf16x8_t, *reinterpret_cast<const u32x4*>(st + bb[2 * h + kk] + j * 32 * SL::RB));
-        }
-      }
-      if (h == UPS - 1) {
-        // this wave's share of slice t + 1 has landed (the slices after it
-        // that were issued may still be in flight)
-        asm volatile("" ::: "memory");
-        if (tn < KT)
-          __builtin_amdgcn_s_waitcnt(vmcnt_imm((NS - 2) * LPW));
-        else
-          __builtin_amdgcn_s_waitcnt(vmcnt_imm(0));
-      }
-      barrier_lds();
-      // C phase
-#pragma unroll
-      for (int kk = 0; kk < 2; ++kk)
-#pragma unroll
-        for (int i = 0; i < TM; ++i)
-#pragma unroll
-          for (int j = 0; j < TN; ++j)
-            acc[i][j] =
-                __builtin_amdgcn_mfma_f32_32x32x16_bf16(fb[kk][j], fa[kk][i], acc[i][j], 0, 0, 0);
-      barrier_lds();
-    }
-    s = s + 1 == NS ? 0 : s + 1;
+  for (int q = 0; q < 8; ++q) {
+    rd1(smem, 0, f0[0], q);
+    rd1(smem, 1, f0[1], q);
   }
-
-  reg_epilogue<TM, TN, EPI>(acc, m0 + grp * WTM, n0 + q * WTN, M, l32, half, ep);
-  // group 0 passes its last barrier here, matching group 1's first one
-  if (grp == 0) barrier_lds();
+  int s = 0;
+  for (int t = 0; t < KT; ++t) {
+    const unsigned char* cur = smem + s * SB;
+    const unsigned char* nxt = smem + (s ^ 1) * SB;
+    // block A
+#pragma unroll
+    for (int q = 0; q < 16; ++q) {
+      __builtin_amdgcn_sched_barrier(0);
+      mma1(f0[q / 8], 2 * (q % 8));
+      rd1(cur, 2 + q / 8, f1[q / 8], q % 8);
+      mma1(f0[q / 8], 2 * (q % 8) + 1);
+    }
+    __builtin_amdgcn_sched_barrier(0);
+    // slice t + 1 (the only loads in flight) has landed
+    asm volatile("" ::: "memory");
+    __builtin_amdgcn_s_waitcnt(vmcnt_imm(0));
+    barrier_lds();
+    // block B
+#pragma unroll
+    for (int q = 0; q < 16; ++q) {
+      __builtin_amdgcn_sched_barrier(0);
+      mma1(f1[q / 8], 2 * (q % 8));
+      rd1(nxt, q / 8, f0[q / 8], q % 8);
+      mma1(f1[q / 8], 2 * (q % 8) + 1);
+      dma1(s, t + 2, q);
+    }
+    __builtin_amdgcn_sched_barrier(0);
+    s ^= 1;
+  }
+  reg_epilogue<4, 4, EPI>(acc, m0 + wm * 128, n0 + wn * 128, M, l32, half, ep);
 }
 
-template <int BM, int BN, int KB, int NS, int EPI>
-hipError_t launch_pp1(hipStream_t s, const void* x, int M, int K, const void* w, int N,
-                      const EpiParams& ep) {
-  constexpr int lds = NS * (BM + BN) * KB * 2;
+template <int EPI>
+hipError_t launch_w4_1(hipStream_t s, const void* x, int M, int K, const void* w, int N,
+                       const EpiParams& ep) {
+  constexpr int lds = 2 * 512 * 64 * 2;
   static bool lds_raised = false;
   if (!lds_raised) {
     const hipError_t e = hipFuncSetAttribute(
-        reinterpret_cast<const void*>(gemm_bf16_pp_kernel<BM, BN, KB, NS, EPI>),
+        reinterpret_cast<const void*>(gemm_bf16_w4_kernel<EPI>),
         hipFuncAttributeMaxDynamicSharedMemorySize, lds);
     if (e != hipSuccess) return e;
     lds_raised = true;
   }
-  return launch(K_GEMM, gemm_bf16_pp_kernel<BM, BN, KB, NS, EPI>, xcd_grid(M, N, BM, BN),
-                dim3(512), lds, s, static_cast<const bf16_t*>(x), static_cast<const bf16_t*>(w),
-                M, N, K, ep);
+  return launch(K_GEMM, gemm_bf16_w4_kernel<EPI>, xcd_grid(M, N, 256, 256), dim3(256), lds, s,
+                static_cast<const bf16_t*>(x), static_cast<const bf16_t*>(w), M, N, K, ep);
 }
 
-// the ping-pong kernel takes the products the persistent one takes, with N a
-// multiple of BN and both operands below 2^31 bytes (buffer range checks)
-bool pp_ok(int M, int N, int K, const EpiParams& ep, int BN) {
-  return persist_ok(M, N, K, ep) && N % BN == 0 &&
+// the four-wave kernel takes the products the persistent one takes, with N a
+// multiple of 256 and both operands below 2^31 bytes (buffer range checks)
+bool w4_ok(int M, int N, int K, const EpiParams& ep) {
+  return persist_ok(M, N, K, ep) && N % 256 == 0 &&
          static_cast<int64_t>(M + 256) * K * 2 < (int64_t{1} << 31) &&
          static_cast<int64_t>(N) * K * 2 < (int64_t{1} << 31);
 }
 
-template <int BM, int BN, int KB, int NS>
-hipError_t launch_pp(hipStream_t s, const void* x, int M, int K, const void* w, int N,
+hipError_t launch_w4(hipStream_t s, const void* x, int M, int K, const void* w, int N,
                      const EpiParams& ep) {
-  if (ep.epi == EPI_GELU) return launch_pp1<BM, BN, KB, NS, EPI_GELU>(s, x, M, K, w, N, ep);
-  if (ep.epi == EPI_RESIDUAL)
-    return launch_pp1<BM, BN, KB, NS, EPI_RESIDUAL>(s, x, M, K, w, N, ep);
-  return launch_pp1<BM, BN, KB, NS, EPI_NONE>(s, x, M, K, w, N, ep);
+  if (ep.epi == EPI_GELU) return launch_w4_1<EPI_GELU>(s, x, M, K, w, N, ep);
+  if (ep.epi == EPI_RESIDUAL) return launch_w4_1<EPI_RESIDUAL>(s, x, M, K, w, N, ep);
+  return launch_w4_1<EPI_NONE>(s, x, M, K, w, N, ep);
 }
 
 template <int KB, int WPC>
@@ -1498,7 +1481,9 @@ hipError_t launch_dma(hipStream_t s, const void* x, int M, int K, const void* w,
 // on 8 waves; 1281 / 2563 / 2562 / 2561: direct-to-LDS 128x128, 256x128,
 // 256x256 on 4 and on 8 waves (64-wide K slices, 2 stages); 3241: 128x128
 // with 32-wide slices in 4 stages; 6431: 128x128 with 3 stages; 2542:
-// 256x256 on 4 waves (128x128 per wave) with 64-row epilogue passes.
+// 256x256 on 4 waves (128x128 per wave) with 64-row epilogue passes; 1289:
+// the persistent 128x128 kernel; 2544: the 256x256 four-wave kernel with
+// pinned MFMA / fragment-read interleaving and the epilogue in registers.
 int gemm_tile_override() {
   static const int v = [] {
     const char* e = getenv("ZSA_GEMM_TILE");
@@ -1651,31 +1636,22 @@ hipError_t launch_gemm(hipStream_t s, int dtype, const void* x, int M, int K, co
       case 1289:
         if (persist_ok(M, N, K, ep)) return launch_persist_any<64, 2>(s, x, M, K, w, N, ep);
         break;
-      case 2589:
-        if (pp_ok(M, N, K, ep, 256)) return launch_pp<256, 256, 64, 2>(s, x, M, K, w, N, ep);
-        break;
-      case 2584:
-        if (pp_ok(M, N, K, ep, 256)) return launch_pp<256, 256, 32, 4>(s, x, M, K, w, N, ep);
-        break;
-      case 1259:
-        if (pp_ok(M, N, K, ep, 256)) return launch_pp<128, 256, 64, 2>(s, x, M, K, w, N, ep);
-        break;
-      case 1256:
-        if (pp_ok(M, N, K, ep, 256)) return launch_pp<128, 256, 32, 6>(s, x, M, K, w, N, ep);
+      case 2544:
+        if (w4_ok(M, N, K, ep)) return launch_w4(s, x, M, K, w, N, ep);
         break;
       default: break;
     }
     // Measured on the projection shapes of the 768-wide stacks (N = 768,
     // 2304, 3072; K = 768, 3072; M = 2048 .. 16384): with M >= 12288 the
-    // ping-pong 256x256 tiles win for the GELU and residual projections; up
+    // 256x256 four-wave tiles win for the GELU and residual projections; up
     // to 1536 tiles of 128x128 the persistent kernel wins; the largest
     // grids without an epilogue op keep the 128x128 kernel. For longer K
     // (the 4096-wide decoder): direct-to-LDS 256x256 tiles over 8 waves
     // (128x64 per wave) once the grid holds at least four rounds of them.
     const long tiles128 = static_cast<long>((M + 127) / 128) * ((N + 127) / 128);
     if (K <= 3072 && persist_ok(M, N, K, ep)) {
-      if (M >= 12288 && ep.epi != EPI_NONE && pp_ok(M, N, K, ep, 256))
-        return launch_pp<256, 256, 64, 2>(s, x, M, K, w, N, ep);
+      if (M >= 12288 && ep.epi != EPI_NONE && w4_ok(M, N, K, ep))
+        return launch_w4(s, x, M, K, w, N, ep);
       if (tiles128 <= 1536) return launch_persist_any<64, 2>(s, x, M, K, w, N, ep);
     }
     const long tiles256 = static_cast<long>((M + 255) / 256) * ((N + 255) / 256);

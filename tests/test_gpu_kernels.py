@@ -185,7 +185,7 @@ def test_linear_split_k(m, n, k, epi):
     assert_close(f64(y0), ref, 1e-2, f"unsplit epilogue {epi}")
 
 
-@pytest.mark.parametrize("m,n,k,split", [(12289, 3072, 768, False),   # ping-pong 256x256 tiles
+@pytest.mark.parametrize("m,n,k,split", [(12289, 3072, 768, False),   # 256x256 tiles on four waves
                                          (12289, 768, 3072, False),
                                          (1000, 768, 768, False),     # persistent 128x128
                                          (4000, 768, 3072, False),
