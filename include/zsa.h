@@ -168,10 +168,11 @@ int zsa_norm(void* stream, int32_t dtype, int32_t kind, const void* x, const voi
  * partial sums. When the output tiles of a bf16 product are too few to
  * fill the GPU, K is split into slices whose fp32 partials are summed in a
  * fixed slice order before the epilogue (results are reproducible; they
- * may differ from the unsplit sum in the last bits). A bf16 product of at
- * most 16 rows (k a multiple of 32) streams w into the matrix cores, one
- * workgroup per 16 output columns whose waves split K and add their sums
- * in a fixed order (no workspace). With ws NULL the product is never split.
+ * may differ from the unsplit sum in the last bits). A short bf16 product
+ * (at most 64 rows, or 256 rows with n and k at most 1024; k a multiple of
+ * 32) streams w into the matrix cores, one workgroup per 16 output columns
+ * and 16 rows whose waves split K and add their sums in a fixed order (no
+ * workspace). With ws NULL the product is never split.
  * ws_bytes below zsa_linear_workspace_size() returns ZSA_EWORKSPACE.
  */
 int zsa_linear(void* stream, int32_t dtype, const void* x, int32_t m, int32_t k, const void* w,

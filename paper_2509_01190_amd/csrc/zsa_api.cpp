@@ -481,10 +481,6 @@ int zsa_linear(void* stream, int32_t dtype, const void* x, int32_t m, int32_t k,
       return fail(ZSA_EWORKSPACE, "linear workspace %zu < %zu bytes", ws_bytes, need);
   }
   hipStream_t s = static_cast<hipStream_t>(stream);
-  if (m > 0 && zsa::skinny_ok(dtype, m, n, k, ep)) {
-    HIP_TRY(zsa::launch_gemm_skinny(s, x, m, k, w, n, ep), "linear");
-    return ZSA_OK;
-  }
   HIP_TRY(zsa::launch_gemm(s, dtype, x, m, k, w, n, ep, ws, ws_bytes), "linear");
   return ZSA_OK;
 }
@@ -1286,7 +1282,6 @@ int zsa_decode_step(void* stream, const zsa_layer_cfg* cfg, const zsa_layer_weig
   // few-row projections stream W through the matrix cores; other shapes
   // take the general GEMM
   auto proj = [&](const void* x, int K, const void* wt, int N, const EpiParams& ep) -> hipError_t {
-    if (skinny_ok(c.dtype, batch, N, K, ep)) return launch_gemm_skinny(s, x, batch, K, wt, N, ep);
     return launch_gemm(s, c.dtype, x, batch, K, wt, N, ep, splitk, L.splitk_bytes);
   };
   // the block's pre-norm and the projection that reads it: folded into the

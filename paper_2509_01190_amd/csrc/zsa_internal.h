@@ -166,8 +166,9 @@ size_t gemm_workspace_bound(int dtype, int max_rows, int N, int K);
 
 int device_cu_count();  // compute units of the current device
 
-// Few-row product (M <= 16 rows of x, bf16): W streamed into MFMA operands,
-// one workgroup per 16 output columns over the whole of K (no workspace).
+// Few-row product (bf16, up to 4096 rows of x in blocks of 16): W streamed
+// into MFMA operands, one workgroup per 16 output columns and 16 rows over
+// the whole of K (no workspace).
 // With pn (gain non-null; skinny_norm_ok: M <= 8, K <= 4096, few output
 // tiles) x is first normalised as launch_norm would (LayerNorm with shift,
 // or RMSNorm).
@@ -178,6 +179,7 @@ struct PreNorm {
   float eps;
 };
 bool skinny_ok(int dtype, int M, int N, int K, const EpiParams& ep);
+bool skinny_pays(int M, int N, int K);  // launch_gemm takes it for such shapes
 bool skinny_norm_ok(int M, int N, int K);
 hipError_t launch_gemm_skinny(hipStream_t s, const void* x, int M, int K, const void* w, int N,
                               const EpiParams& ep, const PreNorm* pn = nullptr);

@@ -221,14 +221,17 @@ def test_linear_kernel_regimes(m, n, k, split, epi, with_bias):
 
 @pytest.mark.parametrize("m,n,k,hd", [(1, 384, 256, 64), (4, 6144, 4096, 128),
                                       (4, 4096, 14336, 128), (16, 3072, 768, 64),
-                                      (3, 400, 512, 16), (7, 2304, 768, 64), (5, 512, 800, 64)])
+                                      (3, 400, 512, 16), (7, 2304, 768, 64), (5, 512, 800, 64),
+                                      (17, 2304, 768, 64), (64, 3072, 768, 64),
+                                      (160, 768, 768, 64), (237, 768, 1024, 128)])
 @pytest.mark.parametrize("epi", EPIS)
 def test_linear_few_rows(m, n, k, hd, epi):
-    """Products of at most 16 rows (one generated row per sequence): W
-    streamed into the matrix cores, one workgroup per 16 output columns
-    whose waves split K (k = 800: the last waves get a short range or
-    none) and add their sums in a fixed order. Every epilogue against the
-    oracle (the rotary one with each workgroup's columns paired across
+    """Short products (generation rows, the short layers of the
+    every-layer schedule): W streamed into the matrix cores, one workgroup
+    per 16 output columns and 16 rows of x (ragged last blocks: 17, 237
+    rows), whose waves split K (k = 800: the last waves get a short range
+    or none) and add their sums in a fixed order. Every epilogue against
+    the oracle (the rotary one with each workgroup's columns paired across
     half heads), results bit-identical over calls."""
     g = np.random.default_rng(100 * m + n + k + epi)
     x = g.standard_normal((m, k)).astype(np.float32)
