@@ -43,14 +43,14 @@ __global__ __launch_bounds__(256) void kv_store_kernel(
 
 // decode_attn: grid (split, key/value head g, sequence b); a workgroup of
 // kDecWaves waves takes `rounds` blocks of kDecRows consecutive cache rows,
-// 64 rows per wave per block, for all G query heads that read head g
+// kDecRowsW rows per wave per block, for all G query heads that read head g
 // (grouped-query attention reads each cache row once per group).
 //  * scores: v_mfma_f32_16x16x32_bf16 with A = the G query rows (lane l:
 //    head l % 16, zero past G) and B = 16 cache rows of K (lane l: row
 //    l % 16), so lane l gets the scores of cache row l % 16 for heads
 //    4 (l / 16) .. + 3; K goes from memory straight into the operands.
 //  * online softmax per wave (running max per head, rescaled sums);
-//    probabilities go through a per-wave LDS strip [64 rows][G];
+//    probabilities go through a per-wave LDS strip [kDecRowsW rows][G];
 //  * P V on the vector ALU: each lane holds 16 bytes (8 columns) of V rows
 //    in registers, loaded row-contiguously together with K;
 //  * the waves' (max, sum, o) merge in wave order into the split's partial.
@@ -59,7 +59,8 @@ __global__ __launch_bounds__(256) void kv_store_kernel(
 // The new row's k / v (head g) are copied into cache row len - 1 by the
 // workgroup whose rows include it, before that workgroup reads the cache.
 constexpr int kDecWaves = 4;                     // waves per workgroup
-constexpr int kDecRowsW = 64;                    // cache rows per wave and block
+constexpr int kDecRowsW = 32;                    // cache rows per wave and block
+constexpr int kDecTiles = kDecRowsW / 16;         // 16-row score tiles per wave
 constexpr int kDecRows = kDecWaves * kDecRowsW;  // cache rows per workgroup and block
 
 typedef __bf16 dec_bf16x8_t __attribute__((ext_vector_type(8)));
@@ -128,9 +129,9 @@ __global__ __launch_bounds__(kDecWaves * 64) void decode_attn_kernel(
   for (int rd = 0; rd < rounds; ++rd) {
     const int r0 = row0 + rd * kDecRows + wave * kDecRowsW;
     if (r0 >= row_end) break;
-    u32x4 kr[4][KS], vreg[NVI];
+    u32x4 kr[kDecTiles][KS], vreg[NVI];
 #pragma unroll
-    for (int i = 0; i < 4; ++i)
+    for (int i = 0; i < kDecTiles; ++i)
 #pragma unroll
       for (int j = 0; j < KS; ++j)
         kr[i][j] = __builtin_bit_cast(
@@ -140,9 +141,9 @@ __global__ __launch_bounds__(kDecWaves * 64) void decode_attn_kernel(
       vreg[jj] = __builtin_bit_cast(
           u32x4, __builtin_amdgcn_raw_buffer_load_b128(res, voff + (r0 + RPI * jj) * rowb, 0, 0));
     __builtin_amdgcn_sched_barrier(0);
-    dec_f32x4_t sc[4];
+    dec_f32x4_t sc[kDecTiles];
 #pragma unroll
-    for (int i = 0; i < 4; ++i) {
+    for (int i = 0; i < kDecTiles; ++i) {
       sc[i] = dec_f32x4_t{0.f, 0.f, 0.f, 0.f};
 #pragma unroll
       for (int j = 0; j < KS; ++j)
@@ -154,7 +155,7 @@ __global__ __launch_bounds__(kDecWaves * 64) void decode_attn_kernel(
     for (int r = 0; r < 4; ++r) {
       float mx = -INFINITY;
 #pragma unroll
-      for (int i = 0; i < 4; ++i) {
+      for (int i = 0; i < kDecTiles; ++i) {
         const float v = r0 + 16 * i + l16 < n ? sc[i][r] * scale_log2 : -INFINITY;
         sc[i][r] = v;
         mx = fmaxf(mx, v);
@@ -166,7 +167,7 @@ __global__ __launch_bounds__(kDecWaves * 64) void decode_attn_kernel(
       m_run[r] = mnew;
       float ls = 0.f;
 #pragma unroll
-      for (int i = 0; i < 4; ++i) {
+      for (int i = 0; i < kDecTiles; ++i) {
         const float p = __builtin_amdgcn_exp2f(sc[i][r] - mnew);
         ls += p;
         if (4 * kg + r < G) pw[(16 * i + l16) * G + 4 * kg + r] = p;
@@ -248,37 +249,45 @@ __global__ __launch_bounds__(kDecWaves * 64) void decode_attn_kernel(
 }
 
 // grid (query head h, sequence b), one thread per channel: the S (at most
-// kDecMaxSplits) split partials of (b, h), all loaded at once, merged in
-// split order; splits without rows hold (-inf, 0, 0) and weigh 0
-constexpr int kDecMaxSplits = 32;
+// kDecMaxSplits) split partials of (b, h) merged in split order, loaded 16
+// at a time; splits without rows hold (-inf, 0, 0) and weigh 0
+constexpr int kDecMaxSplits = 64;
 
 template <int HD>
 __global__ __launch_bounds__(HD) void decode_combine_kernel(
     const float* __restrict__ m_part, const float* __restrict__ l_part,
     const float* __restrict__ o_part, int S, int H, bf16_t* __restrict__ out, int64_t out_stride) {
+  constexpr int U = 16;
   const int h = blockIdx.x, b = blockIdx.y, c = threadIdx.x;
   const int64_t hb = (static_cast<int64_t>(b) * H + h) * S;
-  float mv[kDecMaxSplits], lv[kDecMaxSplits], ov[kDecMaxSplits];
-#pragma unroll
-  for (int y = 0; y < kDecMaxSplits; ++y) {
-    mv[y] = -INFINITY;
-    lv[y] = 0.f;
-    ov[y] = 0.f;
-    if (y < S) {
-      mv[y] = m_part[hb + y];
-      lv[y] = l_part[hb + y];
-      ov[y] = o_part[(hb + y) * HD + c];
-    }
-  }
   float M = -INFINITY;
+  for (int y0 = 0; y0 < S; y0 += U) {
+    float mv[U];
 #pragma unroll
-  for (int y = 0; y < kDecMaxSplits; ++y) M = fmaxf(M, mv[y]);
+    for (int u = 0; u < U; ++u) mv[u] = y0 + u < S ? m_part[hb + y0 + u] : -INFINITY;
+#pragma unroll
+    for (int u = 0; u < U; ++u) M = fmaxf(M, mv[u]);
+  }
   float L = 0.f, Ov = 0.f;
+  for (int y0 = 0; y0 < S; y0 += U) {
+    float mv[U], lv[U], ov[U];
 #pragma unroll
-  for (int y = 0; y < kDecMaxSplits; ++y) {
-    const float f = __builtin_amdgcn_exp2f(mv[y] - M);
-    L = fmaf(lv[y], f, L);
-    Ov = fmaf(ov[y], f, Ov);
+    for (int u = 0; u < U; ++u) {
+      mv[u] = -INFINITY;
+      lv[u] = 0.f;
+      ov[u] = 0.f;
+      if (y0 + u < S) {
+        mv[u] = m_part[hb + y0 + u];
+        lv[u] = l_part[hb + y0 + u];
+        ov[u] = o_part[(hb + y0 + u) * HD + c];
+      }
+    }
+#pragma unroll
+    for (int u = 0; u < U; ++u) {
+      const float f = __builtin_amdgcn_exp2f(mv[u] - M);
+      L = fmaf(lv[u], f, L);
+      Ov = fmaf(ov[u], f, Ov);
+    }
   }
   out[static_cast<int64_t>(b) * out_stride + h * HD + c] = f32_to_bf16(Ov / L);
 }
