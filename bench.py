@@ -77,8 +77,8 @@ def parse():
 
 GEMM_SRC = os.path.join(ROOT, "paper_2509_01190_amd", "csrc", "k_gemm.hip")
 TRAFFIC_FILE = os.path.join(ROOT, "profiles", "gemm_traffic.json")
-GEMM_KERNEL_TAG = "gemm_bf16_"
-REDUCE_KERNEL_TAG = "splitk_reduce"
+GEMM_KERNEL_TAGS = ("gemm_bf16_", "gemm_skinny_")
+REDUCE_KERNEL_TAGS = ("splitk_reduce",)
 
 
 def gemm_source_hash():
@@ -87,40 +87,40 @@ def gemm_source_hash():
         return hashlib.sha256(f.read()).hexdigest()[:16]
 
 
-def pmc_sum(csv_path, counter, name_filter):
+def pmc_sum(csv_path, counter, name_tags):
     """Sum over dispatches (KiB for FETCH_SIZE / WRITE_SIZE) of a counter for
-    the kernels whose name contains name_filter, and the dispatch count."""
+    the kernels whose name contains one of name_tags, and the dispatch count."""
     import csv
     import collections
     per = collections.defaultdict(float)
     with open(csv_path) as f:
         for r in csv.DictReader(f):
-            if r["Counter_Name"] == counter and name_filter in r["Kernel_Name"]:
+            if r["Counter_Name"] == counter and any(g in r["Kernel_Name"] for g in name_tags):
                 per[r["Dispatch_Id"]] += float(r["Counter_Value"])
     return sum(per.values()), len(per)
 
 
 def summarize_pmc(args):
     """FETCH_SIZE / WRITE_SIZE of the projections of a bench run (the GEMM
-    kernel and, where K is split, its reduce kernel), per projection (one
-    GEMM dispatch each), scaled by the ratio of true to counted bytes of a
+    kernel -- one of the tiled kernels or the few-row kernel -- and, where K
+    is split, its reduce kernel), per projection (one GEMM dispatch each), scaled by the ratio of true to counted bytes of a
     plain copy kernel."""
     f_csv, w_csv, cf_csv, cw_csv = args.summarize_pmc
-    fetch_g, n_f = pmc_sum(f_csv, "FETCH_SIZE", GEMM_KERNEL_TAG)
-    write_g, n_w = pmc_sum(w_csv, "WRITE_SIZE", GEMM_KERNEL_TAG)
-    fetch_r, n_fr = pmc_sum(f_csv, "FETCH_SIZE", REDUCE_KERNEL_TAG)
-    write_r, n_wr = pmc_sum(w_csv, "WRITE_SIZE", REDUCE_KERNEL_TAG)
+    fetch_g, n_f = pmc_sum(f_csv, "FETCH_SIZE", GEMM_KERNEL_TAGS)
+    write_g, n_w = pmc_sum(w_csv, "WRITE_SIZE", GEMM_KERNEL_TAGS)
+    fetch_r, n_fr = pmc_sum(f_csv, "FETCH_SIZE", REDUCE_KERNEL_TAGS)
+    write_r, n_wr = pmc_sum(w_csv, "WRITE_SIZE", REDUCE_KERNEL_TAGS)
     if not n_f or not n_w:
         raise SystemExit("no GEMM dispatches in the counter files")
-    copy_f, n_cf = pmc_sum(cf_csv, "FETCH_SIZE", "copyBuffer")
-    copy_w, n_cw = pmc_sum(cw_csv, "WRITE_SIZE", "copyBuffer")
+    copy_f, n_cf = pmc_sum(cf_csv, "FETCH_SIZE", ("copyBuffer",))
+    copy_w, n_cw = pmc_sum(cw_csv, "WRITE_SIZE", ("copyBuffer",))
     copy_f, copy_w = copy_f / max(n_cf, 1), copy_w / max(n_cw, 1)
     f_scale = args.copy_bytes / (copy_f * 1024.0)
     w_scale = args.copy_bytes / (copy_w * 1024.0)
     fetch_kib = (fetch_g + fetch_r) / n_f
     write_kib = (write_g + write_r) / n_w
     out = {
-        "kernel": "projections: gemm_bf16_* plus splitk_reduce_kernel where K is split "
+        "kernel": "projections: gemm_bf16_* or gemm_skinny_kernel, plus splitk_reduce_kernel where K is split "
                   "(one bench run, headline workload)",
         "gemm_source_sha256_16": gemm_source_hash(),
         "gemm_dispatches": [n_f, n_w], "reduce_dispatches": [n_fr, n_wr],
@@ -523,7 +523,7 @@ def main():
     g_flops = sum(results[r]["gemm_flops"] for r in rates)
     achieved = g_flops / (g_ms * 1e-3) / 1e12 if g_ms > 0 else 0.0
     traffic = measured_traffic()
-    roofline = {"kernel": "projections (gemm_bf16_* and, where K is split, splitk_reduce_kernel)",
+    roofline = {"kernel": "projections (gemm_bf16_* or gemm_skinny_kernel, plus splitk_reduce_kernel where K is split)",
                 "bound": "mfma", "achieved": round(achieved, 1), "peak": PEAK_BF16_TFLOPS,
                 "unit": "TFLOP/s", "frac": round(achieved / PEAK_BF16_TFLOPS, 4),
                 "traffic": None if traffic is None else round(traffic),
