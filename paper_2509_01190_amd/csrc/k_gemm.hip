@@ -25,6 +25,7 @@
 #include <stdlib.h>
 
 #include <algorithm>
+#include <type_traits>
 
 #include "zsa_internal.h"
 
@@ -331,6 +332,78 @@ inline dim3 xcd_grid(int M, int N, int BM, int BN) {
   return dim3(static_cast<unsigned>(kXcds * ((tiles + kXcds - 1) / kXcds)));
 }
 
+// Stores from the accumulators. The operand-swapped 32x32 MFMA leaves lane l
+// (half h = l / 32) with four consecutive columns 8g + 4h .. 8g + 4h + 3 of
+// row l % 32 of its 32 x 32 block in register group g, 8 bytes. A
+// v_permlane32_swap of each dword of groups g and g + 1 (g even) exchanges
+// the upper lanes' group-g words with the lower lanes' group-(g + 1) words:
+// the lower lanes then hold all eight columns of group g and the upper lanes
+// those of group g + 1, so each lane stores 16 contiguous bytes and one store
+// instruction covers 32 bytes of each of 32 rows (half as many stores as
+// 8-byte ones). A residual is read the same way and swapped back.
+__device__ __forceinline__ void lane_swap(uint32_t& lo, uint32_t& hi) {
+  const auto r = __builtin_amdgcn_permlane32_swap(lo, hi, false, false);
+  lo = r[0];
+  hi = r[1];
+}
+
+// residual of columns nc .. nc + 31 of row m: r[p] = the 16 bytes at column
+// nc + (2p + half) * 8, as loaded (res_epilogue32 swaps them)
+__device__ __forceinline__ void res_load32(__amdgpu_buffer_rsrc_t rres, uint32_t m, int nc, int half,
+                                           int ldy, uint32_t (&r)[2][4]) {
+#pragma unroll
+  for (int p = 0; p < 2; ++p) {
+    const auto v = __builtin_amdgcn_raw_buffer_load_b128(
+        rres, (m * static_cast<uint32_t>(ldy) + static_cast<uint32_t>(nc + (2 * p + half) * 8)) * 2u, 0, 0);
+    r[p][0] = v[0];
+    r[p][1] = v[1];
+    r[p][2] = v[2];
+    r[p][3] = v[3];
+  }
+}
+
+// epilogue of one 32 x 32 accumulator block: rows m (this lane's), columns
+// nc .. nc + 31; bw[g] = the bias of the lane's four columns of group g
+template <int EPI>
+__device__ __forceinline__ void epi_store32(const f32x16_t& a, const uint2 (&bw)[4], uint32_t (&r)[2][4],
+                                            __amdgpu_buffer_rsrc_t yres, uint32_t m, int nc, int half,
+                                            int ldy) {
+#pragma unroll
+  for (int p = 0; p < 2; ++p) {
+    if (EPI == EPI_RESIDUAL) {
+      lane_swap(r[p][0], r[p][2]);
+      lane_swap(r[p][1], r[p][3]);
+    }
+    uint32_t pk[2][2];
+#pragma unroll
+    for (int gg = 0; gg < 2; ++gg) {
+      const int g = 2 * p + gg;
+      float z[4];
+      z[0] = a[4 * g + 0] + __uint_as_float(bw[g].x << 16);
+      z[1] = a[4 * g + 1] + __uint_as_float(bw[g].x & 0xffff0000u);
+      z[2] = a[4 * g + 2] + __uint_as_float(bw[g].y << 16);
+      z[3] = a[4 * g + 3] + __uint_as_float(bw[g].y & 0xffff0000u);
+      if (EPI == EPI_GELU) {
+#pragma unroll
+        for (int e = 0; e < 4; ++e) z[e] = gelu_erf(z[e]);
+      } else if (EPI == EPI_RESIDUAL) {
+        z[0] += __uint_as_float(r[p][2 * gg] << 16);
+        z[1] += __uint_as_float(r[p][2 * gg] & 0xffff0000u);
+        z[2] += __uint_as_float(r[p][2 * gg + 1] << 16);
+        z[3] += __uint_as_float(r[p][2 * gg + 1] & 0xffff0000u);
+      }
+      pk[gg][0] = pack_bf16x2(z[0], z[1]);
+      pk[gg][1] = pack_bf16x2(z[2], z[3]);
+    }
+    lane_swap(pk[0][0], pk[1][0]);
+    lane_swap(pk[0][1], pk[1][1]);
+    typedef uint32_t u32x4v __attribute__((ext_vector_type(4)));
+    const u32x4v v = {pk[0][0], pk[0][1], pk[1][0], pk[1][1]};
+    __builtin_amdgcn_raw_buffer_store_b128(
+        v, yres, (m * static_cast<uint32_t>(ldy) + static_cast<uint32_t>(nc + (2 * p + half) * 8)) * 2u, 0, 0);
+  }
+}
+
 // Epilogue from the accumulators of a wave whose block starts at row mb,
 // column nb: acc[i][j][4g + e] = C[m][n + e], m = mb + 32 i + l32,
 // n = nb + 32 j + 8 g + 4 half (the operand-swapped MFMA holds C^T); bias,
@@ -355,40 +428,10 @@ __device__ __forceinline__ void reg_epilogue(const f32x16_t (&acc)[TM][TN], int 
                   : make_uint2(0u, 0u);
 #pragma unroll
     for (int i = 0; i < TM; ++i) {
-      const int m = mb + i * 32 + l32;
-      uint32_t res[4][2];
-      if (EPI == EPI_RESIDUAL) {
-#pragma unroll
-        for (int g = 0; g < 4; ++g) {
-          const int n = nb + j * 32 + g * 8 + half * 4;
-          const auto v = __builtin_amdgcn_raw_buffer_load_b64(
-              rres, (static_cast<uint32_t>(m) * ep.ldy + n) * 2u, 0, 0);
-          res[g][0] = v[0];
-          res[g][1] = v[1];
-        }
-      }
-#pragma unroll
-      for (int g = 0; g < 4; ++g) {
-        const int n = nb + j * 32 + g * 8 + half * 4;
-        float z[4];
-        z[0] = acc[i][j][4 * g + 0] + __uint_as_float(bw[g].x << 16);
-        z[1] = acc[i][j][4 * g + 1] + __uint_as_float(bw[g].x & 0xffff0000u);
-        z[2] = acc[i][j][4 * g + 2] + __uint_as_float(bw[g].y << 16);
-        z[3] = acc[i][j][4 * g + 3] + __uint_as_float(bw[g].y & 0xffff0000u);
-        if (EPI == EPI_GELU) {
-#pragma unroll
-          for (int e = 0; e < 4; ++e) z[e] = gelu_erf(z[e]);
-        } else if (EPI == EPI_RESIDUAL) {
-          z[0] += __uint_as_float(res[g][0] << 16);
-          z[1] += __uint_as_float(res[g][0] & 0xffff0000u);
-          z[2] += __uint_as_float(res[g][1] << 16);
-          z[3] += __uint_as_float(res[g][1] & 0xffff0000u);
-        }
-        typedef uint32_t u32x2 __attribute__((ext_vector_type(2)));
-        const u32x2 v = {pack_bf16x2(z[0], z[1]), pack_bf16x2(z[2], z[3])};
-        __builtin_amdgcn_raw_buffer_store_b64(v, yres, (static_cast<uint32_t>(m) * ep.ldy + n) * 2u,
-                                              0, 0);
-      }
+      const uint32_t m = static_cast<uint32_t>(mb + i * 32 + l32);
+      uint32_t r[2][4];
+      if (EPI == EPI_RESIDUAL) res_load32(rres, m, nb + j * 32, half, ep.ldy, r);
+      epi_store32<EPI>(acc[i][j], bw, r, yres, m, nb + j * 32, half, ep.ldy);
     }
   }
 }
@@ -1100,7 +1143,7 @@ gemm_bf16_persist_kernel(const bf16_t* __restrict__ X, const bf16_t* __restrict_
       for (int j = 0; j < TN; ++j)
 #pragma unroll
         for (int r = 0; r < 16; ++r) acc[i][j][r] = 0.f;
-    uint32_t res[TM][TN][4][2];
+    uint32_t res[TM][TN][2][4];
     uint2 bw[TN][4];
 #pragma unroll
     for (int j = 0; j < TN; ++j)
@@ -1126,14 +1169,8 @@ gemm_bf16_persist_kernel(const bf16_t* __restrict__ X, const bf16_t* __restrict_
       if (EPI == EPI_RESIDUAL) {                                                         \
         _Pragma("unroll") for (int i = 0; i < TM; ++i)                                   \
           _Pragma("unroll") for (int j = 0; j < TN; ++j)                                 \
-            _Pragma("unroll") for (int g = 0; g < 4; ++g) {                              \
-              const int m = m0 + wm * WTM + i * 32 + l32;                                \
-              const int n = n0 + wn * WTN + j * 32 + g * 8 + half * 4;                   \
-              const auto v = __builtin_amdgcn_raw_buffer_load_b64(                       \
-                  rres, (static_cast<uint32_t>(m) * ep.ldy + n) * 2u, 0, 0);             \
-              res[i][j][g][0] = v[0];                                                    \
-              res[i][j][g][1] = v[1];                                                    \
-            }                                                                            \
+            res_load32(rres, static_cast<uint32_t>(m0 + wm * WTM + i * 32 + l32),        \
+                       n0 + wn * WTN + j * 32, half, ep.ldy, res[i][j]);                 \
       }                                                                                  \
     }                                                                                    \
     const unsigned char* st = smem + (S) * SB;                                           \
@@ -1193,28 +1230,9 @@ gemm_bf16_persist_kernel(const bf16_t* __restrict__ X, const bf16_t* __restrict_
     for (int i = 0; i < TM; ++i)
 #pragma unroll
       for (int j = 0; j < TN; ++j)
-#pragma unroll
-        for (int g = 0; g < 4; ++g) {
-          const int m = m0 + wm * WTM + i * 32 + l32;
-          const int n = n0 + wn * WTN + j * 32 + g * 8 + half * 4;
-          float z[4];
-          z[0] = acc[i][j][4 * g + 0] + __uint_as_float(bw[j][g].x << 16);
-          z[1] = acc[i][j][4 * g + 1] + __uint_as_float(bw[j][g].x & 0xffff0000u);
-          z[2] = acc[i][j][4 * g + 2] + __uint_as_float(bw[j][g].y << 16);
-          z[3] = acc[i][j][4 * g + 3] + __uint_as_float(bw[j][g].y & 0xffff0000u);
-          if (EPI == EPI_GELU) {
-#pragma unroll
-            for (int e = 0; e < 4; ++e) z[e] = gelu_erf(z[e]);
-          } else if (EPI == EPI_RESIDUAL) {
-            z[0] += __uint_as_float(res[i][j][g][0] << 16);
-            z[1] += __uint_as_float(res[i][j][g][0] & 0xffff0000u);
-            z[2] += __uint_as_float(res[i][j][g][1] << 16);
-            z[3] += __uint_as_float(res[i][j][g][1] & 0xffff0000u);
-          }
-          typedef uint32_t u32x2 __attribute__((ext_vector_type(2)));
-          const u32x2 v = {pack_bf16x2(z[0], z[1]), pack_bf16x2(z[2], z[3])};
-          __builtin_amdgcn_raw_buffer_store_b64(v, yres, (static_cast<uint32_t>(m) * ep.ldy + n) * 2u, 0, 0);
-        }
+        epi_store32<EPI>(acc[i][j], bw[j], res[i][j], yres,
+                         static_cast<uint32_t>(m0 + wm * WTM + i * 32 + l32), n0 + wn * WTN + j * 32,
+                         half, ep.ldy);
     if (!more) break;
     k = knext;
     m0 = m0n;
@@ -1244,10 +1262,13 @@ int device_cus() {
 }
 
 // the persistent kernel takes bf16 products with N a multiple of 128, K a
-// multiple of 64, no rotary / SwiGLU epilogue, and buffers below 2^31 bytes
+// multiple of 64, no rotary / SwiGLU epilogue, buffers below 2^31 bytes, and
+// output (and residual) rows of whole 16-byte units on 16-byte boundaries
 bool persist_ok(int M, int N, int K, const EpiParams& ep) {
   if (N % 128 != 0 || K % 64 != 0 || K < 64 || M <= 0) return false;
-  if (reinterpret_cast<uintptr_t>(ep.bias) % 8 != 0 || ep.ldy % 4 != 0) return false;
+  if (reinterpret_cast<uintptr_t>(ep.bias) % 8 != 0 || ep.ldy % 8 != 0) return false;
+  if (reinterpret_cast<uintptr_t>(ep.y) % 16 != 0 || reinterpret_cast<uintptr_t>(ep.residual) % 16 != 0)
+    return false;
   if (ep.epi != EPI_NONE && ep.epi != EPI_GELU && ep.epi != EPI_RESIDUAL) return false;
   return static_cast<int64_t>(M + 128) * ep.ldy * 2 < (int64_t{1} << 31);
 }
@@ -1423,6 +1444,255 @@ hipError_t launch_w4_1(hipStream_t s, const void* x, int M, int K, const void* w
                 static_cast<const bf16_t*>(x), static_cast<const bf16_t*>(w), M, N, K, ep);
 }
 
+// Epilogue of gemm_bf16_w4p_kernel: reg_epilogue with the bias read from
+// LDS (blds holds the bf16 bias of columns nb, nb + 1, ...; zeros when the
+// product has none), one 32 x 32 block at a time in a pinned order (the
+// scheduler would otherwise read every accumulator out at once).
+template <int TM, int TN, int EPI>
+__device__ __forceinline__ void reg_epilogue_lb(const f32x16_t (&acc)[TM][TN], int mb, int nb, int M,
+                                                int l32, int half, const EpiParams& ep,
+                                                const unsigned char* blds) {
+  const int ybytes = M * ep.ldy * 2;
+  const __amdgpu_buffer_rsrc_t yres = __builtin_amdgcn_make_buffer_rsrc(ep.y, 0, ybytes, 0x00020000);
+  const __amdgpu_buffer_rsrc_t rres = __builtin_amdgcn_make_buffer_rsrc(
+      const_cast<void*>(EPI == EPI_RESIDUAL ? ep.residual : ep.y), 0, ybytes, 0x00020000);
+#pragma unroll
+  for (int j = 0; j < TN; ++j) {
+    uint2 bw[4];
+#pragma unroll
+    for (int g = 0; g < 4; ++g)
+      bw[g] = *reinterpret_cast<const uint2*>(blds + (j * 32 + g * 8 + half * 4) * 2);
+#pragma unroll
+    for (int i = 0; i < TM; ++i) {
+      __builtin_amdgcn_sched_barrier(0);
+      const uint32_t m = static_cast<uint32_t>(mb + i * 32 + l32);
+      uint32_t r[2][4];
+      if (EPI == EPI_RESIDUAL) res_load32(rres, m, nb + j * 32, half, ep.ldy, r);
+      epi_store32<EPI>(acc[i][j], bw, r, yres, m, nb + j * 32, half, ep.ldy);
+    }
+  }
+}
+
+// ---------------------------------------------------------------------------
+// bf16 GEMM, persistent form of the four-wave kernel
+// ---------------------------------------------------------------------------
+// One workgroup per CU walks a strided share of its XCD's range of 256x256
+// tiles (the grouped order above) and streams their K slices as one
+// sequence: the loads of slice g + 2 run on into the next tile, so when the
+// last slice of a tile has been multiplied, the first slices of the next are
+// in flight or landed and the finished tile's epilogue overlaps them (a
+// workgroup per tile would instead start each tile by waiting for its first
+// slice). The slice loop is that of gemm_bf16_w4_kernel. The bias of a tile
+// travels with its first slice, as a direct-to-LDS load into one of two
+// 1 KiB buffers (by tile parity), so the epilogue waits for no global load:
+// such a wait would also wait for the slice loads issued before it, since
+// vector memory operations complete in issue order. A tile's accumulators
+// restart from MFMAs whose C operand is zero. K is at least two slices, so a
+// bias buffer is refilled only after every wave has passed the epilogue that
+// read it (the refill is issued after a barrier of the next tile).
+template <int EPI>
+__global__ __launch_bounds__(256) void gemm_bf16_w4p_kernel(const bf16_t* __restrict__ X,
+                                                           const bf16_t* __restrict__ W, int M,
+                                                           int N, int K, EpiParams ep) {
+  constexpr int BM = 256, BN = 256, KB = 64;
+  using SL = Slice<KB>;
+  constexpr int SB = (BM + BN) * SL::RB;        // bytes per stage
+  constexpr int LPW = (BM + BN) / SL::RPD / 4;  // 1 KiB loads per wave per stage
+  constexpr int ALD = BM / SL::RPD / 4;         // of which A rows
+  static_assert(LPW == 16 && ALD == 8, "stage layout");
+  extern __shared__ __align__(16) unsigned char smem[];
+  unsigned char* const blds = smem + 2 * SB;  // bias buffers, 1 KiB each
+  const int tid = threadIdx.x;
+  const int lane = tid & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+  const int wm = wave >> 1, wn = wave & 1;  // 2 x 2 waves of 128 x 128
+  const int l32 = lane & 31, half = lane >> 5;
+
+  const int nM = (M + BM - 1) / BM, nN = N / BN;
+  const int tiles = nM * nN;
+  const int xcd = blockIdx.x % kXcds, slot = blockIdx.x / kXcds;
+  const int slots = gridDim.x / kXcds;
+  const int per = tiles / kXcds, extra = tiles % kXcds;
+  const int tbeg = xcd * per + min(xcd, extra);
+  const int tcount = per + (xcd < extra ? 1 : 0);
+  if (slot >= tcount) return;
+  const int count = (tcount - slot + slots - 1) / slots;  // tiles of this workgroup
+  const int KT = K / KB;
+  auto tile_at = [&](int p, int* m0, int* n0) {
+    const int t = tbeg + slot + p * slots;
+    const int g = t / (kXcdGroup * nN);
+    const int gm0 = g * kXcdGroup;
+    const int gsz = min(kXcdGroup, nM - gm0);
+    const int r = t - g * kXcdGroup * nN;
+    *n0 = (r / gsz) * BN;
+    *m0 = (gm0 + r % gsz) * BM;
+  };
+  const __amdgpu_buffer_rsrc_t xres =
+      __builtin_amdgcn_make_buffer_rsrc(const_cast<bf16_t*>(X), 0, M * K * 2, 0x00020000);
+  const __amdgpu_buffer_rsrc_t wres =
+      __builtin_amdgcn_make_buffer_rsrc(const_cast<bf16_t*>(W), 0, N * K * 2, 0x00020000);
+  // no bias: an empty range, whose loads read zeros
+  const __amdgpu_buffer_rsrc_t bres = __builtin_amdgcn_make_buffer_rsrc(
+      ep.bias != nullptr ? const_cast<void*>(ep.bias) : const_cast<bf16_t*>(X), 0,
+      ep.bias != nullptr ? N * 2 : 0, 0x00020000);
+  // wave w moves row blocks i * 4 + w of a stage, as in gemm_bf16_w4_kernel
+  const int lr = lane / SL::CPR, lp = lane % SL::CPR;
+  const uint32_t lane_off =
+      static_cast<uint32_t>(lr * K * 2 + swz<KB>((wave & 1) * SL::RPD + lr, lp) * 16);
+  typedef __attribute__((address_space(3))) void lds_void;
+  // abase / bbase: byte offsets of the slice's first A and B rows (its K
+  // step included); 0x80000000 past the stream
+  auto dma1 = [&](int st, uint32_t abase, uint32_t bbase, bool live, int i) {
+    const int blk = i * 4 + wave;
+    const uint32_t off =
+        live ? (i < ALD ? abase + static_cast<uint32_t>(blk * SL::RPD) * K * 2u
+                        : bbase + static_cast<uint32_t>((blk - 4 * ALD) * SL::RPD) * K * 2u) +
+                   lane_off
+             : 0x80000000u;
+    __builtin_amdgcn_raw_ptr_buffer_load_lds(i < ALD ? xres : wres,
+                                             (lds_void*)(smem + st * SB + blk * 1024), 16, off, 0,
+                                             0, 0);
+  };
+  // the bias of the tile at n0 into buffer p & 1 (lanes past the 256 columns
+  // fill the buffer's unused upper half)
+  auto bias_dma = [&](int p, int n0) {
+    __builtin_amdgcn_raw_ptr_buffer_load_lds(bres, (lds_void*)(blds + (p & 1) * 1024), 16,
+                                             static_cast<uint32_t>(n0 * 2 + lane * 16), 0, 0, 0);
+  };
+  const int sw = (l32 / SL::RPP) & (SL::CPR - 1);
+  int ab[4], bb[4];
+#pragma unroll
+  for (int kk = 0; kk < 4; ++kk) {
+    ab[kk] = (wm * 128 + l32) * SL::RB + ((kk * 2 + half) ^ sw) * 16;
+    bb[kk] = BM * SL::RB + (wn * 128 + l32) * SL::RB + ((kk * 2 + half) ^ sw) * 16;
+  }
+  f32x16_t acc[4][4];
+  bf16x8_t f0[2][8], f1[2][8];
+  auto rd1 = [&](const unsigned char* st, int kk, bf16x8_t (&f)[8], int q) {
+    const int off = q < 4 ? ab[kk] + q * 32 * SL::RB : bb[kk] + (q - 4) * 32 * SL::RB;
+    f[q] = __builtin_bit_cast(bf16x8_t, *reinterpret_cast<const u32x4*>(st + off));
+  };
+  auto mma1 = [&](bf16x8_t (&f)[8], int p) {
+    acc[p / 4][p % 4] =
+        __builtin_amdgcn_mfma_f32_32x32x16_bf16(f[4 + p % 4], f[p / 4], acc[p / 4][p % 4], 0, 0, 0);
+  };
+  auto mma0 = [&](bf16x8_t (&f)[8], int p) {
+    const f32x16_t zero = {};
+    acc[p / 4][p % 4] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(f[4 + p % 4], f[p / 4], zero, 0, 0, 0);
+  };
+  // prologue: the first tile's bias and slices 0 and 1 in flight, slice 0
+  // (and the bias) published, its first fragments read
+  int m0, n0;
+  tile_at(0, &m0, &n0);
+  {
+    const uint32_t abase = static_cast<uint32_t>(m0) * K * 2u;
+    const uint32_t bbase = static_cast<uint32_t>(n0) * K * 2u;
+    if (wave == 0) bias_dma(0, n0);
+#pragma unroll
+    for (int i = 0; i < LPW; ++i) dma1(0, abase, bbase, true, i);
+#pragma unroll
+    for (int i = 0; i < LPW; ++i) dma1(1, abase + KB * 2, bbase + KB * 2, true, i);
+  }
+  asm volatile("" ::: "memory");
+  __builtin_amdgcn_s_waitcnt(vmcnt_imm(LPW));
+  barrier_lds();
+#pragma unroll
+  for (int q = 0; q < 8; ++q) {
+    rd1(smem, 0, f0[0], q);
+    rd1(smem, 1, f0[1], q);
+  }
+  // the load stream runs two slices ahead: tile dp, K step dt
+  int dp = KT > 2 ? 0 : 1, dt = KT > 2 ? 2 : 0;
+  int dm0 = m0, dn0 = n0;
+  if (dp == 1 && count > 1) tile_at(1, &dm0, &dn0);
+  int s = 0;
+  // block A: the MFMAs of the slice's first 32 K values with the reads of
+  // its last 32 K values' fragments (the first slice of a tile starts its
+  // sums from zero)
+  auto block_a = [&](auto first) {
+    const unsigned char* cur = smem + s * SB;
+#pragma unroll
+    for (int q = 0; q < 16; ++q) {
+      __builtin_amdgcn_sched_barrier(0);
+      if (decltype(first)::value && q < 8) mma0(f0[0], 2 * q); else mma1(f0[q / 8], 2 * (q % 8));
+      rd1(cur, 2 + q / 8, f1[q / 8], q % 8);
+      if (decltype(first)::value && q < 8) mma0(f0[0], 2 * q + 1); else mma1(f0[q / 8], 2 * (q % 8) + 1);
+    }
+    __builtin_amdgcn_sched_barrier(0);
+    // the next slice (and any earlier epilogue's stores) have landed
+    asm volatile("" ::: "memory");
+    __builtin_amdgcn_s_waitcnt(vmcnt_imm(0));
+    barrier_lds();
+  };
+  // block B: the MFMAs of the last 32 K values with the loads of the stream's
+  // next slice into this slice's stage and (but in a tile's last slice) the
+  // reads of the next slice's first fragments
+  auto block_b = [&](auto last) {
+    const unsigned char* nxt = smem + (s ^ 1) * SB;
+    const bool live = dp < count;
+    const uint32_t abase = static_cast<uint32_t>(dm0) * K * 2u + static_cast<uint32_t>(dt * KB * 2);
+    const uint32_t bbase = static_cast<uint32_t>(dn0) * K * 2u + static_cast<uint32_t>(dt * KB * 2);
+#pragma unroll
+    for (int q = 0; q < 16; ++q) {
+      __builtin_amdgcn_sched_barrier(0);
+      mma1(f1[q / 8], 2 * (q % 8));
+      if (!decltype(last)::value) rd1(nxt, q / 8, f0[q / 8], q % 8);
+      mma1(f1[q / 8], 2 * (q % 8) + 1);
+      dma1(s, abase, bbase, live, q);
+    }
+    __builtin_amdgcn_sched_barrier(0);
+    if (live && dt == 0 && wave == 0) bias_dma(dp, dn0);
+    if (++dt == KT) {
+      dt = 0;
+      if (++dp < count) tile_at(dp, &dm0, &dn0);
+    }
+    s ^= 1;
+  };
+  using yes = std::integral_constant<bool, true>;
+  using no = std::integral_constant<bool, false>;
+  for (int p = 0; p < count; ++p) {
+    block_a(yes{});
+    block_b(no{});
+    for (int t = 1; t + 1 < KT; ++t) {
+      block_a(no{});
+      block_b(no{});
+    }
+    block_a(no{});
+    block_b(yes{});
+    reg_epilogue_lb<4, 4, EPI>(acc, m0 + wm * 128, n0 + wn * 128, M, l32, half, ep,
+                               blds + (p & 1) * 1024 + wn * 256);
+    if (p + 1 < count) {
+      tile_at(p + 1, &m0, &n0);
+      // the next tile's first fragments (its slice 0 was published by the
+      // barrier of this tile's last slice)
+#pragma unroll
+      for (int q = 0; q < 8; ++q) {
+        rd1(smem + s * SB, 0, f0[0], q);
+        rd1(smem + s * SB, 1, f0[1], q);
+      }
+    }
+  }
+}
+
+template <int EPI>
+hipError_t launch_w4p_1(hipStream_t s, const void* x, int M, int K, const void* w, int N,
+                        const EpiParams& ep) {
+  constexpr int lds = 2 * 512 * 64 * 2 + 2 * 1024;
+  static bool lds_raised = false;
+  if (!lds_raised) {
+    const hipError_t e = hipFuncSetAttribute(
+        reinterpret_cast<const void*>(gemm_bf16_w4p_kernel<EPI>),
+        hipFuncAttributeMaxDynamicSharedMemorySize, lds);
+    if (e != hipSuccess) return e;
+    lds_raised = true;
+  }
+  const int tiles = ((M + 255) / 256) * (N / 256);
+  const int wgs = std::min(tiles, device_cus());
+  const int grid = kXcds * ((wgs + kXcds - 1) / kXcds);
+  return launch(K_GEMM, gemm_bf16_w4p_kernel<EPI>, dim3(grid), dim3(256), lds, s,
+                static_cast<const bf16_t*>(x), static_cast<const bf16_t*>(w), M, N, K, ep);
+}
+
 // the four-wave kernel takes the products the persistent one takes, with N a
 // multiple of 256 and both operands below 2^31 bytes (buffer range checks)
 bool w4_ok(int M, int N, int K, const EpiParams& ep) {
@@ -1436,6 +1706,34 @@ hipError_t launch_w4(hipStream_t s, const void* x, int M, int K, const void* w, 
   if (ep.epi == EPI_GELU) return launch_w4_1<EPI_GELU>(s, x, M, K, w, N, ep);
   if (ep.epi == EPI_RESIDUAL) return launch_w4_1<EPI_RESIDUAL>(s, x, M, K, w, N, ep);
   return launch_w4_1<EPI_NONE>(s, x, M, K, w, N, ep);
+}
+
+// the persistent four-wave kernel: the four-wave kernel's products with K of
+// at least two slices
+bool w4p_ok(int M, int N, int K, const EpiParams& ep) { return w4_ok(M, N, K, ep) && K >= 128; }
+
+// Where its 256x256 tiles beat the persistent 128x128 kernel (measured on
+// M = 2048 .. 16384, N = 768 .. 3072, K = 768 and 3072): the tiles fill
+// their last round on the CUs at least three-quarters (16384 x 3072 x 768:
+// 96.6 against 103.1 us), or K is long and there is at least half a round
+// of tiles (16384 x 768 x 3072: 71.5 against 81.3 us; the 128x128 tiles
+// need twice the operand bytes per FLOP). Part-filled rounds lose
+// (16384 x 2304 x 768: 74.1 against 70.5 us; 8192 x 3072 x 768: 58.1
+// against 53.2 us).
+bool w4p_pays(int M, int N, int K) {
+  const long tiles = static_cast<long>((M + 255) / 256) * (N / 256);
+  const long cus = device_cus();
+  if (K >= 2048 && 2 * tiles >= cus) return true;
+  if (tiles < cus) return false;
+  const long rem = tiles % cus;
+  return rem == 0 || 4 * rem >= 3 * cus;
+}
+
+hipError_t launch_w4p(hipStream_t s, const void* x, int M, int K, const void* w, int N,
+                      const EpiParams& ep) {
+  if (ep.epi == EPI_GELU) return launch_w4p_1<EPI_GELU>(s, x, M, K, w, N, ep);
+  if (ep.epi == EPI_RESIDUAL) return launch_w4p_1<EPI_RESIDUAL>(s, x, M, K, w, N, ep);
+  return launch_w4p_1<EPI_NONE>(s, x, M, K, w, N, ep);
 }
 
 template <int KB, int WPC>
@@ -1489,7 +1787,8 @@ hipError_t launch_dma(hipStream_t s, const void* x, int M, int K, const void* w,
 // with 32-wide slices in 4 stages; 6431: 128x128 with 3 stages; 2542:
 // 256x256 on 4 waves (128x128 per wave) with 64-row epilogue passes; 1289:
 // the persistent 128x128 kernel; 2544: the 256x256 four-wave kernel with
-// pinned MFMA / fragment-read interleaving and the epilogue in registers.
+// pinned MFMA / fragment-read interleaving and the epilogue in registers;
+// 2545: its persistent form.
 int gemm_tile_override() {
   static const int v = [] {
     const char* e = getenv("ZSA_GEMM_TILE");
@@ -1500,18 +1799,20 @@ int gemm_tile_override() {
 
 }  // namespace
 
-// Split K when the 128 x 128 output tiles cannot fill the chip (fewer than
-// 256, under one round at two workgroups per CU) and K is long (at least
-// kMinSplitK): S slices of at least kMinSplitSteps K steps, S x tiles <= 512
-// workgroups (one round, no tail). Every slice is non-empty and all but the
-// last have kchunk columns.
+// Split K when the 128 x 128 output tiles fill under three-quarters of the
+// CUs once and K is long (at least kMinSplitK): S slices of at least
+// kMinSplitSteps K steps, S x tiles <= 512 workgroups (one round, no tail).
+// Every slice is non-empty and all but the last have kchunk columns. Per
+// projection (both launches), M x 768 x 3072 with a residual: 256 rows 26.6
+// -> 15.9 us, 2048 rows 31.7 -> 27.1, 3584 rows (168 tiles) 34.0 -> 32.5,
+// 4096 rows (192 tiles) 32.1 -> 35.5 (not split).
 void splitk_plan(int M, int N, int K, int* S, int* kchunk) {
   *S = 1;
   *kchunk = K;
   if (K % kBK != 0 || K < kMinSplitK) return;
   const long tiles = static_cast<long>((M + 127) / 128) * ((N + 127) / 128);
   const int steps = K / kBK;
-  if (tiles >= 256) return;
+  if (4 * tiles >= 3 * device_cus()) return;
   const int want = std::min(static_cast<int>(512 / tiles), steps / kMinSplitSteps);
   if (want < 2) return;
   const int per = (steps + want - 1) / want;
@@ -1658,22 +1959,27 @@ hipError_t launch_gemm(hipStream_t s, int dtype, const void* x, int M, int K, co
       case 2544:
         if (w4_ok(M, N, K, ep)) return launch_w4(s, x, M, K, w, N, ep);
         break;
+      case 2545:
+        if (w4p_ok(M, N, K, ep)) return launch_w4p(s, x, M, K, w, N, ep);
+        break;
       default: break;
     }
     // Measured on the projection shapes of the 768-wide stacks (N = 768,
-    // 2304, 3072; K = 768, 3072; M = 2048 .. 16384): with M >= 12288 the
-    // 256x256 four-wave tiles win for the GELU and residual projections; up
-    // to 1536 tiles of 128x128 the persistent kernel wins; the largest
-    // grids without an epilogue op keep the 128x128 kernel. For longer K
-    // (the 4096-wide decoder): direct-to-LDS 256x256 tiles over 8 waves
-    // (128x64 per wave) once the grid holds at least four rounds of them.
-    const long tiles128 = static_cast<long>((M + 127) / 128) * ((N + 127) / 128);
+    // 2304, 3072; K = 768, 3072; M = 2048 .. 16384): the persistent
+    // four-wave kernel where w4p_pays (whole rounds of 256x256 tiles, or
+    // long K), the persistent 128x128 kernel otherwise. For longer K (the
+    // 4096-wide decoder, K = 4096 and 14336): the persistent four-wave
+    // kernel from one round of its tiles on (8192 x 4096 x 14336: 754
+    // against 994 us for the 8-wave kernel below; 4096 x 6144 x 4096: 173
+    // against 210 us), else -- and for the rotary and SwiGLU epilogues --
+    // direct-to-LDS 256x256 tiles over 8 waves (128x64 per wave) once the
+    // grid holds at least four rounds of them, or 128x128 tiles.
     if (K <= 3072 && persist_ok(M, N, K, ep)) {
-      if (M >= 12288 && ep.epi != EPI_NONE && w4_ok(M, N, K, ep))
-        return launch_w4(s, x, M, K, w, N, ep);
-      if (tiles128 <= 1536) return launch_persist_any<64, 2>(s, x, M, K, w, N, ep);
+      if (w4p_pays(M, N, K) && w4p_ok(M, N, K, ep)) return launch_w4p(s, x, M, K, w, N, ep);
+      return launch_persist_any<64, 2>(s, x, M, K, w, N, ep);
     }
     const long tiles256 = static_cast<long>((M + 255) / 256) * ((N + 255) / 256);
+    if (tiles256 >= device_cus() && w4p_ok(M, N, K, ep)) return launch_w4p(s, x, M, K, w, N, ep);
     if (tiles256 >= 1024) return launch_dma<256, 256, 2, 4, 64, 2, 128>(s, x, M, K, w, N, ep);
     return launch_dma<128, 128, 2, 2, 64, 2, 128>(s, x, M, K, w, N, ep);
   }

@@ -185,11 +185,13 @@ def test_linear_split_k(m, n, k, epi):
     assert_close(f64(y0), ref, 1e-2, f"unsplit epilogue {epi}")
 
 
-@pytest.mark.parametrize("m,n,k,split", [(12289, 3072, 768, False),   # 256x256 tiles on four waves
-                                         (12289, 768, 3072, False),
-                                         (1000, 768, 768, False),     # persistent 128x128
+@pytest.mark.parametrize("m,n,k,split", [(16129, 3072, 768, False),   # persistent 256x256: whole rounds
+                                         (12289, 768, 3072, False),   # persistent 256x256: long K
+                                         (4097, 4096, 4096, False),   # persistent 256x256: K > 3072
+                                         (12289, 3072, 768, False),   # persistent 128x128
+                                         (1000, 768, 768, False),
                                          (4000, 768, 3072, False),
-                                         (16385, 2304, 768, False)])  # 128x128, largest grids
+                                         (16385, 2304, 768, False)])
 @pytest.mark.parametrize("epi", [zsa.EPI_NONE, zsa.EPI_GELU, zsa.EPI_RESIDUAL])
 @pytest.mark.parametrize("with_bias", [True, False])
 def test_linear_kernel_regimes(m, n, k, split, epi, with_bias):
