@@ -59,20 +59,22 @@ __device__ __forceinline__ void store8<float>(float* p, const float* v) {
   reinterpret_cast<uint4*>(p)[1] = pack16(v + 4, 0.f);
 }
 
-// erf by Abramowitz & Stegun, Handbook of Mathematical Functions, 7.1.26:
-// erf(x) = 1 - (a1 t + a2 t^2 + a3 t^3 + a4 t^4 + a5 t^5) exp(-x^2),
-// t = 1 / (1 + p x), x >= 0, |error| <= 1.5e-7; odd extension for x < 0.
-__device__ __forceinline__ float erf_as(float x) {
-  const float ax = fabsf(x);
-  const float t = __builtin_amdgcn_rcpf(1.0f + 0.3275911f * ax);
-  const float poly =
-      t * (0.254829592f + t * (-0.284496736f + t * (1.421413741f + t * (-1.453152027f + t * 1.061405429f))));
-  const float e = 1.0f - poly * __expf(-ax * ax);
-  return copysignf(e, x);
-}
-// exact (erf-based) GELU: z * Phi(z) = 0.5 z (1 + erf(z / sqrt 2))
+// Exact (erf-based) GELU, z Phi(z) = z (1 + erf(z / sqrt 2)) / 2, with erf by
+// Abramowitz & Stegun, Handbook of Mathematical Functions, 7.1.26:
+// erf(x) = 1 - P(t) exp(-x^2), P(t) = a1 t + a2 t^2 + a3 t^3 + a4 t^4 + a5 t^5,
+// t = 1 / (1 + p x), x >= 0, |error| <= 1.5e-7, and erf odd. Oddness gives
+// z Phi(z) = max(z, 0) - |z| P(t) exp(-z^2 / 2) / 2 for either sign of z
+// (t formed from |z| / sqrt 2): one fma instead of a sign transfer and the
+// (1 + erf) / 2 scaling, with the 1/2 folded into the coefficients and the
+// 1/sqrt 2 into p.
 __device__ __forceinline__ float gelu_erf(float z) {
-  return 0.5f * z * (1.0f + erf_as(z * 0.70710678118654752f));
+  const float a = fabsf(z);
+  const float t = __builtin_amdgcn_rcpf(fmaf(0.3275911f * 0.70710678118654752f, a, 1.0f));
+  const float hp =
+      t * (0.5f * 0.254829592f +
+           t * (0.5f * -0.284496736f +
+                t * (0.5f * 1.421413741f + t * (0.5f * -1.453152027f + t * (0.5f * 1.061405429f)))));
+  return fmaf(-a * hp, __expf(-0.5f * z * z), fmaxf(z, 0.0f));
 }
 __device__ __forceinline__ float silu(float z) { return z / (1.0f + expf(-z)); }
 
@@ -1476,36 +1478,45 @@ __device__ __forceinline__ void reg_epilogue_lb(const f32x16_t (&acc)[TM][TN], i
 // ---------------------------------------------------------------------------
 // bf16 GEMM, persistent form of the four-wave kernel
 // ---------------------------------------------------------------------------
-// One workgroup per CU walks a strided share of its XCD's range of 256x256
+// One workgroup per CU walks a strided share of its XCD's range of 256 x BN
 // tiles (the grouped order above) and streams their K slices as one
 // sequence: the loads of slice g + 2 run on into the next tile, so when the
 // last slice of a tile has been multiplied, the first slices of the next are
 // in flight or landed and the finished tile's epilogue overlaps them (a
 // workgroup per tile would instead start each tile by waiting for its first
-// slice). The slice loop is that of gemm_bf16_w4_kernel. The bias of a tile
-// travels with its first slice, as a direct-to-LDS load into one of two
-// 1 KiB buffers (by tile parity), so the epilogue waits for no global load:
-// such a wait would also wait for the slice loads issued before it, since
-// vector memory operations complete in issue order. A tile's accumulators
-// restart from MFMAs whose C operand is zero. K is at least two slices, so a
-// bias buffer is refilled only after every wave has passed the epilogue that
-// read it (the refill is issued after a barrier of the next tile).
-template <int EPI>
+// slice). The slice loop is that of gemm_bf16_w4_kernel, generalised to
+// BN = 256 (waves of 128 x 128) and BN = 192 (waves of 128 x 96, for N = 768
+// and 2304, whose 256-wide tiles leave a round part-filled): each block
+// spreads its fragment reads (and, in block B, its loads) evenly over its
+// MFMAs. The bias of a tile travels with its first slice, as a
+// direct-to-LDS load into one of two 1 KiB buffers (by tile parity), so the
+// epilogue waits for no global load: such a wait would also wait for the
+// slice loads issued before it, since vector memory operations complete in
+// issue order. A tile's accumulators restart from MFMAs whose C operand is
+// zero. K is at least two slices, so a bias buffer is refilled only after
+// every wave has passed the epilogue that read it (the refill is issued
+// after a barrier of the next tile).
+template <int EPI, int BN>
 __global__ __launch_bounds__(256) void gemm_bf16_w4p_kernel(const bf16_t* __restrict__ X,
                                                            const bf16_t* __restrict__ W, int M,
                                                            int N, int K, EpiParams ep) {
-  constexpr int BM = 256, BN = 256, KB = 64;
+  constexpr int BM = 256, KB = 64;
+  constexpr int TM = 4, TN = BN / 64;           // 32 x 32 blocks per wave (rows, columns)
+  constexpr int NF = TM + TN;                   // fragments per 16-wide k-substep
+  constexpr int NP = TM * TN;                   // MFMAs per k-substep
+  constexpr int NMB = 2 * NP, NRB = 2 * NF;     // MFMAs and fragment reads per block
   using SL = Slice<KB>;
   constexpr int SB = (BM + BN) * SL::RB;        // bytes per stage
   constexpr int LPW = (BM + BN) / SL::RPD / 4;  // 1 KiB loads per wave per stage
   constexpr int ALD = BM / SL::RPD / 4;         // of which A rows
-  static_assert(LPW == 16 && ALD == 8, "stage layout");
+  static_assert(BN == 256 || BN == 192, "tile width");
+  static_assert(NMB >= NRB && NMB >= LPW, "interleave");
   extern __shared__ __align__(16) unsigned char smem[];
   unsigned char* const blds = smem + 2 * SB;  // bias buffers, 1 KiB each
   const int tid = threadIdx.x;
   const int lane = tid & 63;
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
-  const int wm = wave >> 1, wn = wave & 1;  // 2 x 2 waves of 128 x 128
+  const int wm = wave >> 1, wn = wave & 1;  // 2 x 2 waves of 128 x BN / 2
   const int l32 = lane & 31, half = lane >> 5;
 
   const int nM = (M + BM - 1) / BM, nN = N / BN;
@@ -1535,7 +1546,9 @@ __global__ __launch_bounds__(256) void gemm_bf16_w4p_kernel(const bf16_t* __rest
   const __amdgpu_buffer_rsrc_t bres = __builtin_amdgcn_make_buffer_rsrc(
       ep.bias != nullptr ? const_cast<void*>(ep.bias) : const_cast<bf16_t*>(X), 0,
       ep.bias != nullptr ? N * 2 : 0, 0x00020000);
-  // wave w moves row blocks i * 4 + w of a stage, as in gemm_bf16_w4_kernel
+  // wave w moves row blocks i * 4 + w of a stage (8 rows each; A rows, then
+  // B rows); stage row r = 8 blk + lr has swizzle (4 blk + lr / 2) & 7,
+  // which depends on blk only through the wave's parity
   const int lr = lane / SL::CPR, lp = lane % SL::CPR;
   const uint32_t lane_off =
       static_cast<uint32_t>(lr * K * 2 + swz<KB>((wave & 1) * SL::RPD + lr, lp) * 16);
@@ -1553,32 +1566,37 @@ __global__ __launch_bounds__(256) void gemm_bf16_w4p_kernel(const bf16_t* __rest
                                              (lds_void*)(smem + st * SB + blk * 1024), 16, off, 0,
                                              0, 0);
   };
-  // the bias of the tile at n0 into buffer p & 1 (lanes past the 256 columns
-  // fill the buffer's unused upper half)
+  // the bias of the tile at n0 into buffer p & 1 (lanes past the BN columns
+  // fill the buffer's unused rest)
   auto bias_dma = [&](int p, int n0) {
     __builtin_amdgcn_raw_ptr_buffer_load_lds(bres, (lds_void*)(blds + (p & 1) * 1024), 16,
                                              static_cast<uint32_t>(n0 * 2 + lane * 16), 0, 0, 0);
   };
+  // fragment q of k-substep kk: A block q (q < TM) or B block q - TM; row r
+  // of a 32-row block sits at r * RB, its chunk c at (c ^ ((r / RPP) & 7)) * 16
   const int sw = (l32 / SL::RPP) & (SL::CPR - 1);
   int ab[4], bb[4];
 #pragma unroll
   for (int kk = 0; kk < 4; ++kk) {
     ab[kk] = (wm * 128 + l32) * SL::RB + ((kk * 2 + half) ^ sw) * 16;
-    bb[kk] = BM * SL::RB + (wn * 128 + l32) * SL::RB + ((kk * 2 + half) ^ sw) * 16;
+    bb[kk] = BM * SL::RB + (wn * (BN / 2) + l32) * SL::RB + ((kk * 2 + half) ^ sw) * 16;
   }
-  f32x16_t acc[4][4];
-  bf16x8_t f0[2][8], f1[2][8];
-  auto rd1 = [&](const unsigned char* st, int kk, bf16x8_t (&f)[8], int q) {
-    const int off = q < 4 ? ab[kk] + q * 32 * SL::RB : bb[kk] + (q - 4) * 32 * SL::RB;
+  f32x16_t acc[TM][TN];
+  // f0: fragments of k-substeps 0, 1 of a slice; f1: of k-substeps 2, 3
+  bf16x8_t f0[2][NF], f1[2][NF];
+  auto rd1 = [&](const unsigned char* st, int kk, bf16x8_t (&f)[NF], int q) {
+    const int off = q < TM ? ab[kk] + q * 32 * SL::RB : bb[kk] + (q - TM) * 32 * SL::RB;
     f[q] = __builtin_bit_cast(bf16x8_t, *reinterpret_cast<const u32x4*>(st + off));
   };
-  auto mma1 = [&](bf16x8_t (&f)[8], int p) {
-    acc[p / 4][p % 4] =
-        __builtin_amdgcn_mfma_f32_32x32x16_bf16(f[4 + p % 4], f[p / 4], acc[p / 4][p % 4], 0, 0, 0);
+  // MFMA p of a k-substep: output block (p / TN, p % TN), operands swapped
+  // so the accumulator holds C^T (four consecutive columns per register group)
+  auto mma1 = [&](bf16x8_t (&f)[NF], int p) {
+    acc[p / TN][p % TN] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(f[TM + p % TN], f[p / TN],
+                                                                  acc[p / TN][p % TN], 0, 0, 0);
   };
-  auto mma0 = [&](bf16x8_t (&f)[8], int p) {
+  auto mma0 = [&](bf16x8_t (&f)[NF], int p) {
     const f32x16_t zero = {};
-    acc[p / 4][p % 4] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(f[4 + p % 4], f[p / 4], zero, 0, 0, 0);
+    acc[p / TN][p % TN] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(f[TM + p % TN], f[p / TN], zero, 0, 0, 0);
   };
   // prologue: the first tile's bias and slices 0 and 1 in flight, slice 0
   // (and the bias) published, its first fragments read
@@ -1597,7 +1615,7 @@ __global__ __launch_bounds__(256) void gemm_bf16_w4p_kernel(const bf16_t* __rest
   __builtin_amdgcn_s_waitcnt(vmcnt_imm(LPW));
   barrier_lds();
 #pragma unroll
-  for (int q = 0; q < 8; ++q) {
+  for (int q = 0; q < NF; ++q) {
     rd1(smem, 0, f0[0], q);
     rd1(smem, 1, f0[1], q);
   }
@@ -1606,17 +1624,21 @@ __global__ __launch_bounds__(256) void gemm_bf16_w4p_kernel(const bf16_t* __rest
   int dm0 = m0, dn0 = n0;
   if (dp == 1 && count > 1) tile_at(1, &dm0, &dn0);
   int s = 0;
+  // fragment read r of a block follows MFMA r * NMB / NRB; load d of block B
+  // follows MFMA d * NMB / LPW + 1 (the order is pinned by the scheduling
+  // barriers)
   // block A: the MFMAs of the slice's first 32 K values with the reads of
   // its last 32 K values' fragments (the first slice of a tile starts its
   // sums from zero)
   auto block_a = [&](auto first) {
     const unsigned char* cur = smem + s * SB;
 #pragma unroll
-    for (int q = 0; q < 16; ++q) {
+    for (int mi = 0; mi < NMB; ++mi) {
       __builtin_amdgcn_sched_barrier(0);
-      if (decltype(first)::value && q < 8) mma0(f0[0], 2 * q); else mma1(f0[q / 8], 2 * (q % 8));
-      rd1(cur, 2 + q / 8, f1[q / 8], q % 8);
-      if (decltype(first)::value && q < 8) mma0(f0[0], 2 * q + 1); else mma1(f0[q / 8], 2 * (q % 8) + 1);
+      if (decltype(first)::value && mi < NP) mma0(f0[0], mi); else mma1(f0[mi / NP], mi % NP);
+#pragma unroll
+      for (int r = 0; r < NRB; ++r)
+        if (r * NMB / NRB == mi) rd1(cur, 2 + r / NF, f1[r / NF], r % NF);
     }
     __builtin_amdgcn_sched_barrier(0);
     // the next slice (and any earlier epilogue's stores) have landed
@@ -1633,12 +1655,15 @@ __global__ __launch_bounds__(256) void gemm_bf16_w4p_kernel(const bf16_t* __rest
     const uint32_t abase = static_cast<uint32_t>(dm0) * K * 2u + static_cast<uint32_t>(dt * KB * 2);
     const uint32_t bbase = static_cast<uint32_t>(dn0) * K * 2u + static_cast<uint32_t>(dt * KB * 2);
 #pragma unroll
-    for (int q = 0; q < 16; ++q) {
+    for (int mi = 0; mi < NMB; ++mi) {
       __builtin_amdgcn_sched_barrier(0);
-      mma1(f1[q / 8], 2 * (q % 8));
-      if (!decltype(last)::value) rd1(nxt, q / 8, f0[q / 8], q % 8);
-      mma1(f1[q / 8], 2 * (q % 8) + 1);
-      dma1(s, abase, bbase, live, q);
+      mma1(f1[mi / NP], mi % NP);
+#pragma unroll
+      for (int r = 0; r < NRB; ++r)
+        if (!decltype(last)::value && r * NMB / NRB == mi) rd1(nxt, r / NF, f0[r / NF], r % NF);
+#pragma unroll
+      for (int d = 0; d < LPW; ++d)
+        if (d * NMB / LPW + 1 == mi) dma1(s, abase, bbase, live, d);
     }
     __builtin_amdgcn_sched_barrier(0);
     if (live && dt == 0 && wave == 0) bias_dma(dp, dn0);
@@ -1659,14 +1684,14 @@ __global__ __launch_bounds__(256) void gemm_bf16_w4p_kernel(const bf16_t* __rest
     }
     block_a(no{});
     block_b(yes{});
-    reg_epilogue_lb<4, 4, EPI>(acc, m0 + wm * 128, n0 + wn * 128, M, l32, half, ep,
-                               blds + (p & 1) * 1024 + wn * 256);
+    reg_epilogue_lb<TM, TN, EPI>(acc, m0 + wm * 128, n0 + wn * (BN / 2), M, l32, half, ep,
+                                 blds + (p & 1) * 1024 + wn * BN);
     if (p + 1 < count) {
       tile_at(p + 1, &m0, &n0);
       // the next tile's first fragments (its slice 0 was published by the
       // barrier of this tile's last slice)
 #pragma unroll
-      for (int q = 0; q < 8; ++q) {
+      for (int q = 0; q < NF; ++q) {
         rd1(smem + s * SB, 0, f0[0], q);
         rd1(smem + s * SB, 1, f0[1], q);
       }
@@ -1674,22 +1699,22 @@ __global__ __launch_bounds__(256) void gemm_bf16_w4p_kernel(const bf16_t* __rest
   }
 }
 
-template <int EPI>
+template <int EPI, int BN>
 hipError_t launch_w4p_1(hipStream_t s, const void* x, int M, int K, const void* w, int N,
                         const EpiParams& ep) {
-  constexpr int lds = 2 * 512 * 64 * 2 + 2 * 1024;
+  constexpr int lds = 2 * (256 + BN) * 64 * 2 + 2 * 1024;
   static bool lds_raised = false;
   if (!lds_raised) {
     const hipError_t e = hipFuncSetAttribute(
-        reinterpret_cast<const void*>(gemm_bf16_w4p_kernel<EPI>),
+        reinterpret_cast<const void*>(gemm_bf16_w4p_kernel<EPI, BN>),
         hipFuncAttributeMaxDynamicSharedMemorySize, lds);
     if (e != hipSuccess) return e;
     lds_raised = true;
   }
-  const int tiles = ((M + 255) / 256) * (N / 256);
+  const int tiles = ((M + 255) / 256) * (N / BN);
   const int wgs = std::min(tiles, device_cus());
   const int grid = kXcds * ((wgs + kXcds - 1) / kXcds);
-  return launch(K_GEMM, gemm_bf16_w4p_kernel<EPI>, dim3(grid), dim3(256), lds, s,
+  return launch(K_GEMM, gemm_bf16_w4p_kernel<EPI, BN>, dim3(grid), dim3(256), lds, s,
                 static_cast<const bf16_t*>(x), static_cast<const bf16_t*>(w), M, N, K, ep);
 }
 
@@ -1709,31 +1734,56 @@ hipError_t launch_w4(hipStream_t s, const void* x, int M, int K, const void* w, 
 }
 
 // the persistent four-wave kernel: the four-wave kernel's products with K of
-// at least two slices
-bool w4p_ok(int M, int N, int K, const EpiParams& ep) { return w4_ok(M, N, K, ep) && K >= 128; }
-
-// Where its 256x256 tiles beat the persistent 128x128 kernel (measured on
-// M = 2048 .. 16384, N = 768 .. 3072, K = 768 and 3072): the tiles fill
-// their last round on the CUs at least three-quarters (16384 x 3072 x 768:
-// 96.6 against 103.1 us), or K is long and there is at least half a round
-// of tiles (16384 x 768 x 3072: 71.5 against 81.3 us; the 128x128 tiles
-// need twice the operand bytes per FLOP). Part-filled rounds lose
-// (16384 x 2304 x 768: 74.1 against 70.5 us; 8192 x 3072 x 768: 58.1
-// against 53.2 us).
-bool w4p_pays(int M, int N, int K) {
-  const long tiles = static_cast<long>((M + 255) / 256) * (N / 256);
-  const long cus = device_cus();
-  if (K >= 2048 && 2 * tiles >= cus) return true;
-  if (tiles < cus) return false;
-  const long rem = tiles % cus;
-  return rem == 0 || 4 * rem >= 3 * cus;
+// at least two slices (bn: the tile width, 256 or 192, which N is a multiple of)
+bool w4p_ok(int M, int N, int K, const EpiParams& ep, int bn = 256) {
+  return persist_ok(M, N, K, ep) && N % bn == 0 && K >= 128 &&
+         static_cast<int64_t>(M + 256) * K * 2 < (int64_t{1} << 31) &&
+         static_cast<int64_t>(N) * K * 2 < (int64_t{1} << 31);
 }
 
+// Tile width (256 or 192) of the persistent four-wave kernel for a product,
+// or 0 where it does not pay. Measured on M = 2048 .. 16384, N = 768 ..
+// 3072, K = 768 and 3072 against the persistent 128x128 kernel (which needs
+// twice the operand bytes per FLOP): a width pays when its tiles fill their
+// last round on the CUs at least three-quarters (16384 x 3072 x 768, 256
+// wide: 96.6 against 103.1 us), or, for K >= 2048, when there are at least
+// three-quarters of a round of them (16384 x 768 x 3072, 256 wide: 71.5
+// against 81.3 us); rounds filled less lose (16384 x 2304 x 768, 256 wide:
+// 74.1 against 70.5 us; 8192 x 768 x 3072, 192 wide: 52.6 against 49.7 us).
+// Of the widths that pay, the better-filled one is taken, 256 on a tie
+// (more FLOPs per operand byte): 192 for 16384 x 2304 x 768 (three whole
+// rounds; 64.4 us) and 16384 x 768 x K (one; 27.3 and 70.5 us for K = 768,
+// 3072). For K > 3072 (the 4096-wide decoder) a width pays from one whole
+// round of tiles on.
+int w4p_width(int M, int N, int K, const EpiParams& ep) {
+  const long cus = device_cus();
+  int best = 0;
+  long best_fill = 0, best_slots = 1;  // the fill best_fill / best_slots
+  for (const int bn : {256, 192}) {
+    if (!w4p_ok(M, N, K, ep, bn)) continue;
+    const long tiles = static_cast<long>((M + 255) / 256) * (N / bn);
+    const long rem = tiles % cus;
+    bool pays;
+    if (K > 3072) pays = tiles >= cus;
+    else if (tiles >= cus) pays = rem == 0 || 4 * rem >= 3 * cus;
+    else pays = K >= 2048 && 4 * tiles >= 3 * cus;
+    if (!pays) continue;
+    const long slots = (tiles + cus - 1) / cus * cus;
+    if (best == 0 || tiles * best_slots > best_fill * slots) {
+      best = bn;
+      best_fill = tiles;
+      best_slots = slots;
+    }
+  }
+  return best;
+}
+
+template <int BN>
 hipError_t launch_w4p(hipStream_t s, const void* x, int M, int K, const void* w, int N,
                       const EpiParams& ep) {
-  if (ep.epi == EPI_GELU) return launch_w4p_1<EPI_GELU>(s, x, M, K, w, N, ep);
-  if (ep.epi == EPI_RESIDUAL) return launch_w4p_1<EPI_RESIDUAL>(s, x, M, K, w, N, ep);
-  return launch_w4p_1<EPI_NONE>(s, x, M, K, w, N, ep);
+  if (ep.epi == EPI_GELU) return launch_w4p_1<EPI_GELU, BN>(s, x, M, K, w, N, ep);
+  if (ep.epi == EPI_RESIDUAL) return launch_w4p_1<EPI_RESIDUAL, BN>(s, x, M, K, w, N, ep);
+  return launch_w4p_1<EPI_NONE, BN>(s, x, M, K, w, N, ep);
 }
 
 template <int KB, int WPC>
@@ -1788,7 +1838,7 @@ hipError_t launch_dma(hipStream_t s, const void* x, int M, int K, const void* w,
 // 256x256 on 4 waves (128x128 per wave) with 64-row epilogue passes; 1289:
 // the persistent 128x128 kernel; 2544: the 256x256 four-wave kernel with
 // pinned MFMA / fragment-read interleaving and the epilogue in registers;
-// 2545: its persistent form.
+// 2545: its persistent form; 1925: that with 256x192 tiles.
 int gemm_tile_override() {
   static const int v = [] {
     const char* e = getenv("ZSA_GEMM_TILE");
@@ -1960,26 +2010,28 @@ hipError_t launch_gemm(hipStream_t s, int dtype, const void* x, int M, int K, co
         if (w4_ok(M, N, K, ep)) return launch_w4(s, x, M, K, w, N, ep);
         break;
       case 2545:
-        if (w4p_ok(M, N, K, ep)) return launch_w4p(s, x, M, K, w, N, ep);
+        if (w4p_ok(M, N, K, ep)) return launch_w4p<256>(s, x, M, K, w, N, ep);
+        break;
+      case 1925:
+        if (w4p_ok(M, N, K, ep, 192)) return launch_w4p<192>(s, x, M, K, w, N, ep);
         break;
       default: break;
     }
     // Measured on the projection shapes of the 768-wide stacks (N = 768,
     // 2304, 3072; K = 768, 3072; M = 2048 .. 16384): the persistent
-    // four-wave kernel where w4p_pays (whole rounds of 256x256 tiles, or
-    // long K), the persistent 128x128 kernel otherwise. For longer K (the
-    // 4096-wide decoder, K = 4096 and 14336): the persistent four-wave
-    // kernel from one round of its tiles on (8192 x 4096 x 14336: 754
-    // against 994 us for the 8-wave kernel below; 4096 x 6144 x 4096: 173
-    // against 210 us), else -- and for the rotary and SwiGLU epilogues --
-    // direct-to-LDS 256x256 tiles over 8 waves (128x64 per wave) once the
-    // grid holds at least four rounds of them, or 128x128 tiles.
-    if (K <= 3072 && persist_ok(M, N, K, ep)) {
-      if (w4p_pays(M, N, K) && w4p_ok(M, N, K, ep)) return launch_w4p(s, x, M, K, w, N, ep);
-      return launch_persist_any<64, 2>(s, x, M, K, w, N, ep);
-    }
+    // four-wave kernel where w4p_width finds a tile width that pays, the
+    // persistent 128x128 kernel otherwise. For longer K (the 4096-wide
+    // decoder, K = 4096 and 14336): the persistent four-wave kernel from one
+    // round of its tiles on (8192 x 4096 x 14336: 754 against 994 us for the
+    // 8-wave kernel below; 4096 x 6144 x 4096: 173 against 210 us), else --
+    // and for the rotary and SwiGLU epilogues -- direct-to-LDS 256x256 tiles
+    // over 8 waves (128x64 per wave) once the grid holds at least four
+    // rounds of them, or 128x128 tiles.
+    const int bn = w4p_width(M, N, K, ep);
+    if (bn == 256) return launch_w4p<256>(s, x, M, K, w, N, ep);
+    if (bn == 192) return launch_w4p<192>(s, x, M, K, w, N, ep);
+    if (K <= 3072 && persist_ok(M, N, K, ep)) return launch_persist_any<64, 2>(s, x, M, K, w, N, ep);
     const long tiles256 = static_cast<long>((M + 255) / 256) * ((N + 255) / 256);
-    if (tiles256 >= device_cus() && w4p_ok(M, N, K, ep)) return launch_w4p(s, x, M, K, w, N, ep);
     if (tiles256 >= 1024) return launch_dma<256, 256, 2, 4, 64, 2, 128>(s, x, M, K, w, N, ep);
     return launch_dma<128, 128, 2, 2, 64, 2, 128>(s, x, M, K, w, N, ep);
   }
