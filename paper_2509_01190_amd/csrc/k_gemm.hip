@@ -1745,16 +1745,17 @@ bool w4p_ok(int M, int N, int K, const EpiParams& ep, int bn = 256) {
 // or 0 where it does not pay. Measured on M = 2048 .. 16384, N = 768 ..
 // 3072, K = 768 and 3072 against the persistent 128x128 kernel (which needs
 // twice the operand bytes per FLOP): a width pays when its tiles fill their
-// last round on the CUs at least three-quarters (16384 x 3072 x 768, 256
-// wide: 96.6 against 103.1 us), or, for K >= 2048, when there are at least
-// three-quarters of a round of them (16384 x 768 x 3072, 256 wide: 71.5
-// against 81.3 us); rounds filled less lose (16384 x 2304 x 768, 256 wide:
-// 74.1 against 70.5 us; 8192 x 768 x 3072, 192 wide: 52.6 against 49.7 us).
-// Of the widths that pay, the better-filled one is taken, 256 on a tie
-// (more FLOPs per operand byte): 192 for 16384 x 2304 x 768 (three whole
-// rounds; 64.4 us) and 16384 x 768 x K (one; 27.3 and 70.5 us for K = 768,
-// 3072). For K > 3072 (the 4096-wide decoder) a width pays from one whole
-// round of tiles on.
+// last round on the CUs at least three-quarters, or number at least
+// three-quarters of one round (16384 x 768 x 3072, 256 wide, 192 tiles:
+// 69.2 against 78.0 us; 4096 x 2304 x 768, 192 wide, 192 tiles: 18.4
+// against 21.5 us); rounds filled less lose (16384 x 2304 x 768, 256 wide,
+// 2.25 rounds: 68.0 against 67.4 us; 8192 x 768 x 3072, 192 wide, half a
+// round: 52.3 against 47.8 us). Of the widths that pay, the better-filled
+// one is taken, 256 on a tie (more FLOPs per operand byte): 192 for
+// 16384 x 2304 x 768 (three whole rounds: 57.9 us) and 16384 x 768 x K (one:
+// 25.8 and 65.2 us for K = 768 and 3072), 256 for 16384 x 3072 x 768 (85.9
+// us; persistent 128x128 95.2). For K > 3072 (the 4096-wide decoder) a
+// width pays from one whole round of tiles on.
 int w4p_width(int M, int N, int K, const EpiParams& ep) {
   const long cus = device_cus();
   int best = 0;
@@ -1766,7 +1767,7 @@ int w4p_width(int M, int N, int K, const EpiParams& ep) {
     bool pays;
     if (K > 3072) pays = tiles >= cus;
     else if (tiles >= cus) pays = rem == 0 || 4 * rem >= 3 * cus;
-    else pays = K >= 2048 && 4 * tiles >= 3 * cus;
+    else pays = 4 * tiles >= 3 * cus;
     if (!pays) continue;
     const long slots = (tiles + cus - 1) / cus * cus;
     if (best == 0 || tiles * best_slots > best_fill * slots) {

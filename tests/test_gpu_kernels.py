@@ -187,7 +187,8 @@ def test_linear_split_k(m, n, k, epi):
 
 @pytest.mark.parametrize("m,n,k,split", [(16129, 3072, 768, False),   # persistent 256x256: whole rounds
                                          (16129, 2304, 768, False),   # persistent 256x192: whole rounds
-                                         (12289, 768, 3072, False),   # persistent 256x192: long K
+                                         (12289, 768, 3072, False),   # persistent 256x192: 0.77 round
+                                         (4001, 2304, 768, False),    # persistent 256x192: 0.75 round
                                          (4097, 4096, 4096, False),   # persistent 256x256: K > 3072
                                          (12289, 3072, 768, False),   # persistent 128x128
                                          (1000, 768, 768, False),
