@@ -320,6 +320,33 @@ def test_attention_with_scores(dtype, hd, causal):
     assert abs(scores.cpu().double().sum() - H * sum(lens)) <= 1e-4 * H * sum(lens)
 
 
+@pytest.mark.parametrize("hd", [64, 128])
+@pytest.mark.parametrize("causal", [False, True])
+def test_attention_long_sequences(hd, causal):
+    """Sequences past 512 rows take 256-query blocks of eight waves (ragged
+    last block; a short sequence in the same launch)."""
+    lens = [700, 90, 513]
+    H = 2
+    qkv, q, k, v = _qkv(lens, H, hd, "bf16", seed=70 + hd + causal)
+    seqs = zsa.Seqs(lens, dev())
+    out, lse, scores = zsa.attention_with_scores(q, k, v, H, seqs, causal)
+    torch.cuda.synchronize()
+    q64, k64, v64 = f64(q), f64(k), f64(v)
+    o_ref, lse_ref, s_ref = [], [], []
+    for b, n in enumerate(lens):
+        lo = int(seqs.host[b])
+        o, l, sc = O.attention(q64[lo:lo + n], k64[lo:lo + n], v64[lo:lo + n], np.arange(n), H,
+                               causal)
+        o_ref.append(o)
+        lse_ref.append(l)
+        s_ref.append(sc)
+    assert_close(f64(out), np.concatenate(o_ref), 1e-2, "attention output")
+    lse_ref = np.concatenate(lse_ref, axis=1)
+    assert np.max(np.abs(lse.cpu().numpy() - lse_ref)) <= 2e-5 * max(1.0, np.abs(lse_ref).max())
+    s_ref = np.concatenate(s_ref)
+    assert np.max(np.abs(scores.cpu().numpy() - s_ref) / s_ref) <= 1e-4
+
+
 @pytest.mark.parametrize("dtype,hd,hkv", [("bf16", 64, 2), ("bf16", 128, 1), ("f32", 32, 2),
                                           ("bf16", 64, 4)])
 @pytest.mark.parametrize("causal", [False, True])
