@@ -202,9 +202,25 @@ __global__ __launch_bounds__(64 * NW) __attribute__((amdgpu_waves_per_eu(HD == 6
         for (int r = 0; r < 16; ++r) mloc = fmaxf(mloc, s[ks][r]);
       mloc = half_swap_max(mloc);
       const float m_new = fmaxf(m_run, mloc);
-      // scale > 0, so the max of the scaled scores is the scaled max
-      const float m_use = m_new == -INFINITY ? 0.f : m_new * scale_log2;
-      const float alpha = __builtin_amdgcn_exp2f(m_run * scale_log2 - m_use);
+      // The reference max moves (and the sums and accumulators are rescaled)
+      // only when some query's max has grown by more than 2^8 in exp2 units
+      // since the reference was set: probabilities stay below 256 (exact in
+      // fp32, full relative precision in bf16), and since the output and the
+      // log-sum-exp are both taken relative to the reference, the result is
+      // the same for any reference. A row's first valid scores always move
+      // it (from -inf). scale > 0, so the max of the scaled scores is the
+      // scaled max.
+      if (__builtin_amdgcn_ballot_w64(m_new == -INFINITY ? false
+                                                         : !((m_new - m_run) * scale_log2 <= 8.0f)) != 0) {
+        const float alpha = m_new == -INFINITY ? 1.0f : __builtin_amdgcn_exp2f((m_run - m_new) * scale_log2);
+        l_run *= alpha;
+#pragma unroll
+        for (int ct = 0; ct < HD / 32; ++ct)
+#pragma unroll
+          for (int r = 0; r < 16; ++r) o[ct][r] *= alpha;
+        m_run = m_new;
+      }
+      const float m_use = m_run == -INFINITY ? 0.f : m_run * scale_log2;
       float rsum = 0.f;
 #pragma unroll
       for (int ks = 0; ks < 2; ++ks)
@@ -215,15 +231,7 @@ __global__ __launch_bounds__(64 * NW) __attribute__((amdgpu_waves_per_eu(HD == 6
           rsum += p;
         }
       rsum = half_swap_sum(rsum);
-      l_run = l_run * alpha + rsum;
-      m_run = m_new;
-      // the accumulators change scale only when some lane's max moved
-      if (__builtin_amdgcn_ballot_w64(alpha != 1.0f) != 0) {
-#pragma unroll
-        for (int ct = 0; ct < HD / 32; ++ct)
-#pragma unroll
-          for (int r = 0; r < 16; ++r) o[ct][r] *= alpha;
-      }
+      l_run += rsum;
 #pragma unroll
       for (int g = 0; g < 4; ++g) {
         const int ks = g >> 1, rb = (g & 1) * 8;
