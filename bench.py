@@ -12,7 +12,11 @@ The keep rate is swept over 1.0, 0.7, 0.5, 0.3, 0.1; `value` is the
 throughput at keep rate 0.5 (input tokens per second), the other points go
 to `sweep` with their speedup over keep rate 1. `other_workloads` adds the
 same sweep for the paper's own schedule (Eq. 2 after every layer, tau = 5)
-on a GPT-2-small-shaped causal stack at 128, 512 and 1024 rows per sequence.
+on a GPT-2-small-shaped causal stack at 128, 512 and 1024 rows per sequence,
+for a LLaMA-3-8B-shaped slice (with its decode step), and for the other
+workloads of the method's scope: a 1B- and a 7B-shaped decoder prefill, a
+ragged batch of one 7B-shaped layer with per-sequence keep rates, and the
+tiny encoder the oracle runs in full.
 
 `roofline` is reported for the kernel class with the largest share of GPU
 time, the projections: algorithmic FLOPs (2 * rows * out * in per
@@ -44,6 +48,8 @@ PEAK_HBM_GBS = 8000.0
 # cycles: 256 CUs x 4 SIMDs x 4 exp per clock x 2.4 GHz
 PEAK_EXP_PER_S = 256 * 4 * 4 * 2.4e9
 HEADLINE_RATE = 0.5
+# sweep key of presets whose keep rates are drawn per sequence
+PER_SEQ = "per_sequence"
 
 
 def parse():
@@ -54,7 +60,7 @@ def parse():
     ap.add_argument("--workload", default="bert")
     ap.add_argument("--keep-rates", default=None, help="comma-separated sweep")
     ap.add_argument("--seed", type=int, default=0)
-    ap.add_argument("--also", default="gpt2,gpt2_n128,gpt2_n1024,llama3_8b",
+    ap.add_argument("--also", default="gpt2,gpt2_n128,gpt2_n1024,llama3_8b,dec1b,dec7b,ragged,tiny",
                     help="comma-separated presets whose keep-rate sweeps are reported beside "
                          "the headline workload")
     ap.add_argument("--no-graph", action="store_true", help="time eager launches instead")
@@ -317,7 +323,7 @@ def measure(p, rates, args, torch, W, zsa, dev, timing):
 
     results = {}
     for rate in rates:
-        kr = W.keep_rates(p, args.seed, rate)
+        kr = W.keep_rates(p, args.seed, None if rate == PER_SEQ else rate)
         outs = stack.forward(xd, posd, seqs, p.prune_after, kr)   # allocates outputs once
         torch.cuda.synchronize()
         if args.no_graph:
@@ -444,7 +450,8 @@ def sweep_of(results, rates):
     out = []
     for rate in rates:
         r = results[rate]
-        out.append({"keep_rate": rate, "tokens_per_s": round(r["tok_s"], 1),
+        label = rate if rate != PER_SEQ else "per sequence, uniform in [0.05, 1]"
+        out.append({"keep_rate": label, "tokens_per_s": round(r["tok_s"], 1),
                     "ms_per_step": round(r["ms"], 4),
                     "speedup_vs_keep_rate_1": None if base is None else round(base["ms"] / r["ms"], 3),
                     "rows_after_last_prune": r["kept_rows_final"]})
@@ -474,8 +481,10 @@ def describe(p):
         where = "after layers " + "/".join(map(str, p.prune_after))
     heads = f"H{p.n_heads}" + (f"/KV{p.kv_heads}" if p.kv_heads != p.n_heads else "")
     last = ", last row always kept" if p.force_keep_last else ""
+    rows = (f"{p.batch} sequences of U[{p.min_len}, {p.seq_len}] rows" if p.ragged
+            else f"{p.batch}x{p.seq_len} rows")
     return (f"{p.name}: {p.n_layers}-layer {mask} {kind} d{p.d_model} {heads} FFN{p.d_ff}, "
-            f"{p.batch}x{p.seq_len} rows, pruned {where} (tau {p.tau}){last}")
+            f"{rows}, pruned {where} (tau {p.tau}){last}")
 
 
 def main():
@@ -564,8 +573,12 @@ def main():
     others = {}
     for name in [w for w in args.also.split(",") if w and w != p.name]:
         q = W.PRESETS[name]
-        _, _, _, res = measure(q, list(q.keep_rates), args, torch, W, zsa, dev, timing=False)
-        others[name] = {"workload": describe(q), "sweep": sweep_of(res, list(q.keep_rates))}
+        # keep rate 1 first, the reference of the speedups
+        rates = [1.0] + [r for r in q.keep_rates if r != 1.0]
+        if q.per_seq_rates:
+            rates.append(PER_SEQ)
+        _, _, _, res = measure(q, rates, args, torch, W, zsa, dev, timing=False)
+        others[name] = {"workload": describe(q), "sweep": sweep_of(res, rates)}
 
     ceil = ceilings(torch, dev)
 
