@@ -76,7 +76,11 @@ __device__ __forceinline__ float gelu_erf(float z) {
                 t * (0.5f * 1.421413741f + t * (0.5f * -1.453152027f + t * (0.5f * 1.061405429f)))));
   return fmaf(-a * hp, __expf(-0.5f * z * z), fmaxf(z, 0.0f));
 }
-__device__ __forceinline__ float silu(float z) { return z / (1.0f + expf(-z)); }
+// z sigmoid(z) with the hardware exp and reciprocal (each within a couple of
+// ulp; the products are rounded to bf16)
+__device__ __forceinline__ float silu(float z) {
+  return z * __builtin_amdgcn_rcpf(1.0f + __expf(-z));
+}
 
 // tile: fp32 [BM][ldt] in LDS holding (x W^T) for rows m0.., columns n0..
 template <typename T, int BM, int BN, int NT>
@@ -370,6 +374,32 @@ template <int EPI>
 __device__ __forceinline__ void epi_store32(const f32x16_t& a, const uint2 (&bw)[4], uint32_t (&r)[2][4],
                                             __amdgpu_buffer_rsrc_t yres, uint32_t m, int nc, int half,
                                             int ldy) {
+  if (EPI == EPI_SWIGLU) {
+    // gate and up on columns 2c, 2c + 1: a lane's four columns of group g
+    // give outputs nc / 2 + 4g + 2 half (+1); after the swap of groups 2p
+    // and 2p + 1 the lower lanes hold outputs nc / 2 + 8p .. + 3 and the
+    // upper lanes the next four, 8 bytes each (ldy is the output width)
+#pragma unroll
+    for (int p = 0; p < 2; ++p) {
+      uint32_t pk[2];
+#pragma unroll
+      for (int gg = 0; gg < 2; ++gg) {
+        const int g = 2 * p + gg;
+        const float z0 = a[4 * g + 0] + __uint_as_float(bw[g].x << 16);
+        const float z1 = a[4 * g + 1] + __uint_as_float(bw[g].x & 0xffff0000u);
+        const float z2 = a[4 * g + 2] + __uint_as_float(bw[g].y << 16);
+        const float z3 = a[4 * g + 3] + __uint_as_float(bw[g].y & 0xffff0000u);
+        pk[gg] = pack_bf16x2(silu(z0) * z1, silu(z2) * z3);
+      }
+      lane_swap(pk[0], pk[1]);
+      typedef uint32_t u32x2 __attribute__((ext_vector_type(2)));
+      const u32x2 v = {pk[0], pk[1]};
+      __builtin_amdgcn_raw_buffer_store_b64(
+          v, yres, (m * static_cast<uint32_t>(ldy) + static_cast<uint32_t>(nc / 2 + 8 * p + 4 * half)) * 2u,
+          0, 0);
+    }
+    return;
+  }
 #pragma unroll
   for (int p = 0; p < 2; ++p) {
     if (EPI == EPI_RESIDUAL) {
@@ -1263,15 +1293,17 @@ int device_cus() {
   return cus[dev];
 }
 
-// the persistent kernel takes bf16 products with N a multiple of 128, K a
-// multiple of 64, no rotary / SwiGLU epilogue, buffers below 2^31 bytes, and
-// output (and residual) rows of whole 16-byte units on 16-byte boundaries
+// the persistent kernels take bf16 products with N a multiple of 128, K a
+// multiple of 64, no rotary epilogue, buffers below 2^31 bytes, and output
+// (and residual) rows of whole 16-byte units on 16-byte boundaries
 bool persist_ok(int M, int N, int K, const EpiParams& ep) {
   if (N % 128 != 0 || K % 64 != 0 || K < 64 || M <= 0) return false;
   if (reinterpret_cast<uintptr_t>(ep.bias) % 8 != 0 || ep.ldy % 8 != 0) return false;
   if (reinterpret_cast<uintptr_t>(ep.y) % 16 != 0 || reinterpret_cast<uintptr_t>(ep.residual) % 16 != 0)
     return false;
-  if (ep.epi != EPI_NONE && ep.epi != EPI_GELU && ep.epi != EPI_RESIDUAL) return false;
+  if (ep.epi != EPI_NONE && ep.epi != EPI_GELU && ep.epi != EPI_RESIDUAL && ep.epi != EPI_SWIGLU)
+    return false;
+  if (ep.epi == EPI_SWIGLU && N % 16 != 0) return false;
   return static_cast<int64_t>(M + 128) * ep.ldy * 2 < (int64_t{1} << 31);
 }
 
@@ -1730,6 +1762,7 @@ hipError_t launch_w4(hipStream_t s, const void* x, int M, int K, const void* w, 
                      const EpiParams& ep) {
   if (ep.epi == EPI_GELU) return launch_w4_1<EPI_GELU>(s, x, M, K, w, N, ep);
   if (ep.epi == EPI_RESIDUAL) return launch_w4_1<EPI_RESIDUAL>(s, x, M, K, w, N, ep);
+  if (ep.epi == EPI_SWIGLU) return launch_w4_1<EPI_SWIGLU>(s, x, M, K, w, N, ep);
   return launch_w4_1<EPI_NONE>(s, x, M, K, w, N, ep);
 }
 
@@ -1784,6 +1817,7 @@ hipError_t launch_w4p(hipStream_t s, const void* x, int M, int K, const void* w,
                       const EpiParams& ep) {
   if (ep.epi == EPI_GELU) return launch_w4p_1<EPI_GELU, BN>(s, x, M, K, w, N, ep);
   if (ep.epi == EPI_RESIDUAL) return launch_w4p_1<EPI_RESIDUAL, BN>(s, x, M, K, w, N, ep);
+  if (ep.epi == EPI_SWIGLU) return launch_w4p_1<EPI_SWIGLU, BN>(s, x, M, K, w, N, ep);
   return launch_w4p_1<EPI_NONE, BN>(s, x, M, K, w, N, ep);
 }
 
@@ -1792,6 +1826,7 @@ hipError_t launch_persist_any(hipStream_t s, const void* x, int M, int K, const 
                               const EpiParams& ep) {
   if (ep.epi == EPI_GELU) return launch_persist<EPI_GELU, KB, WPC>(s, x, M, K, w, N, ep);
   if (ep.epi == EPI_RESIDUAL) return launch_persist<EPI_RESIDUAL, KB, WPC>(s, x, M, K, w, N, ep);
+  if (ep.epi == EPI_SWIGLU) return launch_persist<EPI_SWIGLU, KB, WPC>(s, x, M, K, w, N, ep);
   return launch_persist<EPI_NONE, KB, WPC>(s, x, M, K, w, N, ep);
 }
 

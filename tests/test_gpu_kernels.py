@@ -194,7 +194,7 @@ def test_linear_split_k(m, n, k, epi):
                                          (1000, 768, 768, False),
                                          (4000, 768, 3072, False),
                                          (16385, 2304, 768, False)])
-@pytest.mark.parametrize("epi", [zsa.EPI_NONE, zsa.EPI_GELU, zsa.EPI_RESIDUAL])
+@pytest.mark.parametrize("epi", [zsa.EPI_NONE, zsa.EPI_GELU, zsa.EPI_RESIDUAL, zsa.EPI_SWIGLU])
 @pytest.mark.parametrize("with_bias", [True, False])
 def test_linear_kernel_regimes(m, n, k, split, epi, with_bias):
     """Every GEMM the projection shapes dispatch to (by grid size and
@@ -220,6 +220,8 @@ def test_linear_kernel_regimes(m, n, k, split, epi, with_bias):
         z = O.gelu(z)
     elif epi == zsa.EPI_RESIDUAL:
         z = z + f64(res[rt])
+    elif epi == zsa.EPI_SWIGLU:
+        z = O.silu(z[:, 0::2]) * z[:, 1::2]
     assert_close(f64(y1[rt]), z, 1e-2, f"regime {m}x{n}x{k} epilogue {epi}")
 
 
