@@ -225,6 +225,37 @@ def test_linear_kernel_regimes(m, n, k, split, epi, with_bias):
     assert_close(f64(y1[rt]), z, 1e-2, f"regime {m}x{n}x{k} epilogue {epi}")
 
 
+@pytest.mark.parametrize("m,n,k,hd,rope_cols", [(16129, 3072, 768, 64, 2048),   # 256x256 on 8 waves
+                                               (4097, 4096, 4096, 128, 2048),   # K > 3072
+                                               (4097, 6144, 4096, 128, 5120),   # grouped-query
+                                               (3000, 3072, 768, 64, 2048)])    # 128x128
+@pytest.mark.parametrize("with_bias", [True, False])
+def test_linear_rope_regimes(m, n, k, hd, rope_cols, with_bias):
+    """The rotary epilogue in the kernels the decoders' QKV projections
+    dispatch to (ragged rows, grouped-query widths), against the oracle on
+    sampled rows, and reproducible."""
+    g = np.random.default_rng(m + n + hd + int(with_bias))
+    x = g.standard_normal((m, k)).astype(np.float32)
+    w = (g.standard_normal((n, k)) / math.sqrt(k)).astype(np.float32)
+    xd, wd = to_dev(x, "bf16"), to_dev(w, "bf16")
+    bd = to_dev((0.1 * g.standard_normal(n)).astype(np.float32), "bf16") if with_bias else None
+    pos = g.integers(0, 8192, m).astype(np.int32)
+    posd = torch.from_numpy(pos).to(dev())
+    kw = dict(pos=posd, head_dim=hd, rope_cols=rope_cols, rope_theta=500000.0, split=False)
+    y1 = zsa.linear(xd, wd, bd, zsa.EPI_ROPE, **kw)
+    y2 = zsa.linear(xd, wd, bd, zsa.EPI_ROPE, **kw)
+    torch.cuda.synchronize()
+    assert torch.equal(y1, y2)
+    rows = np.unique(np.concatenate([np.arange(64), np.arange(m - 64, m), g.integers(0, m, 128)]))
+    rt = torch.from_numpy(rows).to(dev())
+    z = f64(xd[rt]) @ f64(wd).T
+    if bd is not None:
+        z = z + f64(bd)
+    ref = z.copy()
+    ref[:, :rope_cols] = O.rope(z[:, :rope_cols], pos[rows].astype(np.int64), rope_cols // hd, 5e5)
+    assert_close(f64(y1[rt]), ref, 1e-2, f"rope regime {m}x{n}x{k} hd {hd}")
+
+
 @pytest.mark.parametrize("m,n,k,hd", [(1, 384, 256, 64), (4, 6144, 4096, 128),
                                       (4, 4096, 14336, 128), (16, 3072, 768, 64),
                                       (3, 400, 512, 16), (7, 2304, 768, 64), (5, 512, 800, 64),
