@@ -5,7 +5,7 @@
 // each query row's final log-sum-exp, which the attention pass has already
 // written, so this is a second sweep over Q K^T that never stores P.
 //
-// bf16, head_dim 64/128 (MFMA): one 256-thread workgroup per (64-key block,
+// bf16, head_dim 64/128 (MFMA): one 256-thread workgroup per (128-key block,
 // head group, sequence). Its K tile sits in registers as the B operand; the
 // 4 waves stride over 32-query tiles and compute S = Q K^T with
 // v_mfma_f32_32x32x16_bf16 in the *non*-transposed layout, where a lane owns
@@ -30,31 +30,37 @@ typedef float f32x16_t __attribute__((ext_vector_type(16)));
 
 constexpr float kLog2e = 1.4426950408889634f;
 constexpr int kLseChunk = 2048;
+// keys per workgroup: every workgroup reads the query rows of its heads once,
+// so wider key blocks move fewer bytes per score
+constexpr int kScoreKeys = 128;
 
-template <int HD>
+template <int HD, int KB>
 __global__ __launch_bounds__(256) void score_mfma_kernel(
     const bf16_t* __restrict__ Q, const bf16_t* __restrict__ K, int64_t rs,
     const float* __restrict__ lse, int H, int kv_group, int causal, float scale_log2,
     const int32_t* __restrict__ cu, int T, int groups, float* __restrict__ partials) {
   constexpr int KLD = HD + 8;
   constexpr int KK = HD / 16;
-  __shared__ __align__(16) bf16_t Ks[64 * KLD];
+  constexpr int KS = KB / 32;  // 32-key column blocks
+  __shared__ __align__(16) bf16_t Ks[KB * KLD];
   __shared__ __align__(16) float Ls[kLseChunk];
-  __shared__ float red[4][64];
+  __shared__ float red[4][KB];
 
   const int b = blockIdx.z, g = blockIdx.y;
   const int lo = cu[b];
   const int n = cu[b + 1] - lo;
-  const int j0 = blockIdx.x * 64;
+  const int j0 = blockIdx.x * KB;
   if (j0 >= n) return;
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int half = lane >> 5, l32 = lane & 31;
-  float colsum[2] = {0.f, 0.f};
+  float colsum[KS];
+#pragma unroll
+  for (int ks = 0; ks < KS; ++ks) colsum[ks] = 0.f;
 
   const int qs = causal ? (j0 & ~31) : 0;
   for (int h = g; h < H; h += groups) {
     __syncthreads();  // previous head's readers are done with Ks / Ls
-    for (int c = tid; c < 64 * HD / 8; c += 256) {
+    for (int c = tid; c < KB * HD / 8; c += 256) {
       const int r = c / (HD / 8), ch = (c % (HD / 8)) * 8;
       const int jr = j0 + r;
       // keys past the sequence repeat the last row; their columns are not written
@@ -63,9 +69,9 @@ __global__ __launch_bounds__(256) void score_mfma_kernel(
                                           (h / kv_group) * HD + ch);
     }
     __syncthreads();
-    bf16x8_t kf[2][KK];
+    bf16x8_t kf[KS][KK];
 #pragma unroll
-    for (int ks = 0; ks < 2; ++ks)
+    for (int ks = 0; ks < KS; ++ks)
 #pragma unroll
       for (int kk = 0; kk < KK; ++kk)
         kf[ks][kk] = __builtin_bit_cast(
@@ -105,9 +111,9 @@ __global__ __launch_bounds__(256) void score_mfma_kernel(
           lq[q4] = *reinterpret_cast<const float4*>(Ls + (i0 - c0) + 8 * q4 + 4 * half);
         // masks matter only where the tile crosses the sequence end or, under
         // the causal mask, reaches keys after some of its queries
-        const bool edge = i0 + 32 > cend || (causal && j0 + 63 > i0);
+        const bool edge = i0 + 32 > cend || (causal && j0 + KB - 1 > i0);
 #pragma unroll
-        for (int ks = 0; ks < 2; ++ks) {
+        for (int ks = 0; ks < KS; ++ks) {
           f32x16_t acc;
 #pragma unroll
           for (int r = 0; r < 16; ++r) acc[r] = 0.f;
@@ -140,13 +146,13 @@ __global__ __launch_bounds__(256) void score_mfma_kernel(
     }
   }
 #pragma unroll
-  for (int ks = 0; ks < 2; ++ks) colsum[ks] = half_swap_sum(colsum[ks]);
+  for (int ks = 0; ks < KS; ++ks) colsum[ks] = half_swap_sum(colsum[ks]);
   if (half == 0) {
-    red[wave][l32] = colsum[0];
-    red[wave][32 + l32] = colsum[1];
+#pragma unroll
+    for (int ks = 0; ks < KS; ++ks) red[wave][32 * ks + l32] = colsum[ks];
   }
   __syncthreads();
-  if (tid < 64) {
+  if (tid < KB) {
     const int j = j0 + tid;
     const float v = ((red[0][tid] + red[1][tid]) + red[2][tid]) + red[3][tid];
     if (j < n) partials[static_cast<int64_t>(g) * T + lo + j] = v;
@@ -225,7 +231,7 @@ hipError_t valu_dispatch(hipStream_t s, const void* q, const void* k, int64_t rs
 // ~1024 workgroups (H when none does); the MFMA path only.
 int score_groups(int dtype, int H, int hd, int T) {
   if (!(dtype == 1 && (hd == 64 || hd == 128))) return 1;
-  const int kblocks = (T + 63) / 64;
+  const int kblocks = (T + kScoreKeys - 1) / kScoreKeys;
   for (int g = 1; g <= H; ++g)
     if (H % g == 0 && kblocks * g >= 1024) return g;
   return H;
@@ -237,15 +243,15 @@ hipError_t launch_score(hipStream_t s, int dtype, const void* q, const void* k,
                         float* partials, int groups) {
   if (B == 0 || max_len == 0) return hipSuccess;
   if (dtype == 1 && (hd == 64 || hd == 128)) {
-    const dim3 grid((max_len + 63) / 64, groups, B), block(256);
+    const dim3 grid((max_len + kScoreKeys - 1) / kScoreKeys, groups, B), block(256);
     const bf16_t* qp = static_cast<const bf16_t*>(q);
     const bf16_t* kp = static_cast<const bf16_t*>(k);
     const float sl = scale * kLog2e;
     if (hd == 64)
-      return launch(K_SCORE, score_mfma_kernel<64>, grid, block, 0, s, qp, kp, row_stride, lse,
-                    H, kv_group, causal, sl, cu_dev, T, groups, partials);
-    return launch(K_SCORE, score_mfma_kernel<128>, grid, block, 0, s, qp, kp, row_stride, lse, H,
-                  kv_group, causal, sl, cu_dev, T, groups, partials);
+      return launch(K_SCORE, score_mfma_kernel<64, kScoreKeys>, grid, block, 0, s, qp, kp, row_stride,
+                    lse, H, kv_group, causal, sl, cu_dev, T, groups, partials);
+    return launch(K_SCORE, score_mfma_kernel<128, kScoreKeys>, grid, block, 0, s, qp, kp, row_stride,
+                  lse, H, kv_group, causal, sl, cu_dev, T, groups, partials);
   }
   if (dtype == 1)
     return valu_dispatch<bf16_t>(s, q, k, row_stride, lse, H, kv_group, hd, causal, scale, B,
