@@ -10,17 +10,24 @@
 //    grids, the slices summed in slice order by splitk_reduce_kernel;
 //  * gemm_bf16_persist_kernel: 128x128 tiles, two workgroups per CU walking
 //    their XCD's range of tiles, the epilogue from registers;
-//  * gemm_bf16_w4_kernel: 256x256 tiles on four waves of 128x128;
-//  * gemm_skinny_kernel: products of at most 16 rows (generation), W
-//    streamed into v_mfma_f32_16x16x32_bf16 operands;
+//  * gemm_bf16_w4p_kernel: 256x256 or 256x192 tiles on four waves (one per
+//    SIMD), one workgroup per CU streaming the K slices of its tiles as one
+//    sequence, the epilogue from registers (products whose tiles fill their
+//    rounds on the CUs, w4p_width);
+//  * gemm_bf16_w4_kernel: its slice loop with one tile per workgroup (a
+//    tuning baseline, ZSA_GEMM_TILE);
+//  * gemm_skinny_kernel: products of at most 64 rows (256 with N, K <=
+//    1024; generation and short pruned layers), W streamed into
+//    v_mfma_f32_16x16x32_bf16 operands;
 //  * gemm_bf16_mfma_kernel: the register-staged 128x128 original, kept as a
 //    tuning baseline (ZSA_GEMM_TILE).
 // The others use v_mfma_f32_32x32x16_bf16. fp32 storage: a 64x128
 // vector-ALU tile (4x8 outputs per thread).
 //
-// Epilogues (all kernels, same order and precision): bias, exact GELU,
-// SwiGLU on interleaved gate/up columns, residual add, or the rotary
-// rotation of head channel pairs (i, i+hd/2).
+// Epilogues (same order and precision in every kernel that takes them):
+// bias, exact GELU, SwiGLU on interleaved gate/up columns, residual add, or
+// the rotary rotation of head channel pairs (i, i+hd/2) -- the last only in
+// the direct-to-LDS, register-staged and few-row kernels.
 #include <math.h>
 #include <stdlib.h>
 
