@@ -353,6 +353,45 @@ def test_attention_with_scores(dtype, hd, causal):
     assert abs(scores.cpu().double().sum() - H * sum(lens)) <= 1e-4 * H * sum(lens)
 
 
+@pytest.mark.parametrize("lens", [[100, 37], [300, 700]])   # 128- and 256-query blocks
+@pytest.mark.parametrize("hd", [64, 128])
+@pytest.mark.parametrize("causal", [False, True])
+def test_attention_growing_scores(lens, hd, causal):
+    """Key rows whose norm grows fivefold along the sequence: queries' running
+    maxima grow by more than 2^8 in exp2 units after their first key tile
+    (12 to 3107 such moves per case, counted on the host from these inputs),
+    so the kernel moves its reference max and rescales its sums and
+    accumulators mid-sequence, not only at the first tile."""
+    H = 2
+    g = np.random.default_rng(90 + hd + causal + len(lens))
+    T, d = sum(lens), H * hd
+    qkv = g.standard_normal((T, 3 * d)).astype(np.float32)
+    qkv[:, :d] *= 1.5
+    lo = 0
+    for n in lens:
+        qkv[lo:lo + n, d:2 * d] *= (1.0 + 4.0 * np.arange(n) / max(n - 1, 1))[:, None]
+        lo += n
+    t = to_dev(qkv, "bf16")
+    q, k, v = t[:, :d], t[:, d:2 * d], t[:, 2 * d:]
+    seqs = zsa.Seqs(lens, dev())
+    out, lse, scores = zsa.attention_with_scores(q, k, v, H, seqs, causal)
+    torch.cuda.synchronize()
+    q64, k64, v64 = f64(q), f64(k), f64(v)
+    o_ref, lse_ref, s_ref = [], [], []
+    for b, n in enumerate(lens):
+        lo = int(seqs.host[b])
+        o, l, sc = O.attention(q64[lo:lo + n], k64[lo:lo + n], v64[lo:lo + n], np.arange(n), H,
+                               causal)
+        o_ref.append(o)
+        lse_ref.append(l)
+        s_ref.append(sc)
+    assert_close(f64(out), np.concatenate(o_ref), 1e-2, "attention output")
+    lse_ref = np.concatenate(lse_ref, axis=1)
+    assert np.max(np.abs(lse.cpu().numpy() - lse_ref)) <= 2e-5 * max(1.0, np.abs(lse_ref).max())
+    s_ref = np.concatenate(s_ref)
+    assert np.max(np.abs(scores.cpu().numpy() - s_ref) / s_ref) <= 1e-4
+
+
 @pytest.mark.parametrize("hd", [64, 128])
 @pytest.mark.parametrize("causal", [False, True])
 def test_attention_long_sequences(hd, causal):
