@@ -186,6 +186,8 @@ def test_linear_split_k(m, n, k, epi):
 
 
 @pytest.mark.parametrize("m,n,k,split", [(16129, 3072, 768, False),   # persistent 256x256: whole rounds
+                                         (16129, 3072, 128, False),   # two K slices per tile
+                                         (16129, 2304, 192, False),   # three, 256x192
                                          (16129, 2304, 768, False),   # persistent 256x192: whole rounds
                                          (12289, 768, 3072, False),   # persistent 256x192: 0.77 round
                                          (4001, 2304, 768, False),    # persistent 256x192: 0.75 round
