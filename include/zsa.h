@@ -33,6 +33,10 @@
  *    a multiple of 16 bytes long.
  *  - Row indices are int32; pos[] holds each row's original sequence
  *    position (0 .. n_b-1 before any pruning) and travels with the row.
+ *  - The rows one attention call reads for a sequence (its longest sequence,
+ *    plus 256 rows, times the Q/K/V row stride) and the rows of one
+ *    key/value cache slot must span less than 4 GiB: the kernels address
+ *    them with 32-bit offsets. Larger calls return ZSA_EUNSUPPORTED.
  *  - Every entry point validates its arguments before it enqueues anything:
  *    on a validation error nothing is written and a negative status is
  *    returned; zsa_last_error() then describes it (thread-local). Faults in
@@ -287,6 +291,10 @@ size_t zsa_layer_workspace_size(const zsa_layer_cfg* cfg, int32_t total_rows, in
  *   scores_dbg fp32 device or NULL: the scores at each pruning point,
  *     concatenated (point p occupies the rows entering that block)
  *   pos_dbg int32 device or NULL: pos after each pruning point, concatenated
+ *   hidden_dbg device or NULL: every block's output rows, dtype, concatenated
+ *     in block order; block l occupies the rows leaving it (after its pruning
+ *     point if it prunes, all current rows otherwise), so the whole buffer
+ *     holds sum over blocks of those row counts times d_model elements
  *   kv_cache device or NULL (causal stacks only): the key/value cache a
  *     decode step attends to (see zsa_decode_step). Block l writes the k
  *     (after RoPE) and v of the rows that entered it, sequence b's row r at
@@ -303,8 +311,8 @@ int zsa_stack_forward(void* stream, const zsa_layer_cfg* cfg, const zsa_layer_we
                       int32_t batch, const int32_t* cu_host, const int32_t* cu_dev,
                       void* hidden_out, int32_t* pos_out, int32_t* cu_out_host,
                       int32_t* cu_out_dev, int32_t* counts_out_host, float* scores_dbg,
-                      int32_t* pos_dbg, void* kv_cache, int32_t kv_capacity, void* ws,
-                      size_t ws_bytes);
+                      int32_t* pos_dbg, void* hidden_dbg, void* kv_cache, int32_t kv_capacity,
+                      void* ws, size_t ws_bytes);
 size_t zsa_stack_workspace_size(const zsa_layer_cfg* cfg, int32_t total_rows, int32_t batch,
                                 int32_t n_prune);
 

@@ -106,6 +106,18 @@ int check_width(int32_t dtype, int64_t width, const char* name) {
   return ZSA_OK;
 }
 
+// The bf16 attention kernels address one sequence's K/V rows (and the decode
+// kernel one cache slot's rows) through a buffer resource whose byte range
+// and per-tile offsets are 32-bit: the rows a kernel can reach must span
+// less than 4 GiB (with a margin of 256 rows for the tile look-ahead).
+int check_row_range(int64_t rows, int64_t row_elems, int dtype, const char* what) {
+  if ((rows + 256) * row_elems * static_cast<int64_t>(esize(dtype)) >= (int64_t{1} << 32))
+    return fail(ZSA_EUNSUPPORTED,
+                "%s: %lld rows of %lld elements span 4 GiB or more (32-bit buffer offsets)", what,
+                (long long)rows, (long long)row_elems);
+  return ZSA_OK;
+}
+
 int check_head_dim(int32_t hd) {
   if (hd != 16 && hd != 32 && hd != 64 && hd != 128)
     return fail(ZSA_EUNSUPPORTED, "head_dim %d (supported: 16, 32, 64, 128)", hd);
@@ -522,6 +534,7 @@ int zsa_attention_with_scores(void* stream, int32_t dtype, const void* q, const 
   if (row_stride < static_cast<int64_t>(n_heads) * head_dim || out_stride < static_cast<int64_t>(n_heads) * head_dim)
     return fail(ZSA_ESHAPE, "row stride shorter than n_heads * head_dim");
   if (!(scale > 0.f)) return fail(ZSA_EINVAL, "scale must be positive");
+  CHECK(check_row_range(max_len, row_stride, dtype, "attention"));
   const size_t need = zsa_attention_workspace_size(n_heads, T, scores != nullptr);
   if (scores != nullptr || lse == nullptr) {
     if (ws_bytes < need || (need > 0 && ws == nullptr))
@@ -567,6 +580,7 @@ int zsa_score_positions(void* stream, int32_t dtype, const void* q, const void* 
   if (row_stride < static_cast<int64_t>(n_heads) * head_dim)
     return fail(ZSA_ESHAPE, "row stride shorter than n_heads * head_dim");
   if (!(scale > 0.f)) return fail(ZSA_EINVAL, "scale must be positive");
+  CHECK(check_row_range(max_len, row_stride, dtype, "score"));
   const size_t need = zsa_score_workspace_size(n_heads, T);
   if (ws_bytes < need || (need > 0 && ws == nullptr))
     return fail(ZSA_EWORKSPACE, "workspace %zu bytes < %zu", ws_bytes, need);
@@ -652,6 +666,7 @@ int zsa_layer_forward(void* stream, const zsa_layer_cfg* cfg, const zsa_layer_we
     if (pos_in == nullptr || pos_out == nullptr) return fail(ZSA_EINVAL, "pos_in / pos_out is NULL");
   }
   if (cu_out_host == nullptr || cu_out_dev == nullptr) return fail(ZSA_EINVAL, "cu_out is NULL");
+  CHECK(check_row_range(max_len, qkv_width(*cfg), cfg->dtype, "attention"));
   const bool prune = keep_rate != nullptr;
   std::vector<int32_t> cu_out(batch + 1, 0);
   int32_t max_out = 0;
@@ -709,8 +724,8 @@ int zsa_stack_forward(void* stream, const zsa_layer_cfg* cfg, const zsa_layer_we
                       int32_t batch, const int32_t* cu_host, const int32_t* cu_dev,
                       void* hidden_out, int32_t* pos_out, int32_t* cu_out_host,
                       int32_t* cu_out_dev, int32_t* counts_out_host, float* scores_dbg,
-                      int32_t* pos_dbg, void* kv_cache, int32_t kv_capacity, void* ws,
-                      size_t ws_bytes) {
+                      int32_t* pos_dbg, void* hidden_dbg, void* kv_cache, int32_t kv_capacity,
+                      void* ws, size_t ws_bytes) {
   CHECK(check_cfg(cfg));
   if (n_layers < 1) return fail(ZSA_EINVAL, "n_layers %d < 1", n_layers);
   if (w == nullptr) return fail(ZSA_EINVAL, "weights are NULL");
@@ -727,6 +742,7 @@ int zsa_stack_forward(void* stream, const zsa_layer_cfg* cfg, const zsa_layer_we
   }
   int32_t T0, max_len0;
   CHECK(check_seqs(batch, cu_host, cu_dev, &T0, &max_len0));
+  CHECK(check_row_range(max_len0, qkv_width(*cfg), cfg->dtype, "attention"));
   if (n_prune > 0 && batch > 0 && keep_rate == nullptr) return fail(ZSA_EINVAL, "keep_rate is NULL");
   for (int b = 0; n_prune > 0 && b < batch; ++b) CHECK(check_rate(keep_rate[b]));
   if (T0 > 0) {
@@ -781,7 +797,8 @@ int zsa_stack_forward(void* stream, const zsa_layer_cfg* cfg, const zsa_layer_we
   const int32_t* cur_pos = pos_in;
   RowSet cur{batch, cus[0].data(), cu_dev, T0, max_len0};
   int point = 0;
-  size_t score_off = 0, pos_off = 0;
+  size_t score_off = 0, pos_off = 0, hid_off = 0;
+  const size_t row_bytes = static_cast<size_t>(cfg->d_model) * esize(cfg->dtype);
   for (int l = 1; l <= n_layers && T0 > 0; ++l) {
     const bool last = l == n_layers;
     const bool prune = point < n_prune && prune_after[point] == l;
@@ -821,6 +838,13 @@ int zsa_stack_forward(void* stream, const zsa_layer_cfg* cfg, const zsa_layer_we
                       nullptr, wb, kv_layer, kv_capacity));
     }
     cur_x = x_out;
+    if (hidden_dbg != nullptr) {  // this block's output rows (cur: the rows leaving it)
+      const size_t bytes = static_cast<size_t>(cur.T) * row_bytes;
+      HIP_TRY(hipMemcpyAsync(static_cast<char*>(hidden_dbg) + hid_off, x_out, bytes,
+                             hipMemcpyDeviceToDevice, s),
+              "hidden debug copy");
+      hid_off += bytes;
+    }
   }
   if (T0 > 0 && cur_pos != pos_out) HIP_TRY(zsa::launch_copy_i32(s, pos_out, cur_pos, cur.T), "pos copy");
   memcpy(cu_out_host, mark ? cus[0].data() : cus[n_prune].data(), sizeof(int32_t) * (batch + 1));
@@ -1079,6 +1103,7 @@ int zsa_stack_backward(void* stream, const zsa_layer_cfg* cfg, const zsa_layer_w
   }
   int32_t T0, max_len0;
   CHECK(check_seqs(batch, cu_host, cu_dev, &T0, &max_len0));
+  CHECK(check_row_range(max_len0, qkv_width(*cfg), cfg->dtype, "attention"));
   if (n_prune > 0 && batch > 0 && keep_rate == nullptr) return fail(ZSA_EINVAL, "keep_rate is NULL");
   for (int b = 0; n_prune > 0 && b < batch; ++b) CHECK(check_rate(keep_rate[b]));
   if (T0 > 0) {
@@ -1239,6 +1264,7 @@ int zsa_decode_step(void* stream, const zsa_layer_cfg* cfg, const zsa_layer_weig
   if (batch < 0) return fail(ZSA_EINVAL, "batch %d", batch);
   if (batch == 0) return ZSA_OK;
   if (kv_capacity < 1) return fail(ZSA_EINVAL, "kv_capacity %d", kv_capacity);
+  CHECK(check_row_range(kv_capacity, 2 * static_cast<int64_t>(kvd), c.dtype, "kv cache"));
   CHECK(check_ptr16(x_in, "x_in"));
   CHECK(check_ptr16(x_out, "x_out"));
   CHECK(check_ptr16(kv_cache, "kv_cache"));

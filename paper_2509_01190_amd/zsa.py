@@ -87,7 +87,7 @@ _SIGS = {
     "zsa_stack_forward": (ctypes.c_int, [_vp, ctypes.POINTER(LayerCfg),
                                          ctypes.POINTER(LayerWeights), _i32, _pi32, _i32, _pf64,
                                          _vp, _vp, _i32, _pi32, _vp, _vp, _vp, _pi32, _vp, _pi32,
-                                         _vp, _vp, _vp, _i32, _vp, _sz]),
+                                         _vp, _vp, _vp, _vp, _i32, _vp, _sz]),
     "zsa_decode_step": (ctypes.c_int, [_vp, ctypes.POINTER(LayerCfg), ctypes.POINTER(LayerWeights),
                                        _i32, _i32, _vp, _pi32, _vp, _i32, _pi32, _vp, _vp, _sz]),
     "zsa_decode_workspace_size": (_sz, [ctypes.POINTER(LayerCfg), _i32, _i32, _i32]),
@@ -433,6 +433,21 @@ class Stack:
         rows_in = [seqs.total] + marked
         return {"counts": counts, "final_rows": final, "rows_in": rows_in, "marked": marked}
 
+    def layer_out_rows(self, seqs: Seqs, prune_after: Sequence[int], keep_rate) -> List[int]:
+        """Rows leaving each block of a stack call (the row counts of the
+        per-block debug output)."""
+        plan = self.plan(seqs, prune_after, keep_rate)
+        pset = list(prune_after)
+        out, point = [], 0
+        cur = seqs.total
+        for l in range(1, self.n_layers + 1):
+            if point < len(pset) and pset[point] == l:
+                point += 1
+                if not self.cfg.mark_only:
+                    cur = plan["rows_in"][point]
+            out.append(cur)
+        return out
+
     def kv_cache(self, batch: int, capacity: int, device) -> torch.Tensor:
         """An empty key/value cache [layers, batch, capacity, 2 * kvd]."""
         kvd = (self.cfg.n_kv_heads or self.cfg.n_heads) * self.cfg.head_dim
@@ -538,6 +553,10 @@ class Stack:
                 out["scores_dbg"] = torch.empty(max(sc_rows, 1), dtype=torch.float32, device=dev)
                 out["pos_dbg"] = torch.empty(max(pos_rows, 1), dtype=torch.int32, device=dev)
                 out["rows_in"] = plan["rows_in"]
+                # every block's output rows, concatenated in block order
+                out["layer_rows"] = self.layer_out_rows(seqs, pa, kr)
+                out["hidden_dbg"] = torch.empty((max(sum(out["layer_rows"]), 1), self.cfg.d_model),
+                                                dtype=hidden.dtype, device=dev)
         ws = out["ws"]
         _check(lib().zsa_stack_forward(
             _stream(dev), ctypes.byref(self.cfg), self._wstructs, self.n_layers,
@@ -545,7 +564,8 @@ class Stack:
             seqs.batch, _hp32(seqs.host), _p(seqs.dev), _p(out["x"]), _p(out["pos"]),
             _hp32(out["cu_host"]), _p(out["cu_dev"]),
             _hp32(out["counts"]) if len(out["pa"]) else None,
-            _p(out.get("scores_dbg")), _p(out.get("pos_dbg")), _p(kv_cache),
+            _p(out.get("scores_dbg")), _p(out.get("pos_dbg")), _p(out.get("hidden_dbg")),
+            _p(kv_cache),
             0 if kv_cache is None else kv_cache.shape[2], _p(ws), ws.numel()))
         return out
 

@@ -193,3 +193,47 @@ def test_stack_rejects_misshaped_weights():
     bad["w_down"] = None
     with pytest.raises(ValueError):
         zsa.Stack(cfg, [bad])
+
+
+def test_rows_beyond_32bit_offsets_are_refused():
+    # the attention kernels reach a sequence's K/V rows through 32-bit byte
+    # offsets: a sequence whose rows span 4 GiB (here 180000 rows of a
+    # 7B-shaped fused q|k|v projection, 12288 bf16 wide) is refused up front
+    lib = zsa.lib()
+    row = 3 * 4096
+    cu = np.array([0, 180000], dtype=np.int32)
+    rc = lib.zsa_attention_with_scores(None, zsa.BF16, ctypes.c_void_p(0x1000),
+                                       ctypes.c_void_p(0x1000), ctypes.c_void_p(0x1000), row, 32,
+                                       0, 128, 1, 0.1, 1, cu.ctypes.data_as(zsa._pi32),
+                                       ctypes.c_void_p(0x4000), ctypes.c_void_p(0x5000), 4096,
+                                       ctypes.c_void_p(0x6000), None, None, 0)
+    assert rc == zsa.EUNSUPPORTED
+    assert "4 GiB" in lib.zsa_last_error().decode()
+    # one row fewer than the limit passes this check (and fails later on the
+    # missing workspace, still before any launch)
+    n_ok = (1 << 32) // (row * 2) - 256 - 1
+    cu = np.array([0, n_ok], dtype=np.int32)
+    rc = lib.zsa_attention_with_scores(None, zsa.BF16, ctypes.c_void_p(0x1000),
+                                       ctypes.c_void_p(0x1000), ctypes.c_void_p(0x1000), row, 32,
+                                       0, 128, 1, 0.1, 1, cu.ctypes.data_as(zsa._pi32),
+                                       ctypes.c_void_p(0x4000), ctypes.c_void_p(0x5000), 4096,
+                                       None, ctypes.c_void_p(0x7000), None, 0)
+    assert rc == zsa.EWORKSPACE
+    # the same limit through the layer entry point (its q|k|v rows)
+    cfg = zsa.make_cfg(zsa.DECODER, 4096, 32, 11008, True, zsa.BF16)
+    w = zsa.LayerWeights(*([0x1000] * 12))
+    cu = np.array([0, 180000], dtype=np.int32)
+    rc = lib.zsa_layer_forward(None, ctypes.byref(cfg), ctypes.byref(w), ctypes.c_void_p(0x1000),
+                               ctypes.c_void_p(0x2000), 1, cu.ctypes.data_as(zsa._pi32),
+                               ctypes.c_void_p(0x3000), None, ctypes.c_void_p(0x4000),
+                               ctypes.c_void_p(0x5000), cu.ctypes.data_as(zsa._pi32),
+                               ctypes.c_void_p(0x6000), None, None, ctypes.c_void_p(0x7000), 1)
+    assert rc == zsa.EUNSUPPORTED
+    # and for a decode step's cache slot (2 * 4096 bf16 per row: 262144 rows)
+    x = ctypes.c_void_p(0x10000)
+    pos = np.zeros(1, dtype=np.int32)
+    kvl = np.zeros(1, dtype=np.int32)
+    rc = lib.zsa_decode_step(None, ctypes.byref(cfg), ctypes.byref(w), 1, 1, x,
+                             pos.ctypes.data_as(zsa._pi32), ctypes.c_void_p(0x20000), 262144,
+                             kvl.ctypes.data_as(zsa._pi32), x, ctypes.c_void_p(0x30000), 1)
+    assert rc == zsa.EUNSUPPORTED

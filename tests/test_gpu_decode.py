@@ -8,8 +8,23 @@ import torch
 from oracle import zsa_oracle as O
 from paper_2509_01190_amd import workloads as W
 from paper_2509_01190_amd import zsa
-from tests.helpers import assert_rel_l2, assert_rows_close, dev, f64, to_dev, weights_f64
+from tests.helpers import (SEQ_TOL, assert_rel_l2, assert_rows_vs_exact, dev, f64, row_errors,
+                           to_dev, weights_f64)
+
 from tests.test_gpu_stack import build, gpu_kept_overrides
+
+TOL = SEQ_TOL["bf16"]
+
+
+def check_rows(got, ref_x, ref_e, what):
+    """Rows that each belong to another sequence (the generated row of every
+    sequence, or one appended cache row): the per-sequence tolerance applies
+    to every row, against the exact oracle; the emulation oracle only names
+    what bf16 storage alone does, in the message."""
+    for i in range(got.shape[0]):
+        assert_rel_l2(got[i:i + 1], ref_x[i:i + 1], TOL,
+                      f"{what} row {i} (bf16 storage alone: "
+                      f"{row_errors(ref_e[i:i + 1], ref_x[i:i + 1])[0]:.3e})")
 
 pytestmark = pytest.mark.gpu
 
@@ -54,11 +69,14 @@ def test_prefill_cache_and_decode(kind, hkv, prune, keep_last, hd):
     for l in range(p.n_layers):
         for b in range(len(lens)):
             k_ref, v_ref = caches["bf16"][b][l]
+            k_x, v_x = caches["exact"][b][l]
             m = int(kv_len[l, b])
             assert m == k_ref.shape[0]
             got = gc[l, b, :m]
-            assert_rows_close(got[:, :kvd], k_ref, 5e-2, f"layer {l} seq {b} k")
-            assert_rows_close(got[:, kvd:], v_ref, 5e-2, f"layer {l} seq {b} v")
+            assert_rel_l2(got[:, :kvd], k_x, TOL, f"layer {l} seq {b} k")
+            assert_rel_l2(got[:, kvd:], v_x, TOL, f"layer {l} seq {b} v")
+            assert_rows_vs_exact(got[:, :kvd], k_x, k_ref, TOL, f"layer {l} seq {b} k")
+            assert_rows_vs_exact(got[:, kvd:], v_x, v_ref, TOL, f"layer {l} seq {b} v")
     # two generated rows per sequence
     g = np.random.default_rng(17)
     ocache = {mode: [[caches[mode][b][l] for b in range(len(lens))] for l in range(p.n_layers)]
@@ -75,15 +93,16 @@ def test_prefill_cache_and_decode(kind, hkv, prune, keep_last, hd):
         x64 = f64(x_new)
         res = {mode: O.decode_step(x64, np.array(pos_new), ocache[mode], ws64, ocfg, mode=mode)
                for mode in ocache}
-        assert_rel_l2(f64(y), res["exact"]["x"], 2e-2, f"decode step {step}")
-        assert_rows_close(f64(y), res["bf16"]["x"], 5e-2, f"decode step {step}")
+        # one row per sequence: per-sequence relative L2 is per row
+        check_rows(f64(y), res["exact"]["x"], res["bf16"]["x"], f"decode step {step}")
         gc = f64(cache)
         for l in range(p.n_layers):
             for b in range(len(lens)):
                 nk, nv = res["bf16"]["kv"][l][b]
+                xk, xv = res["exact"]["kv"][l][b]
                 row = gc[l, b, before[l, b]]
-                assert_rows_close(row[None, :kvd], nk, 5e-2, f"appended k, layer {l} seq {b}")
-                assert_rows_close(row[None, kvd:], nv, 5e-2, f"appended v, layer {l} seq {b}")
+                check_rows(row[None, :kvd], xk, nk, f"appended k, layer {l} seq {b}")
+                check_rows(row[None, kvd:], xv, nv, f"appended v, layer {l} seq {b}")
         for mode in ocache:
             ocache[mode] = [[(np.concatenate([ocache[mode][l][b][0], res[mode]["kv"][l][b][0]]),
                               np.concatenate([ocache[mode][l][b][1], res[mode]["kv"][l][b][1]]))
@@ -138,15 +157,15 @@ def test_decode_long_cache(kind, H, hkv, hd, kv0):
         x64 = f64(x_new)
         res = {mode: O.decode_step(x64, np.array(pos_new), ocache, ws64, ocfg, mode=mode)
                for mode in ("exact", "bf16")}
-        assert_rel_l2(f64(y), res["exact"]["x"], 2e-2, f"decode step {step}")
-        assert_rows_close(f64(y), res["bf16"]["x"], 5e-2, f"decode step {step}")
+        check_rows(f64(y), res["exact"]["x"], res["bf16"]["x"], f"decode step {step}")
         gc = f64(cache)
         for l in range(2):
             for b in range(B):
                 nk, nv = res["bf16"]["kv"][l][b]
+                xk, xv = res["exact"]["kv"][l][b]
                 row = gc[l, b, before[l, b]]
-                assert_rows_close(row[None, :kvd], nk, 5e-2, f"appended k, layer {l} seq {b}")
-                assert_rows_close(row[None, kvd:], nv, 5e-2, f"appended v, layer {l} seq {b}")
+                check_rows(row[None, :kvd], xk, nk, f"appended k, layer {l} seq {b}")
+                check_rows(row[None, kvd:], xv, nv, f"appended v, layer {l} seq {b}")
                 # rows before the new one are untouched
                 old = np.concatenate([ocache[l][b][0], ocache[l][b][1]], axis=1)
                 assert np.array_equal(gc[l, b, :before[l, b]], old)

@@ -1,12 +1,13 @@
 """Parity at the full workload sizes, in the launch configuration the
-benchmark times: the GPU runs the whole batch, the oracle recomputes
-sampled sequences one by one (sequences are independent under the method),
-continuing on the GPU's kept sets. Standard random-init weights. Hidden
-states are held to the relative-L2 tolerance against the exact float64
-oracle; scores, kept sets and the elementwise check use the oracle that
-rounds to bf16 where the GPU stores bf16, and every row must be within
-the same relative tolerance of it."""
-import numpy as np
+benchmark times, at every keep rate the benchmark sweeps: the GPU runs the
+whole batch, the oracle recomputes sampled sequences one by one (sequences
+are independent under the method), continuing on the GPU's kept sets.
+Standard random-init weights. Every layer's output is held to the
+per-sequence relative-L2 tolerance against the exact float64 oracle and
+every row to twice what bf16 storage alone does to it; scores to twice the
+emulation oracle's own error; kept sets exactly to the top-k of the GPU's
+scores, and to the oracle's choice up to swaps inside the score tolerance,
+whose number is reported and bounded."""
 import pytest
 
 from paper_2509_01190_amd import workloads as W
@@ -14,56 +15,72 @@ from tests.test_gpu_stack import build, compare_stack
 
 pytestmark = [pytest.mark.gpu, pytest.mark.slow]
 
+# Swaps with the oracle's kept set happen only between rows whose scores lie
+# within the score tolerance of the k-th score; on random-init weights the
+# scores crowd around it (about a quarter to two fifths of a sequence's rows
+# lie within 1 % of it at the bert shape), so a few percent of the kept rows
+# may swap. More than this share would mean scores off by more than their
+# error budget somewhere near the threshold.
+MAX_SWAP_SHARE = 0.05
 
-@pytest.mark.parametrize("rate", [0.5, 0.1])
+
+def run(name, seed, rate, seqs, sharp=1.0):
+    p = W.PRESETS[name]
+    lens, stack, xd, posd, dws, ocfg = build(p, seed, norm_jitter=False, sharp=sharp)
+    rates = W.keep_rates(p, seed, rate)
+    st = compare_stack(p, lens, stack, xd, posd, dws, ocfg, rates, seqs_check=seqs,
+                       label=f"{name} seed {seed} keep rate {rate} sharp {sharp}")
+    assert st["swaps"] <= MAX_SWAP_SHARE * max(st["kept"], 1) + 1, st["swaps"]
+    return st
+
+
+@pytest.mark.parametrize("rate", [1.0, 0.7, 0.5, 0.3, 0.1])
 def test_bert_full(rate):
-    p = W.PRESETS["bert"]
-    lens, stack, xd, posd, dws, ocfg = build(p, 0, norm_jitter=False)
-    rates = W.keep_rates(p, 0, rate)
-    compare_stack(p, lens, stack, xd, posd, dws, ocfg, rates, seqs_check=[0, 21])
+    run("bert", 0, rate, [0, 21])
 
 
-def test_dec1b_full():
-    p = W.PRESETS["dec1b"]
-    lens, stack, xd, posd, dws, ocfg = build(p, 0, norm_jitter=False)
-    rates = W.keep_rates(p, 0, 0.25)
-    compare_stack(p, lens, stack, xd, posd, dws, ocfg, rates, seqs_check=[5])
+@pytest.mark.parametrize("seed,seqs", [(1, [7]), (2, [30])])
+def test_bert_full_other_seeds(seed, seqs):
+    run("bert", seed, 0.5, seqs)
 
 
-def test_dec7b_full():
-    p = W.PRESETS["dec7b"]
-    lens, stack, xd, posd, dws, ocfg = build(p, 0, norm_jitter=False)
-    rates = W.keep_rates(p, 0, 0.09)
-    compare_stack(p, lens, stack, xd, posd, dws, ocfg, rates, seqs_check=[2])
+def test_bert_full_sharpened():
+    # query / key weights scaled by 3 (logits by 9): scores spread out, so the
+    # kept set is far from the threshold for most rows
+    run("bert", 0, 0.5, [4], sharp=3.0)
+
+
+@pytest.mark.parametrize("rate", [1.0, 0.5, 0.25, 0.1])
+def test_dec1b_full(rate):
+    run("dec1b", 0, rate, [5])
+
+
+@pytest.mark.parametrize("seed,seqs", [(1, [2]), (2, [6])])
+def test_dec1b_full_other_seeds(seed, seqs):
+    run("dec1b", seed, 0.5, seqs)
+
+
+@pytest.mark.parametrize("rate", [1.0, 0.5, 0.2, 0.09])
+def test_dec7b_full(rate):
+    run("dec7b", 0, rate, [2])
 
 
 def test_ragged_full():
     p = W.PRESETS["ragged"]
-    lens, stack, xd, posd, dws, ocfg = build(p, 0, norm_jitter=False)
-    rates = W.keep_rates(p, 0)           # per-sequence rates in [0.05, 1]
-    order = np.argsort(lens)
-    compare_stack(p, lens, stack, xd, posd, dws, ocfg, rates,
-                  seqs_check=[int(order[0]), int(order[-1])])
+    lens = W.lengths(p, 0)
+    order = sorted(range(len(lens)), key=lambda b: lens[b])
+    run("ragged", 0, None, [order[0], order[-1]])
 
 
 @pytest.mark.parametrize("rate", [0.7, 0.3])
 def test_gpt2_every_layer_full(rate):
-    p = W.PRESETS["gpt2"]
-    lens, stack, xd, posd, dws, ocfg = build(p, 0, norm_jitter=False)
-    rates = W.keep_rates(p, 0, rate)
-    compare_stack(p, lens, stack, xd, posd, dws, ocfg, rates, seqs_check=[3])
+    run("gpt2", 0, rate, [3])
 
 
 @pytest.mark.parametrize("name,rate,seq", [("gpt2_n128", 0.3, 100), ("gpt2_n1024", 0.5, 9)])
 def test_gpt2_every_layer_other_lengths(name, rate, seq):
-    p = W.PRESETS[name]
-    lens, stack, xd, posd, dws, ocfg = build(p, 0, norm_jitter=False)
-    rates = W.keep_rates(p, 0, rate)
-    compare_stack(p, lens, stack, xd, posd, dws, ocfg, rates, seqs_check=[seq])
+    run(name, 0, rate, [seq])
 
 
 def test_llama3_gqa_keep_last_full():
-    p = W.PRESETS["llama3_8b"]
-    lens, stack, xd, posd, dws, ocfg = build(p, 0, norm_jitter=False)
-    rates = W.keep_rates(p, 0, 0.2)
-    compare_stack(p, lens, stack, xd, posd, dws, ocfg, rates, seqs_check=[1])
+    run("llama3_8b", 0, 0.2, [1])

@@ -7,8 +7,8 @@ import torch
 from oracle import zsa_oracle as O
 from paper_2509_01190_amd import workloads as W
 from paper_2509_01190_amd import zsa
-from tests.helpers import (assert_close, assert_rel_l2, check_kept_sets, dev, dev_weights, f64,
-                           modes, to_dev, weights_f64)
+from tests.helpers import (SEQ_TOL, assert_close, assert_rel_l2, check_kept_sets, dev,
+                           dev_weights, f64, modes, score_eps, to_dev, weights_f64)
 
 pytestmark = pytest.mark.gpu
 
@@ -61,8 +61,7 @@ def test_layer_forward(name, kind, dtype, d, H, F, prune):
     w64 = weights_f64(wd)
     cu = seqs.host
     m_l2, m_el = modes(dtype)
-    tol_x = 2e-2 if dtype == "bf16" else 1e-4
-    eps_s = 5e-3 if dtype == "bf16" else 1e-5
+    tol_x = SEQ_TOL[dtype]
 
     def check_x(got, ref_l2, ref_el, cu_rows):
         for b in range(len(lens)):
@@ -78,6 +77,7 @@ def test_layer_forward(name, kind, dtype, d, H, F, prune):
         assert np.array_equal(res["seqs"].host, cu)
         return
     own = O.layer_forward(x64, pos.astype(np.int64), cu, w64, ocfg, keep_rate=rates, mode=m_el)
+    own_x = O.layer_forward(x64, pos.astype(np.int64), cu, w64, ocfg, keep_rate=rates, mode=m_l2)
     kept_gpu = res["kept_rows"].cpu().numpy()
     s_gpu = res["scores"].cpu().numpy()
     assert np.array_equal(res["seqs"].host, own["cu"])
@@ -87,8 +87,9 @@ def test_layer_forward(name, kind, dtype, d, H, F, prune):
         kb = own["k"][b]
         kg = kept_gpu[res["seqs"].host[b]:res["seqs"].host[b + 1]] - lo
         kr = own["kept_rows"][own["cu"][b]:own["cu"][b + 1]] - lo
-        swaps += check_kept_sets(s_gpu[lo:lo + n], own["scores"][lo:lo + n], kb, kg, kr, eps_s,
-                                 f"{name} seq {b}")
+        s_e, s_x = own["scores"][lo:lo + n], own_x["scores"][lo:lo + n]
+        swaps += check_kept_sets(s_gpu[lo:lo + n], s_e, kb, kg, kr, score_eps(s_e, s_x, dtype),
+                                 f"{name} seq {b}", exact_scores=s_x)
         override.append(kg)
     if dtype == "f32":
         assert swaps == 0
