@@ -48,7 +48,10 @@ again later (reactivated).
 ``mode="exact"`` keeps everything in float64. ``mode="bf16"`` rounds to
 bfloat16 (nearest-even) exactly where the GPU path stores bfloat16: norm
 outputs, Q/K/V (after RoPE), attention output, MLP intermediate and the
-residual stream after each add.
+residual stream after each add; and where it feeds bfloat16 to the matrix
+cores without storing it: the attention probabilities (relative to the row
+maximum, before the division by the row sum) in the P V product of a
+prefill layer. A generated row's attention keeps them in float32.
 """
 from __future__ import annotations
 
@@ -175,7 +178,8 @@ def rope(x: np.ndarray, pos: np.ndarray, n_heads: int, theta: float) -> np.ndarr
 # Eq. 1 attention and the soft-score contribution of each position
 # ---------------------------------------------------------------------------
 def attention(q: np.ndarray, k: np.ndarray, v: np.ndarray, pos: np.ndarray, n_heads: int,
-              causal: bool, want_scores: bool = True, n_kv_heads: Optional[int] = None):
+              causal: bool, want_scores: bool = True, n_kv_heads: Optional[int] = None,
+              p_round=None):
     """Eq. 1 for one sequence, per head, plus the column sums of the
     soft-score matrix (Sec. 3.2-3.3).
 
@@ -186,6 +190,11 @@ def attention(q: np.ndarray, k: np.ndarray, v: np.ndarray, pos: np.ndarray, n_he
     Returns (o [n, d], lse [n_heads, n], s [n] or None) where lse is the
     natural-log log-sum-exp of each scaled, masked score row and
     s[j] = sum_h sum_i P_h[i, j].
+
+    ``p_round`` (storage emulation only) rounds the unnormalised
+    probabilities exp(S - row max) where they enter the P V product, which
+    is then divided by the unrounded row sum; the scores and the
+    log-sum-exp use the unrounded probabilities.
     """
     n, d = q.shape
     hd = d // n_heads
@@ -210,7 +219,10 @@ def attention(q: np.ndarray, k: np.ndarray, v: np.ndarray, pos: np.ndarray, n_he
         E = np.exp(S - row_max)
         Z = E.sum(axis=1, keepdims=True)
         P = E / Z                               # the soft-score matrix of head h
-        o[:, cols] = P @ v[:, kv]
+        if p_round is None:
+            o[:, cols] = P @ v[:, kv]
+        else:
+            o[:, cols] = (p_round(E) @ v[:, kv]) / Z
         lse[h] = row_max[:, 0] + np.log(Z[:, 0])
         if want_scores:
             s += P.sum(axis=0)                  # weight each V row receives
@@ -282,7 +294,10 @@ def sequence_layer(x: np.ndarray, pos: np.ndarray, w: Dict[str, Optional[np.ndar
         q = rope(q, pos, cfg.n_heads, cfg.rope_theta)
         k = rope(k, pos, cfg.kv_heads, cfg.rope_theta)
     q, k, v = r(q), r(k), r(v)
-    o, lse, s = attention(q, k, v, pos, cfg.n_heads, cfg.causal, want_scores, cfg.kv_heads)
+    # under bf16 storage the probabilities also enter the P V product as
+    # bf16 (the matrix-core operand); exact mode leaves them alone
+    o, lse, s = attention(q, k, v, pos, cfg.n_heads, cfg.causal, want_scores, cfg.kv_heads,
+                          p_round=None if mode == "exact" else r)
     o = r(o)
     x1 = r(x + _linear(o, w["w_o"], w["b_o"]))
     if cfg.kind == ENCODER:

@@ -21,6 +21,8 @@ at the sizes of the workloads this library is measured on.
 from __future__ import annotations
 
 import dataclasses
+import os
+from concurrent.futures import ThreadPoolExecutor
 from typing import Dict, List, Optional, Sequence
 
 import numpy as np
@@ -219,9 +221,24 @@ def layer_weights(p: Preset, layer: int, seed: int = 0, norm_jitter: bool = Fals
     return w
 
 
+def _workers() -> int:
+    try:
+        n = len(os.sched_getaffinity(0))
+    except AttributeError:  # pragma: no cover
+        n = os.cpu_count() or 1
+    return max(1, min(16, n))
+
+
 def stack_weights(p: Preset, seed: int = 0, norm_jitter: bool = False,
                   zero_wq: bool = False) -> List[Dict[str, Optional[np.ndarray]]]:
-    return [layer_weights(p, l, seed, norm_jitter, zero_wq) for l in range(p.n_layers)]
+    """Every layer's weights. Layers are drawn on a few threads at once (the
+    generator releases the interpreter lock); each tensor has its own stream,
+    so the numbers do not depend on the order or the thread count."""
+    if p.n_layers <= 1:
+        return [layer_weights(p, l, seed, norm_jitter, zero_wq) for l in range(p.n_layers)]
+    with ThreadPoolExecutor(max_workers=min(_workers(), p.n_layers)) as ex:
+        return list(ex.map(lambda l: layer_weights(p, l, seed, norm_jitter, zero_wq),
+                           range(p.n_layers)))
 
 
 def injected_scores(lens: Sequence[int], seed: int = 0) -> np.ndarray:

@@ -114,10 +114,16 @@ def max_rel(a: np.ndarray, ref: np.ndarray) -> float:
     return float(np.max(np.abs(a - ref) / np.maximum(np.abs(ref), 1e-30)))
 
 
+def score_eps_from(emul_err: float, dtype: str) -> float:
+    """Score tolerance from the emulation oracle's largest relative score
+    error: SCORE_FACTOR times it, at least the floor."""
+    return max(SCORE_FLOOR[dtype], SCORE_FACTOR * emul_err)
+
+
 def score_eps(s_emu: np.ndarray, s_exact: np.ndarray, dtype: str) -> float:
     """The score tolerance of one sequence at one pruning point: SCORE_FACTOR
     times the emulation oracle's largest relative error, at least the floor."""
-    return max(SCORE_FLOOR[dtype], SCORE_FACTOR * max_rel(s_emu, s_exact))
+    return score_eps_from(max_rel(s_emu, s_exact), dtype)
 
 
 def modes(dtype: str):

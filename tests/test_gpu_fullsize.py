@@ -16,20 +16,21 @@ from tests.test_gpu_stack import build, compare_stack
 pytestmark = [pytest.mark.gpu, pytest.mark.slow]
 
 # Swaps with the oracle's kept set happen only between rows whose scores lie
-# within the score tolerance of the k-th score; on random-init weights the
-# scores crowd around it (about a quarter to two fifths of a sequence's rows
-# lie within 1 % of it at the bert shape), so a few percent of the kept rows
-# may swap. More than this share would mean scores off by more than their
-# error budget somewhere near the threshold.
-MAX_SWAP_SHARE = 0.05
+# within the score tolerance of the k-th score. On random-init weights the
+# scores crowd around it (a quarter to two fifths of a bert sequence's rows
+# lie within 1 % of it), yet at most one kept row in a few hundred was seen
+# to swap; more than one in a hundred would mean scores off by more than
+# their error budget near the threshold.
+MAX_SWAP_SHARE = 0.01
 
 
-def run(name, seed, rate, seqs, sharp=1.0):
+def run(name, seed, rate, seqs, qk_sharp=1.0):
     p = W.PRESETS[name]
-    lens, stack, xd, posd, dws, ocfg = build(p, seed, norm_jitter=False, sharp=sharp)
+    lens, stack, xd, posd, dws, ocfg = build(p, seed, norm_jitter=False, qk_sharp=qk_sharp)
     rates = W.keep_rates(p, seed, rate)
     st = compare_stack(p, lens, stack, xd, posd, dws, ocfg, rates, seqs_check=seqs,
-                       label=f"{name} seed {seed} keep rate {rate} sharp {sharp}")
+                       label=f"{name} seed {seed} keep rate {rate}"
+                             + (f" query/key scale {qk_sharp}" if qk_sharp != 1.0 else ""))
     assert st["swaps"] <= MAX_SWAP_SHARE * max(st["kept"], 1) + 1, st["swaps"]
     return st
 
@@ -45,9 +46,10 @@ def test_bert_full_other_seeds(seed, seqs):
 
 
 def test_bert_full_sharpened():
-    # query / key weights scaled by 3 (logits by 9): scores spread out, so the
-    # kept set is far from the threshold for most rows
-    run("bert", 0, 0.5, [4], sharp=3.0)
+    # query and key weights scaled by 2 (attention logits by 4, from a std of
+    # about 0.3 to 1.3): scores spread out, so fewer rows sit near the
+    # threshold and the kept set is decided by wider margins
+    run("bert", 0, 0.5, [4], qk_sharp=2.0)
 
 
 @pytest.mark.parametrize("rate", [1.0, 0.5, 0.25, 0.1])

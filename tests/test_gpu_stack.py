@@ -10,17 +10,24 @@ from oracle import zsa_oracle as O
 from paper_2509_01190_amd import workloads as W
 from paper_2509_01190_amd import zsa
 from tests.helpers import (SEQ_TOL, assert_rel_l2, assert_rows_vs_exact, check_kept_sets, dev,
-                           dev_weights, f64, max_rel, modes, rel_l2, score_eps, to_dev,
-                           weights_f64)
+                           dev_weights, f64, max_rel, modes, rel_l2, score_eps, score_eps_from,
+                           to_dev, weights_f64)
 
 pytestmark = pytest.mark.gpu
 
 
-def build(p, seed, lens=None, norm_jitter=True, sharp=1.0):
+def build(p, seed, lens=None, norm_jitter=True, sharp=1.0, qk_sharp=1.0):
+    """Device weights, inputs and configurations of a test stack. ``sharp``
+    scales the whole fused q|k|v projection; ``qk_sharp`` only its query and
+    key rows (attention logits grow by its square, values stay)."""
     lens = W.lengths(p, seed) if lens is None else lens
     ws = W.stack_weights(p, seed, norm_jitter=norm_jitter)
+    qk_rows = p.d_model + p.kv_heads * (p.d_model // p.n_heads)
     for w in ws:
         w["w_qkv"] = (w["w_qkv"] * np.float32(sharp)).astype(np.float32)
+        w["w_qkv"][:qk_rows] *= np.float32(qk_sharp)
+        if w["b_qkv"] is not None:
+            w["b_qkv"][:qk_rows] *= np.float32(qk_sharp)
     dws = [dev_weights(w, p.dtype) for w in ws]
     cfg = zsa.make_cfg(p.kind, p.d_model, p.n_heads, p.d_ff, p.causal,
                        zsa.BF16 if p.dtype == "bf16" else zsa.F32, p.tau, p.norm_eps, p.rope_theta,
@@ -118,7 +125,7 @@ def compare_stack(p, lens, stack, xd, posd, dws, ocfg, rates, seqs_check=None, t
     # the last block's debug rows are the output itself
     assert np.array_equal(h_dbg[l_off[-2]:l_off[-1]], x_fin)
     stats = {"swaps": 0, "kept": 0, "score_err_over_eps": 0.0, "row_ratio": 0.0,
-             "seq_err": 0.0, "points": []}
+             "seq_err": 0.0, "emul_seq_err": 0.0, "points": []}
     check = range(len(lens)) if seqs_check is None else seqs_check
     m_l2, m_el = ("exact", "exact") if exact_only else modes(p.dtype)
     for b in check:
@@ -139,13 +146,18 @@ def compare_stack(p, lens, stack, xd, posd, dws, ocfg, rates, seqs_check=None, t
         ref_e = ref if m_el == m_l2 else O.stack_forward(
             xb, posb, [0, n], ws64, ocfg, p.prune_after, [rates[b]], mode=m_el,
             kept_override=override, record=True)
+        # the sequence's score budget: twice the largest error bf16 storage
+        # causes at any of its pruning points (a point with few rows alone is
+        # a noisy estimate of the error at that depth)
+        emul_worst = max([max_rel(ref_e["points"][pt]["scores"], ref["points"][pt]["scores"])
+                          for pt in range(n_pts)] or [0.0])
+        eps = score_eps_from(emul_worst, dt)
         for pt, layer in enumerate(p.prune_after):
             s_gpu = s_dbg[s_off[pt] + cus[pt][b]:s_off[pt] + cus[pt][b + 1]]
             s_x = ref["points"][pt]["scores"]
             s_e = ref_e["points"][pt]["scores"]
             k = ref["points"][pt]["k"][0]
             kg = override[layer][0]
-            eps = score_eps(s_e, s_x, dt)
             # the oracle's own choice given identical inputs to this point
             kr = O.select_topk(s_e, k, ocfg.force_keep_last)
             sw = check_kept_sets(s_gpu, s_e, k, kg, kr, eps, f"{label} seq {b} point {pt}",
@@ -163,14 +175,16 @@ def compare_stack(p, lens, stack, xd, posd, dws, ocfg, rates, seqs_check=None, t
             rx = ref["layers"][l - 1]["x"]
             re_ = ref_e["layers"][l - 1]["x"]
             what = f"{label} seq {b} layer {l}"
-            assert_rel_l2(got, rx, tol, what)
+            stats["emul_seq_err"] = max(stats["emul_seq_err"], rel_l2(re_, rx))
+            assert_rel_l2(got, rx, tol, what + f" (bf16 storage alone: {rel_l2(re_, rx):.3e})")
             stats["seq_err"] = max(stats["seq_err"], rel_l2(got, rx))
             stats["row_ratio"] = max(stats["row_ratio"],
                                      assert_rows_vs_exact(got, rx, re_, tol, what))
         fo, fe = out["cu_host"][b], out["cu_host"][b + 1]
         assert np.array_equal(pos_fin[fo:fe], ref["pos"])
     print(f"[parity] {label or p.name}: seqs {list(check)}, worst seq rel-L2 {stats['seq_err']:.3e} "
-          f"(tol {tol:.0e}), worst row error / bound {stats['row_ratio']:.3f}, "
+          f"(tol {tol:.0e}; bf16 storage alone {stats['emul_seq_err']:.3e}), "
+          f"worst row error / bound {stats['row_ratio']:.3f}, "
           f"worst score error / eps {stats['score_err_over_eps']:.3f}, "
           f"kept-set swaps {stats['swaps']} of {stats['kept']} kept", flush=True)
     for q in stats["points"]:

@@ -13,13 +13,14 @@ from oracle import zsa_oracle as O
 from tests import test_oracle_pins as P
 
 
-def _attention_no_scale(q, k, v, pos, n_heads, causal, want_scores=True, n_kv_heads=None):
+def _attention_no_scale(q, k, v, pos, n_heads, causal, want_scores=True, n_kv_heads=None,
+                        p_round=None):
     return _orig_attention(q * math.sqrt(q.shape[1] // n_heads), k, v, pos, n_heads, causal,
-                           want_scores, n_kv_heads)
+                           want_scores, n_kv_heads, p_round)
 
 
 def _attention_mask_excludes_diagonal(q, k, v, pos, n_heads, causal, want_scores=True,
-                                      n_kv_heads=None):
+                                      n_kv_heads=None, p_round=None):
     return _attention_shifted(q, k, v, pos, n_heads, want_scores)
 
 
@@ -43,19 +44,22 @@ def _attention_shifted(q, k, v, pos, n_heads, want_scores):
     return o, lse, s
 
 
-def _attention_row_sums(q, k, v, pos, n_heads, causal, want_scores=True, n_kv_heads=None):
-    o, lse, s = _orig_attention(q, k, v, pos, n_heads, causal, want_scores, n_kv_heads)
+def _attention_row_sums(q, k, v, pos, n_heads, causal, want_scores=True, n_kv_heads=None,
+                        p_round=None):
+    o, lse, s = _orig_attention(q, k, v, pos, n_heads, causal, want_scores, n_kv_heads, p_round)
     if s is not None:
         s = np.full_like(s, float(n_heads))   # what summing each row (axis 1) gives
     return o, lse, s
 
 
-def _attention_kv_modulo(q, k, v, pos, n_heads, causal, want_scores=True, n_kv_heads=None):
+def _attention_kv_modulo(q, k, v, pos, n_heads, causal, want_scores=True, n_kv_heads=None,
+                         p_round=None):
     # query head h reads key/value head h % H_kv instead of h // (H / H_kv)
     hkv = n_heads if n_kv_heads is None else n_kv_heads
     hd = q.shape[1] // n_heads
     idx = np.concatenate([np.arange((h % hkv) * hd, (h % hkv + 1) * hd) for h in range(n_heads)])
-    return _orig_attention(q, k[:, idx], v[:, idx], pos, n_heads, causal, want_scores)
+    return _orig_attention(q, k[:, idx], v[:, idx], pos, n_heads, causal, want_scores,
+                           p_round=p_round)
 
 
 def _select_ignores_keep_last(s, k, keep_last=False):

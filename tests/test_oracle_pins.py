@@ -514,6 +514,39 @@ def test_bf16_mode_rounds_storage_points():
     assert np.allclose(ex, res["x"], rtol=0.05, atol=0.05)
 
 
+def test_probability_rounding_of_the_emulation():
+    # the emulation rounds the unnormalised probabilities exp(S - row max)
+    # that enter P V, and divides by the unrounded row sum:
+    # (1) probabilities that are powers of two are exact in bf16, so rounding
+    #     changes nothing: queries against keys whose scaled scores differ
+    #     by multiples of ln 2 gives exp(S - max) in {1, 1/2, 1/4, 1/8};
+    hd = 4
+    q = np.zeros((4, hd))          # four identical queries (self-attention shape)
+    q[:, 0] = 1.0
+    k = np.zeros((4, hd))
+    k[:, 0] = np.array([0.0, -1.0, -2.0, -3.0]) * math.log(2.0) * math.sqrt(hd)
+    v = np.random.default_rng(0).standard_normal((4, hd))
+    pos = np.arange(4)
+    o_exact, lse_e, s_e = O.attention(q, k, v, pos, 1, False)
+    o_round, lse_r, s_r = O.attention(q, k, v, pos, 1, False, p_round=O.bf16_round)
+    assert np.allclose(o_round, o_exact, rtol=1e-14, atol=1e-14)
+    # ... while scores and log-sum-exp never see the rounding
+    assert np.array_equal(lse_e, lse_r) and np.array_equal(s_e, s_r)
+    # (2) with general scores the output moves, by at most the bf16 unit
+    #     roundoff (2^-8) of sum |p| |v| over the unrounded sum
+    g = np.random.default_rng(1)
+    q = g.standard_normal((6, 2 * hd))
+    k = g.standard_normal((6, 2 * hd))
+    v = g.standard_normal((6, 2 * hd))
+    pos = np.arange(6)
+    o_exact, _, _ = O.attention(q, k, v, pos, 2, True)
+    o_round, _, _ = O.attention(q, k, v, pos, 2, True, p_round=O.bf16_round)
+    assert not np.array_equal(o_exact, o_round)
+    assert np.all(np.abs(o_round - o_exact) <= 2.0 ** -8 * np.max(np.abs(v)) + 1e-15)
+    # (3) the first causal row attends only to itself: p = 1 is exact
+    assert np.allclose(o_round[0], o_exact[0], rtol=0, atol=1e-15)
+
+
 def test_stack_force_keep_last_keeps_every_last_row():
     # every-layer schedule down to tau: the last input row of every sequence
     # survives every pruning point, and each point keeps the Eq. 2 count
