@@ -178,6 +178,10 @@ int zsa_norm(void* stream, int32_t dtype, int32_t kind, const void* x, const voi
  * and 16 rows whose waves split K and add their sums in a fixed order (no
  * workspace). With ws NULL the product is never split.
  * ws_bytes below zsa_linear_workspace_size() returns ZSA_EWORKSPACE.
+ * ZSA_EPI_ROPE in bf16: a workspace with m * head_dim * 4 more bytes than
+ * that (past its 256-byte rounded size) lets the call first tabulate each
+ * row's rotary (cos, sin) pairs there, which long products then read
+ * instead of forming the angles themselves (same values).
  */
 int zsa_linear(void* stream, int32_t dtype, const void* x, int32_t m, int32_t k, const void* w,
                int32_t n, const void* bias, int32_t epilogue, const void* residual,
@@ -215,6 +219,7 @@ int zsa_attention_with_scores(void* stream, int32_t dtype, const void* q, const 
                               void* out, int64_t out_stride, float* lse, float* scores, void* ws,
                               size_t ws_bytes);
 size_t zsa_attention_workspace_size(int32_t n_heads, int32_t total_rows, int32_t want_scores);
+
 
 /* Contribution scores alone, from Q, K and the attention's log-sum-exp
  * (Sec. 3.2-3.3): scores[j] = sum_h sum_i exp(q_i . k_j * scale - lse[h, i]),

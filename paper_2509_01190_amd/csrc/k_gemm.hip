@@ -43,6 +43,10 @@ typedef __bf16 bf16x8_t __attribute__((ext_vector_type(8)));
 typedef float f32x16_t __attribute__((ext_vector_type(16)));
 typedef float f32x4_t __attribute__((ext_vector_type(4)));
 
+// the persistent four-wave kernel's rotary epilogue for head_dim 128 (its
+// EPI_ROPE instance serves head_dim 64)
+constexpr int kEpiRope128 = 5;
+
 template <typename T>
 __device__ __forceinline__ void load8(const T* p, float* v);
 template <>
@@ -163,7 +167,13 @@ __device__ void epilogue_tile(const float* tile, int ldt, int m0, int n0, int M,
         const float zp = tile[r * ldt + pcol + e] + pb[e];
         const int i = (c0 + e) - (lower ? 0 : half);
         float sn, cs;
-        rope_angle(p, ep.inv_freq[i], &sn, &cs);
+        if (ep.rope_cs != nullptr) {
+          const float2 t = reinterpret_cast<const float2*>(ep.rope_cs)[static_cast<int64_t>(m) * half + i];
+          cs = t.x;
+          sn = t.y;
+        } else {
+          rope_angle(p, ep.inv_freq[i], &sn, &cs);
+        }
         z[e] = lower ? (z[e] * cs - zp * sn) : (z[e] * cs + zp * sn);
       }
     }
@@ -456,21 +466,33 @@ __device__ __forceinline__ void reg_epilogue(const f32x16_t (&acc)[TM][TN], int 
   const __amdgpu_buffer_rsrc_t rres = __builtin_amdgcn_make_buffer_rsrc(
       const_cast<void*>(EPI == EPI_RESIDUAL ? ep.residual : ep.y), 0, ybytes, 0x00020000);
   const bf16_t* bias = static_cast<const bf16_t*>(ep.bias);
-  // one 32 x 32 block at a time keeps the bias and residual registers few
+  // Loads go ahead of stores -- every bias word first, each block's
+  // residual before the previous block's stores: vector memory operations
+  // are counted in issue order, so a load issued after a store could only
+  // be waited for together with that store. One 32 x 32 block at a time
+  // keeps the residual registers few.
+  uint2 bw[TN][4];
 #pragma unroll
-  for (int j = 0; j < TN; ++j) {
-    uint2 bw[4];
+  for (int j = 0; j < TN; ++j)
 #pragma unroll
     for (int g = 0; g < 4; ++g)
-      bw[g] = bias != nullptr
-                  ? *reinterpret_cast<const uint2*>(bias + nb + j * 32 + g * 8 + half * 4)
-                  : make_uint2(0u, 0u);
+      bw[j][g] = bias != nullptr
+                     ? *reinterpret_cast<const uint2*>(bias + nb + j * 32 + g * 8 + half * 4)
+                     : make_uint2(0u, 0u);
+  uint32_t r[2][2][4];
+  if (EPI == EPI_RESIDUAL) res_load32(rres, static_cast<uint32_t>(mb + l32), nb, half, ep.ldy, r[0]);
+#pragma unroll
+  for (int j = 0; j < TN; ++j) {
 #pragma unroll
     for (int i = 0; i < TM; ++i) {
+      const int st = j * TM + i;
+      if (EPI == EPI_RESIDUAL && st + 1 < TM * TN) {
+        const int j1 = (st + 1) / TM, i1 = (st + 1) % TM;
+        res_load32(rres, static_cast<uint32_t>(mb + i1 * 32 + l32), nb + j1 * 32, half, ep.ldy,
+                   r[(st + 1) & 1]);
+      }
       const uint32_t m = static_cast<uint32_t>(mb + i * 32 + l32);
-      uint32_t r[2][4];
-      if (EPI == EPI_RESIDUAL) res_load32(rres, m, nb + j * 32, half, ep.ldy, r);
-      epi_store32<EPI>(acc[i][j], bw, r, yres, m, nb + j * 32, half, ep.ldy);
+      epi_store32<EPI>(acc[i][j], bw[j], r[st & 1], yres, m, nb + j * 32, half, ep.ldy);
     }
   }
 }
@@ -994,8 +1016,15 @@ __global__ __launch_bounds__(kSkWaves * 64) void gemm_skinny_kernel(
     v = z + to_f32(static_cast<const bf16_t*>(ep.residual)[row * ep.ldy + c]);
   } else if (ep.epi == EPI_ROPE && c < ep.rope_cols) {
     const float zp = tile[m][j ^ 8];
+    const int i = (c % ep.head_dim) % rope_half;
     float sn, cs;
-    rope_angle(ep.pos[row], ep.inv_freq[(c % ep.head_dim) % rope_half], &sn, &cs);
+    if (ep.rope_cs != nullptr) {
+      const float2 t = reinterpret_cast<const float2*>(ep.rope_cs)[row * rope_half + i];
+      cs = t.x;
+      sn = t.y;
+    } else {
+      rope_angle(ep.pos[row], ep.inv_freq[i], &sn, &cs);
+    }
     v = j < 8 ? z * cs - zp * sn : z * cs + zp * sn;
   }
   y[c] = f32_to_bf16(v);
@@ -1497,6 +1526,12 @@ __device__ __forceinline__ void reg_epilogue_lb(const f32x16_t (&acc)[TM][TN], i
   const __amdgpu_buffer_rsrc_t yres = __builtin_amdgcn_make_buffer_rsrc(ep.y, 0, ybytes, 0x00020000);
   const __amdgpu_buffer_rsrc_t rres = __builtin_amdgcn_make_buffer_rsrc(
       const_cast<void*>(EPI == EPI_RESIDUAL ? ep.residual : ep.y), 0, ybytes, 0x00020000);
+  // block (i, j) = step j * TM + i. The next step's residual is loaded
+  // before this step's stores: vector memory operations are counted in issue
+  // order, so a load issued after a store could only be waited for together
+  // with that store.
+  uint32_t r[2][2][4];
+  if (EPI == EPI_RESIDUAL) res_load32(rres, static_cast<uint32_t>(mb + l32), nb, half, ep.ldy, r[0]);
 #pragma unroll
   for (int j = 0; j < TN; ++j) {
     uint2 bw[4];
@@ -1506,10 +1541,101 @@ __device__ __forceinline__ void reg_epilogue_lb(const f32x16_t (&acc)[TM][TN], i
 #pragma unroll
     for (int i = 0; i < TM; ++i) {
       __builtin_amdgcn_sched_barrier(0);
+      const int st = j * TM + i;
+      if (EPI == EPI_RESIDUAL && st + 1 < TM * TN) {
+        const int j1 = (st + 1) / TM, i1 = (st + 1) % TM;
+        res_load32(rres, static_cast<uint32_t>(mb + i1 * 32 + l32), nb + j1 * 32, half, ep.ldy,
+                   r[(st + 1) & 1]);
+      }
+      __builtin_amdgcn_sched_barrier(0);
       const uint32_t m = static_cast<uint32_t>(mb + i * 32 + l32);
-      uint32_t r[2][4];
-      if (EPI == EPI_RESIDUAL) res_load32(rres, m, nb + j * 32, half, ep.ldy, r);
-      epi_store32<EPI>(acc[i][j], bw, r, yres, m, nb + j * 32, half, ep.ldy);
+      epi_store32<EPI>(acc[i][j], bw, r[st & 1], yres, m, nb + j * 32, half, ep.ldy);
+    }
+  }
+}
+
+// Rotary epilogue of gemm_bf16_w4p_kernel: 256-wide tiles and head_dim 64
+// or 128, so a wave's 128 columns hold whole heads and the partner c + hd/2
+// of a channel c sits in the same lane, in another 32 x 32 block (the next
+// one for head_dim 64, two further for 128). z = acc + bias; for each head
+// below rope_cols and each channel pair (i, i + hd/2): lower = z_l cos -
+// z_u sin, upper = z_u cos + z_l sin, the (cos, sin) of the row's position
+// read from the per-row table (the values rope_angle gives); heads at or
+// past rope_cols are stored as they are. Table rows past M read zeros
+// through the buffer range check (and their stores are dropped).
+template <int TM, int TN, int HD>
+__device__ __forceinline__ void rope_epilogue_lb(const f32x16_t (&acc)[TM][TN], int mb, int nb, int M,
+                                                 int l32, int half, const EpiParams& ep,
+                                                 const unsigned char* blds) {
+  static_assert(TN == 4 && (HD == 64 || HD == 128), "128-column wave blocks of whole heads");
+  constexpr int HH = HD / 2;
+  // Channel sets: head_dim 64 has one (channels 0..31, shared by the wave's
+  // two heads), 128 two (0..31 and 32..63 of its one head); a step is one
+  // set on one 32-row block
+  constexpr int NSTEP = (HD / 64) * TM;
+  const int ybytes = M * ep.ldy * 2;
+  const __amdgpu_buffer_rsrc_t yres = __builtin_amdgcn_make_buffer_rsrc(ep.y, 0, ybytes, 0x00020000);
+  const __amdgpu_buffer_rsrc_t tres = __builtin_amdgcn_make_buffer_rsrc(
+      const_cast<float*>(ep.rope_cs), 0, M * HH * 8, 0x00020000);
+  uint32_t unused[2][4];
+  const uint2 zb[4] = {make_uint2(0u, 0u), make_uint2(0u, 0u), make_uint2(0u, 0u), make_uint2(0u, 0u)};
+  // table values of step it into buffer b: (cos, sin) of channels
+  // 32 set + 8 g + 4 half .. + 3 of the lane's row, 32 bytes per g
+  uint32_t tv[2][4][2][4];
+  auto load_step = [&](int it, int b) {
+    const int cset = it / TM, i = it % TM;
+    const uint32_t m = static_cast<uint32_t>(mb + i * 32 + l32);
+#pragma unroll
+    for (int g = 0; g < 4; ++g) {
+      const uint32_t toff =
+          (m * static_cast<uint32_t>(HH) + static_cast<uint32_t>(32 * cset + 8 * g + 4 * half)) * 8u;
+#pragma unroll
+      for (int q = 0; q < 2; ++q) {
+        const auto t = __builtin_amdgcn_raw_buffer_load_b128(tres, toff + 16u * q, 0, 0);
+#pragma unroll
+        for (int w = 0; w < 4; ++w) tv[b][g][q][w] = t[w];
+      }
+    }
+  };
+  // The next step's table loads are issued before this step's stores:
+  // vector memory operations are counted in issue order, so a load issued
+  // after a store could only be waited for together with that store.
+  load_step(0, 0);
+#pragma unroll
+  for (int it = 0; it < NSTEP; ++it) {
+    __builtin_amdgcn_sched_barrier(0);
+    if (it + 1 < NSTEP) load_step(it + 1, (it + 1) & 1);
+    __builtin_amdgcn_sched_barrier(0);
+    const int cset = it / TM, i = it % TM;
+    const uint32_t m = static_cast<uint32_t>(mb + i * 32 + l32);
+#pragma unroll
+    for (int pr = 0; pr < 2; ++pr) {
+      if (HD == 128 && pr != cset) continue;
+      // blocks jl (lower channels) and ju (their partners) of one pair
+      const int jl = HD == 64 ? 2 * pr : pr;
+      const int ju = HD == 64 ? jl + 1 : jl + 2;
+      const bool rot = nb + (HD == 64 ? 64 * pr : 0) < ep.rope_cols;
+      f32x16_t lo, up;
+#pragma unroll
+      for (int g = 0; g < 4; ++g) {
+        const uint2 bl = *reinterpret_cast<const uint2*>(blds + (jl * 32 + g * 8 + half * 4) * 2);
+        const uint2 bu = *reinterpret_cast<const uint2*>(blds + (ju * 32 + g * 8 + half * 4) * 2);
+        const float b[2][4] = {{__uint_as_float(bl.x << 16), __uint_as_float(bl.x & 0xffff0000u),
+                                __uint_as_float(bl.y << 16), __uint_as_float(bl.y & 0xffff0000u)},
+                               {__uint_as_float(bu.x << 16), __uint_as_float(bu.x & 0xffff0000u),
+                                __uint_as_float(bu.y << 16), __uint_as_float(bu.y & 0xffff0000u)}};
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+          const float zl = acc[i][jl][4 * g + e] + b[0][e];
+          const float zu = acc[i][ju][4 * g + e] + b[1][e];
+          const float cs = __uint_as_float(tv[it & 1][g][e >> 1][(e & 1) * 2]);
+          const float sn = __uint_as_float(tv[it & 1][g][e >> 1][(e & 1) * 2 + 1]);
+          lo[4 * g + e] = rot ? zl * cs - zu * sn : zl;
+          up[4 * g + e] = rot ? zu * cs + zl * sn : zu;
+        }
+      }
+      epi_store32<EPI_NONE>(lo, zb, unused, yres, m, nb + jl * 32, half, ep.ldy);
+      epi_store32<EPI_NONE>(up, zb, unused, yres, m, nb + ju * 32, half, ep.ldy);
     }
   }
 }
@@ -1723,8 +1849,13 @@ __global__ __launch_bounds__(256) void gemm_bf16_w4p_kernel(const bf16_t* __rest
     }
     block_a(no{});
     block_b(yes{});
-    reg_epilogue_lb<TM, TN, EPI>(acc, m0 + wm * 128, n0 + wn * (BN / 2), M, l32, half, ep,
-                                 blds + (p & 1) * 1024 + wn * BN);
+    if constexpr (EPI == EPI_ROPE || EPI == kEpiRope128)
+      rope_epilogue_lb<TM, TN, EPI == EPI_ROPE ? 64 : 128>(acc, m0 + wm * 128, n0 + wn * (BN / 2), M,
+                                                           l32, half, ep,
+                                                           blds + (p & 1) * 1024 + wn * BN);
+    else
+      reg_epilogue_lb<TM, TN, EPI>(acc, m0 + wm * 128, n0 + wn * (BN / 2), M, l32, half, ep,
+                                   blds + (p & 1) * 1024 + wn * BN);
     if (p + 1 < count) {
       tile_at(p + 1, &m0, &n0);
       // the next tile's first fragments (its slice 0 was published by the
@@ -1776,6 +1907,16 @@ hipError_t launch_w4(hipStream_t s, const void* x, int M, int K, const void* w, 
 // the persistent four-wave kernel: the four-wave kernel's products with K of
 // at least two slices (bn: the tile width, 256 or 192, which N is a multiple of)
 bool w4p_ok(int M, int N, int K, const EpiParams& ep, int bn = 256) {
+  if (ep.epi == EPI_ROPE) {
+    // the rotary epilogue: 256-wide tiles (whole heads per wave) and a table
+    if (bn != 256 || ep.rope_cs == nullptr || (ep.head_dim != 64 && ep.head_dim != 128) ||
+        ep.rope_cols % ep.head_dim != 0 || N % ep.head_dim != 0 ||
+        static_cast<int64_t>(M) * (ep.head_dim / 2) * 8 >= (int64_t{1} << 31))
+      return false;
+    EpiParams plain = ep;
+    plain.epi = EPI_NONE;
+    return w4p_ok(M, N, K, plain, bn);
+  }
   return persist_ok(M, N, K, ep) && N % bn == 0 && K >= 128 &&
          static_cast<int64_t>(M + 256) * K * 2 < (int64_t{1} << 31) &&
          static_cast<int64_t>(N) * K * 2 < (int64_t{1} << 31);
@@ -1822,6 +1963,13 @@ int w4p_width(int M, int N, int K, const EpiParams& ep) {
 template <int BN>
 hipError_t launch_w4p(hipStream_t s, const void* x, int M, int K, const void* w, int N,
                       const EpiParams& ep) {
+  if (ep.epi == EPI_ROPE) {
+    if constexpr (BN == 256) {
+      if (ep.head_dim == 64) return launch_w4p_1<EPI_ROPE, 256>(s, x, M, K, w, N, ep);
+      if (ep.head_dim == 128) return launch_w4p_1<kEpiRope128, 256>(s, x, M, K, w, N, ep);
+    }
+    return hipErrorInvalidValue;
+  }
   if (ep.epi == EPI_GELU) return launch_w4p_1<EPI_GELU, BN>(s, x, M, K, w, N, ep);
   if (ep.epi == EPI_RESIDUAL) return launch_w4p_1<EPI_RESIDUAL, BN>(s, x, M, K, w, N, ep);
   if (ep.epi == EPI_SWIGLU) return launch_w4p_1<EPI_SWIGLU, BN>(s, x, M, K, w, N, ep);
@@ -1986,6 +2134,28 @@ size_t gemm_workspace_bound(int dtype, int max_rows, int N, int K) {
     b = std::max(b, gemm_workspace_bytes(dtype, m, N, K));
   }
   return b;
+}
+
+namespace {
+__global__ __launch_bounds__(256) void rope_table_kernel(const int32_t* __restrict__ pos, int M,
+                                                         int hh, EpiParams ep,
+                                                         float2* __restrict__ out) {
+  const int64_t idx = static_cast<int64_t>(blockIdx.x) * 256 + threadIdx.x;
+  if (idx >= static_cast<int64_t>(M) * hh) return;
+  const int m = static_cast<int>(idx / hh), i = static_cast<int>(idx % hh);
+  float sn, cs;
+  rope_angle(pos[m], ep.inv_freq[i], &sn, &cs);
+  out[idx] = make_float2(cs, sn);
+}
+}  // namespace
+
+hipError_t launch_rope_table(hipStream_t s, const int32_t* pos, int M, const EpiParams& ep,
+                             float* out) {
+  const int hh = ep.head_dim / 2;
+  const int64_t n = static_cast<int64_t>(M) * hh;
+  if (n == 0) return hipSuccess;
+  return launch(K_GEMM, rope_table_kernel, dim3(static_cast<unsigned>((n + 255) / 256)),
+                dim3(256), 0, s, pos, M, hh, ep, reinterpret_cast<float2*>(out));
 }
 
 // out[M][N] = x W^T in fp32 (no epilogue): the weight gradients of the

@@ -185,6 +185,7 @@ struct LayerBufs {
   float* lse;
   float* partials;
   int32_t* kept;
+  float* rope;  // per-row rotary table of the rows entering a decoder block
   void* splitk;
   size_t splitk_bytes;
 };
@@ -199,7 +200,7 @@ struct Carver {
 };
 
 struct LayerLayout {
-  size_t h, qkv, o, f, xg, og, lse, partials, kept, splitk, splitk_bytes, end;
+  size_t h, qkv, o, f, xg, og, lse, partials, kept, rope, rope_bytes, splitk, splitk_bytes, end;
 };
 
 LayerLayout layer_layout(const zsa_layer_cfg* c, int64_t T, Carver& cv) {
@@ -217,6 +218,8 @@ LayerLayout layer_layout(const zsa_layer_cfg* c, int64_t T, Carver& cv) {
   L.lse = cv.take(static_cast<size_t>(c->n_heads) * T * 4);
   L.partials = cv.take(static_cast<size_t>(G) * T * 4);
   L.kept = cv.take(T * 4);
+  L.rope_bytes = c->kind == ZSA_DECODER ? zsa::rope_table_bytes(static_cast<int>(T), c->head_dim) : 0;
+  L.rope = cv.take(L.rope_bytes);
   // split-K partials of the projections, for any row count up to T
   const int dt = c->dtype;
   const int up_n = c->kind == ZSA_DECODER ? 2 * F : F;
@@ -242,6 +245,7 @@ LayerBufs carve_layer(const LayerLayout& L, void* ws) {
   b.lse = reinterpret_cast<float*>(base + L.lse);
   b.partials = reinterpret_cast<float*>(base + L.partials);
   b.kept = reinterpret_cast<int32_t*>(base + L.kept);
+  b.rope = L.rope_bytes ? reinterpret_cast<float*>(base + L.rope) : nullptr;
   b.splitk = L.splitk_bytes ? base + L.splitk : nullptr;
   b.splitk_bytes = L.splitk_bytes;
   return b;
@@ -263,11 +267,14 @@ void fill_rope(zsa::EpiParams& ep, int hd, float theta) {
     ep.inv_freq[i] = i < hd / 2 ? pow(static_cast<double>(theta), -2.0 * i / hd) : 0.0;
 }
 
+// rope_fresh: the rotary table in the workspace does not yet hold the rows
+// entering this block (their positions changed, or it was never built); a
+// decoder block then rebuilds it before its QKV projection
 int run_layer(hipStream_t s, const zsa_layer_cfg& c, const zsa_layer_weights& w,
               const void* x_in, const int32_t* pos_in, const RowSet& in, bool prune,
               const RowSet& out, void* x_out, int32_t* pos_out, float* scores_out,
               int32_t* kept_out, const LayerBufs& wb, void* kv_layer = nullptr, int kv_cap = 0,
-              int32_t* marks_pos = nullptr) {
+              int32_t* marks_pos = nullptr, bool rope_fresh = true) {
   using namespace zsa;
   const int dt = c.dtype;
   const size_t e = esize(dt);
@@ -291,7 +298,13 @@ int run_layer(hipStream_t s, const zsa_layer_cfg& c, const zsa_layer_weights& w,
     ep.pos = pos_in;
     ep.head_dim = hd;
     ep.rope_cols = dec ? d + kvd : 0;
-    if (dec) fill_rope(ep, hd, c.rope_theta);
+    if (dec) {
+      fill_rope(ep, hd, c.rope_theta);
+      if (wb.rope != nullptr && dt == ZSA_BF16) {
+        if (rope_fresh) HIP_TRY(launch_rope_table(s, pos_in, in.T, ep, wb.rope), "rotary table");
+        ep.rope_cs = wb.rope;
+      }
+    }
     HIP_TRY(launch_gemm(s, dt, wb.h, in.T, d, w.w_qkv, qw, ep, wb.splitk, wb.splitk_bytes),
             "qkv projection");
   }
@@ -797,6 +810,7 @@ int zsa_stack_forward(void* stream, const zsa_layer_cfg* cfg, const zsa_layer_we
   const int32_t* cur_pos = pos_in;
   RowSet cur{batch, cus[0].data(), cu_dev, T0, max_len0};
   int point = 0;
+  bool rope_fresh = true;  // the rows entering the block changed since the last table
   size_t score_off = 0, pos_off = 0, hid_off = 0;
   const size_t row_bytes = static_cast<size_t>(cfg->d_model) * esize(cfg->dtype);
   for (int l = 1; l <= n_layers && T0 > 0; ++l) {
@@ -815,7 +829,8 @@ int zsa_stack_forward(void* stream, const zsa_layer_cfg* cfg, const zsa_layer_we
       float* sdbg = scores_dbg != nullptr ? scores_dbg + score_off : nullptr;
       int32_t* mpos = pos_dbg != nullptr ? pos_dbg + pos_off : nullptr;
       CHECK(run_layer(s, *cfg, w[l - 1], cur_x, cur_pos, cur, true, sel, x_out, nullptr, sdbg,
-                      nullptr, wb, kv_layer, kv_capacity, mpos));
+                      nullptr, wb, kv_layer, kv_capacity, mpos, rope_fresh));
+      rope_fresh = false;  // marking keeps every row
       score_off += cur.T;
       pos_off += sel.T;
       ++point;
@@ -825,7 +840,8 @@ int zsa_stack_forward(void* stream, const zsa_layer_cfg* cfg, const zsa_layer_we
       int32_t* pos_next = last ? pos_out : posbuf[point & 1];
       float* sdbg = scores_dbg != nullptr ? scores_dbg + score_off : nullptr;
       CHECK(run_layer(s, *cfg, w[l - 1], cur_x, cur_pos, cur, true, nxt, x_out, pos_next, sdbg,
-                      nullptr, wb, kv_layer, kv_capacity));
+                      nullptr, wb, kv_layer, kv_capacity, nullptr, rope_fresh));
+      rope_fresh = true;  // the next block's rows are the kept ones
       if (pos_dbg != nullptr)
         HIP_TRY(zsa::launch_copy_i32(s, pos_dbg + pos_off, pos_next, nxt.T), "pos debug copy");
       score_off += cur.T;
@@ -835,7 +851,8 @@ int zsa_stack_forward(void* stream, const zsa_layer_cfg* cfg, const zsa_layer_we
       ++point;
     } else {
       CHECK(run_layer(s, *cfg, w[l - 1], cur_x, cur_pos, cur, false, cur, x_out, nullptr, nullptr,
-                      nullptr, wb, kv_layer, kv_capacity));
+                      nullptr, wb, kv_layer, kv_capacity, nullptr, rope_fresh));
+      rope_fresh = false;
     }
     cur_x = x_out;
     if (hidden_dbg != nullptr) {  // this block's output rows (cur: the rows leaving it)

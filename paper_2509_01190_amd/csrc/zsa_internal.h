@@ -144,8 +144,20 @@ struct EpiParams {
   const int32_t* pos;    // [M] rotary positions
   int head_dim;
   int rope_cols;
+  // per-row rotary table [M][head_dim / 2] of (cos, sin) pairs (fp32), the
+  // values rope_angle gives for that row's position; null: each kernel forms
+  // the angles itself
+  const float* rope_cs;
   double inv_freq[kMaxHalfHead];  // theta^(-2i/hd), computed on the host in double
 };
+
+// bytes of a rotary table for M rows (launch_rope_table)
+inline size_t rope_table_bytes(int M, int head_dim) {
+  return static_cast<size_t>(M) * (head_dim / 2) * 2 * sizeof(float);
+}
+// out[m][i] = (cos, sin) of pos[m] * inv_freq[i] for i < head_dim / 2
+hipError_t launch_rope_table(hipStream_t s, const int32_t* pos, int M, const EpiParams& ep,
+                             float* out);
 
 // ---------------------------------------------------------------------------
 // kernel launchers (one translation unit each)

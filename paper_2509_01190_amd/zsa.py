@@ -237,6 +237,9 @@ def linear(x: torch.Tensor, w: torch.Tensor, bias: Optional[torch.Tensor] = None
     y = torch.empty((m, ncols), dtype=x.dtype, device=x.device) if out is None else out
     if ws is None and split:
         need = linear_workspace_size(_dtype_code(x), m, n, k)
+        if epilogue == EPI_ROPE and _dtype_code(x) == BF16 and m > 0:
+            # room for the per-row rotary table past the split-K partials
+            need = (need + 255) // 256 * 256 + m * head_dim * 4
         if need:
             ws = torch.empty(need, dtype=torch.uint8, device=x.device)
     ws_bytes = 0 if ws is None else ws.numel() * ws.element_size()

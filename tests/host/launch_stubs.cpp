@@ -116,6 +116,9 @@ hipError_t launch_attention_bwd(hipStream_t, const void*, const void*, const voi
                                 int64_t) {
   reached("launch_attention_bwd");
 }
+hipError_t launch_rope_table(hipStream_t, const int32_t*, int, const EpiParams&, float*) {
+  reached("launch_rope_table");
+}
 hipError_t launch_gather(hipStream_t, int, int, int, const int32_t*, int, const void*, void*,
                          const void*, void*, const int32_t*, int32_t*) {
   reached("launch_gather");

@@ -232,10 +232,14 @@ def test_linear_kernel_regimes(m, n, k, split, epi, with_bias):
                                                (4097, 6144, 4096, 128, 5120),   # grouped-query
                                                (3000, 3072, 768, 64, 2048)])    # 128x128
 @pytest.mark.parametrize("with_bias", [True, False])
-def test_linear_rope_regimes(m, n, k, hd, rope_cols, with_bias):
+@pytest.mark.parametrize("table", [False, True])
+def test_linear_rope_regimes(m, n, k, hd, rope_cols, with_bias, table):
     """The rotary epilogue in the kernels the decoders' QKV projections
-    dispatch to (ragged rows, grouped-query widths), against the oracle on
-    sampled rows, and reproducible."""
+    dispatch to (ragged rows, grouped-query widths), with the angles formed
+    per element or read from a per-row table built in the workspace (which
+    lets the persistent four-wave kernel take the product: heads past
+    rope_cols pass unrotated), against the oracle on sampled rows, and
+    reproducible."""
     g = np.random.default_rng(m + n + hd + int(with_bias))
     x = g.standard_normal((m, k)).astype(np.float32)
     w = (g.standard_normal((n, k)) / math.sqrt(k)).astype(np.float32)
@@ -243,7 +247,7 @@ def test_linear_rope_regimes(m, n, k, hd, rope_cols, with_bias):
     bd = to_dev((0.1 * g.standard_normal(n)).astype(np.float32), "bf16") if with_bias else None
     pos = g.integers(0, 8192, m).astype(np.int32)
     posd = torch.from_numpy(pos).to(dev())
-    kw = dict(pos=posd, head_dim=hd, rope_cols=rope_cols, rope_theta=500000.0, split=False)
+    kw = dict(pos=posd, head_dim=hd, rope_cols=rope_cols, rope_theta=500000.0, split=table)
     y1 = zsa.linear(xd, wd, bd, zsa.EPI_ROPE, **kw)
     y2 = zsa.linear(xd, wd, bd, zsa.EPI_ROPE, **kw)
     torch.cuda.synchronize()

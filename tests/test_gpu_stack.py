@@ -10,8 +10,8 @@ from oracle import zsa_oracle as O
 from paper_2509_01190_amd import workloads as W
 from paper_2509_01190_amd import zsa
 from tests.helpers import (SEQ_TOL, assert_rel_l2, assert_rows_vs_exact, check_kept_sets, dev,
-                           dev_weights, f64, max_rel, modes, rel_l2, score_eps, score_eps_from,
-                           to_dev, weights_f64)
+                           dev_weights, f64, modes, rel_l2, score_eps, score_eps_from,
+                           score_err, to_dev, weights_f64)
 
 pytestmark = pytest.mark.gpu
 
@@ -149,7 +149,7 @@ def compare_stack(p, lens, stack, xd, posd, dws, ocfg, rates, seqs_check=None, t
         # the sequence's score budget: twice the largest error bf16 storage
         # causes at any of its pruning points (a point with few rows alone is
         # a noisy estimate of the error at that depth)
-        emul_worst = max([max_rel(ref_e["points"][pt]["scores"], ref["points"][pt]["scores"])
+        emul_worst = max([score_err(ref_e["points"][pt]["scores"], ref["points"][pt]["scores"])
                           for pt in range(n_pts)] or [0.0])
         eps = score_eps_from(emul_worst, dt)
         for pt, layer in enumerate(p.prune_after):
@@ -162,12 +162,12 @@ def compare_stack(p, lens, stack, xd, posd, dws, ocfg, rates, seqs_check=None, t
             kr = O.select_topk(s_e, k, ocfg.force_keep_last)
             sw = check_kept_sets(s_gpu, s_e, k, kg, kr, eps, f"{label} seq {b} point {pt}",
                                  ocfg.force_keep_last, exact_scores=s_x)
-            err = max_rel(s_gpu, s_x)
+            err = score_err(s_gpu, s_x)
             stats["swaps"] += sw
             stats["kept"] += k
             stats["score_err_over_eps"] = max(stats["score_err_over_eps"], err / eps)
             stats["points"].append({"seq": b, "point": pt, "k": int(k), "swaps": sw,
-                                    "score_err": err, "emul_score_err": max_rel(s_e, s_x),
+                                    "score_err": err, "emul_score_err": score_err(s_e, s_x),
                                     "eps": eps})
         for l in range(1, p.n_layers + 1):
             cu_l = layer_cu[l - 1]
