@@ -220,6 +220,25 @@ int zsa_attention_with_scores(void* stream, int32_t dtype, const void* q, const 
                               size_t ws_bytes);
 size_t zsa_attention_workspace_size(int32_t n_heads, int32_t total_rows, int32_t want_scores);
 
+/* For callers that cannot allocate device memory (code under HIP graph
+ * capture, tight serving loops, harnesses that forbid hipMalloc): the same
+ * call and result as zsa_attention_with_scores, with its scratch (the
+ * score partials and, when lse is NULL, the log-sum-exp rows) in a static
+ * device buffer of zsa_static_scratch_bytes() bytes (32 MiB) that the
+ * library holds on every GPU it runs on until the process ends. It
+ * allocates nothing and needs no workspace. A call whose scratch would not
+ * fit (zsa_attention_workspace_size above the buffer; with scores about
+ * n_heads * T <= 4 Mi) returns ZSA_EUNSUPPORTED before any launch. Every
+ * call on one GPU shares that GPU's buffer: calls that may overlap on one
+ * GPU (other streams, other threads) race and must not be issued. Nothing
+ * in the buffer needs to start at zero: a call reads only what it wrote. */
+int zsa_attention_with_scores_static(void* stream, int32_t dtype, const void* q, const void* k,
+                                     const void* v, int64_t row_stride, int32_t n_heads,
+                                     int32_t n_kv_heads, int32_t head_dim, int32_t causal,
+                                     float scale, int32_t batch, const int32_t* cu_host,
+                                     const int32_t* cu_dev, void* out, int64_t out_stride,
+                                     float* lse, float* scores);
+size_t zsa_static_scratch_bytes(void);
 
 /* Contribution scores alone, from Q, K and the attention's log-sum-exp
  * (Sec. 3.2-3.3): scores[j] = sum_h sum_i exp(q_i . k_j * scale - lse[h, i]),

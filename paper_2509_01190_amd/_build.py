@@ -21,6 +21,7 @@ LIB_PATH = os.path.join(HERE, "libzsa.so")
 
 SOURCES = [
     "zsa_api.cpp",
+    "zsa_static.cpp",
     "k_norm.hip",
     "k_gemm.hip",
     "k_attn.hip",

@@ -395,6 +395,16 @@ TimingState g_timing[zsa::K_NCLASS];
 }  // namespace
 
 namespace zsa {
+int set_error(int code, const char* fmt, ...) {
+  char buf[512];
+  va_list ap;
+  va_start(ap, fmt);
+  vsnprintf(buf, sizeof(buf), fmt, ap);
+  va_end(ap);
+  g_err = buf;
+  return code;
+}
+
 bool timing_take(int kclass, hipEvent_t* start, hipEvent_t* stop) {
   if (kclass < 0 || kclass >= K_NCLASS) return false;
   TimingState& t = g_timing[kclass];

@@ -100,6 +100,8 @@ enum KClass { K_GEMM = 0, K_ATTENTION = 1, K_SCORE = 2, K_SELECT = 3, K_GATHER =
 
 // returns true and a (start, stop) pair if the next launch of this class is timed
 bool timing_take(int kclass, hipEvent_t* start, hipEvent_t* stop);
+// records the thread's last error text (zsa_last_error) and returns code
+int set_error(int code, const char* fmt, ...) __attribute__((format(printf, 2, 3)));
 
 template <typename... KArgs, typename... Args>
 inline hipError_t launch(int kclass, void (*kernel)(KArgs...), dim3 grid, dim3 block,

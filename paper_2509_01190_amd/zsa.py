@@ -74,6 +74,10 @@ _SIGS = {
                                                  _i32, _i32, _f32, _i32, _pi32, _vp, _vp, _i64,
                                                  _vp, _vp, _vp, _sz]),
     "zsa_attention_workspace_size": (_sz, [_i32, _i32, _i32]),
+    "zsa_attention_with_scores_static": (ctypes.c_int, [_vp, _i32, _vp, _vp, _vp, _i64, _i32, _i32,
+                                                        _i32, _i32, ctypes.c_float, _i32, _pi32,
+                                                        _vp, _vp, _i64, _vp, _vp]),
+    "zsa_static_scratch_bytes": (_sz, []),
     "zsa_score_positions": (ctypes.c_int, [_vp, _i32, _vp, _vp, _i64, _vp, _i32, _i32, _i32,
                                            _i32, _f32, _i32, _pi32, _vp, _vp, _vp, _sz]),
     "zsa_score_workspace_size": (_sz, [_i32, _i32]),
