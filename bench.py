@@ -381,9 +381,13 @@ def time_projection(torch, zsa, dev, m, n, k, epi, p, split, blas=False):
         res = y.normal_() if epi == 3 else None
         pos = torch.arange(m, dtype=torch.int32, device=dev) % p.seq_len if epi == 4 else None
         hd = p.d_model // p.n_heads
+        # the split-K partials, and for the rotary epilogue room for its table
         need = zsa.linear_workspace_size(zsa.BF16, m, n, k) if split else 0
+        if split and epi == 4:
+            need = (need + 255) // 256 * 256 + m * hd * 4
         ws = torch.empty(max(need, 1), dtype=torch.uint8, device=dev) if need else None
-        fn = lambda: zsa.linear(x, w, bias, epi, res, pos, hd, p.d_model + 2 * p.kv_heads * hd
+        # rotary: the q and k columns of the fused projection
+        fn = lambda: zsa.linear(x, w, bias, epi, res, pos, hd, p.d_model + p.kv_heads * hd
                                 if epi == 4 else 0, p.rope_theta, out=y, split=split, ws=ws)
     for _ in range(5):
         fn()

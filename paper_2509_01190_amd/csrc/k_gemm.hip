@@ -2085,8 +2085,14 @@ bool skinny_ok(int dtype, int M, int N, int K, const EpiParams& ep) {
 // 4.6 / 8.5 / 8.5 against 11.6 / 10.6 / 11.0 / 11.4; 160 rows 14.9 / 6.0 /
 // 18.2 / 14.4 against 10.5 / 12.4 / 10.9 / 12.9; 256 rows, 768 x 768: 8.7
 // against 11.7; 512 rows, 768 x 768: 14.6 against 12.0.
+// Each 16-row block of x re-reads W, so past one block the few-row kernel
+// pays only while the 128 x 128 tiles would be too few to spread W's read
+// over the GPU: measured at 40 rows, K = 2048 (us): N = 16384 (128 tiles)
+// 50.2 few-row against 22.8 tiled; N = 6144 (48 tiles) 19.7 against 25.4;
+// N = 2048 9.1 against 18.6; and N = 2048, K = 8192 28.0 against 70.3.
 bool skinny_pays(int M, int N, int K) {
-  return M <= 64 || (M <= 256 && N <= 1024 && K <= 1024);
+  const long tiles128 = static_cast<long>((M + 127) / 128) * ((N + 127) / 128);
+  return (M <= 64 && (M <= 16 || tiles128 < 128)) || (M <= 256 && N <= 1024 && K <= 1024);
 }
 
 bool skinny_norm_ok(int M, int N, int K) {

@@ -509,13 +509,22 @@ int zsa_linear(void* stream, int32_t dtype, const void* x, int32_t m, int32_t k,
     ep.rope_cols = rope_cols;
     fill_rope(ep, head_dim, rope_theta);
   }
+  size_t need = 0;
   if (ws != nullptr) {
     CHECK(check_ptr16(ws, "ws"));
-    const size_t need = zsa_linear_workspace_size(dtype, m, n, k);
+    need = zsa_linear_workspace_size(dtype, m, n, k);
     if (ws_bytes < need)
       return fail(ZSA_EWORKSPACE, "linear workspace %zu < %zu bytes", ws_bytes, need);
   }
   hipStream_t s = static_cast<hipStream_t>(stream);
+  if (epilogue == ZSA_EPI_ROPE && dtype == ZSA_BF16 && ws != nullptr && m > 0 &&
+      ws_bytes >= round256(need) + zsa::rope_table_bytes(m, head_dim)) {
+    // room past the split-K partials: the rotary angles as a per-row table
+    float* table = reinterpret_cast<float*>(static_cast<char*>(ws) + round256(need));
+    HIP_TRY(zsa::launch_rope_table(s, pos, m, ep, table), "rotary table");
+    ep.rope_cs = table;
+    ws_bytes = need;
+  }
   HIP_TRY(zsa::launch_gemm(s, dtype, x, m, k, w, n, ep, ws, ws_bytes), "linear");
   return ZSA_OK;
 }
