@@ -199,16 +199,20 @@ def counters_by_kernel(csv_path):
     import csv
     import collections
     per = collections.defaultdict(lambda: collections.defaultdict(float))
-    names = {}
+    names, span = {}, {}
     with open(csv_path) as f:
         for r in csv.DictReader(f):
             key = r["Dispatch_Id"]
             per[key][r["Counter_Name"]] += float(r["Counter_Value"])
             names[key] = kernel_short(r["Kernel_Name"])
+            if r.get("Start_Timestamp") and r.get("End_Timestamp"):
+                span[key] = (int(r["End_Timestamp"]) - int(r["Start_Timestamp"])) * 1e-9
     out = collections.defaultdict(lambda: collections.defaultdict(list))
     for key, cs in per.items():
         for c, v in cs.items():
             out[names[key]][c].append(v)
+        if key in span:
+            out[names[key]]["_duration"].append(span[key])
     return out
 
 
@@ -251,16 +255,22 @@ def summarize_counters(args):
     per_fwd = {"gemm": 4 * L * len(rates), "attention": L * len(rates),
                "score": n_pts * len(rates), "select": n_pts * len(rates),
                "gather": n_pts * len(rates), "norm": 2 * L * len(rates)}
-    lines = [f"workload {p.name}, keep rates {rates} (equal numbers of forwards each); "
-             f"HBM bytes = FETCH_SIZE x {f_scale:.3f} + "
-             f"WRITE_SIZE x {w_scale:.3f} (KiB per dispatch, scaled by the counts of a plain "
-             f"{args.copy_bytes >> 20} MiB copy); MFMA FLOPs = SQ_INSTS_VALU_MFMA_MOPS_BF16 x 512; "
-             f"MFMA busy = SQ_VALU_MFMA_BUSY_CYCLES / (GRBM_GUI_ACTIVE x 256 CUs x 4 SIMDs).",
+    lines = [f"workload {p.name}, keep rates {rates} (equal numbers of forwards each).",
+             "",
+             f"* HBM bytes = FETCH_SIZE x {f_scale:.3f} + WRITE_SIZE x {w_scale:.3f} (KiB per "
+             f"dispatch, scaled by what the counters read for a plain {args.copy_bytes >> 20} MiB "
+             f"copy).",
+             "* MFMA FLOPs = SQ_INSTS_VALU_MFMA_MOPS_BF16 x 512 (equal to 2 M N K on every "
+             "GEMM dispatch).",
+             "* GRBM_GUI_ACTIVE reads about 8 times the kernel's duration at the GPU clock: it "
+             "sums the 8 XCDs. The clock column is GRBM_GUI_ACTIVE / 8 / duration (same run); "
+             "MFMA busy = SQ_VALU_MFMA_BUSY_CYCLES / (GRBM_GUI_ACTIVE / 8 x 1024 SIMDs), the "
+             "share of SIMD cycles the matrix cores were busy at that clock.",
              "",
              "| kernel | class | calls | avg us | HBM MB / dispatch | HBM GB/s (of 8000) | "
-             "MFMA TFLOP / dispatch | MFMA TFLOP/s (of 2500) | MFMA busy | LDS bank conflicts "
-             "/ LDS instr |",
-             "|---|---|---:|---:|---:|---:|---:|---:|---:|---:|"]
+             "MFMA TFLOP / dispatch | MFMA TFLOP/s (of 2500) | clock GHz | MFMA busy | "
+             "LDS bank conflicts / LDS instr |",
+             "|---|---|---:|---:|---:|---:|---:|---:|---:|---:|---:|"]
     cls_tot = {}
     for name in sorted(dur, key=lambda n: -dur[n][0] * dur[n][1]):
         calls, t = dur[name]
@@ -270,37 +280,41 @@ def summarize_counters(args):
         hbm = fb + wb
         q = sq.get(name, {})
         mops = np.mean(q["SQ_INSTS_VALU_MFMA_MOPS_BF16"]) * 512 if "SQ_INSTS_VALU_MFMA_MOPS_BF16" in q else 0.0
-        busy = (np.mean(q["SQ_VALU_MFMA_BUSY_CYCLES"]) / (np.mean(q["GRBM_GUI_ACTIVE"]) * 256 * 4)
-                if "SQ_VALU_MFMA_BUSY_CYCLES" in q and np.mean(q.get("GRBM_GUI_ACTIVE", [0])) > 0
-                else float("nan"))
+        grbm = np.mean(q["GRBM_GUI_ACTIVE"]) / 8 if "GRBM_GUI_ACTIVE" in q else float("nan")
+        clock = grbm / np.mean(q["_duration"]) / 1e9 if "_duration" in q else float("nan")
+        busy = (np.mean(q["SQ_VALU_MFMA_BUSY_CYCLES"]) / (grbm * 1024)
+                if "SQ_VALU_MFMA_BUSY_CYCLES" in q and grbm > 0 else float("nan"))
         confl = (np.mean(q["SQ_LDS_BANK_CONFLICT"]) / max(np.mean(q["SQ_INSTS_LDS"]), 1.0)
                  if "SQ_LDS_BANK_CONFLICT" in q and "SQ_INSTS_LDS" in q else float("nan"))
         lines.append(f"| `{name}` | {cls} | {calls} | {t * 1e6:.2f} | {hbm / 1e6:.2f} | "
                      f"{hbm / t / 1e9:.0f} | {mops / 1e12:.4f} | {mops / t / 1e12:.0f} | "
-                     f"{busy * 100:.1f} % | {confl:.3f} |")
+                     f"{clock:.2f} | {busy * 100:.1f} % | {confl:.3f} |")
         c = cls_tot.setdefault(cls, [0.0, 0.0, 0.0, 0])
         c[0] += calls * t
         c[1] += calls * hbm
         c[2] += calls * mops
         c[3] += calls
-    lines += ["", "Per class (summed over its kernels; the algorithmic work is that of one "
-              "forward divided by the class's dispatches per forward):", "",
-              "| class | dispatches | avg us | measured HBM MB / dispatch | algorithmic | "
-              "achieved (algorithmic work / avg time) | of peak |",
+    # forwards per keep rate: attention runs once per layer and forward
+    att_calls = cls_tot.get("attention", [0.0, 0.0, 0.0, 0])[3]
+    fwd_per_rate = att_calls / (p.n_layers * len(rates)) if att_calls else float("nan")
+    lines += ["", f"Per class: the algorithmic work of the sweep's forwards ({fwd_per_rate:.0f} per "
+              f"keep rate, counted from the attention dispatches) over the class's summed kernel "
+              f"time:", "",
+              "| class | dispatches | total ms | measured HBM MB / dispatch | algorithmic per "
+              "forward sweep | achieved | of peak |",
               "|---|---:|---:|---:|---:|---:|---:|"]
     for cls, (tt, hb, mf, n) in sorted(cls_tot.items(), key=lambda kv: -kv[1][0]):
         if cls not in per_fwd or n == 0:
             continue
         unit, amount = work[cls]
-        per = amount / per_fwd[cls]
-        avg = tt / n
+        total = amount * fwd_per_rate
         if unit == "TFLOP/s":
-            alg, ach, peak = f"{per / 1e12:.4f} TFLOP", per / avg / 1e12, PEAK_BF16_TFLOPS
+            alg, ach, peak = f"{amount / 1e12:.3f} TFLOP", total / tt / 1e12, PEAK_BF16_TFLOPS
             ach_s = f"{ach:.0f} TFLOP/s"
         else:
-            alg, ach, peak = f"{per / 1e6:.3f} MB", per / avg / 1e9, PEAK_HBM_GBS
+            alg, ach, peak = f"{amount / 1e6:.1f} MB", total / tt / 1e9, PEAK_HBM_GBS
             ach_s = f"{ach:.0f} GB/s"
-        lines.append(f"| {cls} | {n} | {avg * 1e6:.2f} | {hb / n / 1e6:.3f} | {alg} | {ach_s} | "
+        lines.append(f"| {cls} | {n} | {tt * 1e3:.2f} | {hb / n / 1e6:.3f} | {alg} | {ach_s} | "
                      f"{ach / peak:.3f} |")
     print("\n".join(lines))
 
