@@ -46,9 +46,10 @@ if ROOT not in sys.path:
 METRIC = "tokens/sec of pruned layer-stack forward vs keep_rate (1 GPU) + roofline %"
 PEAK_BF16_TFLOPS = 2500.0
 PEAK_HBM_GBS = 8000.0
-# exp throughput: v_exp_f32 is a quarter-rate VALU op, so a wave64 takes 16
-# cycles: 256 CUs x 4 SIMDs x 4 exp per clock x 2.4 GHz
-PEAK_EXP_PER_S = 256 * 4 * 4 * 2.4e9
+# exp throughput: v_exp_f32 is a half-rate VALU op on gfx950 (measured over
+# the whole chip: 18.6 T exp2 per second against 37.6 T fma, lane operations),
+# so a wave64 takes 8 cycles: 256 CUs x 4 SIMDs x 8 exp per clock x 2.4 GHz
+PEAK_EXP_PER_S = 256 * 4 * 8 * 2.4e9
 HEADLINE_RATE = 0.5
 # sweep key of presets whose keep rates are drawn per sequence
 PER_SEQ = "per_sequence"
