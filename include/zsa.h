@@ -328,6 +328,10 @@ size_t zsa_layer_workspace_size(const zsa_layer_cfg* cfg, int32_t total_rows, in
  *     its count after the last pruning point before l.
  *   ws >= zsa_stack_workspace_size(cfg, T, batch, n_prune)
  * No host synchronisation: every shape follows from cu_host and keep_rate.
+ * A pruning point at which Eq. 2 keeps every row of every sequence (each at
+ * its floor tau, say) keeps them all in order: unless scores_dbg is given,
+ * that block then runs unpruned, without the scores, the selection and the
+ * gather, which would leave its output unchanged.
  */
 int zsa_stack_forward(void* stream, const zsa_layer_cfg* cfg, const zsa_layer_weights* w,
                       int32_t n_layers, const int32_t* prune_after, int32_t n_prune,

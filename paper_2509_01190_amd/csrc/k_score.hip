@@ -5,17 +5,20 @@
 // each query row's final log-sum-exp, which the attention pass has already
 // written, so this is a second sweep over Q K^T that never stores P.
 //
-// bf16, head_dim 64/128 (MFMA): one 256-thread workgroup per (128-key block,
-// head group, sequence). Its K tile sits in registers as the B operand; the
-// 4 waves stride over 32-query tiles and compute S = Q K^T with
-// v_mfma_f32_32x32x16_bf16 in the *non*-transposed layout, where a lane owns
-// one key column and 16 query rows, so the column sum is in-lane adds. The
-// log-sum-exp values of the query rows are staged in LDS (2048 at a time).
-// Lane halves and waves are combined in a fixed order and the workgroup
-// writes one partial vector per head group ([G][T]); the top-k kernel adds
-// the G partials in a fixed order. No atomics: the result is bitwise
-// reproducible. Causal workgroups start at the first query that can see
-// their keys.
+// bf16, head_dim 64/128 (MFMA): one workgroup of 8 waves per (key block of
+// KB = 128 or 256 keys, query head, sequence). Its K tile is staged in
+// LDS; the waves stride over 32-query tiles, keep the tile's Q fragments in
+// registers and compute S = Q K^T with v_mfma_f32_32x32x16_bf16 in the
+// *non*-transposed layout, where a lane owns one key column and 16 query
+// rows, so the column sum is in-lane adds. Every workgroup reads the query
+// rows of its head once, so the bytes moved per score fall as the key block
+// grows; the block is the wider one that still gives the grid two
+// workgroups per CU. Lane halves
+// and waves are combined in a fixed order and the workgroup writes one
+// partial vector per head ([H][T]); the top-k kernel adds the H partials in
+// a fixed order. No atomics: the result is bitwise reproducible. Causal
+// workgroups start at the first query that can see their keys and skip the
+// 32-key columns no query of a tile can see.
 //
 // fp32 / other head dims: one thread per key, vector ALU.
 #include <math.h>
@@ -29,133 +32,143 @@ typedef __bf16 bf16x8_t __attribute__((ext_vector_type(8)));
 typedef float f32x16_t __attribute__((ext_vector_type(16)));
 
 constexpr float kLog2e = 1.4426950408889634f;
-constexpr int kLseChunk = 2048;
-// keys per workgroup: every workgroup reads the query rows of its heads once,
-// so wider key blocks move fewer bytes per score
-constexpr int kScoreKeys = 128;
+constexpr int kScoreWaves = 8;
 
 template <int HD, int KB>
-__global__ __launch_bounds__(256) void score_mfma_kernel(
+__global__ __launch_bounds__(64 * kScoreWaves) __attribute__((amdgpu_waves_per_eu(HD == 64 ? 4 : 2))) void score_mfma_kernel(
     const bf16_t* __restrict__ Q, const bf16_t* __restrict__ K, int64_t rs,
     const float* __restrict__ lse, int H, int kv_group, int causal, float scale_log2,
-    const int32_t* __restrict__ cu, int T, int groups, float* __restrict__ partials) {
-  constexpr int KLD = HD + 8;
+    const int32_t* __restrict__ cu, int T, float* __restrict__ partials) {
+  constexpr int NW = kScoreWaves, NT = 64 * NW;
+  constexpr int KLD = HD + 8;  // K tile row stride (bf16): conflict-free fragment reads
   constexpr int KK = HD / 16;
-  constexpr int KS = KB / 32;  // 32-key column blocks
-  __shared__ __align__(16) bf16_t Ks[KB * KLD];
-  __shared__ __align__(16) float Ls[kLseChunk];
-  __shared__ float red[4][KB];
+  constexpr int KS = KB / 32;  // 32-key columns
+  static_assert(KB * KLD * 2 >= NW * KB * 4, "the reduction fits the K tile");
+  __shared__ __align__(16) unsigned char smem[KB * KLD * 2];
+  bf16_t* Ks = reinterpret_cast<bf16_t*>(smem);
 
-  const int b = blockIdx.z, g = blockIdx.y;
+  const int b = blockIdx.z, h = blockIdx.y;
   const int lo = cu[b];
   const int n = cu[b + 1] - lo;
   const int j0 = blockIdx.x * KB;
   if (j0 >= n) return;
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-  const int half = lane >> 5, l32 = lane & 31;
+  const int hf = lane >> 5, l32 = lane & 31;
+
+  for (int c = tid; c < KB * HD / 8; c += NT) {
+    const int r = c / (HD / 8), ch = (c % (HD / 8)) * 8;
+    // keys past the sequence repeat the last row; their columns are not written
+    *reinterpret_cast<uint4*>(Ks + r * KLD + ch) =
+        *reinterpret_cast<const uint4*>(K + static_cast<int64_t>(lo + min(j0 + r, n - 1)) * rs +
+                                        (h / kv_group) * HD + ch);
+  }
+  __syncthreads();
+
   float colsum[KS];
 #pragma unroll
   for (int ks = 0; ks < KS; ++ks) colsum[ks] = 0.f;
-
-  const int qs = causal ? (j0 & ~31) : 0;
-  for (int h = g; h < H; h += groups) {
-    __syncthreads();  // previous head's readers are done with Ks / Ls
-    for (int c = tid; c < KB * HD / 8; c += 256) {
-      const int r = c / (HD / 8), ch = (c % (HD / 8)) * 8;
-      const int jr = j0 + r;
-      // keys past the sequence repeat the last row; their columns are not written
-      *reinterpret_cast<uint4*>(Ks + r * KLD + ch) =
-          *reinterpret_cast<const uint4*>(K + static_cast<int64_t>(lo + min(jr, n - 1)) * rs +
-                                          (h / kv_group) * HD + ch);
-    }
-    __syncthreads();
-    bf16x8_t kf[KS][KK];
+  // this head's log-sum-exp of the sequence's rows, in exp2 units; rows past
+  // the sequence read as zeros (their scores are masked)
+  const __amdgpu_buffer_rsrc_t lres = __builtin_amdgcn_make_buffer_rsrc(
+      const_cast<float*>(lse + static_cast<int64_t>(h) * T + lo), 0, static_cast<uint32_t>(n) * 4u,
+      0x00020000);
+  const bf16_t* qh = Q + static_cast<int64_t>(lo) * rs + h * HD + hf * 8;
+  // query tiles of 32 rows, strided over the waves; the next tile's Q
+  // fragments are loaded while this tile's products and exps run. Rows past
+  // the sequence are clamped and masked.
+  int i0 = (causal ? (j0 & ~31) : 0) + wave * 32;
+  u32x4 qn[KK];
+  if (i0 < n) {
 #pragma unroll
-    for (int ks = 0; ks < KS; ++ks)
+    for (int kk = 0; kk < KK; ++kk)
+      qn[kk] = *reinterpret_cast<const u32x4*>(qh + static_cast<int64_t>(min(i0 + l32, n - 1)) * rs + kk * 16);
+  }
+  for (; i0 < n; i0 += 32 * NW) {
+    bf16x8_t qa[KK];
+#pragma unroll
+    for (int kk = 0; kk < KK; ++kk) qa[kk] = __builtin_bit_cast(bf16x8_t, qn[kk]);
+    const int inext = i0 + 32 * NW;
+    if (inext < n) {
 #pragma unroll
       for (int kk = 0; kk < KK; ++kk)
-        kf[ks][kk] = __builtin_bit_cast(
-            bf16x8_t, *reinterpret_cast<const uint4*>(Ks + (ks * 32 + l32) * KLD + kk * 16 + half * 8));
-
-    const bf16_t* qh = Q + static_cast<int64_t>(lo) * rs + h * HD + half * 8;
-    for (int c0 = qs; c0 < n; c0 += kLseChunk) {
-      const int cend = min(n, c0 + kLseChunk);
-      __syncthreads();
-      for (int i = c0 + tid; i < cend; i += 256)
-        Ls[i - c0] = lse[static_cast<int64_t>(h) * T + lo + i] * kLog2e;
-      __syncthreads();
-      // query tiles of 32 rows, strided over the 4 waves; the next tile's Q
-      // fragments are loaded while this tile's products and exps run. Rows
-      // past the sequence are clamped and masked.
-      int i0 = c0 + wave * 32;
-      u32x4 qn[KK];
-      if (i0 < cend) {
+        qn[kk] = *reinterpret_cast<const u32x4*>(qh + static_cast<int64_t>(min(inext + l32, n - 1)) * rs + kk * 16);
+    }
+    // this lane's 16 query rows: i0 + 8 (r/4) + 4 hf + r%4
+    float L[16];
 #pragma unroll
-        for (int kk = 0; kk < KK; ++kk)
-          qn[kk] = *reinterpret_cast<const u32x4*>(qh + static_cast<int64_t>(min(i0 + l32, n - 1)) * rs + kk * 16);
+    for (int r = 0; r < 16; ++r)
+      L[r] = __builtin_bit_cast(float, __builtin_amdgcn_raw_buffer_load_b32(
+                                           lres, static_cast<uint32_t>(i0 + 8 * (r >> 2) + 4 * hf + (r & 3)) * 4u, 0, 0)) *
+             kLog2e;
+    // S for the tile and key column ks: acc[r] = query i0 + 8 (r/4) + 4 hf + r%4,
+    // key j0 + 32 ks + l32
+    auto block = [&](int ks) {
+      f32x16_t acc;
+#pragma unroll
+      for (int r = 0; r < 16; ++r) acc[r] = 0.f;
+#pragma unroll
+      for (int kk = 0; kk < KK; ++kk) {
+        const bf16x8_t kf = __builtin_bit_cast(
+            bf16x8_t, *reinterpret_cast<const u32x4*>(Ks + (ks * 32 + l32) * KLD + kk * 16 + hf * 8));
+        acc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(qa[kk], kf, acc, 0, 0, 0);
       }
-      for (; i0 < cend; i0 += 128) {
-        bf16x8_t qa[KK];
+      return acc;
+    };
+    if (i0 + 32 <= n && (!causal || i0 >= j0 + KB)) {
+      // every query of the tile sees every key of the block: no masks, and
+      // column ks + 1's products are issued before column ks's exps
+      f32x16_t a0 = block(0);
 #pragma unroll
-        for (int kk = 0; kk < KK; ++kk) qa[kk] = __builtin_bit_cast(bf16x8_t, qn[kk]);
-        const int inext = i0 + 128;
-        if (inext < cend) {
+      for (int ks = 0; ks < KS; ++ks) {
+        f32x16_t a1;
+        if (ks + 1 < KS) a1 = block(ks + 1);
+        float tsum = 0.f;
 #pragma unroll
-          for (int kk = 0; kk < KK; ++kk)
-            qn[kk] = *reinterpret_cast<const u32x4*>(qh + static_cast<int64_t>(min(inext + l32, n - 1)) * rs + kk * 16);
-        }
-        // this lane's 16 query rows: i0 + 8 (r/4) + 4 half + r%4, four runs of 4
-        float4 lq[4];
+        for (int r = 0; r < 16; ++r) tsum += __builtin_amdgcn_exp2f(fmaf(a0[r], scale_log2, -L[r]));
+        colsum[ks] += tsum;
+        if (ks + 1 < KS) a0 = a1;
+      }
+    } else {
+      // the tile crosses the sequence end or the diagonal
+      const bool tail = i0 + 32 > n;
 #pragma unroll
-        for (int q4 = 0; q4 < 4; ++q4)
-          lq[q4] = *reinterpret_cast<const float4*>(Ls + (i0 - c0) + 8 * q4 + 4 * half);
-        // masks matter only where the tile crosses the sequence end or, under
-        // the causal mask, reaches keys after some of its queries
-        const bool edge = i0 + 32 > cend || (causal && j0 + KB - 1 > i0);
+      for (int ks = 0; ks < KS; ++ks) {
+        // under the causal mask no query of the tile sees this or any later
+        // column once its first key is past the tile's last query
+        if (causal && j0 + 32 * ks > i0 + 31) break;
+        const f32x16_t acc = block(ks);
+        float tsum = 0.f;
+        if (!tail && (!causal || j0 + 32 * ks + 31 <= i0)) {
 #pragma unroll
-        for (int ks = 0; ks < KS; ++ks) {
-          f32x16_t acc;
+          for (int r = 0; r < 16; ++r) tsum += __builtin_amdgcn_exp2f(fmaf(acc[r], scale_log2, -L[r]));
+        } else {
+          const int j = j0 + ks * 32 + l32;
 #pragma unroll
-          for (int r = 0; r < 16; ++r) acc[r] = 0.f;
-#pragma unroll
-          for (int kk = 0; kk < KK; ++kk)
-            acc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(qa[kk], kf[ks][kk], acc, 0, 0, 0);
-          // acc[r]: query i0 + 8 (r/4) + 4 half + r%4, key j0 + 32 ks + l32
-          float tsum = 0.f;
-          if (!edge) {
-#pragma unroll
-            for (int r = 0; r < 16; ++r) {
-              const float4 l4 = lq[r >> 2];
-              const float L = (r & 3) == 0 ? l4.x : (r & 3) == 1 ? l4.y : (r & 3) == 2 ? l4.z : l4.w;
-              tsum += __builtin_amdgcn_exp2f(fmaf(acc[r], scale_log2, -L));
-            }
-          } else {
-            const int j = j0 + ks * 32 + l32;
-#pragma unroll
-            for (int r = 0; r < 16; ++r) {
-              const int i = i0 + 8 * (r >> 2) + 4 * half + (r & 3);
-              const float4 l4 = lq[r >> 2];
-              const float L = (r & 3) == 0 ? l4.x : (r & 3) == 1 ? l4.y : (r & 3) == 2 ? l4.z : l4.w;
-              const bool ok = i < cend && (!causal || j <= i);
-              tsum += ok ? __builtin_amdgcn_exp2f(fmaf(acc[r], scale_log2, -L)) : 0.f;
-            }
+          for (int r = 0; r < 16; ++r) {
+            const int i = i0 + 8 * (r >> 2) + 4 * hf + (r & 3);
+            const bool ok = i < n && (!causal || j <= i);
+            tsum += ok ? __builtin_amdgcn_exp2f(fmaf(acc[r], scale_log2, -L[r])) : 0.f;
           }
-          colsum[ks] += tsum;
         }
+        colsum[ks] += tsum;
       }
     }
   }
 #pragma unroll
   for (int ks = 0; ks < KS; ++ks) colsum[ks] = half_swap_sum(colsum[ks]);
-  if (half == 0) {
+  __syncthreads();  // every wave is done with the K tile
+  float* red = reinterpret_cast<float*>(smem);  // [NW][KB]
+  if (hf == 0) {
 #pragma unroll
-    for (int ks = 0; ks < KS; ++ks) red[wave][32 * ks + l32] = colsum[ks];
+    for (int ks = 0; ks < KS; ++ks) red[wave * KB + 32 * ks + l32] = colsum[ks];
   }
   __syncthreads();
-  if (tid < KB) {
-    const int j = j0 + tid;
-    const float v = ((red[0][tid] + red[1][tid]) + red[2][tid]) + red[3][tid];
-    if (j < n) partials[static_cast<int64_t>(g) * T + lo + j] = v;
+  for (int c = tid; c < KB; c += NT) {
+    const int j = j0 + c;
+    float v = red[c];
+#pragma unroll
+    for (int w = 1; w < NW; ++w) v += red[w * KB + c];
+    if (j < n) partials[static_cast<int64_t>(h) * T + lo + j] = v;
   }
 }
 
@@ -227,14 +240,10 @@ hipError_t valu_dispatch(hipStream_t s, const void* q, const void* k, int64_t rs
 
 }  // namespace
 
-// Head groups: the smallest divisor G of H that gives the grid at least
-// ~1024 workgroups (H when none does); the MFMA path only.
+// Partial vectors per row: one per query head on the MFMA path.
 int score_groups(int dtype, int H, int hd, int T) {
-  if (!(dtype == 1 && (hd == 64 || hd == 128))) return 1;
-  const int kblocks = (T + kScoreKeys - 1) / kScoreKeys;
-  for (int g = 1; g <= H; ++g)
-    if (H % g == 0 && kblocks * g >= 1024) return g;
-  return H;
+  (void)T;
+  return dtype == 1 && (hd == 64 || hd == 128) ? H : 1;
 }
 
 hipError_t launch_score(hipStream_t s, int dtype, const void* q, const void* k,
@@ -243,15 +252,30 @@ hipError_t launch_score(hipStream_t s, int dtype, const void* q, const void* k,
                         float* partials, int groups) {
   if (B == 0 || max_len == 0) return hipSuccess;
   if (dtype == 1 && (hd == 64 || hd == 128)) {
-    const dim3 grid((max_len + kScoreKeys - 1) / kScoreKeys, groups, B), block(256);
+    if (groups != H) return hipErrorInvalidValue;
     const bf16_t* qp = static_cast<const bf16_t*>(q);
     const bf16_t* kp = static_cast<const bf16_t*>(k);
     const float sl = scale * kLog2e;
-    if (hd == 64)
-      return launch(K_SCORE, score_mfma_kernel<64, kScoreKeys>, grid, block, 0, s, qp, kp, row_stride,
-                    lse, H, kv_group, causal, sl, cu_dev, T, groups, partials);
-    return launch(K_SCORE, score_mfma_kernel<128, kScoreKeys>, grid, block, 0, s, qp, kp, row_stride,
-                  lse, H, kv_group, causal, sl, cu_dev, T, groups, partials);
+    // 256-key blocks where the grid still holds two workgroups per CU, else
+    // 128 (measured, us, 8 x 2048 causal rows, 32 heads, hd 64: 128-key
+    // blocks 104.5, 256 94.0, 512 105.9 (its 16 column sums and query
+    // fragments spill at four waves per SIMD); 4 x 4096 rows, hd 128: 395
+    // at 128 keys, 305 at 256)
+    const long slots = 2L * device_cu_count();
+    auto wgs = [&](int kb) { return static_cast<long>((max_len + kb - 1) / kb) * H * B; };
+    const int kb = wgs(256) >= slots ? 256 : 128;
+    const dim3 block(64 * kScoreWaves);
+    const dim3 grid((max_len + kb - 1) / kb, H, B);
+#define ZSA_SCORE(HD_, KB_)                                                                      \
+  return launch(K_SCORE, score_mfma_kernel<HD_, KB_>, grid, block, 0, s, qp, kp, row_stride, lse, H, \
+                kv_group, causal, sl, cu_dev, T, partials)
+    if (hd == 64) {
+      if (kb == 256) ZSA_SCORE(64, 256);
+      ZSA_SCORE(64, 128);
+    }
+    if (kb == 256) ZSA_SCORE(128, 256);
+    ZSA_SCORE(128, 128);
+#undef ZSA_SCORE
   }
   if (dtype == 1)
     return valu_dispatch<bf16_t>(s, q, k, row_stride, lse, H, kv_group, hd, causal, scale, B,

@@ -853,6 +853,18 @@ int zsa_stack_forward(void* stream, const zsa_layer_cfg* cfg, const zsa_layer_we
       score_off += cur.T;
       pos_off += sel.T;
       ++point;
+    } else if (prune && scores_dbg == nullptr && cus[point + 1] == cus[point]) {
+      // Eq. 2 keeps every row of every sequence here (each at its floor
+      // tau): the kept set is all rows in order, so the layer runs unpruned
+      // and the scores, the selection and the gather are skipped
+      CHECK(run_layer(s, *cfg, w[l - 1], cur_x, cur_pos, cur, false, cur, x_out, nullptr, nullptr,
+                      nullptr, wb, kv_layer, kv_capacity, nullptr, rope_fresh));
+      rope_fresh = false;
+      if (pos_dbg != nullptr)
+        HIP_TRY(zsa::launch_copy_i32(s, pos_dbg + pos_off, cur_pos, cur.T), "pos debug copy");
+      score_off += cur.T;
+      pos_off += cur.T;
+      ++point;
     } else if (prune) {
       const RowSet nxt{batch, cus[point + 1].data(), meta + static_cast<size_t>(point) * (batch + 1),
                        cus[point + 1][batch], maxl[point + 1]};

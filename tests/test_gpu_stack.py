@@ -271,6 +271,33 @@ def test_small_every_layer_schedule():
         compare_stack(p, lens, stack, xd, posd, dws, ocfg, rates)
 
 
+@pytest.mark.parametrize("kind", ["gpt2", "dec1b"])
+def test_floor_points_run_unpruned(kind):
+    # Pruning after every layer at low keep rates leaves every sequence at
+    # its floor tau after a few layers; from there Eq. 2 keeps all rows, and
+    # without score debugging the stack runs those blocks unpruned (no
+    # scores, selection or gather). The result must be bitwise that of the
+    # run that scores, selects and gathers at every point (debug outputs on).
+    p = W.shrink(W.PRESETS[kind], n_layers=5, d_model=256, n_heads=4, d_ff=512, batch=4,
+                 prune_after=(1, 2, 3, 4, 5))
+    lens = [300, 64, 129, 17]
+    lens, stack, xd, posd, dws, ocfg = build(p, 6, lens, sharp=3.0)
+    seqs = zsa.Seqs(lens, dev())
+    rates = [0.02, 0.1, 0.05, 0.3]
+    plan = stack.plan(seqs, list(p.prune_after), rates)
+    counts = [lens] + [list(c) for c in plan["counts"]]
+    assert any(counts[i] == counts[i + 1] for i in range(len(p.prune_after))), counts
+    fast = stack.forward(xd, posd, seqs, p.prune_after, rates)
+    full = stack.forward(xd, posd, seqs, p.prune_after, rates, debug=True)
+    torch.cuda.synchronize()
+    assert fast["t_final"] == full["t_final"]
+    t = fast["t_final"]
+    assert torch.equal(fast["x"][:t], full["x"][:t])
+    assert torch.equal(fast["pos"][:t], full["pos"][:t])
+    assert np.array_equal(fast["cu_host"], full["cu_host"])
+    assert np.array_equal(fast["counts"], full["counts"])
+
+
 @pytest.mark.parametrize("hkv", [2, 1])
 def test_small_gqa_stack_keep_last(hkv):
     # grouped-query (and multi-query) decoder, every-layer schedule, the last
