@@ -850,21 +850,28 @@ __device__ __forceinline__ int skinny_col(int t, int j, int rope_half) {
 // fp32; the gain (and shift) go to LDS; each x fragment then becomes
 // bf16((x - mean) * rstd * gain + shift) before its MFMA, the values the
 // separate normalisation would have stored.
-template <int CPL>
+//
+// MB > 1: a workgroup takes MB blocks of 16 rows (the same W fragments feed
+// MB MFMAs), for products of more rows: W is then re-read once per 16 MB
+// rows instead of once per 16, with rounds of fewer K values to keep the
+// fragments in registers.
+template <int CPL, int MB>
 __global__ __launch_bounds__(kSkWaves * 64) void gemm_skinny_kernel(
     const bf16_t* __restrict__ X, const bf16_t* __restrict__ W, int M, int N, int K, int kc,
     EpiParams ep, PreNorm pn) {
+  static_assert(CPL == 0 || MB == 1, "the folded norm takes one row block");
+  constexpr int RM = kSkMaxM * MB;  // rows per workgroup
   extern __shared__ __align__(16) uint4 gain_shift[];  // CPL > 0: gain [K / 8], shift [K / 8]
-  __shared__ float red[kSkWaves][kSkMaxM][kSkCols + 1];
-  __shared__ float tile[kSkMaxM][kSkCols + 1];
+  __shared__ float red[kSkWaves][RM][kSkCols + 1];
+  __shared__ float tile[RM][kSkCols + 1];
   __shared__ float row_stat[2][kSkWaves];  // mean, rstd of each x row
   const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63;
   const int l16 = lane & 15, kg = lane >> 4;
   const int t = blockIdx.x;
-  // blockIdx.y picks a block of 16 rows of x (M is then this block's rows)
-  const int mrow0 = blockIdx.y * kSkMaxM;
+  // blockIdx.y picks a block of RM rows of x (M is then this block's rows)
+  const int mrow0 = blockIdx.y * RM;
   X += static_cast<int64_t>(mrow0) * K;
-  M = min(kSkMaxM, M - mrow0);
+  M = min(RM, M - mrow0);
   const int rope_half = ep.epi == EPI_ROPE ? ep.head_dim / 2 : 0;
   const int k0 = wave * kc, k1 = min(K, k0 + kc);
   const __amdgpu_buffer_rsrc_t xres = __builtin_amdgcn_make_buffer_rsrc(
@@ -874,7 +881,8 @@ __global__ __launch_bounds__(kSkWaves * 64) void gemm_skinny_kernel(
   const uint32_t woff = static_cast<uint32_t>(skinny_col(t, l16, rope_half)) * K * 2u + kg * 16u;
   const uint32_t xoff = static_cast<uint32_t>(l16) * K * 2u + kg * 16u;
   constexpr uint32_t kPast = 0x80000000u;  // beyond both buffers: reads zeros
-  constexpr int NF = kSkStep / 32;         // MFMA steps per round
+  constexpr int NF = (MB == 1 ? kSkStep : MB == 2 ? kSkStep / 2 : kSkStep / 4) / 32;  // MFMA steps per round
+  constexpr int RK = NF * 32;                                                        // K values per round
   const int C8 = K / 8;                    // 16-byte chunks of a row
   // the normalisation's inputs are requested first, so waiting for them
   // leaves the first round of W in flight
@@ -899,7 +907,8 @@ __global__ __launch_bounds__(kSkWaves * 64) void gemm_skinny_kernel(
     }
     __builtin_amdgcn_sched_barrier(0);
   }
-  bf16x8_t a[NF], b[NF];
+  bf16x8_t a[NF], b[NF][MB];
+  const uint32_t xblk = static_cast<uint32_t>(kSkMaxM) * K * 2u;  // bytes of 16 rows of x
   auto issue = [&](int k) {
 #pragma unroll
     for (int j = 0; j < NF; ++j) {
@@ -910,8 +919,11 @@ __global__ __launch_bounds__(kSkWaves * 64) void gemm_skinny_kernel(
 #pragma unroll
     for (int j = 0; j < NF; ++j) {
       const bool in = k + 32 * j < k1;
-      b[j] = __builtin_bit_cast(bf16x8_t, __builtin_amdgcn_raw_buffer_load_b128(
-                                              xres, in ? xoff + (k + 32 * j) * 2u : kPast, 0, 0));
+#pragma unroll
+      for (int mb = 0; mb < MB; ++mb)
+        b[j][mb] = __builtin_bit_cast(
+            bf16x8_t, __builtin_amdgcn_raw_buffer_load_b128(
+                          xres, in ? xoff + mb * xblk + (k + 32 * j) * 2u : kPast, 0, 0));
     }
   };
   if (k0 < k1) issue(k0);
@@ -961,14 +973,16 @@ __global__ __launch_bounds__(kSkWaves * 64) void gemm_skinny_kernel(
       rstd = row_stat[1][l16];
     }
   }
-  f32x4_t acc = {0.f, 0.f, 0.f, 0.f};
-  for (int k = k0; k < k1; k += kSkStep) {
+  f32x4_t acc[MB];
+#pragma unroll
+  for (int mb = 0; mb < MB; ++mb) acc[mb] = f32x4_t{0.f, 0.f, 0.f, 0.f};
+  for (int k = k0; k < k1; k += RK) {
     if (k != k0) issue(k);
     // all of the round's loads in flight before the first MFMA waits on one
     __builtin_amdgcn_sched_barrier(0);
 #pragma unroll
     for (int j = 0; j < NF; ++j) {
-      bf16x8_t bj = b[j];
+      bf16x8_t bj = b[j][0];
       if constexpr (CPL > 0) {
         const int c = min(k + 32 * j + 8 * kg, K - 8) / 8;
         float v[8], g[8], sh[8], o[8];
@@ -979,17 +993,23 @@ __global__ __launch_bounds__(kSkWaves * 64) void gemm_skinny_kernel(
         for (int e = 0; e < 8; ++e) o[e] = (v[e] - mean) * rstd * g[e] + sh[e];
         bj = __builtin_bit_cast(bf16x8_t, pack16(o, bf16_t()));
       }
-      acc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a[j], bj, acc, 0, 0, 0);
+      acc[0] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a[j], bj, acc[0], 0, 0, 0);
+#pragma unroll
+      for (int mb = 1; mb < MB; ++mb)
+        acc[mb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a[j], b[j][mb], acc[mb], 0, 0, 0);
     }
   }
-  if (l16 < M) {
 #pragma unroll
-    for (int r = 0; r < 4; ++r) red[wave][l16][4 * kg + r] = acc[r];
+  for (int mb = 0; mb < MB; ++mb) {
+    if (16 * mb + l16 < M) {
+#pragma unroll
+      for (int r = 0; r < 4; ++r) red[wave][16 * mb + l16][4 * kg + r] = acc[mb][r];
+    }
   }
   __syncthreads();
   const int items = M * kSkCols;
-  if (tid < items) {
-    const int m = tid / kSkCols, j = tid % kSkCols;
+  for (int it = tid; it < items; it += kSkWaves * 64) {
+    const int m = it / kSkCols, j = it % kSkCols;
     float z = 0.f;
 #pragma unroll
     for (int w = 0; w < kSkWaves; ++w) z += red[w][m][j];
@@ -998,36 +1018,37 @@ __global__ __launch_bounds__(kSkWaves * 64) void gemm_skinny_kernel(
     tile[m][j] = z;
   }
   __syncthreads();
-  if (tid >= items) return;
-  const int m = tid / kSkCols, j = tid % kSkCols;
-  const int c = skinny_col(t, j, rope_half);
-  if (c >= N) return;
-  const int64_t row = mrow0 + m;  // row of x and of the output
-  bf16_t* y = static_cast<bf16_t*>(ep.y) + row * ep.ldy;
-  const float z = tile[m][j];
-  float v = z;
-  if (ep.epi == EPI_SWIGLU) {  // gate, up on columns 2f, 2f + 1
-    if (j & 1) return;
-    y[c / 2] = f32_to_bf16(silu(z) * tile[m][j + 1]);
-    return;
-  } else if (ep.epi == EPI_GELU) {
-    v = gelu_erf(z);
-  } else if (ep.epi == EPI_RESIDUAL) {
-    v = z + to_f32(static_cast<const bf16_t*>(ep.residual)[row * ep.ldy + c]);
-  } else if (ep.epi == EPI_ROPE && c < ep.rope_cols) {
-    const float zp = tile[m][j ^ 8];
-    const int i = (c % ep.head_dim) % rope_half;
-    float sn, cs;
-    if (ep.rope_cs != nullptr) {
-      const float2 t = reinterpret_cast<const float2*>(ep.rope_cs)[row * rope_half + i];
-      cs = t.x;
-      sn = t.y;
-    } else {
-      rope_angle(ep.pos[row], ep.inv_freq[i], &sn, &cs);
+  for (int it = tid; it < items; it += kSkWaves * 64) {
+    const int m = it / kSkCols, j = it % kSkCols;
+    const int c = skinny_col(t, j, rope_half);
+    if (c >= N) continue;
+    const int64_t row = mrow0 + m;  // row of x and of the output
+    bf16_t* y = static_cast<bf16_t*>(ep.y) + row * ep.ldy;
+    const float z = tile[m][j];
+    float v = z;
+    if (ep.epi == EPI_SWIGLU) {  // gate, up on columns 2f, 2f + 1
+      if (j & 1) continue;
+      y[c / 2] = f32_to_bf16(silu(z) * tile[m][j + 1]);
+      continue;
+    } else if (ep.epi == EPI_GELU) {
+      v = gelu_erf(z);
+    } else if (ep.epi == EPI_RESIDUAL) {
+      v = z + to_f32(static_cast<const bf16_t*>(ep.residual)[row * ep.ldy + c]);
+    } else if (ep.epi == EPI_ROPE && c < ep.rope_cols) {
+      const float zp = tile[m][j ^ 8];
+      const int i = (c % ep.head_dim) % rope_half;
+      float sn, cs;
+      if (ep.rope_cs != nullptr) {
+        const float2 t = reinterpret_cast<const float2*>(ep.rope_cs)[row * rope_half + i];
+        cs = t.x;
+        sn = t.y;
+      } else {
+        rope_angle(ep.pos[row], ep.inv_freq[i], &sn, &cs);
+      }
+      v = j < 8 ? z * cs - zp * sn : z * cs + zp * sn;
     }
-    v = j < 8 ? z * cs - zp * sn : z * cs + zp * sn;
+    y[c] = f32_to_bf16(v);
   }
-  y[c] = f32_to_bf16(v);
 }
 
 // ---------------------------------------------------------------------------
@@ -2090,9 +2111,15 @@ bool skinny_ok(int dtype, int M, int N, int K, const EpiParams& ep) {
 // over the GPU: measured at 40 rows, K = 2048 (us): N = 16384 (128 tiles)
 // 50.2 few-row against 22.8 tiled; N = 6144 (48 tiles) 19.7 against 25.4;
 // N = 2048 9.1 against 18.6; and N = 2048, K = 8192 28.0 against 70.3.
+// With two 16-row blocks per workgroup it also takes products of up to 256
+// rows whose weights are at most 768 x 3072 (the every-layer GPT-2-shaped
+// stack's short layers: its step at keep rate 0.02 0.962 -> 0.872 ms, at
+// 0.1 0.986 -> 0.899 ms); the decoders' wider weights stay tiled (taking
+// them too made the 16-layer decoder at keep rate 0.25 11.9 -> 13.2 ms).
 bool skinny_pays(int M, int N, int K) {
   const long tiles128 = static_cast<long>((M + 127) / 128) * ((N + 127) / 128);
-  return (M <= 64 && (M <= 16 || tiles128 < 128)) || (M <= 256 && N <= 1024 && K <= 1024);
+  return (M <= 64 && (M <= 16 || tiles128 < 128)) || (M <= 256 && N <= 1024 && K <= 1024) ||
+         (M <= 256 && static_cast<long>(N) * K <= 768L * 3072);
 }
 
 bool skinny_norm_ok(int M, int N, int K) {
@@ -2100,24 +2127,48 @@ bool skinny_norm_ok(int M, int N, int K) {
          (N + kSkCols - 1) / kSkCols <= 2 * device_cus();
 }
 
+// 16-row blocks per workgroup of the few-row kernel: two past 16 rows
+// (measured on the every-layer GPT-2-shaped stack, 160-row layers, us per
+// call: 160 x 768 x 768 with residual 6.5 -> 4.8, 160 x 768 x 3072 13.6 ->
+// 10.6, 160 x 2304 x 768 14.0 -> 9.1, 160 x 3072 x 768 with GELU 18.1 ->
+// 11.8; four and eight blocks were slower: fewer workgroups in flight)
+int skinny_mb(int M, int N, int K) {
+  (void)N;
+  (void)K;
+  return M <= kSkMaxM ? 1 : 2;
+}
+
 hipError_t launch_gemm_skinny(hipStream_t s, const void* x, int M, int K, const void* w, int N,
                               const EpiParams& ep, const PreNorm* pn) {
   if (M == 0 || N == 0) return hipSuccess;
   const int kc = ((K + kSkWaves * 32 - 1) / (kSkWaves * 32)) * 32;
-  const dim3 grid((N + kSkCols - 1) / kSkCols, (M + kSkMaxM - 1) / kSkMaxM), block(kSkWaves * 64);
   const bf16_t* xp = static_cast<const bf16_t*>(x);
   const bf16_t* wp = static_cast<const bf16_t*>(w);
-  if (pn == nullptr || pn->g == nullptr)
-    return launch(K_GEMM, gemm_skinny_kernel<0>, grid, block, 0, s, xp, wp, M, N, K, kc, ep,
+  const dim3 block(kSkWaves * 64);
+  if (pn == nullptr || pn->g == nullptr) {
+    const int mb = skinny_mb(M, N, K);
+    const dim3 grid((N + kSkCols - 1) / kSkCols, (M + kSkMaxM * mb - 1) / (kSkMaxM * mb));
+    if (mb >= 8)
+      return launch(K_GEMM, gemm_skinny_kernel<0, 8>, grid, block, 0, s, xp, wp, M, N, K, kc, ep,
+                    PreNorm{});
+    if (mb >= 4)
+      return launch(K_GEMM, gemm_skinny_kernel<0, 4>, grid, block, 0, s, xp, wp, M, N, K, kc, ep,
+                    PreNorm{});
+    if (mb >= 2)
+      return launch(K_GEMM, gemm_skinny_kernel<0, 2>, grid, block, 0, s, xp, wp, M, N, K, kc, ep,
+                    PreNorm{});
+    return launch(K_GEMM, gemm_skinny_kernel<0, 1>, grid, block, 0, s, xp, wp, M, N, K, kc, ep,
                   PreNorm{});
+  }
+  const dim3 grid((N + kSkCols - 1) / kSkCols, (M + kSkMaxM - 1) / kSkMaxM);
   if (!skinny_norm_ok(M, N, K)) return hipErrorInvalidValue;
   const size_t lds = static_cast<size_t>(K) / 8 * 2 * sizeof(uint4);
   const int cpl = (K / 8 + 63) / 64;
   if (cpl <= 2)
-    return launch(K_GEMM, gemm_skinny_kernel<2>, grid, block, lds, s, xp, wp, M, N, K, kc, ep, *pn);
+    return launch(K_GEMM, gemm_skinny_kernel<2, 1>, grid, block, lds, s, xp, wp, M, N, K, kc, ep, *pn);
   if (cpl <= 4)
-    return launch(K_GEMM, gemm_skinny_kernel<4>, grid, block, lds, s, xp, wp, M, N, K, kc, ep, *pn);
-  return launch(K_GEMM, gemm_skinny_kernel<8>, grid, block, lds, s, xp, wp, M, N, K, kc, ep, *pn);
+    return launch(K_GEMM, gemm_skinny_kernel<4, 1>, grid, block, lds, s, xp, wp, M, N, K, kc, ep, *pn);
+  return launch(K_GEMM, gemm_skinny_kernel<8, 1>, grid, block, lds, s, xp, wp, M, N, K, kc, ep, *pn);
 }
 
 size_t splitk_bytes(int S, int M, int N) {

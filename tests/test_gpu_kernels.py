@@ -185,6 +185,42 @@ def test_linear_split_k(m, n, k, epi):
     assert_close(f64(y0), ref, 1e-2, f"unsplit epilogue {epi}")
 
 
+@pytest.mark.parametrize("m,n,k", [(17, 2304, 768),    # the short-product kernel's first row count
+                                   (64, 256, 4096),    # K split over 8 workgroups
+                                   (160, 768, 3072),   # over 4
+                                   (160, 2304, 768),   # one range per workgroup
+                                   (256, 3072, 768),   # its last row count
+                                   (40, 2048, 8192),   # long K in one range
+                                   (100, 48, 64),      # three column blocks, one round
+                                   (200, 1000, 96)])   # ragged N, K not a whole round
+@pytest.mark.parametrize("epi", [zsa.EPI_NONE, zsa.EPI_GELU, zsa.EPI_SWIGLU, zsa.EPI_RESIDUAL])
+@pytest.mark.parametrize("split", [True, False])
+def test_linear_short_products(m, n, k, epi, split):
+    """Products of 17 to 256 rows (all rows of x in one workgroup, K split
+    over its waves and, with a workspace, over workgroups), every epilogue
+    but the rotary one, against the oracle, and reproducible."""
+    if epi == zsa.EPI_SWIGLU:  # the API takes gate/up products of whole 16-column groups
+        n = (n + 15) // 16 * 16
+    g = np.random.default_rng(m + n + k + epi)
+    x = g.standard_normal((m, k)).astype(np.float32)
+    w = (g.standard_normal((n, k)) / math.sqrt(k)).astype(np.float32)
+    bias = (0.1 * g.standard_normal(n)).astype(np.float32)
+    xd, wd, bd = to_dev(x, "bf16"), to_dev(w, "bf16"), to_dev(bias, "bf16")
+    res = to_dev(g.standard_normal((m, n)).astype(np.float32), "bf16") if epi == zsa.EPI_RESIDUAL else None
+    y1 = zsa.linear(xd, wd, bd, epi, residual=res, split=split)
+    y2 = zsa.linear(xd, wd, bd, epi, residual=res, split=split)
+    torch.cuda.synchronize()
+    assert torch.equal(y1, y2)
+    z = f64(xd) @ f64(wd).T + f64(bd)
+    if epi == zsa.EPI_GELU:
+        z = O.gelu(z)
+    elif epi == zsa.EPI_RESIDUAL:
+        z = z + f64(res)
+    elif epi == zsa.EPI_SWIGLU:
+        z = O.silu(z[:, 0::2]) * z[:, 1::2]
+    assert_close(f64(y1), z, 1e-2, f"short product {m}x{n}x{k} epilogue {epi}")
+
+
 @pytest.mark.parametrize("m,n,k,split", [(16129, 3072, 768, False),   # persistent 256x256: whole rounds
                                          (16129, 3072, 128, False),   # two K slices per tile
                                          (16129, 2304, 192, False),   # three, 256x192
