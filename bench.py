@@ -532,12 +532,16 @@ def class_work(p, lens, plan, rows_in, rows_after):
         attn_flops += sum(4.0 * n * n * hd * H * frac for n in cur)
         norm_bytes += 2.0 * rows_in[l - 1] * d * e + 2.0 * rows_after[l - 1] * d * e
         if point < len(p.prune_after) and p.prune_after[point] == l:
-            score_flops += sum(2.0 * n * n * hd * H * frac for n in cur)
+            # a point that keeps every row runs no score sweep (zsa_stack_forward)
+            if counts[point + 1] != counts[point]:
+                score_flops += sum(2.0 * n * n * hd * H * frac for n in cur)
             point += 1
             cur = counts[point]
     gather_bytes = 0.0
     select_bytes = 0.0
     for pt in range(len(p.prune_after)):
+        if counts[pt + 1] == counts[pt]:  # every row kept: no selection or gather
+            continue
         t_in = plan["rows_in"][pt]
         t_out = plan["rows_in"][pt + 1]
         # two row arrays (residual, attention output) read and written, plus
