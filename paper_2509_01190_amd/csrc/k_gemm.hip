@@ -1709,20 +1709,39 @@ __global__ __launch_bounds__(256) void gemm_bf16_w4p_kernel(const bf16_t* __rest
   const int tiles = nM * nN;
   const int xcd = blockIdx.x % kXcds, slot = blockIdx.x / kXcds;
   const int slots = gridDim.x / kXcds;
+  // XCD k's tiles: when the tile grid splits into 8 equal blocks (ra x rb
+  // of them), the block (k / rb, k % rb) whose A rows and W columns add up
+  // to the fewest panels (each XCD then fetches fewer operand bytes into its
+  // L2 than a band of the whole grid would need); otherwise a contiguous,
+  // balanced range of the grouped order. Inside either, groups of
+  // kXcdGroup M-tiles with every N-tile of the range.
+  int ra = 0, rb = 0, best = 0;
+  for (int a = 1; a <= kXcds; a *= 2) {
+    const int b = kXcds / a;
+    if (nM % a != 0 || nN % b != 0) continue;
+    const int cost = nM / a + nN / b;
+    if (ra == 0 || cost < best) {
+      ra = a;
+      rb = b;
+      best = cost;
+    }
+  }
+  const int rm = ra > 0 ? nM / ra : nM, rn = ra > 0 ? nN / rb : nN;  // the range's grid
+  const int rm0 = ra > 0 ? (xcd / rb) * rm : 0, rn0 = ra > 0 ? (xcd % rb) * rn : 0;
   const int per = tiles / kXcds, extra = tiles % kXcds;
-  const int tbeg = xcd * per + min(xcd, extra);
-  const int tcount = per + (xcd < extra ? 1 : 0);
+  const int tbeg = ra > 0 ? 0 : xcd * per + min(xcd, extra);
+  const int tcount = ra > 0 ? rm * rn : per + (xcd < extra ? 1 : 0);
   if (slot >= tcount) return;
   const int count = (tcount - slot + slots - 1) / slots;  // tiles of this workgroup
   const int KT = K / KB;
   auto tile_at = [&](int p, int* m0, int* n0) {
     const int t = tbeg + slot + p * slots;
-    const int g = t / (kXcdGroup * nN);
+    const int g = t / (kXcdGroup * rn);
     const int gm0 = g * kXcdGroup;
-    const int gsz = min(kXcdGroup, nM - gm0);
-    const int r = t - g * kXcdGroup * nN;
-    *n0 = (r / gsz) * BN;
-    *m0 = (gm0 + r % gsz) * BM;
+    const int gsz = min(kXcdGroup, rm - gm0);
+    const int r = t - g * kXcdGroup * rn;
+    *n0 = (rn0 + r / gsz) * BN;
+    *m0 = (rm0 + gm0 + r % gsz) * BM;
   };
   const __amdgpu_buffer_rsrc_t xres =
       __builtin_amdgcn_make_buffer_rsrc(const_cast<bf16_t*>(X), 0, M * K * 2, 0x00020000);
