@@ -87,11 +87,32 @@ __device__ __forceinline__ float gelu_erf(float z) {
                 t * (0.5f * 1.421413741f + t * (0.5f * -1.453152027f + t * (0.5f * 1.061405429f)))));
   return fmaf(-a * hp, __expf(-0.5f * z * z), fmaxf(z, 0.0f));
 }
-// z sigmoid(z) with the library exp and an IEEE division (the hardware exp
-// and reciprocal, a couple of ulp each, flipped enough bf16 roundings of the
-// SwiGLU output to move a 16-layer decoder's scores measurably further from
-// the oracle's)
-__device__ __forceinline__ float silu(float z) { return z / (1.0f + expf(-z)); }
+// z sigmoid(z) = z / (1 + 2^(-z log2 e)) from the hardware exp2 and
+// reciprocal, made as accurate as the library exp with an IEEE division:
+// the exponent is formed with its rounding error (one fma) and the error of
+// log2 e's fp32 value, which then scale the exp2 result to first order
+// (2^(p + dp) = 2^p (1 + dp ln 2)), and one Newton step refines the
+// reciprocal's quotient. Against float64 over 2^20 inputs in [-100, 100]
+// (measured on gfx950): at most 3.0 ulp (mean 0.37) and 6 bf16 roundings in
+// 10^6 different from the exact value's, as for the library form (2.3 ulp,
+// 0.35, 6); the plain hardware pair reached 60 ulp and 30. About 10 vector
+// instructions instead of about 30 (the SwiGLU epilogue was a fifth of a
+// 2048-deep tile's time). Below z = -88.7 (2^p overflows) the result is -0,
+// as z / (1 + inf) is.
+__device__ __forceinline__ float silu(float z) {
+  constexpr float kL2e = 1.44269502f;         // fp32(log2 e)
+  constexpr float kL2eLo = 1.925963033e-08f;  // log2 e - kL2e
+  constexpr float kLn2f = 0.693147182f;
+  const float p = -z * kL2e;
+  const float dp = fmaf(-z, kL2e, -p) - z * kL2eLo;  // p + dp = -z log2 e
+  float e = __builtin_amdgcn_exp2f(p);
+  e = fmaf(e, dp * kLn2f, e);
+  const float d = 1.0f + e;
+  const float r = __builtin_amdgcn_rcpf(d);
+  float q = z * r;
+  q = fmaf(r, fmaf(-d, q, z), q);
+  return p >= 128.0f ? z * 0.0f : q;
+}
 
 // tile: fp32 [BM][ldt] in LDS holding (x W^T) for rows m0.., columns n0..
 template <typename T, int BM, int BN, int NT>
