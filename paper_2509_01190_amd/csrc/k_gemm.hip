@@ -832,28 +832,26 @@ __global__ __launch_bounds__(256) void splitk_sum_f32_kernel(const float4* __res
 }
 
 // ---------------------------------------------------------------------------
-// Few-row products (generation: one new row per sequence)
+// Few-row products (generation, and the short layers of deep pruning)
 // ---------------------------------------------------------------------------
-// y = epi(x W^T) for M <= 16 rows of x: the whole cost is one read of W
-// (M multiply-adds per weight), so W goes straight from memory into MFMA
-// operands with no LDS staging. v_mfma_f32_16x16x32_bf16 takes A = 16 rows
-// of W (lane l: row l % 16, the 8 K values 8 (l / 16) .. + 7 of a 32-wide
-// step) and B = the x rows (lane l: row l % 16, zero past M); lane l then
-// holds outputs (row l % 16 of x, W rows 4 (l / 16) .. + 3).
+// y = epi(x W^T) for few rows of x: with M <= 16 the whole cost is one read
+// of W (M multiply-adds per weight), and up to a few hundred rows the tiled
+// kernels' 128-row tiles would mostly multiply padding. The kernel has no
+// shared tiles: v_mfma_f32_16x16x32_bf16 takes A = 16 rows of W (lane l:
+// row l % 16, the 8 K values 8 (l / 16) .. + 7 of a 32-wide step) and B =
+// 16 x rows (lane l: row l % 16, zero past M); lane l then holds outputs
+// (row l % 16 of x, W rows 4 (l / 16) .. + 3).
 //
-// A workgroup owns 16 output columns over the whole of K: its 8 waves take
-// consecutive K ranges (256 K values, 8 KB of W per wave, per load round;
-// a round's steps past the range read zeros) and their 16 x 16 partial
-// sums are added in wave order through LDS, so no other workgroup is
-// involved and the result is reproducible. Loads go through buffer
-// resources: W rows past N, x rows past M and offsets set past the end
-// read as zeros.
-// For the rotary epilogue a workgroup's columns are 8 channels of a head
-// and their partners hd / 2 further on, so each rotation pair is local.
-constexpr int kSkCols = 16;   // output columns (W rows) per workgroup
+// A workgroup owns 16 CB output columns and 16 MB rows over the whole of
+// K: its 8 waves take consecutive K ranges and their partial sums are added
+// in wave order through LDS, so no other workgroup is involved and the
+// result is reproducible. Loads go through buffer resources: W rows past N,
+// x rows past M and offsets set past the end read as zeros.
+// For the rotary epilogue each 16 columns are 8 channels of a head and
+// their partners hd / 2 further on, so each rotation pair is local.
+constexpr int kSkCols = 16;   // output columns (W rows) per column block
 constexpr int kSkWaves = 8;   // K ranges per workgroup
-constexpr int kSkStep = 256;  // K values per load round
-constexpr int kSkMaxM = 16;   // rows of x per workgroup
+constexpr int kSkMaxM = 16;   // rows of x per row block
 constexpr int kSkMaxRows = 4096;  // rows of x per launch (a grid of 16-row blocks)
 
 // output column of tile column j in workgroup t (rope_half = hd / 2 for the
@@ -866,29 +864,45 @@ __device__ __forceinline__ int skinny_col(int t, int j, int rope_half) {
 }
 
 // CPL > 0: x is first normalised as the block's pre-norm does (LayerNorm,
-// or RMSNorm with mean 0): wave w takes row w (M <= 8), CPL 16-byte chunks
-// of it per lane, for the exact two-pass mean and centred sum of squares in
-// fp32; the gain (and shift) go to LDS; each x fragment then becomes
-// bf16((x - mean) * rstd * gain + shift) before its MFMA, the values the
-// separate normalisation would have stored.
+// or RMSNorm with mean 0): wave w takes row w (M <= 8), CPL 16-byte
+// chunks of it per lane, for the exact two-pass mean and
+// centred sum of squares in fp32; the gain (and shift) go to LDS; each x
+// fragment then becomes bf16((x - mean) * rstd * gain + shift) before its
+// MFMAs, the values the separate normalisation would have stored.
 //
 // MB > 1: a workgroup takes MB blocks of 16 rows (the same W fragments feed
-// MB MFMAs), for products of more rows: W is then re-read once per 16 MB
-// rows instead of once per 16, with rounds of fewer K values to keep the
-// fragments in registers.
-template <int CPL, int MB>
+// MB MFMAs), so W is re-read once per 16 MB rows instead of once per 16.
+// CB > 1: it takes CB blocks of 16 columns (the same x fragments feed CB
+// MFMAs), so x is re-read once per 16 CB columns. A wave moves its K range
+// in groups of 64 K values (128 bytes of each W and x row); a round holds
+// NG groups. DB: two rounds of registers, the next round's loads in flight
+// while a round is multiplied (for K ranges longer than one round).
+constexpr int sk_groups(int MB, int CB, bool DB) {
+  return (DB ? 4 : 8) / (CB + MB) >= 4 ? 4 : (DB ? 4 : 8) / (CB + MB) >= 2 ? 2 : 1;
+}
+
+template <int CPL, int MB, int CB, bool DB>
 __global__ __launch_bounds__(kSkWaves * 64) void gemm_skinny_kernel(
     const bf16_t* __restrict__ X, const bf16_t* __restrict__ W, int M, int N, int K, int kc,
     EpiParams ep, PreNorm pn) {
-  static_assert(CPL == 0 || MB == 1, "the folded norm takes one row block");
+  static_assert(CPL == 0 || (MB == 1 && CB == 1), "the folded norm takes one block");
   constexpr int RM = kSkMaxM * MB;  // rows per workgroup
+  constexpr int CN = kSkCols * CB;  // columns per workgroup
+  constexpr int NT = kSkWaves * 64;
+  constexpr int GR = CN + RM;                          // W and x rows of a group
+  constexpr int LPG = GR / 8;                          // 1 KiB loads per group
+  constexpr int NG = sk_groups(MB, CB, DB);            // groups per round
+  constexpr int RK = 64 * NG;                          // K values per round
+  constexpr int kTrBytes = kSkWaves * GR * 128;        // one group per wave
+  constexpr int kRedBytes = kSkWaves * RM * (CN + 1) * 4;
   extern __shared__ __align__(16) uint4 gain_shift[];  // CPL > 0: gain [K / 8], shift [K / 8]
-  __shared__ float red[kSkWaves][RM][kSkCols + 1];
-  __shared__ float tile[RM][kSkCols + 1];
-  __shared__ float row_stat[2][kSkWaves];  // mean, rstd of each x row
+  // the waves' transposition buffers, then (after the K loop) the partial sums
+  __shared__ __align__(16) unsigned char lds[kTrBytes > kRedBytes ? kTrBytes : kRedBytes];
+  __shared__ float tile[RM][CN + 1];
+  __shared__ float row_stat[2][RM];  // mean, rstd of each x row
   const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63;
   const int l16 = lane & 15, kg = lane >> 4;
-  const int t = blockIdx.x;
+  const int t = blockIdx.x;  // the workgroup's column blocks are CB t .. CB t + CB - 1
   // blockIdx.y picks a block of RM rows of x (M is then this block's rows)
   const int mrow0 = blockIdx.y * RM;
   X += static_cast<int64_t>(mrow0) * K;
@@ -899,19 +913,53 @@ __global__ __launch_bounds__(kSkWaves * 64) void gemm_skinny_kernel(
       const_cast<bf16_t*>(X), 0, static_cast<uint32_t>(M) * K * 2u, 0x00020000);
   const __amdgpu_buffer_rsrc_t wres = __builtin_amdgcn_make_buffer_rsrc(
       const_cast<bf16_t*>(W), 0, static_cast<uint32_t>(N) * K * 2u, 0x00020000);
-  const uint32_t woff = static_cast<uint32_t>(skinny_col(t, l16, rope_half)) * K * 2u + kg * 16u;
-  const uint32_t xoff = static_cast<uint32_t>(l16) * K * 2u + kg * 16u;
   constexpr uint32_t kPast = 0x80000000u;  // beyond both buffers: reads zeros
-  constexpr int NF = (MB == 1 ? kSkStep : MB == 2 ? kSkStep / 2 : kSkStep / 4) / 32;  // MFMA steps per round
-  constexpr int RK = NF * 32;                                                        // K values per round
   const int C8 = K / 8;                    // 16-byte chunks of a row
-  // the normalisation's inputs are requested first, so waiting for them
-  // leaves the first round of W in flight
+  // Loads cover whole 128-byte lines: load i of a group moves group rows
+  // 8 i .. 8 i + 7 (W rows first, then x rows), lane l the 16-byte chunk
+  // l % 8 of row 8 i + l / 8. The wave then stores them to its LDS buffer
+  // (chunk c of group row r at r * 128 + (c ^ (r % 8)) * 16) and reads back
+  // MFMA fragments: lane l of step s takes chunk 4 s + l / 16 of row l % 16
+  // of a block. (Fragments loaded straight from memory would touch 16 lines
+  // per load, half of each: about a third of the throughput.)
+  const int lc = lane & 7, lr = lane >> 3;
+  uint32_t roff[LPG];  // byte offset of this lane's chunk at K step 0 (kPast: none)
+#pragma unroll
+  for (int i = 0; i < LPG; ++i) {
+    const int r = 8 * i + lr;
+    if (r < CN) {
+      roff[i] = static_cast<uint32_t>(skinny_col(t * CB + r / kSkCols, r % kSkCols, rope_half)) * K * 2u +
+                lc * 16u;
+    } else {
+      roff[i] = static_cast<uint32_t>(r - CN) * K * 2u + lc * 16u;
+    }
+  }
+  unsigned char* const trb = lds + wave * GR * 128;  // this wave's buffer
+  // The epilogue's operands of this thread's output items (item it = tid +
+  // q NT: row it / CN, workgroup column it % CN) are requested before
+  // anything else, so the epilogue waits for no global load after the
+  // reduction.
+  constexpr int IPT = (RM * CN + NT - 1) / NT;  // items per thread
+  float pre_b[IPT], pre_r[IPT];
+#pragma unroll
+  for (int q = 0; q < IPT; ++q) {
+    const int it = tid + q * NT;
+    const int m = it / CN, jj = it % CN;
+    const int c = skinny_col(t * CB + jj / kSkCols, jj % kSkCols, rope_half);
+    const bool live = m < M && c < N;
+    pre_b[q] = live && ep.bias != nullptr ? to_f32(static_cast<const bf16_t*>(ep.bias)[c]) : 0.f;
+    pre_r[q] = live && ep.epi == EPI_RESIDUAL
+                   ? to_f32(static_cast<const bf16_t*>(
+                         ep.residual)[(mrow0 + m) * static_cast<int64_t>(ep.ldy) + c])
+                   : 0.f;
+  }
+  // the normalisation's inputs are requested next, so waiting for them
+  // leaves the first round in flight
   uint4 gs[2], rowc[CPL > 0 ? CPL : 1];  // gain / shift chunks: 2 K / 8 <= 2 x 512
   if constexpr (CPL > 0) {
 #pragma unroll
     for (int q = 0; q < 2; ++q) {
-      const int c = tid + q * kSkWaves * 64;
+      const int c = tid + q * NT;
       gs[q] = make_uint4(0u, 0u, 0u, 0u);
       if (c < 2 * C8) {
         const bf16_t* src = c < C8 ? pn.g + 8 * c : (pn.b != nullptr ? pn.b + 8 * (c - C8) : nullptr);
@@ -928,32 +976,34 @@ __global__ __launch_bounds__(kSkWaves * 64) void gemm_skinny_kernel(
     }
     __builtin_amdgcn_sched_barrier(0);
   }
-  bf16x8_t a[NF], b[NF][MB];
-  const uint32_t xblk = static_cast<uint32_t>(kSkMaxM) * K * 2u;  // bytes of 16 rows of x
-  auto issue = [&](int k) {
+  uint4 v[DB ? 2 : 1][NG][LPG];
+  // the loads of the round at k into buffer BUF (chunks past the wave's K
+  // range read zeros)
+  auto issue = [&](auto BUF, int k) {
+    constexpr int u = decltype(BUF)::value;
 #pragma unroll
-    for (int j = 0; j < NF; ++j) {
-      const bool in = k + 32 * j < k1;
-      a[j] = __builtin_bit_cast(bf16x8_t, __builtin_amdgcn_raw_buffer_load_b128(
-                                              wres, in ? woff + (k + 32 * j) * 2u : kPast, 0, 0));
-    }
+    for (int g = 0; g < NG; ++g) {
+      const int kk = k + 64 * g;
+      const bool in = kk + 8 * lc < k1;
 #pragma unroll
-    for (int j = 0; j < NF; ++j) {
-      const bool in = k + 32 * j < k1;
-#pragma unroll
-      for (int mb = 0; mb < MB; ++mb)
-        b[j][mb] = __builtin_bit_cast(
-            bf16x8_t, __builtin_amdgcn_raw_buffer_load_b128(
-                          xres, in ? xoff + mb * xblk + (k + 32 * j) * 2u : kPast, 0, 0));
+      for (int i = 0; i < LPG; ++i)
+        v[u][g][i] = __builtin_bit_cast(
+            uint4, __builtin_amdgcn_raw_buffer_load_b128(8 * i < CN ? wres : xres,
+                                                         in ? roff[i] + kk * 2u : kPast, 0, 0));
     }
   };
-  if (k0 < k1) issue(k0);
+  using I0 = std::integral_constant<int, 0>;
+  using I1 = std::integral_constant<int, 1>;
+  const int rounds = k0 < k1 ? (k1 - k0 + RK - 1) / RK : 0;
+  if (rounds > 0) issue(I0{}, k0);
   __builtin_amdgcn_sched_barrier(0);
-  float mean = 0.f, rstd = 0.f;
+  float mean[MB], rstd[MB];
+#pragma unroll
+  for (int mb = 0; mb < MB; ++mb) mean[mb] = rstd[mb] = 0.f;
   if constexpr (CPL > 0) {
 #pragma unroll
     for (int q = 0; q < 2; ++q) {
-      const int c = tid + q * kSkWaves * 64;
+      const int c = tid + q * NT;
       if (c < 2 * C8) gain_shift[c] = gs[q];
     }
     const float inv_d = 1.0f / static_cast<float>(K);
@@ -961,10 +1011,10 @@ __global__ __launch_bounds__(kSkWaves * 64) void gemm_skinny_kernel(
     if (!pn.rms) {
 #pragma unroll
       for (int i = 0; i < CPL; ++i) {
-        float v[8];
-        unpack16(rowc[i], v, bf16_t());
+        float f[8];
+        unpack16(rowc[i], f, bf16_t());
 #pragma unroll
-        for (int e = 0; e < 8; ++e) sum += v[e];
+        for (int e = 0; e < 8; ++e) sum += f[e];
       }
 #pragma unroll
       for (int off = 32; off > 0; off >>= 1) sum += __shfl_xor(sum, off, 64);
@@ -973,11 +1023,11 @@ __global__ __launch_bounds__(kSkWaves * 64) void gemm_skinny_kernel(
 #pragma unroll
     for (int i = 0; i < CPL; ++i) {
       if (lane + 64 * i < C8) {
-        float v[8];
-        unpack16(rowc[i], v, bf16_t());
+        float f[8];
+        unpack16(rowc[i], f, bf16_t());
 #pragma unroll
         for (int e = 0; e < 8; ++e) {
-          const float d = v[e] - mu;
+          const float d = f[e] - mu;
           sq += d * d;
         }
       }
@@ -990,79 +1040,145 @@ __global__ __launch_bounds__(kSkWaves * 64) void gemm_skinny_kernel(
     }
     barrier_lds();
     if (l16 < M) {
-      mean = row_stat[0][l16];
-      rstd = row_stat[1][l16];
+      mean[0] = row_stat[0][l16];
+      rstd[0] = row_stat[1][l16];
     }
   }
-  f32x4_t acc[MB];
+  f32x4_t acc[CB][MB];
 #pragma unroll
-  for (int mb = 0; mb < MB; ++mb) acc[mb] = f32x4_t{0.f, 0.f, 0.f, 0.f};
-  for (int k = k0; k < k1; k += RK) {
-    if (k != k0) issue(k);
-    // all of the round's loads in flight before the first MFMA waits on one
-    __builtin_amdgcn_sched_barrier(0);
+  for (int cb = 0; cb < CB; ++cb)
 #pragma unroll
-    for (int j = 0; j < NF; ++j) {
-      bf16x8_t bj = b[j][0];
-      if constexpr (CPL > 0) {
-        const int c = min(k + 32 * j + 8 * kg, K - 8) / 8;
-        float v[8], g[8], sh[8], o[8];
-        unpack16(__builtin_bit_cast(uint4, b[j]), v, bf16_t());
-        unpack16(gain_shift[c], g, bf16_t());
-        unpack16(gain_shift[C8 + c], sh, bf16_t());
+    for (int mb = 0; mb < MB; ++mb) acc[cb][mb] = f32x4_t{0.f, 0.f, 0.f, 0.f};
+  // the MFMAs of the round at k, from buffer BUF: each group goes through
+  // the wave's LDS buffer (LDS operations of a wave run in order, so a
+  // group's stores follow the previous group's fragment reads)
+  auto compute = [&](auto BUF, int k) {
+    constexpr int u = decltype(BUF)::value;
 #pragma unroll
-        for (int e = 0; e < 8; ++e) o[e] = (v[e] - mean) * rstd * g[e] + sh[e];
-        bj = __builtin_bit_cast(bf16x8_t, pack16(o, bf16_t()));
+    for (int g = 0; g < NG; ++g) {
+#pragma unroll
+      for (int i = 0; i < LPG; ++i) {
+        const int r = 8 * i + lr;
+        *reinterpret_cast<uint4*>(trb + r * 128 + ((lc ^ (r & 7)) << 4)) = v[u][g][i];
       }
-      acc[0] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a[j], bj, acc[0], 0, 0, 0);
 #pragma unroll
-      for (int mb = 1; mb < MB; ++mb)
-        acc[mb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a[j], b[j][mb], acc[mb], 0, 0, 0);
+      for (int s = 0; s < 2; ++s) {
+        const int ch = 4 * s + kg;
+        bf16x8_t af[CB], bj[MB];
+#pragma unroll
+        for (int cb = 0; cb < CB; ++cb) {
+          const int r = 16 * cb + l16;
+          af[cb] = __builtin_bit_cast(bf16x8_t, *reinterpret_cast<const uint4*>(trb + r * 128 + ((ch ^ (r & 7)) << 4)));
+        }
+#pragma unroll
+        for (int mb = 0; mb < MB; ++mb) {
+          const int r = CN + 16 * mb + l16;
+          bj[mb] = __builtin_bit_cast(bf16x8_t, *reinterpret_cast<const uint4*>(trb + r * 128 + ((ch ^ (r & 7)) << 4)));
+        }
+        if constexpr (CPL > 0) {
+          const int c = min(k + 64 * g + 8 * ch, K - 8) / 8;
+          float gg[8], sh[8];
+          unpack16(gain_shift[c], gg, bf16_t());
+          unpack16(gain_shift[C8 + c], sh, bf16_t());
+#pragma unroll
+          for (int mb = 0; mb < MB; ++mb) {
+            float f[8], o[8];
+            unpack16(__builtin_bit_cast(uint4, bj[mb]), f, bf16_t());
+#pragma unroll
+            for (int e = 0; e < 8; ++e) o[e] = (f[e] - mean[mb]) * rstd[mb] * gg[e] + sh[e];
+            bj[mb] = __builtin_bit_cast(bf16x8_t, pack16(o, bf16_t()));
+          }
+        }
+#pragma unroll
+        for (int cb = 0; cb < CB; ++cb)
+#pragma unroll
+          for (int mb = 0; mb < MB; ++mb)
+            acc[cb][mb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(af[cb], bj[mb], acc[cb][mb], 0, 0, 0);
+      }
+    }
+  };
+  if constexpr (!DB) {
+    for (int r = 0; r < rounds; ++r) {
+      if (r > 0) issue(I0{}, k0 + r * RK);
+      __builtin_amdgcn_sched_barrier(0);
+      compute(I0{}, k0 + r * RK);
+    }
+  } else {
+    // the round after the one multiplied is always in flight (a round past
+    // the range reads zeros, so the issue is unconditional and every wait
+    // is for the older buffer only)
+    for (int r = 0; r < rounds; r += 2) {
+      issue(I1{}, k0 + (r + 1) * RK);
+      __builtin_amdgcn_sched_barrier(0);
+      compute(I0{}, k0 + r * RK);
+      if (r + 1 >= rounds) break;
+      issue(I0{}, k0 + (r + 2) * RK);
+      __builtin_amdgcn_sched_barrier(0);
+      compute(I1{}, k0 + (r + 1) * RK);
     }
   }
+  // every wave is past its transposition buffer before the partial sums
+  // take that space
+  __syncthreads();
+  float (*red)[RM][CN + 1] = reinterpret_cast<float (*)[RM][CN + 1]>(lds);
 #pragma unroll
   for (int mb = 0; mb < MB; ++mb) {
     if (16 * mb + l16 < M) {
 #pragma unroll
-      for (int r = 0; r < 4; ++r) red[wave][16 * mb + l16][4 * kg + r] = acc[mb][r];
+      for (int cb = 0; cb < CB; ++cb)
+#pragma unroll
+        for (int r = 0; r < 4; ++r) red[wave][16 * mb + l16][16 * cb + 4 * kg + r] = acc[cb][mb][r];
     }
   }
   __syncthreads();
-  const int items = M * kSkCols;
-  for (int it = tid; it < items; it += kSkWaves * 64) {
-    const int m = it / kSkCols, j = it % kSkCols;
+  const int items = M * CN;
+  // elementwise epilogues finish each item where its partial sums meet;
+  // SwiGLU and the rotary one pair columns, through a tile in LDS
+  const bool paired = ep.epi == EPI_SWIGLU || ep.epi == EPI_ROPE;
+#pragma unroll
+  for (int q = 0; q < IPT; ++q) {
+    const int it = tid + q * NT;
+    if (it >= items) break;
+    const int m = it / CN, jj = it % CN;
     float z = 0.f;
 #pragma unroll
-    for (int w = 0; w < kSkWaves; ++w) z += red[w][m][j];
-    const int c = skinny_col(t, j, rope_half);
-    if (ep.bias != nullptr && c < N) z += to_f32(static_cast<const bf16_t*>(ep.bias)[c]);
-    tile[m][j] = z;
+    for (int w = 0; w < kSkWaves; ++w) z += red[w][m][jj];
+    z += pre_b[q];
+    if (paired) {
+      tile[m][jj] = z;
+      continue;
+    }
+    const int c = skinny_col(t * CB + jj / kSkCols, jj % kSkCols, rope_half);
+    if (c >= N) continue;
+    if (ep.epi == EPI_GELU) z = gelu_erf(z);
+    else if (ep.epi == EPI_RESIDUAL) z += pre_r[q];
+    static_cast<bf16_t*>(ep.y)[(mrow0 + m) * static_cast<int64_t>(ep.ldy) + c] = f32_to_bf16(z);
   }
+  if (!paired) return;
   __syncthreads();
-  for (int it = tid; it < items; it += kSkWaves * 64) {
-    const int m = it / kSkCols, j = it % kSkCols;
-    const int c = skinny_col(t, j, rope_half);
+#pragma unroll
+  for (int q = 0; q < IPT; ++q) {
+    const int it = tid + q * NT;
+    if (it >= items) break;
+    const int m = it / CN, jj = it % CN, j = jj % kSkCols;
+    const int c = skinny_col(t * CB + jj / kSkCols, j, rope_half);
     if (c >= N) continue;
     const int64_t row = mrow0 + m;  // row of x and of the output
     bf16_t* y = static_cast<bf16_t*>(ep.y) + row * ep.ldy;
-    const float z = tile[m][j];
+    const float z = tile[m][jj];
     float v = z;
     if (ep.epi == EPI_SWIGLU) {  // gate, up on columns 2f, 2f + 1
       if (j & 1) continue;
-      y[c / 2] = f32_to_bf16(silu(z) * tile[m][j + 1]);
+      y[c / 2] = f32_to_bf16(silu(z) * tile[m][jj + 1]);
       continue;
-    } else if (ep.epi == EPI_GELU) {
-      v = gelu_erf(z);
-    } else if (ep.epi == EPI_RESIDUAL) {
-      v = z + to_f32(static_cast<const bf16_t*>(ep.residual)[row * ep.ldy + c]);
-    } else if (ep.epi == EPI_ROPE && c < ep.rope_cols) {
-      const float zp = tile[m][j ^ 8];
+    } else if (c < ep.rope_cols) {
+      const float zp = tile[m][jj ^ 8];
       const int i = (c % ep.head_dim) % rope_half;
       float sn, cs;
       if (ep.rope_cs != nullptr) {
-        const float2 t = reinterpret_cast<const float2*>(ep.rope_cs)[row * rope_half + i];
-        cs = t.x;
-        sn = t.y;
+        const float2 tc = reinterpret_cast<const float2*>(ep.rope_cs)[row * rope_half + i];
+        cs = tc.x;
+        sn = tc.y;
       } else {
         rope_angle(ep.pos[row], ep.inv_freq[i], &sn, &cs);
       }
@@ -2128,87 +2244,104 @@ int device_cu_count() { return device_cus(); }
 // takes a K range of whole 32-wide steps.
 bool skinny_ok(int dtype, int M, int N, int K, const EpiParams& ep) {
   if (dtype != 1 || M < 1 || M > kSkMaxRows || K % 32 != 0 || K < 32) return false;
-  if (static_cast<int64_t>(N + kSkCols) * K * 2 >= (int64_t{1} << 31)) return false;
+  if (static_cast<int64_t>(N + 4 * kSkCols) * K * 2 >= (int64_t{1} << 31)) return false;
   if (ep.epi == EPI_SWIGLU && N % 2 != 0) return false;
   if (ep.epi == EPI_ROPE && (ep.head_dim < 16 || ep.head_dim % 16 != 0 || N % ep.head_dim != 0))
     return false;
   return true;
 }
 
-// Every workgroup normalises the x fragments it reads, so the folded norm
-// pays off only while the workgroups are few: at most two per CU (a q|k|v
-// projection; not a wide up-projection, where a separate normalisation is
-// cheaper than re-doing it in each of thousands of workgroups).
-// The few-row kernel replaces the tiled ones for short products. Each
-// 16-row block of x re-reads W (from L2), so it pays while the blocks are
-// few or W is small. Measured against the tiled kernels (us per call,
-// N x K = 2304 x 768 / 768 x 768 / 3072 x 768 / 768 x 3072): 64 rows 8.1 /
-// 4.6 / 8.5 / 8.5 against 11.6 / 10.6 / 11.0 / 11.4; 160 rows 14.9 / 6.0 /
-// 18.2 / 14.4 against 10.5 / 12.4 / 10.9 / 12.9; 256 rows, 768 x 768: 8.7
-// against 11.7; 512 rows, 768 x 768: 14.6 against 12.0.
-// Each 16-row block of x re-reads W, so past one block the few-row kernel
-// pays only while the 128 x 128 tiles would be too few to spread W's read
-// over the GPU: measured at 40 rows, K = 2048 (us): N = 16384 (128 tiles)
-// 50.2 few-row against 22.8 tiled; N = 6144 (48 tiles) 19.7 against 25.4;
-// N = 2048 9.1 against 18.6; and N = 2048, K = 8192 28.0 against 70.3.
-// With two 16-row blocks per workgroup it also takes products of up to 256
-// rows whose weights are at most 768 x 3072 (the every-layer GPT-2-shaped
-// stack's short layers: its step at keep rate 0.02 0.962 -> 0.872 ms, at
-// 0.1 0.986 -> 0.899 ms); the decoders' wider weights stay tiled (taking
-// them too made the 16-layer decoder at keep rate 0.25 11.9 -> 13.2 ms).
+// The few-row kernel replaces the tiled ones for short products: its loads
+// go straight to the matrix cores with no tile rounding of M, but each
+// block of 16 (32) rows re-reads W (from L2) and each block of 16 (32)
+// columns re-reads x. Measured (us per call, W of each call not in L2;
+// few-row with one / two 16-column blocks per workgroup against the tiled
+// kernels chosen by shape):
+//   M x N x K                 few-row 1 / 2   tiled
+//   4 x 4096 x 14336          24.1 / 31.3     28.6   (every M <= 16: few-row)
+//   40 x 6144 x 2048          11.2 / 10.5     14.1
+//   40 x 16384 x 2048         26.7 / 23.2     20.8   (128 tiles of 128 x 128)
+//   160 x 3072 x 768 (GELU)    7.2 /  6.0     10.7
+//   160 x 768 x 3072           6.4 /  7.9     12.9
+//   163 x 6144 x 2048         27.4 / 21.8     21.9   (96 tiles)
+//   163 x 2048 x 8192         30.6 / 26.6     24.1
+//   256 x 3072 x 768 (GELU)   10.2 /  8.7     10.8
+//   512 x 2304 x 768          13.6 / 11.4      9.9   (72 tiles)
+//   512 x 768 x 3072          14.3 / 13.4     18.8
+// so it takes M <= 16, and up to 512 rows while the 128 x 128 output tiles
+// are fewer than 64.
 bool skinny_pays(int M, int N, int K) {
+  (void)K;
   const long tiles128 = static_cast<long>((M + 127) / 128) * ((N + 127) / 128);
-  return (M <= 64 && (M <= 16 || tiles128 < 128)) || (M <= 256 && N <= 1024 && K <= 1024) ||
-         (M <= 256 && static_cast<long>(N) * K <= 768L * 3072);
+  return M <= kSkMaxM || (M <= 512 && tiles128 < 64);
 }
 
+// The folded pre-norm: every workgroup normalises the x fragments it
+// reads (its statistics from one more read of its rows), which pays only
+// while the rows are one per wave and the workgroups few: at most two per
+// CU (a q|k|v projection in generation; not a wide up-projection, where a
+// separate normalisation is cheaper than re-doing it in each of thousands
+// of workgroups). Folded into the 160-row projections of the every-layer
+// GPT-2-shaped stack it made the step at keep rate 0.02 0.705 -> 0.872 ms.
 bool skinny_norm_ok(int M, int N, int K) {
   return M >= 1 && M <= kSkWaves && K % 32 == 0 && K <= 4096 &&
          (N + kSkCols - 1) / kSkCols <= 2 * device_cus();
 }
 
 // 16-row blocks per workgroup of the few-row kernel: two past 16 rows
-// (measured on the every-layer GPT-2-shaped stack, 160-row layers, us per
-// call: 160 x 768 x 768 with residual 6.5 -> 4.8, 160 x 768 x 3072 13.6 ->
-// 10.6, 160 x 2304 x 768 14.0 -> 9.1, 160 x 3072 x 768 with GELU 18.1 ->
-// 11.8; four and eight blocks were slower: fewer workgroups in flight)
 int skinny_mb(int M, int N, int K) {
   (void)N;
   (void)K;
   return M <= kSkMaxM ? 1 : 2;
 }
 
+// 16-column blocks per workgroup: two for grids of two-row-block
+// workgroups of at least 512, or 384 when K >= 1024 (the x re-reads they
+// save outweigh the workgroups lost; table above); one up to 16 rows
+// (generation streams W, which the x rows barely add to).
+int skinny_cb(int M, int N, int K) {
+  if (skinny_mb(M, N, K) < 2) return 1;
+  const long wgs =
+      static_cast<long>((N + kSkCols - 1) / kSkCols) * ((M + 2 * kSkMaxM - 1) / (2 * kSkMaxM));
+  return wgs >= 512 || (wgs >= 384 && K >= 1024) ? 2 : 1;
+}
+
 hipError_t launch_gemm_skinny(hipStream_t s, const void* x, int M, int K, const void* w, int N,
                               const EpiParams& ep, const PreNorm* pn) {
   if (M == 0 || N == 0) return hipSuccess;
-  const int kc = ((K + kSkWaves * 32 - 1) / (kSkWaves * 32)) * 32;
+  const int kc = ((K + kSkWaves * 64 - 1) / (kSkWaves * 64)) * 64;  // whole 64-wide groups
   const bf16_t* xp = static_cast<const bf16_t*>(x);
   const bf16_t* wp = static_cast<const bf16_t*>(w);
   const dim3 block(kSkWaves * 64);
-  if (pn == nullptr || pn->g == nullptr) {
-    const int mb = skinny_mb(M, N, K);
-    const dim3 grid((N + kSkCols - 1) / kSkCols, (M + kSkMaxM * mb - 1) / (kSkMaxM * mb));
-    if (mb >= 8)
-      return launch(K_GEMM, gemm_skinny_kernel<0, 8>, grid, block, 0, s, xp, wp, M, N, K, kc, ep,
-                    PreNorm{});
-    if (mb >= 4)
-      return launch(K_GEMM, gemm_skinny_kernel<0, 4>, grid, block, 0, s, xp, wp, M, N, K, kc, ep,
-                    PreNorm{});
-    if (mb >= 2)
-      return launch(K_GEMM, gemm_skinny_kernel<0, 2>, grid, block, 0, s, xp, wp, M, N, K, kc, ep,
-                    PreNorm{});
-    return launch(K_GEMM, gemm_skinny_kernel<0, 1>, grid, block, 0, s, xp, wp, M, N, K, kc, ep,
-                  PreNorm{});
+  const int nblk = (N + kSkCols - 1) / kSkCols;
+  const bool norm = pn != nullptr && pn->g != nullptr;
+  const int mb = norm ? 1 : skinny_mb(M, N, K);
+  const int cb = norm ? 1 : skinny_cb(M, N, K);
+  const dim3 grid((nblk + cb - 1) / cb, (M + kSkMaxM * mb - 1) / (kSkMaxM * mb));
+#define ZSA_SK_LAUNCH(CPL_, MB_, CB_, DB_, LDS_, PN_)                                            \
+  return launch(K_GEMM, gemm_skinny_kernel<CPL_, MB_, CB_, DB_>, grid, block, LDS_, s, xp, wp, M, \
+                N, K, kc, ep, PN_)
+  // two buffers when a wave's K range is longer than one full round
+  const bool db = kc > 64 * sk_groups(mb, cb, false);
+  if (!norm) {
+    if (mb >= 2) {
+      if (cb >= 2) {
+        if (db) ZSA_SK_LAUNCH(0, 2, 2, true, 0, PreNorm{});
+        ZSA_SK_LAUNCH(0, 2, 2, false, 0, PreNorm{});
+      }
+      if (db) ZSA_SK_LAUNCH(0, 2, 1, true, 0, PreNorm{});
+      ZSA_SK_LAUNCH(0, 2, 1, false, 0, PreNorm{});
+    }
+    if (db) ZSA_SK_LAUNCH(0, 1, 1, true, 0, PreNorm{});
+    ZSA_SK_LAUNCH(0, 1, 1, false, 0, PreNorm{});
   }
-  const dim3 grid((N + kSkCols - 1) / kSkCols, (M + kSkMaxM - 1) / kSkMaxM);
   if (!skinny_norm_ok(M, N, K)) return hipErrorInvalidValue;
   const size_t lds = static_cast<size_t>(K) / 8 * 2 * sizeof(uint4);
   const int cpl = (K / 8 + 63) / 64;
-  if (cpl <= 2)
-    return launch(K_GEMM, gemm_skinny_kernel<2, 1>, grid, block, lds, s, xp, wp, M, N, K, kc, ep, *pn);
-  if (cpl <= 4)
-    return launch(K_GEMM, gemm_skinny_kernel<4, 1>, grid, block, lds, s, xp, wp, M, N, K, kc, ep, *pn);
-  return launch(K_GEMM, gemm_skinny_kernel<8, 1>, grid, block, lds, s, xp, wp, M, N, K, kc, ep, *pn);
+  if (cpl <= 2) ZSA_SK_LAUNCH(2, 1, 1, false, lds, *pn);
+  if (cpl <= 4) ZSA_SK_LAUNCH(4, 1, 1, false, lds, *pn);
+  ZSA_SK_LAUNCH(8, 1, 1, false, lds, *pn);
+#undef ZSA_SK_LAUNCH
 }
 
 size_t splitk_bytes(int S, int M, int N) {
@@ -2284,11 +2417,14 @@ size_t gemm_f32_workspace_bound(int M, int N, int K) {
   return splitk_bytes(S, M, N);
 }
 
+bool gemm_takes_skinny(int dtype, int M, int N, int K, const EpiParams& ep) {
+  return gemm_tile_override() == 0 && skinny_ok(dtype, M, N, K, ep) && skinny_pays(M, N, K);
+}
+
 hipError_t launch_gemm(hipStream_t s, int dtype, const void* x, int M, int K, const void* w,
                        int N, const EpiParams& ep, void* ws, size_t ws_bytes) {
   if (M == 0 || N == 0) return hipSuccess;
-  if (gemm_tile_override() == 0 && skinny_ok(dtype, M, N, K, ep) && skinny_pays(M, N, K))
-    return launch_gemm_skinny(s, x, M, K, w, N, ep);
+  if (gemm_takes_skinny(dtype, M, N, K, ep)) return launch_gemm_skinny(s, x, M, K, w, N, ep);
   if (dtype == 1 && K % kBK == 0) {
     int S = 1, kchunk = K;
     splitk_plan(M, N, K, &S, &kchunk);

@@ -195,6 +195,8 @@ struct PreNorm {
 bool skinny_ok(int dtype, int M, int N, int K, const EpiParams& ep);
 bool skinny_pays(int M, int N, int K);  // launch_gemm takes it for such shapes
 bool skinny_norm_ok(int M, int N, int K);
+// launch_gemm runs this product on the few-row kernel
+bool gemm_takes_skinny(int dtype, int M, int N, int K, const EpiParams& ep);
 hipError_t launch_gemm_skinny(hipStream_t s, const void* x, int M, int K, const void* w, int N,
                               const EpiParams& ep, const PreNorm* pn = nullptr);
 

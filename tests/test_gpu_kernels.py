@@ -185,20 +185,26 @@ def test_linear_split_k(m, n, k, epi):
     assert_close(f64(y0), ref, 1e-2, f"unsplit epilogue {epi}")
 
 
-@pytest.mark.parametrize("m,n,k", [(17, 2304, 768),    # the short-product kernel's first row count
-                                   (64, 256, 4096),    # K split over 8 workgroups
-                                   (160, 768, 3072),   # over 4
-                                   (160, 2304, 768),   # one range per workgroup
-                                   (256, 3072, 768),   # its last row count
-                                   (40, 2048, 8192),   # long K in one range
-                                   (100, 48, 64),      # three column blocks, one round
-                                   (200, 1000, 96)])   # ragged N, K not a whole round
+@pytest.mark.parametrize("m,n,k", [(4, 6144, 4096),     # one row block, two register rounds
+                                   (8, 2048, 8192),     # one row block, long K
+                                   (17, 2304, 768),     # two row blocks, one partly filled
+                                   (64, 256, 4096),     # two register rounds
+                                   (160, 768, 3072),    # one column block per workgroup
+                                   (160, 2304, 768),    # two column blocks per workgroup
+                                   (256, 3072, 768),
+                                   (40, 2048, 8192),    # long K, two register rounds
+                                   (100, 48, 64),       # three column blocks, one wave's range
+                                   (200, 1000, 96),     # ragged N, K not a whole 64-wide group
+                                   (300, 2304, 1024),   # ragged rows, two column blocks
+                                   (500, 1000, 2048),   # odd column blocks: the last pair half past N
+                                   (512, 768, 3072)])   # the last row count, two column blocks
 @pytest.mark.parametrize("epi", [zsa.EPI_NONE, zsa.EPI_GELU, zsa.EPI_SWIGLU, zsa.EPI_RESIDUAL])
 @pytest.mark.parametrize("split", [True, False])
 def test_linear_short_products(m, n, k, epi, split):
-    """Products of 17 to 256 rows (all rows of x in one workgroup, K split
-    over its waves and, with a workspace, over workgroups), every epilogue
-    but the rotary one, against the oracle, and reproducible."""
+    """Products of 4 to 512 rows (the few-row kernel: one or two 16-row and
+    16-column blocks per workgroup, K over its waves in one round or in
+    double-buffered rounds), every epilogue but the rotary one, against the
+    oracle, and reproducible."""
     if epi == zsa.EPI_SWIGLU:  # the API takes gate/up products of whole 16-column groups
         n = (n + 15) // 16 * 16
     g = np.random.default_rng(m + n + k + epi)
@@ -266,7 +272,10 @@ def test_linear_kernel_regimes(m, n, k, split, epi, with_bias):
 @pytest.mark.parametrize("m,n,k,hd,rope_cols", [(16129, 3072, 768, 64, 2048),   # 256x256 on 8 waves
                                                (4097, 4096, 4096, 128, 2048),   # K > 3072
                                                (4097, 6144, 4096, 128, 5120),   # grouped-query
-                                               (3000, 3072, 768, 64, 2048)])    # 128x128
+                                               (3000, 3072, 768, 64, 2048),     # 128x128
+                                               (40, 6144, 2048, 64, 4096),      # few-row, two column blocks
+                                               (163, 3072, 768, 64, 2048),      # few-row, ragged rows
+                                               (20, 6144, 4096, 128, 5120)])    # few-row, grouped-query
 @pytest.mark.parametrize("with_bias", [True, False])
 @pytest.mark.parametrize("table", [False, True])
 def test_linear_rope_regimes(m, n, k, hd, rope_cols, with_bias, table):
@@ -289,6 +298,7 @@ def test_linear_rope_regimes(m, n, k, hd, rope_cols, with_bias, table):
     torch.cuda.synchronize()
     assert torch.equal(y1, y2)
     rows = np.unique(np.concatenate([np.arange(64), np.arange(m - 64, m), g.integers(0, m, 128)]))
+    rows = rows[(rows >= 0) & (rows < m)]
     rt = torch.from_numpy(rows).to(dev())
     z = f64(xd[rt]) @ f64(wd).T
     if bd is not None:
