@@ -2338,6 +2338,11 @@ hipError_t launch_gemm_skinny(hipStream_t s, const void* x, int M, int K, const 
   if (!skinny_norm_ok(M, N, K)) return hipErrorInvalidValue;
   const size_t lds = static_cast<size_t>(K) / 8 * 2 * sizeof(uint4);
   const int cpl = (K / 8 + 63) / 64;
+  if (db) {
+    if (cpl <= 2) ZSA_SK_LAUNCH(2, 1, 1, true, lds, *pn);
+    if (cpl <= 4) ZSA_SK_LAUNCH(4, 1, 1, true, lds, *pn);
+    ZSA_SK_LAUNCH(8, 1, 1, true, lds, *pn);
+  }
   if (cpl <= 2) ZSA_SK_LAUNCH(2, 1, 1, false, lds, *pn);
   if (cpl <= 4) ZSA_SK_LAUNCH(4, 1, 1, false, lds, *pn);
   ZSA_SK_LAUNCH(8, 1, 1, false, lds, *pn);
