@@ -2268,12 +2268,15 @@ bool skinny_ok(int dtype, int M, int N, int K, const EpiParams& ep) {
 //   256 x 3072 x 768 (GELU)   10.2 /  8.7     10.8
 //   512 x 2304 x 768          13.6 / 11.4      9.9   (72 tiles)
 //   512 x 768 x 3072          14.3 / 13.4     18.8
-// so it takes M <= 16, and up to 512 rows while the 128 x 128 output tiles
-// are fewer than 64.
+//   640 x 768 x 3072               /  14.0     19.4   (policy's choice)
+//   1024 x 768 x 768               /   8.5     10.3
+//   1024 x 768 x 3072              /  20.2     22.8
+// so it takes M <= 16, and up to 1024 rows while the 128 x 128 output
+// tiles are fewer than 64 (past 512 rows: 768-column outputs).
 bool skinny_pays(int M, int N, int K) {
   (void)K;
   const long tiles128 = static_cast<long>((M + 127) / 128) * ((N + 127) / 128);
-  return M <= kSkMaxM || (M <= 512 && tiles128 < 64);
+  return M <= kSkMaxM || (M <= 1024 && tiles128 < 64);
 }
 
 // The folded pre-norm: every workgroup normalises the x fragments it

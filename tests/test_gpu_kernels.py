@@ -197,11 +197,12 @@ def test_linear_split_k(m, n, k, epi):
                                    (200, 1000, 96),     # ragged N, K not a whole 64-wide group
                                    (300, 2304, 1024),   # ragged rows, two column blocks
                                    (500, 1000, 2048),   # odd column blocks: the last pair half past N
-                                   (512, 768, 3072)])   # the last row count, two column blocks
+                                   (512, 768, 3072),    # two column blocks, double-buffered
+                                   (1000, 768, 768)])   # ragged, near the last row count
 @pytest.mark.parametrize("epi", [zsa.EPI_NONE, zsa.EPI_GELU, zsa.EPI_SWIGLU, zsa.EPI_RESIDUAL])
 @pytest.mark.parametrize("split", [True, False])
 def test_linear_short_products(m, n, k, epi, split):
-    """Products of 4 to 512 rows (the few-row kernel: one or two 16-row and
+    """Products of 4 to 1000 rows (the few-row kernel: one or two 16-row and
     16-column blocks per workgroup, K over its waves in one round or in
     double-buffered rounds), every epilogue but the rotary one, against the
     oracle, and reproducible."""
