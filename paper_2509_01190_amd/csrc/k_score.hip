@@ -43,8 +43,12 @@ __global__ __launch_bounds__(64 * kScoreWaves) __attribute__((amdgpu_waves_per_e
   constexpr int KLD = HD + 8;  // K tile row stride (bf16): conflict-free fragment reads
   constexpr int KK = HD / 16;
   constexpr int KS = KB / 32;  // 32-key columns
+  constexpr int LPR = HD / 8;   // lanes per 16-byte-chunked Q row
+  constexpr int RPI = 64 / LPR;  // Q rows per load
+  constexpr int NQI = 32 / RPI;  // loads per 32-row tile
   static_assert(KB * KLD * 2 >= NW * KB * 4, "the reduction fits the K tile");
   __shared__ __align__(16) unsigned char smem[KB * KLD * 2];
+  __shared__ __align__(16) unsigned char qbuf[NW][32 * HD * 2];  // each wave's Q tile
   bf16_t* Ks = reinterpret_cast<bf16_t*>(smem);
 
   const int b = blockIdx.z, h = blockIdx.y;
@@ -72,26 +76,40 @@ __global__ __launch_bounds__(64 * kScoreWaves) __attribute__((amdgpu_waves_per_e
   const __amdgpu_buffer_rsrc_t lres = __builtin_amdgcn_make_buffer_rsrc(
       const_cast<float*>(lse + static_cast<int64_t>(h) * T + lo), 0, static_cast<uint32_t>(n) * 4u,
       0x00020000);
-  const bf16_t* qh = Q + static_cast<int64_t>(lo) * rs + h * HD + hf * 8;
-  // query tiles of 32 rows, strided over the waves; the next tile's Q
-  // fragments are loaded while this tile's products and exps run. Rows past
-  // the sequence are clamped and masked.
+  // Query tiles of 32 rows, strided over the waves; the next tile's Q is
+  // loaded while this tile's products and exps run. Rows past the sequence
+  // are clamped and masked. The loads cover whole cache lines (HD / 8 lanes
+  // per row); the wave passes each tile through its LDS buffer (chunk c of
+  // row r at r * 2 HD + (c ^ (r % 8)) * 16) into the MFMA fragments (lane
+  // l: row l % 32, chunk 2 kk + l / 32). Fragments loaded straight from
+  // memory would touch 32 lines per load, a quarter of each.
+  const bf16_t* qh = Q + static_cast<int64_t>(lo) * rs + h * HD + (lane % LPR) * 8;
+  unsigned char* const qw = qbuf[wave];
   int i0 = (causal ? (j0 & ~31) : 0) + wave * 32;
-  u32x4 qn[KK];
+  u32x4 qn[NQI];
   if (i0 < n) {
 #pragma unroll
-    for (int kk = 0; kk < KK; ++kk)
-      qn[kk] = *reinterpret_cast<const u32x4*>(qh + static_cast<int64_t>(min(i0 + l32, n - 1)) * rs + kk * 16);
+    for (int i = 0; i < NQI; ++i)
+      qn[i] = *reinterpret_cast<const u32x4*>(qh + static_cast<int64_t>(min(i0 + RPI * i + lane / LPR, n - 1)) * rs);
   }
   for (; i0 < n; i0 += 32 * NW) {
+    // LDS operations of a wave run in order: these stores follow the last
+    // tile's fragment reads
+#pragma unroll
+    for (int i = 0; i < NQI; ++i) {
+      const int r = RPI * i + lane / LPR;
+      *reinterpret_cast<u32x4*>(qw + r * (HD * 2) + (((lane % LPR) ^ (r & 7)) << 4)) = qn[i];
+    }
     bf16x8_t qa[KK];
 #pragma unroll
-    for (int kk = 0; kk < KK; ++kk) qa[kk] = __builtin_bit_cast(bf16x8_t, qn[kk]);
+    for (int kk = 0; kk < KK; ++kk)
+      qa[kk] = __builtin_bit_cast(
+          bf16x8_t, *reinterpret_cast<const u32x4*>(qw + l32 * (HD * 2) + (((2 * kk + hf) ^ (l32 & 7)) << 4)));
     const int inext = i0 + 32 * NW;
     if (inext < n) {
 #pragma unroll
-      for (int kk = 0; kk < KK; ++kk)
-        qn[kk] = *reinterpret_cast<const u32x4*>(qh + static_cast<int64_t>(min(inext + l32, n - 1)) * rs + kk * 16);
+      for (int i = 0; i < NQI; ++i)
+        qn[i] = *reinterpret_cast<const u32x4*>(qh + static_cast<int64_t>(min(inext + RPI * i + lane / LPR, n - 1)) * rs);
     }
     // this lane's 16 query rows: i0 + 8 (r/4) + 4 hf + r%4
     float L[16];
