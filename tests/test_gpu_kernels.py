@@ -16,16 +16,22 @@ pytestmark = pytest.mark.gpu
 
 
 # ------------------------------------------------------------------ top-k
-@pytest.mark.parametrize("case", ["ragged_ties", "long_rows", "edges"])
+@pytest.mark.parametrize("case", ["ragged_ties", "long_rows", "edges", "one_magnitude", "all_equal"])
 def test_select_topk_bit_exact(case):
     if case == "ragged_ties":
         lens = W.lengths(W.PRESETS["ragged"], 0)
     elif case == "long_rows":
         lens = [20000, 16384, 16385, 3, 4097]
     else:
-        lens = [0, 1, 5, 6, 64, 1000, 2]
+        lens = [0, 1, 5, 6, 64, 1000, 2, 2048, 2049, 3000]
     g = np.random.default_rng(3)
     scores = W.injected_scores(lens, seed=1)
+    if case == "one_magnitude":
+        # every key shares its top two bytes (the radix passes there put all
+        # rows in one bin), with ties among the rest
+        scores = (10.0 + np.round(g.uniform(0.0, 0.03, len(scores)), 3)).astype(np.float32)
+    elif case == "all_equal":
+        scores = np.full(len(scores), 3.25, np.float32)
     ks = []
     for b, n in enumerate(lens):
         if b % 5 == 3:
