@@ -200,6 +200,7 @@ def test_linear_split_k(m, n, k, epi):
                                    (256, 3072, 768),
                                    (40, 2048, 8192),    # long K, two register rounds
                                    (100, 48, 64),       # three column blocks, one wave's range
+                                   (33, 8, 32),         # N under one column block, K one step
                                    (200, 1000, 96),     # ragged N, K not a whole 64-wide group
                                    (300, 2304, 1024),   # ragged rows, two column blocks
                                    (500, 1000, 2048),   # odd column blocks: the last pair half past N
