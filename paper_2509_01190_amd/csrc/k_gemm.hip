@@ -16,9 +16,11 @@
 //    rounds on the CUs, w4p_width);
 //  * gemm_bf16_w4_kernel: its slice loop with one tile per workgroup (a
 //    tuning baseline, ZSA_GEMM_TILE);
-//  * gemm_skinny_kernel: products of at most 64 rows (256 with N, K <=
-//    1024; generation and short pruned layers), W streamed into
-//    v_mfma_f32_16x16x32_bf16 operands;
+//  * gemm_skinny_kernel: products of at most 16 rows, and of up to 1024
+//    rows whose 128x128 tiles would number under 64 (generation and short
+//    pruned layers): no shared tiles, operands loaded in whole cache lines
+//    and passed through a per-wave LDS buffer into
+//    v_mfma_f32_16x16x32_bf16 fragments;
 //  * gemm_bf16_mfma_kernel: the register-staged 128x128 original, kept as a
 //    tuning baseline (ZSA_GEMM_TILE).
 // The others use v_mfma_f32_32x32x16_bf16. fp32 storage: a 64x128
@@ -835,8 +837,9 @@ __global__ __launch_bounds__(256) void splitk_sum_f32_kernel(const float4* __res
 // Few-row products (generation, and the short layers of deep pruning)
 // ---------------------------------------------------------------------------
 // y = epi(x W^T) for few rows of x: with M <= 16 the whole cost is one read
-// of W (M multiply-adds per weight), and up to a few hundred rows the tiled
-// kernels' 128-row tiles would mostly multiply padding. The kernel has no
+// of W (M multiply-adds per weight), and for narrow outputs up to about a
+// thousand rows the tiled kernels' output tiles are too few to fill the
+// GPU or mostly multiply padding. The kernel has no
 // shared tiles: v_mfma_f32_16x16x32_bf16 takes A = 16 rows of W (lane l:
 // row l % 16, the 8 K values 8 (l / 16) .. + 7 of a 32-wide step) and B =
 // 16 x rows (lane l: row l % 16, zero past M); lane l then holds outputs
@@ -854,11 +857,11 @@ constexpr int kSkWaves = 8;   // K ranges per workgroup
 constexpr int kSkMaxM = 16;   // rows of x per row block
 constexpr int kSkMaxRows = 4096;  // rows of x per launch (a grid of 16-row blocks)
 
-// output column of tile column j in workgroup t (rope_half = hd / 2 for the
-// rotary epilogue, else 0)
+// output column of column j of 16-column block t (rope_half = hd / 2 for
+// the rotary epilogue, else 0)
 __device__ __forceinline__ int skinny_col(int t, int j, int rope_half) {
   if (rope_half == 0) return t * kSkCols + j;
-  const int per_head = rope_half / 8;  // workgroups per head
+  const int per_head = rope_half / 8;  // column blocks per head
   const int h = t / per_head, i0 = (t % per_head) * 8;
   return h * 2 * rope_half + i0 + (j & 7) + (j >> 3) * rope_half;
 }
