@@ -2106,12 +2106,18 @@ bool w4p_ok(int M, int N, int K, const EpiParams& ep, int bn = 256) {
 // or 0 where it does not pay. Measured on M = 2048 .. 16384, N = 768 ..
 // 3072, K = 768 and 3072 against the persistent 128x128 kernel (which needs
 // twice the operand bytes per FLOP): a width pays when its tiles fill their
-// last round on the CUs at least three-quarters, or number at least
-// three-quarters of one round (16384 x 768 x 3072, 256 wide, 192 tiles:
-// 69.2 against 78.0 us; 4096 x 2304 x 768, 192 wide, 192 tiles: 18.4
-// against 21.5 us); rounds filled less lose (16384 x 2304 x 768, 256 wide,
-// 2.25 rounds: 68.0 against 67.4 us; 8192 x 768 x 3072, 192 wide, half a
-// round: 52.3 against 47.8 us). Of the widths that pay, the better-filled
+// last round on the CUs at least half (three-quarters with the GELU
+// epilogue, which one wave per SIMD leaves exposed), or number at least
+// 0.68 of one round (16384 x 768 x 3072, 256 wide, 192 tiles: 69.2 against
+// 78.0 us; 11456 x 768 x 3072, 192 wide, 180 tiles: 58.3 against 77.9;
+// 2748 x 3072 x 768 with GELU, 192 wide, 176 tiles: 22.6 against 25.8;
+// 11456 x 2304 x 768, 256 wide, 1.58 rounds: 47.6 against 51.6; the
+// rotary 4096 x 6144 x 2048, 1.5 rounds: the 16-layer decoder at keep rate
+// 0.5 15.64 -> 15.54 ms); rounds filled less lose (16384 x 2304 x 768, 256
+// wide, 2.25 rounds: 68.0 against 67.4 us; 8192 x 768 x 3072, 192 wide, half
+// a round: 52.3 against 47.8 us; 10485 x 768 x 768, 0.64 of a round: 22.8
+// against 20.4; 6710 x 3072 x 768 with GELU, 1.69 rounds: 45.8 against
+// 41.3). Of the widths that pay, the better-filled
 // one is taken, 256 on a tie (more FLOPs per operand byte): 192 for
 // 16384 x 2304 x 768 (three whole rounds: 57.9 us) and 16384 x 768 x K (one:
 // 25.8 and 65.2 us for K = 768 and 3072), 256 for 16384 x 3072 x 768 (85.9
@@ -2127,8 +2133,8 @@ int w4p_width(int M, int N, int K, const EpiParams& ep) {
     const long rem = tiles % cus;
     bool pays;
     if (K > 3072) pays = tiles >= cus;
-    else if (tiles >= cus) pays = rem == 0 || 4 * rem >= 3 * cus;
-    else pays = 4 * tiles >= 3 * cus;
+    else if (tiles >= cus) pays = rem == 0 || (ep.epi == EPI_GELU ? 4 * rem >= 3 * cus : 2 * rem >= cus);
+    else pays = 100 * tiles >= 68 * cus;
     if (!pays) continue;
     const long slots = (tiles + cus - 1) / cus * cus;
     if (best == 0 || tiles * best_slots > best_fill * slots) {
