@@ -2232,7 +2232,12 @@ int gemm_tile_override() {
 // Every slice is non-empty and all but the last have kchunk columns. Per
 // projection (both launches), M x 768 x 3072 with a residual: 256 rows 26.6
 // -> 15.9 us, 2048 rows 31.7 -> 27.1, 3584 rows (168 tiles) 34.0 -> 32.5,
-// 4096 rows (192 tiles) 32.1 -> 35.5 (not split).
+// 4096 rows (192 tiles) 32.1 -> 35.5 (not split); 1024 x 2048 x 8192 71.5
+// (persistent 128 x 128) -> 53.4. (1024 x 2048 x 2048 with a residual
+// splits at a loss, 27.7 against 22.8 us on the persistent kernel, but the
+// rotary products of the same grids, which that kernel does not take, need
+// the split: the 1B-shaped decoder at keep rate 0.1 9.66 -> 9.73 ms without
+// it.)
 void splitk_plan(int M, int N, int K, int* S, int* kchunk) {
   *S = 1;
   *kchunk = K;
@@ -2483,19 +2488,23 @@ hipError_t launch_gemm(hipStream_t s, int dtype, const void* x, int M, int K, co
     // Measured on the projection shapes of the 768-wide stacks (N = 768,
     // 2304, 3072; K = 768, 3072; M = 2048 .. 16384): the persistent
     // four-wave kernel where w4p_width finds a tile width that pays, the
-    // persistent 128x128 kernel otherwise. For longer K (the 4096-wide
-    // decoder, K = 4096 and 14336): the persistent four-wave kernel from one
-    // round of its tiles on (8192 x 4096 x 14336: 754 against 994 us for the
-    // 8-wave kernel below; 4096 x 6144 x 4096: 173 against 210 us), else --
-    // and for the rotary and SwiGLU epilogues -- direct-to-LDS 256x256 tiles
-    // over 8 waves (128x64 per wave) once the grid holds at least four
-    // rounds of them, or 128x128 tiles.
+    // persistent 128x128 kernel otherwise. For longer K (the decoders, K =
+    // 4096 .. 14336): the persistent four-wave kernel from one round of its
+    // tiles on (8192 x 4096 x 14336: 754 against 994 us for the 8-wave
+    // kernel below; 4096 x 6144 x 4096: 173 against 210 us), else -- and for
+    // the rotary and SwiGLU epilogues -- direct-to-LDS 256x256 tiles over 8
+    // waves (128x64 per wave) once the grid holds at least four rounds of
+    // them, else the persistent 128x128 kernel (1632 x 2048 x 8192: 74.5
+    // against 81.3 us direct-to-LDS 128x128; 1472 x 4096 x 4096 61.8 against
+    // 65.7; 3276 x 4096 x 14336 432 against 430), or direct-to-LDS 128x128
+    // tiles for the epilogues it lacks.
     const int bn = w4p_width(M, N, K, ep);
     if (bn == 256) return launch_w4p<256>(s, x, M, K, w, N, ep);
     if (bn == 192) return launch_w4p<192>(s, x, M, K, w, N, ep);
     if (K <= 3072 && persist_ok(M, N, K, ep)) return launch_persist_any<64, 2>(s, x, M, K, w, N, ep);
     const long tiles256 = static_cast<long>((M + 255) / 256) * ((N + 255) / 256);
     if (tiles256 >= 1024) return launch_dma<256, 256, 2, 4, 64, 2, 128>(s, x, M, K, w, N, ep);
+    if (persist_ok(M, N, K, ep)) return launch_persist_any<64, 2>(s, x, M, K, w, N, ep);
     return launch_dma<128, 128, 2, 2, 64, 2, 128>(s, x, M, K, w, N, ep);
   }
   const dim3 grid((M + vBM - 1) / vBM, (N + vBN - 1) / vBN);

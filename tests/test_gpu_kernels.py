@@ -150,8 +150,7 @@ def test_linear_epilogues(dtype, k, epi):
     assert_close(f64(y), ref, 1e-2 if dtype == "bf16" else 2e-5, f"epilogue {epi}")
 
 
-@pytest.mark.parametrize("m,n,k", [(37, 384, 1024), (300, 384, 1024), (160, 768, 3072),
-                                   (2100, 768, 3072)])
+@pytest.mark.parametrize("m,n,k", [(1100, 384, 3072), (1500, 768, 8192), (2100, 768, 3072)])
 @pytest.mark.parametrize("epi", [zsa.EPI_NONE, zsa.EPI_GELU, zsa.EPI_SWIGLU, zsa.EPI_RESIDUAL,
                                  zsa.EPI_ROPE])
 def test_linear_split_k(m, n, k, epi):
@@ -245,7 +244,9 @@ def test_linear_short_products(m, n, k, epi, split):
                                          (12289, 3072, 768, False),   # persistent 128x128
                                          (1000, 768, 768, False),
                                          (4000, 768, 3072, False),
-                                         (16385, 2304, 768, False)])
+                                         (16385, 2304, 768, False),
+                                         (1500, 2048, 8192, False),   # persistent 128x128, long K
+                                         (1000, 2048, 8192, True)])   # split K over 4 slices
 @pytest.mark.parametrize("epi", [zsa.EPI_NONE, zsa.EPI_GELU, zsa.EPI_RESIDUAL, zsa.EPI_SWIGLU])
 @pytest.mark.parametrize("with_bias", [True, False])
 def test_linear_kernel_regimes(m, n, k, split, epi, with_bias):
