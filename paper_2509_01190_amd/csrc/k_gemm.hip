@@ -2233,11 +2233,11 @@ int gemm_tile_override() {
 // projection (both launches), M x 768 x 3072 with a residual: 256 rows 26.6
 // -> 15.9 us, 2048 rows 31.7 -> 27.1, 3584 rows (168 tiles) 34.0 -> 32.5,
 // 4096 rows (192 tiles) 32.1 -> 35.5 (not split); 1024 x 2048 x 8192 71.5
-// (persistent 128 x 128) -> 53.4. (1024 x 2048 x 2048 with a residual
-// splits at a loss, 27.7 against 22.8 us on the persistent kernel, but the
-// rotary products of the same grids, which that kernel does not take, need
-// the split: the 1B-shaped decoder at keep rate 0.1 9.66 -> 9.73 ms without
-// it.)
+// (persistent 128 x 128) -> 53.4. Up to K = 2048 launch_gemm leaves the
+// products the persistent 128x128 kernel takes unsplit (1024 x 2048 x 2048
+// with a residual: split 27.7 against 22.8 us on that kernel), but the
+// rotary products of the same grids, which it does not take, need the
+// split (the 1B-shaped decoder at keep rate 0.1 9.66 -> 9.73 ms without).
 void splitk_plan(int M, int N, int K, int* S, int* kchunk) {
   *S = 1;
   *kchunk = K;
@@ -2450,7 +2450,10 @@ hipError_t launch_gemm(hipStream_t s, int dtype, const void* x, int M, int K, co
   if (dtype == 1 && K % kBK == 0) {
     int S = 1, kchunk = K;
     splitk_plan(M, N, K, &S, &kchunk);
-    if (S > 1 && ws != nullptr && ws_bytes >= splitk_bytes(S, M, N)) {
+    // (K <= 2048: the persistent 128x128 kernel beats the split where it
+    // takes the epilogue; see splitk_plan)
+    if (S > 1 && ws != nullptr && ws_bytes >= splitk_bytes(S, M, N) &&
+        !(K <= 2048 && persist_ok(M, N, K, ep))) {
       float* part = static_cast<float*>(ws);
       const hipError_t e =
           launch_dma<128, 128, 2, 2, 64, 2, 128>(s, x, M, K, w, N, ep, S, kchunk, part);
