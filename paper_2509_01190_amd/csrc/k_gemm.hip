@@ -2226,13 +2226,14 @@ int gemm_tile_override() {
 
 }  // namespace
 
-// Split K when the 128 x 128 output tiles fill under three-quarters of the
-// CUs once and K is long (at least kMinSplitK): S slices of at least
+// Split K when the 128 x 128 output tiles fill under 0.7 of the CUs once
+// and K is long (at least kMinSplitK): S slices of at least
 // kMinSplitSteps K steps, S x tiles <= 512 workgroups (one round, no tail).
 // Every slice is non-empty and all but the last have kchunk columns. Per
 // projection (both launches), M x 768 x 3072 with a residual: 256 rows 26.6
 // -> 15.9 us, 2048 rows 31.7 -> 27.1, 3584 rows (168 tiles) 34.0 -> 32.5,
-// 4096 rows (192 tiles) 32.1 -> 35.5 (not split); 1024 x 2048 x 8192 71.5
+// 3904 rows (186 tiles) 34.9 -> 39.6 (not split), 4096 rows (192 tiles)
+// 32.1 -> 35.5 (not split); 1024 x 2048 x 8192 71.5
 // (persistent 128 x 128) -> 53.4. Up to K = 2048 launch_gemm leaves the
 // products the persistent 128x128 kernel takes unsplit (1024 x 2048 x 2048
 // with a residual: split 27.7 against 22.8 us on that kernel), but the
@@ -2244,7 +2245,7 @@ void splitk_plan(int M, int N, int K, int* S, int* kchunk) {
   if (K % kBK != 0 || K < kMinSplitK) return;
   const long tiles = static_cast<long>((M + 127) / 128) * ((N + 127) / 128);
   const int steps = K / kBK;
-  if (4 * tiles >= 3 * device_cus()) return;
+  if (10 * tiles >= 7 * device_cus()) return;
   const int want = std::min(static_cast<int>(512 / tiles), steps / kMinSplitSteps);
   if (want < 2) return;
   const int per = (steps + want - 1) / want;
