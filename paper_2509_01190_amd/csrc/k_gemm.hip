@@ -408,12 +408,13 @@ __device__ __forceinline__ void res_load32(__amdgpu_buffer_rsrc_t rres, uint32_t
   }
 }
 
-// epilogue of one 32 x 32 accumulator block: rows m (this lane's), columns
-// nc .. nc + 31; bw[g] = the bias of the lane's four columns of group g
+// finished bf16 values of one 32 x 32 accumulator block (this lane's row,
+// columns nc .. nc + 31; bw[g] = the bias of the lane's four columns of group
+// g): v[p] = the 16 bytes of columns nc + (2p + half) * 8 .. + 7; for SwiGLU
+// v[p].x, .y = the 8 bytes of output columns nc / 2 + 8p + 4 half .. + 3
 template <int EPI>
-__device__ __forceinline__ void epi_store32(const f32x16_t& a, const uint2 (&bw)[4], uint32_t (&r)[2][4],
-                                            __amdgpu_buffer_rsrc_t yres, uint32_t m, int nc, int half,
-                                            int ldy) {
+__device__ __forceinline__ void epi_pack32(const f32x16_t& a, const uint2 (&bw)[4], uint32_t (&r)[2][4],
+                                           int half, u32x4 (&v)[2]) {
   if (EPI == EPI_SWIGLU) {
     // gate and up on columns 2c, 2c + 1: a lane's four columns of group g
     // give outputs nc / 2 + 4g + 2 half (+1); after the swap of groups 2p
@@ -432,11 +433,7 @@ __device__ __forceinline__ void epi_store32(const f32x16_t& a, const uint2 (&bw)
         pk[gg] = pack_bf16x2(silu(z0) * z1, silu(z2) * z3);
       }
       lane_swap(pk[0], pk[1]);
-      typedef uint32_t u32x2 __attribute__((ext_vector_type(2)));
-      const u32x2 v = {pk[0], pk[1]};
-      __builtin_amdgcn_raw_buffer_store_b64(
-          v, yres, (m * static_cast<uint32_t>(ldy) + static_cast<uint32_t>(nc / 2 + 8 * p + 4 * half)) * 2u,
-          0, 0);
+      v[p] = u32x4{pk[0], pk[1], 0u, 0u};
     }
     return;
   }
@@ -469,10 +466,31 @@ __device__ __forceinline__ void epi_store32(const f32x16_t& a, const uint2 (&bw)
     }
     lane_swap(pk[0][0], pk[1][0]);
     lane_swap(pk[0][1], pk[1][1]);
-    typedef uint32_t u32x4v __attribute__((ext_vector_type(4)));
-    const u32x4v v = {pk[0][0], pk[0][1], pk[1][0], pk[1][1]};
-    __builtin_amdgcn_raw_buffer_store_b128(
-        v, yres, (m * static_cast<uint32_t>(ldy) + static_cast<uint32_t>(nc + (2 * p + half) * 8)) * 2u, 0, 0);
+    v[p] = u32x4{pk[0][0], pk[0][1], pk[1][0], pk[1][1]};
+  }
+}
+
+// epilogue of one 32 x 32 accumulator block stored straight from the
+// registers: rows m (this lane's), columns nc .. nc + 31
+template <int EPI>
+__device__ __forceinline__ void epi_store32(const f32x16_t& a, const uint2 (&bw)[4], uint32_t (&r)[2][4],
+                                            __amdgpu_buffer_rsrc_t yres, uint32_t m, int nc, int half,
+                                            int ldy) {
+  u32x4 v[2];
+  epi_pack32<EPI>(a, bw, r, half, v);
+#pragma unroll
+  for (int p = 0; p < 2; ++p) {
+    if (EPI == EPI_SWIGLU) {
+      typedef uint32_t u32x2 __attribute__((ext_vector_type(2)));
+      const u32x2 w = {v[p][0], v[p][1]};
+      __builtin_amdgcn_raw_buffer_store_b64(
+          w, yres, (m * static_cast<uint32_t>(ldy) + static_cast<uint32_t>(nc / 2 + 8 * p + 4 * half)) * 2u,
+          0, 0);
+    } else {
+      __builtin_amdgcn_raw_buffer_store_b128(
+          v[p], yres, (m * static_cast<uint32_t>(ldy) + static_cast<uint32_t>(nc + (2 * p + half) * 8)) * 2u,
+          0, 0);
+    }
   }
 }
 
@@ -1715,6 +1733,138 @@ __device__ __forceinline__ void reg_epilogue_lb(const f32x16_t (&acc)[TM][TN], i
   }
 }
 
+// Epilogue of gemm_bf16_w4p_kernel through a per-wave LDS staging buffer
+// (stg, 4 KiB), for the plain and residual epilogues. A store straight from
+// the accumulators covers 32 bytes of each of 32 rows, a quarter of a
+// 128-byte line each; here the wave takes chunks of 32 rows x 64 columns (two
+// 32 x 32 accumulator blocks), writes the finished bf16 values of a chunk to
+// stg in the accumulator layout and reads them back as 16 bytes of one row
+// per lane, so that each store instruction covers 8 rows x 128 bytes. A
+// residual goes the other way: whole-line loads, issued one chunk ahead,
+// turned into the accumulator layout through stg. Row r of stg holds its
+// 16-byte chunk c at r * 128 + ((c ^ (r & 7)) << 4), so the rows a line read
+// or write covers hit distinct banks. No barrier: a wave's LDS operations run
+// in issue order, and compiler fences keep each cross-lane read after the
+// writes it depends on. A 256 x 192 tile leaves each wave a third 32-column
+// block per row block, which is stored straight from the registers. Measured
+// (us per launch, 256 x 256 tiles): 16384 x 16384 x 2048 902.8 -> 854.9,
+// 16384 x 768 x 3072 with a residual 78.0 -> 76.2, 8192 x 2048 x 8192 with a
+// residual 205.3 -> 201.0; 256 x 192 tiles: 16384 x 2304 x 768 60.3 -> 56.9.
+// The GELU and SwiGLU epilogues keep the direct stores: their arithmetic,
+// not the store pattern, bounds them (16384 x 3072 x 768 with GELU took 91.1
+// us direct, 95.5 staged, and 92.0 with line-shaped stores and no staging).
+template <int TM, int TN, int EPI>
+__device__ __forceinline__ void reg_epilogue_lds(const f32x16_t (&acc)[TM][TN], int mb, int nb, int M,
+                                                 int l32, int half, const EpiParams& ep,
+                                                 const unsigned char* blds, unsigned char* stg) {
+  constexpr int BPC = 2;            // accumulator blocks per chunk
+  constexpr int NCH = TN / BPC;     // staged chunks per row block
+  if constexpr (EPI == EPI_GELU || EPI == EPI_SWIGLU) {
+    reg_epilogue_lb<TM, TN, EPI>(acc, mb, nb, M, l32, half, ep, blds);
+  } else {
+    const int ybytes = M * ep.ldy * 2;
+    const uint32_t ldy = static_cast<uint32_t>(ep.ldy);
+    const __amdgpu_buffer_rsrc_t yres = __builtin_amdgcn_make_buffer_rsrc(ep.y, 0, ybytes, 0x00020000);
+    const __amdgpu_buffer_rsrc_t rres = __builtin_amdgcn_make_buffer_rsrc(
+        const_cast<void*>(EPI == EPI_RESIDUAL ? ep.residual : ep.y), 0, ybytes, 0x00020000);
+    const int lane = l32 + 32 * half;
+    const int lr = lane >> 3, lc = lane & 7;  // line layout: rows lr + 8q, chunk lc
+    unsigned char* const sline = stg + lr * 128 + ((lc ^ lr) << 4);
+    auto sacc = [&](int c) { return stg + l32 * 128 + ((c ^ (l32 & 7)) << 4); };
+    // chunk step t = i * NCH + k: rows mb + 32 i .., columns nb + 64 k ..
+    constexpr int T = TM * NCH;
+    auto goff = [&](int t, int q) {
+      return ((static_cast<uint32_t>(mb + 32 * (t / NCH) + lr + 8 * q)) * ldy +
+              static_cast<uint32_t>(nb + 64 * (t % NCH) + 8 * lc)) * 2u;
+    };
+    u32x4 rq[4];              // a chunk's residual as loaded (line layout)
+    uint32_t r[BPC][2][4];    // the residual of the chunk computed next
+    u32x4 w[4];               // the previous chunk's values, line layout
+    auto rload = [&](int t) {
+#pragma unroll
+      for (int q = 0; q < 4; ++q)
+        rq[q] = __builtin_bit_cast(u32x4, __builtin_amdgcn_raw_buffer_load_b128(rres, goff(t, q), 0, 0));
+    };
+    // rq -> stg (line layout) -> r (accumulator layout, as res_load32 gives)
+    auto stage_res = [&]() {
+#pragma unroll
+      for (int q = 0; q < 4; ++q) *reinterpret_cast<u32x4*>(sline + q * 1024) = rq[q];
+      asm volatile("" ::: "memory");
+#pragma unroll
+      for (int jj = 0; jj < BPC; ++jj)
+#pragma unroll
+        for (int p = 0; p < 2; ++p) {
+          const u32x4 v = *reinterpret_cast<const u32x4*>(sacc(4 * jj + 2 * p + half));
+          r[jj][p][0] = v[0];
+          r[jj][p][1] = v[1];
+          r[jj][p][2] = v[2];
+          r[jj][p][3] = v[3];
+        }
+      asm volatile("" ::: "memory");
+    };
+    // Software-pipelined: chunk t's arithmetic runs while the line reads of
+    // chunk t - 1 are in flight, and its stores follow. Vector memory
+    // operations are counted in issue order, so each residual load is
+    // issued before the stores it must not wait for: chunk t + 2's after
+    // chunk t's stores, waited for after chunk t + 1's.
+    if (EPI == EPI_RESIDUAL) {
+      rload(0);
+      stage_res();
+      if (T > 1) rload(1);
+    }
+#pragma unroll
+    for (int t = 0; t < T; ++t) {
+      const int i = t / NCH, k = t % NCH;
+      __builtin_amdgcn_sched_barrier(0);
+      u32x4 v[BPC][2];
+#pragma unroll
+      for (int jj = 0; jj < BPC; ++jj) {
+        const int j = k * BPC + jj;
+        uint2 bw[4];
+#pragma unroll
+        for (int g = 0; g < 4; ++g)
+          bw[g] = *reinterpret_cast<const uint2*>(blds + (j * 32 + g * 8 + half * 4) * 2);
+        epi_pack32<EPI>(acc[i][j], bw, r[jj], half, v[jj]);
+      }
+      if (t > 0) {
+#pragma unroll
+        for (int q = 0; q < 4; ++q) __builtin_amdgcn_raw_buffer_store_b128(w[q], yres, goff(t - 1, q), 0, 0);
+      }
+      asm volatile("" ::: "memory");
+#pragma unroll
+      for (int jj = 0; jj < BPC; ++jj)
+#pragma unroll
+        for (int p = 0; p < 2; ++p) *reinterpret_cast<u32x4*>(sacc(4 * jj + 2 * p + half)) = v[jj][p];
+      asm volatile("" ::: "memory");
+#pragma unroll
+      for (int q = 0; q < 4; ++q) w[q] = *reinterpret_cast<const u32x4*>(sline + q * 1024);
+      asm volatile("" ::: "memory");
+      if (EPI == EPI_RESIDUAL && t + 1 < T) {
+        stage_res();
+        if (t + 2 < T) rload(t + 2);
+      }
+    }
+#pragma unroll
+    for (int q = 0; q < 4; ++q) __builtin_amdgcn_raw_buffer_store_b128(w[q], yres, goff(T - 1, q), 0, 0);
+    // the third 32-column block of a 256 x 192 tile's waves
+    if constexpr (TN % BPC != 0) {
+      constexpr int j = TN - 1;
+      uint2 bw[4];
+#pragma unroll
+      for (int g = 0; g < 4; ++g)
+        bw[g] = *reinterpret_cast<const uint2*>(blds + (j * 32 + g * 8 + half * 4) * 2);
+#pragma unroll
+      for (int i = 0; i < TM; ++i) {
+        __builtin_amdgcn_sched_barrier(0);
+        uint32_t r[2][4];
+        const uint32_t m = static_cast<uint32_t>(mb + i * 32 + l32);
+        if (EPI == EPI_RESIDUAL) res_load32(rres, m, nb + j * 32, half, ep.ldy, r);
+        epi_store32<EPI>(acc[i][j], bw, r, yres, m, nb + j * 32, half, ep.ldy);
+      }
+    }
+  }
+}
+
 // Rotary epilogue of gemm_bf16_w4p_kernel: 256-wide tiles and head_dim 64
 // or 128, so a wave's 128 columns hold whole heads and the partner c + hd/2
 // of a channel c sits in the same lane, in another 32 x 32 block (the next
@@ -1838,7 +1988,7 @@ __global__ __launch_bounds__(256) void gemm_bf16_w4p_kernel(const bf16_t* __rest
   static_assert(BN == 256 || BN == 192, "tile width");
   static_assert(NMB >= NRB && NMB >= LPW, "interleave");
   extern __shared__ __align__(16) unsigned char smem[];
-  unsigned char* const blds = smem + 2 * SB;  // bias buffers, 1 KiB each
+  unsigned char* const blds = smem + 2 * SB;  // bias buffers, 1 KiB each, then 4 KiB of staging per wave
   const int tid = threadIdx.x;
   const int lane = tid & 63;
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
@@ -2034,8 +2184,8 @@ __global__ __launch_bounds__(256) void gemm_bf16_w4p_kernel(const bf16_t* __rest
                                                            l32, half, ep,
                                                            blds + (p & 1) * 1024 + wn * BN);
     else
-      reg_epilogue_lb<TM, TN, EPI>(acc, m0 + wm * 128, n0 + wn * (BN / 2), M, l32, half, ep,
-                                   blds + (p & 1) * 1024 + wn * BN);
+      reg_epilogue_lds<TM, TN, EPI>(acc, m0 + wm * 128, n0 + wn * (BN / 2), M, l32, half, ep,
+                                    blds + (p & 1) * 1024 + wn * BN, blds + 2048 + wave * 4096);
     if (p + 1 < count) {
       tile_at(p + 1, &m0, &n0);
       // the next tile's first fragments (its slice 0 was published by the
@@ -2052,7 +2202,10 @@ __global__ __launch_bounds__(256) void gemm_bf16_w4p_kernel(const bf16_t* __rest
 template <int EPI, int BN>
 hipError_t launch_w4p_1(hipStream_t s, const void* x, int M, int K, const void* w, int N,
                         const EpiParams& ep) {
-  constexpr int lds = 2 * (256 + BN) * 64 * 2 + 2 * 1024;
+  // stages, bias buffers and (plain and residual epilogues) 4 KiB of
+  // epilogue staging per wave
+  constexpr int lds = 2 * (256 + BN) * 64 * 2 + 2 * 1024 +
+                      (EPI == EPI_NONE || EPI == EPI_RESIDUAL ? 4 * 4096 : 0);
   static bool lds_raised = false;
   if (!lds_raised) {
     const hipError_t e = hipFuncSetAttribute(
