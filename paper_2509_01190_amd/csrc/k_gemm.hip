@@ -1951,6 +1951,111 @@ __device__ __forceinline__ void rope_epilogue_lb(const f32x16_t (&acc)[TM][TN], 
   }
 }
 
+// Rotary epilogue with head_dim 64 through the per-wave staging buffer of
+// reg_epilogue_lds: a step (32 rows, one channel pair of blocks 2 pr and
+// 2 pr + 1) is exactly one 32 x 64 chunk, written in the accumulator layout
+// and stored as whole lines, the step's arithmetic overlapping the previous
+// step's line reads. The table loads of the next row block are issued before
+// the stores that follow them. Same box, us per projection (rotary table
+// included): 16384 x 6144 x 2048 344.7 -> 341.4, 4096 x 6144 x 2048 105.3 ->
+// 103.4. Head dim 128 pairs blocks 0 and 2, which are not adjacent, and
+// keeps rope_epilogue_lb.
+template <int TM, int TN, int HD>
+__device__ __forceinline__ void rope_epilogue_lds(const f32x16_t (&acc)[TM][TN], int mb, int nb, int M,
+                                                  int l32, int half, const EpiParams& ep,
+                                                  const unsigned char* blds, unsigned char* stg) {
+  if constexpr (HD != 64) {
+    rope_epilogue_lb<TM, TN, HD>(acc, mb, nb, M, l32, half, ep, blds);
+  } else {
+    static_assert(TN == 4, "128-column wave blocks of whole heads");
+    constexpr int HH = HD / 2;
+    const int ybytes = M * ep.ldy * 2;
+    const uint32_t ldy = static_cast<uint32_t>(ep.ldy);
+    const __amdgpu_buffer_rsrc_t yres = __builtin_amdgcn_make_buffer_rsrc(ep.y, 0, ybytes, 0x00020000);
+    const __amdgpu_buffer_rsrc_t tres = __builtin_amdgcn_make_buffer_rsrc(
+        const_cast<float*>(ep.rope_cs), 0, M * HH * 8, 0x00020000);
+    uint32_t unused[2][4];
+    const uint2 zb[4] = {make_uint2(0u, 0u), make_uint2(0u, 0u), make_uint2(0u, 0u), make_uint2(0u, 0u)};
+    const int lane = l32 + 32 * half;
+    const int lr = lane >> 3, lc = lane & 7;
+    unsigned char* const sline = stg + lr * 128 + ((lc ^ lr) << 4);
+    auto sacc = [&](int c) { return stg + l32 * 128 + ((c ^ (l32 & 7)) << 4); };
+    // chunk t = 2 i + pr: rows mb + 32 i .., columns nb + 64 pr ..
+    auto goff = [&](int t, int q) {
+      return ((static_cast<uint32_t>(mb + 32 * (t >> 1) + lr + 8 * q)) * ldy +
+              static_cast<uint32_t>(nb + 64 * (t & 1) + 8 * lc)) * 2u;
+    };
+    // (cos, sin) of channels 8 g + 4 half .. + 3 of the lane's row in row
+    // block i, into buffer b
+    uint32_t tv[2][4][2][4];
+    auto load_step = [&](int i, int b) {
+      const uint32_t m = static_cast<uint32_t>(mb + i * 32 + l32);
+#pragma unroll
+      for (int g = 0; g < 4; ++g) {
+        const uint32_t toff = (m * static_cast<uint32_t>(HH) + static_cast<uint32_t>(8 * g + 4 * half)) * 8u;
+#pragma unroll
+        for (int q = 0; q < 2; ++q) {
+          const auto t = __builtin_amdgcn_raw_buffer_load_b128(tres, toff + 16u * q, 0, 0);
+#pragma unroll
+          for (int w = 0; w < 4; ++w) tv[b][g][q][w] = t[w];
+        }
+      }
+    };
+    u32x4 w[4];
+    load_step(0, 0);
+#pragma unroll
+    for (int i = 0; i < TM; ++i) {
+      __builtin_amdgcn_sched_barrier(0);
+      if (i + 1 < TM) load_step(i + 1, (i + 1) & 1);
+      __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+      for (int pr = 0; pr < 2; ++pr) {
+        const int t = 2 * i + pr;
+        const int jl = 2 * pr, ju = jl + 1;
+        const bool rot = nb + 64 * pr < ep.rope_cols;
+        f32x16_t lo, up;
+#pragma unroll
+        for (int g = 0; g < 4; ++g) {
+          const uint2 bl = *reinterpret_cast<const uint2*>(blds + (jl * 32 + g * 8 + half * 4) * 2);
+          const uint2 bu = *reinterpret_cast<const uint2*>(blds + (ju * 32 + g * 8 + half * 4) * 2);
+          const float b[2][4] = {{__uint_as_float(bl.x << 16), __uint_as_float(bl.x & 0xffff0000u),
+                                  __uint_as_float(bl.y << 16), __uint_as_float(bl.y & 0xffff0000u)},
+                                 {__uint_as_float(bu.x << 16), __uint_as_float(bu.x & 0xffff0000u),
+                                  __uint_as_float(bu.y << 16), __uint_as_float(bu.y & 0xffff0000u)}};
+#pragma unroll
+          for (int e = 0; e < 4; ++e) {
+            const float zl = acc[i][jl][4 * g + e] + b[0][e];
+            const float zu = acc[i][ju][4 * g + e] + b[1][e];
+            const float cs = __uint_as_float(tv[i & 1][g][e >> 1][(e & 1) * 2]);
+            const float sn = __uint_as_float(tv[i & 1][g][e >> 1][(e & 1) * 2 + 1]);
+            lo[4 * g + e] = rot ? zl * cs - zu * sn : zl;
+            up[4 * g + e] = rot ? zu * cs + zl * sn : zu;
+          }
+        }
+        u32x4 vl[2], vu[2];
+        epi_pack32<EPI_NONE>(lo, zb, unused, half, vl);
+        epi_pack32<EPI_NONE>(up, zb, unused, half, vu);
+        if (t > 0) {
+#pragma unroll
+          for (int q = 0; q < 4; ++q) __builtin_amdgcn_raw_buffer_store_b128(w[q], yres, goff(t - 1, q), 0, 0);
+        }
+        asm volatile("" ::: "memory");
+#pragma unroll
+        for (int p = 0; p < 2; ++p) {
+          *reinterpret_cast<u32x4*>(sacc(2 * p + half)) = vl[p];
+          *reinterpret_cast<u32x4*>(sacc(4 + 2 * p + half)) = vu[p];
+        }
+        asm volatile("" ::: "memory");
+#pragma unroll
+        for (int q = 0; q < 4; ++q) w[q] = *reinterpret_cast<const u32x4*>(sline + q * 1024);
+        asm volatile("" ::: "memory");
+      }
+    }
+#pragma unroll
+    for (int q = 0; q < 4; ++q) __builtin_amdgcn_raw_buffer_store_b128(w[q], yres, goff(2 * TM - 1, q), 0, 0);
+  }
+}
+
 // ---------------------------------------------------------------------------
 // bf16 GEMM, persistent form of the four-wave kernel
 // ---------------------------------------------------------------------------
@@ -2180,9 +2285,9 @@ __global__ __launch_bounds__(256) void gemm_bf16_w4p_kernel(const bf16_t* __rest
     block_a(no{});
     block_b(yes{});
     if constexpr (EPI == EPI_ROPE || EPI == kEpiRope128)
-      rope_epilogue_lb<TM, TN, EPI == EPI_ROPE ? 64 : 128>(acc, m0 + wm * 128, n0 + wn * (BN / 2), M,
-                                                           l32, half, ep,
-                                                           blds + (p & 1) * 1024 + wn * BN);
+      rope_epilogue_lds<TM, TN, EPI == EPI_ROPE ? 64 : 128>(acc, m0 + wm * 128, n0 + wn * (BN / 2), M,
+                                                            l32, half, ep, blds + (p & 1) * 1024 + wn * BN,
+                                                            blds + 2048 + wave * 4096);
     else
       reg_epilogue_lds<TM, TN, EPI>(acc, m0 + wm * 128, n0 + wn * (BN / 2), M, l32, half, ep,
                                     blds + (p & 1) * 1024 + wn * BN, blds + 2048 + wave * 4096);
@@ -2202,10 +2307,10 @@ __global__ __launch_bounds__(256) void gemm_bf16_w4p_kernel(const bf16_t* __rest
 template <int EPI, int BN>
 hipError_t launch_w4p_1(hipStream_t s, const void* x, int M, int K, const void* w, int N,
                         const EpiParams& ep) {
-  // stages, bias buffers and (plain and residual epilogues) 4 KiB of
-  // epilogue staging per wave
+  // stages, bias buffers and (plain, residual and head-dim-64 rotary
+  // epilogues) 4 KiB of epilogue staging per wave
   constexpr int lds = 2 * (256 + BN) * 64 * 2 + 2 * 1024 +
-                      (EPI == EPI_NONE || EPI == EPI_RESIDUAL ? 4 * 4096 : 0);
+                      (EPI == EPI_NONE || EPI == EPI_RESIDUAL || EPI == EPI_ROPE ? 4 * 4096 : 0);
   static bool lds_raised = false;
   if (!lds_raised) {
     const hipError_t e = hipFuncSetAttribute(

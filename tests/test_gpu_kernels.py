@@ -279,6 +279,7 @@ def test_linear_kernel_regimes(m, n, k, split, epi, with_bias):
 
 
 @pytest.mark.parametrize("m,n,k,hd,rope_cols", [(16129, 3072, 768, 64, 2048),   # 256x256 on 8 waves
+                                               (8191, 6144, 2048, 64, 4096),    # 1B-shaped QKV
                                                (4097, 4096, 4096, 128, 2048),   # K > 3072
                                                (4097, 6144, 4096, 128, 5120),   # grouped-query
                                                (3000, 3072, 768, 64, 2048),     # 128x128
