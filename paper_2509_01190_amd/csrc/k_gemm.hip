@@ -12,8 +12,9 @@
 //    their XCD's range of tiles, the epilogue from registers;
 //  * gemm_bf16_w4p_kernel: 256x256 or 256x192 tiles on four waves (one per
 //    SIMD), one workgroup per CU streaming the K slices of its tiles as one
-//    sequence, the epilogue from registers (products whose tiles fill their
-//    rounds on the CUs, w4p_width);
+//    sequence (products whose tiles fill their rounds on the CUs,
+//    w4p_width); the GELU and SwiGLU epilogues store from registers, the
+//    others whole lines through a per-wave LDS staging buffer;
 //  * gemm_bf16_w4_kernel: its slice loop with one tile per workgroup (a
 //    tuning baseline, ZSA_GEMM_TILE);
 //  * gemm_skinny_kernel: products of at most 16 rows, and of up to 1024
@@ -28,8 +29,9 @@
 //
 // Epilogues (same order and precision in every kernel that takes them):
 // bias, exact GELU, SwiGLU on interleaved gate/up columns, residual add, or
-// the rotary rotation of head channel pairs (i, i+hd/2) -- the last only in
-// the direct-to-LDS, register-staged and few-row kernels.
+// the rotary rotation of head channel pairs (i, i+hd/2) -- the last in the
+// direct-to-LDS, register-staged and few-row kernels, and (angles from a
+// per-row table) in the persistent four-wave kernel.
 #include <math.h>
 #include <stdlib.h>
 
