@@ -1290,6 +1290,17 @@ __global__ __launch_bounds__(256) void gemm_valu_kernel(const T* __restrict__ X,
 // (KB-wide slices, 2 stages, swizzled direct-to-LDS loads; used with
 // 64-wide slices at two workgroups per CU). N must be a multiple of 128;
 // outputs and residual of fewer than 2^31 bytes.
+// The plain and residual epilogues store whole lines through 4 KiB of LDS
+// per wave past the two stages, where WPC workgroups still fit a CU's 160
+// KiB (64-wide slices at two per CU: exactly). Same box, us per launch
+// with the kernel pinned: 8192 x 2304 x 768 37.9 -> 36.0, 4096 x 2304 x 768
+// 22.4 -> 21.5, 2048 x 6144 x 2048 53.6 -> 52.5; the residual products
+// (whose residual is still read 32 bytes per row) within run-to-run noise.
+template <int EPI, int KB, int WPC>
+constexpr bool persist_stages_epilogue() {
+  return (EPI == EPI_NONE || EPI == EPI_RESIDUAL) && WPC * (2 * (128 + 128) * KB * 2 + 4 * 4096) <= 163840;
+}
+
 template <int EPI, int KB, int WPC>
 __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(WPC, WPC))) void
 gemm_bf16_persist_kernel(const bf16_t* __restrict__ X, const bf16_t* __restrict__ W, int M, int N,
@@ -1475,13 +1486,50 @@ gemm_bf16_persist_kernel(const bf16_t* __restrict__ X, const bf16_t* __restrict_
       set_sources(m0n, n0n);
       ZSA_DMA(0, 0)
     }
+    if constexpr (persist_stages_epilogue<EPI, KB, WPC>()) {
+      // whole-line stores through the wave's 4 KiB staging buffer past the
+      // two stages (the layout of reg_epilogue_lds): row block i is one
+      // 32 x 64 chunk, whose values go in while chunk i - 1's line reads are
+      // in flight
+      unsigned char* const stg = smem + 2 * SB + wave * 4096;
+      const int lr8 = lane >> 3, lc8 = lane & 7;
+      unsigned char* const sline = stg + lr8 * 128 + ((lc8 ^ lr8) << 4);
+      auto goff = [&](int i, int q) {
+        return (static_cast<uint32_t>(m0 + wm * WTM + 32 * i + lr8 + 8 * q) * static_cast<uint32_t>(ep.ldy) +
+                static_cast<uint32_t>(n0 + wn * WTN + 8 * lc8)) * 2u;
+      };
+      u32x4 wv[4];
 #pragma unroll
-    for (int i = 0; i < TM; ++i)
+      for (int i = 0; i < TM; ++i) {
+        u32x4 v[TN][2];
 #pragma unroll
-      for (int j = 0; j < TN; ++j)
-        epi_store32<EPI>(acc[i][j], bw[j], res[i][j], yres,
-                         static_cast<uint32_t>(m0 + wm * WTM + i * 32 + l32), n0 + wn * WTN + j * 32,
-                         half, ep.ldy);
+        for (int j = 0; j < TN; ++j) epi_pack32<EPI>(acc[i][j], bw[j], res[i][j], half, v[j]);
+        if (i > 0) {
+#pragma unroll
+          for (int q = 0; q < 4; ++q) __builtin_amdgcn_raw_buffer_store_b128(wv[q], yres, goff(i - 1, q), 0, 0);
+        }
+        asm volatile("" ::: "memory");
+#pragma unroll
+        for (int j = 0; j < TN; ++j)
+#pragma unroll
+          for (int p = 0; p < 2; ++p)
+            *reinterpret_cast<u32x4*>(stg + l32 * 128 + (((4 * j + 2 * p + half) ^ (l32 & 7)) << 4)) = v[j][p];
+        asm volatile("" ::: "memory");
+#pragma unroll
+        for (int q = 0; q < 4; ++q) wv[q] = *reinterpret_cast<const u32x4*>(sline + q * 1024);
+        asm volatile("" ::: "memory");
+      }
+#pragma unroll
+      for (int q = 0; q < 4; ++q) __builtin_amdgcn_raw_buffer_store_b128(wv[q], yres, goff(TM - 1, q), 0, 0);
+    } else {
+#pragma unroll
+      for (int i = 0; i < TM; ++i)
+#pragma unroll
+        for (int j = 0; j < TN; ++j)
+          epi_store32<EPI>(acc[i][j], bw[j], res[i][j], yres,
+                           static_cast<uint32_t>(m0 + wm * WTM + i * 32 + l32), n0 + wn * WTN + j * 32,
+                           half, ep.ldy);
+    }
     if (!more) break;
     k = knext;
     m0 = m0n;
@@ -1527,7 +1575,7 @@ bool persist_ok(int M, int N, int K, const EpiParams& ep) {
 template <int EPI, int KB, int WPC>
 hipError_t launch_persist(hipStream_t s, const void* x, int M, int K, const void* w, int N,
                           const EpiParams& ep) {
-  constexpr int lds = 2 * (128 + 128) * KB * 2;
+  constexpr int lds = 2 * (128 + 128) * KB * 2 + (persist_stages_epilogue<EPI, KB, WPC>() ? 4 * 4096 : 0);
   static bool lds_raised = false;
   if (!lds_raised) {
     const hipError_t e = hipFuncSetAttribute(
