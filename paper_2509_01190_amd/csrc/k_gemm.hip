@@ -1295,7 +1295,9 @@ __global__ __launch_bounds__(256) void gemm_valu_kernel(const T* __restrict__ X,
 // KiB (64-wide slices at two per CU: exactly). Same box, us per launch
 // with the kernel pinned: 8192 x 2304 x 768 37.9 -> 36.0, 4096 x 2304 x 768
 // 22.4 -> 21.5, 2048 x 6144 x 2048 53.6 -> 52.5; the residual products
-// (whose residual is still read 32 bytes per row) within run-to-run noise.
+// within run-to-run noise, also with their residual read as whole lines
+// through the same buffer (kept as 16-byte reads, fetched during the last K
+// step, where their latency is hidden).
 template <int EPI, int KB, int WPC>
 constexpr bool persist_stages_epilogue() {
   return (EPI == EPI_NONE || EPI == EPI_RESIDUAL) && WPC * (2 * (128 + 128) * KB * 2 + 4 * 4096) <= 163840;
