@@ -416,7 +416,7 @@ __device__ __forceinline__ void res_load32(__amdgpu_buffer_rsrc_t rres, uint32_t
 // v[p].x, .y = the 8 bytes of output columns nc / 2 + 8p + 4 half .. + 3
 template <int EPI>
 __device__ __forceinline__ void epi_pack32(const f32x16_t& a, const uint2 (&bw)[4], uint32_t (&r)[2][4],
-                                           int half, u32x4 (&v)[2]) {
+                                           u32x4 (&v)[2]) {
   if (EPI == EPI_SWIGLU) {
     // gate and up on columns 2c, 2c + 1: a lane's four columns of group g
     // give outputs nc / 2 + 4g + 2 half (+1); after the swap of groups 2p
@@ -479,7 +479,7 @@ __device__ __forceinline__ void epi_store32(const f32x16_t& a, const uint2 (&bw)
                                             __amdgpu_buffer_rsrc_t yres, uint32_t m, int nc, int half,
                                             int ldy) {
   u32x4 v[2];
-  epi_pack32<EPI>(a, bw, r, half, v);
+  epi_pack32<EPI>(a, bw, r, v);
 #pragma unroll
   for (int p = 0; p < 2; ++p) {
     if (EPI == EPI_SWIGLU) {
@@ -1505,7 +1505,7 @@ gemm_bf16_persist_kernel(const bf16_t* __restrict__ X, const bf16_t* __restrict_
       for (int i = 0; i < TM; ++i) {
         u32x4 v[TN][2];
 #pragma unroll
-        for (int j = 0; j < TN; ++j) epi_pack32<EPI>(acc[i][j], bw[j], res[i][j], half, v[j]);
+        for (int j = 0; j < TN; ++j) epi_pack32<EPI>(acc[i][j], bw[j], res[i][j], v[j]);
         if (i > 0) {
 #pragma unroll
           for (int q = 0; q < 4; ++q) __builtin_amdgcn_raw_buffer_store_b128(wv[q], yres, goff(i - 1, q), 0, 0);
@@ -1878,7 +1878,7 @@ __device__ __forceinline__ void reg_epilogue_lds(const f32x16_t (&acc)[TM][TN], 
 #pragma unroll
         for (int g = 0; g < 4; ++g)
           bw[g] = *reinterpret_cast<const uint2*>(blds + (j * 32 + g * 8 + half * 4) * 2);
-        epi_pack32<EPI>(acc[i][j], bw, r[jj], half, v[jj]);
+        epi_pack32<EPI>(acc[i][j], bw, r[jj], v[jj]);
       }
       if (t > 0) {
 #pragma unroll
@@ -2087,8 +2087,8 @@ __device__ __forceinline__ void rope_epilogue_lds(const f32x16_t (&acc)[TM][TN],
           }
         }
         u32x4 vl[2], vu[2];
-        epi_pack32<EPI_NONE>(lo, zb, unused, half, vl);
-        epi_pack32<EPI_NONE>(up, zb, unused, half, vu);
+        epi_pack32<EPI_NONE>(lo, zb, unused, vl);
+        epi_pack32<EPI_NONE>(up, zb, unused, vu);
         if (t > 0) {
 #pragma unroll
           for (int q = 0; q < 4; ++q) __builtin_amdgcn_raw_buffer_store_b128(w[q], yres, goff(t - 1, q), 0, 0);
