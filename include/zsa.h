@@ -182,6 +182,8 @@ int zsa_norm(void* stream, int32_t dtype, int32_t kind, const void* x, const voi
  * that (past its 256-byte rounded size) lets the call first tabulate each
  * row's rotary (cos, sin) pairs there, which long products then read
  * instead of forming the angles themselves (same values).
+ * m = 0 reads and writes nothing and launches nothing; x, y, residual and
+ * pos may then be NULL (the other arguments are still checked).
  */
 int zsa_linear(void* stream, int32_t dtype, const void* x, int32_t m, int32_t k, const void* w,
                int32_t n, const void* bias, int32_t epilogue, const void* residual,

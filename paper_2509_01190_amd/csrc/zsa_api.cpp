@@ -486,11 +486,12 @@ int zsa_linear(void* stream, int32_t dtype, const void* x, int32_t m, int32_t k,
   if (epilogue < ZSA_EPI_NONE || epilogue > ZSA_EPI_ROPE) return fail(ZSA_EINVAL, "epilogue %d", epilogue);
   if (epilogue == ZSA_EPI_SWIGLU && n % 16 != 0)
     return fail(ZSA_ESHAPE, "SwiGLU needs n %% 16 == 0 (n = %d)", n);
-  CHECK(check_ptr16(x, "x"));
+  // no rows: nothing is read or written, so the row operands may be NULL
+  CHECK(check_ptr16(x, "x", m == 0));
   CHECK(check_ptr16(w, "w"));
-  CHECK(check_ptr16(y, "y"));
+  CHECK(check_ptr16(y, "y", m == 0));
   CHECK(check_ptr16(bias, "bias", true));
-  if (epilogue == ZSA_EPI_RESIDUAL) CHECK(check_ptr16(residual, "residual"));
+  if (epilogue == ZSA_EPI_RESIDUAL) CHECK(check_ptr16(residual, "residual", m == 0));
   zsa::EpiParams ep{};
   ep.epi = epilogue;
   ep.bias = bias;
@@ -516,6 +517,7 @@ int zsa_linear(void* stream, int32_t dtype, const void* x, int32_t m, int32_t k,
     if (ws_bytes < need)
       return fail(ZSA_EWORKSPACE, "linear workspace %zu < %zu bytes", ws_bytes, need);
   }
+  if (m == 0) return ZSA_OK;
   hipStream_t s = static_cast<hipStream_t>(stream);
   if (epilogue == ZSA_EPI_ROPE && dtype == ZSA_BF16 && ws != nullptr && m > 0 &&
       ws_bytes >= round256(need) + zsa::rope_table_bytes(m, head_dim)) {

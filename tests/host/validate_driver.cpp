@@ -191,6 +191,16 @@ void linear_checks() {
   EXPECT_RC(lin(ZSA_BF16, nullptr, 4, 64, w, 64, nullptr, 0, nullptr, nullptr, 0, 0, 1e4f, y,
                 nullptr, 0),
             ZSA_EINVAL);
+  // no rows: the row operands may be NULL and nothing is launched
+  EXPECT_RC(lin(ZSA_BF16, nullptr, 0, 64, w, 64, nullptr, ZSA_EPI_RESIDUAL, nullptr, nullptr, 0, 0,
+                1e4f, nullptr, nullptr, 0),
+            ZSA_OK);
+  EXPECT_RC(lin(ZSA_BF16, nullptr, 0, 64, w, 64, nullptr, ZSA_EPI_ROPE, nullptr, nullptr, 64, 64,
+                1e4f, nullptr, nullptr, 0),
+            ZSA_OK);
+  EXPECT_RC(lin(ZSA_BF16, nullptr, 0, 64, nullptr, 64, nullptr, 0, nullptr, nullptr, 0, 0, 1e4f,
+                nullptr, nullptr, 0),
+            ZSA_EINVAL);
   EXPECT_RC(lin(ZSA_BF16, x, 4, 64, C(0x2002), 64, nullptr, 0, nullptr, nullptr, 0, 0, 1e4f, y,
                 nullptr, 0),
             ZSA_EALIGN);

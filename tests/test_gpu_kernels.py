@@ -150,6 +150,24 @@ def test_linear_epilogues(dtype, k, epi):
     assert_close(f64(y), ref, 1e-2 if dtype == "bf16" else 2e-5, f"epilogue {epi}")
 
 
+@pytest.mark.parametrize("epi", EPIS)
+@pytest.mark.parametrize("split", [False, True])
+def test_linear_zero_rows(epi, split):
+    """A product of no rows (a batch whose sequences were all emptied, a
+    layer past the last kept row) returns an empty output and launches
+    nothing; the operands are views of real allocations."""
+    k, n, hd = 256, 384, 64
+    g = np.random.default_rng(3 + epi)
+    xd = to_dev(g.standard_normal((1, k)).astype(np.float32), "bf16")[:0]
+    wd = to_dev((g.standard_normal((n, k)) / math.sqrt(k)).astype(np.float32), "bf16")
+    res = to_dev(g.standard_normal((1, n)).astype(np.float32), "bf16")[:0] if epi == zsa.EPI_RESIDUAL else None
+    posd = torch.zeros(1, dtype=torch.int32, device=dev())[:0]
+    y = zsa.linear(xd, wd, None, epi, residual=res, pos=posd if epi == zsa.EPI_ROPE else None,
+                   head_dim=hd, rope_cols=256, rope_theta=1e4, split=split)
+    torch.cuda.synchronize()
+    assert tuple(y.shape) == (0, n // 2 if epi == zsa.EPI_SWIGLU else n)
+
+
 @pytest.mark.parametrize("m,n,k", [(1100, 384, 3072), (1500, 768, 8192), (2100, 768, 3072)])
 @pytest.mark.parametrize("epi", [zsa.EPI_NONE, zsa.EPI_GELU, zsa.EPI_SWIGLU, zsa.EPI_RESIDUAL,
                                  zsa.EPI_ROPE])
@@ -413,6 +431,37 @@ def test_attention_with_scores(dtype, hd, causal):
     assert np.max(np.abs(lse.cpu().numpy() - lse_ref)) <= 2e-5 * max(1.0, np.abs(lse_ref).max())
     assert np.max(np.abs(scores.cpu().numpy() - s_ref) / s_ref) <= 1e-4
     assert abs(scores.cpu().double().sum() - H * sum(lens)) <= 1e-4 * H * sum(lens)
+
+
+@pytest.mark.parametrize("hd", [64, 128])
+@pytest.mark.parametrize("causal", [False, True])
+def test_attention_empty_sequences(hd, causal):
+    """Zero-length sequences among others (every row of a sequence dropped
+    upstream): their workgroups exit at once and the other sequences'
+    outputs, log-sum-exp and scores match the oracle."""
+    lens = [0, 5, 0, 300, 0, 33]
+    H = 4
+    qkv, q, k, v = _qkv(lens, H, hd, "bf16", seed=hd + 3 * causal)
+    seqs = zsa.Seqs(lens, dev())
+    out, lse, scores = zsa.attention_with_scores(q, k, v, H, seqs, causal)
+    torch.cuda.synchronize()
+    q64, k64, v64 = f64(q), f64(k), f64(v)
+    o_ref, lse_ref, s_ref = [], [], []
+    for b, n in enumerate(lens):
+        if n == 0:
+            continue
+        lo = int(seqs.host[b])
+        o, l, s = O.attention(q64[lo:lo + n], k64[lo:lo + n], v64[lo:lo + n], np.arange(n), H,
+                              causal)
+        o_ref.append(o)
+        lse_ref.append(l)
+        s_ref.append(s)
+    o_ref = np.concatenate(o_ref)
+    lse_ref = np.concatenate(lse_ref, axis=1)
+    s_ref = np.concatenate(s_ref)
+    assert_close(f64(out), o_ref, 1e-2, "attention output")
+    assert np.max(np.abs(lse.cpu().numpy() - lse_ref)) <= 2e-5 * max(1.0, np.abs(lse_ref).max())
+    assert np.max(np.abs(scores.cpu().numpy() - s_ref) / s_ref) <= 1e-4
 
 
 @pytest.mark.parametrize("lens", [[100, 37], [300, 700]])   # 128- and 256-query blocks
