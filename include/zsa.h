@@ -155,6 +155,7 @@ int zsa_keep_schedule(int32_t batch, const int32_t* lengths, const double* keep_
  * shift (kind ZSA_NORM_LAYER; biased variance) or y = x / sqrt(mean(x^2) +
  * eps) * gain (ZSA_NORM_RMS; shift ignored, may be NULL).
  * x, y [rows, d] device, dtype; gain, shift [d]. y must not overlap x.
+ * rows = 0 launches nothing; x and y may then be NULL.
  */
 int zsa_norm(void* stream, int32_t dtype, int32_t kind, const void* x, const void* gain,
              const void* shift, int32_t rows, int32_t d, float eps, void* y);
@@ -212,7 +213,8 @@ size_t zsa_linear_workspace_size(int32_t dtype, int32_t m, int32_t n, int32_t k)
  *            ascending original position, as compaction keeps them)
  *   ws       >= zsa_attention_workspace_size(n_heads, T, want_scores)
  * bf16 with head_dim 64 or 128 runs the MFMA kernels; other shapes and fp32
- * run vector-ALU kernels.
+ * run vector-ALU kernels. Sequences may be empty; with T = 0 (all of them)
+ * nothing is launched and q, k, v, out may be NULL.
  */
 int zsa_attention_with_scores(void* stream, int32_t dtype, const void* q, const void* k,
                               const void* v, int64_t row_stride, int32_t n_heads,
@@ -246,7 +248,8 @@ size_t zsa_static_scratch_bytes(void);
  * (Sec. 3.2-3.3): scores[j] = sum_h sum_i exp(q_i . k_j * scale - lse[h, i]),
  * the sum over the rows i allowed by the mask. Deterministic (fixed
  * reduction order, no atomics). Arguments as in zsa_attention_with_scores;
- * lse [n_heads, T] fp32 device. ws >= zsa_score_workspace_size(n_heads, T). */
+ * lse [n_heads, T] fp32 device. ws >= zsa_score_workspace_size(n_heads, T).
+ * With T = 0 nothing is launched and q, k, lse, scores may be NULL. */
 int zsa_score_positions(void* stream, int32_t dtype, const void* q, const void* k,
                         int64_t row_stride, const float* lse, int32_t n_heads,
                         int32_t n_kv_heads, int32_t head_dim, int32_t causal, float scale,

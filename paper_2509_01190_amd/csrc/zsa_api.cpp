@@ -460,10 +460,12 @@ int zsa_norm(void* stream, int32_t dtype, int32_t kind, const void* x, const voi
   if (rows < 0) return fail(ZSA_EINVAL, "rows < 0");
   CHECK(check_width(dtype, d, "d"));
   if (d > (dtype == ZSA_BF16 ? 8192 : 4096)) return fail(ZSA_EUNSUPPORTED, "d %d too wide", d);
-  CHECK(check_ptr16(x, "x"));
+  // no rows: nothing is read or written, so x and y may be NULL
+  CHECK(check_ptr16(x, "x", rows == 0));
   CHECK(check_ptr16(gain, "gain"));
-  CHECK(check_ptr16(y, "y"));
+  CHECK(check_ptr16(y, "y", rows == 0));
   CHECK(check_ptr16(shift, "shift", true));
+  if (rows == 0) return ZSA_OK;
   HIP_TRY(zsa::launch_norm(static_cast<hipStream_t>(stream), dtype, kind, x, gain,
                            kind == ZSA_NORM_LAYER ? shift : nullptr, rows, d, eps, y),
           "norm");
@@ -559,10 +561,12 @@ int zsa_attention_with_scores(void* stream, int32_t dtype, const void* q, const 
   CHECK(check_kv_heads(n_heads, n_kv_heads, &kvg));
   int32_t T, max_len;
   CHECK(check_seqs(batch, cu_host, cu_dev, &T, &max_len));
-  CHECK(check_ptr16(q, "q"));
-  CHECK(check_ptr16(k, "k"));
-  CHECK(check_ptr16(v, "v"));
-  CHECK(check_ptr16(out, "out"));
+  // no rows (every sequence empty): nothing is read or written, so the row
+  // operands may be NULL
+  CHECK(check_ptr16(q, "q", T == 0));
+  CHECK(check_ptr16(k, "k", T == 0));
+  CHECK(check_ptr16(v, "v", T == 0));
+  CHECK(check_ptr16(out, "out", T == 0));
   CHECK(check_width(dtype, row_stride, "row_stride"));
   CHECK(check_width(dtype, out_stride, "out_stride"));
   if (row_stride < static_cast<int64_t>(n_heads) * head_dim || out_stride < static_cast<int64_t>(n_heads) * head_dim)
@@ -574,6 +578,7 @@ int zsa_attention_with_scores(void* stream, int32_t dtype, const void* q, const 
     if (ws_bytes < need || (need > 0 && ws == nullptr))
       return fail(ZSA_EWORKSPACE, "workspace %zu bytes < %zu", ws_bytes, need);
   }
+  if (T == 0) return ZSA_OK;
   hipStream_t s = static_cast<hipStream_t>(stream);
   char* base = static_cast<char*>(ws);
   float* lse_buf = lse != nullptr ? lse : reinterpret_cast<float*>(base);
@@ -607,9 +612,10 @@ int zsa_score_positions(void* stream, int32_t dtype, const void* q, const void* 
   CHECK(check_kv_heads(n_heads, n_kv_heads, &kvg));
   int32_t T, max_len;
   CHECK(check_seqs(batch, cu_host, cu_dev, &T, &max_len));
-  CHECK(check_ptr16(q, "q"));
-  CHECK(check_ptr16(k, "k"));
-  if (lse == nullptr || scores == nullptr) return fail(ZSA_EINVAL, "lse / scores is NULL");
+  // no rows: nothing is read or written, so the row operands may be NULL
+  CHECK(check_ptr16(q, "q", T == 0));
+  CHECK(check_ptr16(k, "k", T == 0));
+  if (T > 0 && (lse == nullptr || scores == nullptr)) return fail(ZSA_EINVAL, "lse / scores is NULL");
   CHECK(check_width(dtype, row_stride, "row_stride"));
   if (row_stride < static_cast<int64_t>(n_heads) * head_dim)
     return fail(ZSA_ESHAPE, "row stride shorter than n_heads * head_dim");
@@ -618,6 +624,7 @@ int zsa_score_positions(void* stream, int32_t dtype, const void* q, const void* 
   const size_t need = zsa_score_workspace_size(n_heads, T);
   if (ws_bytes < need || (need > 0 && ws == nullptr))
     return fail(ZSA_EWORKSPACE, "workspace %zu bytes < %zu", ws_bytes, need);
+  if (T == 0) return ZSA_OK;
   hipStream_t s = static_cast<hipStream_t>(stream);
   const int G = zsa::score_groups(dtype, n_heads, head_dim, T);
   float* partials = static_cast<float*>(ws);

@@ -264,8 +264,9 @@ def attention_with_scores(q: torch.Tensor, k: torch.Tensor, v: torch.Tensor, n_h
     _require_cuda(q, k, v)
     T, width = q.shape
     hd = width // n_heads
-    rs = q.stride(0)
-    if k.stride(0) != rs or v.stride(0) != rs or q.stride(1) != 1:
+    # no rows: nothing is read, and torch may give empty views any strides
+    rs = q.stride(0) if T > 0 else width
+    if T > 0 and (k.stride(0) != rs or v.stride(0) != rs or q.stride(1) != 1):
         raise ValueError("q, k, v must share one row stride")
     if scale is None:
         scale = 1.0 / float(np.sqrt(hd))
@@ -287,8 +288,8 @@ def score_positions(q: torch.Tensor, k: torch.Tensor, lse: torch.Tensor, n_heads
     _require_cuda(q, k, lse)
     T, width = q.shape
     hd = width // n_heads
-    rs = q.stride(0)
-    if k.stride(0) != rs:
+    rs = q.stride(0) if T > 0 else width
+    if T > 0 and k.stride(0) != rs:
         raise ValueError("q and k must share one row stride")
     if scale is None:
         scale = 1.0 / float(np.sqrt(hd))

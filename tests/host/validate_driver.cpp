@@ -163,6 +163,11 @@ void norm_checks() {
   EXPECT_RC(zsa_norm(nullptr, ZSA_F32, 0, C(0x1000), C(0x2000), C(0x2008), 4, 64, 1e-5f,
                      A(0x3000)),
             ZSA_EALIGN);
+  // no rows: x and y may be NULL and nothing is launched
+  EXPECT_RC(zsa_norm(nullptr, ZSA_BF16, 0, nullptr, C(0x2000), nullptr, 0, 64, 1e-5f, nullptr),
+            ZSA_OK);
+  EXPECT_RC(zsa_norm(nullptr, ZSA_BF16, 0, nullptr, nullptr, nullptr, 0, 64, 1e-5f, nullptr),
+            ZSA_EINVAL);
 }
 
 void linear_checks() {
@@ -296,6 +301,19 @@ void attention_checks() {
   EXPECT_RC(att(ZSA_BF16, q, 12288, 32, 0, 128, 0.1f, 1, cu_long, cud, out, 4096, F(0x4000),
                 nullptr, nullptr, 0),
             ZSA_EUNSUPPORTED);
+  // every sequence empty: the row operands may be NULL and nothing is launched
+  const int32_t cu_empty[3] = {0, 0, 0};
+  EXPECT_RC(zsa_attention_with_scores(nullptr, ZSA_BF16, nullptr, nullptr, nullptr, 128, 2, 0, 64,
+                                      1, 0.1f, 2, cu_empty, cud, nullptr, 128, nullptr, nullptr,
+                                      nullptr, 0),
+            ZSA_OK);
+  EXPECT_RC(zsa_score_positions(nullptr, ZSA_BF16, nullptr, nullptr, 128, nullptr, 2, 0, 64, 1,
+                                0.1f, 2, cu_empty, cud, nullptr, nullptr, 0),
+            ZSA_OK);
+  EXPECT_RC(zsa_attention_with_scores(nullptr, ZSA_BF16, nullptr, nullptr, nullptr, 128, 2, 0, 64,
+                                      1, 0.1f, 1, cu, cud, out, 128, F(0x4000), nullptr, nullptr,
+                                      0),
+            ZSA_EINVAL);
   CHECK_TRUE(zsa_attention_workspace_size(0, 8, 1) == 0);
   CHECK_TRUE(zsa_attention_workspace_size(2, 8, 1) > zsa_attention_workspace_size(2, 8, 0));
 

@@ -433,6 +433,22 @@ def test_attention_with_scores(dtype, hd, causal):
     assert abs(scores.cpu().double().sum() - H * sum(lens)) <= 1e-4 * H * sum(lens)
 
 
+def test_all_sequences_empty():
+    """A batch whose sequences are all empty (T = 0) and a norm of no rows:
+    the calls return at once with empty results, through NULL row operands
+    (torch gives zero-size tensors a null address)."""
+    H, hd = 4, 64
+    qkv, q, k, v = _qkv([0, 0, 0], H, hd, "bf16", seed=1)
+    seqs = zsa.Seqs([0, 0, 0], dev())
+    out, lse, scores = zsa.attention_with_scores(q, k, v, H, seqs, True)
+    s2 = zsa.score_positions(q, k, lse, H, seqs, True)
+    g = to_dev(np.ones(256, dtype=np.float32), "bf16")
+    y = zsa.norm(to_dev(np.zeros((1, 256), dtype=np.float32), "bf16")[:0], g, g, zsa.NORM_LAYER)
+    torch.cuda.synchronize()
+    assert tuple(out.shape) == (0, H * hd) and tuple(lse.shape) == (H, 0)
+    assert scores.numel() == 0 and s2.numel() == 0 and tuple(y.shape) == (0, 256)
+
+
 @pytest.mark.parametrize("hd", [64, 128])
 @pytest.mark.parametrize("causal", [False, True])
 def test_attention_empty_sequences(hd, causal):
