@@ -212,6 +212,17 @@ def test_small_bf16_stack(kind):
     compare_stack(p, lens, stack, xd, posd, dws, ocfg, rates)
 
 
+def test_stack_with_empty_sequences():
+    """Empty sequences inside a batch pass every pruning point with zero rows
+    (their kept counts are 0) and leave the other sequences' rows, scores,
+    kept sets and positions as the oracle has them."""
+    p = W.shrink(W.PRESETS["dec1b"], n_layers=3, d_model=256, n_heads=4, d_ff=256, batch=5,
+                 prune_after=(1, 2))
+    lens, stack, xd, posd, dws, ocfg = build(p, 2, [0, 37, 0, 120, 5])
+    compare_stack(p, lens, stack, xd, posd, dws, ocfg, [0.5, 0.5, 0.3, 0.7, 0.9],
+                  seqs_check=[1, 3, 4], label="empty sequences")
+
+
 def test_stack_deterministic_and_keep_one():
     p = W.shrink(W.PRESETS["dec1b"], n_layers=3, d_model=256, n_heads=4, d_ff=256, batch=3,
                  prune_after=(1, 2))
