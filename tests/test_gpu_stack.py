@@ -221,6 +221,11 @@ def test_stack_with_empty_sequences():
     lens, stack, xd, posd, dws, ocfg = build(p, 2, [0, 37, 0, 120, 5])
     compare_stack(p, lens, stack, xd, posd, dws, ocfg, [0.5, 0.5, 0.3, 0.7, 0.9],
                   seqs_check=[1, 3, 4], label="empty sequences")
+    # a batch of empty sequences only: nothing to compute, zero rows out
+    seqs0 = zsa.Seqs([0, 0, 0], dev())
+    out = stack.forward(xd[:0], posd[:0], seqs0, p.prune_after, [0.5, 0.5, 0.5])
+    torch.cuda.synchronize()
+    assert out["t_final"] == 0 and not np.any(out["cu_host"])
 
 
 def test_stack_deterministic_and_keep_one():
