@@ -30,11 +30,6 @@ typedef float f32x16_t __attribute__((ext_vector_type(16)));
 constexpr float kLog2e = 1.4426950408889634f;
 constexpr float kLn2 = 0.6931471805599453f;
 
-__device__ __forceinline__ uint32_t bf16_at(const uint4& v, int e) {
-  const uint32_t w = e < 2 ? v.x : e < 4 ? v.y : e < 6 ? v.z : v.w;
-  return (e & 1) ? (w >> 16) : (w & 0xffffu);
-}
-
 // Head dim 64 fits four waves per SIMD (128 registers), 128 two. A workgroup
 // reads every K and V row of its sequence and head once, so the bytes moved
 // per query fall as the query block grows: the loads, not the MFMAs or the
@@ -60,8 +55,14 @@ __global__ __launch_bounds__(64 * NW) __attribute__((amdgpu_waves_per_eu(HD == 6
   // plain layout: the swizzle there measured 2 % slower.
   constexpr int VLD = BKEY + 4;
   constexpr int VSW = HD == 64 ? 4 : 0;
+  // Head dim 128 stores V as it comes (key rows, the K tile's row stride)
+  // and reads the V^T fragments with gfx950's transposing LDS reads
+  // (ds_read_b64_tr_b16): 4 x 4096 causal rows, 32 heads, 986 -> 929 us.
+  // At head dim 64 the same reads took 296 -> 296 us on 8 x 2048 causal
+  // rows and 40.6 -> 42.2 us on 32 x 512, so it keeps the transposed tile.
+  constexpr bool VTR = HD == 128;
   constexpr int OLD = HD + 8;    // output staging row stride
-  constexpr int KBYTES = BKEY * KLD * 2, VBYTES = HD * VLD * 2;
+  constexpr int KBYTES = BKEY * KLD * 2, VBYTES = VTR ? KBYTES : HD * VLD * 2;
   constexpr int BUF = KBYTES + VBYTES;
   // K/V tile buffers: eight-wave blocks keep four (tiles stored two ahead,
   // a barrier after every second tile: 297.0 -> 292.2 us on 8 x 2048 causal
@@ -125,13 +126,20 @@ __global__ __launch_bounds__(64 * NW) __attribute__((amdgpu_waves_per_eu(HD == 6
                   : 0x80000000u;
   }
   const uint32_t row_bytes = static_cast<uint32_t>(rs * 2);
-  u32x4 kreg[KCH], vreg[VPR][2];
+  u32x4 kreg[KCH], vreg[VPR][2], vrow[KCH];
   auto load_tile = [&](int j0) {
     const uint32_t t0 = static_cast<uint32_t>(j0) * row_bytes;
     // the whole offset goes in the vector operand, which the range check covers
 #pragma unroll
     for (int i = 0; i < KCH; ++i)
       kreg[i] = __builtin_bit_cast(u32x4, __builtin_amdgcn_raw_buffer_load_b128(kres, koff[i] + t0, 0, 0));
+    if constexpr (VTR) {
+      // V rows at the K offsets (one row stride)
+#pragma unroll
+      for (int i = 0; i < KCH; ++i)
+        vrow[i] = __builtin_bit_cast(u32x4, __builtin_amdgcn_raw_buffer_load_b128(vres, koff[i] + t0, 0, 0));
+      return;
+    }
 #pragma unroll
     for (int i = 0; i < VPR; ++i) {
       vreg[i][0] = __builtin_bit_cast(
@@ -148,8 +156,9 @@ __global__ __launch_bounds__(64 * NW) __attribute__((amdgpu_waves_per_eu(HD == 6
       const int c = tid + i * NT;
       const int r = c / (HD / 8), ch = (c % (HD / 8)) * 8;
       *reinterpret_cast<u32x4*>(Ks + r * KLD + ch) = kreg[i];
+      if constexpr (VTR) *reinterpret_cast<u32x4*>(Vt + r * KLD + ch) = vrow[i];
     }
-    if (!vth) return;
+    if (VTR || !vth) return;
 #pragma unroll
     for (int i = 0; i < VPR; ++i) {
       const int c = tid + i * NT;
@@ -260,6 +269,32 @@ __global__ __launch_bounds__(64 * NW) __attribute__((amdgpu_waves_per_eu(HD == 6
         const u32x4 pw = {pack_bf16x2(s[ks][rb], s[ks][rb + 1]), pack_bf16x2(s[ks][rb + 2], s[ks][rb + 3]),
                           pack_bf16x2(s[ks][rb + 4], s[ks][rb + 5]), pack_bf16x2(s[ks][rb + 6], s[ks][rb + 7])};
         const bf16x8_t pb = __builtin_bit_cast(bf16x8_t, pw);
+        if constexpr (VTR) {
+          // pb's slots 0..3 hold keys kb + 4 half + 0..3 and slots 4..7 keys
+          // kb + 8 + 4 half + 0..3 (kb = 32 ks + 16 (g & 1)); the V^T
+          // fragment gives channel ct * 32 + l32 the same keys in the same
+          // slots. A transposing read gives each lane of a 16-lane group
+          // element c (its lane number in the group) of four 16-element
+          // rows, row r pieced together from the 4-element runs at the
+          // addresses of the group's lanes 4r .. 4r + 3: so the group's
+          // lanes point at key rows kb + 4 half + r and channel runs
+          // 16 ((lane / 16) & 1) + 4 (lane & 3).
+          typedef short s16x4 __attribute__((ext_vector_type(4)));
+          typedef __attribute__((address_space(3))) s16x4 lds_s16x4;
+          typedef __attribute__((address_space(3))) const char lds_char;
+          const bf16_t* tr0 = Vt + (ks * 32 + (g & 1) * 16 + 4 * half + ((lane & 15) >> 2)) * KLD +
+                              16 * ((lane >> 4) & 1) + 4 * (lane & 3);
+#pragma unroll
+          for (int ct = 0; ct < HD / 32; ++ct) {
+            const bf16_t* vr = tr0 + ct * 32;
+            const s16x4 lo4 = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_s16x4*)((lds_char*)vr));
+            const s16x4 hi4 = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_s16x4*)((lds_char*)(vr + 8 * KLD)));
+            const uint2 l2 = __builtin_bit_cast(uint2, lo4), h2 = __builtin_bit_cast(uint2, hi4);
+            const u32x4 av = {l2.x, l2.y, h2.x, h2.y};
+            o[ct] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(__builtin_bit_cast(bf16x8_t, av), pb, o[ct], 0, 0, 0);
+          }
+          continue;
+        }
         // key chunks 8 ks + 4 (g & 1) + half and that + 2; the swizzle is even,
         // so it leaves half (the only lane-dependent part) alone and the
         // offsets stay immediates on one base address
