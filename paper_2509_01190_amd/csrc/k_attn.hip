@@ -5,7 +5,8 @@
 //
 // bf16, head_dim 64/128 (MFMA): one workgroup of NW waves per (32 NW-query
 // block, head, sequence); each wave owns 32 queries and walks 64-key tiles
-// staged in LDS (K row-major, V transposed). The wave computes the
+// staged in LDS (K row-major; V transposed at head_dim 64, row-major at 128
+// and read through transposing LDS reads). The wave computes the
 // *transposed* score tile S^T = K Q^T with v_mfma_f32_32x32x16_bf16, so a
 // lane holds 32 key scores of one query: the online-softmax max and sum are
 // in-lane plus one swap with lane l^32, and the probabilities already sit in
